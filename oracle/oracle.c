@@ -1,0 +1,247 @@
+/*
+ * oracle.c -- plain double-precision CPU reference for ConvCRF mean-field
+ * inference (Teichmann & Cipolla, "Convolutional CRFs for Semantic
+ * Segmentation", arXiv 1805.04777).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the checker the GPU library is
+ * compared against.  Only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark may load it.  It shares no code, header, table or
+ * constant with the HIP library and includes nothing from it.
+ *
+ * It is written to be read against the paper, not to be fast:
+ *   - every quantity is a double and every exponential is libm exp();
+ *   - loops follow the definitions literally (one pixel, one neighbour, one
+ *     class at a time); the only concession to speed is an OpenMP split of
+ *     the outer pixel loop, which does not change any summation order.
+ *
+ * Readings of the paper that this file fixes (each also tested):
+ *   - inputs are logits U = -psi_u; Q0 = softmax(U)          (Alg. 1, init)
+ *   - message M_p(l) = sum over window neighbours q != p of K(p,q) Q_q(l)
+ *                                                     (Eq. 6, Alg. 1 message)
+ *     window = square (2r+1)x(2r+1), r = (k-1)/2, centred on p, neighbours
+ *     outside the image contribute nothing (Sec. 4 locality assumption)
+ *   - K(p,q) = w_app exp(-|p-q|^2/2ta^2 - |I_p-I_q|^2/2tb^2)
+ *            + w_smooth exp(-|p-q|^2/2tg^2)                     (Eq. 4)
+ *     the centre tap (q == p) is excluded unless include_center is set, in
+ *     which case it contributes K(p,p) = w_app + w_smooth    (Eq. 2 vs Eq. 6)
+ *   - Z_p(l) = U_p(l) - sum_l' mu[l][l'] M_p(l'),  Q = softmax(Z)
+ *                        (Alg. 1 compatibility, unary, normalise; Eq. 1-3)
+ *     mu == NULL means Potts, mu[l][l'] = [l != l']          (Sec. 3, 4.2)
+ *   - blur s > 1: Q and features are s x s average pooled, the message is
+ *     taken on the pooled grid (positions = block centres, so pooled offsets
+ *     are s times the grid offsets), then bilinearly upsampled with
+ *     half-pixel centres and edge clamping before the compatibility step
+ *                                                             (Sec. 4.2)
+ */
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+typedef struct {
+    int filter_size;      /* k: odd window side */
+    int blur;             /* s: 1 = off; else pool factor, must divide H, W */
+    int include_center;   /* 0: exclude q == p (Alg. 1); 1: include (Eq. 6) */
+    int reserved;
+    double w_app, theta_alpha, theta_beta;  /* appearance kernel (Eq. 4) */
+    double w_smooth, theta_gamma;           /* smoothness kernel (Eq. 4) */
+} oracle_params;
+
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* Eq. 4: the merged Gaussian kernel as a function of the squared position
+ * distance (in full-resolution pixels) and the squared colour distance. */
+double oracle_kernel(double pos_d2, double col_d2, const oracle_params *p)
+{
+    double app = p->w_app * exp(-pos_d2 / (2.0 * p->theta_alpha * p->theta_alpha)
+                                - col_d2 / (2.0 * p->theta_beta * p->theta_beta));
+    double smo = p->w_smooth * exp(-pos_d2 / (2.0 * p->theta_gamma * p->theta_gamma));
+    return app + smo;
+}
+
+/* Alg. 1 initialisation and normalisation: softmax over the C classes of one
+ * pixel, with the maximum subtracted first.  Class l of the input is z[l*zs],
+ * of the output q[l*qs]. */
+static void softmax_pixel(const double *z, long zs, double *q, long qs, int C)
+{
+    double m = z[0];
+    for (int l = 1; l < C; ++l)
+        if (z[l * zs] > m) m = z[l * zs];
+    double sum = 0.0;
+    for (int l = 0; l < C; ++l) {
+        double e = exp(z[l * zs] - m);
+        q[l * qs] = e;
+        sum += e;
+    }
+    for (int l = 0; l < C; ++l) q[l * qs] /= sum;
+}
+
+/* Q0 = softmax(U) for one image, layout [C][H][W]. */
+void oracle_softmax(const double *U, int C, int H, int W, double *Q)
+{
+    long HW = (long)H * W;
+    for (long i = 0; i < HW; ++i) softmax_pixel(U + i, HW, Q + i, HW, C);
+}
+
+/* Eq. 6 / Alg. 1 message passing for one image on an H x W grid.
+ * Q, M: [C][H][W]; I: [3][H][W].  pos_scale multiplies grid offsets to give
+ * the position difference in full-resolution pixels (1 without blur, s on the
+ * pooled grid).  M is overwritten. */
+void oracle_message(const double *Q, const double *I, int C, int H, int W,
+                    const oracle_params *p, double pos_scale, double *M)
+{
+    const int r = (p->filter_size - 1) / 2;
+    const long HW = (long)H * W;
+#pragma omp parallel for schedule(static)
+    for (int y = 0; y < H; ++y) {
+        for (int x = 0; x < W; ++x) {
+            const long pi = (long)y * W + x;
+            for (int l = 0; l < C; ++l) M[l * HW + pi] = 0.0;
+            for (int y2 = y - r; y2 <= y + r; ++y2) {
+                if (y2 < 0 || y2 >= H) continue;           /* outside: no term */
+                for (int x2 = x - r; x2 <= x + r; ++x2) {
+                    if (x2 < 0 || x2 >= W) continue;
+                    if (y2 == y && x2 == x && !p->include_center) continue;
+                    const long qi = (long)y2 * W + x2;
+                    double dy = pos_scale * (y2 - y), dx = pos_scale * (x2 - x);
+                    double col = 0.0;
+                    for (int ch = 0; ch < 3; ++ch) {
+                        double d = I[ch * HW + pi] - I[ch * HW + qi];
+                        col += d * d;
+                    }
+                    double kq = oracle_kernel(dy * dy + dx * dx, col, p);
+                    for (int l = 0; l < C; ++l) M[l * HW + pi] += kq * Q[l * HW + qi];
+                }
+            }
+        }
+    }
+}
+
+/* Alg. 1 compatibility transform, unary addition and normalisation for
+ * `npix` pixels: Z(l) = U(l) - sum_l' mu[l][l'] M(l'), Q = softmax(Z).
+ * mu is row-major C x C, or NULL for Potts mu[l][l'] = [l != l']. */
+void oracle_update(const double *U, const double *M, const double *mu,
+                   int C, long npix, double *Q)
+{
+#pragma omp parallel
+    {
+        double *z = (double *)malloc(sizeof(double) * (size_t)C);
+#pragma omp for schedule(static)
+        for (long i = 0; i < npix; ++i) {
+            for (int l = 0; l < C; ++l) {
+                double t = 0.0;
+                for (int lp = 0; lp < C; ++lp) {
+                    double m = mu ? mu[l * C + lp] : (l != lp ? 1.0 : 0.0);
+                    t += m * M[lp * npix + i];
+                }
+                z[l] = U[l * npix + i] - t;
+            }
+            softmax_pixel(z, 1, Q + i, npix, C);
+        }
+        free(z);
+    }
+}
+
+/* s x s average pooling of `nch` planes of H x W into H/s x W/s. */
+void oracle_avgpool(const double *X, int nch, int H, int W, int s, double *Y)
+{
+    const int Hp = H / s, Wp = W / s;
+    for (int c = 0; c < nch; ++c)
+        for (int Y0 = 0; Y0 < Hp; ++Y0)
+            for (int X0 = 0; X0 < Wp; ++X0) {
+                double acc = 0.0;
+                for (int i = 0; i < s; ++i)
+                    for (int j = 0; j < s; ++j)
+                        acc += X[((long)c * H + Y0 * s + i) * W + X0 * s + j];
+                Y[((long)c * Hp + Y0) * Wp + X0] = acc / (double)(s * s);
+            }
+}
+
+/* Bilinear upsampling by s of `nch` planes of Hp x Wp, with half-pixel
+ * centres: output pixel y samples source coordinate (y + 0.5)/s - 0.5,
+ * clamped below at 0; the upper neighbour index is clamped at Hp - 1. */
+static void src_coord(int o, int s, int n, int *i0, int *i1, double *f)
+{
+    double u = ((double)o + 0.5) / (double)s - 0.5;
+    if (u < 0.0) u = 0.0;
+    int a = (int)floor(u);
+    if (a > n - 1) a = n - 1;
+    *i0 = a;
+    *i1 = a < n - 1 ? a + 1 : n - 1;
+    *f = u - (double)a;
+}
+
+void oracle_upsample(const double *X, int nch, int Hp, int Wp, int s, double *Y)
+{
+    const int H = Hp * s, W = Wp * s;
+    for (int c = 0; c < nch; ++c)
+        for (int y = 0; y < H; ++y) {
+            int y0, y1;
+            double fy;
+            src_coord(y, s, Hp, &y0, &y1, &fy);
+            for (int x = 0; x < W; ++x) {
+                int x0, x1;
+                double fx;
+                src_coord(x, s, Wp, &x0, &x1, &fx);
+                const double *P = X + (long)c * Hp * Wp;
+                double top = (1.0 - fx) * P[y0 * Wp + x0] + fx * P[y0 * Wp + x1];
+                double bot = (1.0 - fx) * P[y1 * Wp + x0] + fx * P[y1 * Wp + x1];
+                Y[((long)c * H + y) * W + x] = (1.0 - fy) * top + fy * bot;
+            }
+        }
+}
+
+/* Alg. 1 end to end: T rounds of message passing, compatibility transform,
+ * unary addition and softmax, starting from softmax(U).  U, Q: [B][C][H][W];
+ * I: [B][3][H][W] (RGB on its own 0..255 scale).  Returns 0 on success, -1 on
+ * an argument the definition does not cover. */
+int oracle_meanfield(const double *U, const double *I, int B, int C, int H, int W,
+                     const oracle_params *p, const double *mu, int T, double *Q)
+{
+    if (B < 0 || C < 1 || H < 1 || W < 1 || T < 0 || !p) return -1;
+    if (p->filter_size < 1 || (p->filter_size & 1) == 0) return -1;
+    const int s = p->blur;
+    if (s < 1 || H % s || W % s) return -1;
+    const long HW = (long)H * W;
+    const int Hp = H / s, Wp = W / s;
+    const long HWp = (long)Hp * Wp;
+
+    double *Qt = (double *)malloc(sizeof(double) * C * HW);
+    double *M = (double *)malloc(sizeof(double) * C * HW);
+    double *Qp = s > 1 ? (double *)malloc(sizeof(double) * C * HWp) : NULL;
+    double *Mp = s > 1 ? (double *)malloc(sizeof(double) * C * HWp) : NULL;
+    double *Ip = s > 1 ? (double *)malloc(sizeof(double) * 3 * HWp) : NULL;
+
+    for (int b = 0; b < B; ++b) {
+        const double *Ub = U + (long)b * C * HW;
+        const double *Ib = I + (long)b * 3 * HW;
+        oracle_softmax(Ub, C, H, W, Qt);
+        if (s > 1) oracle_avgpool(Ib, 3, H, W, s, Ip);
+        for (int t = 0; t < T; ++t) {
+            if (s == 1) {
+                oracle_message(Qt, Ib, C, H, W, p, 1.0, M);
+            } else {
+                oracle_avgpool(Qt, C, H, W, s, Qp);
+                oracle_message(Qp, Ip, C, Hp, Wp, p, (double)s, Mp);
+                oracle_upsample(Mp, C, Hp, Wp, s, M);
+            }
+            oracle_update(Ub, M, mu, C, HW, Qt);
+        }
+        memcpy(Q + (long)b * C * HW, Qt, sizeof(double) * C * HW);
+    }
+    free(Qt);
+    free(M);
+    free(Qp);
+    free(Mp);
+    free(Ip);
+    return 0;
+}
