@@ -1,0 +1,205 @@
+"""Benchmark: ConvCRF mean-field inference on one MI355X.
+
+One step = one full call of the library (softmax init + T mean-field rounds)
+on one synthetic batch already resident in HBM.  Prints one JSON line with
+the throughput in megapixel-iterations per second, the roofline of the
+dominant kernel (timed with HIP events recorded by the library around every
+launch, on the launch stream) and the double-precision CPU oracle timed on
+this host as a baseline.
+
+    python bench.py [--steps K] [--warmup W] [--workload pascal]
+                    [--variant fused|materialised] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "megapixel·iterations/sec and ms per 5-iter inference (C=21, 512², k=7)"
+UNIT = "MP·iter/s"
+
+# MI355X: 256 CUs x 4 SIMD x 16 lanes, 2.4 GHz.  One FP32 FMA (2 flop) per
+# lane per clock without packed FP32 (the library is built without it):
+# 256 * 64 * 2 * 2.4e9 = 78.6 TFLOP/s.  HBM3E: 8 TB/s.
+PEAK_VALU_FP32 = 256 * 64 * 2 * 2.4e9
+PEAK_VALU_FP32_PACKED = 2 * PEAK_VALU_FP32
+PEAK_HBM = 8.0e12
+
+ITER_SRC = os.path.join(ROOT, "paper_1805_04777_amd", "csrc", "iter.hip")
+TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def flops_per_pixel_iter(C: int, k: int, potts: bool) -> int:
+    """Algorithmic flops of one pixel-iteration of the fused path: message
+    2C(k^2-1), Gaussian weights 12 per tap (3 differences, squared norm,
+    exponent, exp, add), compatibility 2C^2 (C for Potts: Z = U + M), unary
+    add and softmax 5C + 1."""
+    taps = k * k - 1
+    compat = C if potts else 2 * C * C
+    return 2 * C * taps + 12 * taps + compat + 5 * C + 1
+
+
+def bytes_per_pixel(C: int, first: bool) -> int:
+    """Algorithmic HBM bytes of one fused launch per pixel: read Q_t (not on
+    the first launch, which reads U instead), U and the RGB image, write
+    Q_{t+1}; fp32."""
+    return 4 * C * (2 if first else 3) + 12
+
+
+def source_hash() -> str:
+    with open(ITER_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(workload: str, kernel: str):
+    """HBM bytes per launch from committed rocprofv3 counters, if they were
+    taken on the current kernel source."""
+    try:
+        with open(TRAFFIC) as f:
+            rec = json.load(f)[f"{workload}/{kernel}"]
+    except (OSError, KeyError, ValueError):
+        return None
+    if rec.get("source_sha256_16") != source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, U, I, budget_s: float = 10.0):
+    """The oracle as it stands, on this host: the full workload, repeated
+    until `budget_s` seconds have passed (median per call)."""
+    import numpy as np
+    import oracle
+    oracle.build()
+    p = oracle.OracleParams(filter_size=wl.filter_size, blur=wl.blur, w_app=wl.w_app,
+                            theta_alpha=wl.theta_alpha, theta_beta=wl.theta_beta,
+                            w_smooth=wl.w_smooth, theta_gamma=wl.theta_gamma)
+    times = []
+    t_all = time.perf_counter()
+    while True:
+        t0 = time.perf_counter()
+        oracle.meanfield(U, I, p, wl.iters)
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() - t_all >= budget_s or len(times) >= 50:
+            break
+    t = float(np.median(times))
+    mpi = wl.pixels * wl.iters / 1e6
+    return {"value": round(mpi / t, 3), "unit": UNIT, "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"the full {wl.name} workload ({wl.B}x{wl.C}x{wl.H}x{wl.W}, k={wl.filter_size}, "
+                      f"blur={wl.blur}, T={wl.iters}), {len(times)} calls, median "
+                      f"{t * 1e3:.1f} ms/call, double precision"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="pascal")
+    ap.add_argument("--variant", choices=["fused", "materialised"], default="fused")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py: this library runs on one GPU; --gpus {args.gpus} is not supported "
+              "(batch items or row bands would shard across GPUs, which is not built)",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_1805_04777_amd import convcrf as cc
+    from paper_1805_04777_amd import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    U, I, _ = synth.make_inputs(wl)
+    dev = torch.device("cuda:0")
+    Ut = torch.from_numpy(U).to(dev)
+    It = torch.from_numpy(I).to(dev)
+    out = torch.empty_like(Ut)
+    variant = cc.VARIANT_FUSED if args.variant == "fused" else cc.VARIANT_MATERIALISED
+    p = cc.Params(filter_size=wl.filter_size, blur=wl.blur, variant=variant, w_app=wl.w_app,
+                  theta_alpha=wl.theta_alpha, theta_beta=wl.theta_beta, w_smooth=wl.w_smooth,
+                  theta_gamma=wl.theta_gamma)
+    crf = cc.ConvCRF(0)
+    stream = torch.cuda.current_stream(dev)
+
+    for _ in range(args.warmup):
+        crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
+    torch.cuda.synchronize()
+    crf.profile_enable(True)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = ev0.elapsed_time(ev1)
+    ms = total_ms / args.steps
+    value = wl.pixels * wl.iters / 1e6 / (ms / 1e3)
+
+    # dominant kernel: the per-iteration kernel of the chosen path
+    if wl.blur > 1:
+        kname = "blur_message"
+    else:
+        kname = "fused_iter" if variant == cc.VARIANT_FUSED else "materialised_iter"
+    k_ms, k_n = crf.profile_read(kname)
+    crf.profile_enable(False)
+    avg_s = k_ms / 1e3 / max(k_n, 1)
+    T = wl.iters
+    if wl.blur == 1:
+        F = flops_per_pixel_iter(wl.C, wl.filter_size, True) * wl.pixels
+        Bytes = (bytes_per_pixel(wl.C, True) + (T - 1) * bytes_per_pixel(wl.C, False)) / T * wl.pixels
+        if variant == cc.VARIANT_MATERIALISED:
+            F -= 12 * (wl.filter_size ** 2 - 1) * wl.pixels      # weights are read, not computed
+            Bytes += 4 * (wl.filter_size ** 2 - 1) * wl.pixels   # ... from HBM
+    else:
+        npx = wl.pixels // (wl.blur ** 2)
+        F = flops_per_pixel_iter(wl.C, wl.filter_size, True) * npx
+        Bytes = (8 * wl.C + 12) * npx
+    alu_frac = F / avg_s / PEAK_VALU_FP32 if k_n else None
+    hbm_frac = Bytes / avg_s / PEAK_HBM if k_n else None
+    bound = "alu" if (alu_frac or 0) >= (hbm_frac or 0) else "hbm"
+    if bound == "alu":
+        roof = {"bound": "alu", "achieved": round(F / avg_s / 1e12, 3), "peak": round(PEAK_VALU_FP32 / 1e12, 1),
+                "unit": "TFLOP/s", "frac": round(alu_frac, 4)}
+    else:
+        roof = {"bound": "hbm", "achieved": round(Bytes / avg_s / 1e9, 1), "peak": PEAK_HBM / 1e9,
+                "unit": "GB/s", "frac": round(hbm_frac, 4)}
+    roof["traffic"] = load_traffic(args.workload, kname)
+    roof.update({
+        "kernel": kname, "launches": k_n, "avg_launch_us": round(avg_s * 1e6, 3),
+        "algorithmic_flop_per_launch": int(F), "algorithmic_bytes_per_launch": int(Bytes),
+        "alu_frac": round(alu_frac, 4) if alu_frac else None,
+        "alu_frac_vs_packed_peak": round(F / avg_s / PEAK_VALU_FP32_PACKED, 4) if k_n else None,
+        "hbm_frac": round(hbm_frac, 4) if hbm_frac else None,
+    })
+
+    rec = {
+        "metric": METRIC, "value": round(value, 2), "unit": UNIT, "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded Voronoi images and noisy unaries)",
+        "config": {"workload": f"{wl.name}: B={wl.B} C={wl.C} {wl.H}x{wl.W} k={wl.filter_size} "
+                               f"blur={wl.blur} T={wl.iters} Potts, {args.variant}",
+                   "global_batch": wl.B, "variant": args.variant},
+        "roofline": roof,
+    }
+    crf.close()
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(wl, U, I)
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

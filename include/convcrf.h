@@ -1,0 +1,157 @@
+/*
+ * convcrf.h -- C ABI of the ConvCRF mean-field library for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The library computes truncated mean-field inference in a Convolutional CRF
+ * (Teichmann & Cipolla, "Convolutional CRFs for Semantic Segmentation",
+ * arXiv 1805.04777):
+ *
+ *   Q0 = softmax(U)                                 (Alg. 1, initialisation)
+ *   repeat `iters` times:
+ *     M_p(l) = sum_{q in W(p), q != p} K(p,q) Q_q(l)       (Eq. 6, Alg. 1
+ *                                                            message passing)
+ *     K(p,q) = w_app   exp(-|p-q|^2/2 theta_alpha^2 - |I_p-I_q|^2/2 theta_beta^2)
+ *            + w_smooth exp(-|p-q|^2/2 theta_gamma^2)             (Eq. 4)
+ *     Z_p(l) = U_p(l) - sum_l' mu[l][l'] M_p(l')     (Alg. 1 compatibility
+ *                                                     transform, unary add)
+ *     Q_p    = softmax(Z_p)                          (Alg. 1 normalisation)
+ *
+ * W(p) is the k x k window centred on p (Sec. 4: pixels farther apart are
+ * conditionally independent); neighbours outside the image contribute
+ * nothing.  U are unary logits (minus the unary energy psi_u of Eq. 2), I the
+ * RGB image on its own 0..255 scale, positions are integer pixel coordinates.
+ *
+ * Conventions of every entry point:
+ *   - Tensors are dense, C-contiguous float32 in NCHW order:
+ *       unary [B][C][H][W], image [B][3][H][W], q_out [B][C][H][W].
+ *     All three are DEVICE pointers on the context's GPU, owned by the
+ *     caller; the library never frees or retains them.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Work is enqueued on it and the call returns without waiting; the
+ *     caller synchronises before reading q_out.
+ *   - Every function returns a status code; nothing throws.  Arguments are
+ *     validated before any HIP call, so on an error nothing is enqueued and
+ *     q_out is left untouched.  convcrf_last_error() gives a message.
+ *   - A context is not thread-safe: use one per host thread.  Concurrent
+ *     calls on one context from different streams share its workspace and
+ *     must be ordered by the caller.
+ */
+#ifndef CONVCRF_H
+#define CONVCRF_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CONVCRF_OK = 0,
+    CONVCRF_E_INVALID_ARG = -1,  /* NULL pointer, bad size or parameter */
+    CONVCRF_E_UNSUPPORTED = -2,  /* valid by the definition but not built
+                                    here (C > 32, k > 15, H or W not a
+                                    multiple of the blur factor, ...) */
+    CONVCRF_E_NO_DEVICE = -3,    /* no usable gfx950 device */
+    CONVCRF_E_HIP = -4,          /* a HIP runtime call failed */
+    CONVCRF_E_OOM = -5           /* workspace allocation failed */
+} convcrf_status;
+
+/* Which kernels compute the message (all give the same Q up to rounding). */
+enum {
+    CONVCRF_VARIANT_FUSED = 0,        /* weights recomputed in registers from
+                                         LDS-staged colour tiles (default) */
+    CONVCRF_VARIANT_MATERIALISED = 1  /* kernel matrix K[B][k*k][H][W]
+                                         written once per call (Eq. 5), then
+                                         read by every iteration */
+};
+
+/* Model parameters.  Plain host struct; copied during the call. */
+typedef struct {
+    int32_t filter_size;    /* k, odd, 1 <= k <= 15 (Sec. 4 filter size;
+                               the window is k x k, radius r = (k-1)/2) */
+    int32_t blur;           /* s in {1, 2, 4, 8}.  s = 1: off.  s > 1: the
+                               pooled message of Sec. 4.2 ("blur"): Q and the
+                               features are s x s average pooled (pooled
+                               positions = block centres, so a pooled offset d
+                               is s*d pixels), the k x k message runs on the
+                               pooled grid and is bilinearly upsampled (half-
+                               pixel centres, edge clamp) before the
+                               compatibility step.  H and W must be multiples
+                               of s.  Only the fused variant implements it. */
+    int32_t include_center; /* 0: the centre tap q == p is excluded (Alg. 1
+                               sums over i != j; default).  1: it is included
+                               with weight K(p,p) = w_app + w_smooth, the
+                               literal reading of Eq. 6. */
+    int32_t variant;        /* CONVCRF_VARIANT_* */
+    float w_app;            /* w(1) of Eq. 4, >= 0 */
+    float theta_alpha;      /* position scale of the appearance kernel, > 0 */
+    float theta_beta;       /* colour scale of the appearance kernel, > 0 */
+    float w_smooth;         /* w(2) of Eq. 4, >= 0 */
+    float theta_gamma;      /* position scale of the smoothness kernel, > 0 */
+    const float *compat;    /* HOST pointer to C*C floats, row-major
+                               mu[l][l'] (the 1x1-convolution compatibility
+                               of Sec. 4.2), or NULL for Potts
+                               mu[l][l'] = [l != l'] (Sec. 3). */
+} convcrf_params;
+
+typedef struct convcrf_ctx convcrf_ctx;
+
+/* Fill *p with the defaults used throughout the paper's experiments (Sec. 5:
+ * the DenseCRF hand-crafted kernel): k = 7, no blur, centre excluded, fused,
+ * w_app = 10, theta_alpha = 80, theta_beta = 13, w_smooth = 3,
+ * theta_gamma = 3, Potts.  Returns CONVCRF_E_INVALID_ARG if p is NULL. */
+convcrf_status convcrf_default_params(convcrf_params *p);
+
+/* Check sizes and parameters exactly as convcrf_meanfield does, without a
+ * context, a device or any HIP call.  B, C, H, W: batch, classes, height,
+ * width.  iters >= 0.  Returns CONVCRF_OK or the status meanfield would. */
+convcrf_status convcrf_validate(int B, int C, int H, int W,
+                                const convcrf_params *params, int iters);
+
+/* Create a context bound to HIP device `device` (its gfx950 code objects
+ * are loaded, no workspace is allocated yet).  *out receives the context,
+ * or NULL on failure.  CONVCRF_E_NO_DEVICE if the device does not exist or
+ * is not gfx950. */
+convcrf_status convcrf_init(convcrf_ctx **out, int device);
+
+/* Release the context and its workspace (waits for the device).  NULL is a
+ * no-op. */
+void convcrf_destroy(convcrf_ctx *ctx);
+
+/* Mean-field inference (Alg. 1) for `iters` rounds; see the file comment.
+ * iters = 0 writes softmax(U).  The context owns a workspace (one extra
+ * [B][C][H][W] buffer for the ping-pong of Q, plus pooled buffers for blur
+ * or the kernel matrix for the materialised variant); it grows on demand,
+ * is reused by later calls, and is freed by convcrf_destroy.  q_out must not
+ * overlap unary or image.  Returns CONVCRF_E_HIP on a launch failure (the
+ * message names the HIP error). */
+convcrf_status convcrf_meanfield(convcrf_ctx *ctx, const float *unary,
+                                 const float *image, int B, int C, int H,
+                                 int W, const convcrf_params *params,
+                                 int iters, float *q_out, void *stream);
+
+/* Per-kernel timing with HIP events recorded on the launch stream around
+ * every kernel the library enqueues, for measurement.  enable = 1 starts
+ * (and clears) the record, 0 stops it.  Off by default. */
+convcrf_status convcrf_profile_enable(convcrf_ctx *ctx, int enable);
+
+/* Total elapsed milliseconds and launch count of the kernels named `name`
+ * ("fused_iter", "softmax", "build_kernel", "materialised_iter",
+ * "blur_pool", "blur_message", "blur_update") since profiling was enabled.
+ * Synchronises on the recorded events.  An unknown or unused name gives
+ * 0 ms and 0 launches. */
+convcrf_status convcrf_profile_read(convcrf_ctx *ctx, const char *name,
+                                    double *total_ms, int64_t *launches);
+
+/* Message describing the last failure on ctx (or of a context-free call if
+ * ctx is NULL).  Never NULL; valid until the next call on the same ctx. */
+const char *convcrf_last_error(const convcrf_ctx *ctx);
+
+/* Static name of a status code. */
+const char *convcrf_status_string(convcrf_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CONVCRF_H */

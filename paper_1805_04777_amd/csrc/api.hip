@@ -1,0 +1,490 @@
+// api.hip -- host side of libconvcrf: the C ABI of include/convcrf.h.
+//
+// Validation happens before any HIP call.  The context owns a workspace
+// that grows on demand: one [B][C][H][W] buffer for the ping-pong of Q
+// (the other half of the ping-pong is the caller's q_out), the kernel matrix
+// for the materialised variant, pooled buffers for the blur path, and a
+// small device block holding the compatibility matrix.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/convcrf.h"
+#include "crf_internal.h"
+
+using namespace convcrf;
+
+namespace {
+
+constexpr double kLog2eD = 1.4426950408889634073599;
+constexpr size_t kLdsLimit = 160 * 1024;  // gfx950 LDS per work-group
+
+const char* const kKernelNames[] = {"fused_iter",   "softmax",     "build_kernel",
+                                    "materialised_iter", "blur_pool", "blur_message",
+                                    "blur_update"};
+enum KernelId { kFused = 0, kSoftmax, kBuild, kMatIter, kPool, kBlurMsg, kBlurUpd, kNumKernels };
+
+struct DevBuf {
+    void* p = nullptr;
+    size_t bytes = 0;
+};
+
+struct ProfRec {
+    int kernel;
+    hipEvent_t start, stop;
+};
+
+thread_local std::string g_last_error = "no error";
+
+}  // namespace
+
+struct convcrf_ctx {
+    int device = 0;
+    std::string err = "no error";
+    DevBuf q_ws, kmat, pool_q, pool_m, pool_f, mu;
+    std::vector<float> mu_last;   // host copy of the uploaded compatibility
+    float* mu_pinned = nullptr;   // pinned staging for the upload
+    size_t mu_pinned_cap = 0;
+    hipEvent_t mu_copied = nullptr;
+    bool profiling = false;
+    std::vector<ProfRec> prof;
+    std::vector<hipEvent_t> free_events;
+};
+
+namespace {
+
+convcrf_status fail(convcrf_ctx* ctx, convcrf_status s, const std::string& msg) {
+    if (ctx) ctx->err = msg;
+    else g_last_error = msg;
+    return s;
+}
+
+convcrf_status hip_fail(convcrf_ctx* ctx, hipError_t e, const char* what) {
+    std::string m = std::string(what) + ": " + hipGetErrorString(e);
+    return fail(ctx, CONVCRF_E_HIP, m);
+}
+
+bool finite_pos(float v) { return std::isfinite(v) && v > 0.f; }
+
+convcrf_status validate(convcrf_ctx* ctx, int B, int C, int H, int W, const convcrf_params* p,
+                        int iters) {
+    if (!p) return fail(ctx, CONVCRF_E_INVALID_ARG, "params is NULL");
+    if (B < 0 || H < 0 || W < 0) return fail(ctx, CONVCRF_E_INVALID_ARG, "negative B, H or W");
+    if (C < 1) return fail(ctx, CONVCRF_E_INVALID_ARG, "C must be >= 1");
+    if (iters < 0) return fail(ctx, CONVCRF_E_INVALID_ARG, "iters must be >= 0");
+    const int k = p->filter_size;
+    if (k < 1 || (k & 1) == 0) return fail(ctx, CONVCRF_E_INVALID_ARG, "filter_size must be odd and >= 1");
+    if (k > kMaxK) return fail(ctx, CONVCRF_E_UNSUPPORTED, "filter_size > 15 is not built");
+    if (C > kMaxC) return fail(ctx, CONVCRF_E_UNSUPPORTED, "more than 24 classes is not built");
+    if (p->include_center != 0 && p->include_center != 1)
+        return fail(ctx, CONVCRF_E_INVALID_ARG, "include_center must be 0 or 1");
+    if (p->variant != CONVCRF_VARIANT_FUSED && p->variant != CONVCRF_VARIANT_MATERIALISED)
+        return fail(ctx, CONVCRF_E_INVALID_ARG, "unknown variant");
+    if (!std::isfinite(p->w_app) || !std::isfinite(p->w_smooth))
+        return fail(ctx, CONVCRF_E_INVALID_ARG, "kernel weights must be finite");
+    if (p->w_app < 0.f)
+        return fail(ctx, CONVCRF_E_UNSUPPORTED, "a negative appearance weight is not built");
+    if (!finite_pos(p->theta_alpha) || !finite_pos(p->theta_beta) || !finite_pos(p->theta_gamma))
+        return fail(ctx, CONVCRF_E_INVALID_ARG, "theta parameters must be finite and > 0");
+    const int s = p->blur;
+    if (s != 1 && s != 2 && s != 4 && s != 8)
+        return fail(ctx, CONVCRF_E_INVALID_ARG, "blur must be 1, 2, 4 or 8");
+    if (s > 1 && p->variant != CONVCRF_VARIANT_FUSED)
+        return fail(ctx, CONVCRF_E_UNSUPPORTED, "blur is only built for the fused variant");
+    if (s > 1 && (H % s != 0 || W % s != 0))
+        return fail(ctx, CONVCRF_E_UNSUPPORTED, "H and W must be multiples of the blur factor");
+    const long long npix = (long long)B * H * W;
+    if (npix * (long long)C > (1LL << 40))
+        return fail(ctx, CONVCRF_E_UNSUPPORTED, "tensor too large");
+    if ((long long)H * W > (1LL << 31) - 1)
+        return fail(ctx, CONVCRF_E_UNSUPPORTED, "image plane larger than 2^31 pixels");
+    return CONVCRF_OK;
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    const char* pa = static_cast<const char*>(a);
+    const char* pb = static_cast<const char*>(b);
+    return pa < pb + nb && pb < pa + na;
+}
+
+convcrf_status ensure(convcrf_ctx* ctx, DevBuf& buf, size_t bytes) {
+    if (buf.bytes >= bytes) return CONVCRF_OK;
+    if (buf.p) {
+        hipError_t e = hipDeviceSynchronize();
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipDeviceSynchronize");
+        hipFree(buf.p);
+        buf.p = nullptr;
+        buf.bytes = 0;
+    }
+    hipError_t e = hipMalloc(&buf.p, bytes);
+    if (e != hipSuccess) {
+        buf.p = nullptr;
+        (void)hipGetLastError();
+        return fail(ctx, CONVCRF_E_OOM, std::string("workspace allocation failed: ") + hipGetErrorString(e));
+    }
+    buf.bytes = bytes;
+    return CONVCRF_OK;
+}
+
+// Per-offset constants of Eq. 4 for a k x k window whose grid step is
+// `step` full-resolution pixels (1, or the blur factor on the pooled grid).
+void fill_taps(const convcrf_params& p, int k, int step, TapTable& t) {
+    const int r = (k - 1) / 2;
+    const double ta2 = 2.0 * (double)p.theta_alpha * p.theta_alpha;
+    const double tg2 = 2.0 * (double)p.theta_gamma * p.theta_gamma;
+    const double lw = p.w_app > 0 ? std::log2((double)p.w_app) : -INFINITY;
+    for (int i = 0; i < kMaxTaps; ++i) t.app_log2[i] = t.smooth[i] = 0.f;
+    for (int dy = -r; dy <= r; ++dy)
+        for (int dx = -r; dx <= r; ++dx) {
+            const double d2 = (double)step * step * (dx * dx + dy * dy);
+            const int idx = (dy + r) * k + (dx + r);
+            t.app_log2[idx] = p.w_app > 0 ? (float)(lw - d2 * kLog2eD / ta2) : -INFINITY;
+            t.smooth[idx] = (float)(p.w_smooth * std::exp(-d2 / tg2));
+        }
+}
+
+hipEvent_t take_event(convcrf_ctx* ctx) {
+    if (!ctx->free_events.empty()) {
+        hipEvent_t e = ctx->free_events.back();
+        ctx->free_events.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Launch wrapper: records an event pair around the launch when profiling.
+template <typename F>
+convcrf_status launch(convcrf_ctx* ctx, int kernel, hipStream_t stream, const char* what, F&& fn) {
+    ProfRec rec{kernel, nullptr, nullptr};
+    if (ctx->profiling) {
+        rec.start = take_event(ctx);
+        rec.stop = take_event(ctx);
+        if (rec.start) hipEventRecord(rec.start, stream);
+    }
+    hipError_t e = fn();
+    if (ctx->profiling && rec.start && rec.stop) {
+        hipEventRecord(rec.stop, stream);
+        ctx->prof.push_back(rec);
+    }
+    if (e != hipSuccess) return hip_fail(ctx, e, what);
+    return CONVCRF_OK;
+}
+
+hipError_t launch_iter(const IterArgs& a, int k, bool mat, int rows, size_t lds, hipStream_t s) {
+    switch (k) {
+        case 1: return launch_iter_k1(a, mat, rows, lds, s);
+        case 3: return launch_iter_k3(a, mat, rows, lds, s);
+        case 5: return launch_iter_k5(a, mat, rows, lds, s);
+        case 7: return launch_iter_k7(a, mat, rows, lds, s);
+        case 9: return launch_iter_k9(a, mat, rows, lds, s);
+        case 11: return launch_iter_k11(a, mat, rows, lds, s);
+        case 13: return launch_iter_k13(a, mat, rows, lds, s);
+        case 15: return launch_iter_k15(a, mat, rows, lds, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+// Largest tile height whose LDS fits one work-group.
+int pick_rows(int k, int C, bool colour) {
+    for (int rows : {32, 16, 8})
+        if (iter_lds_bytes(k, C, rows, colour) <= kLdsLimit) return rows;
+    return 0;
+}
+
+// Upload mu (C*C floats) if it differs from what the device holds.
+convcrf_status upload_mu(convcrf_ctx* ctx, const float* mu, int C, hipStream_t stream) {
+    const size_t n = (size_t)C * C;
+    if (ctx->mu_last.size() == n && std::memcmp(ctx->mu_last.data(), mu, n * sizeof(float)) == 0)
+        return CONVCRF_OK;
+    convcrf_status st = ensure(ctx, ctx->mu, n * sizeof(float));
+    if (st != CONVCRF_OK) return st;
+    hipError_t e;
+    if (ctx->mu_pinned_cap < n) {
+        if (ctx->mu_pinned) {
+            if (ctx->mu_copied) hipEventSynchronize(ctx->mu_copied);
+            hipHostFree(ctx->mu_pinned);
+            ctx->mu_pinned = nullptr;
+        }
+        e = hipHostMalloc(reinterpret_cast<void**>(&ctx->mu_pinned), kMaxC * kMaxC * sizeof(float), 0);
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipHostMalloc");
+        ctx->mu_pinned_cap = kMaxC * kMaxC;
+    }
+    if (!ctx->mu_copied) {
+        e = hipEventCreateWithFlags(&ctx->mu_copied, hipEventDisableTiming);
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipEventCreate");
+    } else {
+        e = hipEventSynchronize(ctx->mu_copied);  // previous upload has left the staging
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipEventSynchronize");
+    }
+    std::memcpy(ctx->mu_pinned, mu, n * sizeof(float));
+    e = hipMemcpyAsync(ctx->mu.p, ctx->mu_pinned, n * sizeof(float), hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipMemcpyAsync(compat)");
+    e = hipEventRecord(ctx->mu_copied, stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipEventRecord");
+    ctx->mu_last.assign(mu, mu + n);
+    return CONVCRF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* convcrf_status_string(convcrf_status s) {
+    switch (s) {
+        case CONVCRF_OK: return "CONVCRF_OK";
+        case CONVCRF_E_INVALID_ARG: return "CONVCRF_E_INVALID_ARG";
+        case CONVCRF_E_UNSUPPORTED: return "CONVCRF_E_UNSUPPORTED";
+        case CONVCRF_E_NO_DEVICE: return "CONVCRF_E_NO_DEVICE";
+        case CONVCRF_E_HIP: return "CONVCRF_E_HIP";
+        case CONVCRF_E_OOM: return "CONVCRF_E_OOM";
+    }
+    return "CONVCRF_E_UNKNOWN";
+}
+
+const char* convcrf_last_error(const convcrf_ctx* ctx) {
+    return ctx ? ctx->err.c_str() : g_last_error.c_str();
+}
+
+convcrf_status convcrf_default_params(convcrf_params* p) {
+    if (!p) return fail(nullptr, CONVCRF_E_INVALID_ARG, "params is NULL");
+    p->filter_size = 7;
+    p->blur = 1;
+    p->include_center = 0;
+    p->variant = CONVCRF_VARIANT_FUSED;
+    p->w_app = 10.f;
+    p->theta_alpha = 80.f;
+    p->theta_beta = 13.f;
+    p->w_smooth = 3.f;
+    p->theta_gamma = 3.f;
+    p->compat = nullptr;
+    return CONVCRF_OK;
+}
+
+convcrf_status convcrf_validate(int B, int C, int H, int W, const convcrf_params* params,
+                                int iters) {
+    return validate(nullptr, B, C, H, W, params, iters);
+}
+
+convcrf_status convcrf_init(convcrf_ctx** out, int device) {
+    if (!out) return fail(nullptr, CONVCRF_E_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    int n = 0;
+    hipError_t e = hipGetDeviceCount(&n);
+    if (e != hipSuccess || n <= 0) {
+        (void)hipGetLastError();
+        return fail(nullptr, CONVCRF_E_NO_DEVICE, "no HIP device is visible");
+    }
+    if (device < 0 || device >= n) return fail(nullptr, CONVCRF_E_NO_DEVICE, "device index out of range");
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, device);
+    if (e != hipSuccess) return fail(nullptr, CONVCRF_E_NO_DEVICE, hipGetErrorString(e));
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(nullptr, CONVCRF_E_NO_DEVICE,
+                    std::string("device is ") + prop.gcnArchName + ", library is built for gfx950");
+    convcrf_ctx* ctx = new (std::nothrow) convcrf_ctx();
+    if (!ctx) return fail(nullptr, CONVCRF_E_OOM, "context allocation failed");
+    ctx->device = device;
+    *out = ctx;
+    return CONVCRF_OK;
+}
+
+void convcrf_destroy(convcrf_ctx* ctx) {
+    if (!ctx) return;
+    int prev = 0;
+    hipGetDevice(&prev);
+    hipSetDevice(ctx->device);
+    hipDeviceSynchronize();
+    for (DevBuf* b : {&ctx->q_ws, &ctx->kmat, &ctx->pool_q, &ctx->pool_m, &ctx->pool_f, &ctx->mu})
+        if (b->p) hipFree(b->p);
+    if (ctx->mu_pinned) hipHostFree(ctx->mu_pinned);
+    if (ctx->mu_copied) hipEventDestroy(ctx->mu_copied);
+    for (auto& r : ctx->prof) {
+        hipEventDestroy(r.start);
+        hipEventDestroy(r.stop);
+    }
+    for (hipEvent_t e : ctx->free_events) hipEventDestroy(e);
+    hipSetDevice(prev);
+    delete ctx;
+}
+
+convcrf_status convcrf_profile_enable(convcrf_ctx* ctx, int enable) {
+    if (!ctx) return fail(nullptr, CONVCRF_E_INVALID_ARG, "ctx is NULL");
+    if (enable) {
+        for (auto& r : ctx->prof) {
+            hipEventSynchronize(r.stop);
+            ctx->free_events.push_back(r.start);
+            ctx->free_events.push_back(r.stop);
+        }
+        ctx->prof.clear();
+    }
+    ctx->profiling = enable != 0;
+    return CONVCRF_OK;
+}
+
+convcrf_status convcrf_profile_read(convcrf_ctx* ctx, const char* name, double* total_ms,
+                                    int64_t* launches) {
+    if (!ctx || !name || !total_ms || !launches)
+        return fail(ctx, CONVCRF_E_INVALID_ARG, "NULL argument");
+    int id = -1;
+    for (int i = 0; i < kNumKernels; ++i)
+        if (std::strcmp(name, kKernelNames[i]) == 0) id = i;
+    double tot = 0.0;
+    int64_t cnt = 0;
+    for (auto& r : ctx->prof) {
+        if (r.kernel != id) continue;
+        hipError_t e = hipEventSynchronize(r.stop);
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipEventSynchronize");
+        float ms = 0.f;
+        e = hipEventElapsedTime(&ms, r.start, r.stop);
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipEventElapsedTime");
+        tot += ms;
+        ++cnt;
+    }
+    *total_ms = tot;
+    *launches = cnt;
+    return CONVCRF_OK;
+}
+
+convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const float* image, int B,
+                                 int C, int H, int W, const convcrf_params* params, int iters,
+                                 float* q_out, void* stream_ptr) {
+    if (!ctx) return fail(nullptr, CONVCRF_E_INVALID_ARG, "ctx is NULL");
+    convcrf_status st = validate(ctx, B, C, H, W, params, iters);
+    if (st != CONVCRF_OK) return st;
+    const long long npix = (long long)B * H * W;
+    if (npix == 0) return CONVCRF_OK;  // empty input: nothing to compute
+    if (!unary || !image || !q_out) return fail(ctx, CONVCRF_E_INVALID_ARG, "NULL tensor pointer");
+    const size_t qbytes = sizeof(float) * (size_t)npix * C;
+    const size_t ibytes = sizeof(float) * (size_t)npix * 3;
+    if (overlaps(q_out, qbytes, unary, qbytes) || overlaps(q_out, qbytes, image, ibytes))
+        return fail(ctx, CONVCRF_E_INVALID_ARG, "q_out overlaps unary or image");
+
+    const convcrf_params p = *params;
+    hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+
+    if (iters == 0)
+        return launch(ctx, kSoftmax, stream, "softmax",
+                      [&] { return launch_softmax(unary, q_out, B, C, H * W, stream); });
+
+    const int k = p.filter_size;
+    const int s = p.blur;
+    const bool mat = p.variant == CONVCRF_VARIANT_MATERIALISED;
+    const float* mu_dev = nullptr;
+    if (p.compat) {
+        st = upload_mu(ctx, p.compat, C, stream);
+        if (st != CONVCRF_OK) return st;
+        mu_dev = static_cast<const float*>(ctx->mu.p);
+    }
+
+    IterArgs a{};
+    a.mu = mu_dev;
+    a.include_center = p.include_center;
+    a.neg_beta = (float)(-kLog2eD / (2.0 * (double)p.theta_beta * p.theta_beta));
+    a.center_w = (float)((double)p.w_app + (double)p.w_smooth);
+    fill_taps(p, k, s, a.taps);
+
+    if (s == 1) {
+        const int rows = pick_rows(k, C, !mat);
+        if (rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
+        const size_t lds = iter_lds_bytes(k, C, rows, !mat);
+        if (iters > 1) {
+            st = ensure(ctx, ctx->q_ws, qbytes);
+            if (st != CONVCRF_OK) return st;
+        }
+        if (mat) {
+            st = ensure(ctx, ctx->kmat, sizeof(float) * (size_t)npix * (k * k - 1));
+            if (st != CONVCRF_OK) return st;
+            if (k > 1) {
+                st = launch(ctx, kBuild, stream, "build_kernel", [&] {
+                    return launch_build_kernel(image, static_cast<float*>(ctx->kmat.p), B, H, W, k,
+                                               a.neg_beta, a.taps, stream);
+                });
+                if (st != CONVCRF_OK) return st;
+            }
+        }
+        a.C = C;
+        a.H = H;
+        a.W = W;
+        a.unary = unary;
+        a.feat = image;
+        a.kmat = static_cast<const float*>(ctx->kmat.p);
+        a.tiles_x = (W + kTileW - 1) / kTileW;
+        a.tiles_per_img = a.tiles_x * ((H + rows - 1) / rows);
+        a.ntiles = a.tiles_per_img * B;
+        a.mode = kModeUpdate;
+        const bool aligned = (reinterpret_cast<uintptr_t>(unary) % 16 == 0) &&
+                             (reinterpret_cast<uintptr_t>(q_out) % 16 == 0) &&
+                             (!ctx->q_ws.p || reinterpret_cast<uintptr_t>(ctx->q_ws.p) % 16 == 0);
+        a.vec4 = (W % 4 == 0) && aligned;
+        float* ws = static_cast<float*>(ctx->q_ws.p);
+        // the last iteration writes q_out; earlier ones alternate so that
+        // source and destination always differ
+        const float* cur = unary;
+        for (int t = 0; t < iters; ++t) {
+            float* dst = ((iters - 1 - t) % 2 == 0) ? q_out : ws;
+            a.src = cur;
+            a.dst = dst;
+            a.first = t == 0;
+            st = launch(ctx, mat ? kMatIter : kFused, stream, mat ? "materialised_iter" : "fused_iter",
+                        [&] { return launch_iter(a, k, mat, rows, lds, stream); });
+            if (st != CONVCRF_OK) return st;
+            cur = dst;
+        }
+        return CONVCRF_OK;
+    }
+
+    // ---- blur: message on the s x s pooled grid (Sec. 4.2)
+    const int Hp = H / s, Wp = W / s;
+    const size_t pbytes = sizeof(float) * (size_t)B * Hp * Wp;
+    if ((st = ensure(ctx, ctx->pool_q, pbytes * C)) != CONVCRF_OK) return st;
+    if ((st = ensure(ctx, ctx->pool_m, pbytes * C)) != CONVCRF_OK) return st;
+    if ((st = ensure(ctx, ctx->pool_f, pbytes * 3)) != CONVCRF_OK) return st;
+    float* qp = static_cast<float*>(ctx->pool_q.p);
+    float* mp = static_cast<float*>(ctx->pool_m.p);
+    float* fp = static_cast<float*>(ctx->pool_f.p);
+    const int rows = pick_rows(k, C, true);
+    if (rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
+    const size_t lds = iter_lds_bytes(k, C, rows, true);
+
+    st = launch(ctx, kPool, stream, "blur_pool",
+                [&] { return launch_pool(image, fp, B, 3, H, W, s, 0, stream); });
+    if (st != CONVCRF_OK) return st;
+    st = launch(ctx, kPool, stream, "blur_pool",
+                [&] { return launch_pool(unary, qp, B, C, H, W, s, 1, stream); });
+    if (st != CONVCRF_OK) return st;
+
+    a.C = C;
+    a.H = Hp;
+    a.W = Wp;
+    a.unary = nullptr;
+    a.feat = fp;
+    a.kmat = nullptr;
+    a.src = qp;
+    a.dst = mp;
+    a.first = 0;
+    a.mode = kModeMessage;
+    a.tiles_x = (Wp + kTileW - 1) / kTileW;
+    a.tiles_per_img = a.tiles_x * ((Hp + rows - 1) / rows);
+    a.ntiles = a.tiles_per_img * B;
+    a.vec4 = (Wp % 4 == 0);
+    for (int t = 0; t < iters; ++t) {
+        st = launch(ctx, kBlurMsg, stream, "blur_message",
+                    [&] { return launch_iter(a, k, false, rows, lds, stream); });
+        if (st != CONVCRF_OK) return st;
+        const bool last = t == iters - 1;
+        st = launch(ctx, kBlurUpd, stream, "blur_update", [&] {
+            return launch_blur_update(mp, unary, mu_dev, last ? q_out : nullptr, last ? nullptr : qp,
+                                      B, C, H, W, s, stream);
+        });
+        if (st != CONVCRF_OK) return st;
+    }
+    return CONVCRF_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,120 @@
+// crf_internal.h -- launch structures and launcher declarations shared by the
+// HIP translation units of libconvcrf.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstddef>
+#include <cstdint>
+
+namespace convcrf {
+
+// Largest window side k and class count the kernels are built for.
+constexpr int kMaxK = 15;
+constexpr int kMaxTaps = kMaxK * kMaxK;
+constexpr int kMaxC = 24;
+
+// Output tile: TW columns, tile_rows rows (chosen per launch); each thread
+// owns PX horizontally adjacent pixels of one row.
+constexpr int kTileW = 32;
+constexpr int kPix = 4;
+constexpr int kThreadsPerRow = kTileW / kPix;
+
+// The Eq. 4 kernel split into its per-offset and its per-pixel parts.  For
+// the offset d = (dx, dy) of tap t = (dy + r) * k + (dx + r), with |d|^2
+// measured in full-resolution pixels:
+//   app_log2[t] = log2(w_app) - |d|^2 log2(e) / (2 theta_alpha^2)
+//   smooth[t]   = w_smooth exp(-|d|^2 / (2 theta_gamma^2))
+// so that K(p, p + d) = exp2(app_log2[t] + neg_beta |I_p - I_{p+d}|^2)
+//                       + smooth[t],  neg_beta = -log2(e) / (2 theta_beta^2).
+struct TapTable {
+    float app_log2[kMaxTaps];
+    float smooth[kMaxTaps];
+};
+
+enum IterMode : int {
+    kModeUpdate = 0,   // message -> compatibility -> + unary -> softmax -> Q
+    kModeMessage = 1,  // message only -> M (pooled message of the blur path)
+};
+
+// Arguments of one message-passing launch over a grid of H x W cells.
+struct IterArgs {
+    const float* src;     // Q_t [B][C][H][W], or U when `first` (softmax
+                          // applied while staging)
+    const float* unary;   // U [B][C][H][W] (update mode)
+    const float* feat;    // colour planes [B][3][H][W] of the same grid
+    const float* kmat;    // materialised weights [B][k*k-1][H][W] or null
+    const float* mu;      // device C x C row-major compatibility, null = Potts
+    float* dst;           // Q_{t+1} (update) or M (message), [B][C][H][W]
+    int C, H, W;
+    int tiles_x, tiles_per_img, ntiles;
+    int first;            // stage softmax(src) instead of src
+    int include_center;   // add (w_app + w_smooth) Q_p to the message
+    int mode;             // IterMode
+    int vec4;             // W % 4 == 0 and 16-byte aligned planes
+    float neg_beta;
+    float center_w;
+    TapTable taps;
+};
+
+// LDS bytes of one iteration work-group for a k x k window, C classes,
+// `rows` tile rows, with or without the three colour planes.
+inline size_t iter_lds_bytes(int k, int C, int rows, bool with_colour) {
+    const int r = (k - 1) / 2;
+    const int lw = kTileW + 2 * r;
+    const int ls = (lw + 3) & ~3;
+    const int lh = rows + 2 * r;
+    return sizeof(float) * (size_t)(C + (with_colour ? 3 : 0)) * lh * ls;
+}
+
+// One launcher per window side k (each compiled in its own object).
+// `rows` in {8, 16, 32}; `nblocks` = a.ntiles.
+#define CONVCRF_DECLARE_ITER(K)                                              \
+    hipError_t launch_iter_k##K(const IterArgs& a, bool materialised,        \
+                                int rows, size_t lds, hipStream_t stream);
+CONVCRF_DECLARE_ITER(1)
+CONVCRF_DECLARE_ITER(3)
+CONVCRF_DECLARE_ITER(5)
+CONVCRF_DECLARE_ITER(7)
+CONVCRF_DECLARE_ITER(9)
+CONVCRF_DECLARE_ITER(11)
+CONVCRF_DECLARE_ITER(13)
+CONVCRF_DECLARE_ITER(15)
+#undef CONVCRF_DECLARE_ITER
+
+// Q = softmax(U) over classes, per pixel (Alg. 1 initialisation).
+hipError_t launch_softmax(const float* U, float* Q, int B, int C, int HW,
+                          hipStream_t stream);
+
+// Materialised kernel matrix (Eq. 5 merged over both Gaussians): for every
+// pixel and every off-centre tap, K(p, p + d), or 0 where p + d lies outside
+// the image.  out [B][k*k-1][H][W].
+hipError_t launch_build_kernel(const float* image, float* out, int B, int H,
+                               int W, int k, float neg_beta,
+                               const TapTable& taps, hipStream_t stream);
+
+// Blur path (pooled message).
+// s x s average of `nch` planes per image; if `softmax_first`, each pixel's
+// C values are replaced by their softmax before averaging.
+hipError_t launch_pool(const float* src, float* dst, int B, int nch, int H,
+                       int W, int s, int softmax_first, hipStream_t stream);
+// Bilinear upsampling of the pooled message M [B][C][H/s][W/s], then
+// compatibility, unary and softmax at full resolution.  If q_full is set
+// it receives Q [B][C][H][W]; otherwise q_pooled receives the s x s average
+// of Q, [B][C][H/s][W/s].
+hipError_t launch_blur_update(const float* m_pooled, const float* unary,
+                              const float* mu, float* q_full, float* q_pooled,
+                              int B, int C, int H, int W, int s,
+                              hipStream_t stream);
+
+// Block-to-tile order that keeps the tiles of one XCD spatially contiguous.
+// Work-groups are dispatched round-robin over the 8 XCDs of the chip, so
+// block b runs on XCD b % 8; XCD x receives the contiguous tile range that
+// starts at x * (n / 8) + min(x, n % 8).
+__device__ __forceinline__ int xcd_tile(int b, int n) {
+    const int x = b & 7;
+    const int q = n >> 3;
+    const int rem = n & 7;
+    return x * q + (x < rem ? x : rem) + (b >> 3);
+}
+
+}  // namespace convcrf

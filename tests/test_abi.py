@@ -1,0 +1,128 @@
+"""The C ABI of libconvcrf, checked without a GPU.
+
+The library must load, export every function that include/convcrf.h declares,
+and reject invalid arguments with the documented status before touching the
+device (convcrf_validate needs no context and makes no HIP call).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1805_04777_amd import convcrf as cc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "convcrf.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(convcrf_[a-z_]+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(cc.LIB_PATH):
+        from paper_1805_04777_amd import build
+        build.build()
+    return cc.load_library()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("convcrf_init", "convcrf_meanfield", "convcrf_destroy", "convcrf_validate",
+              "convcrf_last_error"):
+        assert n in names
+    assert set(names) == set(cc.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_struct_layout_matches_header(lib):
+    # 4 int32 + 5 float + pointer, no packing surprises
+    assert ctypes.sizeof(cc.CParams) == 4 * 4 + 5 * 4 + 4 + 8
+    assert cc.CParams.compat.offset == 40
+
+
+def test_default_params(lib):
+    p = cc.default_params()
+    assert (p.filter_size, p.blur, p.include_center, p.variant) == (7, 1, False, cc.VARIANT_FUSED)
+    assert (p.w_app, p.theta_alpha, p.theta_beta, p.w_smooth, p.theta_gamma) == (10, 80, 13, 3, 3)
+    assert p.compat is None
+
+
+def test_status_strings(lib):
+    for code, name in [(cc.OK, "CONVCRF_OK"), (cc.E_INVALID_ARG, "CONVCRF_E_INVALID_ARG"),
+                       (cc.E_UNSUPPORTED, "CONVCRF_E_UNSUPPORTED"),
+                       (cc.E_NO_DEVICE, "CONVCRF_E_NO_DEVICE"), (cc.E_HIP, "CONVCRF_E_HIP"),
+                       (cc.E_OOM, "CONVCRF_E_OOM")]:
+        assert lib.convcrf_status_string(code).decode() == name
+
+
+def P(**kw):
+    return cc.Params(**kw)
+
+
+@pytest.mark.parametrize("args,status", [
+    ((1, 21, 64, 64, P(), 5), cc.OK),
+    ((8, 19, 1024, 2048, P(), 5), cc.OK),
+    ((1, 21, 512, 512, P(filter_size=11, blur=4), 5), cc.OK),
+    ((0, 21, 64, 64, P(), 5), cc.OK),                      # empty batch
+    ((1, 21, 0, 64, P(), 5), cc.OK),                       # empty image
+    ((1, 21, 64, 64, P(), 0), cc.OK),
+    ((1, 1, 3, 3, P(filter_size=1), 2), cc.OK),
+    ((1, 24, 8, 8, P(filter_size=15), 1), cc.OK),
+    ((-1, 21, 64, 64, P(), 5), cc.E_INVALID_ARG),
+    ((1, 0, 64, 64, P(), 5), cc.E_INVALID_ARG),
+    ((1, 21, -4, 64, P(), 5), cc.E_INVALID_ARG),
+    ((1, 21, 64, 64, P(), -1), cc.E_INVALID_ARG),
+    ((1, 21, 64, 64, P(filter_size=6), 5), cc.E_INVALID_ARG),
+    ((1, 21, 64, 64, P(filter_size=0), 5), cc.E_INVALID_ARG),
+    ((1, 21, 64, 64, P(filter_size=17), 5), cc.E_UNSUPPORTED),
+    ((1, 25, 64, 64, P(), 5), cc.E_UNSUPPORTED),
+    ((1, 21, 64, 64, P(include_center=2), 5), cc.E_INVALID_ARG),
+    ((1, 21, 64, 64, P(variant=7), 5), cc.E_INVALID_ARG),
+    ((1, 21, 64, 64, P(theta_alpha=0.0), 5), cc.E_INVALID_ARG),
+    ((1, 21, 64, 64, P(theta_beta=-1.0), 5), cc.E_INVALID_ARG),
+    ((1, 21, 64, 64, P(theta_gamma=float("inf")), 5), cc.E_INVALID_ARG),
+    ((1, 21, 64, 64, P(w_smooth=float("nan")), 5), cc.E_INVALID_ARG),
+    ((1, 21, 64, 64, P(w_app=-1.0), 5), cc.E_UNSUPPORTED),
+    ((1, 21, 64, 64, P(blur=3), 5), cc.E_INVALID_ARG),
+    ((1, 21, 66, 64, P(blur=4), 5), cc.E_UNSUPPORTED),     # H not a multiple of s
+    ((1, 21, 64, 64, P(blur=2, variant=cc.VARIANT_MATERIALISED), 5), cc.E_UNSUPPORTED),
+])
+def test_validation(lib, args, status):
+    B, C, H, W, p, T = args
+    assert cc.validate(B, C, H, W, p, T) == status
+
+
+def test_validation_null_params(lib):
+    assert lib.convcrf_validate(1, 21, 8, 8, None, 1) == cc.E_INVALID_ARG
+    assert "params" in lib.convcrf_last_error(None).decode()
+
+
+def test_null_context_is_rejected(lib):
+    p = P().c()
+    st = lib.convcrf_meanfield(None, 1, 2, 1, 21, 8, 8, ctypes.byref(p), 1, 3, None)
+    assert st == cc.E_INVALID_ARG
+    assert lib.convcrf_profile_enable(None, 1) == cc.E_INVALID_ARG
+    lib.convcrf_destroy(None)  # no-op
+
+
+def test_init_rejects_null_out(lib):
+    assert lib.convcrf_init(None, 0) == cc.E_INVALID_ARG
+
+
+def test_init_without_a_gpu_reports_no_device(lib):
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    h = ctypes.c_void_p(1234)
+    assert lib.convcrf_init(ctypes.byref(h), 0) == cc.E_NO_DEVICE
+    assert h.value is None
