@@ -98,6 +98,26 @@ def cpu_baseline(wl, U, I, budget_s: float = 10.0):
                       f"{t * 1e3:.1f} ms/call, double precision"}
 
 
+def copy_reference(torch, mib: int, steps: int) -> int:
+    """Plain copy of `mib` MiB, `steps` times: each dispatch reads and writes
+    exactly mib MiB, which calibrates the rocprofv3 byte counters."""
+    n = mib * (1 << 20) // 4
+    x = torch.rand(n, device="cuda:0")
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        y.copy_(x)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    print(json.dumps({"copy_mib": mib, "ms_per_copy": round(ms, 5),
+                      "GB_per_s": round(2 * mib * (1 << 20) / (ms / 1e3) / 1e9, 1)}), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -106,6 +126,9 @@ def main(argv=None):
     ap.add_argument("--workload", default="pascal")
     ap.add_argument("--variant", choices=["fused", "materialised"], default="fused")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="instead: time a plain device-to-device copy of this many MiB "
+                         "(reference dispatch for the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py: this library runs on one GPU; --gpus {args.gpus} is not supported "
@@ -114,6 +137,9 @@ def main(argv=None):
         return 2
 
     import torch
+
+    if args.copy_mib:
+        return copy_reference(torch, args.copy_mib, args.steps)
 
     from paper_1805_04777_amd import convcrf as cc
     from paper_1805_04777_amd import synth
@@ -134,10 +160,9 @@ def main(argv=None):
     for _ in range(args.warmup):
         crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
     torch.cuda.synchronize()
-    crf.profile_enable(True)
+    # timed pass: K steps, nothing recorded between the library's launches
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     ev0.record(stream)
     for _ in range(args.steps):
         crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
@@ -146,6 +171,12 @@ def main(argv=None):
     total_ms = ev0.elapsed_time(ev1)
     ms = total_ms / args.steps
     value = wl.pixels * wl.iters / 1e6 / (ms / 1e3)
+    # kernel pass: the same K steps with HIP events recorded by the library
+    # around every launch, on the launch stream
+    crf.profile_enable(True)
+    for _ in range(args.steps):
+        crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
+    torch.cuda.synchronize()
 
     # dominant kernel: the per-iteration kernel of the chosen path
     if wl.blur > 1:

@@ -11,7 +11,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/convcrf.h"
+#include "convcrf.h"
 #include "crf_internal.h"
 
 using namespace convcrf;
@@ -128,21 +128,18 @@ convcrf_status ensure(convcrf_ctx* ctx, DevBuf& buf, size_t bytes) {
     return CONVCRF_OK;
 }
 
-// Per-offset constants of Eq. 4 for a k x k window whose grid step is
-// `step` full-resolution pixels (1, or the blur factor on the pooled grid).
-void fill_taps(const convcrf_params& p, int k, int step, TapTable& t) {
-    const int r = (k - 1) / 2;
+// Per-offset constants of Eq. 4, indexed by n = dx^2 + dy^2 on a grid whose
+// step is `step` full-resolution pixels (1, or the blur factor on the pooled
+// grid).
+void fill_taps(const convcrf_params& p, int step, TapTable& t) {
     const double ta2 = 2.0 * (double)p.theta_alpha * p.theta_alpha;
     const double tg2 = 2.0 * (double)p.theta_gamma * p.theta_gamma;
     const double lw = p.w_app > 0 ? std::log2((double)p.w_app) : -INFINITY;
-    for (int i = 0; i < kMaxTaps; ++i) t.app_log2[i] = t.smooth[i] = 0.f;
-    for (int dy = -r; dy <= r; ++dy)
-        for (int dx = -r; dx <= r; ++dx) {
-            const double d2 = (double)step * step * (dx * dx + dy * dy);
-            const int idx = (dy + r) * k + (dx + r);
-            t.app_log2[idx] = p.w_app > 0 ? (float)(lw - d2 * kLog2eD / ta2) : -INFINITY;
-            t.smooth[idx] = (float)(p.w_smooth * std::exp(-d2 / tg2));
-        }
+    for (int n = 0; n <= kMaxN; ++n) {
+        const double d2 = (double)step * step * n;
+        t.app_log2[n] = p.w_app > 0 ? (float)(lw - d2 * kLog2eD / ta2) : -INFINITY;
+        t.smooth[n] = (float)(p.w_smooth * std::exp(-d2 / tg2));
+    }
 }
 
 hipEvent_t take_event(convcrf_ctx* ctx) {
@@ -174,25 +171,31 @@ convcrf_status launch(convcrf_ctx* ctx, int kernel, hipStream_t stream, const ch
     return CONVCRF_OK;
 }
 
-hipError_t launch_iter(const IterArgs& a, int k, bool mat, int rows, size_t lds, hipStream_t s) {
+hipError_t launch_iter(const IterArgs& a, int k, bool mat, TileConfig t, size_t lds, hipStream_t s) {
     switch (k) {
-        case 1: return launch_iter_k1(a, mat, rows, lds, s);
-        case 3: return launch_iter_k3(a, mat, rows, lds, s);
-        case 5: return launch_iter_k5(a, mat, rows, lds, s);
-        case 7: return launch_iter_k7(a, mat, rows, lds, s);
-        case 9: return launch_iter_k9(a, mat, rows, lds, s);
-        case 11: return launch_iter_k11(a, mat, rows, lds, s);
-        case 13: return launch_iter_k13(a, mat, rows, lds, s);
-        case 15: return launch_iter_k15(a, mat, rows, lds, s);
+        case 1: return launch_iter_k1(a, mat, t, lds, s);
+        case 3: return launch_iter_k3(a, mat, t, lds, s);
+        case 5: return launch_iter_k5(a, mat, t, lds, s);
+        case 7: return launch_iter_k7(a, mat, t, lds, s);
+        case 9: return launch_iter_k9(a, mat, t, lds, s);
+        case 11: return launch_iter_k11(a, mat, t, lds, s);
+        case 13: return launch_iter_k13(a, mat, t, lds, s);
+        case 15: return launch_iter_k15(a, mat, t, lds, s);
         default: return hipErrorInvalidValue;
     }
 }
 
-// Largest tile height whose LDS fits one work-group.
-int pick_rows(int k, int C, bool colour) {
-    for (int rows : {32, 16, 8})
-        if (iter_lds_bytes(k, C, rows, colour) <= kLdsLimit) return rows;
-    return 0;
+// Tile of the iteration kernel: the first candidate whose LDS fits one
+// work-group (rows = 0 if none does).  Up to k = 7, two pixels per thread
+// (512 threads, two waves per SIMD) hide LDS latency best; wider windows
+// keep four pixels per thread, where the two-pixel body no longer fits the
+// registers of two waves.
+TileConfig pick_tile(int k, int C, bool colour, bool compat) {
+    const TileConfig narrow[] = {{32, 2}, {16, 2}, {8, 2}};
+    const TileConfig wide[] = {{32, 4}, {16, 4}, {8, 4}};
+    for (TileConfig t : (k <= 7 ? narrow : wide))
+        if (iter_lds_bytes(k, C, t, colour, compat) <= kLdsLimit) return t;
+    return TileConfig{0, 4};
 }
 
 // Upload mu (C*C floats) if it differs from what the device holds.
@@ -387,12 +390,12 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     a.include_center = p.include_center;
     a.neg_beta = (float)(-kLog2eD / (2.0 * (double)p.theta_beta * p.theta_beta));
     a.center_w = (float)((double)p.w_app + (double)p.w_smooth);
-    fill_taps(p, k, s, a.taps);
+    fill_taps(p, s, a.taps);
 
     if (s == 1) {
-        const int rows = pick_rows(k, C, !mat);
-        if (rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
-        const size_t lds = iter_lds_bytes(k, C, rows, !mat);
+        const TileConfig tile = pick_tile(k, C, !mat, mu_dev != nullptr);
+        if (tile.rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
+        const size_t lds = iter_lds_bytes(k, C, tile, !mat, mu_dev != nullptr);
         if (iters > 1) {
             st = ensure(ctx, ctx->q_ws, qbytes);
             if (st != CONVCRF_OK) return st;
@@ -415,13 +418,14 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
         a.feat = image;
         a.kmat = static_cast<const float*>(ctx->kmat.p);
         a.tiles_x = (W + kTileW - 1) / kTileW;
-        a.tiles_per_img = a.tiles_x * ((H + rows - 1) / rows);
+        a.tiles_per_img = a.tiles_x * ((H + tile.rows - 1) / tile.rows);
         a.ntiles = a.tiles_per_img * B;
         a.mode = kModeUpdate;
-        const bool aligned = (reinterpret_cast<uintptr_t>(unary) % 16 == 0) &&
-                             (reinterpret_cast<uintptr_t>(q_out) % 16 == 0) &&
-                             (!ctx->q_ws.p || reinterpret_cast<uintptr_t>(ctx->q_ws.p) % 16 == 0);
-        a.vec4 = (W % 4 == 0) && aligned;
+        const uintptr_t va = 4u * tile.pix;
+        const bool aligned = (reinterpret_cast<uintptr_t>(unary) % va == 0) &&
+                             (reinterpret_cast<uintptr_t>(q_out) % va == 0) &&
+                             (!ctx->q_ws.p || reinterpret_cast<uintptr_t>(ctx->q_ws.p) % va == 0);
+        a.vec = (W % tile.pix == 0) && aligned;
         float* ws = static_cast<float*>(ctx->q_ws.p);
         // the last iteration writes q_out; earlier ones alternate so that
         // source and destination always differ
@@ -432,7 +436,7 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
             a.dst = dst;
             a.first = t == 0;
             st = launch(ctx, mat ? kMatIter : kFused, stream, mat ? "materialised_iter" : "fused_iter",
-                        [&] { return launch_iter(a, k, mat, rows, lds, stream); });
+                        [&] { return launch_iter(a, k, mat, tile, lds, stream); });
             if (st != CONVCRF_OK) return st;
             cur = dst;
         }
@@ -448,9 +452,9 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     float* qp = static_cast<float*>(ctx->pool_q.p);
     float* mp = static_cast<float*>(ctx->pool_m.p);
     float* fp = static_cast<float*>(ctx->pool_f.p);
-    const int rows = pick_rows(k, C, true);
-    if (rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
-    const size_t lds = iter_lds_bytes(k, C, rows, true);
+    const TileConfig tile = pick_tile(k, C, true, false);
+    if (tile.rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
+    const size_t lds = iter_lds_bytes(k, C, tile, true, false);
 
     st = launch(ctx, kPool, stream, "blur_pool",
                 [&] { return launch_pool(image, fp, B, 3, H, W, s, 0, stream); });
@@ -470,12 +474,12 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     a.first = 0;
     a.mode = kModeMessage;
     a.tiles_x = (Wp + kTileW - 1) / kTileW;
-    a.tiles_per_img = a.tiles_x * ((Hp + rows - 1) / rows);
+    a.tiles_per_img = a.tiles_x * ((Hp + tile.rows - 1) / tile.rows);
     a.ntiles = a.tiles_per_img * B;
-    a.vec4 = (Wp % 4 == 0);
+    a.vec = (Wp % tile.pix == 0);
     for (int t = 0; t < iters; ++t) {
         st = launch(ctx, kBlurMsg, stream, "blur_message",
-                    [&] { return launch_iter(a, k, false, rows, lds, stream); });
+                    [&] { return launch_iter(a, k, false, tile, lds, stream); });
         if (st != CONVCRF_OK) return st;
         const bool last = t == iters - 1;
         st = launch(ctx, kBlurUpd, stream, "blur_update", [&] {

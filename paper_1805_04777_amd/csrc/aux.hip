@@ -73,13 +73,14 @@ __global__ __launch_bounds__(256) void build_kernel_kernel(const float* __restri
     for (int t = 0; t < k * k; ++t) {
         if (t == ctr) continue;
         const int dy = t / k - r, dx = t % k - r;
+        const int n = dx * dx + dy * dy;
         const int yy = y + dy, xx = x + dx;
         float w = 0.f;
         if (yy >= 0 && yy < H && xx >= 0 && xx < W) {
             const long long q = (long long)yy * W + xx;
             const float d0 = r0 - img[q], d1 = g0 - img[HW + q], d2 = b0 - img[2 * HW + q];
             const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
-            w = __builtin_amdgcn_exp2f(fmaf(col2, neg_beta, taps.app_log2[t])) + taps.smooth[t];
+            w = __builtin_amdgcn_exp2f(fmaf(col2, neg_beta, taps.app_log2[n])) + taps.smooth[n];
         }
         o[(size_t)(t < ctr ? t : t - 1) * HW] = w;
     }

@@ -10,25 +10,30 @@ namespace convcrf {
 
 // Largest window side k and class count the kernels are built for.
 constexpr int kMaxK = 15;
-constexpr int kMaxTaps = kMaxK * kMaxK;
 constexpr int kMaxC = 24;
 
-// Output tile: TW columns, tile_rows rows (chosen per launch); each thread
-// owns PX horizontally adjacent pixels of one row.
+// Output tile: 32 columns by `rows` rows (chosen per launch); each thread
+// owns `pix` (2 or 4) horizontally adjacent pixels of one row.
 constexpr int kTileW = 32;
-constexpr int kPix = 4;
-constexpr int kThreadsPerRow = kTileW / kPix;
 
-// The Eq. 4 kernel split into its per-offset and its per-pixel parts.  For
-// the offset d = (dx, dy) of tap t = (dy + r) * k + (dx + r), with |d|^2
-// measured in full-resolution pixels:
-//   app_log2[t] = log2(w_app) - |d|^2 log2(e) / (2 theta_alpha^2)
-//   smooth[t]   = w_smooth exp(-|d|^2 / (2 theta_gamma^2))
-// so that K(p, p + d) = exp2(app_log2[t] + neg_beta |I_p - I_{p+d}|^2)
-//                       + smooth[t],  neg_beta = -log2(e) / (2 theta_beta^2).
+struct TileConfig {
+    int rows;  // output rows per work-group
+    int pix;   // pixels per thread: 2 or 4
+    int threads() const { return (kTileW / pix) * rows; }
+};
+
+// The Eq. 4 kernel split into its per-offset and its per-pixel parts.  Both
+// Gaussians depend on the offset d = (dx, dy) only through n = dx^2 + dy^2
+// (grid units; a grid step is `step` full-resolution pixels, so
+// |d|^2 = step^2 n), which takes few distinct values in a window:
+//   app_log2[n] = log2(w_app) - step^2 n log2(e) / (2 theta_alpha^2)
+//   smooth[n]   = w_smooth exp(-step^2 n / (2 theta_gamma^2))
+// so that K(p, p + d) = exp2(app_log2[n] + neg_beta |I_p - I_{p+d}|^2)
+//                       + smooth[n],  neg_beta = -log2(e) / (2 theta_beta^2).
+constexpr int kMaxN = 2 * ((kMaxK - 1) / 2) * ((kMaxK - 1) / 2);
 struct TapTable {
-    float app_log2[kMaxTaps];
-    float smooth[kMaxTaps];
+    float app_log2[kMaxN + 1];
+    float smooth[kMaxN + 1];
 };
 
 enum IterMode : int {
@@ -50,27 +55,35 @@ struct IterArgs {
     int first;            // stage softmax(src) instead of src
     int include_center;   // add (w_app + w_smooth) Q_p to the message
     int mode;             // IterMode
-    int vec4;             // W % 4 == 0 and 16-byte aligned planes
+    int vec;              // W % pix == 0 and planes aligned to 4*pix bytes:
+                          // each thread loads and stores its pixels as one
+                          // vector per plane
     float neg_beta;
     float center_w;
     TapTable taps;
 };
 
-// LDS bytes of one iteration work-group for a k x k window, C classes,
-// `rows` tile rows, with or without the three colour planes.
-inline size_t iter_lds_bytes(int k, int C, int rows, bool with_colour) {
-    const int r = (k - 1) / 2;
-    const int lw = kTileW + 2 * r;
-    const int ls = (lw + 3) & ~3;
-    const int lh = rows + 2 * r;
-    return sizeof(float) * (size_t)(C + (with_colour ? 3 : 0)) * lh * ls;
+// LDS row stride (floats) of a staged tile row: the 32 + 2r staged columns
+// rounded up to a multiple of the per-thread pixel count, so that every
+// thread's window row starts on a 4*pix-byte boundary.
+constexpr int iter_lds_stride(int k, int pix) {
+    return (kTileW + (k - 1) + pix - 1) / pix * pix;
 }
 
-// One launcher per window side k (each compiled in its own object).
-// `rows` in {8, 16, 32}; `nblocks` = a.ntiles.
+// LDS bytes of one iteration work-group for a k x k window, C classes,
+// with or without the three colour planes and the C x C compatibility.
+inline size_t iter_lds_bytes(int k, int C, TileConfig t, bool with_colour, bool with_compat) {
+    const int lh = t.rows + (k - 1);
+    return sizeof(float) * ((size_t)(C + (with_colour ? 3 : 0)) * lh * iter_lds_stride(k, t.pix) +
+                            (with_compat ? (size_t)C * C : 0));
+}
+
+// One launcher per window side k (each compiled in its own object); one
+// work-group per tile, a.ntiles work-groups.
 #define CONVCRF_DECLARE_ITER(K)                                              \
     hipError_t launch_iter_k##K(const IterArgs& a, bool materialised,        \
-                                int rows, size_t lds, hipStream_t stream);
+                                TileConfig tile, size_t lds,                 \
+                                hipStream_t stream);
 CONVCRF_DECLARE_ITER(1)
 CONVCRF_DECLARE_ITER(3)
 CONVCRF_DECLARE_ITER(5)
