@@ -42,6 +42,7 @@ thread_local std::string g_last_error = "no error";
 
 struct convcrf_ctx {
     int device = 0;
+    int num_cus = 256;
     std::string err = "no error";
     DevBuf q_ws, kmat, pool_q, pool_m, pool_f, mu;
     std::vector<float> mu_last;   // host copy of the uploaded compatibility
@@ -114,7 +115,7 @@ convcrf_status ensure(convcrf_ctx* ctx, DevBuf& buf, size_t bytes) {
     if (buf.p) {
         hipError_t e = hipDeviceSynchronize();
         if (e != hipSuccess) return hip_fail(ctx, e, "hipDeviceSynchronize");
-        hipFree(buf.p);
+        (void)hipFree(buf.p);
         buf.p = nullptr;
         buf.bytes = 0;
     }
@@ -160,42 +161,53 @@ convcrf_status launch(convcrf_ctx* ctx, int kernel, hipStream_t stream, const ch
     if (ctx->profiling) {
         rec.start = take_event(ctx);
         rec.stop = take_event(ctx);
-        if (rec.start) hipEventRecord(rec.start, stream);
+        if (rec.start) (void)hipEventRecord(rec.start, stream);
     }
     hipError_t e = fn();
     if (ctx->profiling && rec.start && rec.stop) {
-        hipEventRecord(rec.stop, stream);
+        (void)hipEventRecord(rec.stop, stream);
         ctx->prof.push_back(rec);
     }
     if (e != hipSuccess) return hip_fail(ctx, e, what);
     return CONVCRF_OK;
 }
 
-hipError_t launch_iter(const IterArgs& a, int k, bool mat, TileConfig t, size_t lds, hipStream_t s) {
+hipError_t launch_iter(const IterArgs& a, int k, bool mat, TileConfig t, int nchunks, size_t lds,
+                       hipStream_t s) {
     switch (k) {
-        case 1: return launch_iter_k1(a, mat, t, lds, s);
-        case 3: return launch_iter_k3(a, mat, t, lds, s);
-        case 5: return launch_iter_k5(a, mat, t, lds, s);
-        case 7: return launch_iter_k7(a, mat, t, lds, s);
-        case 9: return launch_iter_k9(a, mat, t, lds, s);
-        case 11: return launch_iter_k11(a, mat, t, lds, s);
-        case 13: return launch_iter_k13(a, mat, t, lds, s);
-        case 15: return launch_iter_k15(a, mat, t, lds, s);
+        case 1: return launch_iter_k1(a, mat, t, nchunks, lds, s);
+        case 3: return launch_iter_k3(a, mat, t, nchunks, lds, s);
+        case 5: return launch_iter_k5(a, mat, t, nchunks, lds, s);
+        case 7: return launch_iter_k7(a, mat, t, nchunks, lds, s);
+        case 9: return launch_iter_k9(a, mat, t, nchunks, lds, s);
+        case 11: return launch_iter_k11(a, mat, t, nchunks, lds, s);
+        case 13: return launch_iter_k13(a, mat, t, nchunks, lds, s);
+        case 15: return launch_iter_k15(a, mat, t, nchunks, lds, s);
         default: return hipErrorInvalidValue;
     }
 }
 
+int tiles_of(TileConfig t, int B, int H, int W) {
+    return B * ((H + t.rows - 1) / t.rows) * ((W + t.width - 1) / t.width);
+}
+
 // Tile of the iteration kernel: the first candidate whose LDS fits one
-// work-group (rows = 0 if none does).  Up to k = 7, two pixels per thread
-// (512 threads, two waves per SIMD) hide LDS latency best; wider windows
-// keep four pixels per thread, where the two-pixel body no longer fits the
-// registers of two waves.
-TileConfig pick_tile(int k, int C, bool colour, bool compat) {
-    const TileConfig narrow[] = {{32, 2}, {16, 2}, {8, 2}};
-    const TileConfig wide[] = {{32, 4}, {16, 4}, {8, 4}};
-    for (TileConfig t : (k <= 7 ? narrow : wide))
+// work-group (rows = 0 if none does).  Up to k = 7 the fused kernel runs 1024
+// threads on a 32 x 32 tile, two pixels per thread and two row groups (four
+// waves per SIMD hide the LDS and memory latency best); the materialised
+// variant and wider windows keep one row group, the latter with four pixels
+// per thread.
+TileConfig pick_tile(int k, int C, bool colour, bool compat, bool mat) {
+    const TileConfig narrow[] = {{32, 2, 32, 1}, {16, 2, 32, 1}, {8, 2, 32, 1}, {32, 2, 32, 2}};
+    const TileConfig wide[] = {{32, 4, 32, 1}, {16, 4, 32, 1}, {8, 4, 32, 1}};
+    const TileConfig* cand = k <= 7 ? narrow : wide;
+    const int ncand = k <= 7 ? 4 : 3;
+    for (int i = 0; i < ncand; ++i) {
+        const TileConfig t = cand[i];
+        if (t.split > 1 && mat) continue;
         if (iter_lds_bytes(k, C, t, colour, compat) <= kLdsLimit) return t;
-    return TileConfig{0, 4};
+    }
+    return TileConfig{0, 4, 32, 1};
 }
 
 // Upload mu (C*C floats) if it differs from what the device holds.
@@ -208,8 +220,8 @@ convcrf_status upload_mu(convcrf_ctx* ctx, const float* mu, int C, hipStream_t s
     hipError_t e;
     if (ctx->mu_pinned_cap < n) {
         if (ctx->mu_pinned) {
-            if (ctx->mu_copied) hipEventSynchronize(ctx->mu_copied);
-            hipHostFree(ctx->mu_pinned);
+            if (ctx->mu_copied) (void)hipEventSynchronize(ctx->mu_copied);
+            (void)hipHostFree(ctx->mu_pinned);
             ctx->mu_pinned = nullptr;
         }
         e = hipHostMalloc(reinterpret_cast<void**>(&ctx->mu_pinned), kMaxC * kMaxC * sizeof(float), 0);
@@ -291,6 +303,7 @@ convcrf_status convcrf_init(convcrf_ctx** out, int device) {
     convcrf_ctx* ctx = new (std::nothrow) convcrf_ctx();
     if (!ctx) return fail(nullptr, CONVCRF_E_OOM, "context allocation failed");
     ctx->device = device;
+    ctx->num_cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
     *out = ctx;
     return CONVCRF_OK;
 }
@@ -298,19 +311,19 @@ convcrf_status convcrf_init(convcrf_ctx** out, int device) {
 void convcrf_destroy(convcrf_ctx* ctx) {
     if (!ctx) return;
     int prev = 0;
-    hipGetDevice(&prev);
-    hipSetDevice(ctx->device);
-    hipDeviceSynchronize();
+    (void)hipGetDevice(&prev);
+    (void)hipSetDevice(ctx->device);
+    (void)hipDeviceSynchronize();
     for (DevBuf* b : {&ctx->q_ws, &ctx->kmat, &ctx->pool_q, &ctx->pool_m, &ctx->pool_f, &ctx->mu})
-        if (b->p) hipFree(b->p);
-    if (ctx->mu_pinned) hipHostFree(ctx->mu_pinned);
-    if (ctx->mu_copied) hipEventDestroy(ctx->mu_copied);
+        if (b->p) (void)hipFree(b->p);
+    if (ctx->mu_pinned) (void)hipHostFree(ctx->mu_pinned);
+    if (ctx->mu_copied) (void)hipEventDestroy(ctx->mu_copied);
     for (auto& r : ctx->prof) {
-        hipEventDestroy(r.start);
-        hipEventDestroy(r.stop);
+        (void)hipEventDestroy(r.start);
+        (void)hipEventDestroy(r.stop);
     }
-    for (hipEvent_t e : ctx->free_events) hipEventDestroy(e);
-    hipSetDevice(prev);
+    for (hipEvent_t e : ctx->free_events) (void)hipEventDestroy(e);
+    (void)hipSetDevice(prev);
     delete ctx;
 }
 
@@ -318,7 +331,7 @@ convcrf_status convcrf_profile_enable(convcrf_ctx* ctx, int enable) {
     if (!ctx) return fail(nullptr, CONVCRF_E_INVALID_ARG, "ctx is NULL");
     if (enable) {
         for (auto& r : ctx->prof) {
-            hipEventSynchronize(r.stop);
+            (void)hipEventSynchronize(r.stop);
             ctx->free_events.push_back(r.start);
             ctx->free_events.push_back(r.stop);
         }
@@ -393,7 +406,7 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     fill_taps(p, s, a.taps);
 
     if (s == 1) {
-        const TileConfig tile = pick_tile(k, C, !mat, mu_dev != nullptr);
+        const TileConfig tile = pick_tile(k, C, !mat, mu_dev != nullptr, mat);
         if (tile.rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
         const size_t lds = iter_lds_bytes(k, C, tile, !mat, mu_dev != nullptr);
         if (iters > 1) {
@@ -412,12 +425,13 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
             }
         }
         a.C = C;
+        a.planes = C;
         a.H = H;
         a.W = W;
         a.unary = unary;
         a.feat = image;
         a.kmat = static_cast<const float*>(ctx->kmat.p);
-        a.tiles_x = (W + kTileW - 1) / kTileW;
+        a.tiles_x = (W + tile.width - 1) / tile.width;
         a.tiles_per_img = a.tiles_x * ((H + tile.rows - 1) / tile.rows);
         a.ntiles = a.tiles_per_img * B;
         a.mode = kModeUpdate;
@@ -436,7 +450,7 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
             a.dst = dst;
             a.first = t == 0;
             st = launch(ctx, mat ? kMatIter : kFused, stream, mat ? "materialised_iter" : "fused_iter",
-                        [&] { return launch_iter(a, k, mat, tile, lds, stream); });
+                        [&] { return launch_iter(a, k, mat, tile, 1, lds, stream); });
             if (st != CONVCRF_OK) return st;
             cur = dst;
         }
@@ -452,10 +466,22 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     float* qp = static_cast<float*>(ctx->pool_q.p);
     float* mp = static_cast<float*>(ctx->pool_m.p);
     float* fp = static_cast<float*>(ctx->pool_f.p);
-    const TileConfig tile = pick_tile(k, C, true, false);
+    // pooled grid: full-width tiles if they give every CU two work-groups,
+    // otherwise 16 x 16 tiles shared by four row groups, with the classes
+    // split into chunks (the message does not mix classes; each chunk
+    // recomputes the weights)
+    TileConfig tile = pick_tile(k, C, true, false, false);
     if (tile.rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
-    const size_t lds = iter_lds_bytes(k, C, tile, true, false);
-
+    int nchunks = 1, chunk = C;
+    if (tiles_of(tile, B, Hp, Wp) < 2 * ctx->num_cus) {
+        tile = TileConfig{16, 4, 16, 4};
+        const int tiles = tiles_of(tile, B, Hp, Wp);
+        nchunks = (2 * ctx->num_cus + tiles - 1) / tiles;
+        nchunks = nchunks < 1 ? 1 : (nchunks > (C + 3) / 4 ? (C + 3) / 4 : nchunks);  // >= 4 classes each
+        chunk = (C + nchunks - 1) / nchunks;
+        nchunks = (C + chunk - 1) / chunk;
+    }
+    const size_t lds = iter_lds_bytes(k, chunk, tile, true, false);
     st = launch(ctx, kPool, stream, "blur_pool",
                 [&] { return launch_pool(image, fp, B, 3, H, W, s, 0, stream); });
     if (st != CONVCRF_OK) return st;
@@ -463,7 +489,8 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
                 [&] { return launch_pool(unary, qp, B, C, H, W, s, 1, stream); });
     if (st != CONVCRF_OK) return st;
 
-    a.C = C;
+    a.C = chunk;
+    a.planes = C;
     a.H = Hp;
     a.W = Wp;
     a.unary = nullptr;
@@ -473,13 +500,13 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     a.dst = mp;
     a.first = 0;
     a.mode = kModeMessage;
-    a.tiles_x = (Wp + kTileW - 1) / kTileW;
+    a.tiles_x = (Wp + tile.width - 1) / tile.width;
     a.tiles_per_img = a.tiles_x * ((Hp + tile.rows - 1) / tile.rows);
     a.ntiles = a.tiles_per_img * B;
     a.vec = (Wp % tile.pix == 0);
     for (int t = 0; t < iters; ++t) {
         st = launch(ctx, kBlurMsg, stream, "blur_message",
-                    [&] { return launch_iter(a, k, false, tile, lds, stream); });
+                    [&] { return launch_iter(a, k, false, tile, nchunks, lds, stream); });
         if (st != CONVCRF_OK) return st;
         const bool last = t == iters - 1;
         st = launch(ctx, kBlurUpd, stream, "blur_update", [&] {

@@ -12,14 +12,14 @@ namespace convcrf {
 constexpr int kMaxK = 15;
 constexpr int kMaxC = 24;
 
-// Output tile: 32 columns by `rows` rows (chosen per launch); each thread
-// owns `pix` (2 or 4) horizontally adjacent pixels of one row.
-constexpr int kTileW = 32;
-
+// Output tile: `width` (32, or 16 for small grids) columns by `rows` rows;
+// each thread owns `pix` (2 or 4) horizontally adjacent pixels of one row.
 struct TileConfig {
-    int rows;  // output rows per work-group
-    int pix;   // pixels per thread: 2 or 4
-    int threads() const { return (kTileW / pix) * rows; }
+    int rows;       // output rows per work-group
+    int pix;        // pixels per thread: 2 or 4
+    int width = 32; // output columns per work-group: 32 or 16
+    int split = 1;  // row groups sharing the tile (each a band of window rows)
+    int threads() const { return (width / pix) * rows * split; }
 };
 
 // The Eq. 4 kernel split into its per-offset and its per-pixel parts.  Both
@@ -50,7 +50,9 @@ struct IterArgs {
     const float* kmat;    // materialised weights [B][k*k-1][H][W] or null
     const float* mu;      // device C x C row-major compatibility, null = Potts
     float* dst;           // Q_{t+1} (update) or M (message), [B][C][H][W]
-    int C, H, W;
+    int C, H, W;          // C: classes this launch computes (a chunk of the
+                          // image's classes in message mode, grid dim y)
+    int planes;           // class planes per image in src / dst / unary
     int tiles_x, tiles_per_img, ntiles;
     int first;            // stage softmax(src) instead of src
     int include_center;   // add (w_app + w_smooth) Q_p to the message
@@ -63,26 +65,39 @@ struct IterArgs {
     TapTable taps;
 };
 
-// LDS row stride (floats) of a staged tile row: the 32 + 2r staged columns
-// rounded up to a multiple of the per-thread pixel count, so that every
-// thread's window row starts on a 4*pix-byte boundary.
-constexpr int iter_lds_stride(int k, int pix) {
-    return (kTileW + (k - 1) + pix - 1) / pix * pix;
+// LDS row stride (floats) of a staged tile row: the width + 2r staged
+// columns rounded up to a multiple of the per-thread pixel count, so that
+// every thread's window row starts on a 4*pix-byte boundary.
+constexpr int iter_lds_stride(int k, int pix, int width) {
+    return (width + (k - 1) + pix - 1) / pix * pix;
 }
 
 // LDS bytes of one iteration work-group for a k x k window, C classes,
 // with or without the three colour planes and the C x C compatibility.
+// Floats of the LDS region shared by the staged planes (Q and, unless
+// materialised, the three colour planes) and, after the message, the row
+// groups' S - 1 partial messages per pixel: the larger of the two.  The
+// C x C compatibility matrix, when given, follows it.
+inline size_t iter_lds_stage_floats(int k, int C, TileConfig t, bool with_colour) {
+    const size_t staged = (size_t)(C + (with_colour ? 3 : 0)) * (t.rows + (k - 1)) *
+                          iter_lds_stride(k, t.pix, t.width);
+    const size_t partials = (size_t)(t.split - 1) * C * t.rows * t.width;
+    return staged > partials ? staged : partials;
+}
+
+// LDS bytes of one iteration work-group for a k x k window and C classes.
 inline size_t iter_lds_bytes(int k, int C, TileConfig t, bool with_colour, bool with_compat) {
-    const int lh = t.rows + (k - 1);
-    return sizeof(float) * ((size_t)(C + (with_colour ? 3 : 0)) * lh * iter_lds_stride(k, t.pix) +
+    return sizeof(float) * (iter_lds_stage_floats(k, C, t, with_colour) +
                             (with_compat ? (size_t)C * C : 0));
 }
 
 // One launcher per window side k (each compiled in its own object); one
-// work-group per tile, a.ntiles work-groups.
+// work-group per tile and class chunk: a.ntiles x nchunks work-groups, chunk
+// j computing classes [j*a.C, (j+1)*a.C) (message mode only; nchunks = 1
+// otherwise).
 #define CONVCRF_DECLARE_ITER(K)                                              \
     hipError_t launch_iter_k##K(const IterArgs& a, bool materialised,        \
-                                TileConfig tile, size_t lds,                 \
+                                TileConfig tile, int nchunks, size_t lds,    \
                                 hipStream_t stream);
 CONVCRF_DECLARE_ITER(1)
 CONVCRF_DECLARE_ITER(3)

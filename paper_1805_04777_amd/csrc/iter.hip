@@ -1,7 +1,7 @@
 // iter.hip -- one mean-field iteration of a Convolutional CRF on gfx950.
 //
 // Compiled once per window side k (-DCRF_K=k).  One work-group owns a tile
-// of 32 x rows output pixels of one image; it stages Q_t (or softmax(U) on the
+// of TW x rows output pixels of one image (TW = 32, or 16 for small grids); it stages Q_t (or softmax(U) on the
 // first iteration, Alg. 1 initialisation) and the colour planes of the tile
 // plus an r-pixel halo in LDS, with zeros outside the image, so that
 // neighbours outside the image contribute nothing to the message.  Each
@@ -31,9 +31,15 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
-// P floats as one vector (P = 2 or 4).
+// P floats as one vector (P = 1, 2 or 4).
 template <int P>
 struct Vec;
+template <>
+struct Vec<1> {
+    using T = float;
+    __device__ static void get(const T& v, float* o) { o[0] = v; }
+    __device__ static T make(const float* i) { return i[0]; }
+};
 template <>
 struct Vec<2> {
     using T = float2;
@@ -94,30 +100,38 @@ __device__ __forceinline__ void softmax_regs(float (&z)[CM], int C) {
     for (int c = 0; c < CM; ++c) z[c] *= inv;
 }
 
-template <int K, int CM, bool EXACT, bool MAT, int P>
-// P = 4: 256 threads and a 146 KB tile, one wave per SIMD; P = 2: 512
-// threads, two waves per SIMD.  Declaring that occupancy lets the scheduler
-// spend registers on keeping LDS reads in flight.
-__global__ __launch_bounds__(P == 4 ? 256 : 512)
-__attribute__((amdgpu_waves_per_eu(P == 4 ? 1 : 2, P == 4 ? 1 : 2)))
+// Threads = (TW / P) * rows * S: S groups of whole wavefronts share one
+// staged tile, group g taking window rows [g*K/S, (g+1)*K/S) of every pixel.
+// At the 146 KB tile of k = 7 that gives 1 (P = 4), 2 (P = 2) or 4 (P = 2,
+// S = 2) waves per SIMD; declaring it lets the scheduler size registers.
+template <int K, int CM, bool EXACT, bool MAT, int P, int TW, int S>
+__global__ __launch_bounds__(TW == 16 ? 256 : (P == 4 ? 256 : 512) * S)
+__attribute__((amdgpu_waves_per_eu(TW == 16 ? 1 : (P == 4 ? 1 : 2) * S,
+                                   TW == 16 ? 4 : (P == 4 ? 1 : 2) * S)))
 void iter_kernel(const IterArgs a) {
     constexpr int R = (K - 1) / 2;
-    constexpr int LW = kTileW + 2 * R;        // staged columns
-    constexpr int LS = iter_lds_stride(K, P);
+    constexpr int LW = TW + 2 * R;            // staged columns
+    constexpr int LS = iter_lds_stride(K, P, TW);
     constexpr int NW = P + K - 1;             // staged values per window row
     constexpr int KK = K * K;
     constexpr int CTR = R * K + R;            // centre tap index
-    constexpr int TPR = kTileW / P;           // threads per tile row
-    constexpr int kStagePix = 3;
+    constexpr int TPR = TW / P;               // threads per tile row
+    constexpr int kStagePix = S == 1 ? 3 : 2;
+    constexpr int FP = P / S;                 // pixels each thread finalises
+    static_assert(P % S == 0, "each row group finalises P / S pixels");
     using V = Vec<P>;
+    using VF = Vec<FP>;
 
     extern __shared__ float4 smem4[];
     float* const smem = reinterpret_cast<float*>(smem4);
 
-    const int C = EXACT ? CM : a.C;
+    // classes of this work-group: all of them, or one chunk (message mode;
+    // the last chunk may be short)
+    const int C = EXACT ? CM : min(a.C, a.planes - (int)blockIdx.y * a.C);
     const int H = a.H, W = a.W;
     const int nthreads = blockDim.x;
-    const int rows = nthreads / TPR;
+    const int gthreads = nthreads / S;        // threads per row group
+    const int rows = gthreads / TPR;
     const int LH = rows + 2 * R;
     const int plane = LH * LS;
 
@@ -144,16 +158,20 @@ void iter_kernel(const IterArgs a) {
     const int trem = tile - b * a.tiles_per_img;
     const int tyi = trem / a.tiles_x;
     const int y0 = tyi * rows;
-    const int x0 = (trem - tyi * a.tiles_x) * kTileW;
+    const int x0 = (trem - tyi * a.tiles_x) * TW;
+    // class chunk of this work-group (message mode): planes [c0, c0 + C)
+    const size_t cbase = (size_t)b * a.planes + (size_t)blockIdx.y * a.C;
 
     const size_t HW = (size_t)H * W;
-    const float* __restrict__ src = a.src + (size_t)b * C * HW;
+    const float* __restrict__ src = a.src + cbase * HW;
     const float* __restrict__ feat = a.feat + (size_t)b * 3 * HW;
 
     float* const Qs = smem;                   // [C][LH][LS]
     float* const Cs = smem + C * plane;       // [3][LH][LS]
-    // compatibility matrix [C][C] (only when given; read back as broadcasts)
-    float* const Ms = smem + (C + (MAT ? 0 : 3)) * plane;
+    // compatibility matrix [C][C] (only when given; read back as broadcasts),
+    // after the larger of the staged planes and the row groups' partials
+    const int stage_floats = max((C + (MAT ? 0 : 3)) * plane, (S - 1) * C * rows * TW);
+    float* const Ms = smem + stage_floats;
 
     // ---- stage Q_t (or softmax(U)) and colours, tile + halo, zero outside.
     // kStagePix halo pixels per thread and round; every plane of all of them
@@ -190,9 +208,12 @@ void iter_kernel(const IterArgs a) {
             for (int ch = 0; ch < 3; ++ch) Cs[ch * plane + l] = f[ch];
         }
     };
-    const int tx = tid % TPR;
-    const int ty = tid / TPR;
+    const int grp = tid / gthreads;           // row group (uniform per wave)
+    const int gtid = tid - grp * gthreads;
+    const int tx = gtid % TPR;
+    const int ty = gtid / TPR;
     const int col0 = tx * P;                  // first staged column read
+    const int dy_lo = grp * K / S, dy_hi = (grp + 1) * K / S;
     const int y = y0 + ty;
     const int xb = x0 + col0;
     const bool pix_ok = y < H;
@@ -209,7 +230,7 @@ void iter_kernel(const IterArgs a) {
     for (int i = 0; i < P; ++i)
 #pragma unroll
         for (int c = 0; c < CM; ++c) acc[i][c] = 0.f;
-    if (unary_first && pix_ok) load_pixels(acc, a.unary + (size_t)b * C * HW + (size_t)y * W + xb, xb, fullv);
+    if (unary_first && pix_ok && grp == 0) load_pixels(acc, a.unary + cbase * HW + (size_t)y * W + xb, xb, fullv);
 
     if (general_compat)
         for (int i = tid; i < C * C; i += nthreads) Ms[i] = a.mu[i];
@@ -286,8 +307,8 @@ void iter_kernel(const IterArgs a) {
                 }
             }
         }
-        // classes two at a time, the next row of Q read while the current
-        // one is applied
+        // classes in order, the rows of the next kDepth - 1 classes read from
+        // LDS while the current one is applied (a rolling pipeline)
         auto apply = [&](const float (&q)[NW], int c) {
 #pragma unroll
             for (int i = 0; i < P; ++i)
@@ -298,29 +319,32 @@ void iter_kernel(const IterArgs a) {
                         acc[i][c] = fmaf(w[i][dx], q[i + dx], acc[i][c]);
         };
         const float* qrow = Qs + row * LS + col0;
-        float qa[NW], qb[NW];
-        lds_row<NW, P>(qrow, qa);
+        constexpr int kDepth = 3;
+        float qr[kDepth][NW];
 #pragma unroll
-        for (int c = 0; c < CM; c += 2) {
+        for (int j = 0; j < kDepth - 1; ++j)
+            if (j < CM && (EXACT || j < C)) lds_row<NW, P>(qrow + j * plane, qr[j]);
+#pragma unroll
+        for (int c = 0; c < CM; ++c) {
             if (EXACT || c < C) {
-                const bool has1 = c + 1 < CM && (EXACT || c + 1 < C);
-                if (has1) lds_row<NW, P>(qrow + (c + 1) * plane, qb);
-                apply(qa, c);
-                if (has1) {
-                    if (c + 2 < CM && (EXACT || c + 2 < C)) lds_row<NW, P>(qrow + (c + 2) * plane, qa);
-                    apply(qb, c + 1);
-                }
+                const int nx = c + kDepth - 1;
+                if (nx < CM && (EXACT || nx < C)) lds_row<NW, P>(qrow + nx * plane, qr[nx % kDepth]);
+                apply(qr[c % kDepth], c);
+                // one class per scheduling region: its reads are issued
+                // kDepth - 1 classes ahead and are not batched with later ones
+                if constexpr (kUnrollRows) __builtin_amdgcn_sched_barrier(0);
             }
         }
     };
     if constexpr (kUnrollRows) {
 #pragma unroll
-        for (int dy = 0; dy < K; ++dy) window_row(dy);
+        for (int dy = 0; dy < K; ++dy)
+            if (S == 1 || (dy >= dy_lo && dy < dy_hi)) window_row(dy);
     } else {
 #pragma unroll 1
-        for (int dy = 0; dy < K; ++dy) window_row(dy);
+        for (int dy = dy_lo; dy < dy_hi; ++dy) window_row(dy);
     }
-    if (a.include_center) {
+    if (a.include_center && grp == 0) {
 #pragma unroll
         for (int c = 0; c < CM; ++c) {
             if (EXACT || c < C) {
@@ -331,62 +355,123 @@ void iter_kernel(const IterArgs a) {
         }
     }
 
+    // ---- combine the row groups: pixel i of a thread is finalised by group
+    // i / FP; the other groups leave their partial messages for it in LDS
+    // (the staging area, no longer read), summed in a fixed group order
+    float fin[FP][CM];
+    if constexpr (S == 1) {
+#pragma unroll
+        for (int i = 0; i < P; ++i)
+#pragma unroll
+            for (int c = 0; c < CM; ++c) fin[i][c] = acc[i][c];
+    } else {
+        const int npx = rows * TW;
+        float* const Rs = smem;               // [S - 1][C][npx]
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < P; ++i) {
+            const int f = i / FP;
+            if (f != grp) {
+                const int slot = (grp - f - 1 + S) % S;
+                float* r = Rs + (size_t)slot * C * npx + ty * TW + col0 + i;
+#pragma unroll
+                for (int c = 0; c < CM; ++c)
+                    if (EXACT || c < C) r[c * npx] = acc[i][c];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int g = 0; g < S; ++g) {
+            if (g != grp) continue;           // uniform: one branch taken
+#pragma unroll
+            for (int j = 0; j < FP; ++j) {
+                const int i = g * FP + j;
+                const float* r = Rs + ty * TW + col0 + i;
+#pragma unroll
+                for (int c = 0; c < CM; ++c) {
+                    float v = acc[i][c];
+                    if (EXACT || c < C) {
+                        // partials in the order of their groups after g
+#pragma unroll
+                        for (int sl = 0; sl < S - 1; ++sl) v += r[((size_t)sl * C + c) * npx];
+                    }
+                    fin[j][c] = v;
+                }
+            }
+        }
+    }
+
+    const int xf = xb + grp * FP;             // first finalised pixel
+    const bool fullf = a.vec && xf + FP <= W && (FP == P || (xf % FP) == 0);
     if (!pix_ok) return;
-    float* __restrict__ dst = a.dst + (size_t)b * C * HW + (size_t)y * W + xb;
+    float* __restrict__ dst = a.dst + cbase * HW + (size_t)y * W + xf;
 
     if (a.mode == kModeUpdate) {
-        // compatibility transform: acc <- -mu * M (general mu only; with
-        // Potts acc already holds U + M)
+        // compatibility transform: fin <- U - mu * M (general mu only; with
+        // Potts fin already holds U + M)
         if (general_compat) {
-            // Z = U - mu M, one row of mu at a time (a scheduling barrier per
-            // row keeps the broadcast reads of mu from all being hoisted);
-            // the unary is loaded first so that it arrives meanwhile
-            float u[P][CM];
-            load_pixels(u, a.unary + (size_t)b * C * HW + (size_t)y * W + xb, xb, fullv);
-            float z[P][CM];
+            // one row of mu at a time (a scheduling barrier per row keeps the
+            // broadcast reads of mu from all being hoisted); the unary is
+            // loaded first so that it arrives meanwhile
+            float u[FP][CM];
+            const float* ug = a.unary + cbase * HW + (size_t)y * W + xf;
+#pragma unroll
+            for (int c = 0; c < CM; ++c) {
+                if (!EXACT && c >= C) continue;
+                if (fullf) {
+                    float tmp[FP];
+                    VF::get(*reinterpret_cast<const typename VF::T*>(ug + c * HW), tmp);
+#pragma unroll
+                    for (int j = 0; j < FP; ++j) u[j][c] = tmp[j];
+                } else {
+#pragma unroll
+                    for (int j = 0; j < FP; ++j) u[j][c] = (xf + j < W) ? ug[c * HW + j] : 0.f;
+                }
+            }
+            float z[FP][CM];
 #pragma unroll
             for (int l = 0; l < CM; ++l) {
                 if (EXACT || l < C) {
-                    float t[P];
+                    float t[FP];
 #pragma unroll
-                    for (int i = 0; i < P; ++i) t[i] = 0.f;
+                    for (int j = 0; j < FP; ++j) t[j] = 0.f;
 #pragma unroll
                     for (int lp = 0; lp < CM; ++lp) {
                         if (EXACT || lp < C) {
                             const float m = Ms[l * C + lp];
 #pragma unroll
-                            for (int i = 0; i < P; ++i) t[i] = fmaf(m, acc[i][lp], t[i]);
+                            for (int j = 0; j < FP; ++j) t[j] = fmaf(m, fin[j][lp], t[j]);
                         }
                     }
 #pragma unroll
-                    for (int i = 0; i < P; ++i) z[i][l] = u[i][l] - t[i];
+                    for (int j = 0; j < FP; ++j) z[j][l] = u[j][l] - t[j];
                 } else {
 #pragma unroll
-                    for (int i = 0; i < P; ++i) z[i][l] = 0.f;
+                    for (int j = 0; j < FP; ++j) z[j][l] = 0.f;
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
 #pragma unroll
-            for (int i = 0; i < P; ++i)
+            for (int j = 0; j < FP; ++j)
 #pragma unroll
-                for (int c = 0; c < CM; ++c) acc[i][c] = z[i][c];
+                for (int c = 0; c < CM; ++c) fin[j][c] = z[j][c];
         }
 #pragma unroll
-        for (int i = 0; i < P; ++i) softmax_regs<CM, EXACT>(acc[i], C);
+        for (int j = 0; j < FP; ++j) softmax_regs<CM, EXACT>(fin[j], C);
     }
 
 #pragma unroll
     for (int c = 0; c < CM; ++c) {
         if (!EXACT && c >= C) continue;
-        if (fullv) {
-            float tmp[P];
+        if (fullf) {
+            float tmp[FP];
 #pragma unroll
-            for (int i = 0; i < P; ++i) tmp[i] = acc[i][c];
-            *reinterpret_cast<typename V::T*>(dst + c * HW) = V::make(tmp);
+            for (int j = 0; j < FP; ++j) tmp[j] = fin[j][c];
+            *reinterpret_cast<typename VF::T*>(dst + c * HW) = VF::make(tmp);
         } else {
 #pragma unroll
-            for (int i = 0; i < P; ++i)
-                if (xb + i < W) dst[c * HW + i] = acc[i][c];
+            for (int j = 0; j < FP; ++j)
+                if (xf + j < W) dst[c * HW + j] = fin[j][c];
         }
     }
 }
@@ -406,22 +491,35 @@ hipError_t allow_full_lds(Fn fn) {
     return e;
 }
 
-template <int K, int CM, bool EXACT, bool MAT, int P>
-hipError_t launch_one(const IterArgs& a, TileConfig t, size_t lds, hipStream_t stream) {
-    auto fn = iter_kernel<K, CM, EXACT, MAT, P>;
+template <int K, int CM, bool EXACT, bool MAT, int P, int TW, int S>
+hipError_t launch_one(const IterArgs& a, TileConfig t, int nchunks, size_t lds,
+                      hipStream_t stream) {
+    auto fn = iter_kernel<K, CM, EXACT, MAT, P, TW, S>;
     hipError_t e = allow_full_lds(fn);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(fn, dim3(a.ntiles), dim3(t.threads()), lds, stream, a);
+    hipLaunchKernelGGL(fn, dim3(a.ntiles, nchunks), dim3(t.threads()), lds, stream, a);
     return hipGetLastError();
 }
 
+// The built tile shapes: {P = 2 or 4, width 32, S = 1}, {P = 2, width 32,
+// S = 2} (fused only) and {P = 4, width 16, S = 4} (fused, small grids).
 template <int K, int CM, bool EXACT>
-hipError_t launch_cm(const IterArgs& a, bool mat, TileConfig t, size_t lds, hipStream_t stream) {
+hipError_t launch_cm(const IterArgs& a, bool mat, TileConfig t, int nchunks, size_t lds,
+                     hipStream_t stream) {
+    if (t.width == 16) {
+        if (mat || t.pix != 4 || t.split != 4) return hipErrorInvalidValue;
+        return launch_one<K, CM, EXACT, false, 4, 16, 4>(a, t, nchunks, lds, stream);
+    }
+    if (t.split == 2) {
+        if (mat || t.pix != 2) return hipErrorInvalidValue;
+        return launch_one<K, CM, EXACT, false, 2, 32, 2>(a, t, nchunks, lds, stream);
+    }
+    if (t.split != 1) return hipErrorInvalidValue;
     if (t.pix == 2)
-        return mat ? launch_one<K, CM, EXACT, true, 2>(a, t, lds, stream)
-                   : launch_one<K, CM, EXACT, false, 2>(a, t, lds, stream);
-    return mat ? launch_one<K, CM, EXACT, true, 4>(a, t, lds, stream)
-               : launch_one<K, CM, EXACT, false, 4>(a, t, lds, stream);
+        return mat ? launch_one<K, CM, EXACT, true, 2, 32, 1>(a, t, nchunks, lds, stream)
+                   : launch_one<K, CM, EXACT, false, 2, 32, 1>(a, t, nchunks, lds, stream);
+    return mat ? launch_one<K, CM, EXACT, true, 4, 32, 1>(a, t, nchunks, lds, stream)
+               : launch_one<K, CM, EXACT, false, 4, 32, 1>(a, t, nchunks, lds, stream);
 }
 
 }  // namespace
@@ -430,20 +528,25 @@ hipError_t launch_cm(const IterArgs& a, bool mat, TileConfig t, size_t lds, hipS
 #define CRF_CAT(a, b) CRF_CAT2(a, b)
 
 hipError_t CRF_CAT(launch_iter_k, CRF_K)(const IterArgs& a, bool materialised, TileConfig tile,
-                                         size_t lds, hipStream_t stream) {
+                                         int nchunks, size_t lds, hipStream_t stream) {
     constexpr int K = CRF_K;
     if (tile.pix != 2 && tile.pix != 4) return hipErrorInvalidValue;
-    if (tile.threads() > (tile.pix == 4 ? 256 : 512) || tile.threads() % 64 != 0)
+    if (tile.width != 32 && tile.width != 16) return hipErrorInvalidValue;
+    if ((tile.width / tile.pix) * tile.rows % 64 != 0) return hipErrorInvalidValue;  // whole-wave groups
+    const int max_threads = tile.width == 16 ? 256 : (tile.pix == 4 ? 256 : 512) * tile.split;
+    if (tile.threads() > max_threads) return hipErrorInvalidValue;
+    if (nchunks < 1 || (nchunks > 1 && a.mode != kModeMessage) || nchunks * a.C < a.planes ||
+        (nchunks - 1) * a.C >= a.planes)
         return hipErrorInvalidValue;
     switch (a.C) {
-        case 19: return launch_cm<K, 19, true>(a, materialised, tile, lds, stream);
-        case 21: return launch_cm<K, 21, true>(a, materialised, tile, lds, stream);
+        case 19: return launch_cm<K, 19, true>(a, materialised, tile, nchunks, lds, stream);
+        case 21: return launch_cm<K, 21, true>(a, materialised, tile, nchunks, lds, stream);
         default: break;
     }
-    if (a.C <= 4) return launch_cm<K, 4, false>(a, materialised, tile, lds, stream);
-    if (a.C <= 8) return launch_cm<K, 8, false>(a, materialised, tile, lds, stream);
-    if (a.C <= 16) return launch_cm<K, 16, false>(a, materialised, tile, lds, stream);
-    return launch_cm<K, 24, false>(a, materialised, tile, lds, stream);
+    if (a.C <= 4) return launch_cm<K, 4, false>(a, materialised, tile, nchunks, lds, stream);
+    if (a.C <= 8) return launch_cm<K, 8, false>(a, materialised, tile, nchunks, lds, stream);
+    if (a.C <= 16) return launch_cm<K, 16, false>(a, materialised, tile, nchunks, lds, stream);
+    return launch_cm<K, 24, false>(a, materialised, tile, nchunks, lds, stream);
 }
 
 }  // namespace convcrf
