@@ -124,7 +124,7 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="pascal")
-    ap.add_argument("--variant", choices=["fused", "materialised"], default="fused")
+    ap.add_argument("--variant", choices=["fused", "materialised", "resident"], default="fused")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead: time a plain device-to-device copy of this many MiB "
@@ -150,7 +150,8 @@ def main(argv=None):
     Ut = torch.from_numpy(U).to(dev)
     It = torch.from_numpy(I).to(dev)
     out = torch.empty_like(Ut)
-    variant = cc.VARIANT_FUSED if args.variant == "fused" else cc.VARIANT_MATERIALISED
+    variant = {"fused": cc.VARIANT_FUSED, "materialised": cc.VARIANT_MATERIALISED,
+               "resident": cc.VARIANT_RESIDENT}[args.variant]
     p = cc.Params(filter_size=wl.filter_size, blur=wl.blur, variant=variant, w_app=wl.w_app,
                   theta_alpha=wl.theta_alpha, theta_beta=wl.theta_beta, w_smooth=wl.w_smooth,
                   theta_gamma=wl.theta_gamma)
@@ -178,16 +179,28 @@ def main(argv=None):
         crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
     torch.cuda.synchronize()
 
-    # dominant kernel: the per-iteration kernel of the chosen path
+    # dominant kernel: the per-iteration kernel of the chosen path, or the
+    # resident launch that runs all iterations of a call
+    resident = False
     if wl.blur > 1:
         kname = "blur_message"
+    elif variant in (cc.VARIANT_FUSED, cc.VARIANT_RESIDENT):
+        kname = "fused_iter"
+        if crf.profile_read("fused_resident")[1] > 0:
+            kname, resident = "fused_resident", True
     else:
-        kname = "fused_iter" if variant == cc.VARIANT_FUSED else "materialised_iter"
+        kname = "materialised_iter"
     k_ms, k_n = crf.profile_read(kname)
     crf.profile_enable(False)
     avg_s = k_ms / 1e3 / max(k_n, 1)
     T = wl.iters
-    if wl.blur == 1:
+    if resident:
+        # one launch = T iterations; bytes: the irreducible input and output
+        # (U and the image read, Q written), everything else stays on chip
+        # but the tiles' border rings
+        F = T * flops_per_pixel_iter(wl.C, wl.filter_size, True) * wl.pixels
+        Bytes = (8 * wl.C + 12) * wl.pixels
+    elif wl.blur == 1:
         F = flops_per_pixel_iter(wl.C, wl.filter_size, True) * wl.pixels
         Bytes = (bytes_per_pixel(wl.C, True) + (T - 1) * bytes_per_pixel(wl.C, False)) / T * wl.pixels
         if variant == cc.VARIANT_MATERIALISED:

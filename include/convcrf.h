@@ -59,10 +59,20 @@ typedef enum {
 /* Which kernels compute the message (all give the same Q up to rounding). */
 enum {
     CONVCRF_VARIANT_FUSED = 0,        /* weights recomputed in registers from
-                                         LDS-staged colour tiles (default) */
-    CONVCRF_VARIANT_MATERIALISED = 1  /* kernel matrix K[B][k*k][H][W]
+                                         LDS-staged colour tiles, one launch
+                                         per iteration (default) */
+    CONVCRF_VARIANT_MATERIALISED = 1, /* kernel matrix K[B][k*k-1][H][W]
                                          written once per call (Eq. 5), then
                                          read by every iteration */
+    CONVCRF_VARIANT_RESIDENT = 2      /* the fused kernel running all
+                                         iterations in one launch: each tile
+                                         stays in LDS and neighbouring tiles
+                                         exchange their border rings between
+                                         iterations.  Used for Potts and
+                                         k <= 7 when every tile's work-group
+                                         fits on the device at once (and
+                                         iters >= 2); otherwise the call
+                                         runs as CONVCRF_VARIANT_FUSED. */
 };
 
 /* Model parameters.  Plain host struct; copied during the call. */
@@ -77,7 +87,8 @@ typedef struct {
                                pooled grid and is bilinearly upsampled (half-
                                pixel centres, edge clamp) before the
                                compatibility step.  H and W must be multiples
-                               of s.  Only the fused variant implements it. */
+                               of s.  Only the fused variant implements it
+                               (the resident variant runs it as fused). */
     int32_t include_center; /* 0: the centre tap q == p is excluded (Alg. 1
                                sums over i != j; default).  1: it is included
                                with weight K(p,p) = w_app + w_smooth, the
@@ -136,15 +147,20 @@ convcrf_status convcrf_meanfield(convcrf_ctx *ctx, const float *unary,
 convcrf_status convcrf_profile_enable(convcrf_ctx *ctx, int enable);
 
 /* Total elapsed milliseconds and launch count of the kernels named `name`
- * ("fused_iter", "softmax", "build_kernel", "materialised_iter",
- * "blur_pool", "blur_message", "blur_update") since profiling was enabled.
+ * ("fused_iter", "fused_resident", "sync_reset", "softmax", "build_kernel",
+ * "materialised_iter", "blur_pool", "blur_message", "blur_update") since
+ * profiling was enabled.  "fused_resident" is one launch running all
+ * iterations of a call (CONVCRF_VARIANT_RESIDENT); "fused_iter" one
+ * iteration.
  * Synchronises on the recorded events.  An unknown or unused name gives
  * 0 ms and 0 launches. */
 convcrf_status convcrf_profile_read(convcrf_ctx *ctx, const char *name,
                                     double *total_ms, int64_t *launches);
 
 /* Message describing the last failure on ctx (or of a context-free call if
- * ctx is NULL).  Never NULL; valid until the next call on the same ctx. */
+ * ctx is NULL), or why the last CONVCRF_VARIANT_RESIDENT call on ctx ran one
+ * launch per iteration instead.  Never NULL; valid until the next call on
+ * the same ctx. */
 const char *convcrf_last_error(const convcrf_ctx *ctx);
 
 /* Static name of a status code. */

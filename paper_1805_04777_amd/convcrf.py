@@ -24,9 +24,10 @@ E_OOM = -5
 
 VARIANT_FUSED = 0
 VARIANT_MATERIALISED = 1
+VARIANT_RESIDENT = 2
 
-KERNEL_NAMES = ("fused_iter", "softmax", "build_kernel", "materialised_iter",
-                "blur_pool", "blur_message", "blur_update")
+KERNEL_NAMES = ("fused_iter", "fused_resident", "sync_reset", "softmax", "build_kernel",
+                "materialised_iter", "blur_pool", "blur_message", "blur_update")
 
 EXPORTED = ("convcrf_default_params", "convcrf_validate", "convcrf_init", "convcrf_destroy",
             "convcrf_meanfield", "convcrf_profile_enable", "convcrf_profile_read",
@@ -191,6 +192,10 @@ class ConvCRF:
                                            ctypes.byref(cp), int(iters), out.data_ptr(), sp),
                self._h)
         return out
+
+    def last_error(self) -> str:
+        """The library's last message for this context."""
+        return self._lib.convcrf_last_error(self._h).decode()
 
     def profile_enable(self, on: bool = True):
         _check(self._lib.convcrf_profile_enable(self._h, int(bool(on))), self._h)

@@ -21,10 +21,13 @@ namespace {
 constexpr double kLog2eD = 1.4426950408889634073599;
 constexpr size_t kLdsLimit = 160 * 1024;  // gfx950 LDS per work-group
 
-const char* const kKernelNames[] = {"fused_iter",   "softmax",     "build_kernel",
+const char* const kKernelNames[] = {"fused_iter",   "softmax",      "build_kernel",
                                     "materialised_iter", "blur_pool", "blur_message",
-                                    "blur_update"};
-enum KernelId { kFused = 0, kSoftmax, kBuild, kMatIter, kPool, kBlurMsg, kBlurUpd, kNumKernels };
+                                    "blur_update",  "fused_resident", "sync_reset"};
+enum KernelId {
+    kFused = 0, kSoftmax, kBuild, kMatIter, kPool, kBlurMsg, kBlurUpd, kResident, kSyncReset,
+    kNumKernels
+};
 
 struct DevBuf {
     void* p = nullptr;
@@ -43,8 +46,9 @@ thread_local std::string g_last_error = "no error";
 struct convcrf_ctx {
     int device = 0;
     int num_cus = 256;
+    bool coop = false;              // cooperative launches supported
     std::string err = "no error";
-    DevBuf q_ws, kmat, pool_q, pool_m, pool_f, mu;
+    DevBuf q_ws, q_ws2, kmat, pool_q, pool_m, pool_f, mu, sync;
     std::vector<float> mu_last;   // host copy of the uploaded compatibility
     float* mu_pinned = nullptr;   // pinned staging for the upload
     size_t mu_pinned_cap = 0;
@@ -81,7 +85,8 @@ convcrf_status validate(convcrf_ctx* ctx, int B, int C, int H, int W, const conv
     if (C > kMaxC) return fail(ctx, CONVCRF_E_UNSUPPORTED, "more than 24 classes is not built");
     if (p->include_center != 0 && p->include_center != 1)
         return fail(ctx, CONVCRF_E_INVALID_ARG, "include_center must be 0 or 1");
-    if (p->variant != CONVCRF_VARIANT_FUSED && p->variant != CONVCRF_VARIANT_MATERIALISED)
+    if (p->variant != CONVCRF_VARIANT_FUSED && p->variant != CONVCRF_VARIANT_MATERIALISED &&
+        p->variant != CONVCRF_VARIANT_RESIDENT)
         return fail(ctx, CONVCRF_E_INVALID_ARG, "unknown variant");
     if (!std::isfinite(p->w_app) || !std::isfinite(p->w_smooth))
         return fail(ctx, CONVCRF_E_INVALID_ARG, "kernel weights must be finite");
@@ -92,8 +97,8 @@ convcrf_status validate(convcrf_ctx* ctx, int B, int C, int H, int W, const conv
     const int s = p->blur;
     if (s != 1 && s != 2 && s != 4 && s != 8)
         return fail(ctx, CONVCRF_E_INVALID_ARG, "blur must be 1, 2, 4 or 8");
-    if (s > 1 && p->variant != CONVCRF_VARIANT_FUSED)
-        return fail(ctx, CONVCRF_E_UNSUPPORTED, "blur is only built for the fused variant");
+    if (s > 1 && p->variant == CONVCRF_VARIANT_MATERIALISED)
+        return fail(ctx, CONVCRF_E_UNSUPPORTED, "blur is not built for the materialised variant");
     if (s > 1 && (H % s != 0 || W % s != 0))
         return fail(ctx, CONVCRF_E_UNSUPPORTED, "H and W must be multiples of the blur factor");
     const long long npix = (long long)B * H * W;
@@ -184,6 +189,17 @@ hipError_t launch_iter(const IterArgs& a, int k, bool mat, TileConfig t, int nch
         case 13: return launch_iter_k13(a, mat, t, nchunks, lds, s);
         case 15: return launch_iter_k15(a, mat, t, nchunks, lds, s);
         default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_resident(const IterArgs& a, int k, TileConfig t, size_t lds, int num_cus,
+                           hipStream_t s, bool probe) {
+    switch (k) {
+        case 1: return launch_resident_k1(a, t, lds, num_cus, s, probe);
+        case 3: return launch_resident_k3(a, t, lds, num_cus, s, probe);
+        case 5: return launch_resident_k5(a, t, lds, num_cus, s, probe);
+        case 7: return launch_resident_k7(a, t, lds, num_cus, s, probe);
+        default: return hipErrorNotSupported;
     }
 }
 
@@ -304,6 +320,10 @@ convcrf_status convcrf_init(convcrf_ctx** out, int device) {
     if (!ctx) return fail(nullptr, CONVCRF_E_OOM, "context allocation failed");
     ctx->device = device;
     ctx->num_cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
+    int coop = 0;
+    if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, device) == hipSuccess)
+        ctx->coop = coop != 0;
+    (void)hipGetLastError();
     *out = ctx;
     return CONVCRF_OK;
 }
@@ -314,7 +334,8 @@ void convcrf_destroy(convcrf_ctx* ctx) {
     (void)hipGetDevice(&prev);
     (void)hipSetDevice(ctx->device);
     (void)hipDeviceSynchronize();
-    for (DevBuf* b : {&ctx->q_ws, &ctx->kmat, &ctx->pool_q, &ctx->pool_m, &ctx->pool_f, &ctx->mu})
+    for (DevBuf* b : {&ctx->q_ws, &ctx->q_ws2, &ctx->kmat, &ctx->pool_q, &ctx->pool_m,
+                      &ctx->pool_f, &ctx->mu, &ctx->sync})
         if (b->p) (void)hipFree(b->p);
     if (ctx->mu_pinned) (void)hipHostFree(ctx->mu_pinned);
     if (ctx->mu_copied) (void)hipEventDestroy(ctx->mu_copied);
@@ -440,6 +461,37 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
                              (reinterpret_cast<uintptr_t>(q_out) % va == 0) &&
                              (!ctx->q_ws.p || reinterpret_cast<uintptr_t>(ctx->q_ws.p) % va == 0);
         a.vec = (W % tile.pix == 0) && aligned;
+        // Resident variant: all iterations in one launch when every tile's
+        // work-group fits on the device at once (Potts, the two-pixel tile):
+        // the tile stays in LDS and only border rings cross memory.
+        if (p.variant == CONVCRF_VARIANT_RESIDENT && !mu_dev && iters >= 2 && ctx->coop &&
+            tile.pix == 2 && tile.split == 1 && tile.width == 32 && k <= 7 &&
+            a.ntiles <= 4 * ctx->num_cus) {
+            if ((st = ensure(ctx, ctx->q_ws2, qbytes)) != CONVCRF_OK) return st;
+            if ((st = ensure(ctx, ctx->sync, (1 + (size_t)a.ntiles) * sizeof(unsigned int))) !=
+                CONVCRF_OK)
+                return st;
+            IterArgs r = a;
+            r.src = unary;
+            r.dst = q_out;
+            r.first = 1;
+            r.iters = iters;
+            r.ring[0] = static_cast<float*>(ctx->q_ws.p);
+            r.ring[1] = static_cast<float*>(ctx->q_ws2.p);
+            r.sync = static_cast<unsigned int*>(ctx->sync.p);
+            const hipError_t fits = launch_resident(r, k, tile, lds, ctx->num_cus, stream, true);
+            if (fits == hipSuccess) {
+                st = launch(ctx, kSyncReset, stream, "sync_reset",
+                            [&] { return launch_zero_u32(r.sync, 1 + a.ntiles, stream); });
+                if (st != CONVCRF_OK) return st;
+                return launch(ctx, kResident, stream, "fused_resident", [&] {
+                    return launch_resident(r, k, tile, lds, ctx->num_cus, stream, false);
+                });
+            }
+            (void)hipGetLastError();  // refused: one launch per iteration below
+            ctx->err = std::string("resident launch refused (") + hipGetErrorString(fits) +
+                       "); ran one launch per iteration";
+        }
         float* ws = static_cast<float*>(ctx->q_ws.p);
         // the last iteration writes q_out; earlier ones alternate so that
         // source and destination always differ

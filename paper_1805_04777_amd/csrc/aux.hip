@@ -1,4 +1,5 @@
 // aux.hip -- the kernels around the fused iteration on gfx950:
+//   zero_u32_kernel      clears the synchronisation flags of a resident launch
 //   softmax_kernel       Q = softmax(U)                 (Alg. 1 initialisation)
 //   build_kernel_kernel  kernel matrix of Eq. 5, merged over both Gaussians
 //                        (materialised comparison variant, Sec. 4.1)
@@ -215,9 +216,19 @@ __global__ __launch_bounds__(256) void blur_update_kernel(
     }
 }
 
+__global__ __launch_bounds__(256) void zero_u32_kernel(unsigned int* p, int n) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+        p[i] = 0u;
+}
+
 inline unsigned nblocks(long long n, int bs) { return (unsigned)((n + bs - 1) / bs); }
 
 }  // namespace
+
+hipError_t launch_zero_u32(unsigned int* p, int n, hipStream_t stream) {
+    hipLaunchKernelGGL(zero_u32_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, p, n);
+    return hipGetLastError();
+}
 
 hipError_t launch_softmax(const float* U, float* Q, int B, int C, int HW, hipStream_t stream) {
     const long long n = (long long)B * HW;

@@ -55,6 +55,13 @@ struct IterArgs {
     int planes;           // class planes per image in src / dst / unary
     int tiles_x, tiles_per_img, ntiles;
     int first;            // stage softmax(src) instead of src
+    // resident launch (all iterations in one launch, every tile's work-group
+    // co-resident): iterations to run, the two exchange buffers [B][C][H][W]
+    // for the tiles' border rings, and the synchronisation words
+    int iters;
+    float* ring[2];
+    unsigned int* sync;   // [0] error flag, [1 + tile] rings published by each
+                          // tile; all zero before the launch
     int include_center;   // add (w_app + w_smooth) Q_p to the message
     int mode;             // IterMode
     int vec;              // W % pix == 0 and planes aligned to 4*pix bytes:
@@ -94,11 +101,16 @@ inline size_t iter_lds_bytes(int k, int C, TileConfig t, bool with_colour, bool 
 // One launcher per window side k (each compiled in its own object); one
 // work-group per tile and class chunk: a.ntiles x nchunks work-groups, chunk
 // j computing classes [j*a.C, (j+1)*a.C) (message mode only; nchunks = 1
-// otherwise).
+// otherwise).  launch_resident runs all a.iters iterations in one
+// cooperative launch; with probe = true it only reports whether it would
+// (hipSuccess) or not (hipErrorNotSupported / hipErrorCooperativeLaunchTooLarge).
 #define CONVCRF_DECLARE_ITER(K)                                              \
     hipError_t launch_iter_k##K(const IterArgs& a, bool materialised,        \
                                 TileConfig tile, int nchunks, size_t lds,    \
-                                hipStream_t stream);
+                                hipStream_t stream);                         \
+    hipError_t launch_resident_k##K(const IterArgs& a, TileConfig tile,      \
+                                    size_t lds, int num_cus,                 \
+                                    hipStream_t stream, bool probe);
 CONVCRF_DECLARE_ITER(1)
 CONVCRF_DECLARE_ITER(3)
 CONVCRF_DECLARE_ITER(5)
@@ -108,6 +120,10 @@ CONVCRF_DECLARE_ITER(11)
 CONVCRF_DECLARE_ITER(13)
 CONVCRF_DECLARE_ITER(15)
 #undef CONVCRF_DECLARE_ITER
+
+// Fill n words with zero (the flags of a resident launch: a kernel, not a
+// memset, so that the sequence may be captured in a graph).
+hipError_t launch_zero_u32(unsigned int* p, int n, hipStream_t stream);
 
 // Q = softmax(U) over classes, per pixel (Alg. 1 initialisation).
 hipError_t launch_softmax(const float* U, float* Q, int B, int C, int HW,

@@ -100,11 +100,60 @@ __device__ __forceinline__ void softmax_regs(float (&z)[CM], int C) {
     for (int c = 0; c < CM; ++c) z[c] *= inv;
 }
 
+// Neighbour synchronisation of a resident launch (every work-group
+// co-resident).  A work-group depends only on the border rings of the up to
+// eight tiles around it, so instead of a grid barrier each tile publishes
+// how many rings it has written (flags[tile] = value) and waits until each
+// neighbour has published `value`.  Ordering: every wave first makes its own
+// ring stores visible device-wide (an agent-scope release fence: L2
+// write-back for the other XCDs, then a wait for the wave's stores -- the
+// work-group barrier alone does not wait for other waves' stores), the
+// work-group barrier then orders thread 0's flag store after all of them;
+// the waiting lanes (one per neighbour) poll with relaxed loads and one
+// agent-scope acquire drops stale cache lines before the work-group reads
+// the rings.  With the rings double-buffered this also keeps a tile from
+// overwriting a buffer a neighbour still reads: that neighbour publishes
+// value + 1 only after its read.  The wait is bounded: past kSpinLimit polls
+// the lane records an error in *flag_err and goes on (wrong results, never a
+// hang).
+constexpr unsigned int kSpinLimit = 1u << 22;
+
+__device__ __forceinline__ void neighbour_sync(unsigned int* flags, unsigned int* flag_err,
+                                               int tile, int tiles_x, int tiles_y,
+                                               unsigned int value) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __syncthreads();
+    if (threadIdx.x == 0)
+        __hip_atomic_store(flags + tile, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x < 9) {
+        const int per_img = tiles_x * tiles_y;
+        const int ti = tile % per_img;
+        const int ty = ti / tiles_x + (int)threadIdx.x / 3 - 1;
+        const int tx = ti % tiles_x + (int)threadIdx.x % 3 - 1;
+        if (threadIdx.x != 4 && ty >= 0 && ty < tiles_y && tx >= 0 && tx < tiles_x) {
+            const unsigned int* f = flags + (tile - ti) + ty * tiles_x + tx;
+            unsigned int polls = 0;
+            while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < value) {
+                __builtin_amdgcn_s_sleep(1);
+                if (++polls == kSpinLimit) {
+                    __hip_atomic_store(flag_err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+    __syncthreads();
+}
+
 // Threads = (TW / P) * rows * S: S groups of whole wavefronts share one
 // staged tile, group g taking window rows [g*K/S, (g+1)*K/S) of every pixel.
 // At the 146 KB tile of k = 7 that gives 1 (P = 4), 2 (P = 2) or 4 (P = 2,
 // S = 2) waves per SIMD; declaring it lets the scheduler size registers.
-template <int K, int CM, bool EXACT, bool MAT, int P, int TW, int S>
+// RES: resident launch running all a.iters iterations; the tile stays in LDS
+// and between iterations the work-groups only exchange the r-pixel border
+// rings of their tiles through a.ring[], synchronised with their neighbours.
+template <int K, int CM, bool EXACT, bool MAT, int P, int TW, int S, bool RES>
 __global__ __launch_bounds__(TW == 16 ? 256 : (P == 4 ? 256 : 512) * S)
 __attribute__((amdgpu_waves_per_eu(TW == 16 ? 1 : (P == 4 ? 1 : 2) * S,
                                    TW == 16 ? 4 : (P == 4 ? 1 : 2) * S)))
@@ -119,6 +168,7 @@ void iter_kernel(const IterArgs a) {
     constexpr int kStagePix = S == 1 ? 3 : 2;
     constexpr int FP = P / S;                 // pixels each thread finalises
     static_assert(P % S == 0, "each row group finalises P / S pixels");
+    static_assert(!RES || (!MAT && S == 1), "resident launches are fused, one row group");
     using V = Vec<P>;
     using VF = Vec<FP>;
 
@@ -218,13 +268,15 @@ void iter_kernel(const IterArgs a) {
     const int xb = x0 + col0;
     const bool pix_ok = y < H;
     const bool fullv = a.vec && xb + P <= W;
-    const bool general_compat = a.mode == kModeUpdate && a.mu != nullptr;
+    // (resident launches are built for Potts only)
+    const bool general_compat = !RES && a.mode == kModeUpdate && a.mu != nullptr;
 
     // With Potts the update is softmax(U + M) (the compatibility transform
     // -(sum M - M) differs from +M by a per-pixel constant), so the message
     // accumulates straight onto the unary, which is loaded here and arrives
     // while the tile is being staged.
     const bool unary_first = a.mode == kModeUpdate && !general_compat;
+    const float* const unary_px = a.unary + cbase * HW + (size_t)y * W + xb;
     float acc[P][CM];
 #pragma unroll
     for (int i = 0; i < P; ++i)
@@ -245,6 +297,14 @@ void iter_kernel(const IterArgs a) {
     __syncthreads();
 
     // ---- message: acc[i][c] = sum_d K(p_i, p_i + d) Q_t(p_i + d, c)
+    for (int it = 0;; ++it) {
+    if (it > 0) {  // resident launch: the next iteration starts from U again
+#pragma unroll
+        for (int i = 0; i < P; ++i)
+#pragma unroll
+            for (int c = 0; c < CM; ++c) acc[i][c] = 0.f;
+        if (unary_first && pix_ok && grp == 0) load_pixels(acc, unary_px, xb, fullv);
+    }
 
     float own[3][P];
     if constexpr (!MAT) {
@@ -403,8 +463,6 @@ void iter_kernel(const IterArgs a) {
 
     const int xf = xb + grp * FP;             // first finalised pixel
     const bool fullf = a.vec && xf + FP <= W && (FP == P || (xf % FP) == 0);
-    if (!pix_ok) return;
-    float* __restrict__ dst = a.dst + cbase * HW + (size_t)y * W + xf;
 
     if (a.mode == kModeUpdate) {
         // compatibility transform: fin <- U - mu * M (general mu only; with
@@ -414,18 +472,21 @@ void iter_kernel(const IterArgs a) {
             // broadcast reads of mu from all being hoisted); the unary is
             // loaded first so that it arrives meanwhile
             float u[FP][CM];
-            const float* ug = a.unary + cbase * HW + (size_t)y * W + xf;
+            {
+                const float* ug = a.unary + cbase * HW + (size_t)y * W + xf;
 #pragma unroll
-            for (int c = 0; c < CM; ++c) {
-                if (!EXACT && c >= C) continue;
-                if (fullf) {
-                    float tmp[FP];
-                    VF::get(*reinterpret_cast<const typename VF::T*>(ug + c * HW), tmp);
+                for (int c = 0; c < CM; ++c) {
+                    if (!EXACT && c >= C) continue;
+                    if (fullf && pix_ok) {
+                        float tmp[FP];
+                        VF::get(*reinterpret_cast<const typename VF::T*>(ug + c * HW), tmp);
 #pragma unroll
-                    for (int j = 0; j < FP; ++j) u[j][c] = tmp[j];
-                } else {
+                        for (int j = 0; j < FP; ++j) u[j][c] = tmp[j];
+                    } else {
 #pragma unroll
-                    for (int j = 0; j < FP; ++j) u[j][c] = (xf + j < W) ? ug[c * HW + j] : 0.f;
+                        for (int j = 0; j < FP; ++j)
+                            u[j][c] = (pix_ok && xf + j < W) ? ug[c * HW + j] : 0.f;
+                    }
                 }
             }
             float z[FP][CM];
@@ -460,20 +521,79 @@ void iter_kernel(const IterArgs a) {
         for (int j = 0; j < FP; ++j) softmax_regs<CM, EXACT>(fin[j], C);
     }
 
+    if (!RES || it == a.iters - 1) {
+        if (pix_ok) {
+            float* __restrict__ dst = a.dst + cbase * HW + (size_t)y * W + xf;
 #pragma unroll
-    for (int c = 0; c < CM; ++c) {
-        if (!EXACT && c >= C) continue;
-        if (fullf) {
-            float tmp[FP];
+            for (int c = 0; c < CM; ++c) {
+                if (!EXACT && c >= C) continue;
+                if (fullf) {
+                    float tmp[FP];
 #pragma unroll
-            for (int j = 0; j < FP; ++j) tmp[j] = fin[j][c];
-            *reinterpret_cast<typename VF::T*>(dst + c * HW) = VF::make(tmp);
-        } else {
+                    for (int j = 0; j < FP; ++j) tmp[j] = fin[j][c];
+                    *reinterpret_cast<typename VF::T*>(dst + c * HW) = VF::make(tmp);
+                } else {
 #pragma unroll
-            for (int j = 0; j < FP; ++j)
-                if (xf + j < W) dst[c * HW + j] = fin[j][c];
+                    for (int j = 0; j < FP; ++j)
+                        if (xf + j < W) dst[c * HW + j] = fin[j][c];
+                }
+            }
         }
+        break;
     }
+
+    if constexpr (RES) {
+        // Q_{t+1} of this tile into the LDS interior (in-image pixels; the
+        // rest stays zero), its r-pixel border ring into the exchange buffer
+        __syncthreads();                      // every read of Q_t is done
+        float* __restrict__ ring = a.ring[(it + 1) & 1] + cbase * HW;
+#pragma unroll
+        for (int i = 0; i < P; ++i) {
+            const int col = col0 + i;
+            if (!pix_ok || xb + i >= W) continue;
+            float* q = Qs + (ty + R) * LS + col + R;
+#pragma unroll
+            for (int c = 0; c < CM; ++c)
+                if (EXACT || c < C) q[c * plane] = fin[i][c];
+            if (ty < R || ty >= rows - R || col < R || col >= TW - R) {
+                float* g = ring + (size_t)y * W + xb + i;
+#pragma unroll
+                for (int c = 0; c < CM; ++c)
+                    if (EXACT || c < C) g[c * HW] = fin[i][c];
+            }
+        }
+        neighbour_sync(a.sync + 1, a.sync, tile, a.tiles_x, a.tiles_per_img / a.tiles_x,
+                       (unsigned int)(it + 1));
+        // the halo of Q_{t+1}: the neighbouring tiles' rings (positions
+        // outside the image keep the zero staged at the start)
+        const float* __restrict__ nb = a.ring[(it + 1) & 1] + cbase * HW;
+        const int band = R * LW, side = R * (LH - 2 * R);
+        for (int idx = tid; idx < 2 * band + 2 * side; idx += nthreads) {
+            int r, cc;
+            if (idx < 2 * band) {
+                const int k2 = idx - (idx >= band ? band : 0);
+                r = (idx >= band ? LH - R : 0) + k2 / LW;
+                cc = k2 - (k2 / LW) * LW;
+            } else {
+                const int j = idx - 2 * band;
+                const int k2 = j - (j >= side ? side : 0);
+                r = R + k2 / R;
+                cc = (j >= side ? LW - R : 0) + (k2 - (k2 / R) * R);
+            }
+            const int gy = y0 - R + r, gx = x0 - R + cc;
+            if (gy < 0 || gy >= H || gx < 0 || gx >= W) continue;
+            const float* g = nb + (size_t)gy * W + gx;
+            float v[CM];
+#pragma unroll
+            for (int c = 0; c < CM; ++c) v[c] = (EXACT || c < C) ? g[c * HW] : 0.f;
+            float* q = Qs + r * LS + cc;
+#pragma unroll
+            for (int c = 0; c < CM; ++c)
+                if (EXACT || c < C) q[c * plane] = v[c];
+        }
+        __syncthreads();
+    }
+    }  // iterations
 }
 
 // Opt a kernel into the full 160 KB of LDS once per device.
@@ -494,11 +614,34 @@ hipError_t allow_full_lds(Fn fn) {
 template <int K, int CM, bool EXACT, bool MAT, int P, int TW, int S>
 hipError_t launch_one(const IterArgs& a, TileConfig t, int nchunks, size_t lds,
                       hipStream_t stream) {
-    auto fn = iter_kernel<K, CM, EXACT, MAT, P, TW, S>;
+    auto fn = iter_kernel<K, CM, EXACT, MAT, P, TW, S, false>;
     hipError_t e = allow_full_lds(fn);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(a.ntiles, nchunks), dim3(t.threads()), lds, stream, a);
     return hipGetLastError();
+}
+
+// Resident launch: cooperative, so that the runtime refuses it (rather than
+// the grid barrier waiting forever) unless every work-group is co-resident;
+// hipErrorCooperativeLaunchTooLarge also when the occupancy query says the
+// tiles do not fit at once, so the caller falls back to one launch per
+// iteration.
+template <int K, int CM, bool EXACT>
+hipError_t launch_res(const IterArgs& a, TileConfig t, size_t lds, int num_cus,
+                      hipStream_t stream, bool probe) {
+    auto fn = iter_kernel<K, CM, EXACT, false, 2, 32, 1, true>;
+    hipError_t e = allow_full_lds(fn);
+    if (e != hipSuccess) return e;
+    int per_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fn),
+                                                     t.threads(), lds);
+    if (e != hipSuccess) return e;
+    if ((long long)per_cu * num_cus < a.ntiles) return hipErrorCooperativeLaunchTooLarge;
+    if (probe) return hipSuccess;
+    IterArgs args = a;
+    void* params[] = {&args};
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(fn), dim3(a.ntiles),
+                                      dim3(t.threads()), params, (unsigned int)lds, stream);
 }
 
 // The built tile shapes: {P = 2 or 4, width 32, S = 1}, {P = 2, width 32,
@@ -547,6 +690,29 @@ hipError_t CRF_CAT(launch_iter_k, CRF_K)(const IterArgs& a, bool materialised, T
     if (a.C <= 8) return launch_cm<K, 8, false>(a, materialised, tile, nchunks, lds, stream);
     if (a.C <= 16) return launch_cm<K, 16, false>(a, materialised, tile, nchunks, lds, stream);
     return launch_cm<K, 24, false>(a, materialised, tile, nchunks, lds, stream);
+}
+
+// Resident launches are built for the two-pixel, one-group tile of k <= 7
+// and Potts compatibility.
+hipError_t CRF_CAT(launch_resident_k, CRF_K)(const IterArgs& a, TileConfig tile, size_t lds,
+                                             int num_cus, hipStream_t stream, bool probe) {
+    constexpr int K = CRF_K;
+    if constexpr (K > 7) {
+        return hipErrorNotSupported;
+    } else {
+        if (tile.pix != 2 || tile.width != 32 || tile.split != 1 || tile.threads() > 512 ||
+            a.mode != kModeUpdate || a.iters < 2 || a.planes != a.C || a.mu != nullptr)
+            return hipErrorNotSupported;
+        switch (a.C) {
+            case 19: return launch_res<K, 19, true>(a, tile, lds, num_cus, stream, probe);
+            case 21: return launch_res<K, 21, true>(a, tile, lds, num_cus, stream, probe);
+            default: break;
+        }
+        if (a.C <= 4) return launch_res<K, 4, false>(a, tile, lds, num_cus, stream, probe);
+        if (a.C <= 8) return launch_res<K, 8, false>(a, tile, lds, num_cus, stream, probe);
+        if (a.C <= 16) return launch_res<K, 16, false>(a, tile, lds, num_cus, stream, probe);
+        return launch_res<K, 24, false>(a, tile, lds, num_cus, stream, probe);
+    }
 }
 
 }  // namespace convcrf

@@ -96,6 +96,8 @@ def P(**kw):
     ((1, 21, 64, 64, P(blur=3), 5), cc.E_INVALID_ARG),
     ((1, 21, 66, 64, P(blur=4), 5), cc.E_UNSUPPORTED),     # H not a multiple of s
     ((1, 21, 64, 64, P(blur=2, variant=cc.VARIANT_MATERIALISED), 5), cc.E_UNSUPPORTED),
+    ((1, 21, 64, 64, P(blur=2, variant=cc.VARIANT_RESIDENT), 5), cc.OK),
+    ((1, 21, 64, 64, P(variant=cc.VARIANT_RESIDENT), 5), cc.OK),
 ])
 def test_validation(lib, args, status):
     B, C, H, W, p, T = args

@@ -100,14 +100,18 @@ def test_tiny_workload_fused_and_materialised(torch_cuda, crf, oracle_mod):
         check(run_gpu(torch_cuda, crf, U, I, p, wl.iters), Qo, f"tiny variant {variant}")
 
 
-@pytest.mark.parametrize("variant", [0, 1])
+@pytest.mark.parametrize("variant", [0, 1, 2])
 def test_pascal_workload_full(torch_cuda, crf, oracle_mod, variant):
     # 1 x 21 x 512 x 512, k = 7, 5 iterations: every pixel against the oracle
     wl = synth.WORKLOADS["pascal"]
     U, I, L = synth.make_inputs(wl)
     p = lib_params(wl, variant=variant)
     Qo = run_oracle(oracle_mod, U, I, p, wl.iters)
+    crf.profile_enable(True)
     Qg = run_gpu(torch_cuda, crf, U, I, p, wl.iters)
+    n_res = crf.profile_read("fused_resident")[1]
+    crf.profile_enable(False)
+    assert n_res == (1 if variant == 2 else 0), crf.last_error()
     check(Qg, Qo, f"pascal variant {variant}")
     # the CRF denoises the synthetic unaries (sanity, not a parity bar)
     assert (Qg.argmax(1) == L).mean() > (U.argmax(1) == L).mean() + 0.2
@@ -270,6 +274,45 @@ def test_uniform_scene_interior(torch_cuda, crf):
     assert np.abs(inner - q[:, None, None]).max() <= 1e-5
 
 
+@pytest.mark.parametrize("B,C,H,W,k,T", [(1, 21, 512, 512, 7, 5), (1, 21, 200, 328, 7, 5),
+                                         (2, 19, 96, 160, 5, 3), (1, 24, 130, 70, 3, 4)])
+def test_resident_bitwise_equals_fused(torch_cuda, crf, B, C, H, W, k, T):
+    # The resident launch runs the same per-pixel arithmetic as one launch
+    # per iteration; only where Q_t lives between iterations differs (LDS plus
+    # exchanged border rings instead of HBM).  A stale or misplaced halo value
+    # would change bits, so the two must agree exactly, here on i.i.d. random
+    # logits and colours, up to 256 tiles with ragged edges.  (At 512 x 512
+    # both differ from the oracle by up to 1.7e-4 at 8 of 262144 pixels: fp32
+    # rounding of messages near 90, amplified over five iterations at pixels
+    # on a decision boundary; the workload-shaped scenes stay within 1e-4,
+    # see test_pascal_workload_full.)
+    from paper_1805_04777_amd import convcrf as cc
+    U, I = rand_case(1000 + C + H, B, C, H, W)
+    a = run_gpu(torch_cuda, crf, U, I, lib_params(filter_size=k), T)
+    crf.profile_enable(True)
+    b = run_gpu(torch_cuda, crf, U, I, lib_params(filter_size=k, variant=cc.VARIANT_RESIDENT), T)
+    n_res = crf.profile_read("fused_resident")[1]
+    crf.profile_enable(False)
+    assert n_res == 1, crf.last_error()
+    np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("B,C,H,W,k,T", [(2, 21, 67, 131, 7, 4), (1, 5, 97, 33, 5, 3),
+                                         (1, 19, 40, 64, 3, 2), (3, 8, 30, 30, 1, 3),
+                                         (1, 24, 64, 96, 7, 6)])
+def test_resident_variant(torch_cuda, crf, oracle_mod, B, C, H, W, k, T):
+    # all iterations in one launch, tiles exchanging border rings
+    from paper_1805_04777_amd import convcrf as cc
+    U, I = rand_case(1000 + C + H, B, C, H, W)
+    p = lib_params(filter_size=k, variant=cc.VARIANT_RESIDENT)
+    crf.profile_enable(True)
+    Qg = run_gpu(torch_cuda, crf, U, I, p, T)
+    n_res = crf.profile_read("fused_resident")[1]
+    crf.profile_enable(False)
+    assert n_res == 1, crf.last_error()
+    check(Qg, run_oracle(oracle_mod, U, I, p, T), f"resident {B}x{C}x{H}x{W} k={k} T={T}")
+
+
 # ------------------------------------------------------------ API behaviour
 
 def test_empty_inputs(torch_cuda, crf):
@@ -350,9 +393,15 @@ def test_profiling_counts_launches(torch_cuda, crf):
         crf.meanfield(U, I, lib_params(), 5)
     crf.meanfield(U, I, lib_params(variant=1), 4)
     crf.meanfield(U, I, lib_params(blur=4, filter_size=5), 2)
+    crf.meanfield(U, I, lib_params(variant=2), 5)   # resident: one launch for 5 iterations
+    mu = synth.random_compat(21, seed=1)
+    crf.meanfield(U, I, lib_params(variant=2, compat=mu), 3)   # general mu: runs as fused
     torch.cuda.synchronize()
     ms, n = crf.profile_read("fused_iter")
-    assert n == 15 and ms > 0
+    assert n == 18 and ms > 0
+    ms, n = crf.profile_read("fused_resident")
+    assert n == 1 and ms > 0
+    assert crf.profile_read("sync_reset")[1] == 1
     assert crf.profile_read("materialised_iter")[1] == 4
     assert crf.profile_read("build_kernel")[1] == 1
     assert crf.profile_read("blur_message")[1] == 2
