@@ -3,12 +3,13 @@
 One step = one full call of the library (softmax init + T mean-field rounds)
 on one synthetic batch already resident in HBM.  Prints one JSON line with
 the throughput in megapixel-iterations per second, the roofline of the
-dominant kernel (timed with HIP events recorded by the library around every
-launch, on the launch stream) and the double-precision CPU oracle timed on
-this host as a baseline.
+dominant kernel (the kernel with the largest share of the time, by HIP events
+recorded by the library around every launch on the launch stream; its
+duration is that share of the timed region) and the double-precision CPU
+oracle timed on this host as a baseline.
 
     python bench.py [--steps K] [--warmup W] [--workload pascal]
-                    [--variant fused|materialised] [--no-cpu-baseline]
+                    [--variant fused|materialised|resident] [--no-cpu-baseline]
 """
 from __future__ import annotations
 
@@ -52,6 +53,46 @@ def bytes_per_pixel(C: int, first: bool) -> int:
     the first launch, which reads U instead), U and the RGB image, write
     Q_{t+1}; fp32."""
     return 4 * C * (2 if first else 3) + 12
+
+
+def algorithmic_per_launch(kname: str, wl):
+    """(flops, HBM bytes) one launch of `kname` must spend on workload `wl`,
+    averaged over the launches of one call; fp32, Potts compatibility."""
+    C, k, T, px = wl.C, wl.filter_size, wl.iters, wl.pixels
+    if kname == "fused_iter":
+        return (flops_per_pixel_iter(C, k, True) * px,
+                (bytes_per_pixel(C, True) + (T - 1) * bytes_per_pixel(C, False)) / T * px)
+    if kname == "materialised_iter":
+        taps = k * k - 1
+        return ((flops_per_pixel_iter(C, k, True) - 12 * taps) * px,
+                ((bytes_per_pixel(C, True) + (T - 1) * bytes_per_pixel(C, False)) / T + 4 * taps) * px)
+    if kname == "build_kernel":
+        taps = k * k - 1
+        return 12 * taps * px, (12 + 4 * taps) * px
+    if kname == "fused_resident":
+        # one launch = T iterations; bytes: U and the image read, Q written
+        # (the tiles' border rings are the only other traffic)
+        return T * flops_per_pixel_iter(C, k, True) * px, (8 * C + 12) * px
+    s2 = wl.blur * wl.blur
+    npx = px // s2
+    if kname == "blur_message":
+        # pooled grid: read pooled Q and features, write pooled message
+        return (2 * C * (k * k - 1) + 12 * (k * k - 1)) * npx, (8 * C + 12) * npx
+    if kname == "blur_update":
+        # per pixel: bilinear sample of C pooled messages (3 FMA each), unary
+        # add, softmax, s*s average; reads U, writes the pooled Q (T - 1
+        # launches) or the full Q (the last one)
+        return ((6 + 1 + 5 + 1) * C * px,
+                4 * C * px + 4 * C * npx + ((T - 1) * 4 * C * npx + 4 * C * px) / T)
+    if kname == "blur_pool":
+        # two launches per call: softmax(U) pooled (21 planes) and the image
+        # (3 planes); averaged
+        return ((5 * C + 1) * px + C * px + 3 * px) / 2, (4 * (C + 3) * (px + npx)) / 2
+    if kname == "softmax":
+        return (5 * C + 1) * px, 8 * C * px
+    if kname == "sync_reset":
+        return 0, 0
+    raise KeyError(kname)
 
 
 def source_hash() -> str:
@@ -179,41 +220,25 @@ def main(argv=None):
         crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
     torch.cuda.synchronize()
 
-    # dominant kernel: the per-iteration kernel of the chosen path, or the
-    # resident launch that runs all iterations of a call
-    resident = False
-    if wl.blur > 1:
-        kname = "blur_message"
-    elif variant in (cc.VARIANT_FUSED, cc.VARIANT_RESIDENT):
-        kname = "fused_iter"
-        if crf.profile_read("fused_resident")[1] > 0:
-            kname, resident = "fused_resident", True
-    else:
-        kname = "materialised_iter"
-    k_ms, k_n = crf.profile_read(kname)
+    # per-kernel time of the K calls; the dominant kernel is the one with the
+    # largest total, priced by its own algorithmic flops and bytes
+    per = {n: crf.profile_read(n) for n in cc.KERNEL_NAMES}
     crf.profile_enable(False)
-    avg_s = k_ms / 1e3 / max(k_n, 1)
-    T = wl.iters
-    if resident:
-        # one launch = T iterations; bytes: the irreducible input and output
-        # (U and the image read, Q written), everything else stays on chip
-        # but the tiles' border rings
-        F = T * flops_per_pixel_iter(wl.C, wl.filter_size, True) * wl.pixels
-        Bytes = (8 * wl.C + 12) * wl.pixels
-    elif wl.blur == 1:
-        F = flops_per_pixel_iter(wl.C, wl.filter_size, True) * wl.pixels
-        Bytes = (bytes_per_pixel(wl.C, True) + (T - 1) * bytes_per_pixel(wl.C, False)) / T * wl.pixels
-        if variant == cc.VARIANT_MATERIALISED:
-            F -= 12 * (wl.filter_size ** 2 - 1) * wl.pixels      # weights are read, not computed
-            Bytes += 4 * (wl.filter_size ** 2 - 1) * wl.pixels   # ... from HBM
-    else:
-        npx = wl.pixels // (wl.blur ** 2)
-        F = flops_per_pixel_iter(wl.C, wl.filter_size, True) * npx
-        Bytes = (8 * wl.C + 12) * npx
-    alu_frac = F / avg_s / PEAK_VALU_FP32 if k_n else None
-    hbm_frac = Bytes / avg_s / PEAK_HBM if k_n else None
+    launched = {n: v for n, v in per.items() if v[1] > 0}
+    kname = max(launched, key=lambda n: launched[n][0])
+    k_ms, k_n = launched[kname]
+    # Events around every launch add about a microsecond each, so the
+    # kernel's duration is taken from the timed region instead: its share of
+    # the evented time, applied to the time per call, over its launches per
+    # call (on the fused path every launch is this kernel).
+    share = k_ms / sum(v[0] for v in launched.values())
+    avg_s = ms / 1e3 * share / (k_n / args.steps)
+    avg_s_events = k_ms / 1e3 / k_n
+    F, Bytes = algorithmic_per_launch(kname, wl)
+    alu_frac = F / avg_s / PEAK_VALU_FP32
+    hbm_frac = Bytes / avg_s / PEAK_HBM
     # the roofline the kernel is closer to (the counters show neither saturated)
-    bound = "alu" if (alu_frac or 0) >= (hbm_frac or 0) else "hbm"
+    bound = "alu" if alu_frac >= hbm_frac else "hbm"
     if bound == "alu":
         roof = {"bound": "alu", "achieved": round(F / avg_s / 1e12, 3), "peak": round(PEAK_VALU_FP32 / 1e12, 1),
                 "unit": "TFLOP/s", "frac": round(alu_frac, 4)}
@@ -223,9 +248,10 @@ def main(argv=None):
     roof["traffic"] = load_traffic(args.workload, kname)
     roof.update({
         "kernel": kname, "launches": k_n, "avg_launch_us": round(avg_s * 1e6, 3),
+        "avg_launch_us_per_launch_events": round(avg_s_events * 1e6, 3),
         "algorithmic_flop_per_launch": int(F), "algorithmic_bytes_per_launch": int(Bytes),
-        "alu_frac": round(alu_frac, 4) if alu_frac else None,
-        "hbm_frac": round(hbm_frac, 4) if hbm_frac else None,
+        "alu_frac": round(alu_frac, 4), "hbm_frac": round(hbm_frac, 4),
+        "kernels_us_per_step": {n: round(v[0] * 1e3 / args.steps, 3) for n, v in launched.items()},
     })
 
     rec = {

@@ -104,27 +104,34 @@ __device__ __forceinline__ void softmax_regs(float (&z)[CM], int C) {
 // co-resident).  A work-group depends only on the border rings of the up to
 // eight tiles around it, so instead of a grid barrier each tile publishes
 // how many rings it has written (flags[tile] = value) and waits until each
-// neighbour has published `value`.  Ordering: every wave first makes its own
-// ring stores visible device-wide (an agent-scope release fence: L2
-// write-back for the other XCDs, then a wait for the wave's stores -- the
-// work-group barrier alone does not wait for other waves' stores), the
-// work-group barrier then orders thread 0's flag store after all of them;
-// the waiting lanes (one per neighbour) poll with relaxed loads and one
-// agent-scope acquire drops stale cache lines before the work-group reads
-// the rings.  With the rings double-buffered this also keeps a tile from
+// neighbour has published `value`.  Ordering: every wave waits until its
+// own ring stores are acknowledged by L2 (the work-group barrier alone does
+// not wait for them), so that after the barrier one agent-scope release by
+// thread 0 (an L2 write-back, for the tiles on other XCDs) covers the stores
+// of the whole work-group before its flag store; the waiting lanes (one per
+// neighbour) poll with relaxed loads and one agent-scope acquire drops stale
+// cache lines before the work-group reads the rings.  With the rings double-buffered this also keeps a tile from
 // overwriting a buffer a neighbour still reads: that neighbour publishes
 // value + 1 only after its read.  The wait is bounded: past kSpinLimit polls
 // the lane records an error in *flag_err and goes on (wrong results, never a
 // hang).
 constexpr unsigned int kSpinLimit = 1u << 22;
+// s_waitcnt operand for vmcnt(0) alone on gfx9-family targets: vmcnt in bits
+// 3:0 and 15:14 zero, expcnt (6:4) and lgkmcnt (11:8) at their maxima
+constexpr int kWaitVmem = 0x0F70;
 
 __device__ __forceinline__ void neighbour_sync(unsigned int* flags, unsigned int* flag_err,
                                                int tile, int tiles_x, int tiles_y,
                                                unsigned int value) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __builtin_amdgcn_s_waitcnt(kWaitVmem);
     __syncthreads();
-    if (threadIdx.x == 0)
+    if (threadIdx.x == 0) {
+        // the write-back must have finished before the flag is visible; the
+        // compiler's own wait after it is dropped when no store is pending
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __builtin_amdgcn_s_waitcnt(kWaitVmem);
         __hip_atomic_store(flags + tile, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     if (threadIdx.x < 9) {
         const int per_img = tiles_x * tiles_y;
         const int ti = tile % per_img;
@@ -142,6 +149,7 @@ __device__ __forceinline__ void neighbour_sync(unsigned int* flags, unsigned int
             }
         }
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        __builtin_amdgcn_s_waitcnt(kWaitVmem);   // invalidation done before the barrier
     }
     __syncthreads();
 }
