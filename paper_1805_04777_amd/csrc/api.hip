@@ -192,6 +192,15 @@ hipError_t launch_iter(const IterArgs& a, int k, bool mat, TileConfig t, int nch
     }
 }
 
+hipError_t launch_stream(const IterArgs& a, int k, size_t lds, hipStream_t s) {
+    switch (k) {
+        case 3: return launch_stream_k3(a, lds, s);
+        case 5: return launch_stream_k5(a, lds, s);
+        case 7: return launch_stream_k7(a, lds, s);
+        default: return hipErrorNotSupported;
+    }
+}
+
 hipError_t launch_resident(const IterArgs& a, int k, TileConfig t, size_t lds, int num_cus,
                            hipStream_t s, bool probe) {
     switch (k) {
@@ -493,16 +502,31 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
                        "); ran one launch per iteration";
         }
         float* ws = static_cast<float*>(ctx->q_ws.p);
+        // Iterations after the first stream their staging under the
+        // computation where that kernel is built (the two-pixel 32 x 32 tile,
+        // k = 3..7, C = 19 or 21, whole float2 rows, unary rows in 16-byte
+        // pieces, buffers under 2 GB).
+        const size_t lds_s = stream_lds_bytes(k, C, mu_dev != nullptr);
+        const bool streamed = !mat && k >= 3 && k <= 7 && (C == 19 || C == 21) && a.vec &&
+                              W % 4 == 0 && reinterpret_cast<uintptr_t>(unary) % 16 == 0 &&
+                              lds_s <= kLdsLimit && (size_t)C * H * W * 4 < (1ull << 31);
+        IterArgs as = a;                      // the streamed launches' tiling
+        as.tiles_x = (W + kStreamTW - 1) / kStreamTW;
+        as.tiles_per_img = as.tiles_x * ((H + kStreamRows - 1) / kStreamRows);
+        as.ntiles = as.tiles_per_img * B;
         // the last iteration writes q_out; earlier ones alternate so that
         // source and destination always differ
         const float* cur = unary;
         for (int t = 0; t < iters; ++t) {
             float* dst = ((iters - 1 - t) % 2 == 0) ? q_out : ws;
-            a.src = cur;
-            a.dst = dst;
-            a.first = t == 0;
+            a.src = as.src = cur;
+            a.dst = as.dst = dst;
+            a.first = as.first = t == 0;
             st = launch(ctx, mat ? kMatIter : kFused, stream, mat ? "materialised_iter" : "fused_iter",
-                        [&] { return launch_iter(a, k, mat, tile, 1, lds, stream); });
+                        [&] {
+                            return (streamed && t > 0) ? launch_stream(as, k, lds_s, stream)
+                                                       : launch_iter(a, k, mat, tile, 1, lds, stream);
+                        });
             if (st != CONVCRF_OK) return st;
             cur = dst;
         }

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <cstddef>
 #include <cstdint>
+#include <utility>
 
 namespace convcrf {
 
@@ -79,6 +80,21 @@ constexpr int iter_lds_stride(int k, int pix, int width) {
     return (width + (k - 1) + pix - 1) / pix * pix;
 }
 
+// Streamed update (k <= 7): two pixels per thread on tiles of kStreamTW x
+// kStreamRows pixels (wide and short, so that each staged row touches few
+// partial cache lines); floats of one staged plane, padded to whole 64-float
+// rows of LDS loads, and the LDS bytes of a work-group (C + 3 planes, the
+// compatibility matrix in whole rows when given, one dummy row of 256 floats
+// for padding loads).
+constexpr int kStreamTW = 64, kStreamRows = 16;
+constexpr int stream_plane(int k) {
+    return ((kStreamRows + k - 1) * iter_lds_stride(k, 2, kStreamTW) + 63) / 64 * 64;
+}
+inline size_t stream_lds_bytes(int k, int C, bool with_compat) {
+    return sizeof(float) * ((size_t)(C + 3) * stream_plane(k) +
+                            (with_compat ? ((size_t)C * C + 63) / 64 * 64 : 0) + 256);
+}
+
 // LDS bytes of one iteration work-group for a k x k window, C classes,
 // with or without the three colour planes and the C x C compatibility.
 // Floats of the LDS region shared by the staged planes (Q and, unless
@@ -104,10 +120,15 @@ inline size_t iter_lds_bytes(int k, int C, TileConfig t, bool with_colour, bool 
 // otherwise).  launch_resident runs all a.iters iterations in one
 // cooperative launch; with probe = true it only reports whether it would
 // (hipSuccess) or not (hipErrorNotSupported / hipErrorCooperativeLaunchTooLarge).
+// launch_stream runs one update with the staging streamed under the
+// computation (not the first iteration; k = 3, 5, 7, C = 19 or 21, vector
+// path); hipErrorNotSupported when the arguments are outside that.
 #define CONVCRF_DECLARE_ITER(K)                                              \
     hipError_t launch_iter_k##K(const IterArgs& a, bool materialised,        \
                                 TileConfig tile, int nchunks, size_t lds,    \
                                 hipStream_t stream);                         \
+    hipError_t launch_stream_k##K(const IterArgs& a, size_t lds,             \
+                                  hipStream_t stream);                       \
     hipError_t launch_resident_k##K(const IterArgs& a, TileConfig tile,      \
                                     size_t lds, int num_cus,                 \
                                     hipStream_t stream, bool probe);

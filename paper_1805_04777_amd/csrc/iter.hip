@@ -652,6 +652,339 @@ hipError_t launch_res(const IterArgs& a, TileConfig t, size_t lds, int num_cus,
                                       dim3(t.threads()), params, (unsigned int)lds, stream);
 }
 
+// ------------------------------------------------------------ streamed update
+// s_waitcnt operand that waits until at most n vector-memory operations of
+// the wave are outstanding (gfx9 encoding; expcnt and lgkmcnt untouched).
+constexpr int vm_wait(int n) {
+    const int v = n < 0 ? 0 : (n > 63 ? 63 : n);
+    return (v & 15) | (v >> 4) << 14 | 7 << 4 | 15 << 8;
+}
+
+// f(integral_constant<int, 0>), ..., f(integral_constant<int, N - 1>)
+template <typename F, int... I>
+__device__ __forceinline__ void static_for(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+
+// Fused update with the staging streamed under the computation (iterations
+// after the first; two pixels per thread on 64 x 16 tiles, all classes,
+// k <= 7).  Instead
+// of loading the whole halo'd tile before the message, every wave issues
+// buffer loads that write straight into LDS (no registers held): the three
+// colour planes and the first two chunks of class planes of Q_t.  As soon
+// as the colours have landed the work-group computes all of its pixels'
+// window weights (Eq. 4) into registers; then it applies them to the classes
+// chunk by chunk, each chunk starting when its planes have landed and
+// issuing the loads of the chunk two ahead, so that at most two chunks are
+// in flight and the early ones do not queue behind the late ones.  The
+// unary tile is loaded the same way, into the planes of chunks already
+// applied, and added in the epilogue (compatibility, softmax, store).
+//
+// Each staged plane is padded to whole 64-float DMA rows and every wave
+// issues the same number of loads per plane (a load past the plane goes to
+// a dummy LDS row), so that a wave waits for a chunk with one constant
+// vmcnt.  Pixels outside the image get an out-of-range buffer offset, which
+// reads as zero: neighbours outside the image contribute nothing.
+// One 64-lane buffer load into LDS: lane l writes the dword at byte offset
+// voffset + soffset of the buffer (zero when out of range) to LDS byte
+// lds_base + 4 l.  Written as assembly so that the compiler neither counts
+// it nor waits for it before LDS reads of other rows: the caller waits with
+// an explicit vmcnt and a work-group barrier before reading what it wrote.
+typedef int rsrc_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void lds_dma(rsrc_t rsrc, unsigned voffset, int soffset,
+                                        unsigned lds_base) {
+    asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dword %0, %1, %2 offen lds"
+                 :
+                 : "v"(voffset), "s"(rsrc), "s"(soffset), "s"(lds_base)
+                 : "memory", "m0");
+}
+
+// The same with 16 bytes per lane (LDS byte lds_base + 16 l); voffset and
+// soffset must be multiples of 16.
+__device__ __forceinline__ void lds_dma16(rsrc_t rsrc, unsigned voffset, int soffset,
+                                          unsigned lds_base) {
+    asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+                 :
+                 : "v"(voffset), "s"(rsrc), "s"(soffset), "s"(lds_base)
+                 : "memory", "m0");
+}
+
+__device__ __forceinline__ rsrc_t buffer_rsrc(const float* base, unsigned bytes) {
+    const unsigned long long p = reinterpret_cast<unsigned long long>(base);
+    rsrc_t r;
+    r.x = (int)(unsigned)p;
+    r.y = (int)(unsigned)(p >> 32);            // stride 0
+    r.z = (int)bytes;                           // num_records
+    r.w = 0x00020000;                           // raw dword access
+    return r;
+}
+
+// Loads per wave of chunk k (classes [k CH, min((k + 1) CH, C))), 0 past
+// the last chunk.
+constexpr int stream_chunk_loads(int k, int C, int CH, int NJ) {
+    return k * CH >= C ? 0 : NJ * (((k + 1) * CH < C ? (k + 1) * CH : C) - k * CH);
+}
+
+template <int K>
+struct StreamShape {
+    static constexpr int R = (K - 1) / 2;
+    static constexpr int TW = kStreamTW, ROWS = kStreamRows;
+    static constexpr int LW = TW + 2 * R, LH = ROWS + 2 * R;
+    static constexpr int LS = iter_lds_stride(K, 2, TW);
+    static constexpr int PLANE = stream_plane(K);
+    static constexpr int NI = PLANE / 64;        // 64-float loads per plane
+    static constexpr int NJ = (NI + 7) / 8;      // per wave and plane
+};
+
+template <int K, int CM, int CH>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void stream_kernel(const IterArgs a) {
+    using SS = StreamShape<K>;
+    constexpr int R = SS::R, LW = SS::LW, LH = SS::LH, LS = SS::LS;
+    constexpr int PLANE = SS::PLANE, NI = SS::NI, NJ = SS::NJ;
+    constexpr int P = 2, TW = SS::TW, ROWS = SS::ROWS, TPR = TW / P;
+    static_assert(TPR * ROWS == 512 && TW * ROWS == 1024, "512 threads, two pixels each");
+    constexpr int NW = P + K - 1;
+    constexpr int CTR = R * K + R;
+    constexpr int NCH = (CM + CH - 1) / CH;
+    constexpr unsigned kOob = 0x80000000u;   // offset past any buffer: reads 0
+
+    constexpr int MUP = (CM * CM + 63) / 64 * 64;   // compatibility, whole rows
+    // the unary tile [CM][ROWS x TW] goes to the planes of chunks 0 .. UCH - 1
+    // once they have been applied (the first chunk whose start frees enough)
+    constexpr int UCH = (CM * 1024 + CH * PLANE - 1) / (CH * PLANE);
+    static_assert(UCH < NCH, "the unary tile fits in the planes of the chunks before the last");
+    constexpr int NU = (CM * 4 + 7) / 8;         // 16-byte loads of 8 rows, per wave
+    extern __shared__ float4 smem4[];
+    float* const smem = reinterpret_cast<float*>(smem4);
+    float* const Qs = smem;                      // [CM][PLANE]
+    float* const Cs = smem + CM * PLANE;         // [3][PLANE]
+    float* const Ms = Cs + 3 * PLANE;            // [CM][CM] (+ padding) when given
+    float* const dummy = Ms + (a.mu ? MUP : 0);  // one 256-float row
+    const unsigned lds0 = (unsigned)(size_t)(__attribute__((address_space(3))) float*)smem;
+    auto lds_addr = [&](const float* p) { return lds0 + (unsigned)((p - smem) * 4); };
+
+    const int H = a.H, W = a.W;
+    const int tile = xcd_tile(blockIdx.x, a.ntiles);
+    const int b = tile / a.tiles_per_img;
+    const int trem = tile - b * a.tiles_per_img;
+    const int tyi = trem / a.tiles_x;
+    const int y0 = tyi * ROWS;
+    const int x0 = (trem - tyi * a.tiles_x) * TW;
+    const size_t HW = (size_t)H * W;
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+
+    // ---- issue every load into LDS: colours, then Q_t class by class
+    unsigned voff[NJ];
+    int dst[NJ];                                 // float offset in a plane, or -1: dummy
+#pragma unroll
+    for (int s = 0; s < NJ; ++s) {
+        const int j = wave + 8 * s;
+        const int f = j * 64 + lane;
+        const int r = f / LS, col = f - (f / LS) * LS;
+        const int gy = y0 - R + r, gx = x0 - R + col;
+        const bool in = j < NI && f < LH * LS && col < LW && gy >= 0 && gy < H && gx >= 0 && gx < W;
+        voff[s] = in ? (unsigned)((gy * W + gx) * 4) : kOob;
+        dst[s] = j < NI ? j * 64 : -1;
+    }
+    const rsrc_t rf = buffer_rsrc(a.feat + (size_t)b * 3 * HW, (unsigned)(3 * HW * 4));
+    const rsrc_t rq = buffer_rsrc(a.src + (size_t)b * CM * HW, (unsigned)(CM * HW * 4));
+    // the compatibility matrix rides with the colours: MUP / 64 rows, one
+    // per wave in turn (the same count on every wave: wave-uniform loads
+    // past the matrix go to the dummy row)
+    constexpr int NMU = (MUP / 64 + 7) / 8;
+    const int nmu = a.mu ? NMU : 0;
+    const rsrc_t rm = buffer_rsrc(a.mu ? a.mu : a.feat, (unsigned)(CM * CM * 4));
+    for (int s = 0; s < nmu; ++s) {
+        const int j = wave + 8 * s;
+        lds_dma(rm, (unsigned)((j * 64 + lane) * 4), 0, lds_addr(j < MUP / 64 ? Ms + j * 64 : dummy));
+    }
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch)
+#pragma unroll
+        for (int s = 0; s < NJ; ++s)
+            lds_dma(rf, voff[s], (int)(ch * HW * 4),
+                    lds_addr(dst[s] >= 0 ? Cs + ch * PLANE + dst[s] : dummy));
+    auto issue_chunk = [&](int k) {
+        const int c_hi = (k + 1) * CH < CM ? (k + 1) * CH : CM;
+        for (int c = k * CH; c < c_hi; ++c)
+#pragma unroll
+            for (int s = 0; s < NJ; ++s)
+                lds_dma(rq, voff[s], (int)(c * HW * 4),
+                        lds_addr(dst[s] >= 0 ? Qs + c * PLANE + dst[s] : dummy));
+    };
+    issue_chunk(0);
+    if (NCH > 1) issue_chunk(1);
+
+    const int tx = tid % TPR, ty = tid / TPR;
+    const int col0 = tx * P;
+    const int y = y0 + ty, xb = x0 + col0;
+    const bool pix_ok = y < H && xb < W;        // W even: both pixels or neither
+
+    // ---- colours landed: the window weights of both pixels, all rows
+    __builtin_amdgcn_s_waitcnt(vm_wait(stream_chunk_loads(0, CM, CH, NJ) +
+                                       stream_chunk_loads(1, CM, CH, NJ)));
+    __syncthreads();
+    float w[K][P][K];
+    {
+        float own[3][P];
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch)
+#pragma unroll
+            for (int i = 0; i < P; ++i) own[ch][i] = Cs[ch * PLANE + (ty + R) * LS + col0 + R + i];
+#pragma unroll
+        for (int dy = 0; dy < K; ++dy) {
+            float nc[3][NW];
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) lds_row<NW, P>(Cs + ch * PLANE + (ty + dy) * LS + col0, nc[ch]);
+#pragma unroll
+            for (int i = 0; i < P; ++i) {
+#pragma unroll
+                for (int dx = 0; dx < K; ++dx) {
+                    if (dy * K + dx == CTR) { w[dy][i][dx] = 0.f; continue; }
+                    const int n = (dx - R) * (dx - R) + (dy - R) * (dy - R);
+                    const float d0 = own[0][i] - nc[0][i + dx];
+                    const float d1 = own[1][i] - nc[1][i + dx];
+                    const float d2 = own[2][i] - nc[2][i + dx];
+                    const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
+                    w[dy][i][dx] = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, a.taps.app_log2[n])) +
+                                   a.taps.smooth[n];
+                }
+            }
+        }
+    }
+
+    // ---- the message, chunk by chunk as the planes land
+    float acc[P][CM];
+#pragma unroll
+    for (int i = 0; i < P; ++i)
+#pragma unroll
+        for (int c = 0; c < CM; ++c) acc[i][c] = 0.f;
+    float* const Us = Qs;                        // [CM][ROWS x TW], from chunk UCH on
+    const rsrc_t ru = buffer_rsrc(a.unary + (size_t)b * CM * HW, (unsigned)(CM * HW * 4));
+    static_for([&](auto kc) {
+        constexpr int k = decltype(kc)::value;
+        constexpr int c_lo = k * CH;
+        constexpr int c_hi = (k + 1) * CH < CM ? (k + 1) * CH : CM;
+        // chunk k landed.  Issued after its loads (at chunk k - 2) and
+        // before this wait: chunk k + 1 (at chunk k - 1), and the unary if
+        // it went out at chunk k - 2 or k - 1.
+        __builtin_amdgcn_s_waitcnt(vm_wait(stream_chunk_loads(k + 1, CM, CH, NJ) +
+                                           (UCH < k && k <= UCH + 2 ? NU : 0)));
+        __syncthreads();
+        if constexpr (k + 2 < NCH) issue_chunk(k + 2);
+        if constexpr (k == UCH) {
+            // every wave is past the chunks before k: their planes take the
+            // unary tile, plane c at Us + 1024 c, 256 / TW rows per load
+#pragma unroll
+            for (int s = 0; s < NU; ++s) {
+                const int j = wave + 8 * s;          // (plane, band of 256 / TW rows)
+                constexpr int LPR = TW / 4;          // lanes per row
+                const int c = j / 4, r = (j % 4) * (256 / TW) + lane / LPR, col = (lane % LPR) * 4;
+                const bool in = j < CM * 4 && y0 + r < H && x0 + col < W;
+                lds_dma16(ru, in ? (unsigned)(((y0 + r) * W + x0 + col) * 4) : kOob,
+                          (int)((j < CM * 4 ? c : 0) * HW * 4),
+                          lds_addr(j < CM * 4 ? Us + j * 256 : dummy));
+            }
+        }
+        // (class, window row) steps of this chunk, LDS rows read two steps
+        // ahead of the one being applied
+        constexpr int kDepth = 3;
+        constexpr int nsteps = (c_hi - c_lo) * K;
+        float qr[kDepth][NW];
+#pragma unroll
+        for (int t = 0; t < kDepth - 1; ++t)
+            if (t < nsteps)
+                lds_row<NW, P>(Qs + (c_lo + t / K) * PLANE + (ty + t % K) * LS + col0, qr[t]);
+#pragma unroll
+        for (int t = 0; t < CH * K; ++t) {
+            if (t < nsteps) {
+                const int nx = t + kDepth - 1;
+                if (nx < nsteps)
+                    lds_row<NW, P>(Qs + (c_lo + nx / K) * PLANE + (ty + nx % K) * LS + col0,
+                                   qr[nx % kDepth]);
+                const int c = c_lo + t / K, dy = t % K;
+#pragma unroll
+                for (int i = 0; i < P; ++i)
+#pragma unroll
+                    for (int dx = 0; dx < K; ++dx)
+                        if (dy * K + dx != CTR)
+                            acc[i][c] = fmaf(w[dy][i][dx], qr[t % kDepth][i + dx], acc[i][c]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        if (a.include_center) {
+#pragma unroll
+            for (int c = c_lo; c < c_hi; ++c)
+#pragma unroll
+                for (int i = 0; i < P; ++i)
+                    acc[i][c] = fmaf(a.center_w, Qs[c * PLANE + (ty + R) * LS + col0 + R + i],
+                                     acc[i][c]);
+        }
+    }, std::make_integer_sequence<int, NCH>{});
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));
+    __syncthreads();
+    float u[P][CM];
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        const float2 t = *reinterpret_cast<const float2*>(Us + c * 1024 + ty * TW + col0);
+        u[0][c] = t.x;
+        u[1][c] = t.y;
+    }
+    if (!pix_ok) return;
+
+    // ---- compatibility, unary, softmax (Alg. 1), store Q_{t+1}
+    if (a.mu) {
+        float z[P][CM];
+#pragma unroll
+        for (int l = 0; l < CM; ++l) {
+            float t[P];
+#pragma unroll
+            for (int i = 0; i < P; ++i) t[i] = 0.f;
+#pragma unroll
+            for (int lp = 0; lp < CM; ++lp) {
+                const float m = Ms[l * CM + lp];
+#pragma unroll
+                for (int i = 0; i < P; ++i) t[i] = fmaf(m, acc[i][lp], t[i]);
+            }
+#pragma unroll
+            for (int i = 0; i < P; ++i) z[i][l] = u[i][l] - t[i];
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int i = 0; i < P; ++i)
+#pragma unroll
+            for (int c = 0; c < CM; ++c) acc[i][c] = z[i][c];
+    } else {
+        // Potts: softmax(U + M)
+#pragma unroll
+        for (int i = 0; i < P; ++i)
+#pragma unroll
+            for (int c = 0; c < CM; ++c) acc[i][c] += u[i][c];
+    }
+#pragma unroll
+    for (int i = 0; i < P; ++i) softmax_regs<CM, true>(acc[i], CM);
+    float* __restrict__ qd = a.dst + (size_t)b * CM * HW + (size_t)y * W + xb;
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        float tmp[P];
+#pragma unroll
+        for (int i = 0; i < P; ++i) tmp[i] = acc[i][c];
+        *reinterpret_cast<typename Vec<P>::T*>(qd + c * HW) = Vec<P>::make(tmp);
+    }
+}
+
+template <int K, int CM, int CH>
+hipError_t launch_stream(const IterArgs& a, size_t lds, hipStream_t stream) {
+    auto fn = stream_kernel<K, CM, CH>;
+    hipError_t e = allow_full_lds(fn);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fn, dim3(a.ntiles), dim3(512), lds, stream, a);
+    return hipGetLastError();
+}
+
 // The built tile shapes: {P = 2 or 4, width 32, S = 1}, {P = 2, width 32,
 // S = 2} (fused only) and {P = 4, width 16, S = 4} (fused, small grids).
 template <int K, int CM, bool EXACT>
@@ -698,6 +1031,24 @@ hipError_t CRF_CAT(launch_iter_k, CRF_K)(const IterArgs& a, bool materialised, T
     if (a.C <= 8) return launch_cm<K, 8, false>(a, materialised, tile, nchunks, lds, stream);
     if (a.C <= 16) return launch_cm<K, 16, false>(a, materialised, tile, nchunks, lds, stream);
     return launch_cm<K, 24, false>(a, materialised, tile, nchunks, lds, stream);
+}
+
+// Streamed updates are built for k = 3, 5, 7 and the class counts 19 and 21.
+hipError_t CRF_CAT(launch_stream_k, CRF_K)(const IterArgs& a, size_t lds, hipStream_t stream) {
+    constexpr int K = CRF_K;
+    if constexpr (K < 3 || K > 7) {
+        return hipErrorNotSupported;
+    } else {
+        if (a.mode != kModeUpdate || a.first || a.planes != a.C || !a.vec || (a.W & 3) ||
+            reinterpret_cast<uintptr_t>(a.unary) % 16 != 0 ||
+            (size_t)a.C * a.H * a.W * 4 >= (1ull << 31))
+            return hipErrorNotSupported;
+        switch (a.C) {
+            case 19: return launch_stream<K, 19, 4>(a, lds, stream);
+            case 21: return launch_stream<K, 21, 3>(a, lds, stream);
+            default: return hipErrorNotSupported;
+        }
+    }
 }
 
 // Resident launches are built for the two-pixel, one-group tile of k <= 7
