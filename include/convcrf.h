@@ -87,8 +87,9 @@ typedef struct {
                                pooled grid and is bilinearly upsampled (half-
                                pixel centres, edge clamp) before the
                                compatibility step.  H and W must be multiples
-                               of s.  Only the fused variant implements it
-                               (the resident variant runs it as fused). */
+                               of s, H / s and B at most 65535.  Only the
+                               fused variant implements it (the resident
+                               variant runs it as fused). */
     int32_t include_center; /* 0: the centre tap q == p is excluded (Alg. 1
                                sums over i != j; default).  1: it is included
                                with weight K(p,p) = w_app + w_smooth, the

@@ -101,6 +101,8 @@ convcrf_status validate(convcrf_ctx* ctx, int B, int C, int H, int W, const conv
         return fail(ctx, CONVCRF_E_UNSUPPORTED, "blur is not built for the materialised variant");
     if (s > 1 && (H % s != 0 || W % s != 0))
         return fail(ctx, CONVCRF_E_UNSUPPORTED, "H and W must be multiples of the blur factor");
+    if (s > 1 && (H / s > 65535 || B > 65535))
+        return fail(ctx, CONVCRF_E_UNSUPPORTED, "blur grid: H / blur and B must be at most 65535");
     const long long npix = (long long)B * H * W;
     if (npix * (long long)C > (1LL << 40))
         return fail(ctx, CONVCRF_E_UNSUPPORTED, "tensor too large");

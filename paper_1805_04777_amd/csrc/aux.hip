@@ -88,47 +88,72 @@ __global__ __launch_bounds__(256) void build_kernel_kernel(const float* __restri
 }
 
 // ------------------------------------------------------------------ pooling
-// One thread per pooled cell; `nch` planes (up to CM), optional softmax.
+// Blur path layout: one thread per full-resolution pixel; a block covers the
+// s rows of one pooled row Y and 64 columns (block = s waves, lanes along x,
+// so every load and store is a contiguous row piece).  The s x s average of
+// a cell is a sum over its s adjacent lanes (shuffles; W and 64 are
+// multiples of s) and then over the block's s waves (LDS).
+constexpr int kPoolCols = 64;
+
+// Average of v over the s x s cell of this thread; valid in the threads of
+// row 0 whose column is the cell's first (returns true there).
 template <int CM, bool EXACT>
-__global__ __launch_bounds__(256) void pool_kernel(const float* __restrict__ src,
-                                                   float* __restrict__ dst, int B, int nch,
-                                                   int H, int W, int s, int softmax_first) {
-    const int Hp = H / s, Wp = W / s;
-    const long long HWp = (long long)Hp * Wp;
-    const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (gid >= (long long)B * HWp) return;
-    const int b = (int)(gid / HWp);
-    const int pc = (int)(gid - b * HWp);
-    const int Y = pc / Wp, X = pc - (pc / Wp) * Wp;
-    const size_t HW = (size_t)H * W;
-    const float* sp = src + (size_t)b * nch * HW;
-    float acc[CM];
+__device__ __forceinline__ bool cell_average(float (&v)[CM], int C, int s, float* red) {
+    const int l = threadIdx.x % kPoolCols, r = threadIdx.x / kPoolCols;
 #pragma unroll
-    for (int c = 0; c < CM; ++c) acc[c] = 0.f;
-    for (int i = 0; i < s; ++i) {
-        for (int j = 0; j < s; ++j) {
-            const size_t p = (size_t)(Y * s + i) * W + X * s + j;
-            float v[CM];
-#pragma unroll
-            for (int c = 0; c < CM; ++c) v[c] = (EXACT || c < nch) ? sp[c * HW + p] : 0.f;
-            if (softmax_first) softmax_regs<CM, EXACT>(v, nch);
-#pragma unroll
-            for (int c = 0; c < CM; ++c) acc[c] += v[c];
-        }
+    for (int c = 0; c < CM; ++c) {
+        if (!EXACT && c >= C) continue;
+        for (int off = 1; off < s; off <<= 1) v[c] += __shfl_xor(v[c], off, 64);
     }
-    const float inv = 1.0f / (float)(s * s);
-    float* dp = dst + (size_t)b * nch * HWp + pc;
+    if (l % s == 0) {
 #pragma unroll
-    for (int c = 0; c < CM; ++c)
-        if (EXACT || c < nch) dp[c * HWp] = acc[c] * inv;
+        for (int c = 0; c < CM; ++c)
+            if (EXACT || c < C) red[(r * (kPoolCols / s) + l / s) * CM + c] = v[c];
+    }
+    __syncthreads();
+    if (r != 0 || l % s != 0) return false;
+    const float inv = 1.0f / (float)(s * s);
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        if (!EXACT && c >= C) continue;
+        float t = 0.f;
+        for (int rr = 0; rr < s; ++rr) t += red[(rr * (kPoolCols / s) + l / s) * CM + c];
+        v[c] = t * inv;
+    }
+    return true;
+}
+
+// s x s average pooling of nch planes (Sec. 4.2), optionally of softmax(src)
+// over the planes.  Grid (ceil(W / 64), H / s, B), block s * 64.
+template <int CM, bool EXACT>
+__global__ __launch_bounds__(512) void pool_kernel(const float* __restrict__ src,
+                                                   float* __restrict__ dst, int nch, int H,
+                                                   int W, int s, int softmax_first) {
+    __shared__ float red[kPoolCols * CM];
+    const int Hp = H / s, Wp = W / s;
+    const int Y = blockIdx.y, b = blockIdx.z;
+    const int x = blockIdx.x * kPoolCols + threadIdx.x % kPoolCols;
+    const int y = Y * s + threadIdx.x / kPoolCols;
+    const bool active = x < W;
+    const size_t HW = (size_t)H * W;
+    const float* sp = src + (size_t)b * nch * HW + (size_t)y * W + (active ? x : W - 1);
+    float v[CM];
+#pragma unroll
+    for (int c = 0; c < CM; ++c) v[c] = (EXACT || c < nch) ? sp[c * HW] : 0.f;
+    if (softmax_first) softmax_regs<CM, EXACT>(v, nch);
+    if (cell_average<CM, EXACT>(v, nch, s, red) && active) {
+        const size_t HWp = (size_t)Hp * Wp;
+        float* dp = dst + (size_t)b * nch * HWp + (size_t)Y * Wp + x / s;
+#pragma unroll
+        for (int c = 0; c < CM; ++c)
+            if (EXACT || c < nch) dp[c * HWp] = v[c];
+    }
 }
 
 // ------------------------------------------------------------- blur update
-// Thread order: (b, Y, X) pooled cell major, (i, j) within the s x s block
-// minor, so that the s*s pixels of one pooled cell are adjacent lanes of one
-// wavefront (s*s divides 64) and their average is a lane reduction.
+// Half-pixel-centred bilinear source coordinate of output o on a grid of n
+// cells of s pixels: o samples (o + 0.5) / s - 0.5, clamped at 0 and n - 1.
 __device__ __forceinline__ void src_coord(int o, int s, int n, int& i0, int& i1, float& f) {
-    // half-pixel centres: output o samples (o + 0.5) / s - 0.5, clamped at 0
     float u = ((float)o + 0.5f) / (float)s - 0.5f;
     u = fmaxf(u, 0.f);
     int a = (int)u;
@@ -138,81 +163,279 @@ __device__ __forceinline__ void src_coord(int o, int s, int n, int& i0, int& i1,
     f = u - (float)a;
 }
 
+// One blur iteration after the pooled message: bilinear upsampling of the
+// message, compatibility, unary and softmax (Alg. 1) per pixel, then the
+// full Q (last iteration) or its s x s average for the next pooled message.
+// Same layout as pool_kernel.
 template <int CM, bool EXACT>
-__global__ __launch_bounds__(256) void blur_update_kernel(
+__global__ __launch_bounds__(512) void blur_update_kernel(
     const float* __restrict__ mp, const float* __restrict__ unary, const float* __restrict__ mu,
-    float* __restrict__ q_full, float* __restrict__ q_pooled, int B, int C, int H, int W, int s) {
+    float* __restrict__ q_full, float* __restrict__ q_pooled, int C, int H, int W, int s) {
+    __shared__ float red[kPoolCols * CM];
     const int Hp = H / s, Wp = W / s;
-    const int ss = s * s;
-    const long long HWp = (long long)Hp * Wp;
-    const long long n = (long long)B * HWp * ss;
-    const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    // every lane of a block group is active or inactive together (ss | 64)
-    const bool active = gid < n;
-    const long long cell = active ? gid / ss : 0;
-    const int within = (int)(gid - cell * ss);
-    const int b = (int)(cell / HWp);
-    const int pc = (int)(cell - b * HWp);
-    const int Y = pc / Wp, X = pc - (pc / Wp) * Wp;
-    const int y = Y * s + within / s, x = X * s + (within - (within / s) * s);
-
+    const int Y = blockIdx.y, b = blockIdx.z;
+    const int x = blockIdx.x * kPoolCols + threadIdx.x % kPoolCols;
+    const int y = Y * s + threadIdx.x / kPoolCols;
+    const bool active = x < W;
+    const int xc = active ? x : W - 1;
+    const size_t HW = (size_t)H * W, HWp = (size_t)Hp * Wp;
+    int x0, x1, y0, y1;
+    float fx, fy;
+    src_coord(xc, s, Wp, x0, x1, fx);
+    src_coord(y, s, Hp, y0, y1, fy);
+    const float* m = mp + (size_t)b * C * HWp;
+    const int o00 = y0 * Wp + x0, o01 = y0 * Wp + x1, o10 = y1 * Wp + x0, o11 = y1 * Wp + x1;
+    const float* u = unary + (size_t)b * C * HW + (size_t)y * W + xc;
+    // every load first (the four bilinear taps of each class and the unary),
+    // so that they are in flight together rather than one class at a time
+    float t00[CM], t01[CM], t10[CM], t11[CM], uv[CM];
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        const bool on = EXACT || c < C;
+        const float* mc = m + (size_t)(on ? c : 0) * HWp;
+        t00[c] = on ? mc[o00] : 0.f;
+        t01[c] = on ? mc[o01] : 0.f;
+        t10[c] = on ? mc[o10] : 0.f;
+        t11[c] = on ? mc[o11] : 0.f;
+        uv[c] = on ? u[(size_t)c * HW] : 0.f;
+    }
     float z[CM];
-    if (active) {
-        int y0, y1, x0, x1;
-        float fy, fx;
-        src_coord(y, s, Hp, y0, y1, fy);
-        src_coord(x, s, Wp, x0, x1, fx);
-        const float* m = mp + (size_t)b * C * HWp;
-        const int o00 = y0 * Wp + x0, o01 = y0 * Wp + x1, o10 = y1 * Wp + x0, o11 = y1 * Wp + x1;
-        float mv[CM];
 #pragma unroll
-        for (int c = 0; c < CM; ++c) {
-            if (EXACT || c < C) {
-                const float* mc = m + (size_t)c * HWp;
-                const float top = fmaf(fx, mc[o01] - mc[o00], mc[o00]);
-                const float bot = fmaf(fx, mc[o11] - mc[o10], mc[o10]);
-                mv[c] = fmaf(fy, bot - top, top);
-            } else {
-                mv[c] = 0.f;
+    for (int c = 0; c < CM; ++c) {
+        const float top = fmaf(fx, t01[c] - t00[c], t00[c]);
+        const float bot = fmaf(fx, t11[c] - t10[c], t10[c]);
+        z[c] = fmaf(fy, bot - top, top);
+    }
+    if (mu != nullptr) {
+        float t[CM];
+#pragma unroll
+        for (int l = 0; l < CM; ++l) {
+            t[l] = 0.f;
+            if (EXACT || l < C) {
+#pragma unroll
+                for (int lp = 0; lp < CM; ++lp)
+                    if (EXACT || lp < C) t[l] = fmaf(mu[l * C + lp], z[lp], t[l]);
             }
         }
-        if (mu != nullptr) {
 #pragma unroll
-            for (int l = 0; l < CM; ++l) {
-                float t = 0.f;
-                if (EXACT || l < C) {
+        for (int l = 0; l < CM; ++l) z[l] = -t[l];
+    }
 #pragma unroll
-                    for (int lp = 0; lp < CM; ++lp)
-                        if (EXACT || lp < C) t = fmaf(mu[l * C + lp], mv[lp], t);
-                }
-                z[l] = -t;
-            }
-        } else {
-#pragma unroll
-            for (int l = 0; l < CM; ++l) z[l] = mv[l];
-        }
-        const size_t HW = (size_t)H * W;
-        const float* u = unary + (size_t)b * C * HW + (size_t)y * W + x;
-#pragma unroll
-        for (int c = 0; c < CM; ++c)
-            if (EXACT || c < C) z[c] += u[c * HW];
-        softmax_regs<CM, EXACT>(z, C);
-        if (q_full != nullptr) {
+    for (int c = 0; c < CM; ++c) z[c] += uv[c];
+    softmax_regs<CM, EXACT>(z, C);
+    if (q_full != nullptr) {
+        if (active) {
             float* q = q_full + (size_t)b * C * HW + (size_t)y * W + x;
 #pragma unroll
             for (int c = 0; c < CM; ++c)
                 if (EXACT || c < C) q[c * HW] = z[c];
         }
+        return;                                   // uniform over the grid
     }
-    if (q_full != nullptr) return;
-    // s*s-lane average (lanes of one cell are contiguous and aligned)
-    const float inv = 1.0f / (float)ss;
+    if (cell_average<CM, EXACT>(z, C, s, red) && active) {
+        float* dp = q_pooled + (size_t)b * C * HWp + (size_t)Y * Wp + x / s;
+#pragma unroll
+        for (int c = 0; c < CM; ++c)
+            if (EXACT || c < C) dp[c * HWp] = z[c];
+    }
+}
+
+// ---------------------------------------------- four pixels per thread
+// For s = 4 and 8 (W a multiple of 4, 16-byte aligned tensors): a thread
+// owns four adjacent pixels of one row, which lie in one pooled cell, so it
+// loads and stores float4 row pieces (a quarter of the memory instructions)
+// and its bilinear taps come from pooled columns X - 1, X, X + 1 only.  A
+// block covers the s rows of one pooled row Y and 256 columns; the cell sum
+// is in-thread, over the s / 4 lanes of a cell (shuffles) and over the s
+// rows (LDS).
+constexpr int kPool4Lanes = 64;
+
+// red holds s * 64 / (s / 4) = 256 cells of CM values.
+template <int CM, bool EXACT>
+__device__ __forceinline__ bool cell_average4(float (&v)[CM], int C, int s, float* red) {
+    const int l = threadIdx.x % kPool4Lanes, r = threadIdx.x / kPool4Lanes;
+    const int lpc = s / 4;                         // lanes per cell: 1 or 2
 #pragma unroll
     for (int c = 0; c < CM; ++c) {
         if (!EXACT && c >= C) continue;
-        float v = active ? z[c] : 0.f;
-        for (int off = 1; off < ss; off <<= 1) v += __shfl_xor(v, off, 64);
-        if (active && within == 0) q_pooled[(size_t)b * C * HWp + (size_t)c * HWp + pc] = v * inv;
+        if (lpc == 2) v[c] += __shfl_xor(v[c], 1, 64);
+    }
+    if (l % lpc == 0) {
+#pragma unroll
+        for (int c = 0; c < CM; ++c)
+            if (EXACT || c < C) red[(r * (kPool4Lanes / lpc) + l / lpc) * CM + c] = v[c];
+    }
+    __syncthreads();
+    if (r != 0 || l % lpc != 0) return false;
+    const float inv = 1.0f / (float)(s * s);
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        if (!EXACT && c >= C) continue;
+        float t = 0.f;
+        for (int rr = 0; rr < s; ++rr) t += red[(rr * (kPool4Lanes / lpc) + l / lpc) * CM + c];
+        v[c] = t * inv;
+    }
+    return true;
+}
+
+// Grid (ceil(W / 256), H / s, B), block 64 s.
+template <int CM, bool EXACT>
+__global__ __launch_bounds__(512) void pool4_kernel(const float* __restrict__ src,
+                                                    float* __restrict__ dst, int nch, int H,
+                                                    int W, int s, int softmax_first) {
+    __shared__ float red[4 * kPool4Lanes * CM];   // s rows x 64 / (s / 4) cells
+    const int Hp = H / s, Wp = W / s;
+    const int Y = blockIdx.y, b = blockIdx.z;
+    const int x = (blockIdx.x * kPool4Lanes + threadIdx.x % kPool4Lanes) * 4;
+    const int y = Y * s + threadIdx.x / kPool4Lanes;
+    const bool active = x < W;
+    const size_t HW = (size_t)H * W;
+    const float* sp = src + (size_t)b * nch * HW + (size_t)y * W + (active ? x : W - 4);
+    float v[4][CM];
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        const float4 t = (EXACT || c < nch) ? *reinterpret_cast<const float4*>(sp + c * HW)
+                                            : make_float4(0.f, 0.f, 0.f, 0.f);
+        v[0][c] = t.x; v[1][c] = t.y; v[2][c] = t.z; v[3][c] = t.w;
+    }
+    float a[CM];
+#pragma unroll
+    for (int c = 0; c < CM; ++c) a[c] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (softmax_first) softmax_regs<CM, EXACT>(v[j], nch);
+#pragma unroll
+        for (int c = 0; c < CM; ++c) a[c] += v[j][c];
+    }
+    if (cell_average4<CM, EXACT>(a, nch, s, red) && active) {
+        const size_t HWp = (size_t)Hp * Wp;
+        float* dp = dst + (size_t)b * nch * HWp + (size_t)Y * Wp + x / s;
+#pragma unroll
+        for (int c = 0; c < CM; ++c)
+            if (EXACT || c < nch) dp[c * HWp] = a[c];
+    }
+}
+
+template <int CM, bool EXACT>
+__global__ __launch_bounds__(512) void blur_update4_kernel(
+    const float* __restrict__ mp, const float* __restrict__ unary, const float* __restrict__ mu,
+    float* __restrict__ q_full, float* __restrict__ q_pooled, int C, int H, int W, int s) {
+    __shared__ float red[4 * kPool4Lanes * CM];   // s rows x 64 / (s / 4) cells
+    const int Hp = H / s, Wp = W / s;
+    const int Y = blockIdx.y, b = blockIdx.z;
+    const int x = (blockIdx.x * kPool4Lanes + threadIdx.x % kPool4Lanes) * 4;
+    const int y = Y * s + threadIdx.x / kPool4Lanes;
+    const bool active = x < W;
+    const int xc = active ? x : W - 4;
+    const int X = xc / s;                          // the cell of all four pixels
+    const size_t HW = (size_t)H * W, HWp = (size_t)Hp * Wp;
+    int y0, y1;
+    float fy;
+    src_coord(y, s, Hp, y0, y1, fy);
+    const int cm = X > 0 ? X - 1 : 0, cp = X < Wp - 1 ? X + 1 : Wp - 1;
+    // per pixel: the horizontal interpolation as weights on the pooled
+    // columns (X - 1, X, X + 1) -- its two source columns are among them,
+    // and at the clamped ends the two coincide
+    float wx[4][3];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        int a0, a1;
+        float f;
+        src_coord(xc + j, s, Wp, a0, a1, f);
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+            const int col = X - 1 + k;
+            wx[j][k] = (a0 == col ? 1.f - f : 0.f) + (a1 == col ? f : 0.f);
+        }
+        if (X == 0) { wx[j][1] += wx[j][0]; wx[j][0] = 0.f; }            // column -1 is column 0
+        if (X == Wp - 1) { wx[j][1] += wx[j][2]; wx[j][2] = 0.f; }       // column Wp is Wp - 1
+    }
+    const float* m = mp + (size_t)b * C * HWp;
+    const float* u = unary + (size_t)b * C * HW + (size_t)y * W + xc;
+    // logits of the four pixels, built in groups of classes (each group's
+    // loads in flight together, registers bounded)
+    constexpr int G = 7;
+    float z[4][CM];
+#pragma unroll
+    for (int g0 = 0; g0 < CM; g0 += G) {
+        float mv[2][3][G];
+        float4 uv[G];
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+            const int c = g0 + i;
+            const bool on = c < CM && (EXACT || c < C);
+            const float* mc = m + (size_t)(on ? c : 0) * HWp;
+            mv[0][0][i] = on ? mc[y0 * Wp + cm] : 0.f;
+            mv[0][1][i] = on ? mc[y0 * Wp + X] : 0.f;
+            mv[0][2][i] = on ? mc[y0 * Wp + cp] : 0.f;
+            mv[1][0][i] = on ? mc[y1 * Wp + cm] : 0.f;
+            mv[1][1][i] = on ? mc[y1 * Wp + X] : 0.f;
+            mv[1][2][i] = on ? mc[y1 * Wp + cp] : 0.f;
+            uv[i] = on ? *reinterpret_cast<const float4*>(u + (size_t)c * HW)
+                       : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < G; ++i) {
+            const int c = g0 + i;
+            if (c >= CM) continue;
+            const float ua[4] = {uv[i].x, uv[i].y, uv[i].z, uv[i].w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const float top = fmaf(wx[j][2], mv[0][2][i], fmaf(wx[j][1], mv[0][1][i], wx[j][0] * mv[0][0][i]));
+                const float bot = fmaf(wx[j][2], mv[1][2][i], fmaf(wx[j][1], mv[1][1][i], wx[j][0] * mv[1][0][i]));
+                // Potts: U + M; with a general compatibility the unary
+                // is read again after the matvec below
+                z[j][c] = fmaf(fy, bot - top, top);
+                if (mu == nullptr) z[j][c] += ua[j];
+            }
+        }
+    }
+    if (mu != nullptr) {
+        // general compatibility: z <- U - mu M, pixel by pixel
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            float t[CM];
+#pragma unroll
+            for (int l = 0; l < CM; ++l) {
+                t[l] = 0.f;
+                if (EXACT || l < C) {
+#pragma unroll
+                    for (int lp = 0; lp < CM; ++lp)
+                        if (EXACT || lp < C) t[l] = fmaf(mu[l * C + lp], z[j][lp], t[l]);
+                }
+            }
+#pragma unroll
+            for (int l = 0; l < CM; ++l) {
+                const bool on = EXACT || l < C;
+                z[j][l] = on ? u[(size_t)l * HW + j] - t[l] : 0.f;
+            }
+        }
+    }
+    float psum[CM];
+#pragma unroll
+    for (int c = 0; c < CM; ++c) psum[c] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        softmax_regs<CM, EXACT>(z[j], C);
+#pragma unroll
+        for (int c = 0; c < CM; ++c) psum[c] += z[j][c];
+    }
+    if (q_full != nullptr) {
+        if (active) {
+            float* qd = q_full + (size_t)b * C * HW + (size_t)y * W + x;
+#pragma unroll
+            for (int c = 0; c < CM; ++c)
+                if (EXACT || c < C)
+                    *reinterpret_cast<float4*>(qd + (size_t)c * HW) =
+                        make_float4(z[0][c], z[1][c], z[2][c], z[3][c]);
+        }
+        return;                                   // uniform over the grid
+    }
+    if (cell_average4<CM, EXACT>(psum, C, s, red) && active) {
+        float* dp = q_pooled + (size_t)b * C * HWp + (size_t)Y * Wp + x / s;
+#pragma unroll
+        for (int c = 0; c < CM; ++c)
+            if (EXACT || c < C) dp[c * HWp] = psum[c];
     }
 }
 
@@ -248,27 +471,52 @@ hipError_t launch_build_kernel(const float* image, float* out, int B, int H, int
     return hipGetLastError();
 }
 
+// The four-pixel kernels need s >= 4, W a multiple of 4 and 16-byte aligned
+// full-resolution tensors.
+inline bool four_ok(int s, int W, const void* a, const void* b) {
+    return (s == 4 || s == 8) && W % 4 == 0 && reinterpret_cast<uintptr_t>(a) % 16 == 0 &&
+           reinterpret_cast<uintptr_t>(b) % 16 == 0;
+}
+
 hipError_t launch_pool(const float* src, float* dst, int B, int nch, int H, int W, int s,
                        int softmax_first, hipStream_t stream) {
-    const long long n = (long long)B * (H / s) * (W / s);
-    const dim3 grid(nblocks(n, 256)), block(256);
-    if (nch == 21) hipLaunchKernelGGL((pool_kernel<21, true>), grid, block, 0, stream, src, dst, B, nch, H, W, s, softmax_first);
-    else if (nch == 19) hipLaunchKernelGGL((pool_kernel<19, true>), grid, block, 0, stream, src, dst, B, nch, H, W, s, softmax_first);
-    else if (nch == 3) hipLaunchKernelGGL((pool_kernel<3, true>), grid, block, 0, stream, src, dst, B, nch, H, W, s, softmax_first);
-    else if (nch <= 8) hipLaunchKernelGGL((pool_kernel<8, false>), grid, block, 0, stream, src, dst, B, nch, H, W, s, softmax_first);
-    else hipLaunchKernelGGL((pool_kernel<24, false>), grid, block, 0, stream, src, dst, B, nch, H, W, s, softmax_first);
+    if ((long long)B * H * W == 0) return hipSuccess;
+    if (four_ok(s, W, src, src)) {
+        const dim3 grid((W + 4 * kPool4Lanes - 1) / (4 * kPool4Lanes), H / s, B), block(kPool4Lanes * s);
+        if (nch == 21) hipLaunchKernelGGL((pool4_kernel<21, true>), grid, block, 0, stream, src, dst, nch, H, W, s, softmax_first);
+        else if (nch == 19) hipLaunchKernelGGL((pool4_kernel<19, true>), grid, block, 0, stream, src, dst, nch, H, W, s, softmax_first);
+        else if (nch == 3) hipLaunchKernelGGL((pool4_kernel<3, true>), grid, block, 0, stream, src, dst, nch, H, W, s, softmax_first);
+        else if (nch <= 8) hipLaunchKernelGGL((pool4_kernel<8, false>), grid, block, 0, stream, src, dst, nch, H, W, s, softmax_first);
+        else hipLaunchKernelGGL((pool4_kernel<24, false>), grid, block, 0, stream, src, dst, nch, H, W, s, softmax_first);
+        return hipGetLastError();
+    }
+    const dim3 grid((W + kPoolCols - 1) / kPoolCols, H / s, B), block(kPoolCols * s);
+    if (nch == 21) hipLaunchKernelGGL((pool_kernel<21, true>), grid, block, 0, stream, src, dst, nch, H, W, s, softmax_first);
+    else if (nch == 19) hipLaunchKernelGGL((pool_kernel<19, true>), grid, block, 0, stream, src, dst, nch, H, W, s, softmax_first);
+    else if (nch == 3) hipLaunchKernelGGL((pool_kernel<3, true>), grid, block, 0, stream, src, dst, nch, H, W, s, softmax_first);
+    else if (nch <= 8) hipLaunchKernelGGL((pool_kernel<8, false>), grid, block, 0, stream, src, dst, nch, H, W, s, softmax_first);
+    else hipLaunchKernelGGL((pool_kernel<24, false>), grid, block, 0, stream, src, dst, nch, H, W, s, softmax_first);
     return hipGetLastError();
 }
 
 hipError_t launch_blur_update(const float* m_pooled, const float* unary, const float* mu,
                               float* q_full, float* q_pooled, int B, int C, int H, int W, int s,
                               hipStream_t stream) {
-    const long long n = (long long)B * H * W;
-    const dim3 grid(nblocks(n, 256)), block(256);
-    if (C == 21) hipLaunchKernelGGL((blur_update_kernel<21, true>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, B, C, H, W, s);
-    else if (C == 19) hipLaunchKernelGGL((blur_update_kernel<19, true>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, B, C, H, W, s);
-    else if (C <= 8) hipLaunchKernelGGL((blur_update_kernel<8, false>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, B, C, H, W, s);
-    else hipLaunchKernelGGL((blur_update_kernel<24, false>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, B, C, H, W, s);
+    if ((long long)B * H * W == 0) return hipSuccess;
+    // (built for 19, 21 and up to 8 classes; other counts hold too many
+    // values per thread and take the one-pixel kernel)
+    if (four_ok(s, W, unary, q_full ? q_full : unary) && (C == 19 || C == 21 || C <= 8)) {
+        const dim3 grid((W + 4 * kPool4Lanes - 1) / (4 * kPool4Lanes), H / s, B), block(kPool4Lanes * s);
+        if (C == 21) hipLaunchKernelGGL((blur_update4_kernel<21, true>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, C, H, W, s);
+        else if (C == 19) hipLaunchKernelGGL((blur_update4_kernel<19, true>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, C, H, W, s);
+        else hipLaunchKernelGGL((blur_update4_kernel<8, false>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, C, H, W, s);
+        return hipGetLastError();
+    }
+    const dim3 grid((W + kPoolCols - 1) / kPoolCols, H / s, B), block(kPoolCols * s);
+    if (C == 21) hipLaunchKernelGGL((blur_update_kernel<21, true>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, C, H, W, s);
+    else if (C == 19) hipLaunchKernelGGL((blur_update_kernel<19, true>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, C, H, W, s);
+    else if (C <= 8) hipLaunchKernelGGL((blur_update_kernel<8, false>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, C, H, W, s);
+    else hipLaunchKernelGGL((blur_update_kernel<24, false>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, C, H, W, s);
     return hipGetLastError();
 }
 

@@ -95,6 +95,9 @@ def P(**kw):
     ((1, 21, 64, 64, P(w_app=-1.0), 5), cc.E_UNSUPPORTED),
     ((1, 21, 64, 64, P(blur=3), 5), cc.E_INVALID_ARG),
     ((1, 21, 66, 64, P(blur=4), 5), cc.E_UNSUPPORTED),     # H not a multiple of s
+    ((1, 21, 2 * 65536, 8, P(blur=2), 5), cc.E_UNSUPPORTED),  # pooled rows beyond the grid
+    ((65536, 21, 8, 8, P(blur=2), 5), cc.E_UNSUPPORTED),      # batch beyond the grid
+    ((1, 21, 2 * 65535, 8, P(blur=2), 5), cc.OK),
     ((1, 21, 64, 64, P(blur=2, variant=cc.VARIANT_MATERIALISED), 5), cc.E_UNSUPPORTED),
     ((1, 21, 64, 64, P(blur=2, variant=cc.VARIANT_RESIDENT), 5), cc.OK),
     ((1, 21, 64, 64, P(variant=cc.VARIANT_RESIDENT), 5), cc.OK),

@@ -236,7 +236,8 @@ def test_include_center(torch_cuda, crf, oracle_mod):
 
 @pytest.mark.parametrize("s,k,C,H,W", [(2, 3, 3, 16, 24), (2, 5, 21, 34, 50), (4, 11, 21, 64, 96),
                                        (4, 5, 19, 36, 44), (8, 3, 21, 64, 128), (8, 7, 4, 40, 8),
-                                       (4, 5, 21, 64, 64), (4, 3, 21, 128, 128), (2, 15, 13, 96, 80)])
+                                       (4, 5, 21, 64, 64), (4, 3, 21, 128, 128), (2, 15, 13, 96, 80),
+                                       (4, 5, 13, 32, 48), (8, 5, 19, 64, 72)])
 def test_blur_shapes(torch_cuda, crf, oracle_mod, s, k, C, H, W):
     U, I = rand_case(700 + s * k + C, 2, C, H, W)
     p = lib_params(filter_size=k, blur=s)
