@@ -213,6 +213,19 @@ def main(argv=None):
     total_ms = ev0.elapsed_time(ev1)
     ms = total_ms / args.steps
     value = wl.pixels * wl.iters / 1e6 / (ms / 1e3)
+    # distribution pass: each call between its own pair of events
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(args.steps)]
+    for e_start, e_stop in pairs:
+        e_start.record(stream)
+        crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
+        e_stop.record(stream)
+    torch.cuda.synchronize()
+    import numpy as np
+    per_call = np.array([a.elapsed_time(b) for a, b in pairs])
+    dist = {"p10": round(float(np.percentile(per_call, 10)), 5),
+            "p50": round(float(np.median(per_call)), 5),
+            "p90": round(float(np.percentile(per_call, 90)), 5)}
     # kernel pass: the same K steps with HIP events recorded by the library
     # around every launch, on the launch stream
     crf.profile_enable(True)
@@ -257,6 +270,7 @@ def main(argv=None):
     rec = {
         "metric": METRIC, "value": round(value, 2), "unit": UNIT, "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "ms_per_call_distribution": dist,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded Voronoi images and noisy unaries)",
         "config": {"workload": f"{wl.name}: B={wl.B} C={wl.C} {wl.H}x{wl.W} k={wl.filter_size} "

@@ -194,6 +194,20 @@ hipError_t launch_iter(const IterArgs& a, int k, bool mat, TileConfig t, int nch
     }
 }
 
+hipError_t launch_pmsg(const IterArgs& a, int k, int nchunks, size_t lds, hipStream_t s) {
+    switch (k) {
+        case 1: return launch_pmsg_k1(a, nchunks, lds, s);
+        case 3: return launch_pmsg_k3(a, nchunks, lds, s);
+        case 5: return launch_pmsg_k5(a, nchunks, lds, s);
+        case 7: return launch_pmsg_k7(a, nchunks, lds, s);
+        case 9: return launch_pmsg_k9(a, nchunks, lds, s);
+        case 11: return launch_pmsg_k11(a, nchunks, lds, s);
+        case 13: return launch_pmsg_k13(a, nchunks, lds, s);
+        case 15: return launch_pmsg_k15(a, nchunks, lds, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 hipError_t launch_stream(const IterArgs& a, int k, size_t lds, hipStream_t s) {
     switch (k) {
         case 3: return launch_stream_k3(a, lds, s);
@@ -212,10 +226,6 @@ hipError_t launch_resident(const IterArgs& a, int k, TileConfig t, size_t lds, i
         case 7: return launch_resident_k7(a, t, lds, num_cus, s, probe);
         default: return hipErrorNotSupported;
     }
-}
-
-int tiles_of(TileConfig t, int B, int H, int W) {
-    return B * ((H + t.rows - 1) / t.rows) * ((W + t.width - 1) / t.width);
 }
 
 // Tile of the iteration kernel: the first candidate whose LDS fits one
@@ -544,22 +554,13 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     float* qp = static_cast<float*>(ctx->pool_q.p);
     float* mp = static_cast<float*>(ctx->pool_m.p);
     float* fp = static_cast<float*>(ctx->pool_f.p);
-    // pooled grid: full-width tiles if they give every CU two work-groups,
-    // otherwise 16 x 16 tiles shared by four row groups, with the classes
-    // split into chunks (the message does not mix classes; each chunk
-    // recomputes the weights)
-    TileConfig tile = pick_tile(k, C, true, false, false);
-    if (tile.rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
-    int nchunks = 1, chunk = C;
-    if (tiles_of(tile, B, Hp, Wp) < 2 * ctx->num_cus) {
-        tile = TileConfig{16, 4, 16, 4};
-        const int tiles = tiles_of(tile, B, Hp, Wp);
-        nchunks = (2 * ctx->num_cus + tiles - 1) / tiles;
-        nchunks = nchunks < 1 ? 1 : (nchunks > (C + 3) / 4 ? (C + 3) / 4 : nchunks);  // >= 4 classes each
-        chunk = (C + nchunks - 1) / nchunks;
-        nchunks = (C + chunk - 1) / chunk;
-    }
-    const size_t lds = iter_lds_bytes(k, chunk, tile, true, false);
+    // pooled message: 16 x 8 cell tiles, one wavefront per window row, the
+    // classes in chunks of at most kPmsgClasses (the message does not mix
+    // classes; each chunk recomputes the weights)
+    const int nchunks = (C + kPmsgClasses - 1) / kPmsgClasses;
+    const int chunk = (C + nchunks - 1) / nchunks;
+    const size_t lds = pmsg_lds_bytes(k);
+    if (lds > kLdsLimit) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window exceeds LDS");
     st = launch(ctx, kPool, stream, "blur_pool",
                 [&] { return launch_pool(image, fp, B, 3, H, W, s, 0, stream); });
     if (st != CONVCRF_OK) return st;
@@ -578,13 +579,13 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     a.dst = mp;
     a.first = 0;
     a.mode = kModeMessage;
-    a.tiles_x = (Wp + tile.width - 1) / tile.width;
-    a.tiles_per_img = a.tiles_x * ((Hp + tile.rows - 1) / tile.rows);
+    a.tiles_x = (Wp + kPmsgTW - 1) / kPmsgTW;
+    a.tiles_per_img = a.tiles_x * ((Hp + kPmsgTH - 1) / kPmsgTH);
     a.ntiles = a.tiles_per_img * B;
-    a.vec = (Wp % tile.pix == 0);
+    a.vec = 0;
     for (int t = 0; t < iters; ++t) {
         st = launch(ctx, kBlurMsg, stream, "blur_message",
-                    [&] { return launch_iter(a, k, false, tile, nchunks, lds, stream); });
+                    [&] { return launch_pmsg(a, k, nchunks, lds, stream); });
         if (st != CONVCRF_OK) return st;
         const bool last = t == iters - 1;
         st = launch(ctx, kBlurUpd, stream, "blur_update", [&] {

@@ -95,6 +95,17 @@ inline size_t stream_lds_bytes(int k, int C, bool with_compat) {
                             (with_compat ? ((size_t)C * C + 63) / 64 * 64 : 0) + 256);
 }
 
+// Pooled message of the blur path: tiles of 16 x 8 cells, one wavefront per
+// window row (64 k threads), chunks of at most kPmsgClasses classes; LDS
+// bytes of a work-group (the chunk's planes and the colours with their halo,
+// and the k row partials of every class and cell).
+constexpr int kPmsgClasses = 12, kPmsgTW = 16, kPmsgTH = 8;
+inline size_t pmsg_lds_bytes(int k) {
+    const int lh = kPmsgTH + k - 1, ls = (kPmsgTW + k - 1 + 1) / 2 * 2;
+    return sizeof(float) * ((size_t)(kPmsgClasses + 3) * lh * ls +
+                            (size_t)k * kPmsgClasses * kPmsgTW * kPmsgTH);
+}
+
 // LDS bytes of one iteration work-group for a k x k window, C classes,
 // with or without the three colour planes and the C x C compatibility.
 // Floats of the LDS region shared by the staged planes (Q and, unless
@@ -129,6 +140,8 @@ inline size_t iter_lds_bytes(int k, int C, TileConfig t, bool with_colour, bool 
                                 hipStream_t stream);                         \
     hipError_t launch_stream_k##K(const IterArgs& a, size_t lds,             \
                                   hipStream_t stream);                       \
+    hipError_t launch_pmsg_k##K(const IterArgs& a, int nchunks, size_t lds,  \
+                                hipStream_t stream);                         \
     hipError_t launch_resident_k##K(const IterArgs& a, TileConfig tile,      \
                                     size_t lds, int num_cus,                 \
                                     hipStream_t stream, bool probe);

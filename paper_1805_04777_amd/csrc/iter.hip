@@ -1,7 +1,7 @@
 // iter.hip -- one mean-field iteration of a Convolutional CRF on gfx950.
 //
 // Compiled once per window side k (-DCRF_K=k).  One work-group owns a tile
-// of TW x rows output pixels of one image (TW = 32, or 16 for small grids); it stages Q_t (or softmax(U) on the
+// of 32 x rows output pixels of one image; it stages Q_t (or softmax(U) on the
 // first iteration, Alg. 1 initialisation) and the colour planes of the tile
 // plus an r-pixel halo in LDS, with zeros outside the image, so that
 // neighbours outside the image contribute nothing to the message.  Each
@@ -14,11 +14,15 @@
 //      and applies them to all P pixels (the locally-connected,
 //      channel-constant filter of Eq. 6), one FMA per (pixel, tap, class).
 // The epilogue applies the compatibility transform, adds the unary and
-// normalises with a softmax (Alg. 1), writing Q_{t+1}; in message mode (the
-// pooled message of the blur path, Sec. 4.2) it writes the raw message.
+// normalises with a softmax (Alg. 1), writing Q_{t+1}; in message mode it
+// writes the raw message.
 //
 // The materialised variant reads the weights from a precomputed kernel
 // matrix instead of step 1 (the two-stage structure of Sec. 4.1).
+//
+// Also here: stream_kernel, the same update for the iterations after the
+// first with the staging streamed under the computation, and pmsg_kernel,
+// the message of the blur path on the pooled grid (Sec. 4.2).
 
 #include "crf_internal.h"
 
@@ -162,9 +166,8 @@ __device__ __forceinline__ void neighbour_sync(unsigned int* flags, unsigned int
 // and between iterations the work-groups only exchange the r-pixel border
 // rings of their tiles through a.ring[], synchronised with their neighbours.
 template <int K, int CM, bool EXACT, bool MAT, int P, int TW, int S, bool RES>
-__global__ __launch_bounds__(TW == 16 ? 256 : (P == 4 ? 256 : 512) * S)
-__attribute__((amdgpu_waves_per_eu(TW == 16 ? 1 : (P == 4 ? 1 : 2) * S,
-                                   TW == 16 ? 4 : (P == 4 ? 1 : 2) * S)))
+__global__ __launch_bounds__((P == 4 ? 256 : 512) * S)
+__attribute__((amdgpu_waves_per_eu((P == 4 ? 1 : 2) * S, (P == 4 ? 1 : 2) * S)))
 void iter_kernel(const IterArgs a) {
     constexpr int R = (K - 1) / 2;
     constexpr int LW = TW + 2 * R;            // staged columns
@@ -894,17 +897,25 @@ void stream_kernel(const IterArgs a) {
         constexpr int kDepth = 3;
         constexpr int nsteps = (c_hi - c_lo) * K;
         float qr[kDepth][NW];
+        // per class one base offset the compiler cannot merge with the row
+        // offsets, so that those fold into the LDS reads' immediates
+        const float* qb[CH];
+#pragma unroll
+        for (int i = 0; i < CH; ++i) {
+            unsigned off = (unsigned)((c_lo + i) * PLANE + ty * LS + col0);
+            asm volatile("" : "+v"(off));
+            qb[i] = Qs + off;
+        }
 #pragma unroll
         for (int t = 0; t < kDepth - 1; ++t)
             if (t < nsteps)
-                lds_row<NW, P>(Qs + (c_lo + t / K) * PLANE + (ty + t % K) * LS + col0, qr[t]);
+                lds_row<NW, P>(qb[t / K] + (t % K) * LS, qr[t]);
 #pragma unroll
         for (int t = 0; t < CH * K; ++t) {
             if (t < nsteps) {
                 const int nx = t + kDepth - 1;
                 if (nx < nsteps)
-                    lds_row<NW, P>(Qs + (c_lo + nx / K) * PLANE + (ty + nx % K) * LS + col0,
-                                   qr[nx % kDepth]);
+                    lds_row<NW, P>(qb[nx / K] + (nx % K) * LS, qr[nx % kDepth]);
                 const int c = c_lo + t / K, dy = t % K;
 #pragma unroll
                 for (int i = 0; i < P; ++i)
@@ -985,15 +996,160 @@ hipError_t launch_stream(const IterArgs& a, size_t lds, hipStream_t stream) {
     return hipGetLastError();
 }
 
-// The built tile shapes: {P = 2 or 4, width 32, S = 1}, {P = 2, width 32,
-// S = 2} (fused only) and {P = 4, width 16, S = 4} (fused, small grids).
+// ------------------------------------------------------------ pooled message
+// The message of the blur path (Sec. 4.2) on the s x s pooled grid, which is
+// small (128 x 128 cells at 512^2, s = 4), so parallelism comes from the
+// window: one wavefront per window row.  A work-group owns a tile of 16 x 8
+// cells and a chunk of at most CM classes; it stages the chunk's planes and
+// the pooled colours with their r-cell halo (zeros outside the grid), every
+// wave computes the weights of its window row once (2 cells per lane) and
+// applies them to all classes of the chunk, and the k row partials are
+// summed in LDS, each wave finalising every k-th class.  Output: the raw
+// message M (no compatibility, unary or softmax).
+template <int K>
+struct PmsgShape {
+    static constexpr int R = (K - 1) / 2, P = 2, TW = 16, TH = 8;
+    static constexpr int LW = TW + 2 * R, LH = TH + 2 * R, LS = (LW + 1) / 2 * 2;
+    static constexpr int PLANE = LH * LS, NPX = TW * TH;
+};
+
+template <int K, int CM>
+__global__ __launch_bounds__(64 * K) void pmsg_kernel(const IterArgs a) {
+    using PS = PmsgShape<K>;
+    constexpr int R = PS::R, P = PS::P, TW = PS::TW, TH = PS::TH, LW = PS::LW, LH = PS::LH;
+    constexpr int LS = PS::LS, PLANE = PS::PLANE, NPX = PS::NPX;
+    constexpr int TPR = TW / P, NW = P + K - 1;
+    static_assert(TPR * TH == 64, "one wavefront per window row");
+
+    extern __shared__ float4 smem4[];
+    float* const smem = reinterpret_cast<float*>(smem4);
+    float* const Qs = smem;                      // [CM][PLANE]
+    float* const Cs = smem + CM * PLANE;         // [3][PLANE]
+    float* const Ps = Cs + 3 * PLANE;            // [K][CM][NPX] row partials
+
+    const int C = min(a.C, a.planes - (int)blockIdx.y * a.C);
+    const int H = a.H, W = a.W;
+    const int tile = xcd_tile(blockIdx.x, a.ntiles);
+    const int b = tile / a.tiles_per_img;
+    const int trem = tile - b * a.tiles_per_img;
+    const int tyi = trem / a.tiles_x;
+    const int y0 = tyi * TH, x0 = (trem - tyi * a.tiles_x) * TW;
+    const size_t HW = (size_t)H * W;
+    const float* __restrict__ src = a.src + ((size_t)b * a.planes + (size_t)blockIdx.y * a.C) * HW;
+    const float* __restrict__ feat = a.feat + (size_t)b * 3 * HW;
+
+    // ---- stage the chunk's planes and the colours, zero outside the grid;
+    // every load of a thread is issued before its LDS stores
+    constexpr int NT = 64 * K;
+    constexpr int PER = ((CM + 3) * LH * LW + NT - 1) / NT;
+    const int tid = threadIdx.x;
+    const int nstage = (C + 3) * LH * LW;
+    float v[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int idx = tid + j * NT;
+        const int pl = idx / (LH * LW), rem = idx - pl * (LH * LW);
+        const int r = rem / LW, cc = rem - (rem / LW) * LW;
+        const int gy = y0 - R + r, gx = x0 - R + cc;
+        const bool in = idx < nstage && gy >= 0 && gy < H && gx >= 0 && gx < W;
+        const size_t g = in ? (size_t)gy * W + gx : 0;
+        v[j] = in ? (pl < C ? src[(size_t)pl * HW + g] : feat[(size_t)(pl - C) * HW + g]) : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+        const int idx = tid + j * NT;
+        if (idx >= nstage) continue;
+        const int pl = idx / (LH * LW), rem = idx - pl * (LH * LW);
+        const int r = rem / LW, cc = rem - (rem / LW) * LW;
+        (pl < C ? Qs + pl * PLANE : Cs + (pl - C) * PLANE)[r * LS + cc] = v[j];
+    }
+    __syncthreads();
+
+    // ---- window row g of both cells of this lane
+    const int grp = tid >> 6, lane = tid & 63;
+    const int tx = lane % TPR, ty = lane / TPR, col0 = tx * P;
+    float w[P][K];
+    {
+        float own[3][P], nc[3][NW];
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch) {
+#pragma unroll
+            for (int i = 0; i < P; ++i) own[ch][i] = Cs[ch * PLANE + (ty + R) * LS + col0 + R + i];
+            lds_row<NW, P>(Cs + ch * PLANE + (ty + grp) * LS + col0, nc[ch]);
+        }
+        const int dy = grp - R;
+#pragma unroll
+        for (int i = 0; i < P; ++i) {
+#pragma unroll
+            for (int dx = 0; dx < K; ++dx) {
+                const int n = (dx - R) * (dx - R) + dy * dy;
+                const float d0 = own[0][i] - nc[0][i + dx];
+                const float d1 = own[1][i] - nc[1][i + dx];
+                const float d2 = own[2][i] - nc[2][i + dx];
+                const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
+                const float v = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, a.taps.app_log2[n])) +
+                                a.taps.smooth[n];
+                // the centre: excluded, or K(p, p) when it is included
+                w[i][dx] = (n == 0) ? (a.include_center ? a.center_w : 0.f) : v;
+            }
+        }
+    }
+    float acc[P][CM];
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        if (c >= C) {
+#pragma unroll
+            for (int i = 0; i < P; ++i) acc[i][c] = 0.f;
+            continue;
+        }
+        float q[NW];
+        lds_row<NW, P>(Qs + c * PLANE + (ty + grp) * LS + col0, q);
+#pragma unroll
+        for (int i = 0; i < P; ++i) {
+            float t = 0.f;
+#pragma unroll
+            for (int dx = 0; dx < K; ++dx) t = fmaf(w[i][dx], q[i + dx], t);
+            acc[i][c] = t;
+        }
+    }
+    // ---- sum the K row partials; wave g finalises classes g, g + K, ...
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        if (c >= C) continue;
+        *reinterpret_cast<float2*>(Ps + (grp * CM + c) * NPX + ty * TW + col0) =
+            make_float2(acc[0][c], acc[1][c]);
+    }
+    __syncthreads();
+    const int y = y0 + ty, xb = x0 + col0;
+    if (y >= H) return;
+    float* __restrict__ dst = a.dst + ((size_t)b * a.planes + (size_t)blockIdx.y * a.C) * HW +
+                              (size_t)y * W + xb;
+    for (int c = grp; c < C; c += K) {
+        float m0 = 0.f, m1 = 0.f;
+        for (int gg = 0; gg < K; ++gg) {
+            const float2 t = *reinterpret_cast<const float2*>(Ps + (gg * CM + c) * NPX + ty * TW + col0);
+            m0 += t.x;
+            m1 += t.y;
+        }
+        if (xb < W) dst[(size_t)c * HW] = m0;
+        if (xb + 1 < W) dst[(size_t)c * HW + 1] = m1;
+    }
+}
+
+template <int K>
+hipError_t launch_pmsg_cm(const IterArgs& a, int nchunks, size_t lds, hipStream_t stream) {
+    auto fn = pmsg_kernel<K, kPmsgClasses>;
+    hipError_t e = allow_full_lds(fn);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fn, dim3(a.ntiles, nchunks), dim3(64 * K), lds, stream, a);
+    return hipGetLastError();
+}
+
+// The built tile shapes: {P = 2 or 4, width 32, S = 1} and {P = 2, width 32,
+// S = 2} (fused only).
 template <int K, int CM, bool EXACT>
 hipError_t launch_cm(const IterArgs& a, bool mat, TileConfig t, int nchunks, size_t lds,
                      hipStream_t stream) {
-    if (t.width == 16) {
-        if (mat || t.pix != 4 || t.split != 4) return hipErrorInvalidValue;
-        return launch_one<K, CM, EXACT, false, 4, 16, 4>(a, t, nchunks, lds, stream);
-    }
     if (t.split == 2) {
         if (mat || t.pix != 2) return hipErrorInvalidValue;
         return launch_one<K, CM, EXACT, false, 2, 32, 2>(a, t, nchunks, lds, stream);
@@ -1015,7 +1171,7 @@ hipError_t CRF_CAT(launch_iter_k, CRF_K)(const IterArgs& a, bool materialised, T
                                          int nchunks, size_t lds, hipStream_t stream) {
     constexpr int K = CRF_K;
     if (tile.pix != 2 && tile.pix != 4) return hipErrorInvalidValue;
-    if (tile.width != 32 && tile.width != 16) return hipErrorInvalidValue;
+    if (tile.width != 32) return hipErrorInvalidValue;
     if ((tile.width / tile.pix) * tile.rows % 64 != 0) return hipErrorInvalidValue;  // whole-wave groups
     const int max_threads = tile.width == 16 ? 256 : (tile.pix == 4 ? 256 : 512) * tile.split;
     if (tile.threads() > max_threads) return hipErrorInvalidValue;
@@ -1031,6 +1187,15 @@ hipError_t CRF_CAT(launch_iter_k, CRF_K)(const IterArgs& a, bool materialised, T
     if (a.C <= 8) return launch_cm<K, 8, false>(a, materialised, tile, nchunks, lds, stream);
     if (a.C <= 16) return launch_cm<K, 16, false>(a, materialised, tile, nchunks, lds, stream);
     return launch_cm<K, 24, false>(a, materialised, tile, nchunks, lds, stream);
+}
+
+// Pooled message of the blur path, any k, chunks of at most kPmsgClasses.
+hipError_t CRF_CAT(launch_pmsg_k, CRF_K)(const IterArgs& a, int nchunks, size_t lds,
+                                         hipStream_t stream) {
+    if (a.mode != kModeMessage || a.C < 1 || a.C > kPmsgClasses || nchunks < 1 ||
+        nchunks * a.C < a.planes || (nchunks - 1) * a.C >= a.planes)
+        return hipErrorInvalidValue;
+    return launch_pmsg_cm<CRF_K>(a, nchunks, lds, stream);
 }
 
 // Streamed updates are built for k = 3, 5, 7 and the class counts 19 and 21.
