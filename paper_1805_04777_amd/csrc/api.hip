@@ -514,10 +514,9 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
                        "); ran one launch per iteration";
         }
         float* ws = static_cast<float*>(ctx->q_ws.p);
-        // Iterations after the first stream their staging under the
-        // computation where that kernel is built (the two-pixel 32 x 32 tile,
-        // k = 3..7, C = 19 or 21, whole float2 rows, unary rows in 16-byte
-        // pieces, buffers under 2 GB).
+        // The iterations stream their staging under the computation where
+        // that kernel is built (k = 3..7, C = 19 or 21, whole float2 rows,
+        // unary rows in 16-byte pieces, buffers under 2 GB).
         const size_t lds_s = stream_lds_bytes(k, C, mu_dev != nullptr);
         const bool streamed = !mat && k >= 3 && k <= 7 && (C == 19 || C == 21) && a.vec &&
                               W % 4 == 0 && reinterpret_cast<uintptr_t>(unary) % 16 == 0 &&
@@ -536,8 +535,8 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
             a.first = as.first = t == 0;
             st = launch(ctx, mat ? kMatIter : kFused, stream, mat ? "materialised_iter" : "fused_iter",
                         [&] {
-                            return (streamed && t > 0) ? launch_stream(as, k, lds_s, stream)
-                                                       : launch_iter(a, k, mat, tile, 1, lds, stream);
+                            return streamed ? launch_stream(as, k, lds_s, stream)
+                                            : launch_iter(a, k, mat, tile, 1, lds, stream);
                         });
             if (st != CONVCRF_OK) return st;
             cur = dst;

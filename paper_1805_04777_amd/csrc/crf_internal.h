@@ -132,8 +132,9 @@ inline size_t iter_lds_bytes(int k, int C, TileConfig t, bool with_colour, bool 
 // cooperative launch; with probe = true it only reports whether it would
 // (hipSuccess) or not (hipErrorNotSupported / hipErrorCooperativeLaunchTooLarge).
 // launch_stream runs one update with the staging streamed under the
-// computation (not the first iteration; k = 3, 5, 7, C = 19 or 21, vector
-// path); hipErrorNotSupported when the arguments are outside that.
+// computation (k = 3, 5, 7, C = 19 or 21, vector path; the first iteration
+// applies softmax(U) in LDS); hipErrorNotSupported when the arguments are
+// outside that.
 #define CONVCRF_DECLARE_ITER(K)                                              \
     hipError_t launch_iter_k##K(const IterArgs& a, bool materialised,        \
                                 TileConfig tile, int nchunks, size_t lds,    \

@@ -739,7 +739,11 @@ struct StreamShape {
     static constexpr int NJ = (NI + 7) / 8;      // per wave and plane
 };
 
-template <int K, int CM, int CH>
+// FIRST: the first iteration, whose source is U itself: all planes are
+// loaded at once, each thread keeps the unary of its own pixels in
+// registers, and the staged halo tile is turned into softmax(U) in place
+// (Alg. 1 initialisation) before the message.
+template <int K, int CM, int CH, bool FIRST>
 __global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void stream_kernel(const IterArgs a) {
     using SS = StreamShape<K>;
@@ -818,8 +822,12 @@ void stream_kernel(const IterArgs a) {
                 lds_dma(rq, voff[s], (int)(c * HW * 4),
                         lds_addr(dst[s] >= 0 ? Qs + c * PLANE + dst[s] : dummy));
     };
-    issue_chunk(0);
-    if (NCH > 1) issue_chunk(1);
+    if constexpr (FIRST) {
+        for (int k = 0; k < NCH; ++k) issue_chunk(k);
+    } else {
+        issue_chunk(0);
+        if (NCH > 1) issue_chunk(1);
+    }
 
     const int tx = tid % TPR, ty = tid / TPR;
     const int col0 = tx * P;
@@ -827,8 +835,11 @@ void stream_kernel(const IterArgs a) {
     const bool pix_ok = y < H && xb < W;        // W even: both pixels or neither
 
     // ---- colours landed: the window weights of both pixels, all rows
-    __builtin_amdgcn_s_waitcnt(vm_wait(stream_chunk_loads(0, CM, CH, NJ) +
-                                       stream_chunk_loads(1, CM, CH, NJ)));
+    // (a wait beyond the 63 loads a wave can have outstanding is clamped:
+    // the loads before the last 63 issued have completed by then)
+    __builtin_amdgcn_s_waitcnt(vm_wait(FIRST ? NJ * CM
+                                             : stream_chunk_loads(0, CM, CH, NJ) +
+                                                   stream_chunk_loads(1, CM, CH, NJ)));
     __syncthreads();
     float w[K][P][K];
     {
@@ -859,6 +870,31 @@ void stream_kernel(const IterArgs a) {
         }
     }
 
+    float u[P][CM];
+    if constexpr (FIRST) {
+        // every plane landed: keep this thread's unary, then softmax(U) over
+        // the staged in-image positions (outside the image stays zero)
+        __builtin_amdgcn_s_waitcnt(vm_wait(0));
+        __syncthreads();
+#pragma unroll
+        for (int c = 0; c < CM; ++c)
+#pragma unroll
+            for (int i = 0; i < P; ++i) u[i][c] = Qs[c * PLANE + (ty + R) * LS + col0 + R + i];
+        __syncthreads();
+        for (int pos = tid; pos < LH * LS; pos += 512) {
+            const int r = pos / LS, col = pos - (pos / LS) * LS;
+            const int gy = y0 - R + r, gx = x0 - R + col;
+            if (col >= LW || gy < 0 || gy >= H || gx < 0 || gx >= W) continue;
+            float z[CM];
+#pragma unroll
+            for (int c = 0; c < CM; ++c) z[c] = Qs[c * PLANE + pos];
+            softmax_regs<CM, true>(z, CM);
+#pragma unroll
+            for (int c = 0; c < CM; ++c) Qs[c * PLANE + pos] = z[c];
+        }
+        __syncthreads();
+    }
+
     // ---- the message, chunk by chunk as the planes land
     float acc[P][CM];
 #pragma unroll
@@ -874,11 +910,13 @@ void stream_kernel(const IterArgs a) {
         // chunk k landed.  Issued after its loads (at chunk k - 2) and
         // before this wait: chunk k + 1 (at chunk k - 1), and the unary if
         // it went out at chunk k - 2 or k - 1.
-        __builtin_amdgcn_s_waitcnt(vm_wait(stream_chunk_loads(k + 1, CM, CH, NJ) +
-                                           (UCH < k && k <= UCH + 2 ? NU : 0)));
-        __syncthreads();
-        if constexpr (k + 2 < NCH) issue_chunk(k + 2);
-        if constexpr (k == UCH) {
+        if constexpr (!FIRST) {
+            __builtin_amdgcn_s_waitcnt(vm_wait(stream_chunk_loads(k + 1, CM, CH, NJ) +
+                                               (UCH < k && k <= UCH + 2 ? NU : 0)));
+            __syncthreads();
+        }
+        if constexpr (!FIRST && k + 2 < NCH) issue_chunk(k + 2);
+        if constexpr (!FIRST && k == UCH) {
             // every wave is past the chunks before k: their planes take the
             // unary tile, plane c at Us + 1024 c, 256 / TW rows per load
 #pragma unroll
@@ -935,14 +973,15 @@ void stream_kernel(const IterArgs a) {
                                      acc[i][c]);
         }
     }, std::make_integer_sequence<int, NCH>{});
-    __builtin_amdgcn_s_waitcnt(vm_wait(0));
-    __syncthreads();
-    float u[P][CM];
+    if constexpr (!FIRST) {
+        __builtin_amdgcn_s_waitcnt(vm_wait(0));
+        __syncthreads();
 #pragma unroll
-    for (int c = 0; c < CM; ++c) {
-        const float2 t = *reinterpret_cast<const float2*>(Us + c * 1024 + ty * TW + col0);
-        u[0][c] = t.x;
-        u[1][c] = t.y;
+        for (int c = 0; c < CM; ++c) {
+            const float2 t = *reinterpret_cast<const float2*>(Us + c * 1024 + ty * TW + col0);
+            u[0][c] = t.x;
+            u[1][c] = t.y;
+        }
     }
     if (!pix_ok) return;
 
@@ -989,7 +1028,7 @@ void stream_kernel(const IterArgs a) {
 
 template <int K, int CM, int CH>
 hipError_t launch_stream(const IterArgs& a, size_t lds, hipStream_t stream) {
-    auto fn = stream_kernel<K, CM, CH>;
+    auto fn = a.first ? stream_kernel<K, CM, CH, true> : stream_kernel<K, CM, CH, false>;
     hipError_t e = allow_full_lds(fn);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(a.ntiles), dim3(512), lds, stream, a);
@@ -1204,7 +1243,7 @@ hipError_t CRF_CAT(launch_stream_k, CRF_K)(const IterArgs& a, size_t lds, hipStr
     if constexpr (K < 3 || K > 7) {
         return hipErrorNotSupported;
     } else {
-        if (a.mode != kModeUpdate || a.first || a.planes != a.C || !a.vec || (a.W & 3) ||
+        if (a.mode != kModeUpdate || a.planes != a.C || !a.vec || (a.W & 3) ||
             reinterpret_cast<uintptr_t>(a.unary) % 16 != 0 ||
             (size_t)a.C * a.H * a.W * 4 >= (1ull << 31))
             return hipErrorNotSupported;
