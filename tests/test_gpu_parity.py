@@ -195,6 +195,21 @@ def test_ragged_shapes(torch_cuda, crf, oracle_mod, H, W):
     check(run_gpu(torch_cuda, crf, U, I, p, 4), run_oracle(oracle_mod, U, I, p, 4), f"{H}x{W}")
 
 
+@pytest.mark.parametrize("B,C,k,H,W,T,compat", [
+    (1, 21, 7, 40, 72, 3, False), (1, 21, 7, 40, 72, 3, True), (2, 19, 5, 18, 68, 2, True),
+    (1, 21, 3, 33, 100, 4, False), (1, 19, 7, 70, 132, 1, False), (1, 21, 5, 16, 64, 2, True),
+    (2, 21, 7, 17, 4, 3, False)])
+def test_streamed_path(torch_cuda, crf, oracle_mod, B, C, k, H, W, T, compat):
+    # widths that are multiples of 4 with 19 or 21 classes and k <= 7 take the
+    # streamed update (64 x 16 tiles here partial on both axes; T = 1 runs
+    # its first-iteration form only)
+    U, I = rand_case(1300 + C + k + H + W, B, C, H, W)
+    mu = synth.random_compat(C, seed=k) if compat else None
+    p = lib_params(filter_size=k, compat=mu, w_app=2.0, w_smooth=0.7) if compat else lib_params(filter_size=k)
+    check(run_gpu(torch_cuda, crf, U, I, p, T), run_oracle(oracle_mod, U, I, p, T),
+          f"streamed B={B} C={C} k={k} {H}x{W} T={T} compat={compat}")
+
+
 @pytest.mark.parametrize("T", [0, 1, 2, 3, 6])
 def test_iteration_counts(torch_cuda, crf, oracle_mod, T):
     U, I = rand_case(400 + T, 1, 21, 40, 52)
@@ -237,7 +252,8 @@ def test_include_center(torch_cuda, crf, oracle_mod):
 @pytest.mark.parametrize("s,k,C,H,W", [(2, 3, 3, 16, 24), (2, 5, 21, 34, 50), (4, 11, 21, 64, 96),
                                        (4, 5, 19, 36, 44), (8, 3, 21, 64, 128), (8, 7, 4, 40, 8),
                                        (4, 5, 21, 64, 64), (4, 3, 21, 128, 128), (2, 15, 13, 96, 80),
-                                       (4, 5, 13, 32, 48), (8, 5, 19, 64, 72)])
+                                       (4, 5, 13, 32, 48), (8, 5, 19, 64, 72), (2, 9, 21, 32, 48),
+                                       (4, 13, 19, 64, 64)])
 def test_blur_shapes(torch_cuda, crf, oracle_mod, s, k, C, H, W):
     U, I = rand_case(700 + s * k + C, 2, C, H, W)
     p = lib_params(filter_size=k, blur=s)
