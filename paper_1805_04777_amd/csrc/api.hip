@@ -179,17 +179,17 @@ convcrf_status launch(convcrf_ctx* ctx, int kernel, hipStream_t stream, const ch
     return CONVCRF_OK;
 }
 
-hipError_t launch_iter(const IterArgs& a, int k, bool mat, TileConfig t, int nchunks, size_t lds,
+hipError_t launch_iter(const IterArgs& a, int k, bool mat, TileConfig t, size_t lds,
                        hipStream_t s) {
     switch (k) {
-        case 1: return launch_iter_k1(a, mat, t, nchunks, lds, s);
-        case 3: return launch_iter_k3(a, mat, t, nchunks, lds, s);
-        case 5: return launch_iter_k5(a, mat, t, nchunks, lds, s);
-        case 7: return launch_iter_k7(a, mat, t, nchunks, lds, s);
-        case 9: return launch_iter_k9(a, mat, t, nchunks, lds, s);
-        case 11: return launch_iter_k11(a, mat, t, nchunks, lds, s);
-        case 13: return launch_iter_k13(a, mat, t, nchunks, lds, s);
-        case 15: return launch_iter_k15(a, mat, t, nchunks, lds, s);
+        case 1: return launch_iter_k1(a, mat, t, lds, s);
+        case 3: return launch_iter_k3(a, mat, t, lds, s);
+        case 5: return launch_iter_k5(a, mat, t, lds, s);
+        case 7: return launch_iter_k7(a, mat, t, lds, s);
+        case 9: return launch_iter_k9(a, mat, t, lds, s);
+        case 11: return launch_iter_k11(a, mat, t, lds, s);
+        case 13: return launch_iter_k13(a, mat, t, lds, s);
+        case 15: return launch_iter_k15(a, mat, t, lds, s);
         default: return hipErrorInvalidValue;
     }
 }
@@ -228,23 +228,17 @@ hipError_t launch_resident(const IterArgs& a, int k, TileConfig t, size_t lds, i
     }
 }
 
-// Tile of the iteration kernel: the first candidate whose LDS fits one
-// work-group (rows = 0 if none does).  Up to k = 7 the fused kernel runs 1024
-// threads on a 32 x 32 tile, two pixels per thread and two row groups (four
-// waves per SIMD hide the LDS and memory latency best); the materialised
-// variant and wider windows keep one row group, the latter with four pixels
-// per thread.
-TileConfig pick_tile(int k, int C, bool colour, bool compat, bool mat) {
-    const TileConfig narrow[] = {{32, 2, 32, 1}, {16, 2, 32, 1}, {8, 2, 32, 1}, {32, 2, 32, 2}};
-    const TileConfig wide[] = {{32, 4, 32, 1}, {16, 4, 32, 1}, {8, 4, 32, 1}};
+// Tile of iter_kernel: the first candidate whose LDS fits one work-group
+// (rows = 0 if none does).  32 columns; up to k = 7 two pixels per thread
+// (512 threads on 32 rows, two waves per SIMD), wider windows four pixels
+// per thread; fewer rows when the classes and the halo outgrow the LDS.
+TileConfig pick_tile(int k, int C, bool colour, bool compat) {
+    const TileConfig narrow[] = {{32, 2, 32}, {16, 2, 32}, {8, 2, 32}};
+    const TileConfig wide[] = {{32, 4, 32}, {16, 4, 32}, {8, 4, 32}};
     const TileConfig* cand = k <= 7 ? narrow : wide;
-    const int ncand = k <= 7 ? 4 : 3;
-    for (int i = 0; i < ncand; ++i) {
-        const TileConfig t = cand[i];
-        if (t.split > 1 && mat) continue;
-        if (iter_lds_bytes(k, C, t, colour, compat) <= kLdsLimit) return t;
-    }
-    return TileConfig{0, 4, 32, 1};
+    for (int i = 0; i < 3; ++i)
+        if (iter_lds_bytes(k, C, cand[i], colour, compat) <= kLdsLimit) return cand[i];
+    return TileConfig{0, 4, 32};
 }
 
 // Upload mu (C*C floats) if it differs from what the device holds.
@@ -448,7 +442,7 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     fill_taps(p, s, a.taps);
 
     if (s == 1) {
-        const TileConfig tile = pick_tile(k, C, !mat, mu_dev != nullptr, mat);
+        const TileConfig tile = pick_tile(k, C, !mat, mu_dev != nullptr);
         if (tile.rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
         const size_t lds = iter_lds_bytes(k, C, tile, !mat, mu_dev != nullptr);
         if (iters > 1) {
@@ -486,7 +480,7 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
         // work-group fits on the device at once (Potts, the two-pixel tile):
         // the tile stays in LDS and only border rings cross memory.
         if (p.variant == CONVCRF_VARIANT_RESIDENT && !mu_dev && iters >= 2 && ctx->coop &&
-            tile.pix == 2 && tile.split == 1 && tile.width == 32 && k <= 7 &&
+            tile.pix == 2 && tile.width == 32 && k <= 7 &&
             a.ntiles <= 4 * ctx->num_cus) {
             if ((st = ensure(ctx, ctx->q_ws2, qbytes)) != CONVCRF_OK) return st;
             if ((st = ensure(ctx, ctx->sync, (1 + (size_t)a.ntiles) * sizeof(unsigned int))) !=
@@ -536,7 +530,7 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
             st = launch(ctx, mat ? kMatIter : kFused, stream, mat ? "materialised_iter" : "fused_iter",
                         [&] {
                             return streamed ? launch_stream(as, k, lds_s, stream)
-                                            : launch_iter(a, k, mat, tile, 1, lds, stream);
+                                            : launch_iter(a, k, mat, tile, lds, stream);
                         });
             if (st != CONVCRF_OK) return st;
             cur = dst;

@@ -18,9 +18,8 @@ constexpr int kMaxC = 24;
 struct TileConfig {
     int rows;       // output rows per work-group
     int pix;        // pixels per thread: 2 or 4
-    int width = 32; // output columns per work-group: 32 or 16
-    int split = 1;  // row groups sharing the tile (each a band of window rows)
-    int threads() const { return (width / pix) * rows * split; }
+    int width = 32; // output columns per work-group
+    int threads() const { return (width / pix) * rows; }
 };
 
 // The Eq. 4 kernel split into its per-offset and its per-pixel parts.  Both
@@ -108,15 +107,12 @@ inline size_t pmsg_lds_bytes(int k) {
 
 // LDS bytes of one iteration work-group for a k x k window, C classes,
 // with or without the three colour planes and the C x C compatibility.
-// Floats of the LDS region shared by the staged planes (Q and, unless
-// materialised, the three colour planes) and, after the message, the row
-// groups' S - 1 partial messages per pixel: the larger of the two.  The
-// C x C compatibility matrix, when given, follows it.
+// Floats of the staged planes of one iteration work-group: Q and, unless
+// materialised, the three colour planes, tile plus halo.  The C x C
+// compatibility matrix, when given, follows them.
 inline size_t iter_lds_stage_floats(int k, int C, TileConfig t, bool with_colour) {
-    const size_t staged = (size_t)(C + (with_colour ? 3 : 0)) * (t.rows + (k - 1)) *
-                          iter_lds_stride(k, t.pix, t.width);
-    const size_t partials = (size_t)(t.split - 1) * C * t.rows * t.width;
-    return staged > partials ? staged : partials;
+    return (size_t)(C + (with_colour ? 3 : 0)) * (t.rows + (k - 1)) *
+           iter_lds_stride(k, t.pix, t.width);
 }
 
 // LDS bytes of one iteration work-group for a k x k window and C classes.
@@ -125,10 +121,9 @@ inline size_t iter_lds_bytes(int k, int C, TileConfig t, bool with_colour, bool 
                             (with_compat ? (size_t)C * C : 0));
 }
 
-// One launcher per window side k (each compiled in its own object); one
-// work-group per tile and class chunk: a.ntiles x nchunks work-groups, chunk
-// j computing classes [j*a.C, (j+1)*a.C) (message mode only; nchunks = 1
-// otherwise).  launch_resident runs all a.iters iterations in one
+// One launcher per window side k (each compiled in its own object);
+// launch_iter runs one update, one work-group per tile (a.ntiles of them).
+// launch_resident runs all a.iters iterations in one
 // cooperative launch; with probe = true it only reports whether it would
 // (hipSuccess) or not (hipErrorNotSupported / hipErrorCooperativeLaunchTooLarge).
 // launch_stream runs one update with the staging streamed under the
@@ -137,7 +132,7 @@ inline size_t iter_lds_bytes(int k, int C, TileConfig t, bool with_colour, bool 
 // outside that.
 #define CONVCRF_DECLARE_ITER(K)                                              \
     hipError_t launch_iter_k##K(const IterArgs& a, bool materialised,        \
-                                TileConfig tile, int nchunks, size_t lds,    \
+                                TileConfig tile, size_t lds,                 \
                                 hipStream_t stream);                         \
     hipError_t launch_stream_k##K(const IterArgs& a, size_t lds,             \
                                   hipStream_t stream);                       \

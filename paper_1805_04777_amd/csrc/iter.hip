@@ -158,17 +158,17 @@ __device__ __forceinline__ void neighbour_sync(unsigned int* flags, unsigned int
     __syncthreads();
 }
 
-// Threads = (TW / P) * rows * S: S groups of whole wavefronts share one
-// staged tile, group g taking window rows [g*K/S, (g+1)*K/S) of every pixel.
-// At the 146 KB tile of k = 7 that gives 1 (P = 4), 2 (P = 2) or 4 (P = 2,
-// S = 2) waves per SIMD; declaring it lets the scheduler size registers.
-// RES: resident launch running all a.iters iterations; the tile stays in LDS
-// and between iterations the work-groups only exchange the r-pixel border
-// rings of their tiles through a.ring[], synchronised with their neighbours.
-template <int K, int CM, bool EXACT, bool MAT, int P, int TW, int S, bool RES>
-__global__ __launch_bounds__((P == 4 ? 256 : 512) * S)
-__attribute__((amdgpu_waves_per_eu((P == 4 ? 1 : 2) * S, (P == 4 ? 1 : 2) * S)))
+// Threads = (32 / P) * rows: at the 146 KB tile of k = 7 that gives 1
+// (P = 4) or 2 (P = 2) waves per SIMD; declaring it lets the scheduler size
+// registers.  RES: resident launch running all a.iters iterations; the tile
+// stays in LDS and between iterations the work-groups only exchange the
+// r-pixel border rings of their tiles through a.ring[], synchronised with
+// their neighbours.
+template <int K, int CM, bool EXACT, bool MAT, int P, bool RES>
+__global__ __launch_bounds__(P == 4 ? 256 : 512)
+__attribute__((amdgpu_waves_per_eu(P == 4 ? 1 : 2, P == 4 ? 1 : 2)))
 void iter_kernel(const IterArgs a) {
+    constexpr int TW = 32;
     constexpr int R = (K - 1) / 2;
     constexpr int LW = TW + 2 * R;            // staged columns
     constexpr int LS = iter_lds_stride(K, P, TW);
@@ -176,23 +176,17 @@ void iter_kernel(const IterArgs a) {
     constexpr int KK = K * K;
     constexpr int CTR = R * K + R;            // centre tap index
     constexpr int TPR = TW / P;               // threads per tile row
-    constexpr int kStagePix = S == 1 ? 3 : 2;
-    constexpr int FP = P / S;                 // pixels each thread finalises
-    static_assert(P % S == 0, "each row group finalises P / S pixels");
-    static_assert(!RES || (!MAT && S == 1), "resident launches are fused, one row group");
+    constexpr int kStagePix = 3;
+    static_assert(!RES || !MAT, "resident launches are fused");
     using V = Vec<P>;
-    using VF = Vec<FP>;
 
     extern __shared__ float4 smem4[];
     float* const smem = reinterpret_cast<float*>(smem4);
 
-    // classes of this work-group: all of them, or one chunk (message mode;
-    // the last chunk may be short)
-    const int C = EXACT ? CM : min(a.C, a.planes - (int)blockIdx.y * a.C);
+    const int C = EXACT ? CM : a.C;
     const int H = a.H, W = a.W;
     const int nthreads = blockDim.x;
-    const int gthreads = nthreads / S;        // threads per row group
-    const int rows = gthreads / TPR;
+    const int rows = nthreads / TPR;
     const int LH = rows + 2 * R;
     const int plane = LH * LS;
 
@@ -220,8 +214,7 @@ void iter_kernel(const IterArgs a) {
     const int tyi = trem / a.tiles_x;
     const int y0 = tyi * rows;
     const int x0 = (trem - tyi * a.tiles_x) * TW;
-    // class chunk of this work-group (message mode): planes [c0, c0 + C)
-    const size_t cbase = (size_t)b * a.planes + (size_t)blockIdx.y * a.C;
+    const size_t cbase = (size_t)b * C;       // this image's first plane
 
     const size_t HW = (size_t)H * W;
     const float* __restrict__ src = a.src + cbase * HW;
@@ -229,10 +222,8 @@ void iter_kernel(const IterArgs a) {
 
     float* const Qs = smem;                   // [C][LH][LS]
     float* const Cs = smem + C * plane;       // [3][LH][LS]
-    // compatibility matrix [C][C] (only when given; read back as broadcasts),
-    // after the larger of the staged planes and the row groups' partials
-    const int stage_floats = max((C + (MAT ? 0 : 3)) * plane, (S - 1) * C * rows * TW);
-    float* const Ms = smem + stage_floats;
+    // compatibility matrix [C][C] (only when given; read back as broadcasts)
+    float* const Ms = smem + (C + (MAT ? 0 : 3)) * plane;
 
     // ---- stage Q_t (or softmax(U)) and colours, tile + halo, zero outside.
     // kStagePix halo pixels per thread and round; every plane of all of them
@@ -269,31 +260,28 @@ void iter_kernel(const IterArgs a) {
             for (int ch = 0; ch < 3; ++ch) Cs[ch * plane + l] = f[ch];
         }
     };
-    const int grp = tid / gthreads;           // row group (uniform per wave)
-    const int gtid = tid - grp * gthreads;
-    const int tx = gtid % TPR;
-    const int ty = gtid / TPR;
+    const int tx = tid % TPR;
+    const int ty = tid / TPR;
     const int col0 = tx * P;                  // first staged column read
-    const int dy_lo = grp * K / S, dy_hi = (grp + 1) * K / S;
     const int y = y0 + ty;
     const int xb = x0 + col0;
     const bool pix_ok = y < H;
     const bool fullv = a.vec && xb + P <= W;
     // (resident launches are built for Potts only)
-    const bool general_compat = !RES && a.mode == kModeUpdate && a.mu != nullptr;
+    const bool general_compat = !RES && a.mu != nullptr;
 
     // With Potts the update is softmax(U + M) (the compatibility transform
     // -(sum M - M) differs from +M by a per-pixel constant), so the message
     // accumulates straight onto the unary, which is loaded here and arrives
     // while the tile is being staged.
-    const bool unary_first = a.mode == kModeUpdate && !general_compat;
+    const bool unary_first = !general_compat;
     const float* const unary_px = a.unary + cbase * HW + (size_t)y * W + xb;
     float acc[P][CM];
 #pragma unroll
     for (int i = 0; i < P; ++i)
 #pragma unroll
         for (int c = 0; c < CM; ++c) acc[i][c] = 0.f;
-    if (unary_first && pix_ok && grp == 0) load_pixels(acc, a.unary + cbase * HW + (size_t)y * W + xb, xb, fullv);
+    if (unary_first && pix_ok) load_pixels(acc, unary_px, xb, fullv);
 
     if (general_compat)
         for (int i = tid; i < C * C; i += nthreads) Ms[i] = a.mu[i];
@@ -314,7 +302,7 @@ void iter_kernel(const IterArgs a) {
         for (int i = 0; i < P; ++i)
 #pragma unroll
             for (int c = 0; c < CM; ++c) acc[i][c] = 0.f;
-        if (unary_first && pix_ok && grp == 0) load_pixels(acc, unary_px, xb, fullv);
+        if (unary_first && pix_ok) load_pixels(acc, unary_px, xb, fullv);
     }
 
     float own[3][P];
@@ -409,13 +397,12 @@ void iter_kernel(const IterArgs a) {
     };
     if constexpr (kUnrollRows) {
 #pragma unroll
-        for (int dy = 0; dy < K; ++dy)
-            if (S == 1 || (dy >= dy_lo && dy < dy_hi)) window_row(dy);
+        for (int dy = 0; dy < K; ++dy) window_row(dy);
     } else {
 #pragma unroll 1
-        for (int dy = dy_lo; dy < dy_hi; ++dy) window_row(dy);
+        for (int dy = 0; dy < K; ++dy) window_row(dy);
     }
-    if (a.include_center && grp == 0) {
+    if (a.include_center) {
 #pragma unroll
         for (int c = 0; c < CM; ++c) {
             if (EXACT || c < C) {
@@ -426,110 +413,65 @@ void iter_kernel(const IterArgs a) {
         }
     }
 
-    // ---- combine the row groups: pixel i of a thread is finalised by group
-    // i / FP; the other groups leave their partial messages for it in LDS
-    // (the staging area, no longer read), summed in a fixed group order
-    float fin[FP][CM];
-    if constexpr (S == 1) {
-#pragma unroll
-        for (int i = 0; i < P; ++i)
-#pragma unroll
-            for (int c = 0; c < CM; ++c) fin[i][c] = acc[i][c];
-    } else {
-        const int npx = rows * TW;
-        float* const Rs = smem;               // [S - 1][C][npx]
-        __syncthreads();
-#pragma unroll
-        for (int i = 0; i < P; ++i) {
-            const int f = i / FP;
-            if (f != grp) {
-                const int slot = (grp - f - 1 + S) % S;
-                float* r = Rs + (size_t)slot * C * npx + ty * TW + col0 + i;
-#pragma unroll
-                for (int c = 0; c < CM; ++c)
-                    if (EXACT || c < C) r[c * npx] = acc[i][c];
-            }
-        }
-        __syncthreads();
-#pragma unroll
-        for (int g = 0; g < S; ++g) {
-            if (g != grp) continue;           // uniform: one branch taken
-#pragma unroll
-            for (int j = 0; j < FP; ++j) {
-                const int i = g * FP + j;
-                const float* r = Rs + ty * TW + col0 + i;
-#pragma unroll
-                for (int c = 0; c < CM; ++c) {
-                    float v = acc[i][c];
-                    if (EXACT || c < C) {
-                        // partials in the order of their groups after g
-#pragma unroll
-                        for (int sl = 0; sl < S - 1; ++sl) v += r[((size_t)sl * C + c) * npx];
-                    }
-                    fin[j][c] = v;
-                }
-            }
-        }
-    }
+    float (&fin)[P][CM] = acc;
+    const int xf = xb;
+    const bool fullf = fullv;
 
-    const int xf = xb + grp * FP;             // first finalised pixel
-    const bool fullf = a.vec && xf + FP <= W && (FP == P || (xf % FP) == 0);
-
-    if (a.mode == kModeUpdate) {
+    {
         // compatibility transform: fin <- U - mu * M (general mu only; with
         // Potts fin already holds U + M)
         if (general_compat) {
             // one row of mu at a time (a scheduling barrier per row keeps the
             // broadcast reads of mu from all being hoisted); the unary is
             // loaded first so that it arrives meanwhile
-            float u[FP][CM];
+            float u[P][CM];
             {
                 const float* ug = a.unary + cbase * HW + (size_t)y * W + xf;
 #pragma unroll
                 for (int c = 0; c < CM; ++c) {
                     if (!EXACT && c >= C) continue;
                     if (fullf && pix_ok) {
-                        float tmp[FP];
-                        VF::get(*reinterpret_cast<const typename VF::T*>(ug + c * HW), tmp);
+                        float tmp[P];
+                        V::get(*reinterpret_cast<const typename V::T*>(ug + c * HW), tmp);
 #pragma unroll
-                        for (int j = 0; j < FP; ++j) u[j][c] = tmp[j];
+                        for (int j = 0; j < P; ++j) u[j][c] = tmp[j];
                     } else {
 #pragma unroll
-                        for (int j = 0; j < FP; ++j)
+                        for (int j = 0; j < P; ++j)
                             u[j][c] = (pix_ok && xf + j < W) ? ug[c * HW + j] : 0.f;
                     }
                 }
             }
-            float z[FP][CM];
+            float z[P][CM];
 #pragma unroll
             for (int l = 0; l < CM; ++l) {
                 if (EXACT || l < C) {
-                    float t[FP];
+                    float t[P];
 #pragma unroll
-                    for (int j = 0; j < FP; ++j) t[j] = 0.f;
+                    for (int j = 0; j < P; ++j) t[j] = 0.f;
 #pragma unroll
                     for (int lp = 0; lp < CM; ++lp) {
                         if (EXACT || lp < C) {
                             const float m = Ms[l * C + lp];
 #pragma unroll
-                            for (int j = 0; j < FP; ++j) t[j] = fmaf(m, fin[j][lp], t[j]);
+                            for (int j = 0; j < P; ++j) t[j] = fmaf(m, fin[j][lp], t[j]);
                         }
                     }
 #pragma unroll
-                    for (int j = 0; j < FP; ++j) z[j][l] = u[j][l] - t[j];
+                    for (int j = 0; j < P; ++j) z[j][l] = u[j][l] - t[j];
                 } else {
 #pragma unroll
-                    for (int j = 0; j < FP; ++j) z[j][l] = 0.f;
+                    for (int j = 0; j < P; ++j) z[j][l] = 0.f;
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
 #pragma unroll
-            for (int j = 0; j < FP; ++j)
+            for (int j = 0; j < P; ++j)
 #pragma unroll
                 for (int c = 0; c < CM; ++c) fin[j][c] = z[j][c];
         }
 #pragma unroll
-        for (int j = 0; j < FP; ++j) softmax_regs<CM, EXACT>(fin[j], C);
+        for (int j = 0; j < P; ++j) softmax_regs<CM, EXACT>(fin[j], C);
     }
 
     if (!RES || it == a.iters - 1) {
@@ -539,13 +481,13 @@ void iter_kernel(const IterArgs a) {
             for (int c = 0; c < CM; ++c) {
                 if (!EXACT && c >= C) continue;
                 if (fullf) {
-                    float tmp[FP];
+                    float tmp[P];
 #pragma unroll
-                    for (int j = 0; j < FP; ++j) tmp[j] = fin[j][c];
-                    *reinterpret_cast<typename VF::T*>(dst + c * HW) = VF::make(tmp);
+                    for (int j = 0; j < P; ++j) tmp[j] = fin[j][c];
+                    *reinterpret_cast<typename V::T*>(dst + c * HW) = V::make(tmp);
                 } else {
 #pragma unroll
-                    for (int j = 0; j < FP; ++j)
+                    for (int j = 0; j < P; ++j)
                         if (xf + j < W) dst[c * HW + j] = fin[j][c];
                 }
             }
@@ -622,13 +564,12 @@ hipError_t allow_full_lds(Fn fn) {
     return e;
 }
 
-template <int K, int CM, bool EXACT, bool MAT, int P, int TW, int S>
-hipError_t launch_one(const IterArgs& a, TileConfig t, int nchunks, size_t lds,
-                      hipStream_t stream) {
-    auto fn = iter_kernel<K, CM, EXACT, MAT, P, TW, S, false>;
+template <int K, int CM, bool EXACT, bool MAT, int P>
+hipError_t launch_one(const IterArgs& a, TileConfig t, size_t lds, hipStream_t stream) {
+    auto fn = iter_kernel<K, CM, EXACT, MAT, P, false>;
     hipError_t e = allow_full_lds(fn);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(fn, dim3(a.ntiles, nchunks), dim3(t.threads()), lds, stream, a);
+    hipLaunchKernelGGL(fn, dim3(a.ntiles), dim3(t.threads()), lds, stream, a);
     return hipGetLastError();
 }
 
@@ -640,7 +581,7 @@ hipError_t launch_one(const IterArgs& a, TileConfig t, int nchunks, size_t lds,
 template <int K, int CM, bool EXACT>
 hipError_t launch_res(const IterArgs& a, TileConfig t, size_t lds, int num_cus,
                       hipStream_t stream, bool probe) {
-    auto fn = iter_kernel<K, CM, EXACT, false, 2, 32, 1, true>;
+    auto fn = iter_kernel<K, CM, EXACT, false, 2, true>;
     hipError_t e = allow_full_lds(fn);
     if (e != hipSuccess) return e;
     int per_cu = 0;
@@ -1184,21 +1125,14 @@ hipError_t launch_pmsg_cm(const IterArgs& a, int nchunks, size_t lds, hipStream_
     return hipGetLastError();
 }
 
-// The built tile shapes: {P = 2 or 4, width 32, S = 1} and {P = 2, width 32,
-// S = 2} (fused only).
+// The built tile shapes: P = 2 or 4 pixels per thread, width 32.
 template <int K, int CM, bool EXACT>
-hipError_t launch_cm(const IterArgs& a, bool mat, TileConfig t, int nchunks, size_t lds,
-                     hipStream_t stream) {
-    if (t.split == 2) {
-        if (mat || t.pix != 2) return hipErrorInvalidValue;
-        return launch_one<K, CM, EXACT, false, 2, 32, 2>(a, t, nchunks, lds, stream);
-    }
-    if (t.split != 1) return hipErrorInvalidValue;
+hipError_t launch_cm(const IterArgs& a, bool mat, TileConfig t, size_t lds, hipStream_t stream) {
     if (t.pix == 2)
-        return mat ? launch_one<K, CM, EXACT, true, 2, 32, 1>(a, t, nchunks, lds, stream)
-                   : launch_one<K, CM, EXACT, false, 2, 32, 1>(a, t, nchunks, lds, stream);
-    return mat ? launch_one<K, CM, EXACT, true, 4, 32, 1>(a, t, nchunks, lds, stream)
-               : launch_one<K, CM, EXACT, false, 4, 32, 1>(a, t, nchunks, lds, stream);
+        return mat ? launch_one<K, CM, EXACT, true, 2>(a, t, lds, stream)
+                   : launch_one<K, CM, EXACT, false, 2>(a, t, lds, stream);
+    return mat ? launch_one<K, CM, EXACT, true, 4>(a, t, lds, stream)
+               : launch_one<K, CM, EXACT, false, 4>(a, t, lds, stream);
 }
 
 }  // namespace
@@ -1207,25 +1141,22 @@ hipError_t launch_cm(const IterArgs& a, bool mat, TileConfig t, int nchunks, siz
 #define CRF_CAT(a, b) CRF_CAT2(a, b)
 
 hipError_t CRF_CAT(launch_iter_k, CRF_K)(const IterArgs& a, bool materialised, TileConfig tile,
-                                         int nchunks, size_t lds, hipStream_t stream) {
+                                         size_t lds, hipStream_t stream) {
     constexpr int K = CRF_K;
     if (tile.pix != 2 && tile.pix != 4) return hipErrorInvalidValue;
     if (tile.width != 32) return hipErrorInvalidValue;
-    if ((tile.width / tile.pix) * tile.rows % 64 != 0) return hipErrorInvalidValue;  // whole-wave groups
-    const int max_threads = tile.width == 16 ? 256 : (tile.pix == 4 ? 256 : 512) * tile.split;
-    if (tile.threads() > max_threads) return hipErrorInvalidValue;
-    if (nchunks < 1 || (nchunks > 1 && a.mode != kModeMessage) || nchunks * a.C < a.planes ||
-        (nchunks - 1) * a.C >= a.planes)
-        return hipErrorInvalidValue;
+    if ((tile.width / tile.pix) * tile.rows % 64 != 0) return hipErrorInvalidValue;  // whole waves
+    if (tile.threads() > (tile.pix == 4 ? 256 : 512)) return hipErrorInvalidValue;
+    if (a.mode != kModeUpdate || a.planes != a.C) return hipErrorInvalidValue;
     switch (a.C) {
-        case 19: return launch_cm<K, 19, true>(a, materialised, tile, nchunks, lds, stream);
-        case 21: return launch_cm<K, 21, true>(a, materialised, tile, nchunks, lds, stream);
+        case 19: return launch_cm<K, 19, true>(a, materialised, tile, lds, stream);
+        case 21: return launch_cm<K, 21, true>(a, materialised, tile, lds, stream);
         default: break;
     }
-    if (a.C <= 4) return launch_cm<K, 4, false>(a, materialised, tile, nchunks, lds, stream);
-    if (a.C <= 8) return launch_cm<K, 8, false>(a, materialised, tile, nchunks, lds, stream);
-    if (a.C <= 16) return launch_cm<K, 16, false>(a, materialised, tile, nchunks, lds, stream);
-    return launch_cm<K, 24, false>(a, materialised, tile, nchunks, lds, stream);
+    if (a.C <= 4) return launch_cm<K, 4, false>(a, materialised, tile, lds, stream);
+    if (a.C <= 8) return launch_cm<K, 8, false>(a, materialised, tile, lds, stream);
+    if (a.C <= 16) return launch_cm<K, 16, false>(a, materialised, tile, lds, stream);
+    return launch_cm<K, 24, false>(a, materialised, tile, lds, stream);
 }
 
 // Pooled message of the blur path, any k, chunks of at most kPmsgClasses.
@@ -1263,7 +1194,7 @@ hipError_t CRF_CAT(launch_resident_k, CRF_K)(const IterArgs& a, TileConfig tile,
     if constexpr (K > 7) {
         return hipErrorNotSupported;
     } else {
-        if (tile.pix != 2 || tile.width != 32 || tile.split != 1 || tile.threads() > 512 ||
+        if (tile.pix != 2 || tile.width != 32 || tile.threads() > 512 ||
             a.mode != kModeUpdate || a.iters < 2 || a.planes != a.C || a.mu != nullptr)
             return hipErrorNotSupported;
         switch (a.C) {
