@@ -208,6 +208,16 @@ hipError_t launch_pmsg(const IterArgs& a, int k, int nchunks, size_t lds, hipStr
     }
 }
 
+hipError_t launch_rstream(const IterArgs& a, int k, size_t lds, int num_cus, hipStream_t s,
+                          bool probe) {
+    switch (k) {
+        case 3: return launch_rstream_k3(a, lds, num_cus, s, probe);
+        case 5: return launch_rstream_k5(a, lds, num_cus, s, probe);
+        case 7: return launch_rstream_k7(a, lds, num_cus, s, probe);
+        default: return hipErrorNotSupported;
+    }
+}
+
 hipError_t launch_stream(const IterArgs& a, int k, size_t lds, hipStream_t s) {
     switch (k) {
         case 3: return launch_stream_k3(a, lds, s);
@@ -476,12 +486,50 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
                              (reinterpret_cast<uintptr_t>(q_out) % va == 0) &&
                              (!ctx->q_ws.p || reinterpret_cast<uintptr_t>(ctx->q_ws.p) % va == 0);
         a.vec = (W % tile.pix == 0) && aligned;
+        // The iterations stream their staging under the computation where
+        // that kernel is built (k = 3..7, C = 19 or 21, whole float2 rows,
+        // unary rows in 16-byte pieces, buffers under 2 GB).
+        const size_t lds_s = stream_lds_bytes(k, C, mu_dev != nullptr);
+        const bool streamed = !mat && k >= 3 && k <= 7 && (C == 19 || C == 21) && a.vec &&
+                              W % 4 == 0 && reinterpret_cast<uintptr_t>(unary) % 16 == 0 &&
+                              lds_s <= kLdsLimit && (size_t)C * H * W * 4 < (1ull << 31);
+        IterArgs as = a;                      // the streamed launches' tiling
+        as.tiles_x = (W + kStreamTW - 1) / kStreamTW;
+        as.tiles_per_img = as.tiles_x * ((H + kStreamRows - 1) / kStreamRows);
+        as.ntiles = as.tiles_per_img * B;
         // Resident variant: all iterations in one launch when every tile's
-        // work-group fits on the device at once (Potts, the two-pixel tile):
-        // the tile stays in LDS and only border rings cross memory.
+        // work-group fits on the device at once (Potts): the tile stays in
+        // LDS and only border rings cross memory.  On the streamed tiles the
+        // weights and the unary also stay in registers for the whole call.
         if (p.variant == CONVCRF_VARIANT_RESIDENT && !mu_dev && iters >= 2 && ctx->coop &&
-            tile.pix == 2 && tile.width == 32 && k <= 7 &&
-            a.ntiles <= 4 * ctx->num_cus) {
+            streamed && as.ntiles <= 4 * ctx->num_cus) {
+            if ((st = ensure(ctx, ctx->q_ws2, qbytes)) != CONVCRF_OK) return st;
+            if ((st = ensure(ctx, ctx->sync, (1 + (size_t)as.ntiles) * sizeof(unsigned int))) !=
+                CONVCRF_OK)
+                return st;
+            IterArgs r = as;
+            r.src = unary;
+            r.dst = q_out;
+            r.first = 1;
+            r.iters = iters;
+            r.ring[0] = static_cast<float*>(ctx->q_ws.p);
+            r.ring[1] = static_cast<float*>(ctx->q_ws2.p);
+            r.sync = static_cast<unsigned int*>(ctx->sync.p);
+            const hipError_t fits = launch_rstream(r, k, lds_s, ctx->num_cus, stream, true);
+            if (fits == hipSuccess) {
+                st = launch(ctx, kSyncReset, stream, "sync_reset",
+                            [&] { return launch_zero_u32(r.sync, 1 + as.ntiles, stream); });
+                if (st != CONVCRF_OK) return st;
+                return launch(ctx, kResident, stream, "fused_resident", [&] {
+                    return launch_rstream(r, k, lds_s, ctx->num_cus, stream, false);
+                });
+            }
+            (void)hipGetLastError();  // refused: one launch per iteration below
+            ctx->err = std::string("resident launch refused (") + hipGetErrorString(fits) +
+                       "); ran one launch per iteration";
+        } else if (p.variant == CONVCRF_VARIANT_RESIDENT && !mu_dev && iters >= 2 && ctx->coop &&
+                   tile.pix == 2 && tile.width == 32 && k <= 7 &&
+                   a.ntiles <= 4 * ctx->num_cus) {
             if ((st = ensure(ctx, ctx->q_ws2, qbytes)) != CONVCRF_OK) return st;
             if ((st = ensure(ctx, ctx->sync, (1 + (size_t)a.ntiles) * sizeof(unsigned int))) !=
                 CONVCRF_OK)
@@ -508,17 +556,6 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
                        "); ran one launch per iteration";
         }
         float* ws = static_cast<float*>(ctx->q_ws.p);
-        // The iterations stream their staging under the computation where
-        // that kernel is built (k = 3..7, C = 19 or 21, whole float2 rows,
-        // unary rows in 16-byte pieces, buffers under 2 GB).
-        const size_t lds_s = stream_lds_bytes(k, C, mu_dev != nullptr);
-        const bool streamed = !mat && k >= 3 && k <= 7 && (C == 19 || C == 21) && a.vec &&
-                              W % 4 == 0 && reinterpret_cast<uintptr_t>(unary) % 16 == 0 &&
-                              lds_s <= kLdsLimit && (size_t)C * H * W * 4 < (1ull << 31);
-        IterArgs as = a;                      // the streamed launches' tiling
-        as.tiles_x = (W + kStreamTW - 1) / kStreamTW;
-        as.tiles_per_img = as.tiles_x * ((H + kStreamRows - 1) / kStreamRows);
-        as.ntiles = as.tiles_per_img * B;
         // the last iteration writes q_out; earlier ones alternate so that
         // source and destination always differ
         const float* cur = unary;

@@ -126,6 +126,8 @@ inline size_t iter_lds_bytes(int k, int C, TileConfig t, bool with_colour, bool 
 // launch_resident runs all a.iters iterations in one
 // cooperative launch; with probe = true it only reports whether it would
 // (hipSuccess) or not (hipErrorNotSupported / hipErrorCooperativeLaunchTooLarge).
+// launch_rstream runs all a.iters iterations in one cooperative launch on
+// the tiles of launch_stream (the resident variant; probe as above).
 // launch_stream runs one update with the staging streamed under the
 // computation (k = 3, 5, 7, C = 19 or 21, vector path; the first iteration
 // applies softmax(U) in LDS); hipErrorNotSupported when the arguments are
@@ -138,6 +140,9 @@ inline size_t iter_lds_bytes(int k, int C, TileConfig t, bool with_colour, bool 
                                   hipStream_t stream);                       \
     hipError_t launch_pmsg_k##K(const IterArgs& a, int nchunks, size_t lds,  \
                                 hipStream_t stream);                         \
+    hipError_t launch_rstream_k##K(const IterArgs& a, size_t lds,            \
+                                   int num_cus, hipStream_t stream,          \
+                                   bool probe);                              \
     hipError_t launch_resident_k##K(const IterArgs& a, TileConfig tile,      \
                                     size_t lds, int num_cus,                 \
                                     hipStream_t stream, bool probe);

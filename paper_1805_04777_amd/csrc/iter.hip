@@ -158,6 +158,40 @@ __device__ __forceinline__ void neighbour_sync(unsigned int* flags, unsigned int
     __syncthreads();
 }
 
+// The same wait for data that every work-group writes and reads with
+// agent-scope atomic accesses (coherent across the XCDs' L2 caches, written
+// through): each wave waits until its stores are performed, the work-group
+// barrier orders thread 0's flag store after all of them, and the readers'
+// own atomic loads need no cache invalidation -- no L2 write-back or
+// invalidate of the XCD, which the release/acquire fences of neighbour_sync
+// cost.  Bounded like neighbour_sync.
+__device__ __forceinline__ void neighbour_sync_coherent(unsigned int* flags, unsigned int* flag_err,
+                                                        int tile, int tiles_x, int tiles_y,
+                                                        unsigned int value) {
+    __builtin_amdgcn_s_waitcnt(kWaitVmem);
+    __syncthreads();
+    if (threadIdx.x == 0)
+        __hip_atomic_store(flags + tile, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x < 9) {
+        const int per_img = tiles_x * tiles_y;
+        const int ti = tile % per_img;
+        const int ty = ti / tiles_x + (int)threadIdx.x / 3 - 1;
+        const int tx = ti % tiles_x + (int)threadIdx.x % 3 - 1;
+        if (threadIdx.x != 4 && ty >= 0 && ty < tiles_y && tx >= 0 && tx < tiles_x) {
+            const unsigned int* f = flags + (tile - ti) + ty * tiles_x + tx;
+            unsigned int polls = 0;
+            while (__hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < value) {
+                __builtin_amdgcn_s_sleep(1);
+                if (++polls == kSpinLimit) {
+                    __hip_atomic_store(flag_err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+            }
+        }
+    }
+    __syncthreads();
+}
+
 // Threads = (32 / P) * rows: at the 146 KB tile of k = 7 that gives 1
 // (P = 4) or 2 (P = 2) waves per SIMD; declaring it lets the scheduler size
 // registers.  RES: resident launch running all a.iters iterations; the tile
@@ -680,6 +714,47 @@ struct StreamShape {
     static constexpr int NJ = (NI + 7) / 8;      // per wave and plane
 };
 
+// One chunk of the message, classes [C_LO, C_HI): for every (class, window
+// row) step, the row of P + K - 1 staged values is read from LDS two steps
+// ahead of the one being applied (a rolling pipeline, one scheduling region
+// per step), and applied to both pixels with the weights held in registers.
+// Qs points at plane 0 of the staged Q; the tile row of the thread is ty and
+// its first staged column col0.
+template <int K, int P, int LS, int PLANE, int CM, int C_LO, int C_HI>
+__device__ __forceinline__ void message_chunk(const float* Qs, int ty, int col0,
+                                              const float (&w)[K][P][K], float (&acc)[P][CM]) {
+    constexpr int R = (K - 1) / 2, CTR = R * K + R, NW = P + K - 1;
+    constexpr int kDepth = 3;
+    constexpr int NC = C_HI - C_LO;
+    constexpr int nsteps = NC * K;
+    float qr[kDepth][NW];
+    // per class one base offset the compiler cannot merge with the row
+    // offsets, so that those fold into the LDS reads' immediates
+    const float* qb[NC];
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+        unsigned off = (unsigned)((C_LO + i) * PLANE + ty * LS + col0);
+        asm volatile("" : "+v"(off));
+        qb[i] = Qs + off;
+    }
+#pragma unroll
+    for (int t = 0; t < kDepth - 1; ++t)
+        if (t < nsteps) lds_row<NW, P>(qb[t / K] + (t % K) * LS, qr[t]);
+#pragma unroll
+    for (int t = 0; t < nsteps; ++t) {
+        const int nx = t + kDepth - 1;
+        if (nx < nsteps) lds_row<NW, P>(qb[nx / K] + (nx % K) * LS, qr[nx % kDepth]);
+        const int c = C_LO + t / K, dy = t % K;
+#pragma unroll
+        for (int i = 0; i < P; ++i)
+#pragma unroll
+            for (int dx = 0; dx < K; ++dx)
+                if (dy * K + dx != CTR)
+                    acc[i][c] = fmaf(w[dy][i][dx], qr[t % kDepth][i + dx], acc[i][c]);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
 // FIRST: the first iteration, whose source is U itself: all planes are
 // loaded at once, each thread keeps the unary of its own pixels in
 // registers, and the staged halo tile is turned into softmax(U) in place
@@ -871,40 +946,7 @@ void stream_kernel(const IterArgs a) {
                           lds_addr(j < CM * 4 ? Us + j * 256 : dummy));
             }
         }
-        // (class, window row) steps of this chunk, LDS rows read two steps
-        // ahead of the one being applied
-        constexpr int kDepth = 3;
-        constexpr int nsteps = (c_hi - c_lo) * K;
-        float qr[kDepth][NW];
-        // per class one base offset the compiler cannot merge with the row
-        // offsets, so that those fold into the LDS reads' immediates
-        const float* qb[CH];
-#pragma unroll
-        for (int i = 0; i < CH; ++i) {
-            unsigned off = (unsigned)((c_lo + i) * PLANE + ty * LS + col0);
-            asm volatile("" : "+v"(off));
-            qb[i] = Qs + off;
-        }
-#pragma unroll
-        for (int t = 0; t < kDepth - 1; ++t)
-            if (t < nsteps)
-                lds_row<NW, P>(qb[t / K] + (t % K) * LS, qr[t]);
-#pragma unroll
-        for (int t = 0; t < CH * K; ++t) {
-            if (t < nsteps) {
-                const int nx = t + kDepth - 1;
-                if (nx < nsteps)
-                    lds_row<NW, P>(qb[nx / K] + (nx % K) * LS, qr[nx % kDepth]);
-                const int c = c_lo + t / K, dy = t % K;
-#pragma unroll
-                for (int i = 0; i < P; ++i)
-#pragma unroll
-                    for (int dx = 0; dx < K; ++dx)
-                        if (dy * K + dx != CTR)
-                            acc[i][c] = fmaf(w[dy][i][dx], qr[t % kDepth][i + dx], acc[i][c]);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
+        message_chunk<K, P, LS, PLANE, CM, c_lo, c_hi>(Qs, ty, col0, w, acc);
         if (a.include_center) {
 #pragma unroll
             for (int c = c_lo; c < c_hi; ++c)
@@ -974,6 +1016,237 @@ hipError_t launch_stream(const IterArgs& a, size_t lds, hipStream_t stream) {
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(a.ntiles), dim3(512), lds, stream, a);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------- resident streamed form
+// All T iterations in one cooperative launch on the tiles of stream_kernel
+// (every tile's work-group co-resident).  The window weights (the colours do
+// not change) and the unary of each thread's pixels stay in registers for
+// the whole call; Q_t of the tile stays in LDS.  Between iterations a tile
+// writes only its r-pixel border ring to an exchange buffer (agent-scope
+// atomic stores), synchronises with its up to eight neighbours
+// (neighbour_sync_coherent) and reads the r-pixel frame around it back from
+// theirs (agent-scope atomic loads).  Potts compatibility only.
+template <int K, int CM, int CH>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void rstream_kernel(const IterArgs a) {
+    using SS = StreamShape<K>;
+    constexpr int R = SS::R, LW = SS::LW, LH = SS::LH, LS = SS::LS;
+    constexpr int PLANE = SS::PLANE, NI = SS::NI, NJ = SS::NJ;
+    constexpr int P = 2, TW = SS::TW, ROWS = SS::ROWS, TPR = TW / P;
+    constexpr int NW = P + K - 1, CTR = R * K + R;
+    constexpr int NCH = (CM + CH - 1) / CH;
+    constexpr unsigned kOob = 0x80000000u;
+    static_assert(ROWS >= 2 * R && TW >= 2 * R, "border rings of a tile do not overlap");
+
+    extern __shared__ float4 smem4[];
+    float* const smem = reinterpret_cast<float*>(smem4);
+    float* const Qs = smem;                      // [CM][PLANE]
+    float* const Cs = smem + CM * PLANE;         // [3][PLANE]
+    float* const dummy = Cs + 3 * PLANE;         // one 256-float row
+    const unsigned lds0 = (unsigned)(size_t)(__attribute__((address_space(3))) float*)smem;
+    auto lds_addr = [&](const float* q) { return lds0 + (unsigned)((q - smem) * 4); };
+
+    const int H = a.H, W = a.W;
+    const int tile = xcd_tile(blockIdx.x, a.ntiles);
+    const int b = tile / a.tiles_per_img;
+    const int trem = tile - b * a.tiles_per_img;
+    const int tyi = trem / a.tiles_x;
+    const int y0 = tyi * ROWS;
+    const int x0 = (trem - tyi * a.tiles_x) * TW;
+    const size_t HW = (size_t)H * W;
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+
+    // ---- stage the colours and U (the source of the first iteration)
+    unsigned voff[NJ];
+    int dst[NJ];
+#pragma unroll
+    for (int s = 0; s < NJ; ++s) {
+        const int j = wave + 8 * s;
+        const int f = j * 64 + lane;
+        const int r = f / LS, col = f - (f / LS) * LS;
+        const int gy = y0 - R + r, gx = x0 - R + col;
+        const bool in = j < NI && f < LH * LS && col < LW && gy >= 0 && gy < H && gx >= 0 && gx < W;
+        voff[s] = in ? (unsigned)((gy * W + gx) * 4) : kOob;
+        dst[s] = j < NI ? j * 64 : -1;
+    }
+    const rsrc_t rf = buffer_rsrc(a.feat + (size_t)b * 3 * HW, (unsigned)(3 * HW * 4));
+    const rsrc_t rq = buffer_rsrc(a.src + (size_t)b * CM * HW, (unsigned)(CM * HW * 4));
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch)
+#pragma unroll
+        for (int s = 0; s < NJ; ++s)
+            lds_dma(rf, voff[s], (int)(ch * HW * 4),
+                    lds_addr(dst[s] >= 0 ? Cs + ch * PLANE + dst[s] : dummy));
+    for (int c = 0; c < CM; ++c)
+#pragma unroll
+        for (int s = 0; s < NJ; ++s)
+            lds_dma(rq, voff[s], (int)(c * HW * 4),
+                    lds_addr(dst[s] >= 0 ? Qs + c * PLANE + dst[s] : dummy));
+
+    const int tx = tid % TPR, ty = tid / TPR;
+    const int col0 = tx * P;
+    const int y = y0 + ty, xb = x0 + col0;
+    const bool pix_ok = y < H && xb < W;        // W even: both pixels or neither
+
+    // ---- the window weights, once for all iterations
+    __builtin_amdgcn_s_waitcnt(vm_wait(NJ * CM));   // (clamped: see stream_kernel)
+    __syncthreads();
+    float w[K][P][K];
+    {
+        float own[3][P];
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch)
+#pragma unroll
+            for (int i = 0; i < P; ++i) own[ch][i] = Cs[ch * PLANE + (ty + R) * LS + col0 + R + i];
+#pragma unroll
+        for (int dy = 0; dy < K; ++dy) {
+            float nc[3][NW];
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) lds_row<NW, P>(Cs + ch * PLANE + (ty + dy) * LS + col0, nc[ch]);
+#pragma unroll
+            for (int i = 0; i < P; ++i) {
+#pragma unroll
+                for (int dx = 0; dx < K; ++dx) {
+                    if (dy * K + dx == CTR) { w[dy][i][dx] = 0.f; continue; }
+                    const int n = (dx - R) * (dx - R) + (dy - R) * (dy - R);
+                    const float d0 = own[0][i] - nc[0][i + dx];
+                    const float d1 = own[1][i] - nc[1][i + dx];
+                    const float d2 = own[2][i] - nc[2][i + dx];
+                    const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
+                    w[dy][i][dx] = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, a.taps.app_log2[n])) +
+                                   a.taps.smooth[n];
+                }
+            }
+        }
+    }
+    // ---- the unary of this thread's pixels, then softmax(U) in place
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));
+    __syncthreads();
+    float u[P][CM];
+#pragma unroll
+    for (int c = 0; c < CM; ++c)
+#pragma unroll
+        for (int i = 0; i < P; ++i) u[i][c] = Qs[c * PLANE + (ty + R) * LS + col0 + R + i];
+    __syncthreads();
+    for (int pos = tid; pos < LH * LS; pos += 512) {
+        const int r = pos / LS, col = pos - (pos / LS) * LS;
+        const int gy = y0 - R + r, gx = x0 - R + col;
+        if (col >= LW || gy < 0 || gy >= H || gx < 0 || gx >= W) continue;
+        float z[CM];
+#pragma unroll
+        for (int c = 0; c < CM; ++c) z[c] = Qs[c * PLANE + pos];
+        softmax_regs<CM, true>(z, CM);
+#pragma unroll
+        for (int c = 0; c < CM; ++c) Qs[c * PLANE + pos] = z[c];
+    }
+    __syncthreads();
+
+    for (int it = 0;; ++it) {
+        float acc[P][CM];
+#pragma unroll
+        for (int i = 0; i < P; ++i)
+#pragma unroll
+            for (int c = 0; c < CM; ++c) acc[i][c] = 0.f;
+        static_for([&](auto kc) {
+            constexpr int k = decltype(kc)::value;
+            constexpr int c_lo = k * CH;
+            constexpr int c_hi = (k + 1) * CH < CM ? (k + 1) * CH : CM;
+            message_chunk<K, P, LS, PLANE, CM, c_lo, c_hi>(Qs, ty, col0, w, acc);
+        }, std::make_integer_sequence<int, NCH>{});
+        if (a.include_center) {
+#pragma unroll
+            for (int c = 0; c < CM; ++c)
+#pragma unroll
+                for (int i = 0; i < P; ++i)
+                    acc[i][c] = fmaf(a.center_w, Qs[c * PLANE + (ty + R) * LS + col0 + R + i], acc[i][c]);
+        }
+        // Potts: Q_{t+1} = softmax(U + M)
+#pragma unroll
+        for (int i = 0; i < P; ++i) {
+#pragma unroll
+            for (int c = 0; c < CM; ++c) acc[i][c] += u[i][c];
+            softmax_regs<CM, true>(acc[i], CM);
+        }
+        if (it == a.iters - 1) {
+            if (pix_ok) {
+                float* __restrict__ qd = a.dst + (size_t)b * CM * HW + (size_t)y * W + xb;
+#pragma unroll
+                for (int c = 0; c < CM; ++c)
+                    *reinterpret_cast<float2*>(qd + c * HW) = make_float2(acc[0][c], acc[1][c]);
+            }
+            break;
+        }
+        // Q_{t+1}: the interior back into LDS, the border ring to the
+        // exchange buffer of this parity
+        __syncthreads();                          // every read of Q_t is done
+        float* __restrict__ ring = a.ring[(it + 1) & 1] + (size_t)b * CM * HW;
+        if (pix_ok) {
+            const bool border = ty < R || ty >= ROWS - R || col0 < R || col0 + 1 >= TW - R;
+#pragma unroll
+            for (int c = 0; c < CM; ++c) {
+                // (an odd offset when r is odd: two single stores)
+                float* q = Qs + c * PLANE + (ty + R) * LS + col0 + R;
+                q[0] = acc[0][c];
+                q[1] = acc[1][c];
+                if (border) {
+                    float* g = ring + c * HW + (size_t)y * W + xb;
+                    __hip_atomic_store(g, acc[0][c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(g + 1, acc[1][c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+        }
+        neighbour_sync_coherent(a.sync + 1, a.sync, tile, a.tiles_x, a.tiles_per_img / a.tiles_x,
+                                (unsigned int)(it + 1));
+        // the frame around the tile from the neighbours' rings (outside the
+        // image stays zero)
+        const float* __restrict__ nb = a.ring[(it + 1) & 1] + (size_t)b * CM * HW;
+        constexpr int band = R * LW, side = R * (LH - 2 * R);
+        for (int idx = tid; idx < 2 * band + 2 * side; idx += 512) {
+            int r, cc;
+            if (idx < 2 * band) {
+                const int k2 = idx - (idx >= band ? band : 0);
+                r = (idx >= band ? LH - R : 0) + k2 / LW;
+                cc = k2 - (k2 / LW) * LW;
+            } else {
+                const int j = idx - 2 * band;
+                const int k2 = j - (j >= side ? side : 0);
+                r = R + k2 / R;
+                cc = (j >= side ? LW - R : 0) + (k2 - (k2 / R) * R);
+            }
+            const int gy = y0 - R + r, gx = x0 - R + cc;
+            if (gy < 0 || gy >= H || gx < 0 || gx >= W) continue;
+            const float* g = nb + (size_t)gy * W + gx;
+            float v[CM];
+#pragma unroll
+            for (int c = 0; c < CM; ++c)
+                v[c] = __hip_atomic_load(g + c * HW, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+            for (int c = 0; c < CM; ++c) Qs[c * PLANE + r * LS + cc] = v[c];
+        }
+        __syncthreads();
+    }
+}
+
+// Cooperative: the runtime refuses the launch (rather than a neighbour wait
+// never ending) unless every work-group is co-resident; the occupancy query
+// refuses it first when the tiles cannot all be resident at once.
+template <int K, int CM, int CH>
+hipError_t launch_rstream(const IterArgs& a, size_t lds, int num_cus, hipStream_t stream,
+                          bool probe) {
+    auto fn = rstream_kernel<K, CM, CH>;
+    hipError_t e = allow_full_lds(fn);
+    if (e != hipSuccess) return e;
+    int per_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fn), 512, lds);
+    if (e != hipSuccess) return e;
+    if ((long long)per_cu * num_cus < a.ntiles) return hipErrorCooperativeLaunchTooLarge;
+    if (probe) return hipSuccess;
+    IterArgs args = a;
+    void* params[] = {&args};
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void*>(fn), dim3(a.ntiles), dim3(512),
+                                      params, (unsigned int)lds, stream);
 }
 
 // ------------------------------------------------------------ pooled message
@@ -1157,6 +1430,25 @@ hipError_t CRF_CAT(launch_iter_k, CRF_K)(const IterArgs& a, bool materialised, T
     if (a.C <= 8) return launch_cm<K, 8, false>(a, materialised, tile, lds, stream);
     if (a.C <= 16) return launch_cm<K, 16, false>(a, materialised, tile, lds, stream);
     return launch_cm<K, 24, false>(a, materialised, tile, lds, stream);
+}
+
+// Resident streamed form: k = 3, 5, 7, C = 19 or 21, Potts, vector path.
+hipError_t CRF_CAT(launch_rstream_k, CRF_K)(const IterArgs& a, size_t lds, int num_cus,
+                                            hipStream_t stream, bool probe) {
+    constexpr int K = CRF_K;
+    if constexpr (K < 3 || K > 7) {
+        return hipErrorNotSupported;
+    } else {
+        if (a.mode != kModeUpdate || a.planes != a.C || !a.vec || (a.W & 3) || a.mu != nullptr ||
+            a.iters < 2 || reinterpret_cast<uintptr_t>(a.src) % 16 != 0 ||
+            (size_t)a.C * a.H * a.W * 4 >= (1ull << 31))
+            return hipErrorNotSupported;
+        switch (a.C) {
+            case 19: return launch_rstream<K, 19, 4>(a, lds, num_cus, stream, probe);
+            case 21: return launch_rstream<K, 21, 3>(a, lds, num_cus, stream, probe);
+            default: return hipErrorNotSupported;
+        }
+    }
 }
 
 // Pooled message of the blur path, any k, chunks of at most kPmsgClasses.
