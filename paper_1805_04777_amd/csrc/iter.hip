@@ -14,15 +14,15 @@
 //      and applies them to all P pixels (the locally-connected,
 //      channel-constant filter of Eq. 6), one FMA per (pixel, tap, class).
 // The epilogue applies the compatibility transform, adds the unary and
-// normalises with a softmax (Alg. 1), writing Q_{t+1}; in message mode it
-// writes the raw message.
+// normalises with a softmax (Alg. 1), writing Q_{t+1}.
 //
 // The materialised variant reads the weights from a precomputed kernel
 // matrix instead of step 1 (the two-stage structure of Sec. 4.1).
 //
-// Also here: stream_kernel, the same update for the iterations after the
-// first with the staging streamed under the computation, and pmsg_kernel,
-// the message of the blur path on the pooled grid (Sec. 4.2).
+// Also here: stream_kernel, the same update with the staging streamed under
+// the computation; rstream_kernel, its resident form (all iterations in one
+// launch); and pmsg_kernel, the message of the blur path on the pooled grid
+// (Sec. 4.2).
 
 #include "crf_internal.h"
 
