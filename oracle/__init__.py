@@ -9,7 +9,10 @@ Contents
 --------
 - ``oracle.c`` (built to ``liboracle.so`` with gcc -O2 -fopenmp, no fast-math):
   the windowed mean-field of Alg. 1 with the Eq. 4 kernel and the Eq. 6
-  message, plus the pooled ("blur", Sec. 4.2) variant.  Wrapped here.
+  message, plus the pooled ("blur", Sec. 4.2) variant, and the reverse-mode
+  derivative of the unpooled mean-field (the loss gradient with respect to
+  the unaries, the compatibility and the five Eq. 4 parameters, obtained by
+  undoing each step of Alg. 1).  Wrapped here.
 - ``bruteforce.py``: two slower, differently-structured forms used to pin
   ``oracle.c`` (dense all-pairs FullCRF mean-field, and mean-field derived by
   enumerating the Gibbs energy of Eq. 1-3).
@@ -32,8 +35,11 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 __all__ = [
     "OracleParams", "build", "meanfield", "message", "update", "softmax",
-    "avgpool", "upsample", "kernel", "num_threads",
+    "avgpool", "upsample", "kernel", "num_threads", "meanfield_backward", "PARAM_NAMES",
 ]
+
+# order of the Eq. 4 parameters in meanfield_backward's dparams
+PARAM_NAMES = ("w_app", "theta_alpha", "theta_beta", "w_smooth", "theta_gamma")
 
 
 def build(force: bool = False) -> str:
@@ -106,6 +112,11 @@ def _load():
                                         ctypes.c_int, _dp]
         lib.oracle_kernel.restype = ctypes.c_double
         lib.oracle_kernel.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.POINTER(_CParams)]
+        lib.oracle_meanfield_backward.restype = ctypes.c_int
+        lib.oracle_meanfield_backward.argtypes = [_dp, _dp, ctypes.c_int, ctypes.c_int,
+                                                  ctypes.c_int, ctypes.c_int,
+                                                  ctypes.POINTER(_CParams), _dp, ctypes.c_int,
+                                                  _dp, _dp, _dp, _dp]
         lib.oracle_num_threads.restype = ctypes.c_int
         lib.oracle_num_threads.argtypes = []
         _lib = lib
@@ -146,6 +157,32 @@ def meanfield(U, I, params: OracleParams, iters: int, compat=None) -> np.ndarray
     if rc != 0:
         raise ValueError("oracle_meanfield rejected its arguments")
     return Q
+
+
+def meanfield_backward(U, I, params: OracleParams, iters: int, G, compat=None):
+    """Reverse-mode derivative of ``meanfield`` (no blur) for a loss whose
+    derivative with respect to the returned Q is G [B,C,H,W].  Returns
+    (dU [B,C,H,W], dmu [C,C], dparams [5] in PARAM_NAMES order); dmu is the
+    derivative with respect to the compatibility at ``compat`` (Potts when
+    None), dparams with respect to the Eq. 4 parameters; both are summed over
+    the batch."""
+    U = _f64(U)
+    I = _f64(I)
+    G = _f64(G)
+    if U.ndim != 4 or G.shape != U.shape or I.shape != (U.shape[0], 3) + U.shape[2:]:
+        raise ValueError("expected U, G [B,C,H,W] and I [B,3,H,W]")
+    B, C, H, W = U.shape
+    mu = None if compat is None else _f64(compat).reshape(C, C)
+    dU = np.empty_like(U)
+    dmu = np.empty((C, C))
+    dp = np.empty(5)
+    rc = _load().oracle_meanfield_backward(_ptr(U), _ptr(I), B, C, H, W,
+                                           ctypes.byref(params.c()),
+                                           None if mu is None else _ptr(mu), int(iters),
+                                           _ptr(G), _ptr(dU), _ptr(dmu), _ptr(dp))
+    if rc != 0:
+        raise ValueError("oracle_meanfield_backward rejected its arguments")
+    return dU, dmu, dp
 
 
 def message(Q, I, params: OracleParams, pos_scale: float = 1.0) -> np.ndarray:

@@ -245,3 +245,208 @@ int oracle_meanfield(const double *U, const double *I, int B, int C, int H, int 
     free(Ip);
     return 0;
 }
+
+/* ------------------------------------------------------------------------
+ * Reverse-mode derivative of oracle_meanfield without blur (s = 1).
+ *
+ * The loss is a scalar L whose derivative with respect to the returned Q^T
+ * is G.  Every round of Alg. 1 is undone in reverse order, each step being
+ * the derivative of the forward step it undoes:
+ *   normalise   Q = softmax(Z):  dZ(l) = Q(l) (dQ(l) - sum_l' Q(l') dQ(l'))
+ *   unary add   Z = U - P:       dU += dZ,   dP = -dZ
+ *   compat      P(l) = sum_l' mu[l][l'] M(l'):
+ *                                dM(l') = sum_l mu[l][l'] dP(l)
+ *                                dmu[l][l'] += sum_p dP_p(l) M_p(l')
+ *   message     M_p(l) = sum_{q in W(p)} K(p,q) Q_q(l)            (Eq. 6):
+ *                                dQ_q(l) = sum over p with q in W(p) of
+ *                                          K(p,q) dM_p(l)   (the transpose)
+ *                                dK(p,q) = sum_l dM_p(l) Q_q(l)
+ *   kernel      K of Eq. 4 through its five parameters (w_app, theta_alpha,
+ *               theta_beta, w_smooth, theta_gamma), with A, S the two
+ *               Gaussians without their weights:
+ *                 dK/dw_app = A,  dK/dtheta_alpha = w_app A |p-q|^2/ta^3,
+ *                 dK/dtheta_beta = w_app A |I_p-I_q|^2/tb^3,
+ *                 dK/dw_smooth = S,  dK/dtheta_gamma = w_smooth S |p-q|^2/tg^3
+ *   initialise  Q0 = softmax(U):  dU += Q0 (dQ0 - <Q0, dQ0>)
+ * The forward rounds are recomputed first and every Q^t and M^t is kept.
+ * dU [B][C][H][W] is written; dmu (C*C, row-major, the derivative with
+ * respect to mu at the given mu, Potts included) and dparams (5 values in
+ * the order above) are written when not NULL, summed over the batch.
+ * Returns 0, or -1 on arguments outside the definition (blur included).
+ * ------------------------------------------------------------------------ */
+
+/* dK(p,q)/d(parameter) for the five Eq. 4 parameters. */
+static void kernel_param_derivs(double pos_d2, double col_d2, const oracle_params *p,
+                                double out[5])
+{
+    const double ta = p->theta_alpha, tb = p->theta_beta, tg = p->theta_gamma;
+    const double A = exp(-pos_d2 / (2.0 * ta * ta) - col_d2 / (2.0 * tb * tb));
+    const double S = exp(-pos_d2 / (2.0 * tg * tg));
+    out[0] = A;
+    out[1] = p->w_app * A * pos_d2 / (ta * ta * ta);
+    out[2] = p->w_app * A * col_d2 / (tb * tb * tb);
+    out[3] = S;
+    out[4] = p->w_smooth * S * pos_d2 / (tg * tg * tg);
+}
+
+/* q lies in the message window of p (Eq. 6 / Alg. 1 neighbourhood). */
+static int in_window(int py, int px, int qy, int qx, int r, int include_center)
+{
+    if (qy < py - r || qy > py + r || qx < px - r || qx > px + r) return 0;
+    if (qy == py && qx == px && !include_center) return 0;
+    return 1;
+}
+
+/* Transpose of the Eq. 6 message for one image: dQ_q(l) = sum over the
+ * pixels p whose window holds q of K(p,q) dM_p(l). */
+static void message_transpose(const double *dM, const double *I, int C, int H, int W,
+                              const oracle_params *p, double *dQ)
+{
+    const int r = (p->filter_size - 1) / 2;
+    const long HW = (long)H * W;
+#pragma omp parallel for schedule(static)
+    for (int qy = 0; qy < H; ++qy) {
+        for (int qx = 0; qx < W; ++qx) {
+            const long qi = (long)qy * W + qx;
+            for (int l = 0; l < C; ++l) dQ[l * HW + qi] = 0.0;
+            /* a window of radius r holds q only if its centre p lies within
+             * r of q: scan that box, test the window itself */
+            for (int py = qy - r; py <= qy + r; ++py) {
+                if (py < 0 || py >= H) continue;
+                for (int px = qx - r; px <= qx + r; ++px) {
+                    if (px < 0 || px >= W) continue;
+                    if (!in_window(py, px, qy, qx, r, p->include_center)) continue;
+                    const long pi = (long)py * W + px;
+                    double col = 0.0;
+                    for (int ch = 0; ch < 3; ++ch) {
+                        double d = I[ch * HW + pi] - I[ch * HW + qi];
+                        col += d * d;
+                    }
+                    double dy = py - qy, dx = px - qx;
+                    double kpq = oracle_kernel(dy * dy + dx * dx, col, p);
+                    for (int l = 0; l < C; ++l) dQ[l * HW + qi] += kpq * dM[l * HW + pi];
+                }
+            }
+        }
+    }
+}
+
+/* Parameter derivative of one message: sum over p, q in W(p) of
+ * dK(p,q) * dK(p,q)/d(parameter), dK(p,q) = sum_l dM_p(l) Q_q(l). */
+static void message_param_grad(const double *dM, const double *Q, const double *I, int C,
+                               int H, int W, const oracle_params *p, double acc[5])
+{
+    const int r = (p->filter_size - 1) / 2;
+    const long HW = (long)H * W;
+    for (int py = 0; py < H; ++py) {
+        for (int px = 0; px < W; ++px) {
+            const long pi = (long)py * W + px;
+            for (int qy = py - r; qy <= py + r; ++qy) {
+                if (qy < 0 || qy >= H) continue;
+                for (int qx = px - r; qx <= px + r; ++qx) {
+                    if (qx < 0 || qx >= W) continue;
+                    if (!in_window(py, px, qy, qx, r, p->include_center)) continue;
+                    const long qi = (long)qy * W + qx;
+                    double col = 0.0;
+                    for (int ch = 0; ch < 3; ++ch) {
+                        double d = I[ch * HW + pi] - I[ch * HW + qi];
+                        col += d * d;
+                    }
+                    double dy = qy - py, dx = qx - px;
+                    double g[5];
+                    kernel_param_derivs(dy * dy + dx * dx, col, p, g);
+                    double dk = 0.0;
+                    for (int l = 0; l < C; ++l) dk += dM[l * HW + pi] * Q[l * HW + qi];
+                    for (int j = 0; j < 5; ++j) acc[j] += dk * g[j];
+                }
+            }
+        }
+    }
+}
+
+/* Derivative of the softmax of one pixel: dz(l) = q(l) (dq(l) - <q, dq>). */
+static void softmax_adjoint_pixel(const double *q, const double *dq, long s, double *dz,
+                                  long zs, int C)
+{
+    double dot = 0.0;
+    for (int l = 0; l < C; ++l) dot += q[l * s] * dq[l * s];
+    for (int l = 0; l < C; ++l) dz[l * zs] = q[l * s] * (dq[l * s] - dot);
+}
+
+int oracle_meanfield_backward(const double *U, const double *I, int B, int C, int H, int W,
+                              const oracle_params *p, const double *mu, int T,
+                              const double *G, double *dU, double *dmu, double *dparams)
+{
+    if (B < 0 || C < 1 || H < 1 || W < 1 || T < 0 || !p) return -1;
+    if (p->filter_size < 1 || (p->filter_size & 1) == 0 || p->blur != 1) return -1;
+    if (C > 64) return -1;
+    const long HW = (long)H * W;
+    const long n = (long)C * HW;
+    double *Qs = (double *)malloc(sizeof(double) * (size_t)(T + 1) * n);
+    double *Ms = (double *)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1) * n);
+    double *dQ = (double *)malloc(sizeof(double) * n);
+    double *dQprev = (double *)malloc(sizeof(double) * n);
+    double *dP = (double *)malloc(sizeof(double) * n);
+    double *dM = (double *)malloc(sizeof(double) * n);
+    if (dmu) memset(dmu, 0, sizeof(double) * (size_t)C * C);
+    if (dparams) memset(dparams, 0, sizeof(double) * 5);
+
+    for (int b = 0; b < B; ++b) {
+        const double *Ub = U + (long)b * n;
+        const double *Ib = I + (long)b * 3 * HW;
+        double *dUb = dU + (long)b * n;
+        /* forward, keeping every Q^t and M^t */
+        oracle_softmax(Ub, C, H, W, Qs);
+        for (int t = 0; t < T; ++t) {
+            oracle_message(Qs + (long)t * n, Ib, C, H, W, p, 1.0, Ms + (long)t * n);
+            oracle_update(Ub, Ms + (long)t * n, mu, C, HW, Qs + (long)(t + 1) * n);
+        }
+        /* reverse */
+        memcpy(dQ, G + (long)b * n, sizeof(double) * n);
+        memset(dUb, 0, sizeof(double) * n);
+        for (int t = T - 1; t >= 0; --t) {
+            const double *Qn = Qs + (long)(t + 1) * n;   /* Q^{t+1} */
+            const double *Qt = Qs + (long)t * n;         /* Q^t */
+            const double *Mt = Ms + (long)t * n;         /* M^t */
+            for (long i = 0; i < HW; ++i) {
+                double dz[64];
+                softmax_adjoint_pixel(Qn + i, dQ + i, HW, dz, 1, C);
+                for (int l = 0; l < C; ++l) {
+                    dUb[l * HW + i] += dz[l];
+                    dP[l * HW + i] = -dz[l];
+                }
+            }
+            for (long i = 0; i < HW; ++i)
+                for (int lp = 0; lp < C; ++lp) {
+                    double acc = 0.0;
+                    for (int l = 0; l < C; ++l) {
+                        double m = mu ? mu[l * C + lp] : (l != lp ? 1.0 : 0.0);
+                        acc += m * dP[l * HW + i];
+                    }
+                    dM[lp * HW + i] = acc;
+                }
+            if (dmu)
+                for (int l = 0; l < C; ++l)
+                    for (int lp = 0; lp < C; ++lp) {
+                        double acc = 0.0;
+                        for (long i = 0; i < HW; ++i) acc += dP[l * HW + i] * Mt[lp * HW + i];
+                        dmu[l * C + lp] += acc;
+                    }
+            if (dparams) message_param_grad(dM, Qt, Ib, C, H, W, p, dparams);
+            message_transpose(dM, Ib, C, H, W, p, dQprev);
+            memcpy(dQ, dQprev, sizeof(double) * n);
+        }
+        for (long i = 0; i < HW; ++i) {
+            double dz[64];
+            softmax_adjoint_pixel(Qs + i, dQ + i, HW, dz, 1, C);
+            for (int l = 0; l < C; ++l) dUb[l * HW + i] += dz[l];
+        }
+    }
+    free(Qs);
+    free(Ms);
+    free(dQ);
+    free(dQprev);
+    free(dP);
+    free(dM);
+    return 0;
+}
