@@ -49,7 +49,7 @@ typedef enum {
     CONVCRF_OK = 0,
     CONVCRF_E_INVALID_ARG = -1,  /* NULL pointer, bad size or parameter */
     CONVCRF_E_UNSUPPORTED = -2,  /* valid by the definition but not built
-                                    here (C > 32, k > 15, H or W not a
+                                    here (C > 24, k > 15, H or W not a
                                     multiple of the blur factor, ...) */
     CONVCRF_E_NO_DEVICE = -3,    /* no usable gfx950 device */
     CONVCRF_E_HIP = -4,          /* a HIP runtime call failed */
@@ -142,6 +142,42 @@ convcrf_status convcrf_meanfield(convcrf_ctx *ctx, const float *unary,
                                  int W, const convcrf_params *params,
                                  int iters, float *q_out, void *stream);
 
+/* Reverse mode: the derivative of a scalar loss L through convcrf_meanfield
+ * (no blur), for training the CRF by backpropagation through the unrolled
+ * mean-field rounds of Alg. 1 (Sec. 1; Sec. 5.3 trains end to end through
+ * five rounds).  The learnable parameters are the Eq. 4 weights and scales
+ * (Sec. 3) and the compatibility (Sec. 4.2).  Given grad_q = dL/dQ for the
+ * Q that convcrf_meanfield returns with the same arguments, it writes
+ *   grad_unary  [B][C][H][W]  dL/dU                    (DEVICE, required)
+ *   grad_compat [C][C]        dL/dmu[l][l'], the derivative with respect to
+ *                             the compatibility at params->compat (at the
+ *                             Potts matrix mu[l][l'] = [l != l'] when that is
+ *                             NULL), summed over the batch  (DEVICE or NULL)
+ *   grad_kernel [5]           dL/d(w_app, theta_alpha, theta_beta, w_smooth,
+ *                             theta_gamma) of Eq. 4, summed over the batch
+ *                                                         (DEVICE or NULL)
+ * Each round of Alg. 1 is undone in reverse order: the softmax adjoint
+ * dZ = Q (dQ - <Q, dQ>), dU += dZ, the compatibility transposed, and the
+ * message transposed, which is the message itself applied to dL/dM because
+ * K(p,q) = K(q,p) and the window is symmetric; the kernel-parameter terms are
+ * sum over p and window neighbours q of (sum_l dL/dM_p(l) Q_q(l)) dK(p,q)/d.
+ * The forward rounds are recomputed inside the call (the unaries, image and
+ * params must be those of the forward call); `variant` is ignored.
+ * unary, image, grad_q: DEVICE pointers, as for convcrf_meanfield; grad_q
+ * [B][C][H][W].  grad_unary must not overlap unary, image or grad_q.
+ * The context's workspace grows by (iters + 1) + 4 buffers of [B][C][H][W]
+ * floats (Q^0..Q^T, two for dL/dQ, dL/dM, and with grad_compat two more).
+ * Returns CONVCRF_E_UNSUPPORTED for blur != 1 or when the window and classes
+ * exceed the LDS of one work-group (2C + 3 planes of the tile plus halo);
+ * otherwise as convcrf_meanfield.  Asynchronous on `stream`. */
+convcrf_status convcrf_meanfield_backward(convcrf_ctx *ctx, const float *unary,
+                                          const float *image, int B, int C,
+                                          int H, int W,
+                                          const convcrf_params *params,
+                                          int iters, const float *grad_q,
+                                          float *grad_unary, float *grad_compat,
+                                          float *grad_kernel, void *stream);
+
 /* Per-kernel timing with HIP events recorded on the launch stream around
  * every kernel the library enqueues, for measurement.  enable = 1 starts
  * (and clears) the record, 0 stops it.  Off by default. */
@@ -149,8 +185,9 @@ convcrf_status convcrf_profile_enable(convcrf_ctx *ctx, int enable);
 
 /* Total elapsed milliseconds and launch count of the kernels named `name`
  * ("fused_iter", "fused_resident", "sync_reset", "softmax", "build_kernel",
- * "materialised_iter", "blur_pool", "blur_message", "blur_update") since
- * profiling was enabled.  "fused_resident" is one launch running all
+ * "materialised_iter", "blur_pool", "blur_message", "blur_update", and for
+ * convcrf_meanfield_backward "bwd_point", "bwd_message", "bwd_gram",
+ * "bwd_reduce" besides the forward's) since profiling was enabled.  "fused_resident" is one launch running all
  * iterations of a call (CONVCRF_VARIANT_RESIDENT); "fused_iter" one
  * iteration.
  * Synchronises on the recorded events.  An unknown or unused name gives

@@ -27,11 +27,15 @@ VARIANT_MATERIALISED = 1
 VARIANT_RESIDENT = 2
 
 KERNEL_NAMES = ("fused_iter", "fused_resident", "sync_reset", "softmax", "build_kernel",
-                "materialised_iter", "blur_pool", "blur_message", "blur_update")
+                "materialised_iter", "blur_pool", "blur_message", "blur_update",
+                "bwd_point", "bwd_message", "bwd_gram", "bwd_reduce")
 
 EXPORTED = ("convcrf_default_params", "convcrf_validate", "convcrf_init", "convcrf_destroy",
-            "convcrf_meanfield", "convcrf_profile_enable", "convcrf_profile_read",
-            "convcrf_last_error", "convcrf_status_string")
+            "convcrf_meanfield", "convcrf_meanfield_backward", "convcrf_profile_enable",
+            "convcrf_profile_read", "convcrf_last_error", "convcrf_status_string")
+
+# order of grad_kernel in convcrf_meanfield_backward
+KERNEL_PARAM_NAMES = ("w_app", "theta_alpha", "theta_beta", "w_smooth", "theta_gamma")
 
 
 class ConvCRFError(RuntimeError):
@@ -109,6 +113,10 @@ def load_library(path: str = LIB_PATH):
     lib.convcrf_meanfield.restype = st
     lib.convcrf_meanfield.argtypes = [vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                       ctypes.c_int, P(CParams), ctypes.c_int, vp, vp]
+    lib.convcrf_meanfield_backward.restype = st
+    lib.convcrf_meanfield_backward.argtypes = [vp, vp, vp, ctypes.c_int, ctypes.c_int,
+                                               ctypes.c_int, ctypes.c_int, P(CParams),
+                                               ctypes.c_int, vp, vp, vp, vp, vp]
     lib.convcrf_profile_enable.restype = st
     lib.convcrf_profile_enable.argtypes = [vp, ctypes.c_int]
     lib.convcrf_profile_read.restype = st
@@ -192,6 +200,38 @@ class ConvCRF:
                                            ctypes.byref(cp), int(iters), out.data_ptr(), sp),
                self._h)
         return out
+
+    def meanfield_backward(self, unary, image, params: Params, iters: int, grad_q,
+                           grad_compat: bool = False, grad_kernel: bool = False,
+                           out=None, stream=None):
+        """Derivative of a loss through ``meanfield`` (no blur): returns
+        (dL/dU [B,C,H,W], dL/dmu [C,C] or None, dL/d(Eq. 4 parameters) [5]
+        or None) as float32 tensors on the unary's device; ``grad_q`` is
+        dL/dQ.  Enqueued on ``stream`` (default: torch's current stream)."""
+        import torch
+        for name, t in (("unary", unary), ("image", image), ("grad_q", grad_q)):
+            if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous() or t.dim() != 4:
+                raise ConvCRFError(E_INVALID_ARG, f"{name} must be a contiguous 4-D float32 GPU tensor")
+        B, C, H, W = unary.shape
+        if tuple(image.shape) != (B, 3, H, W) or tuple(grad_q.shape) != (B, C, H, W):
+            raise ConvCRFError(E_INVALID_ARG, "image must be [B,3,H,W] and grad_q [B,C,H,W]")
+        if out is None:
+            out = torch.empty_like(unary)
+        elif (out.dtype != torch.float32 or not out.is_contiguous()
+              or tuple(out.shape) != tuple(unary.shape) or out.device != unary.device):
+            raise ConvCRFError(E_INVALID_ARG, "out must match unary")
+        gmu = torch.empty((C, C), dtype=torch.float32, device=unary.device) if grad_compat else None
+        gk = torch.empty(5, dtype=torch.float32, device=unary.device) if grad_kernel else None
+        if stream is None:
+            stream = torch.cuda.current_stream(unary.device)
+        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        cp = params.c()
+        _check(self._lib.convcrf_meanfield_backward(
+            self._h, unary.data_ptr(), image.data_ptr(), B, C, H, W, ctypes.byref(cp),
+            int(iters), grad_q.data_ptr(), out.data_ptr(),
+            gmu.data_ptr() if gmu is not None else None,
+            gk.data_ptr() if gk is not None else None, sp), self._h)
+        return out, gmu, gk
 
     def last_error(self) -> str:
         """The library's last message for this context."""

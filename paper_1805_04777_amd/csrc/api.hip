@@ -5,9 +5,11 @@
 // (the other half of the ping-pong is the caller's q_out), the kernel matrix
 // for the materialised variant, pooled buffers for the blur path, and a
 // small device block holding the compatibility matrix.
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <string>
 #include <vector>
 
@@ -23,10 +25,11 @@ constexpr size_t kLdsLimit = 160 * 1024;  // gfx950 LDS per work-group
 
 const char* const kKernelNames[] = {"fused_iter",   "softmax",      "build_kernel",
                                     "materialised_iter", "blur_pool", "blur_message",
-                                    "blur_update",  "fused_resident", "sync_reset"};
+                                    "blur_update",  "fused_resident", "sync_reset",
+                                    "bwd_point", "bwd_message", "bwd_gram", "bwd_reduce"};
 enum KernelId {
     kFused = 0, kSoftmax, kBuild, kMatIter, kPool, kBlurMsg, kBlurUpd, kResident, kSyncReset,
-    kNumKernels
+    kBwdPoint, kBwdMsg, kBwdGram, kBwdReduce, kNumKernels
 };
 
 struct DevBuf {
@@ -49,6 +52,8 @@ struct convcrf_ctx {
     bool coop = false;              // cooperative launches supported
     std::string err = "no error";
     DevBuf q_ws, q_ws2, kmat, pool_q, pool_m, pool_f, mu, sync;
+    // reverse mode: Q^0..Q^T, dL/dQ ping-pong, dL/dM, -dL/dZ, M^t, partial sums
+    DevBuf b_q, b_dq, b_dm, b_dp, b_m, b_gpart, b_kpart;
     std::vector<float> mu_last;   // host copy of the uploaded compatibility
     float* mu_pinned = nullptr;   // pinned staging for the upload
     size_t mu_pinned_cap = 0;
@@ -251,6 +256,41 @@ TileConfig pick_tile(int k, int C, bool colour, bool compat) {
     return TileConfig{0, 4, 32};
 }
 
+// Tiling of the unpooled iterations over B x C x H x W.  `a` already holds
+// the parameters (compatibility, centre, taps); this sets its sizes and
+// tiles, and `as`, the copy with the tiling of the streamed kernel.
+// `bufs` are the Q buffers the launches read or write besides the unary.
+// streamed: whether the streamed kernel runs the iterations (k = 3..7,
+// C = 19 or 21, whole float2 rows, unary rows in 16-byte pieces, buffers
+// under 2 GB, the LDS within bounds).
+void plan_unpooled(IterArgs& a, IterArgs& as, bool& streamed, size_t& lds_s, TileConfig tile,
+                   bool mat, int k, int B, int C, int H, int W, const float* unary,
+                   const float* image, const float* kmat, std::initializer_list<const void*> bufs) {
+    a.C = C;
+    a.planes = C;
+    a.H = H;
+    a.W = W;
+    a.unary = unary;
+    a.feat = image;
+    a.kmat = kmat;
+    a.tiles_x = (W + tile.width - 1) / tile.width;
+    a.tiles_per_img = a.tiles_x * ((H + tile.rows - 1) / tile.rows);
+    a.ntiles = a.tiles_per_img * B;
+    a.mode = kModeUpdate;
+    const uintptr_t va = 4u * tile.pix;
+    bool aligned = reinterpret_cast<uintptr_t>(unary) % va == 0;
+    for (const void* b : bufs) aligned = aligned && reinterpret_cast<uintptr_t>(b) % va == 0;
+    a.vec = (W % tile.pix == 0) && aligned;
+    lds_s = stream_lds_bytes(k, C, a.mu != nullptr);
+    streamed = !mat && k >= 3 && k <= 7 && (C == 19 || C == 21) && a.vec && W % 4 == 0 &&
+               reinterpret_cast<uintptr_t>(unary) % 16 == 0 && lds_s <= kLdsLimit &&
+               (size_t)C * H * W * 4 < (1ull << 31);
+    as = a;
+    as.tiles_x = (W + kStreamTW - 1) / kStreamTW;
+    as.tiles_per_img = as.tiles_x * ((H + kStreamRows - 1) / kStreamRows);
+    as.ntiles = as.tiles_per_img * B;
+}
+
 // Upload mu (C*C floats) if it differs from what the device holds.
 convcrf_status upload_mu(convcrf_ctx* ctx, const float* mu, int C, hipStream_t stream) {
     const size_t n = (size_t)C * C;
@@ -360,7 +400,8 @@ void convcrf_destroy(convcrf_ctx* ctx) {
     (void)hipSetDevice(ctx->device);
     (void)hipDeviceSynchronize();
     for (DevBuf* b : {&ctx->q_ws, &ctx->q_ws2, &ctx->kmat, &ctx->pool_q, &ctx->pool_m,
-                      &ctx->pool_f, &ctx->mu, &ctx->sync})
+                      &ctx->pool_f, &ctx->mu, &ctx->sync, &ctx->b_q, &ctx->b_dq, &ctx->b_dm,
+                      &ctx->b_dp, &ctx->b_m, &ctx->b_gpart, &ctx->b_kpart})
         if (b->p) (void)hipFree(b->p);
     if (ctx->mu_pinned) (void)hipHostFree(ctx->mu_pinned);
     if (ctx->mu_copied) (void)hipEventDestroy(ctx->mu_copied);
@@ -470,33 +511,11 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
                 if (st != CONVCRF_OK) return st;
             }
         }
-        a.C = C;
-        a.planes = C;
-        a.H = H;
-        a.W = W;
-        a.unary = unary;
-        a.feat = image;
-        a.kmat = static_cast<const float*>(ctx->kmat.p);
-        a.tiles_x = (W + tile.width - 1) / tile.width;
-        a.tiles_per_img = a.tiles_x * ((H + tile.rows - 1) / tile.rows);
-        a.ntiles = a.tiles_per_img * B;
-        a.mode = kModeUpdate;
-        const uintptr_t va = 4u * tile.pix;
-        const bool aligned = (reinterpret_cast<uintptr_t>(unary) % va == 0) &&
-                             (reinterpret_cast<uintptr_t>(q_out) % va == 0) &&
-                             (!ctx->q_ws.p || reinterpret_cast<uintptr_t>(ctx->q_ws.p) % va == 0);
-        a.vec = (W % tile.pix == 0) && aligned;
-        // The iterations stream their staging under the computation where
-        // that kernel is built (k = 3..7, C = 19 or 21, whole float2 rows,
-        // unary rows in 16-byte pieces, buffers under 2 GB).
-        const size_t lds_s = stream_lds_bytes(k, C, mu_dev != nullptr);
-        const bool streamed = !mat && k >= 3 && k <= 7 && (C == 19 || C == 21) && a.vec &&
-                              W % 4 == 0 && reinterpret_cast<uintptr_t>(unary) % 16 == 0 &&
-                              lds_s <= kLdsLimit && (size_t)C * H * W * 4 < (1ull << 31);
-        IterArgs as = a;                      // the streamed launches' tiling
-        as.tiles_x = (W + kStreamTW - 1) / kStreamTW;
-        as.tiles_per_img = as.tiles_x * ((H + kStreamRows - 1) / kStreamRows);
-        as.ntiles = as.tiles_per_img * B;
+        IterArgs as;                          // the streamed launches' tiling
+        bool streamed = false;
+        size_t lds_s = 0;
+        plan_unpooled(a, as, streamed, lds_s, tile, mat, k, B, C, H, W, unary, image,
+                      static_cast<const float*>(ctx->kmat.p), {q_out, ctx->q_ws.p});
         // Resident variant: all iterations in one launch when every tile's
         // work-group fits on the device at once (Potts): the tile stays in
         // LDS and only border rings cross memory.  On the streamed tiles the
@@ -624,6 +643,168 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
         });
         if (st != CONVCRF_OK) return st;
     }
+    return CONVCRF_OK;
+}
+
+convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
+                                          const float* image, int B, int C, int H, int W,
+                                          const convcrf_params* params, int iters,
+                                          const float* grad_q, float* grad_unary,
+                                          float* grad_compat, float* grad_kernel,
+                                          void* stream_ptr) {
+    if (!ctx) return fail(nullptr, CONVCRF_E_INVALID_ARG, "ctx is NULL");
+    convcrf_status st = validate(ctx, B, C, H, W, params, iters);
+    if (st != CONVCRF_OK) return st;
+    if (params->blur != 1)
+        return fail(ctx, CONVCRF_E_UNSUPPORTED, "the derivative is built for blur = 1 only");
+    const convcrf_params p = *params;
+    const int k = p.filter_size;
+    if (bwd_lds_bytes(k, C) > kLdsLimit)
+        return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
+    const long long npix = (long long)B * H * W;
+    const size_t qbytes = sizeof(float) * (size_t)npix * C;
+    const size_t ibytes = sizeof(float) * (size_t)npix * 3;
+    if (npix > 0 && (!unary || !image || !grad_q || !grad_unary))
+        return fail(ctx, CONVCRF_E_INVALID_ARG, "NULL tensor pointer");
+    if (npix > 0 && (overlaps(grad_unary, qbytes, unary, qbytes) ||
+                     overlaps(grad_unary, qbytes, image, ibytes) ||
+                     overlaps(grad_unary, qbytes, grad_q, qbytes)))
+        return fail(ctx, CONVCRF_E_INVALID_ARG, "grad_unary overlaps unary, image or grad_q");
+    hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+
+    const double ta = p.theta_alpha, tb = p.theta_beta, tg = p.theta_gamma;
+    const float scale[5] = {1.f, (float)(p.w_app / (ta * ta * ta)),
+                            (float)(p.w_app / (tb * tb * tb)), 1.f,
+                            (float)(p.w_smooth / (tg * tg * tg))};
+    const int tw = bwd_tile_w(k), th = bwd_tile_h(k, C);
+    const long long ntiles_ll = (long long)((W + tw - 1) / tw) * ((H + th - 1) / th) * B;
+    if (ntiles_ll > 0x7fffffffLL) return fail(ctx, CONVCRF_E_UNSUPPORTED, "too many tiles");
+    const int ntiles = (int)ntiles_ll;
+    const int groups = (int)std::min<long long>(1024, std::max<long long>(1, (npix + 1023) / 1024));
+    const bool run = npix > 0 && iters > 0;
+    if (npix == 0) {
+        if (grad_compat || grad_kernel)   // nothing to sum: zeros
+            return launch(ctx, kBwdReduce, stream, "bwd_reduce", [&] {
+                return launch_bwd_reduce(nullptr, 0, C, grad_compat, nullptr, 0, scale,
+                                         grad_kernel, stream);
+            });
+        return CONVCRF_OK;
+    }
+
+    const float* mu_dev = nullptr;
+    if (p.compat) {
+        if ((st = upload_mu(ctx, p.compat, C, stream)) != CONVCRF_OK) return st;
+        mu_dev = static_cast<const float*>(ctx->mu.p);
+    }
+    // workspace: Q^0 .. Q^T in 256-byte aligned slices
+    const size_t slice = (qbytes + 255) / 256 * 256;
+    if ((st = ensure(ctx, ctx->b_q, slice * (iters + 1))) != CONVCRF_OK) return st;
+    if (run) {
+        if ((st = ensure(ctx, ctx->b_dq, slice * 2)) != CONVCRF_OK) return st;
+        if ((st = ensure(ctx, ctx->b_dm, slice)) != CONVCRF_OK) return st;
+        if (grad_compat) {
+            if ((st = ensure(ctx, ctx->b_dp, slice)) != CONVCRF_OK) return st;
+            if ((st = ensure(ctx, ctx->b_m, slice)) != CONVCRF_OK) return st;
+            if ((st = ensure(ctx, ctx->b_gpart, sizeof(float) * (size_t)groups * C * C)) !=
+                CONVCRF_OK)
+                return st;
+        }
+        if ((st = ensure(ctx, ctx->b_kpart, sizeof(float) * (size_t)ntiles * 5)) != CONVCRF_OK)
+            return st;
+    }
+    char* qbase = static_cast<char*>(ctx->b_q.p);
+    auto qs = [&](int t) { return reinterpret_cast<float*>(qbase + slice * t); };
+
+    // forward: Q^0 = softmax(U), then the fused rounds, keeping every Q^t
+    st = launch(ctx, kSoftmax, stream, "softmax",
+                [&] { return launch_softmax(unary, qs(0), B, C, H * W, stream); });
+    if (st != CONVCRF_OK) return st;
+    if (run) {
+        IterArgs a{};
+        a.mu = mu_dev;
+        a.include_center = p.include_center;
+        a.neg_beta = (float)(-kLog2eD / (2.0 * tb * tb));
+        a.center_w = (float)((double)p.w_app + (double)p.w_smooth);
+        fill_taps(p, 1, a.taps);
+        const TileConfig tile = pick_tile(k, C, true, mu_dev != nullptr);
+        if (tile.rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
+        const size_t lds = iter_lds_bytes(k, C, tile, true, mu_dev != nullptr);
+        IterArgs as;
+        bool streamed = false;
+        size_t lds_s = 0;
+        plan_unpooled(a, as, streamed, lds_s, tile, false, k, B, C, H, W, unary, image, nullptr,
+                      {qbase});
+        for (int t = 0; t < iters; ++t) {
+            a.src = as.src = t == 0 ? unary : qs(t);
+            a.dst = as.dst = qs(t + 1);
+            a.first = as.first = t == 0;
+            st = launch(ctx, kFused, stream, "fused_iter", [&] {
+                return streamed ? launch_stream(as, k, lds_s, stream)
+                                : launch_iter(a, k, false, tile, lds, stream);
+            });
+            if (st != CONVCRF_OK) return st;
+        }
+    }
+
+    // reverse rounds
+    BwdArgs ba{};
+    ba.feat = image;
+    ba.C = C;
+    ba.H = H;
+    ba.W = W;
+    ba.tiles_x = (W + tw - 1) / tw;
+    ba.tiles_per_img = ba.tiles_x * ((H + th - 1) / th);
+    ba.ntiles = ntiles;
+    ba.include_center = p.include_center;
+    ba.neg_beta = (float)(-kLog2eD / (2.0 * tb * tb));
+    ba.w_app = p.w_app;
+    ba.w_smooth = p.w_smooth;
+    for (int n = 0; n <= kMaxN; ++n) {
+        ba.a_log2[n] = (float)(-(double)n * kLog2eD / (2.0 * ta * ta));
+        ba.smooth[n] = (float)std::exp(-(double)n / (2.0 * tg * tg));
+    }
+    ba.dm = static_cast<const float*>(ctx->b_dm.p);
+    ba.kpart = static_cast<float*>(ctx->b_kpart.p);
+    ba.m_out = grad_compat ? static_cast<float*>(ctx->b_m.p) : nullptr;
+    float* dp = grad_compat ? static_cast<float*>(ctx->b_dp.p) : nullptr;
+    float* dm = static_cast<float*>(ctx->b_dm.p);
+    const float* dq = grad_q;
+    for (int t = iters - 1; t >= 0; --t) {
+        const int acc = t != iters - 1;
+        st = launch(ctx, kBwdPoint, stream, "bwd_point", [&] {
+            return launch_bwd_point(qs(t + 1), dq, mu_dev, grad_unary, dm, dp, B, C,
+                                    (long long)H * W, acc, stream);
+        });
+        if (st != CONVCRF_OK) return st;
+        ba.q = qs(t);
+        ba.dq_out = reinterpret_cast<float*>(static_cast<char*>(ctx->b_dq.p) + slice * (t & 1));
+        ba.accumulate = acc;
+        st = launch(ctx, kBwdMsg, stream, "bwd_message",
+                    [&] { return launch_bwd_message(ba, k, stream); });
+        if (st != CONVCRF_OK) return st;
+        if (grad_compat) {
+            st = launch(ctx, kBwdGram, stream, "bwd_gram", [&] {
+                return launch_bwd_gram(dp, ba.m_out, static_cast<float*>(ctx->b_gpart.p), B, C,
+                                       (long long)H * W, groups, acc, stream);
+            });
+            if (st != CONVCRF_OK) return st;
+        }
+        dq = ba.dq_out;
+    }
+    // Q^0 = softmax(U)
+    st = launch(ctx, kBwdPoint, stream, "bwd_point", [&] {
+        return launch_bwd_point(qs(0), dq, nullptr, grad_unary, nullptr, nullptr, B, C,
+                                (long long)H * W, iters > 0, stream);
+    });
+    if (st != CONVCRF_OK) return st;
+    if (grad_compat || grad_kernel)
+        return launch(ctx, kBwdReduce, stream, "bwd_reduce", [&] {
+            return launch_bwd_reduce(static_cast<const float*>(ctx->b_gpart.p), run ? groups : 0,
+                                     C, grad_compat, static_cast<const float*>(ctx->b_kpart.p),
+                                     run ? ntiles : 0, scale, grad_kernel, stream);
+        });
     return CONVCRF_OK;
 }
 

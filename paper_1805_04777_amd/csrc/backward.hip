@@ -1,0 +1,341 @@
+// backward.hip -- reverse-mode derivative of the unpooled mean-field
+// (Alg. 1 unrolled over its T rounds, Eq. 4 kernel, Eq. 6 message).
+//
+// Each round is undone by two kernels:
+//   bwd_point_kernel   the adjoints of the softmax (normalisation), the unary
+//                      addition and the compatibility transform, per pixel;
+//   bwd_msg_kernel     the adjoint of the message: because K(p,q) = K(q,p)
+//                      and q lies in the window of p exactly when p lies in
+//                      the window of q, the transpose of the message is the
+//                      message itself applied to dL/dM.  The same pass sums
+//                      the derivative with respect to the Eq. 4 parameters
+//                      and, when the compatibility derivative is wanted,
+//                      recomputes the forward message M^t.
+// bwd_gram_kernel accumulates sum_p dP_p(l) M_p(l') for the compatibility
+// derivative and bwd_reduce_kernel folds the per-block partial sums.
+#include "crf_internal.h"
+
+namespace convcrf {
+namespace {
+
+// ---------------------------------------------------------------- pointwise
+template <int CM>
+__global__ __launch_bounds__(256) void bwd_point_kernel(
+    const float* __restrict__ q, const float* __restrict__ dq, const float* __restrict__ mu,
+    float* __restrict__ du, float* __restrict__ dm, float* __restrict__ dp, int C,
+    long long hw, long long npix, int accumulate) {
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= npix) return;
+    const long long b = i / hw;
+    const long long base = b * C * hw + (i - b * hw);
+    float qv[CM], dz[CM];
+    float dot = 0.f;
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        if (c < C) {
+            qv[c] = q[base + c * hw];
+            dz[c] = dq[base + c * hw];
+            dot = fmaf(qv[c], dz[c], dot);
+        }
+    }
+    float sum = 0.f;
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        if (c < C) {
+            dz[c] = qv[c] * (dz[c] - dot);
+            sum += dz[c];
+            float* o = du + base + c * hw;
+            *o = accumulate ? *o + dz[c] : dz[c];
+            if (dp) dp[base + c * hw] = -dz[c];
+        }
+    }
+    if (!dm) return;
+    if (mu) {
+        for (int lp = 0; lp < C; ++lp) {
+            float acc = 0.f;
+#pragma unroll
+            for (int l = 0; l < CM; ++l)
+                if (l < C) acc = fmaf(mu[l * C + lp], -dz[l], acc);
+            dm[base + lp * hw] = acc;
+        }
+    } else {
+        // Potts, mu[l][l'] = [l != l']: dm(l') = -(sum_l dZ(l) - dZ(l'))
+#pragma unroll
+        for (int c = 0; c < CM; ++c)
+            if (c < C) dm[base + c * hw] = dz[c] - sum;
+    }
+}
+
+// ---------------------------------------------------------- adjoint message
+template <int K, int TH, bool WM>
+__global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) {
+    constexpr int TW = bwd_tile_w(K), NT = TW * TH;
+    constexpr int R = (K - 1) / 2, LW = TW + K - 1, LH = TH + K - 1, PL = LW * LH;
+    constexpr int CM = kMaxC;
+    extern __shared__ float lds[];
+    __shared__ float red[5][NT / 64];
+    const int C = a.C;
+    const float* sc = lds;               // 3 colour planes
+    const float* sq = lds + 3 * PL;      // C planes of Q^t
+    const float* sm = sq + C * PL;       // C planes of dL/dM^t
+    const int tile = blockIdx.x;
+    const int b = tile / a.tiles_per_img;
+    const int tr = tile - b * a.tiles_per_img;
+    const int ty = tr / a.tiles_x, tx = tr - ty * a.tiles_x;
+    const int y0 = ty * TH - R, x0 = tx * TW - R;
+    const long long hw = (long long)a.H * a.W;
+    const float* fb = a.feat + (long long)b * 3 * hw;
+    const float* qb = a.q + (long long)b * C * hw;
+    const float* mb = a.dm + (long long)b * C * hw;
+
+    // tile plus halo of every plane; zero outside the image, so that taps
+    // there contribute nothing to any sum
+    const int nplanes = 2 * C + 3;
+#pragma unroll 4
+    for (int e = threadIdx.x; e < nplanes * PL; e += NT) {
+        const int pl = e / PL, o = e - pl * PL;
+        const int ly = o / LW, lx = o - ly * LW;
+        const int gy = y0 + ly, gx = x0 + lx;
+        const float* src = pl < 3 ? fb + pl * hw : (pl < 3 + C ? qb + (pl - 3) * hw
+                                                               : mb + (pl - 3 - C) * hw);
+        float v = 0.f;
+        if (gy >= 0 && gy < a.H && gx >= 0 && gx < a.W) v = src[(long long)gy * a.W + gx];
+        lds[e] = v;
+    }
+    __syncthreads();
+
+    const int lx = threadIdx.x % TW, ly = threadIdx.x / TW;
+    const int px = tx * TW + lx, py = ty * TH + ly;
+    float g0 = 0.f, g1 = 0.f, g2 = 0.f, g3 = 0.f, g4 = 0.f;
+    if (px < a.W && py < a.H) {
+        const int oc = (ly + R) * LW + lx + R;
+        const float ir = sc[oc], ig = sc[PL + oc], ib = sc[2 * PL + oc];
+        float dmq[CM], dqa[CM], ma[CM];
+#pragma unroll
+        for (int c = 0; c < CM; ++c) {
+            dmq[c] = c < C ? sm[c * PL + oc] : 0.f;
+            dqa[c] = 0.f;
+            ma[c] = 0.f;
+        }
+#pragma unroll 1
+        for (int dy = -R; dy <= R; ++dy) {
+#pragma unroll 1
+            for (int dx = -R; dx <= R; ++dx) {
+                if (dx == 0 && dy == 0 && !a.include_center) continue;
+                const int o = oc + dy * LW + dx;
+                const float er = ir - sc[o], eg = ig - sc[PL + o], eb = ib - sc[2 * PL + o];
+                const float cd2 = fmaf(er, er, fmaf(eg, eg, eb * eb));
+                const int n = dx * dx + dy * dy;
+                const float av = exp2f(fmaf(a.neg_beta, cd2, a.a_log2[n]));
+                const float sv = a.smooth[n];
+                const float w = fmaf(a.w_app, av, a.w_smooth * sv);
+                float dk = 0.f;
+#pragma unroll
+                for (int c = 0; c < CM; ++c) {
+                    if (c < C) {
+                        const float qn = sq[c * PL + o];
+                        dk = fmaf(dmq[c], qn, dk);
+                        dqa[c] = fmaf(w, sm[c * PL + o], dqa[c]);
+                        if (WM) ma[c] = fmaf(w, qn, ma[c]);
+                    }
+                }
+                const float da = dk * av, ds = dk * sv;
+                g0 += da;
+                g1 = fmaf(da, (float)n, g1);
+                g2 = fmaf(da, cd2, g2);
+                g3 += ds;
+                g4 = fmaf(ds, (float)n, g4);
+            }
+        }
+        const long long pix = (long long)b * C * hw + (long long)py * a.W + px;
+#pragma unroll
+        for (int c = 0; c < CM; ++c) {
+            if (c < C) {
+                a.dq_out[pix + c * hw] = dqa[c];
+                if (WM) a.m_out[pix + c * hw] = ma[c];
+            }
+        }
+    }
+    // tile sums of the five parameter terms, in a fixed order
+    float g[5] = {g0, g1, g2, g3, g4};
+#pragma unroll
+    for (int j = 0; j < 5; ++j)
+        for (int off = 32; off > 0; off >>= 1) g[j] += __shfl_xor(g[j], off, 64);
+    const int wave = threadIdx.x / 64;
+    if ((threadIdx.x & 63) == 0)
+#pragma unroll
+        for (int j = 0; j < 5; ++j) red[j][wave] = g[j];
+    __syncthreads();
+    if (threadIdx.x < 5) {
+        const int j = threadIdx.x;
+        float s = 0.f;
+        for (int w = 0; w < NT / 64; ++w) s += red[j][w];
+        float* o = a.kpart + (long long)tile * 5 + j;
+        *o = a.accumulate ? *o + s : s;
+    }
+}
+
+// ------------------------------------------------------------ compat gram
+constexpr int kGramPix = 256, kGramStride = kGramPix + 1;
+
+__global__ __launch_bounds__(256) void bwd_gram_kernel(const float* __restrict__ dp,
+                                                       const float* __restrict__ m,
+                                                       float* __restrict__ part, int C,
+                                                       long long hw, long long npix,
+                                                       long long chunk, int accumulate) {
+    extern __shared__ float lds[];
+    float* sp = lds;                       // [C][kGramStride]
+    float* sm = lds + C * kGramStride;     // [C][kGramStride]
+    const long long beg = (long long)blockIdx.x * chunk;
+    const long long end = beg + chunk < npix ? beg + chunk : npix;
+    const int ne = C * C;
+    float acc[3] = {0.f, 0.f, 0.f};
+    for (long long s0 = beg; s0 < end; s0 += kGramPix) {
+        __syncthreads();  // the previous pixels have been consumed
+        const long long i = s0 + threadIdx.x;
+        const bool in = i < end;
+        const long long b = in ? i / hw : 0;
+        const long long base = b * C * hw + (in ? i - b * hw : 0);
+        for (int c = 0; c < C; ++c) {
+            sp[c * kGramStride + threadIdx.x] = in ? dp[base + c * hw] : 0.f;
+            sm[c * kGramStride + threadIdx.x] = in ? m[base + c * hw] : 0.f;
+        }
+        __syncthreads();
+        const int cnt = end - s0 < kGramPix ? (int)(end - s0) : kGramPix;
+#pragma unroll
+        for (int r = 0; r < 3; ++r) {
+            const int e = threadIdx.x + 256 * r;
+            if (e < ne) {
+                const float* x = sp + (e / C) * kGramStride;
+                const float* y = sm + (e % C) * kGramStride;
+                float s = 0.f;
+                for (int j = 0; j < cnt; ++j) s = fmaf(x[j], y[j], s);
+                acc[r] += s;
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+        const int e = threadIdx.x + 256 * r;
+        if (e < ne) {
+            float* o = part + (long long)blockIdx.x * ne + e;
+            *o = accumulate ? *o + acc[r] : acc[r];
+        }
+    }
+}
+
+// ---------------------------------------------------------------- reduce
+struct ReduceArgs {
+    const float* gpart;
+    const float* kpart;
+    float* out_compat;
+    float* out_kernel;
+    int groups, C, ntiles;
+    float scale[5];
+};
+
+// Block e < C*C folds column e of gpart over its groups rows; block C*C + j
+// folds column j of kpart over its ntiles rows.  Strided per-thread sums,
+// then a tree, all in double.
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(ReduceArgs a) {
+    __shared__ double red[256];
+    const int ne = a.C * a.C;
+    const int e = blockIdx.x;
+    const bool compat = e < ne;
+    if (compat ? !a.out_compat : !a.out_kernel) return;
+    const int rows = compat ? a.groups : a.ntiles;
+    const int stride = compat ? ne : 5;
+    const float* col = compat ? a.gpart + e : a.kpart + (e - ne);
+    double s = 0.0;
+    for (int r = threadIdx.x; r < rows; r += 256) s += (double)col[(long long)r * stride];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        if (compat) a.out_compat[e] = (float)red[0];
+        else a.out_kernel[e - ne] = (float)(red[0] * (double)a.scale[e - ne]);
+    }
+}
+
+template <int K, int TH>
+hipError_t launch_msg_kt(const BwdArgs& a, hipStream_t stream) {
+    const size_t lds = bwd_lds_bytes(K, a.C, TH);
+    const dim3 block(bwd_tile_w(K) * TH);
+    if (a.m_out)
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, true>), dim3(a.ntiles), block, lds, stream, a);
+    else
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, false>), dim3(a.ntiles), block, lds, stream, a);
+    return hipGetLastError();
+}
+
+// The host derives the tiling (tiles_x, tiles_per_img, ntiles) from the
+// same bwd_tile_w / bwd_tile_h.
+template <int K>
+hipError_t launch_msg_k(const BwdArgs& a, hipStream_t stream) {
+    if (bwd_tile_h(K, a.C) == 16) {
+        if constexpr (K <= 7) return launch_msg_kt<K, 16>(a, stream);
+        return hipErrorInvalidValue;
+    }
+    return launch_msg_kt<K, 8>(a, stream);
+}
+
+}  // namespace
+
+hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream) {
+    if (a.C < 1 || a.C > kMaxC || a.ntiles <= 0) return hipErrorInvalidValue;
+    if (bwd_lds_bytes(k, a.C) > 160 * 1024) return hipErrorInvalidValue;
+    switch (k) {
+        case 1: return launch_msg_k<1>(a, stream);
+        case 3: return launch_msg_k<3>(a, stream);
+        case 5: return launch_msg_k<5>(a, stream);
+        case 7: return launch_msg_k<7>(a, stream);
+        case 9: return launch_msg_k<9>(a, stream);
+        case 11: return launch_msg_k<11>(a, stream);
+        case 13: return launch_msg_k<13>(a, stream);
+        case 15: return launch_msg_k<15>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_bwd_point(const float* q, const float* dq, const float* mu, float* du,
+                            float* dm, float* dp, int B, int C, long long HW, int accumulate,
+                            hipStream_t stream) {
+    const long long npix = (long long)B * HW;
+    if (npix == 0) return hipSuccess;
+    if (C < 1 || C > kMaxC) return hipErrorInvalidValue;
+    const long long blocks = (npix + 255) / 256;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    if (C <= 8)
+        hipLaunchKernelGGL((bwd_point_kernel<8>), dim3((unsigned)blocks), dim3(256), 0, stream,
+                           q, dq, mu, du, dm, dp, C, HW, npix, accumulate);
+    else
+        hipLaunchKernelGGL((bwd_point_kernel<kMaxC>), dim3((unsigned)blocks), dim3(256), 0,
+                           stream, q, dq, mu, du, dm, dp, C, HW, npix, accumulate);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_gram(const float* dp, const float* m, float* part, int B, int C,
+                           long long HW, int groups, int accumulate, hipStream_t stream) {
+    const long long npix = (long long)B * HW;
+    if (C < 1 || C > kMaxC || groups < 1) return hipErrorInvalidValue;
+    const long long chunk = (npix + groups - 1) / groups;
+    const size_t lds = sizeof(float) * 2 * C * kGramStride;
+    hipLaunchKernelGGL(bwd_gram_kernel, dim3(groups), dim3(256), lds, stream, dp, m, part, C, HW,
+                       npix, chunk, accumulate);
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_reduce(const float* gpart, int groups, int C, float* out_compat,
+                             const float* kpart, int ntiles, const float scale[5],
+                             float* out_kernel, hipStream_t stream) {
+    if (C < 1 || C > kMaxC) return hipErrorInvalidValue;
+    ReduceArgs a{gpart, kpart, out_compat, out_kernel, groups, C, ntiles, {}};
+    for (int j = 0; j < 5; ++j) a.scale[j] = scale[j];
+    hipLaunchKernelGGL(bwd_reduce_kernel, dim3(C * C + 5), dim3(256), 0, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace convcrf

@@ -185,6 +185,68 @@ hipError_t launch_blur_update(const float* m_pooled, const float* unary,
                               int B, int C, int H, int W, int s,
                               hipStream_t stream);
 
+// ---- reverse mode (derivative of the unpooled mean-field)
+// Arguments of one adjoint-message launch: for every pixel x of the grid,
+//   dq_out_x(l) = sum_d K(x, x+d) dm_{x+d}(l)   (the transpose of the Eq. 6
+//                 message, using K(p,q) = K(q,p) and the symmetric window)
+//   m_out_x(l)  = sum_d K(x, x+d) q_{x+d}(l)     (the forward message, when
+//                 m_out is set)
+// and the tile's sums over its pixels and taps of dk = sum_l dm_x(l) q_{x+d}(l)
+// times A, A |d|^2, A |I_x - I_{x+d}|^2, S, S |d|^2, where A and S are the
+// two Eq. 4 Gaussians without their weights, added into kpart[tile][5]
+// (written instead when `accumulate` is 0).
+struct BwdArgs {
+    const float* q;      // Q^t [B][C][H][W]
+    const float* dm;     // dL/dM^t [B][C][H][W]
+    const float* feat;   // image [B][3][H][W]
+    float* dq_out;       // dL/dQ^t [B][C][H][W]
+    float* m_out;        // M^t [B][C][H][W] or null
+    float* kpart;        // [ntiles][5]
+    int C, H, W;
+    int tiles_x, tiles_per_img, ntiles;
+    int include_center;
+    int accumulate;
+    float neg_beta;      // -log2(e) / (2 theta_beta^2)
+    float w_app, w_smooth;
+    float a_log2[kMaxN + 1];    // -n log2(e) / (2 theta_alpha^2)
+    float smooth[kMaxN + 1];    // exp(-n / (2 theta_gamma^2))
+};
+
+// Tile of the adjoint message for window side k and C classes, one pixel
+// per thread: 32 columns up to k = 7, 16 above; 16 rows where the 2C + 3
+// staged planes of tile plus halo fit the 160 KB of LDS, else 8.
+constexpr int bwd_tile_w(int k) { return k <= 7 ? 32 : 16; }
+constexpr size_t bwd_lds_bytes(int k, int C, int rows) {
+    return sizeof(float) * (size_t)(2 * C + 3) * (bwd_tile_w(k) + k - 1) * (rows + k - 1);
+}
+constexpr int bwd_tile_h(int k, int C) {
+    return k <= 7 && bwd_lds_bytes(k, C, 16) <= 160 * 1024 ? 16 : 8;
+}
+inline size_t bwd_lds_bytes(int k, int C) { return bwd_lds_bytes(k, C, bwd_tile_h(k, C)); }
+
+hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream);
+
+// Softmax, unary and compatibility adjoints of one round, per pixel:
+//   dZ = Q (dQ - <Q, dQ>);  du = dZ (+ du when accumulate);
+//   dm(l') = -sum_l mu[l][l'] dZ(l) (mu null = Potts) when dm is set;
+//   dp = -dZ when dp is set.
+// q, dq, du, dm, dp: [B][C][H][W] with HW = H * W pixels per plane.
+hipError_t launch_bwd_point(const float* q, const float* dq, const float* mu, float* du,
+                            float* dm, float* dp, int B, int C, long long HW,
+                            int accumulate, hipStream_t stream);
+
+// part[g][l * C + l'] (+)= sum over block g's pixels of dp(l) m(l'), over
+// `groups` blocks that split the B*HW pixels evenly.
+hipError_t launch_bwd_gram(const float* dp, const float* m, float* part, int B, int C,
+                           long long HW, int groups, int accumulate, hipStream_t stream);
+
+// out_compat[e] = sum_g gpart[g][e] (C*C entries, when out_compat is set);
+// out_kernel[j] = scale[j] * sum_t kpart[t][j] (5 entries, when set).
+// Sums in double, in a fixed order.
+hipError_t launch_bwd_reduce(const float* gpart, int groups, int C, float* out_compat,
+                             const float* kpart, int ntiles, const float scale[5],
+                             float* out_kernel, hipStream_t stream);
+
 // Block-to-tile order that keeps the tiles of one XCD spatially contiguous.
 // Work-groups are dispatched round-robin over the 8 XCDs of the chip, so
 // block b runs on XCD b % 8; XCD x receives the contiguous tile range that
