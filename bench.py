@@ -10,6 +10,11 @@ oracle timed on this host as a baseline.
 
     python bench.py [--steps K] [--warmup W] [--workload pascal]
                     [--variant fused|materialised|resident] [--no-cpu-baseline]
+                    [--backward]
+
+--backward times the reverse mode instead: one step = one call of
+convcrf_meanfield_backward (the forward rounds recomputed and kept, then every
+round undone, with the compatibility and kernel-parameter derivatives).
 """
 from __future__ import annotations
 
@@ -25,6 +30,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "megapixel·iterations/sec and ms per 5-iter inference (C=21, 512², k=7)"
+METRIC_BWD = ("megapixel·iterations/sec and ms per 5-iter derivative (forward recomputed, "
+              "then reversed; C=21, 512², k=7)")
 UNIT = "MP·iter/s"
 
 # MI355X: FP32 vector peak 157.3 TFLOP/s (256 CUs at 2.4 GHz, 128 FP32 FMA
@@ -92,6 +99,24 @@ def algorithmic_per_launch(kname: str, wl):
         return (5 * C + 1) * px, 8 * C * px
     if kname == "sync_reset":
         return 0, 0
+    # reverse mode (compatibility and kernel-parameter derivatives requested)
+    taps = k * k - 1
+    if kname == "bwd_message":
+        # per tap: the weight (12), dk = <dM_p, Q_q> (2C), dQ += w dM (2C),
+        # M += w Q (2C), the five parameter sums (10); reads Q^t, dM and the
+        # image, writes dQ^t and M^t
+        return (6 * C + 22) * taps * px, (16 * C + 12) * px
+    if kname == "bwd_point":
+        # T + 1 launches per call: T undo a round (dot, dZ, dU, Potts dM: 7C
+        # flops; read Q, dQ and dU except on the first, write dU, dM and -dZ),
+        # the last one only the initial softmax (5C; read Q, dQ, dU, write dU)
+        rounds = 7 * C * T + 5 * C
+        rbytes = 20 * C * T + 4 * C * (T - 1) + 16 * C
+        return rounds * px / (T + 1), rbytes * px / (T + 1)
+    if kname == "bwd_gram":
+        return 2 * C * C * px, 8 * C * px
+    if kname == "bwd_reduce":
+        return 0, 0
     raise KeyError(kname)
 
 
@@ -113,9 +138,10 @@ def load_traffic(workload: str, kernel: str):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(wl, U, I, budget_s: float = 10.0):
+def cpu_baseline(wl, U, I, budget_s: float = 10.0, backward: bool = False):
     """The oracle as it stands, on this host: the full workload, repeated
-    until `budget_s` seconds have passed (median per call)."""
+    until `budget_s` seconds have passed (median per call); with `backward`,
+    its derivative (forward recomputed, then reversed) on the same inputs."""
     import numpy as np
     import oracle
     oracle.build()
@@ -124,9 +150,13 @@ def cpu_baseline(wl, U, I, budget_s: float = 10.0):
                             w_smooth=wl.w_smooth, theta_gamma=wl.theta_gamma)
     times = []
     t_all = time.perf_counter()
+    G = np.random.default_rng(77).normal(0.0, 1.0, U.shape) if backward else None
     while True:
         t0 = time.perf_counter()
-        oracle.meanfield(U, I, p, wl.iters)
+        if backward:
+            oracle.meanfield_backward(U, I, p, wl.iters, G)
+        else:
+            oracle.meanfield(U, I, p, wl.iters)
         times.append(time.perf_counter() - t0)
         if time.perf_counter() - t_all >= budget_s or len(times) >= 50:
             break
@@ -135,8 +165,8 @@ def cpu_baseline(wl, U, I, budget_s: float = 10.0):
     return {"value": round(mpi / t, 3), "unit": UNIT, "cores": oracle.num_threads(),
             "kind": "oracle",
             "sample": f"the full {wl.name} workload ({wl.B}x{wl.C}x{wl.H}x{wl.W}, k={wl.filter_size}, "
-                      f"blur={wl.blur}, T={wl.iters}), {len(times)} calls, median "
-                      f"{t * 1e3:.1f} ms/call, double precision"}
+                      f"blur={wl.blur}, T={wl.iters}){', derivative' if backward else ''}, "
+                      f"{len(times)} calls, median {t * 1e3:.1f} ms/call, double precision"}
 
 
 def copy_reference(torch, mib: int, steps: int) -> int:
@@ -167,6 +197,8 @@ def main(argv=None):
     ap.add_argument("--workload", default="pascal")
     ap.add_argument("--variant", choices=["fused", "materialised", "resident"], default="fused")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--backward", action="store_true",
+                    help="time convcrf_meanfield_backward instead of the inference")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead: time a plain device-to-device copy of this many MiB "
                          "(reference dispatch for the FETCH_SIZE / WRITE_SIZE counters)")
@@ -198,16 +230,30 @@ def main(argv=None):
                   theta_gamma=wl.theta_gamma)
     crf = cc.ConvCRF(0)
     stream = torch.cuda.current_stream(dev)
+    if args.backward:
+        if wl.blur != 1:
+            print("bench.py: the reverse mode is built for blur = 1 only", file=sys.stderr)
+            return 2
+        import numpy as np
+        Gt = torch.from_numpy(np.random.default_rng(77).normal(
+            0.0, 1.0, U.shape).astype(np.float32)).to(dev)
+
+        def step():
+            crf.meanfield_backward(Ut, It, p, wl.iters, Gt, grad_compat=True, grad_kernel=True,
+                                   out=out, stream=stream)
+    else:
+        def step():
+            crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
 
     for _ in range(args.warmup):
-        crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
+        step()
     torch.cuda.synchronize()
     # timed pass: K steps, nothing recorded between the library's launches
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
     for _ in range(args.steps):
-        crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
+        step()
     ev1.record(stream)
     torch.cuda.synchronize()
     total_ms = ev0.elapsed_time(ev1)
@@ -218,7 +264,7 @@ def main(argv=None):
              for _ in range(args.steps)]
     for e_start, e_stop in pairs:
         e_start.record(stream)
-        crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
+        step()
         e_stop.record(stream)
     torch.cuda.synchronize()
     import numpy as np
@@ -230,7 +276,7 @@ def main(argv=None):
     # around every launch, on the launch stream
     crf.profile_enable(True)
     for _ in range(args.steps):
-        crf.meanfield(Ut, It, p, wl.iters, out=out, stream=stream)
+        step()
     torch.cuda.synchronize()
 
     # per-kernel time of the K calls; the dominant kernel is the one with the
@@ -268,19 +314,23 @@ def main(argv=None):
     })
 
     rec = {
-        "metric": METRIC, "value": round(value, 2), "unit": UNIT, "n_gpus": 1,
+        "metric": METRIC_BWD if args.backward else METRIC, "value": round(value, 2),
+        "unit": UNIT, "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
         "ms_per_call_distribution": dist,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded Voronoi images and noisy unaries)",
         "config": {"workload": f"{wl.name}: B={wl.B} C={wl.C} {wl.H}x{wl.W} k={wl.filter_size} "
-                               f"blur={wl.blur} T={wl.iters} Potts, {args.variant}",
-                   "global_batch": wl.B, "variant": args.variant},
+                               f"blur={wl.blur} T={wl.iters} Potts, "
+                               + ("derivative (dU, dmu, d kernel parameters)" if args.backward
+                                  else args.variant),
+                   "global_batch": wl.B, "variant": args.variant,
+                   "direction": "backward" if args.backward else "forward"},
         "roofline": roof,
     }
     crf.close()
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(wl, U, I)
+        rec["cpu_baseline"] = cpu_baseline(wl, U, I, backward=args.backward)
     print(json.dumps(rec), flush=True)
     return 0
 

@@ -682,7 +682,8 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     const long long ntiles_ll = (long long)((W + tw - 1) / tw) * ((H + th - 1) / th) * B;
     if (ntiles_ll > 0x7fffffffLL) return fail(ctx, CONVCRF_E_UNSUPPORTED, "too many tiles");
     const int ntiles = (int)ntiles_ll;
-    const int groups = (int)std::min<long long>(1024, std::max<long long>(1, (npix + 1023) / 1024));
+    // Gram blocks: about 512 pixels each (8 per lane), at most 2048 blocks
+    const int groups = (int)std::min<long long>(2048, std::max<long long>(1, (npix + 511) / 512));
     const bool run = npix > 0 && iters > 0;
     if (npix == 0) {
         if (grad_compat || grad_kernel)   // nothing to sum: zeros

@@ -67,11 +67,13 @@ __global__ __launch_bounds__(256) void bwd_point_kernel(
 }
 
 // ---------------------------------------------------------- adjoint message
-template <int K, int TH, bool WM>
+// CM >= C classes are computed without branches: planes past C - 1 read
+// plane C - 1 again and are never stored, and their dL/dM is zero, so they
+// add nothing to dk.
+template <int K, int TH, int CM, bool WM>
 __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) {
     constexpr int TW = bwd_tile_w(K), NT = TW * TH;
     constexpr int R = (K - 1) / 2, LW = TW + K - 1, LH = TH + K - 1, PL = LW * LH;
-    constexpr int CM = kMaxC;
     extern __shared__ float lds[];
     __shared__ float red[5][NT / 64];
     const int C = a.C;
@@ -111,15 +113,17 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
         const int oc = (ly + R) * LW + lx + R;
         const float ir = sc[oc], ig = sc[PL + oc], ib = sc[2 * PL + oc];
         float dmq[CM], dqa[CM], ma[CM];
+        int poff[CM];
 #pragma unroll
         for (int c = 0; c < CM; ++c) {
-            dmq[c] = c < C ? sm[c * PL + oc] : 0.f;
+            poff[c] = (c < C ? c : C - 1) * PL;
+            dmq[c] = c < C ? sm[poff[c] + oc] : 0.f;
             dqa[c] = 0.f;
             ma[c] = 0.f;
         }
 #pragma unroll 1
         for (int dy = -R; dy <= R; ++dy) {
-#pragma unroll 1
+#pragma unroll (K <= 7 ? K : 1)
             for (int dx = -R; dx <= R; ++dx) {
                 if (dx == 0 && dy == 0 && !a.include_center) continue;
                 const int o = oc + dy * LW + dx;
@@ -132,12 +136,10 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
                 float dk = 0.f;
 #pragma unroll
                 for (int c = 0; c < CM; ++c) {
-                    if (c < C) {
-                        const float qn = sq[c * PL + o];
-                        dk = fmaf(dmq[c], qn, dk);
-                        dqa[c] = fmaf(w, sm[c * PL + o], dqa[c]);
-                        if (WM) ma[c] = fmaf(w, qn, ma[c]);
-                    }
+                    const float qn = sq[poff[c] + o];
+                    dk = fmaf(dmq[c], qn, dk);
+                    dqa[c] = fmaf(w, sm[poff[c] + o], dqa[c]);
+                    if (WM) ma[c] = fmaf(w, qn, ma[c]);
                 }
                 const float da = dk * av, ds = dk * sv;
                 g0 += da;
@@ -176,50 +178,78 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
 }
 
 // ------------------------------------------------------------ compat gram
-constexpr int kGramPix = 256, kGramStride = kGramPix + 1;
+// Four waves per block; wave w holds the accumulators of columns l' in
+// [6w, 6w + 6) for every row l (24 x 6 registers per lane), and its lanes
+// walk the block's pixels 64 apart, reading dp and m straight from memory
+// (consecutive lanes, consecutive pixels).  The lanes' sums are folded by a
+// shuffle tree at the end.
+constexpr int kGramCols = 6;
 
 __global__ __launch_bounds__(256) void bwd_gram_kernel(const float* __restrict__ dp,
                                                        const float* __restrict__ m,
                                                        float* __restrict__ part, int C,
                                                        long long hw, long long npix,
                                                        long long chunk, int accumulate) {
-    extern __shared__ float lds[];
-    float* sp = lds;                       // [C][kGramStride]
-    float* sm = lds + C * kGramStride;     // [C][kGramStride]
+    constexpr int CM = kMaxC;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int c0 = wave * kGramCols;
     const long long beg = (long long)blockIdx.x * chunk;
     const long long end = beg + chunk < npix ? beg + chunk : npix;
-    const int ne = C * C;
-    float acc[3] = {0.f, 0.f, 0.f};
-    for (long long s0 = beg; s0 < end; s0 += kGramPix) {
-        __syncthreads();  // the previous pixels have been consumed
-        const long long i = s0 + threadIdx.x;
-        const bool in = i < end;
-        const long long b = in ? i / hw : 0;
-        const long long base = b * C * hw + (in ? i - b * hw : 0);
-        for (int c = 0; c < C; ++c) {
-            sp[c * kGramStride + threadIdx.x] = in ? dp[base + c * hw] : 0.f;
-            sm[c * kGramStride + threadIdx.x] = in ? m[base + c * hw] : 0.f;
-        }
-        __syncthreads();
-        const int cnt = end - s0 < kGramPix ? (int)(end - s0) : kGramPix;
+    float acc[CM][kGramCols];
 #pragma unroll
-        for (int r = 0; r < 3; ++r) {
-            const int e = threadIdx.x + 256 * r;
-            if (e < ne) {
-                const float* x = sp + (e / C) * kGramStride;
-                const float* y = sm + (e % C) * kGramStride;
-                float s = 0.f;
-                for (int j = 0; j < cnt; ++j) s = fmaf(x[j], y[j], s);
-                acc[r] += s;
+    for (int l = 0; l < CM; ++l)
+#pragma unroll
+        for (int j = 0; j < kGramCols; ++j) acc[l][j] = 0.f;
+    if (c0 < C && beg + lane < end) {
+        // the lane's pixels i = beg + lane + 64 n, as image b and offset j
+        // within it (the division once, then steps of 64 with a wrap)
+        long long b = (beg + lane) / hw;
+        long long j = beg + lane - b * hw;
+        const int cl = c0 + kGramCols <= C ? kGramCols : C - c0;  // columns held
+        auto step = [&](long long& bb, long long& jj) {
+            jj += 64;
+            while (jj >= hw) { jj -= hw; ++bb; }
+        };
+        for (long long i = beg + lane; i < end; i += 128) {
+            // two pixels in flight: i and i + 64 (the second may be past end)
+            long long b2 = b, j2 = j;
+            step(b2, j2);
+            const bool two = i + 64 < end;
+            const long long p1 = b * C * hw + j, p2 = two ? b2 * C * hw + j2 : p1;
+            float x1[CM], x2[CM], y1[kGramCols], y2[kGramCols];
+#pragma unroll
+            for (int l = 0; l < CM; ++l) {
+                const int lc = l < C ? l : C - 1;
+                x1[l] = l < C ? dp[p1 + lc * hw] : 0.f;
+                x2[l] = l < C && two ? dp[p2 + lc * hw] : 0.f;
             }
+#pragma unroll
+            for (int t = 0; t < kGramCols; ++t) {
+                const int tc = c0 + (t < cl ? t : cl - 1);
+                y1[t] = m[p1 + tc * hw];
+                y2[t] = m[p2 + tc * hw];
+            }
+#pragma unroll
+            for (int l = 0; l < CM; ++l)
+#pragma unroll
+                for (int t = 0; t < kGramCols; ++t)
+                    acc[l][t] = fmaf(x2[l], y2[t], fmaf(x1[l], y1[t], acc[l][t]));
+            b = b2;
+            j = j2;
+            step(b, j);
         }
     }
+    const long long ne = (long long)C * C;
 #pragma unroll
-    for (int r = 0; r < 3; ++r) {
-        const int e = threadIdx.x + 256 * r;
-        if (e < ne) {
-            float* o = part + (long long)blockIdx.x * ne + e;
-            *o = accumulate ? *o + acc[r] : acc[r];
+    for (int l = 0; l < CM; ++l) {
+#pragma unroll
+        for (int j = 0; j < kGramCols; ++j) {
+            float v = acc[l][j];
+            for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+            if (lane == 0 && l < C && c0 + j < C) {
+                float* o = part + (long long)blockIdx.x * ne + l * C + c0 + j;
+                *o = accumulate ? *o + v : v;
+            }
         }
     }
 }
@@ -260,15 +290,23 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(ReduceArgs a) {
     }
 }
 
-template <int K, int TH>
-hipError_t launch_msg_kt(const BwdArgs& a, hipStream_t stream) {
+template <int K, int TH, int CM>
+hipError_t launch_msg_ktc(const BwdArgs& a, hipStream_t stream) {
     const size_t lds = bwd_lds_bytes(K, a.C, TH);
     const dim3 block(bwd_tile_w(K) * TH);
     if (a.m_out)
-        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, true>), dim3(a.ntiles), block, lds, stream, a);
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, true>), dim3(a.ntiles), block, lds, stream,
+                           a);
     else
-        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, false>), dim3(a.ntiles), block, lds, stream, a);
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, false>), dim3(a.ntiles), block, lds, stream,
+                           a);
     return hipGetLastError();
+}
+
+template <int K, int TH>
+hipError_t launch_msg_kt(const BwdArgs& a, hipStream_t stream) {
+    if (a.C <= 8) return launch_msg_ktc<K, TH, 8>(a, stream);
+    return launch_msg_ktc<K, TH, kMaxC>(a, stream);
 }
 
 // The host derives the tiling (tiles_x, tiles_per_img, ntiles) from the
@@ -322,8 +360,7 @@ hipError_t launch_bwd_gram(const float* dp, const float* m, float* part, int B, 
     const long long npix = (long long)B * HW;
     if (C < 1 || C > kMaxC || groups < 1) return hipErrorInvalidValue;
     const long long chunk = (npix + groups - 1) / groups;
-    const size_t lds = sizeof(float) * 2 * C * kGramStride;
-    hipLaunchKernelGGL(bwd_gram_kernel, dim3(groups), dim3(256), lds, stream, dp, m, part, C, HW,
+    hipLaunchKernelGGL(bwd_gram_kernel, dim3(groups), dim3(256), 0, stream, dp, m, part, C, HW,
                        npix, chunk, accumulate);
     return hipGetLastError();
 }
