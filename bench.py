@@ -103,9 +103,9 @@ def algorithmic_per_launch(kname: str, wl):
     taps = k * k - 1
     if kname == "bwd_message":
         # per tap: the weight (12), dk = <dM_p, Q_q> (2C), dQ += w dM (2C),
-        # M += w Q (2C), the five parameter sums (10); reads Q^t, dM and the
-        # image, writes dQ^t and M^t
-        return (6 * C + 22) * taps * px, (16 * C + 12) * px
+        # M += w Q (2C), the five parameter sums (10); per pixel the outer
+        # product dP M^T (2C^2); reads Q^t, dM, dP and the image, writes dQ^t
+        return (6 * C + 22) * taps * px + 2 * C * C * px, (16 * C + 12) * px
     if kname == "bwd_point":
         # T + 1 launches per call: T undo a round (dot, dZ, dU, Potts dM: 7C
         # flops; read Q, dQ and dU except on the first, write dU, dM and -dZ),
@@ -113,8 +113,6 @@ def algorithmic_per_launch(kname: str, wl):
         rounds = 7 * C * T + 5 * C
         rbytes = 20 * C * T + 4 * C * (T - 1) + 16 * C
         return rounds * px / (T + 1), rbytes * px / (T + 1)
-    if kname == "bwd_gram":
-        return 2 * C * C * px, 8 * C * px
     if kname == "bwd_reduce":
         return 0, 0
     raise KeyError(kname)

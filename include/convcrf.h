@@ -165,8 +165,9 @@ convcrf_status convcrf_meanfield(convcrf_ctx *ctx, const float *unary,
  * params must be those of the forward call); `variant` is ignored.
  * unary, image, grad_q: DEVICE pointers, as for convcrf_meanfield; grad_q
  * [B][C][H][W].  grad_unary must not overlap unary, image or grad_q.
- * The context's workspace grows by (iters + 1) + 4 buffers of [B][C][H][W]
- * floats (Q^0..Q^T, two for dL/dQ, dL/dM, and with grad_compat two more).
+ * The context's workspace grows by (iters + 1) + 3 buffers of [B][C][H][W]
+ * floats (Q^0..Q^T, two for dL/dQ, dL/dM), one more with grad_compat, and
+ * per-tile partial sums.
  * Returns CONVCRF_E_UNSUPPORTED for blur != 1 or when the window and classes
  * exceed the LDS of one work-group (2C + 3 planes of the tile plus halo);
  * otherwise as convcrf_meanfield.  Asynchronous on `stream`. */
@@ -186,8 +187,8 @@ convcrf_status convcrf_profile_enable(convcrf_ctx *ctx, int enable);
 /* Total elapsed milliseconds and launch count of the kernels named `name`
  * ("fused_iter", "fused_resident", "sync_reset", "softmax", "build_kernel",
  * "materialised_iter", "blur_pool", "blur_message", "blur_update", and for
- * convcrf_meanfield_backward "bwd_point", "bwd_message", "bwd_gram",
- * "bwd_reduce" besides the forward's) since profiling was enabled.  "fused_resident" is one launch running all
+ * convcrf_meanfield_backward "bwd_point", "bwd_message", "bwd_reduce"
+ * besides the forward's) since profiling was enabled.  "fused_resident" is one launch running all
  * iterations of a call (CONVCRF_VARIANT_RESIDENT); "fused_iter" one
  * iteration.
  * Synchronises on the recorded events.  An unknown or unused name gives

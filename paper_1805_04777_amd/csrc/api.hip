@@ -26,10 +26,10 @@ constexpr size_t kLdsLimit = 160 * 1024;  // gfx950 LDS per work-group
 const char* const kKernelNames[] = {"fused_iter",   "softmax",      "build_kernel",
                                     "materialised_iter", "blur_pool", "blur_message",
                                     "blur_update",  "fused_resident", "sync_reset",
-                                    "bwd_point", "bwd_message", "bwd_gram", "bwd_reduce"};
+                                    "bwd_point", "bwd_message", "bwd_reduce"};
 enum KernelId {
     kFused = 0, kSoftmax, kBuild, kMatIter, kPool, kBlurMsg, kBlurUpd, kResident, kSyncReset,
-    kBwdPoint, kBwdMsg, kBwdGram, kBwdReduce, kNumKernels
+    kBwdPoint, kBwdMsg, kBwdReduce, kNumKernels
 };
 
 struct DevBuf {
@@ -52,8 +52,8 @@ struct convcrf_ctx {
     bool coop = false;              // cooperative launches supported
     std::string err = "no error";
     DevBuf q_ws, q_ws2, kmat, pool_q, pool_m, pool_f, mu, sync;
-    // reverse mode: Q^0..Q^T, dL/dQ ping-pong, dL/dM, -dL/dZ, M^t, partial sums
-    DevBuf b_q, b_dq, b_dm, b_dp, b_m, b_gpart, b_kpart;
+    // reverse mode: Q^0..Q^T, dL/dQ ping-pong, dL/dM, -dL/dZ, per-tile sums
+    DevBuf b_q, b_dq, b_dm, b_dp, b_gpart, b_kpart;
     std::vector<float> mu_last;   // host copy of the uploaded compatibility
     float* mu_pinned = nullptr;   // pinned staging for the upload
     size_t mu_pinned_cap = 0;
@@ -401,7 +401,7 @@ void convcrf_destroy(convcrf_ctx* ctx) {
     (void)hipDeviceSynchronize();
     for (DevBuf* b : {&ctx->q_ws, &ctx->q_ws2, &ctx->kmat, &ctx->pool_q, &ctx->pool_m,
                       &ctx->pool_f, &ctx->mu, &ctx->sync, &ctx->b_q, &ctx->b_dq, &ctx->b_dm,
-                      &ctx->b_dp, &ctx->b_m, &ctx->b_gpart, &ctx->b_kpart})
+                      &ctx->b_dp, &ctx->b_gpart, &ctx->b_kpart})
         if (b->p) (void)hipFree(b->p);
     if (ctx->mu_pinned) (void)hipHostFree(ctx->mu_pinned);
     if (ctx->mu_copied) (void)hipEventDestroy(ctx->mu_copied);
@@ -682,8 +682,6 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     const long long ntiles_ll = (long long)((W + tw - 1) / tw) * ((H + th - 1) / th) * B;
     if (ntiles_ll > 0x7fffffffLL) return fail(ctx, CONVCRF_E_UNSUPPORTED, "too many tiles");
     const int ntiles = (int)ntiles_ll;
-    // Gram blocks: about 512 pixels each (8 per lane), at most 2048 blocks
-    const int groups = (int)std::min<long long>(2048, std::max<long long>(1, (npix + 511) / 512));
     const bool run = npix > 0 && iters > 0;
     if (npix == 0) {
         if (grad_compat || grad_kernel)   // nothing to sum: zeros
@@ -707,8 +705,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         if ((st = ensure(ctx, ctx->b_dm, slice)) != CONVCRF_OK) return st;
         if (grad_compat) {
             if ((st = ensure(ctx, ctx->b_dp, slice)) != CONVCRF_OK) return st;
-            if ((st = ensure(ctx, ctx->b_m, slice)) != CONVCRF_OK) return st;
-            if ((st = ensure(ctx, ctx->b_gpart, sizeof(float) * (size_t)groups * C * C)) !=
+            if ((st = ensure(ctx, ctx->b_gpart, sizeof(float) * (size_t)ntiles * C * C)) !=
                 CONVCRF_OK)
                 return st;
         }
@@ -768,8 +765,9 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     }
     ba.dm = static_cast<const float*>(ctx->b_dm.p);
     ba.kpart = static_cast<float*>(ctx->b_kpart.p);
-    ba.m_out = grad_compat ? static_cast<float*>(ctx->b_m.p) : nullptr;
     float* dp = grad_compat ? static_cast<float*>(ctx->b_dp.p) : nullptr;
+    ba.dp = dp;
+    ba.gpart = grad_compat ? static_cast<float*>(ctx->b_gpart.p) : nullptr;
     float* dm = static_cast<float*>(ctx->b_dm.p);
     const float* dq = grad_q;
     for (int t = iters - 1; t >= 0; --t) {
@@ -785,13 +783,6 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         st = launch(ctx, kBwdMsg, stream, "bwd_message",
                     [&] { return launch_bwd_message(ba, k, stream); });
         if (st != CONVCRF_OK) return st;
-        if (grad_compat) {
-            st = launch(ctx, kBwdGram, stream, "bwd_gram", [&] {
-                return launch_bwd_gram(dp, ba.m_out, static_cast<float*>(ctx->b_gpart.p), B, C,
-                                       (long long)H * W, groups, acc, stream);
-            });
-            if (st != CONVCRF_OK) return st;
-        }
         dq = ba.dq_out;
     }
     // Q^0 = softmax(U)
@@ -802,7 +793,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     if (st != CONVCRF_OK) return st;
     if (grad_compat || grad_kernel)
         return launch(ctx, kBwdReduce, stream, "bwd_reduce", [&] {
-            return launch_bwd_reduce(static_cast<const float*>(ctx->b_gpart.p), run ? groups : 0,
+            return launch_bwd_reduce(static_cast<const float*>(ctx->b_gpart.p), run ? ntiles : 0,
                                      C, grad_compat, static_cast<const float*>(ctx->b_kpart.p),
                                      run ? ntiles : 0, scale, grad_kernel, stream);
         });

@@ -10,9 +10,9 @@
 //                      message itself applied to dL/dM.  The same pass sums
 //                      the derivative with respect to the Eq. 4 parameters
 //                      and, when the compatibility derivative is wanted,
-//                      recomputes the forward message M^t.
-// bwd_gram_kernel accumulates sum_p dP_p(l) M_p(l') for the compatibility
-// derivative and bwd_reduce_kernel folds the per-block partial sums.
+//                      recomputes the forward message M^t and sums
+//                      dP_p(l) M_p(l') over the tile's pixels.
+// bwd_reduce_kernel folds the per-tile partial sums.
 #include "crf_internal.h"
 
 namespace convcrf {
@@ -109,21 +109,24 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
     const int lx = threadIdx.x % TW, ly = threadIdx.x / TW;
     const int px = tx * TW + lx, py = ty * TH + ly;
     float g0 = 0.f, g1 = 0.f, g2 = 0.f, g3 = 0.f, g4 = 0.f;
+    float ma[CM];   // the forward message of the pixel (compatibility derivative)
+#pragma unroll
+    for (int c = 0; c < CM; ++c) ma[c] = 0.f;
     if (px < a.W && py < a.H) {
         const int oc = (ly + R) * LW + lx + R;
         const float ir = sc[oc], ig = sc[PL + oc], ib = sc[2 * PL + oc];
-        float dmq[CM], dqa[CM], ma[CM];
+        float dmq[CM], dqa[CM];
         int poff[CM];
 #pragma unroll
         for (int c = 0; c < CM; ++c) {
             poff[c] = (c < C ? c : C - 1) * PL;
             dmq[c] = c < C ? sm[poff[c] + oc] : 0.f;
             dqa[c] = 0.f;
-            ma[c] = 0.f;
         }
+        constexpr int kRowUnroll = K <= 7 ? K : 1;   // a window row at once
 #pragma unroll 1
         for (int dy = -R; dy <= R; ++dy) {
-#pragma unroll (K <= 7 ? K : 1)
+#pragma unroll kRowUnroll
             for (int dx = -R; dx <= R; ++dx) {
                 if (dx == 0 && dy == 0 && !a.include_center) continue;
                 const int o = oc + dy * LW + dx;
@@ -151,10 +154,64 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
         }
         const long long pix = (long long)b * C * hw + (long long)py * a.W + px;
 #pragma unroll
+        for (int c = 0; c < CM; ++c)
+            if (c < C) a.dq_out[pix + c * hw] = dqa[c];
+    }
+    if constexpr (WM) {
+        // the tile's sum of dp_x(l) M_x(l'): dp and M of its pixels go to
+        // LDS (zero for pixels outside the image and rows past C), then each
+        // thread sums one 3 x 3 block of (l, l') over one group of pixels
+        constexpr int SP = NT + 1;
+        const int CP = bwd_gram_rows(C);
+        float* gp = lds;
+        float* gm = lds + CP * SP;
+        __syncthreads();  // the staged planes have been read
+        const bool in = px < a.W && py < a.H;
+        const long long pix = (long long)b * C * hw + (long long)py * a.W + px;
+#pragma unroll
         for (int c = 0; c < CM; ++c) {
-            if (c < C) {
-                a.dq_out[pix + c * hw] = dqa[c];
-                if (WM) a.m_out[pix + c * hw] = ma[c];
+            if (c < CP) {
+                gp[c * SP + threadIdx.x] = in && c < C ? a.dp[pix + c * hw] : 0.f;
+                gm[c * SP + threadIdx.x] = in && c < C ? ma[c] : 0.f;
+            }
+        }
+        for (int c = CM; c < CP; ++c) {   // rows past the held classes
+            gp[c * SP + threadIdx.x] = 0.f;
+            gm[c * SP + threadIdx.x] = 0.f;
+        }
+        __syncthreads();
+        const int nbc = CP / 3, nb = nbc * nbc;
+        const int ng = NT / nb;
+        const int bi = threadIdx.x % nb, pg = threadIdx.x / nb;
+        const int l0 = 3 * (bi / nbc), m0 = 3 * (bi % nbc);
+        float s9[9];
+#pragma unroll
+        for (int e = 0; e < 9; ++e) s9[e] = 0.f;
+        if (pg < ng) {
+            for (int x = pg; x < NT; x += ng) {
+                const float p0 = gp[l0 * SP + x], p1 = gp[(l0 + 1) * SP + x],
+                            p2 = gp[(l0 + 2) * SP + x];
+                const float q0 = gm[m0 * SP + x], q1 = gm[(m0 + 1) * SP + x],
+                            q2 = gm[(m0 + 2) * SP + x];
+                s9[0] = fmaf(p0, q0, s9[0]); s9[1] = fmaf(p0, q1, s9[1]); s9[2] = fmaf(p0, q2, s9[2]);
+                s9[3] = fmaf(p1, q0, s9[3]); s9[4] = fmaf(p1, q1, s9[4]); s9[5] = fmaf(p1, q2, s9[5]);
+                s9[6] = fmaf(p2, q0, s9[6]); s9[7] = fmaf(p2, q1, s9[7]); s9[8] = fmaf(p2, q2, s9[8]);
+            }
+        }
+        __syncthreads();  // dp and M have been read
+        float* gr = lds;   // [ng][nb][9]
+        if (pg < ng)
+#pragma unroll
+            for (int e = 0; e < 9; ++e) gr[(pg * nb + bi) * 9 + e] = s9[e];
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < nb * 9; idx += NT) {
+            float sum = 0.f;
+            for (int g = 0; g < ng; ++g) sum += gr[g * nb * 9 + idx];
+            const int blk = idx / 9, e = idx - blk * 9;
+            const int l = 3 * (blk / nbc) + e / 3, lp = 3 * (blk % nbc) + e % 3;
+            if (l < C && lp < C) {
+                float* o = a.gpart + (long long)tile * C * C + l * C + lp;
+                *o = a.accumulate ? *o + sum : sum;
             }
         }
     }
@@ -174,83 +231,6 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
         for (int w = 0; w < NT / 64; ++w) s += red[j][w];
         float* o = a.kpart + (long long)tile * 5 + j;
         *o = a.accumulate ? *o + s : s;
-    }
-}
-
-// ------------------------------------------------------------ compat gram
-// Four waves per block; wave w holds the accumulators of columns l' in
-// [6w, 6w + 6) for every row l (24 x 6 registers per lane), and its lanes
-// walk the block's pixels 64 apart, reading dp and m straight from memory
-// (consecutive lanes, consecutive pixels).  The lanes' sums are folded by a
-// shuffle tree at the end.
-constexpr int kGramCols = 6;
-
-__global__ __launch_bounds__(256) void bwd_gram_kernel(const float* __restrict__ dp,
-                                                       const float* __restrict__ m,
-                                                       float* __restrict__ part, int C,
-                                                       long long hw, long long npix,
-                                                       long long chunk, int accumulate) {
-    constexpr int CM = kMaxC;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int c0 = wave * kGramCols;
-    const long long beg = (long long)blockIdx.x * chunk;
-    const long long end = beg + chunk < npix ? beg + chunk : npix;
-    float acc[CM][kGramCols];
-#pragma unroll
-    for (int l = 0; l < CM; ++l)
-#pragma unroll
-        for (int j = 0; j < kGramCols; ++j) acc[l][j] = 0.f;
-    if (c0 < C && beg + lane < end) {
-        // the lane's pixels i = beg + lane + 64 n, as image b and offset j
-        // within it (the division once, then steps of 64 with a wrap)
-        long long b = (beg + lane) / hw;
-        long long j = beg + lane - b * hw;
-        const int cl = c0 + kGramCols <= C ? kGramCols : C - c0;  // columns held
-        auto step = [&](long long& bb, long long& jj) {
-            jj += 64;
-            while (jj >= hw) { jj -= hw; ++bb; }
-        };
-        for (long long i = beg + lane; i < end; i += 128) {
-            // two pixels in flight: i and i + 64 (the second may be past end)
-            long long b2 = b, j2 = j;
-            step(b2, j2);
-            const bool two = i + 64 < end;
-            const long long p1 = b * C * hw + j, p2 = two ? b2 * C * hw + j2 : p1;
-            float x1[CM], x2[CM], y1[kGramCols], y2[kGramCols];
-#pragma unroll
-            for (int l = 0; l < CM; ++l) {
-                const int lc = l < C ? l : C - 1;
-                x1[l] = l < C ? dp[p1 + lc * hw] : 0.f;
-                x2[l] = l < C && two ? dp[p2 + lc * hw] : 0.f;
-            }
-#pragma unroll
-            for (int t = 0; t < kGramCols; ++t) {
-                const int tc = c0 + (t < cl ? t : cl - 1);
-                y1[t] = m[p1 + tc * hw];
-                y2[t] = m[p2 + tc * hw];
-            }
-#pragma unroll
-            for (int l = 0; l < CM; ++l)
-#pragma unroll
-                for (int t = 0; t < kGramCols; ++t)
-                    acc[l][t] = fmaf(x2[l], y2[t], fmaf(x1[l], y1[t], acc[l][t]));
-            b = b2;
-            j = j2;
-            step(b, j);
-        }
-    }
-    const long long ne = (long long)C * C;
-#pragma unroll
-    for (int l = 0; l < CM; ++l) {
-#pragma unroll
-        for (int j = 0; j < kGramCols; ++j) {
-            float v = acc[l][j];
-            for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-            if (lane == 0 && l < C && c0 + j < C) {
-                float* o = part + (long long)blockIdx.x * ne + l * C + c0 + j;
-                *o = accumulate ? *o + v : v;
-            }
-        }
     }
 }
 
@@ -294,7 +274,7 @@ template <int K, int TH, int CM>
 hipError_t launch_msg_ktc(const BwdArgs& a, hipStream_t stream) {
     const size_t lds = bwd_lds_bytes(K, a.C, TH);
     const dim3 block(bwd_tile_w(K) * TH);
-    if (a.m_out)
+    if (a.gpart)
         hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, true>), dim3(a.ntiles), block, lds, stream,
                            a);
     else
@@ -352,16 +332,6 @@ hipError_t launch_bwd_point(const float* q, const float* dq, const float* mu, fl
     else
         hipLaunchKernelGGL((bwd_point_kernel<kMaxC>), dim3((unsigned)blocks), dim3(256), 0,
                            stream, q, dq, mu, du, dm, dp, C, HW, npix, accumulate);
-    return hipGetLastError();
-}
-
-hipError_t launch_bwd_gram(const float* dp, const float* m, float* part, int B, int C,
-                           long long HW, int groups, int accumulate, hipStream_t stream) {
-    const long long npix = (long long)B * HW;
-    if (C < 1 || C > kMaxC || groups < 1) return hipErrorInvalidValue;
-    const long long chunk = (npix + groups - 1) / groups;
-    hipLaunchKernelGGL(bwd_gram_kernel, dim3(groups), dim3(256), 0, stream, dp, m, part, C, HW,
-                       npix, chunk, accumulate);
     return hipGetLastError();
 }
 

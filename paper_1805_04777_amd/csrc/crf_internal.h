@@ -189,18 +189,20 @@ hipError_t launch_blur_update(const float* m_pooled, const float* unary,
 // Arguments of one adjoint-message launch: for every pixel x of the grid,
 //   dq_out_x(l) = sum_d K(x, x+d) dm_{x+d}(l)   (the transpose of the Eq. 6
 //                 message, using K(p,q) = K(q,p) and the symmetric window)
-//   m_out_x(l)  = sum_d K(x, x+d) q_{x+d}(l)     (the forward message, when
-//                 m_out is set)
 // and the tile's sums over its pixels and taps of dk = sum_l dm_x(l) q_{x+d}(l)
 // times A, A |d|^2, A |I_x - I_{x+d}|^2, S, S |d|^2, where A and S are the
-// two Eq. 4 Gaussians without their weights, added into kpart[tile][5]
-// (written instead when `accumulate` is 0).
+// two Eq. 4 Gaussians without their weights, added into kpart[tile][5];
+// when gpart is set, also the forward message M_x(l) = sum_d K(x, x+d)
+// q_{x+d}(l) and the tile's sum over its pixels of dp_x(l) M_x(l') (the
+// compatibility derivative), added into gpart[tile][l * C + l'].  Partial
+// sums are written instead of added when `accumulate` is 0.
 struct BwdArgs {
     const float* q;      // Q^t [B][C][H][W]
     const float* dm;     // dL/dM^t [B][C][H][W]
     const float* feat;   // image [B][3][H][W]
+    const float* dp;     // -dL/dZ^t [B][C][H][W] (read when gpart is set)
     float* dq_out;       // dL/dQ^t [B][C][H][W]
-    float* m_out;        // M^t [B][C][H][W] or null
+    float* gpart;        // [ntiles][C * C] or null
     float* kpart;        // [ntiles][5]
     int C, H, W;
     int tiles_x, tiles_per_img, ntiles;
@@ -215,9 +217,19 @@ struct BwdArgs {
 // Tile of the adjoint message for window side k and C classes, one pixel
 // per thread: 32 columns up to k = 7, 16 above; 16 rows where the 2C + 3
 // staged planes of tile plus halo fit the 160 KB of LDS, else 8.
+// The LDS then holds the staged planes; with the compatibility derivative it
+// is reused afterwards for the tile's dp and M, C rounded up to a multiple
+// of 3, one row of tile pixels plus one each, and for the partial sums of
+// the 3 x 3 blocks (9 per thread).
 constexpr int bwd_tile_w(int k) { return k <= 7 ? 32 : 16; }
+constexpr int bwd_gram_rows(int C) { return (C + 2) / 3 * 3; }
 constexpr size_t bwd_lds_bytes(int k, int C, int rows) {
-    return sizeof(float) * (size_t)(2 * C + 3) * (bwd_tile_w(k) + k - 1) * (rows + k - 1);
+    const size_t stage = (size_t)(2 * C + 3) * (bwd_tile_w(k) + k - 1) * (rows + k - 1);
+    const size_t nt = (size_t)bwd_tile_w(k) * rows;
+    const size_t gram = 2 * (size_t)bwd_gram_rows(C) * (nt + 1);
+    const size_t red = 9 * nt;
+    const size_t g = gram > red ? gram : red;
+    return sizeof(float) * (stage > g ? stage : g);
 }
 constexpr int bwd_tile_h(int k, int C) {
     return k <= 7 && bwd_lds_bytes(k, C, 16) <= 160 * 1024 ? 16 : 8;
@@ -235,12 +247,8 @@ hipError_t launch_bwd_point(const float* q, const float* dq, const float* mu, fl
                             float* dm, float* dp, int B, int C, long long HW,
                             int accumulate, hipStream_t stream);
 
-// part[g][l * C + l'] (+)= sum over block g's pixels of dp(l) m(l'), over
-// `groups` blocks that split the B*HW pixels evenly.
-hipError_t launch_bwd_gram(const float* dp, const float* m, float* part, int B, int C,
-                           long long HW, int groups, int accumulate, hipStream_t stream);
-
-// out_compat[e] = sum_g gpart[g][e] (C*C entries, when out_compat is set);
+// out_compat[e] = sum_g gpart[g][e] over `groups` rows (C*C entries, when
+// out_compat is set);
 // out_kernel[j] = scale[j] * sum_t kpart[t][j] (5 entries, when set).
 // Sums in double, in a fixed order.
 hipError_t launch_bwd_reduce(const float* gpart, int groups, int C, float* out_compat,
