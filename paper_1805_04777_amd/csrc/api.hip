@@ -756,6 +756,12 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     ba.tiles_per_img = ba.tiles_x * ((H + th - 1) / th);
     ba.ntiles = ntiles;
     ba.include_center = p.include_center;
+    // 16-byte staging: whole vectors per row, every plane 16-byte aligned
+    // (the image and the workspace slices; W % 4 == 0 keeps the planes so)
+    ba.vec4 = bwd_vec4_fits(k, C) && W % 4 == 0 &&
+              reinterpret_cast<uintptr_t>(image) % 16 == 0 &&
+              reinterpret_cast<uintptr_t>(ctx->b_dm.p) % 16 == 0 &&
+              reinterpret_cast<uintptr_t>(qbase) % 16 == 0;
     ba.neg_beta = (float)(-kLog2eD / (2.0 * tb * tb));
     ba.w_app = p.w_app;
     ba.w_smooth = p.w_smooth;

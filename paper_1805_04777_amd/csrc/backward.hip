@@ -67,15 +67,159 @@ __global__ __launch_bounds__(256) void bwd_point_kernel(
 }
 
 // ---------------------------------------------------------- adjoint message
-// CM >= C classes are computed without branches: planes past C - 1 read
-// plane C - 1 again and are never stored, and their dL/dM is zero, so they
-// add nothing to dk.
-template <int K, int TH, int CM, bool WM>
+
+// Tile plus halo of the 3 colour planes, the C planes of Q^t and the C
+// planes of dL/dM^t into LDS (LW x LH each, the first staged column is x0,
+// the first row y0); zero outside the image, so that taps there contribute
+// nothing to any sum.  V4: 16-byte vectors (x0 and LW multiples of 4, W a
+// multiple of 4, 16-byte aligned planes).
+template <int NT, int LW, int PL, bool V4>
+__device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b, int y0,
+                                             int x0) {
+    if constexpr (V4) {
+        constexpr int LQ = LW / 4, LH = PL / LW;
+        const int C = a.C;
+        const long long hw = (long long)a.H * a.W;
+        const float* fb = a.feat + (long long)b * 3 * hw;
+        const float* qb = a.q + (long long)b * C * hw;
+        const float* mb = a.dm + (long long)b * C * hw;
+        const int nvec = (2 * C + 3) * LH * LQ;
+#pragma unroll 8
+        for (int e = threadIdx.x; e < nvec; e += NT) {
+            const int pl = e / (LH * LQ), o = e - pl * (LH * LQ);
+            const int ly = o / LQ, lq = o - ly * LQ;
+            const int gy = y0 + ly, gx = x0 + 4 * lq;
+            const float* src = pl < 3 ? fb + pl * hw : (pl < 3 + C ? qb + (pl - 3) * hw
+                                                                   : mb + (pl - 3 - C) * hw);
+            const bool ok = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
+            const float4 v = *reinterpret_cast<const float4*>(src + (ok ? (long long)gy * a.W + gx : 0));
+            *reinterpret_cast<float4*>(lds + pl * PL + ly * LW + 4 * lq) =
+                ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        return;
+    }
+    const int C = a.C;
+    const long long hw = (long long)a.H * a.W;
+    const float* fb = a.feat + (long long)b * 3 * hw;
+    const float* qb = a.q + (long long)b * C * hw;
+    const float* mb = a.dm + (long long)b * C * hw;
+    const int nplanes = 2 * C + 3;
+    // branch-free (an in-image address is read for every element and the
+    // value dropped outside), so that many loads are in flight per thread
+#pragma unroll 16
+    for (int e = threadIdx.x; e < nplanes * PL; e += NT) {
+        const int pl = e / PL, o = e - pl * PL;
+        const int ly = o / LW, lx = o - ly * LW;
+        const int gy = y0 + ly, gx = x0 + lx;
+        const float* src = pl < 3 ? fb + pl * hw : (pl < 3 + C ? qb + (pl - 3) * hw
+                                                               : mb + (pl - 3 - C) * hw);
+        const bool ok = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
+        const float v = src[ok ? (long long)gy * a.W + gx : 0];
+        lds[e] = ok ? v : 0.f;
+    }
+}
+
+// The tile's sums of the five parameter terms over its threads, in a fixed
+// order, added into kpart[tile] (or written).
+template <int NT>
+__device__ __forceinline__ void tile_param_sums(float (&g)[5], const BwdArgs& a, int tile) {
+    __shared__ float red[5][NT / 64];
+#pragma unroll
+    for (int j = 0; j < 5; ++j)
+        for (int off = 32; off > 0; off >>= 1) g[j] += __shfl_xor(g[j], off, 64);
+    const int wave = threadIdx.x / 64;
+    if ((threadIdx.x & 63) == 0)
+#pragma unroll
+        for (int j = 0; j < 5; ++j) red[j][wave] = g[j];
+    __syncthreads();
+    if (threadIdx.x < 5) {
+        const int j = threadIdx.x;
+        float s = 0.f;
+        for (int w = 0; w < NT / 64; ++w) s += red[j][w];
+        float* o = a.kpart + (long long)tile * 5 + j;
+        *o = a.accumulate ? *o + s : s;
+    }
+}
+
+// The tile's sum of dp_x(l) M_x(l') over its NT * PX pixels, added into
+// gpart[tile] (or written).  Each thread hands in PX pixels: their forward
+// message mv, whether they lie in the image, and their offset in the
+// [B][C][H][W] planes.  dp and M go to LDS (zero for pixels outside the
+// image and rows past C), then each thread sums one 3 x 3 block of (l, l')
+// over one group of pixels, and the groups are added in order.
+template <int NT, int PX, int CM>
+__device__ __forceinline__ void tile_gram(float* lds, const BwdArgs& a, int tile,
+                                          const float (&mv)[PX][CM], const bool (&in)[PX],
+                                          const long long (&pix)[PX]) {
+    constexpr int NPIX = NT * PX, SP = NPIX + 1;
+    const int C = a.C;
+    const long long hw = (long long)a.H * a.W;
+    const int CP = bwd_gram_rows(C);
+    float* gp = lds;
+    float* gm = lds + CP * SP;
+    __syncthreads();  // the staged planes have been read
+#pragma unroll
+    for (int i = 0; i < PX; ++i) {
+        const int col = PX * threadIdx.x + i;
+#pragma unroll
+        for (int c = 0; c < CM; ++c) {
+            if (c < CP) {
+                gp[c * SP + col] = in[i] && c < C ? a.dp[pix[i] + c * hw] : 0.f;
+                gm[c * SP + col] = in[i] && c < C ? mv[i][c] : 0.f;
+            }
+        }
+        for (int c = CM; c < CP; ++c) {   // rows past the held classes
+            gp[c * SP + col] = 0.f;
+            gm[c * SP + col] = 0.f;
+        }
+    }
+    __syncthreads();
+    const int nbc = CP / 3, nb = nbc * nbc;
+    const int ng = NT / nb;
+    const int bi = threadIdx.x % nb, pg = threadIdx.x / nb;
+    const int l0 = 3 * (bi / nbc), m0 = 3 * (bi % nbc);
+    float s9[9];
+#pragma unroll
+    for (int e = 0; e < 9; ++e) s9[e] = 0.f;
+    if (pg < ng) {
+        for (int x = pg; x < NPIX; x += ng) {
+            const float p0 = gp[l0 * SP + x], p1 = gp[(l0 + 1) * SP + x],
+                        p2 = gp[(l0 + 2) * SP + x];
+            const float q0 = gm[m0 * SP + x], q1 = gm[(m0 + 1) * SP + x],
+                        q2 = gm[(m0 + 2) * SP + x];
+            s9[0] = fmaf(p0, q0, s9[0]); s9[1] = fmaf(p0, q1, s9[1]); s9[2] = fmaf(p0, q2, s9[2]);
+            s9[3] = fmaf(p1, q0, s9[3]); s9[4] = fmaf(p1, q1, s9[4]); s9[5] = fmaf(p1, q2, s9[5]);
+            s9[6] = fmaf(p2, q0, s9[6]); s9[7] = fmaf(p2, q1, s9[7]); s9[8] = fmaf(p2, q2, s9[8]);
+        }
+    }
+    __syncthreads();  // dp and M have been read
+    float* gr = lds;   // [ng][nb][9]
+    if (pg < ng)
+#pragma unroll
+        for (int e = 0; e < 9; ++e) gr[(pg * nb + bi) * 9 + e] = s9[e];
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < nb * 9; idx += NT) {
+        float sum = 0.f;
+        for (int g = 0; g < ng; ++g) sum += gr[g * nb * 9 + idx];
+        const int blk = idx / 9, e = idx - blk * 9;
+        const int l = 3 * (blk / nbc) + e / 3, lp = 3 * (blk % nbc) + e % 3;
+        if (l < C && lp < C) {
+            float* o = a.gpart + (long long)tile * C * C + l * C + lp;
+            *o = a.accumulate ? *o + sum : sum;
+        }
+    }
+}
+
+// One pixel per thread, 32 x TH tiles up to k = 7 (16 x 8 above).  CM >= C
+// classes are computed without branches: planes past C - 1 read plane C - 1 again and
+// are never stored, and their dL/dM is zero, so they add nothing to dk.
+template <int K, int TH, int CM, bool WM, bool V4>
 __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) {
     constexpr int TW = bwd_tile_w(K), NT = TW * TH;
-    constexpr int R = (K - 1) / 2, LW = TW + K - 1, LH = TH + K - 1, PL = LW * LH;
+    constexpr int R = (K - 1) / 2, LW = bwd_stage_w(K, V4), PL = LW * (TH + K - 1);
+    constexpr int XO = V4 ? 4 : R;   // staged columns left of the tile
+    static_assert(XO >= R, "vector staging needs k <= 9");
     extern __shared__ float lds[];
-    __shared__ float red[5][NT / 64];
     const int C = a.C;
     const float* sc = lds;               // 3 colour planes
     const float* sq = lds + 3 * PL;      // C planes of Q^t
@@ -84,36 +228,20 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
     const int b = tile / a.tiles_per_img;
     const int tr = tile - b * a.tiles_per_img;
     const int ty = tr / a.tiles_x, tx = tr - ty * a.tiles_x;
-    const int y0 = ty * TH - R, x0 = tx * TW - R;
     const long long hw = (long long)a.H * a.W;
-    const float* fb = a.feat + (long long)b * 3 * hw;
-    const float* qb = a.q + (long long)b * C * hw;
-    const float* mb = a.dm + (long long)b * C * hw;
-
-    // tile plus halo of every plane; zero outside the image, so that taps
-    // there contribute nothing to any sum
-    const int nplanes = 2 * C + 3;
-#pragma unroll 4
-    for (int e = threadIdx.x; e < nplanes * PL; e += NT) {
-        const int pl = e / PL, o = e - pl * PL;
-        const int ly = o / LW, lx = o - ly * LW;
-        const int gy = y0 + ly, gx = x0 + lx;
-        const float* src = pl < 3 ? fb + pl * hw : (pl < 3 + C ? qb + (pl - 3) * hw
-                                                               : mb + (pl - 3 - C) * hw);
-        float v = 0.f;
-        if (gy >= 0 && gy < a.H && gx >= 0 && gx < a.W) v = src[(long long)gy * a.W + gx];
-        lds[e] = v;
-    }
+    stage_planes<NT, LW, PL, V4>(lds, a, b, ty * TH - R, tx * TW - XO);
     __syncthreads();
 
     const int lx = threadIdx.x % TW, ly = threadIdx.x / TW;
     const int px = tx * TW + lx, py = ty * TH + ly;
-    float g0 = 0.f, g1 = 0.f, g2 = 0.f, g3 = 0.f, g4 = 0.f;
-    float ma[CM];   // the forward message of the pixel (compatibility derivative)
+    const bool in = px < a.W && py < a.H;
+    const long long pix = (long long)b * C * hw + (long long)py * a.W + px;
+    float g[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
+    float ma[1][CM];   // the forward message of the pixel (compatibility derivative)
 #pragma unroll
-    for (int c = 0; c < CM; ++c) ma[c] = 0.f;
-    if (px < a.W && py < a.H) {
-        const int oc = (ly + R) * LW + lx + R;
+    for (int c = 0; c < CM; ++c) ma[0][c] = 0.f;
+    if (in) {
+        const int oc = (ly + R) * LW + lx + XO;
         const float ir = sc[oc], ig = sc[PL + oc], ib = sc[2 * PL + oc];
         float dmq[CM], dqa[CM];
         int poff[CM];
@@ -142,162 +270,64 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
                     const float qn = sq[poff[c] + o];
                     dk = fmaf(dmq[c], qn, dk);
                     dqa[c] = fmaf(w, sm[poff[c] + o], dqa[c]);
-                    if (WM) ma[c] = fmaf(w, qn, ma[c]);
+                    if (WM) ma[0][c] = fmaf(w, qn, ma[0][c]);
                 }
                 const float da = dk * av, ds = dk * sv;
-                g0 += da;
-                g1 = fmaf(da, (float)n, g1);
-                g2 = fmaf(da, cd2, g2);
-                g3 += ds;
-                g4 = fmaf(ds, (float)n, g4);
+                g[0] += da;
+                g[1] = fmaf(da, (float)n, g[1]);
+                g[2] = fmaf(da, cd2, g[2]);
+                g[3] += ds;
+                g[4] = fmaf(ds, (float)n, g[4]);
             }
         }
-        const long long pix = (long long)b * C * hw + (long long)py * a.W + px;
 #pragma unroll
         for (int c = 0; c < CM; ++c)
             if (c < C) a.dq_out[pix + c * hw] = dqa[c];
     }
     if constexpr (WM) {
-        // the tile's sum of dp_x(l) M_x(l'): dp and M of its pixels go to
-        // LDS (zero for pixels outside the image and rows past C), then each
-        // thread sums one 3 x 3 block of (l, l') over one group of pixels
-        constexpr int SP = NT + 1;
-        const int CP = bwd_gram_rows(C);
-        float* gp = lds;
-        float* gm = lds + CP * SP;
-        __syncthreads();  // the staged planes have been read
-        const bool in = px < a.W && py < a.H;
-        const long long pix = (long long)b * C * hw + (long long)py * a.W + px;
-#pragma unroll
-        for (int c = 0; c < CM; ++c) {
-            if (c < CP) {
-                gp[c * SP + threadIdx.x] = in && c < C ? a.dp[pix + c * hw] : 0.f;
-                gm[c * SP + threadIdx.x] = in && c < C ? ma[c] : 0.f;
-            }
-        }
-        for (int c = CM; c < CP; ++c) {   // rows past the held classes
-            gp[c * SP + threadIdx.x] = 0.f;
-            gm[c * SP + threadIdx.x] = 0.f;
-        }
-        __syncthreads();
-        const int nbc = CP / 3, nb = nbc * nbc;
-        const int ng = NT / nb;
-        const int bi = threadIdx.x % nb, pg = threadIdx.x / nb;
-        const int l0 = 3 * (bi / nbc), m0 = 3 * (bi % nbc);
-        float s9[9];
-#pragma unroll
-        for (int e = 0; e < 9; ++e) s9[e] = 0.f;
-        if (pg < ng) {
-            for (int x = pg; x < NT; x += ng) {
-                const float p0 = gp[l0 * SP + x], p1 = gp[(l0 + 1) * SP + x],
-                            p2 = gp[(l0 + 2) * SP + x];
-                const float q0 = gm[m0 * SP + x], q1 = gm[(m0 + 1) * SP + x],
-                            q2 = gm[(m0 + 2) * SP + x];
-                s9[0] = fmaf(p0, q0, s9[0]); s9[1] = fmaf(p0, q1, s9[1]); s9[2] = fmaf(p0, q2, s9[2]);
-                s9[3] = fmaf(p1, q0, s9[3]); s9[4] = fmaf(p1, q1, s9[4]); s9[5] = fmaf(p1, q2, s9[5]);
-                s9[6] = fmaf(p2, q0, s9[6]); s9[7] = fmaf(p2, q1, s9[7]); s9[8] = fmaf(p2, q2, s9[8]);
-            }
-        }
-        __syncthreads();  // dp and M have been read
-        float* gr = lds;   // [ng][nb][9]
-        if (pg < ng)
-#pragma unroll
-            for (int e = 0; e < 9; ++e) gr[(pg * nb + bi) * 9 + e] = s9[e];
-        __syncthreads();
-        for (int idx = threadIdx.x; idx < nb * 9; idx += NT) {
-            float sum = 0.f;
-            for (int g = 0; g < ng; ++g) sum += gr[g * nb * 9 + idx];
-            const int blk = idx / 9, e = idx - blk * 9;
-            const int l = 3 * (blk / nbc) + e / 3, lp = 3 * (blk % nbc) + e % 3;
-            if (l < C && lp < C) {
-                float* o = a.gpart + (long long)tile * C * C + l * C + lp;
-                *o = a.accumulate ? *o + sum : sum;
-            }
-        }
+        const bool ins[1] = {in};
+        const long long pixs[1] = {pix};
+        tile_gram<NT, 1, CM>(lds, a, tile, ma, ins, pixs);
     }
-    // tile sums of the five parameter terms, in a fixed order
-    float g[5] = {g0, g1, g2, g3, g4};
-#pragma unroll
-    for (int j = 0; j < 5; ++j)
-        for (int off = 32; off > 0; off >>= 1) g[j] += __shfl_xor(g[j], off, 64);
-    const int wave = threadIdx.x / 64;
-    if ((threadIdx.x & 63) == 0)
-#pragma unroll
-        for (int j = 0; j < 5; ++j) red[j][wave] = g[j];
-    __syncthreads();
-    if (threadIdx.x < 5) {
-        const int j = threadIdx.x;
-        float s = 0.f;
-        for (int w = 0; w < NT / 64; ++w) s += red[j][w];
-        float* o = a.kpart + (long long)tile * 5 + j;
-        *o = a.accumulate ? *o + s : s;
-    }
+    tile_param_sums<NT>(g, a, tile);
 }
 
-// ---------------------------------------------------------------- reduce
-struct ReduceArgs {
-    const float* gpart;
-    const float* kpart;
-    float* out_compat;
-    float* out_kernel;
-    int groups, C, ntiles;
-    float scale[5];
-};
-
-// Block e < C*C folds column e of gpart over its groups rows; block C*C + j
-// folds column j of kpart over its ntiles rows.  Strided per-thread sums,
-// then a tree, all in double.
-__global__ __launch_bounds__(256) void bwd_reduce_kernel(ReduceArgs a) {
-    __shared__ double red[256];
-    const int ne = a.C * a.C;
-    const int e = blockIdx.x;
-    const bool compat = e < ne;
-    if (compat ? !a.out_compat : !a.out_kernel) return;
-    const int rows = compat ? a.groups : a.ntiles;
-    const int stride = compat ? ne : 5;
-    const float* col = compat ? a.gpart + e : a.kpart + (e - ne);
-    double s = 0.0;
-    for (int r = threadIdx.x; r < rows; r += 256) s += (double)col[(long long)r * stride];
-    red[threadIdx.x] = s;
-    __syncthreads();
-    for (int h = 128; h > 0; h >>= 1) {
-        if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) {
-        if (compat) a.out_compat[e] = (float)red[0];
-        else a.out_kernel[e - ne] = (float)(red[0] * (double)a.scale[e - ne]);
-    }
-}
-
-template <int K, int TH, int CM>
+template <int K, int TH, int CM, bool V4>
 hipError_t launch_msg_ktc(const BwdArgs& a, hipStream_t stream) {
-    const size_t lds = bwd_lds_bytes(K, a.C, TH);
+    const size_t lds = bwd_lds_bytes(K, a.C, TH, V4);
     const dim3 block(bwd_tile_w(K) * TH);
     if (a.gpart)
-        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, true>), dim3(a.ntiles), block, lds, stream,
-                           a);
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, true, V4>), dim3(a.ntiles), block, lds,
+                           stream, a);
     else
-        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, false>), dim3(a.ntiles), block, lds, stream,
-                           a);
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, false, V4>), dim3(a.ntiles), block, lds,
+                           stream, a);
     return hipGetLastError();
 }
 
-template <int K, int TH>
-hipError_t launch_msg_kt(const BwdArgs& a, hipStream_t stream) {
-    if (a.C <= 8) return launch_msg_ktc<K, TH, 8>(a, stream);
-    return launch_msg_ktc<K, TH, kMaxC>(a, stream);
+template <int K, int TH, int CM>
+hipError_t launch_msg_ktv(const BwdArgs& a, hipStream_t stream) {
+    if constexpr (K <= 7) {
+        if (a.vec4) return launch_msg_ktc<K, TH, CM, true>(a, stream);
+    }
+    return launch_msg_ktc<K, TH, CM, false>(a, stream);
 }
 
 // The host derives the tiling (tiles_x, tiles_per_img, ntiles) from the
-// same bwd_tile_w / bwd_tile_h.
+// same bwd_tile_w / bwd_tile_h, and vec4 from bwd_vec4_fits.
 template <int K>
 hipError_t launch_msg_k(const BwdArgs& a, hipStream_t stream) {
-    if (bwd_tile_h(K, a.C) == 16) {
-        if constexpr (K <= 7) return launch_msg_kt<K, 16>(a, stream);
-        return hipErrorInvalidValue;
+    if (a.C <= 8) {
+        if constexpr (K <= 7) return launch_msg_ktv<K, 16, 8>(a, stream);
+        else return launch_msg_ktv<K, 8, 8>(a, stream);
     }
-    return launch_msg_kt<K, 8>(a, stream);
+    if constexpr (K <= 7) {
+        if (bwd_tile_h(K, a.C) == 8) return launch_msg_ktv<K, 8, kMaxC>(a, stream);
+        if (a.C <= 21) return launch_msg_ktv<K, 16, 21>(a, stream);
+        return launch_msg_ktv<K, 16, kMaxC>(a, stream);
+    } else {
+        return launch_msg_ktv<K, 8, kMaxC>(a, stream);
+    }
 }
 
 }  // namespace
@@ -305,6 +335,7 @@ hipError_t launch_msg_k(const BwdArgs& a, hipStream_t stream) {
 hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream) {
     if (a.C < 1 || a.C > kMaxC || a.ntiles <= 0) return hipErrorInvalidValue;
     if (bwd_lds_bytes(k, a.C) > 160 * 1024) return hipErrorInvalidValue;
+    if (a.vec4 && (!bwd_vec4_fits(k, a.C) || a.W % 4 != 0)) return hipErrorInvalidValue;
     switch (k) {
         case 1: return launch_msg_k<1>(a, stream);
         case 3: return launch_msg_k<3>(a, stream);
