@@ -292,6 +292,42 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
     tile_param_sums<NT>(g, a, tile);
 }
 
+// ---------------------------------------------------------------- reduce
+struct ReduceArgs {
+    const float* gpart;
+    const float* kpart;
+    float* out_compat;
+    float* out_kernel;
+    int groups, C, ntiles;
+    float scale[5];
+};
+
+// Block e < C*C folds column e of gpart over its groups rows; block C*C + j
+// folds column j of kpart over its ntiles rows.  Strided per-thread sums,
+// then a tree, all in double.
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(ReduceArgs a) {
+    __shared__ double red[256];
+    const int ne = a.C * a.C;
+    const int e = blockIdx.x;
+    const bool compat = e < ne;
+    if (compat ? !a.out_compat : !a.out_kernel) return;
+    const int rows = compat ? a.groups : a.ntiles;
+    const int stride = compat ? ne : 5;
+    const float* col = compat ? a.gpart + e : a.kpart + (e - ne);
+    double s = 0.0;
+    for (int r = threadIdx.x; r < rows; r += 256) s += (double)col[(long long)r * stride];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        if (compat) a.out_compat[e] = (float)red[0];
+        else a.out_kernel[e - ne] = (float)(red[0] * (double)a.scale[e - ne]);
+    }
+}
+
 template <int K, int TH, int CM, bool V4>
 hipError_t launch_msg_ktc(const BwdArgs& a, hipStream_t stream) {
     const size_t lds = bwd_lds_bytes(K, a.C, TH, V4);
