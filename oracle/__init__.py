@@ -112,6 +112,15 @@ def _load():
                                         ctypes.c_int, _dp]
         lib.oracle_kernel.restype = ctypes.c_double
         lib.oracle_kernel.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.POINTER(_CParams)]
+        lib.oracle_meanfield_f.restype = ctypes.c_int
+        lib.oracle_meanfield_f.argtypes = [_dp, _dp, _dp, ctypes.c_int, ctypes.c_int,
+                                           ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                           ctypes.POINTER(_CParams), _dp, ctypes.c_int, _dp]
+        lib.oracle_meanfield_backward_f.restype = ctypes.c_int
+        lib.oracle_meanfield_backward_f.argtypes = [_dp, _dp, _dp, ctypes.c_int, ctypes.c_int,
+                                                    ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                                    ctypes.POINTER(_CParams), _dp,
+                                                    ctypes.c_int, _dp, _dp, _dp, _dp, _dp]
         lib.oracle_meanfield_backward.restype = ctypes.c_int
         lib.oracle_meanfield_backward.argtypes = [_dp, _dp, ctypes.c_int, ctypes.c_int,
                                                   ctypes.c_int, ctypes.c_int,
@@ -141,48 +150,67 @@ def kernel(pos_d2: float, col_d2: float, params: OracleParams) -> float:
     return float(_load().oracle_kernel(pos_d2, col_d2, ctypes.byref(params.c())))
 
 
-def meanfield(U, I, params: OracleParams, iters: int, compat=None) -> np.ndarray:
+def _features(F, B, H, W):
+    if F is None:
+        return None, 0
+    F = _f64(F)
+    if F.ndim != 4 or F.shape[0] != B or F.shape[2:] != (H, W) or F.shape[1] < 1:
+        raise ValueError("expected features [B,d,H,W]")
+    return F, F.shape[1]
+
+
+def meanfield(U, I, params: OracleParams, iters: int, compat=None, features=None) -> np.ndarray:
     """Alg. 1: ``iters`` mean-field rounds from softmax(U).  U [B,C,H,W],
-    I [B,3,H,W]; compat = row-major C x C mu[l][l'] or None for Potts."""
+    I [B,3,H,W]; compat = row-major C x C mu[l][l'] or None for Potts;
+    features = learnable smoothness features [B,d,H,W] (the "+T" variant of
+    Sec. 4.2) or None for the positions."""
     U = _f64(U)
     I = _f64(I)
     if U.ndim != 4 or I.ndim != 4 or I.shape[1] != 3 or I.shape[0] != U.shape[0] \
             or I.shape[2:] != U.shape[2:]:
         raise ValueError("expected U [B,C,H,W] and I [B,3,H,W]")
     B, C, H, W = U.shape
+    F, d = _features(features, B, H, W)
     mu = None if compat is None else _f64(compat).reshape(C, C)
     Q = np.empty_like(U)
-    rc = _load().oracle_meanfield(_ptr(U), _ptr(I), B, C, H, W, ctypes.byref(params.c()),
-                                  None if mu is None else _ptr(mu), int(iters), _ptr(Q))
+    rc = _load().oracle_meanfield_f(_ptr(U), _ptr(I), None if F is None else _ptr(F), d,
+                                    B, C, H, W, ctypes.byref(params.c()),
+                                    None if mu is None else _ptr(mu), int(iters), _ptr(Q))
     if rc != 0:
         raise ValueError("oracle_meanfield rejected its arguments")
     return Q
 
 
-def meanfield_backward(U, I, params: OracleParams, iters: int, G, compat=None):
+def meanfield_backward(U, I, params: OracleParams, iters: int, G, compat=None,
+                       features=None):
     """Reverse-mode derivative of ``meanfield`` (no blur) for a loss whose
     derivative with respect to the returned Q is G [B,C,H,W].  Returns
     (dU [B,C,H,W], dmu [C,C], dparams [5] in PARAM_NAMES order); dmu is the
     derivative with respect to the compatibility at ``compat`` (Potts when
     None), dparams with respect to the Eq. 4 parameters; both are summed over
-    the batch."""
+    the batch.  With ``features`` [B,d,H,W] a fourth value, dL/dfeatures of
+    the same shape, is returned."""
     U = _f64(U)
     I = _f64(I)
     G = _f64(G)
     if U.ndim != 4 or G.shape != U.shape or I.shape != (U.shape[0], 3) + U.shape[2:]:
         raise ValueError("expected U, G [B,C,H,W] and I [B,3,H,W]")
     B, C, H, W = U.shape
+    F, d = _features(features, B, H, W)
     mu = None if compat is None else _f64(compat).reshape(C, C)
     dU = np.empty_like(U)
     dmu = np.empty((C, C))
     dp = np.empty(5)
-    rc = _load().oracle_meanfield_backward(_ptr(U), _ptr(I), B, C, H, W,
-                                           ctypes.byref(params.c()),
-                                           None if mu is None else _ptr(mu), int(iters),
-                                           _ptr(G), _ptr(dU), _ptr(dmu), _ptr(dp))
+    dF = None if F is None else np.empty_like(F)
+    rc = _load().oracle_meanfield_backward_f(_ptr(U), _ptr(I),
+                                             None if F is None else _ptr(F), d, B, C, H, W,
+                                             ctypes.byref(params.c()),
+                                             None if mu is None else _ptr(mu), int(iters),
+                                             _ptr(G), _ptr(dU), _ptr(dmu), _ptr(dp),
+                                             None if dF is None else _ptr(dF))
     if rc != 0:
         raise ValueError("oracle_meanfield_backward rejected its arguments")
-    return dU, dmu, dp
+    return (dU, dmu, dp) if F is None else (dU, dmu, dp, dF)
 
 
 def message(Q, I, params: OracleParams, pos_scale: float = 1.0) -> np.ndarray:

@@ -27,6 +27,10 @@
  *   - Z_p(l) = U_p(l) - sum_l' mu[l][l'] M_p(l'),  Q = softmax(Z)
  *                        (Alg. 1 compatibility, unary, normalise; Eq. 1-3)
  *     mu == NULL means Potts, mu[l][l'] = [l != l']          (Sec. 3, 4.2)
+ *   - learnable smoothness features (the "+T" variant of Sec. 4.2): when a
+ *     map F [d][H][W] is given, the smoothness Gaussian takes |F_p - F_q|^2
+ *     in place of |p - q|^2 (F initialised to the positions reproduces
+ *     Eq. 4); the appearance Gaussian keeps the positions
  *   - blur s > 1: Q and features are s x s average pooled, the message is
  *     taken on the pooled grid (positions = block centres, so pooled offsets
  *     are s times the grid offsets), then bilinearly upsampled with
@@ -58,14 +62,36 @@ int oracle_num_threads(void)
 #endif
 }
 
+/* Eq. 4 with the smoothness Gaussian on its own squared distance smo_d2
+ * (the squared position distance, or the squared distance of the learnable
+ * features of the "+T" variant). */
+static double kernel_eval(double pos_d2, double col_d2, double smo_d2, const oracle_params *p)
+{
+    double app = p->w_app * exp(-pos_d2 / (2.0 * p->theta_alpha * p->theta_alpha)
+                                - col_d2 / (2.0 * p->theta_beta * p->theta_beta));
+    double smo = p->w_smooth * exp(-smo_d2 / (2.0 * p->theta_gamma * p->theta_gamma));
+    return app + smo;
+}
+
 /* Eq. 4: the merged Gaussian kernel as a function of the squared position
  * distance (in full-resolution pixels) and the squared colour distance. */
 double oracle_kernel(double pos_d2, double col_d2, const oracle_params *p)
 {
-    double app = p->w_app * exp(-pos_d2 / (2.0 * p->theta_alpha * p->theta_alpha)
-                                - col_d2 / (2.0 * p->theta_beta * p->theta_beta));
-    double smo = p->w_smooth * exp(-pos_d2 / (2.0 * p->theta_gamma * p->theta_gamma));
-    return app + smo;
+    return kernel_eval(pos_d2, col_d2, pos_d2, p);
+}
+
+/* Squared distance of the smoothness Gaussian between pixels pi and qi of
+ * one image: the feature distance when a map F [d][HW] is given, else the
+ * squared position distance pos_d2. */
+static double smooth_d2(const double *F, int d, long HW, long pi, long qi, double pos_d2)
+{
+    if (!F) return pos_d2;
+    double acc = 0.0;
+    for (int c = 0; c < d; ++c) {
+        double t = F[c * HW + pi] - F[c * HW + qi];
+        acc += t * t;
+    }
+    return acc;
 }
 
 /* Alg. 1 initialisation and normalisation: softmax over the C classes of one
@@ -93,11 +119,12 @@ void oracle_softmax(const double *U, int C, int H, int W, double *Q)
 }
 
 /* Eq. 6 / Alg. 1 message passing for one image on an H x W grid.
- * Q, M: [C][H][W]; I: [3][H][W].  pos_scale multiplies grid offsets to give
- * the position difference in full-resolution pixels (1 without blur, s on the
- * pooled grid).  M is overwritten. */
-void oracle_message(const double *Q, const double *I, int C, int H, int W,
-                    const oracle_params *p, double pos_scale, double *M)
+ * Q, M: [C][H][W]; I: [3][H][W]; F: [d][H][W] smoothness features or NULL.
+ * pos_scale multiplies grid offsets to give the position difference in
+ * full-resolution pixels (1 without blur, s on the pooled grid).  M is
+ * overwritten. */
+static void message_f(const double *Q, const double *I, const double *F, int d, int C,
+                      int H, int W, const oracle_params *p, double pos_scale, double *M)
 {
     const int r = (p->filter_size - 1) / 2;
     const long HW = (long)H * W;
@@ -115,15 +142,22 @@ void oracle_message(const double *Q, const double *I, int C, int H, int W,
                     double dy = pos_scale * (y2 - y), dx = pos_scale * (x2 - x);
                     double col = 0.0;
                     for (int ch = 0; ch < 3; ++ch) {
-                        double d = I[ch * HW + pi] - I[ch * HW + qi];
-                        col += d * d;
+                        double e = I[ch * HW + pi] - I[ch * HW + qi];
+                        col += e * e;
                     }
-                    double kq = oracle_kernel(dy * dy + dx * dx, col, p);
+                    double pos = dy * dy + dx * dx;
+                    double kq = kernel_eval(pos, col, smooth_d2(F, d, HW, pi, qi, pos), p);
                     for (int l = 0; l < C; ++l) M[l * HW + pi] += kq * Q[l * HW + qi];
                 }
             }
         }
     }
+}
+
+void oracle_message(const double *Q, const double *I, int C, int H, int W,
+                    const oracle_params *p, double pos_scale, double *M)
+{
+    message_f(Q, I, NULL, 0, C, H, W, p, pos_scale, M);
 }
 
 /* Alg. 1 compatibility transform, unary addition and normalisation for
@@ -204,13 +238,17 @@ void oracle_upsample(const double *X, int nch, int Hp, int Wp, int s, double *Y)
  * unary addition and softmax, starting from softmax(U).  U, Q: [B][C][H][W];
  * I: [B][3][H][W] (RGB on its own 0..255 scale).  Returns 0 on success, -1 on
  * an argument the definition does not cover. */
-int oracle_meanfield(const double *U, const double *I, int B, int C, int H, int W,
-                     const oracle_params *p, const double *mu, int T, double *Q)
+/* F: learnable smoothness features [B][d][H][W], or NULL for the positions
+ * (no blur with F). */
+int oracle_meanfield_f(const double *U, const double *I, const double *F, int d, int B,
+                       int C, int H, int W, const oracle_params *p, const double *mu, int T,
+                       double *Q)
 {
     if (B < 0 || C < 1 || H < 1 || W < 1 || T < 0 || !p) return -1;
     if (p->filter_size < 1 || (p->filter_size & 1) == 0) return -1;
     const int s = p->blur;
     if (s < 1 || H % s || W % s) return -1;
+    if (F && (d < 1 || s != 1)) return -1;
     const long HW = (long)H * W;
     const int Hp = H / s, Wp = W / s;
     const long HWp = (long)Hp * Wp;
@@ -228,7 +266,7 @@ int oracle_meanfield(const double *U, const double *I, int B, int C, int H, int 
         if (s > 1) oracle_avgpool(Ib, 3, H, W, s, Ip);
         for (int t = 0; t < T; ++t) {
             if (s == 1) {
-                oracle_message(Qt, Ib, C, H, W, p, 1.0, M);
+                message_f(Qt, Ib, F ? F + (long)b * d * HW : NULL, d, C, H, W, p, 1.0, M);
             } else {
                 oracle_avgpool(Qt, C, H, W, s, Qp);
                 oracle_message(Qp, Ip, C, Hp, Wp, p, (double)s, Mp);
@@ -244,6 +282,12 @@ int oracle_meanfield(const double *U, const double *I, int B, int C, int H, int 
     free(Mp);
     free(Ip);
     return 0;
+}
+
+int oracle_meanfield(const double *U, const double *I, int B, int C, int H, int W,
+                     const oracle_params *p, const double *mu, int T, double *Q)
+{
+    return oracle_meanfield_f(U, I, NULL, 0, B, C, H, W, p, mu, T, Q);
 }
 
 /* ------------------------------------------------------------------------
@@ -263,10 +307,13 @@ int oracle_meanfield(const double *U, const double *I, int B, int C, int H, int 
  *                                dK(p,q) = sum_l dM_p(l) Q_q(l)
  *   kernel      K of Eq. 4 through its five parameters (w_app, theta_alpha,
  *               theta_beta, w_smooth, theta_gamma), with A, S the two
- *               Gaussians without their weights:
+ *               Gaussians without their weights and D the squared distance
+ *               of the smoothness Gaussian (|p-q|^2, or |F_p-F_q|^2):
  *                 dK/dw_app = A,  dK/dtheta_alpha = w_app A |p-q|^2/ta^3,
  *                 dK/dtheta_beta = w_app A |I_p-I_q|^2/tb^3,
- *                 dK/dw_smooth = S,  dK/dtheta_gamma = w_smooth S |p-q|^2/tg^3
+ *                 dK/dw_smooth = S,  dK/dtheta_gamma = w_smooth S D/tg^3
+ *               and, with learnable features, through F at both ends:
+ *                 dK/dF_p = -w_smooth S (F_p - F_q)/tg^2 = -dK/dF_q
  *   initialise  Q0 = softmax(U):  dU += Q0 (dQ0 - <Q0, dQ0>)
  * The forward rounds are recomputed first and every Q^t and M^t is kept.
  * dU [B][C][H][W] is written; dmu (C*C, row-major, the derivative with
@@ -275,18 +322,19 @@ int oracle_meanfield(const double *U, const double *I, int B, int C, int H, int 
  * Returns 0, or -1 on arguments outside the definition (blur included).
  * ------------------------------------------------------------------------ */
 
-/* dK(p,q)/d(parameter) for the five Eq. 4 parameters. */
-static void kernel_param_derivs(double pos_d2, double col_d2, const oracle_params *p,
-                                double out[5])
+/* dK(p,q)/d(parameter) for the five Eq. 4 parameters; smo_d2 is the
+ * squared distance of the smoothness Gaussian. */
+static void kernel_param_derivs(double pos_d2, double col_d2, double smo_d2,
+                                const oracle_params *p, double out[5])
 {
     const double ta = p->theta_alpha, tb = p->theta_beta, tg = p->theta_gamma;
     const double A = exp(-pos_d2 / (2.0 * ta * ta) - col_d2 / (2.0 * tb * tb));
-    const double S = exp(-pos_d2 / (2.0 * tg * tg));
+    const double S = exp(-smo_d2 / (2.0 * tg * tg));
     out[0] = A;
     out[1] = p->w_app * A * pos_d2 / (ta * ta * ta);
     out[2] = p->w_app * A * col_d2 / (tb * tb * tb);
     out[3] = S;
-    out[4] = p->w_smooth * S * pos_d2 / (tg * tg * tg);
+    out[4] = p->w_smooth * S * smo_d2 / (tg * tg * tg);
 }
 
 /* q lies in the message window of p (Eq. 6 / Alg. 1 neighbourhood). */
@@ -299,8 +347,8 @@ static int in_window(int py, int px, int qy, int qx, int r, int include_center)
 
 /* Transpose of the Eq. 6 message for one image: dQ_q(l) = sum over the
  * pixels p whose window holds q of K(p,q) dM_p(l). */
-static void message_transpose(const double *dM, const double *I, int C, int H, int W,
-                              const oracle_params *p, double *dQ)
+static void message_transpose(const double *dM, const double *I, const double *F, int d,
+                              int C, int H, int W, const oracle_params *p, double *dQ)
 {
     const int r = (p->filter_size - 1) / 2;
     const long HW = (long)H * W;
@@ -319,11 +367,12 @@ static void message_transpose(const double *dM, const double *I, int C, int H, i
                     const long pi = (long)py * W + px;
                     double col = 0.0;
                     for (int ch = 0; ch < 3; ++ch) {
-                        double d = I[ch * HW + pi] - I[ch * HW + qi];
-                        col += d * d;
+                        double e = I[ch * HW + pi] - I[ch * HW + qi];
+                        col += e * e;
                     }
                     double dy = py - qy, dx = px - qx;
-                    double kpq = oracle_kernel(dy * dy + dx * dx, col, p);
+                    double pos = dy * dy + dx * dx;
+                    double kpq = kernel_eval(pos, col, smooth_d2(F, d, HW, pi, qi, pos), p);
                     for (int l = 0; l < C; ++l) dQ[l * HW + qi] += kpq * dM[l * HW + pi];
                 }
             }
@@ -333,8 +382,9 @@ static void message_transpose(const double *dM, const double *I, int C, int H, i
 
 /* Parameter derivative of one message: sum over p, q in W(p) of
  * dK(p,q) * dK(p,q)/d(parameter), dK(p,q) = sum_l dM_p(l) Q_q(l). */
-static void message_param_grad(const double *dM, const double *Q, const double *I, int C,
-                               int H, int W, const oracle_params *p, double acc[5])
+static void message_param_grad(const double *dM, const double *Q, const double *I,
+                               const double *F, int d, int C, int H, int W,
+                               const oracle_params *p, double acc[5])
 {
     const int r = (p->filter_size - 1) / 2;
     const long HW = (long)H * W;
@@ -349,15 +399,49 @@ static void message_param_grad(const double *dM, const double *Q, const double *
                     const long qi = (long)qy * W + qx;
                     double col = 0.0;
                     for (int ch = 0; ch < 3; ++ch) {
-                        double d = I[ch * HW + pi] - I[ch * HW + qi];
-                        col += d * d;
+                        double e = I[ch * HW + pi] - I[ch * HW + qi];
+                        col += e * e;
                     }
                     double dy = qy - py, dx = qx - px;
+                    double pos = dy * dy + dx * dx;
                     double g[5];
-                    kernel_param_derivs(dy * dy + dx * dx, col, p, g);
+                    kernel_param_derivs(pos, col, smooth_d2(F, d, HW, pi, qi, pos), p, g);
                     double dk = 0.0;
                     for (int l = 0; l < C; ++l) dk += dM[l * HW + pi] * Q[l * HW + qi];
                     for (int j = 0; j < 5; ++j) acc[j] += dk * g[j];
+                }
+            }
+        }
+    }
+}
+
+/* Feature derivative of one message ("+T" variant): for every pixel p and
+ * window neighbour q, dk(p,q) = sum_l dM_p(l) Q_q(l) times dK/dF_p is added
+ * into dF_p and times dK/dF_q = -dK/dF_p into dF_q. */
+static void message_feature_grad(const double *dM, const double *Q, const double *F, int d,
+                                 int C, int H, int W, const oracle_params *p, double *dF)
+{
+    const int r = (p->filter_size - 1) / 2;
+    const long HW = (long)H * W;
+    const double tg = p->theta_gamma;
+    for (int py = 0; py < H; ++py) {
+        for (int px = 0; px < W; ++px) {
+            const long pi = (long)py * W + px;
+            for (int qy = py - r; qy <= py + r; ++qy) {
+                if (qy < 0 || qy >= H) continue;
+                for (int qx = px - r; qx <= px + r; ++qx) {
+                    if (qx < 0 || qx >= W) continue;
+                    if (!in_window(py, px, qy, qx, r, p->include_center)) continue;
+                    const long qi = (long)qy * W + qx;
+                    double dk = 0.0;
+                    for (int l = 0; l < C; ++l) dk += dM[l * HW + pi] * Q[l * HW + qi];
+                    const double S = exp(-smooth_d2(F, d, HW, pi, qi, 0.0) / (2.0 * tg * tg));
+                    for (int c = 0; c < d; ++c) {
+                        const double dkdfp = -p->w_smooth * S * (F[c * HW + pi] - F[c * HW + qi])
+                                             / (tg * tg);
+                        dF[c * HW + pi] += dk * dkdfp;
+                        dF[c * HW + qi] -= dk * dkdfp;
+                    }
                 }
             }
         }
@@ -373,13 +457,16 @@ static void softmax_adjoint_pixel(const double *q, const double *dq, long s, dou
     for (int l = 0; l < C; ++l) dz[l * zs] = q[l * s] * (dq[l * s] - dot);
 }
 
-int oracle_meanfield_backward(const double *U, const double *I, int B, int C, int H, int W,
-                              const oracle_params *p, const double *mu, int T,
-                              const double *G, double *dU, double *dmu, double *dparams)
+/* F: learnable smoothness features [B][d][H][W] or NULL; dF (same shape,
+ * written when F and dF are given) receives dL/dF. */
+int oracle_meanfield_backward_f(const double *U, const double *I, const double *F, int d,
+                                int B, int C, int H, int W, const oracle_params *p,
+                                const double *mu, int T, const double *G, double *dU,
+                                double *dmu, double *dparams, double *dF)
 {
     if (B < 0 || C < 1 || H < 1 || W < 1 || T < 0 || !p) return -1;
     if (p->filter_size < 1 || (p->filter_size & 1) == 0 || p->blur != 1) return -1;
-    if (C > 64) return -1;
+    if (C > 64 || (F && d < 1)) return -1;
     const long HW = (long)H * W;
     const long n = (long)C * HW;
     double *Qs = (double *)malloc(sizeof(double) * (size_t)(T + 1) * n);
@@ -394,11 +481,14 @@ int oracle_meanfield_backward(const double *U, const double *I, int B, int C, in
     for (int b = 0; b < B; ++b) {
         const double *Ub = U + (long)b * n;
         const double *Ib = I + (long)b * 3 * HW;
+        const double *Fb = F ? F + (long)b * d * HW : NULL;
+        double *dFb = F && dF ? dF + (long)b * d * HW : NULL;
         double *dUb = dU + (long)b * n;
+        if (dFb) memset(dFb, 0, sizeof(double) * (size_t)d * HW);
         /* forward, keeping every Q^t and M^t */
         oracle_softmax(Ub, C, H, W, Qs);
         for (int t = 0; t < T; ++t) {
-            oracle_message(Qs + (long)t * n, Ib, C, H, W, p, 1.0, Ms + (long)t * n);
+            message_f(Qs + (long)t * n, Ib, Fb, d, C, H, W, p, 1.0, Ms + (long)t * n);
             oracle_update(Ub, Ms + (long)t * n, mu, C, HW, Qs + (long)(t + 1) * n);
         }
         /* reverse */
@@ -432,8 +522,9 @@ int oracle_meanfield_backward(const double *U, const double *I, int B, int C, in
                         for (long i = 0; i < HW; ++i) acc += dP[l * HW + i] * Mt[lp * HW + i];
                         dmu[l * C + lp] += acc;
                     }
-            if (dparams) message_param_grad(dM, Qt, Ib, C, H, W, p, dparams);
-            message_transpose(dM, Ib, C, H, W, p, dQprev);
+            if (dparams) message_param_grad(dM, Qt, Ib, Fb, d, C, H, W, p, dparams);
+            if (dFb) message_feature_grad(dM, Qt, Fb, d, C, H, W, p, dFb);
+            message_transpose(dM, Ib, Fb, d, C, H, W, p, dQprev);
             memcpy(dQ, dQprev, sizeof(double) * n);
         }
         for (long i = 0; i < HW; ++i) {
@@ -449,4 +540,12 @@ int oracle_meanfield_backward(const double *U, const double *I, int B, int C, in
     free(dP);
     free(dM);
     return 0;
+}
+
+int oracle_meanfield_backward(const double *U, const double *I, int B, int C, int H, int W,
+                              const oracle_params *p, const double *mu, int T,
+                              const double *G, double *dU, double *dmu, double *dparams)
+{
+    return oracle_meanfield_backward_f(U, I, NULL, 0, B, C, H, W, p, mu, T, G, dU, dmu,
+                                       dparams, NULL);
 }
