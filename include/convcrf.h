@@ -104,6 +104,16 @@ typedef struct {
                                mu[l][l'] (the 1x1-convolution compatibility
                                of Sec. 4.2), or NULL for Potts
                                mu[l][l'] = [l != l'] (Sec. 3). */
+    const float *features;  /* DEVICE pointer to learnable smoothness
+                               features F [B][feature_dim][H][W], or NULL.
+                               Given, the smoothness Gaussian of Eq. 4 takes
+                               |F_p - F_q|^2 in place of |p - q|^2 (the "+T"
+                               variant of Sec. 4.2, whose features start as
+                               the pixel positions); the appearance Gaussian
+                               keeps the positions.  blur must be 1; the
+                               variant field is ignored (one kernel computes
+                               it, weights recomputed per pixel and tap). */
+    int32_t feature_dim;    /* D, 1 <= D <= 4, with features */
 } convcrf_params;
 
 typedef struct convcrf_ctx convcrf_ctx;
@@ -111,7 +121,8 @@ typedef struct convcrf_ctx convcrf_ctx;
 /* Fill *p with the defaults used throughout the paper's experiments (Sec. 5:
  * the DenseCRF hand-crafted kernel): k = 7, no blur, centre excluded, fused,
  * w_app = 10, theta_alpha = 80, theta_beta = 13, w_smooth = 3,
- * theta_gamma = 3, Potts.  Returns CONVCRF_E_INVALID_ARG if p is NULL. */
+ * theta_gamma = 3, Potts, no learnable features.  Returns
+ * CONVCRF_E_INVALID_ARG if p is NULL. */
 convcrf_status convcrf_default_params(convcrf_params *p);
 
 /* Check sizes and parameters exactly as convcrf_meanfield does, without a
@@ -156,11 +167,15 @@ convcrf_status convcrf_meanfield(convcrf_ctx *ctx, const float *unary,
  *   grad_kernel [5]           dL/d(w_app, theta_alpha, theta_beta, w_smooth,
  *                             theta_gamma) of Eq. 4, summed over the batch
  *                                                         (DEVICE or NULL)
+ *   grad_features [B][D][H][W] dL/dF for params->features (DEVICE or NULL;
+ *                             ignored without features)
  * Each round of Alg. 1 is undone in reverse order: the softmax adjoint
  * dZ = Q (dQ - <Q, dQ>), dU += dZ, the compatibility transposed, and the
  * message transposed, which is the message itself applied to dL/dM because
  * K(p,q) = K(q,p) and the window is symmetric; the kernel-parameter terms are
- * sum over p and window neighbours q of (sum_l dL/dM_p(l) Q_q(l)) dK(p,q)/d.
+ * sum over p and window neighbours q of (sum_l dL/dM_p(l) Q_q(l)) dK(p,q)/d;
+ * with learnable features, dK/dF_p = -w_smooth S (F_p - F_q)/theta_gamma^2
+ * = -dK/dF_q, gathered per pixel from both ends of every pair.
  * The forward rounds are recomputed inside the call (the unaries, image and
  * params must be those of the forward call); `variant` is ignored.
  * unary, image, grad_q: DEVICE pointers, as for convcrf_meanfield; grad_q
@@ -177,7 +192,8 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx *ctx, const float *unary,
                                           const convcrf_params *params,
                                           int iters, const float *grad_q,
                                           float *grad_unary, float *grad_compat,
-                                          float *grad_kernel, void *stream);
+                                          float *grad_kernel, float *grad_features,
+                                          void *stream);
 
 /* Per-kernel timing with HIP events recorded on the launch stream around
  * every kernel the library enqueues, for measurement.  enable = 1 starts

@@ -45,7 +45,7 @@ def _units():
     for k in WINDOW_SIDES:
         units.append((os.path.join(CSRC, "iter.hip"), os.path.join(BUILD, f"iter_k{k}.o"),
                       [f"-DCRF_K={k}"]))
-    for name in ("aux", "backward", "api"):
+    for name in ("aux", "backward", "features", "api"):
         units.append((os.path.join(CSRC, f"{name}.hip"), os.path.join(BUILD, f"{name}.o"), []))
     return units
 

@@ -28,7 +28,7 @@ VARIANT_RESIDENT = 2
 
 KERNEL_NAMES = ("fused_iter", "fused_resident", "sync_reset", "softmax", "build_kernel",
                 "materialised_iter", "blur_pool", "blur_message", "blur_update",
-                "bwd_point", "bwd_message", "bwd_reduce")
+                "bwd_point", "bwd_message", "bwd_reduce", "feature_iter")
 
 EXPORTED = ("convcrf_default_params", "convcrf_validate", "convcrf_init", "convcrf_destroy",
             "convcrf_meanfield", "convcrf_meanfield_backward", "convcrf_profile_enable",
@@ -56,13 +56,16 @@ class CParams(ctypes.Structure):
         ("w_smooth", ctypes.c_float),
         ("theta_gamma", ctypes.c_float),
         ("compat", ctypes.POINTER(ctypes.c_float)),
+        ("features", ctypes.c_void_p),
+        ("feature_dim", ctypes.c_int32),
     ]
 
 
 @dataclass
 class Params:
     """Mirror of ``convcrf_params``; ``compat`` is a C x C host sequence or
-    None for Potts."""
+    None for Potts; ``features`` a contiguous float32 GPU tensor
+    [B, D, H, W] of learnable smoothness features, or None."""
     filter_size: int = 7
     blur: int = 1
     include_center: bool = False
@@ -73,12 +76,20 @@ class Params:
     w_smooth: float = 3.0
     theta_gamma: float = 3.0
     compat: object = None
+    features: object = None
     _keep: list = field(default_factory=list, repr=False, compare=False)
 
     def c(self) -> CParams:
         p = CParams(int(self.filter_size), int(self.blur), int(self.include_center),
                     int(self.variant), float(self.w_app), float(self.theta_alpha),
-                    float(self.theta_beta), float(self.w_smooth), float(self.theta_gamma), None)
+                    float(self.theta_beta), float(self.w_smooth), float(self.theta_gamma), None,
+                    None, 0)
+        if self.features is not None:
+            f = self.features
+            if f.dtype.itemsize != 4 or not f.is_cuda or not f.is_contiguous() or f.dim() != 4:
+                raise ConvCRFError(E_INVALID_ARG, "features must be a contiguous 4-D float32 GPU tensor")
+            p.features = f.data_ptr()
+            p.feature_dim = int(f.shape[1])
         if self.compat is not None:
             import numpy as np
             mu = np.ascontiguousarray(np.asarray(self.compat, dtype=np.float32).ravel())
@@ -116,7 +127,7 @@ def load_library(path: str = LIB_PATH):
     lib.convcrf_meanfield_backward.restype = st
     lib.convcrf_meanfield_backward.argtypes = [vp, vp, vp, ctypes.c_int, ctypes.c_int,
                                                ctypes.c_int, ctypes.c_int, P(CParams),
-                                               ctypes.c_int, vp, vp, vp, vp, vp]
+                                               ctypes.c_int, vp, vp, vp, vp, vp, vp]
     lib.convcrf_profile_enable.restype = st
     lib.convcrf_profile_enable.argtypes = [vp, ctypes.c_int]
     lib.convcrf_profile_read.restype = st
@@ -206,7 +217,8 @@ class ConvCRF:
                            out=None, stream=None):
         """Derivative of a loss through ``meanfield`` (no blur): returns
         (dL/dU [B,C,H,W], dL/dmu [C,C] or None, dL/d(Eq. 4 parameters) [5]
-        or None) as float32 tensors on the unary's device; ``grad_q`` is
+        or None) as float32 tensors on the unary's device, and with
+        ``params.features`` a fourth value, dL/dfeatures; ``grad_q`` is
         dL/dQ.  Enqueued on ``stream`` (default: torch's current stream)."""
         import torch
         for name, t in (("unary", unary), ("image", image), ("grad_q", grad_q)):
@@ -222,6 +234,7 @@ class ConvCRF:
             raise ConvCRFError(E_INVALID_ARG, "out must match unary")
         gmu = torch.empty((C, C), dtype=torch.float32, device=unary.device) if grad_compat else None
         gk = torch.empty(5, dtype=torch.float32, device=unary.device) if grad_kernel else None
+        gf = None if params.features is None else torch.empty_like(params.features)
         if stream is None:
             stream = torch.cuda.current_stream(unary.device)
         sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
@@ -230,8 +243,9 @@ class ConvCRF:
             self._h, unary.data_ptr(), image.data_ptr(), B, C, H, W, ctypes.byref(cp),
             int(iters), grad_q.data_ptr(), out.data_ptr(),
             gmu.data_ptr() if gmu is not None else None,
-            gk.data_ptr() if gk is not None else None, sp), self._h)
-        return out, gmu, gk
+            gk.data_ptr() if gk is not None else None,
+            gf.data_ptr() if gf is not None else None, sp), self._h)
+        return (out, gmu, gk) if gf is None else (out, gmu, gk, gf)
 
     def last_error(self) -> str:
         """The library's last message for this context."""

@@ -26,10 +26,10 @@ constexpr size_t kLdsLimit = 160 * 1024;  // gfx950 LDS per work-group
 const char* const kKernelNames[] = {"fused_iter",   "softmax",      "build_kernel",
                                     "materialised_iter", "blur_pool", "blur_message",
                                     "blur_update",  "fused_resident", "sync_reset",
-                                    "bwd_point", "bwd_message", "bwd_reduce"};
+                                    "bwd_point", "bwd_message", "bwd_reduce", "feature_iter"};
 enum KernelId {
     kFused = 0, kSoftmax, kBuild, kMatIter, kPool, kBlurMsg, kBlurUpd, kResident, kSyncReset,
-    kBwdPoint, kBwdMsg, kBwdReduce, kNumKernels
+    kBwdPoint, kBwdMsg, kBwdReduce, kFeatIter, kNumKernels
 };
 
 struct DevBuf {
@@ -53,7 +53,7 @@ struct convcrf_ctx {
     std::string err = "no error";
     DevBuf q_ws, q_ws2, kmat, pool_q, pool_m, pool_f, mu, sync;
     // reverse mode: Q^0..Q^T, dL/dQ ping-pong, dL/dM, -dL/dZ, per-tile sums
-    DevBuf b_q, b_dq, b_dm, b_dp, b_gpart, b_kpart;
+    DevBuf b_q, b_dq, b_dm, b_dp, b_gpart, b_kpart, b_df;
     std::vector<float> mu_last;   // host copy of the uploaded compatibility
     float* mu_pinned = nullptr;   // pinned staging for the upload
     size_t mu_pinned_cap = 0;
@@ -108,6 +108,14 @@ convcrf_status validate(convcrf_ctx* ctx, int B, int C, int H, int W, const conv
         return fail(ctx, CONVCRF_E_UNSUPPORTED, "H and W must be multiples of the blur factor");
     if (s > 1 && (H / s > 65535 || B > 65535))
         return fail(ctx, CONVCRF_E_UNSUPPORTED, "blur grid: H / blur and B must be at most 65535");
+    if (p->features) {
+        if (p->feature_dim < 1 || p->feature_dim > kMaxFeat)
+            return fail(ctx, CONVCRF_E_INVALID_ARG, "feature_dim must be 1 .. 4 with features");
+        if (s != 1)
+            return fail(ctx, CONVCRF_E_UNSUPPORTED, "learnable features are built for blur = 1 only");
+        if (feat_lds_bytes(k, C, p->feature_dim) > kLdsLimit)
+            return fail(ctx, CONVCRF_E_UNSUPPORTED, "window, classes and features exceed LDS");
+    }
     const long long npix = (long long)B * H * W;
     if (npix * (long long)C > (1LL << 40))
         return fail(ctx, CONVCRF_E_UNSUPPORTED, "tensor too large");
@@ -291,6 +299,32 @@ void plan_unpooled(IterArgs& a, IterArgs& as, bool& streamed, size_t& lds_s, Til
     as.ntiles = as.tiles_per_img * B;
 }
 
+// Arguments of the learnable-feature update over B x C x H x W.
+FeatArgs feat_args(const convcrf_params& p, const float* unary, const float* image,
+                   const float* mu_dev, int B, int C, int H, int W) {
+    FeatArgs f{};
+    f.unary = unary;
+    f.image = image;
+    f.feat = p.features;
+    f.mu = mu_dev;
+    f.C = C;
+    f.H = H;
+    f.W = W;
+    f.D = p.feature_dim;
+    f.tiles_x = (W + kFeatTW - 1) / kFeatTW;
+    f.tiles_per_img = f.tiles_x * ((H + kFeatTH - 1) / kFeatTH);
+    f.ntiles = f.tiles_per_img * B;
+    f.include_center = p.include_center;
+    f.neg_beta = (float)(-kLog2eD / (2.0 * (double)p.theta_beta * p.theta_beta));
+    f.neg_gamma = (float)(-kLog2eD / (2.0 * (double)p.theta_gamma * p.theta_gamma));
+    f.w_app = p.w_app;
+    f.w_smooth = p.w_smooth;
+    for (int n = 0; n <= kMaxN; ++n)
+        f.a_log2[n] = (float)(-(double)n * kLog2eD /
+                              (2.0 * (double)p.theta_alpha * p.theta_alpha));
+    return f;
+}
+
 // Upload mu (C*C floats) if it differs from what the device holds.
 convcrf_status upload_mu(convcrf_ctx* ctx, const float* mu, int C, hipStream_t stream) {
     const size_t n = (size_t)C * C;
@@ -357,6 +391,8 @@ convcrf_status convcrf_default_params(convcrf_params* p) {
     p->w_smooth = 3.f;
     p->theta_gamma = 3.f;
     p->compat = nullptr;
+    p->features = nullptr;
+    p->feature_dim = 0;
     return CONVCRF_OK;
 }
 
@@ -401,7 +437,7 @@ void convcrf_destroy(convcrf_ctx* ctx) {
     (void)hipDeviceSynchronize();
     for (DevBuf* b : {&ctx->q_ws, &ctx->q_ws2, &ctx->kmat, &ctx->pool_q, &ctx->pool_m,
                       &ctx->pool_f, &ctx->mu, &ctx->sync, &ctx->b_q, &ctx->b_dq, &ctx->b_dm,
-                      &ctx->b_dp, &ctx->b_gpart, &ctx->b_kpart})
+                      &ctx->b_dp, &ctx->b_gpart, &ctx->b_kpart, &ctx->b_df})
         if (b->p) (void)hipFree(b->p);
     if (ctx->mu_pinned) (void)hipHostFree(ctx->mu_pinned);
     if (ctx->mu_copied) (void)hipEventDestroy(ctx->mu_copied);
@@ -483,6 +519,28 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
         st = upload_mu(ctx, p.compat, C, stream);
         if (st != CONVCRF_OK) return st;
         mu_dev = static_cast<const float*>(ctx->mu.p);
+    }
+
+    if (p.features) {
+        // learnable smoothness features: Q0 = softmax(U), then one update
+        // launch per iteration, the last one into q_out
+        if ((st = ensure(ctx, ctx->q_ws, qbytes)) != CONVCRF_OK) return st;
+        float* ws = static_cast<float*>(ctx->q_ws.p);
+        FeatArgs f = feat_args(p, unary, image, mu_dev, B, C, H, W);
+        float* q0 = iters % 2 == 0 ? q_out : ws;
+        st = launch(ctx, kSoftmax, stream, "softmax",
+                    [&] { return launch_softmax(unary, q0, B, C, H * W, stream); });
+        if (st != CONVCRF_OK) return st;
+        const float* cur = q0;
+        for (int t = 0; t < iters; ++t) {
+            f.src = cur;
+            f.dst = ((iters - 1 - t) % 2 == 0) ? q_out : ws;
+            st = launch(ctx, kFeatIter, stream, "feature_iter",
+                        [&] { return launch_feat_update(f, k, stream); });
+            if (st != CONVCRF_OK) return st;
+            cur = f.dst;
+        }
+        return CONVCRF_OK;
     }
 
     IterArgs a{};
@@ -651,7 +709,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
                                           const convcrf_params* params, int iters,
                                           const float* grad_q, float* grad_unary,
                                           float* grad_compat, float* grad_kernel,
-                                          void* stream_ptr) {
+                                          float* grad_features, void* stream_ptr) {
     if (!ctx) return fail(nullptr, CONVCRF_E_INVALID_ARG, "ctx is NULL");
     convcrf_status st = validate(ctx, B, C, H, W, params, iters);
     if (st != CONVCRF_OK) return st;
@@ -659,7 +717,8 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         return fail(ctx, CONVCRF_E_UNSUPPORTED, "the derivative is built for blur = 1 only");
     const convcrf_params p = *params;
     const int k = p.filter_size;
-    if (bwd_lds_bytes(k, C) > kLdsLimit)
+    const int D = p.features ? p.feature_dim : 0;
+    if (bwd_lds_bytes(k, C, D) > kLdsLimit)
         return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
     const long long npix = (long long)B * H * W;
     const size_t qbytes = sizeof(float) * (size_t)npix * C;
@@ -678,11 +737,15 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     const float scale[5] = {1.f, (float)(p.w_app / (ta * ta * ta)),
                             (float)(p.w_app / (tb * tb * tb)), 1.f,
                             (float)(p.w_smooth / (tg * tg * tg))};
-    const int tw = bwd_tile_w(k), th = bwd_tile_h(k, C);
+    const int tw = bwd_tile_w(k), th = bwd_tile_h(k, C, D);
     const long long ntiles_ll = (long long)((W + tw - 1) / tw) * ((H + th - 1) / th) * B;
     if (ntiles_ll > 0x7fffffffLL) return fail(ctx, CONVCRF_E_UNSUPPORTED, "too many tiles");
     const int ntiles = (int)ntiles_ll;
     const bool run = npix > 0 && iters > 0;
+    if (p.features && grad_features && npix > 0 &&
+        overlaps(grad_features, sizeof(float) * (size_t)npix * D, p.features,
+                 sizeof(float) * (size_t)npix * D))
+        return fail(ctx, CONVCRF_E_INVALID_ARG, "grad_features overlaps the features");
     if (npix == 0) {
         if (grad_compat || grad_kernel)   // nothing to sum: zeros
             return launch(ctx, kBwdReduce, stream, "bwd_reduce", [&] {
@@ -711,6 +774,9 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         }
         if ((st = ensure(ctx, ctx->b_kpart, sizeof(float) * (size_t)ntiles * 5)) != CONVCRF_OK)
             return st;
+        if (p.features && !grad_features &&
+            (st = ensure(ctx, ctx->b_df, sizeof(float) * (size_t)npix * D)) != CONVCRF_OK)
+            return st;
     }
     char* qbase = static_cast<char*>(ctx->b_q.p);
     auto qs = [&](int t) { return reinterpret_cast<float*>(qbase + slice * t); };
@@ -719,7 +785,16 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     st = launch(ctx, kSoftmax, stream, "softmax",
                 [&] { return launch_softmax(unary, qs(0), B, C, H * W, stream); });
     if (st != CONVCRF_OK) return st;
-    if (run) {
+    if (run && p.features) {
+        FeatArgs f = feat_args(p, unary, image, mu_dev, B, C, H, W);
+        for (int t = 0; t < iters; ++t) {
+            f.src = qs(t);
+            f.dst = qs(t + 1);
+            st = launch(ctx, kFeatIter, stream, "feature_iter",
+                        [&] { return launch_feat_update(f, k, stream); });
+            if (st != CONVCRF_OK) return st;
+        }
+    } else if (run) {
         IterArgs a{};
         a.mu = mu_dev;
         a.include_center = p.include_center;
@@ -758,7 +833,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     ba.include_center = p.include_center;
     // 16-byte staging: whole vectors per row, every plane 16-byte aligned
     // (the image and the workspace slices; W % 4 == 0 keeps the planes so)
-    ba.vec4 = bwd_vec4_fits(k, C) && W % 4 == 0 &&
+    ba.vec4 = !p.features && bwd_vec4_fits(k, C) && W % 4 == 0 &&
               reinterpret_cast<uintptr_t>(image) % 16 == 0 &&
               reinterpret_cast<uintptr_t>(ctx->b_dm.p) % 16 == 0 &&
               reinterpret_cast<uintptr_t>(qbase) % 16 == 0;
@@ -771,6 +846,13 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     }
     ba.dm = static_cast<const float*>(ctx->b_dm.p);
     ba.kpart = static_cast<float*>(ctx->b_kpart.p);
+    if (p.features) {
+        ba.sfeat = p.features;
+        ba.dfeat = grad_features ? grad_features : static_cast<float*>(ctx->b_df.p);
+        ba.D = D;
+        ba.neg_gamma = (float)(-kLog2eD / (2.0 * tg * tg));
+        ba.inv_gamma2 = (float)(1.0 / (tg * tg));
+    }
     float* dp = grad_compat ? static_cast<float*>(ctx->b_dp.p) : nullptr;
     ba.dp = dp;
     ba.gpart = grad_compat ? static_cast<float*>(ctx->b_gpart.p) : nullptr;
@@ -790,6 +872,17 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
                     [&] { return launch_bwd_message(ba, k, stream); });
         if (st != CONVCRF_OK) return st;
         dq = ba.dq_out;
+    }
+    if (p.features && grad_features && !run) {
+        // T = 0: Q = softmax(U) does not depend on the features
+        for (long long off = 0; off < npix * D; off += 1LL << 30) {
+            const int n = (int)std::min<long long>(1LL << 30, npix * D - off);
+            st = launch(ctx, kSyncReset, stream, "sync_reset", [&] {
+                return launch_zero_u32(reinterpret_cast<unsigned int*>(grad_features + off), n,
+                                       stream);
+            });
+            if (st != CONVCRF_OK) return st;
+        }
     }
     // Q^0 = softmax(U)
     st = launch(ctx, kBwdPoint, stream, "bwd_point", [&] {

@@ -68,11 +68,11 @@ __global__ __launch_bounds__(256) void bwd_point_kernel(
 
 // ---------------------------------------------------------- adjoint message
 
-// Tile plus halo of the 3 colour planes, the C planes of Q^t and the C
-// planes of dL/dM^t into LDS (LW x LH each, the first staged column is x0,
-// the first row y0); zero outside the image, so that taps there contribute
-// nothing to any sum.  V4: 16-byte vectors (x0 and LW multiples of 4, W a
-// multiple of 4, 16-byte aligned planes).
+// Tile plus halo of the 3 colour planes, the D feature planes (FT), the C
+// planes of Q^t and the C planes of dL/dM^t into LDS (LW x LH each, the
+// first staged column is x0, the first row y0); zero outside the image, so
+// that taps there contribute nothing to any sum.  V4: 16-byte vectors (x0
+// and LW multiples of 4, W a multiple of 4, 16-byte aligned planes).
 template <int NT, int LW, int PL, bool V4>
 __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b, int y0,
                                              int x0) {
@@ -103,7 +103,9 @@ __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b
     const float* fb = a.feat + (long long)b * 3 * hw;
     const float* qb = a.q + (long long)b * C * hw;
     const float* mb = a.dm + (long long)b * C * hw;
-    const int nplanes = 2 * C + 3;
+    const int D = a.sfeat ? a.D : 0;
+    const float* sb = a.sfeat ? a.sfeat + (long long)b * D * hw : fb;
+    const int nplanes = 2 * C + 3 + D;
     // branch-free (an in-image address is read for every element and the
     // value dropped outside), so that many loads are in flight per thread
 #pragma unroll 16
@@ -111,8 +113,10 @@ __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b
         const int pl = e / PL, o = e - pl * PL;
         const int ly = o / LW, lx = o - ly * LW;
         const int gy = y0 + ly, gx = x0 + lx;
-        const float* src = pl < 3 ? fb + pl * hw : (pl < 3 + C ? qb + (pl - 3) * hw
-                                                               : mb + (pl - 3 - C) * hw);
+        const int pq = pl - 3 - D;   // index among the Q and dL/dM planes
+        const float* src = pl < 3 ? fb + pl * hw
+                                  : (pq < 0 ? sb + (pl - 3) * hw
+                                            : (pq < C ? qb + pq * hw : mb + (pq - C) * hw));
         const bool ok = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
         const float v = src[ok ? (long long)gy * a.W + gx : 0];
         lds[e] = ok ? v : 0.f;
@@ -213,16 +217,19 @@ __device__ __forceinline__ void tile_gram(float* lds, const BwdArgs& a, int tile
 // One pixel per thread, 32 x TH tiles up to k = 7 (16 x 8 above).  CM >= C
 // classes are computed without branches: planes past C - 1 read plane C - 1 again and
 // are never stored, and their dL/dM is zero, so they add nothing to dk.
-template <int K, int TH, int CM, bool WM, bool V4>
+template <int K, int TH, int CM, bool WM, bool V4, bool FT>
 __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) {
     constexpr int TW = bwd_tile_w(K), NT = TW * TH;
     constexpr int R = (K - 1) / 2, LW = bwd_stage_w(K, V4), PL = LW * (TH + K - 1);
     constexpr int XO = V4 ? 4 : R;   // staged columns left of the tile
     static_assert(XO >= R, "vector staging needs k <= 9");
+    static_assert(!(V4 && FT), "feature planes are staged by scalars");
     extern __shared__ float lds[];
     const int C = a.C;
+    const int D = FT ? a.D : 0;
     const float* sc = lds;               // 3 colour planes
-    const float* sq = lds + 3 * PL;      // C planes of Q^t
+    const float* sf = lds + 3 * PL;      // D feature planes (FT)
+    const float* sq = sf + D * PL;       // C planes of Q^t
     const float* sm = sq + C * PL;       // C planes of dL/dM^t
     const int tile = blockIdx.x;
     const int b = tile / a.tiles_per_img;
@@ -251,6 +258,17 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
             dmq[c] = c < C ? sm[poff[c] + oc] : 0.f;
             dqa[c] = 0.f;
         }
+        // FT: own features and Q, and the feature derivative of the pixel
+        float fo[kMaxFeat], dfa[kMaxFeat], qo[FT ? CM : 1];
+#pragma unroll
+        for (int c = 0; c < kMaxFeat; ++c) {
+            fo[c] = FT && c < D ? sf[c * PL + oc] : 0.f;
+            dfa[c] = 0.f;
+        }
+        if constexpr (FT) {
+#pragma unroll
+            for (int c = 0; c < CM; ++c) qo[c] = c < C ? sq[poff[c] + oc] : 0.f;
+        }
         constexpr int kRowUnroll = K <= 7 ? K : 1;   // a window row at once
 #pragma unroll 1
         for (int dy = -R; dy <= R; ++dy) {
@@ -262,27 +280,52 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
                 const float cd2 = fmaf(er, er, fmaf(eg, eg, eb * eb));
                 const int n = dx * dx + dy * dy;
                 const float av = exp2f(fmaf(a.neg_beta, cd2, a.a_log2[n]));
-                const float sv = a.smooth[n];
+                // the smoothness Gaussian and its squared distance: the
+                // positions, or the learnable features (FT)
+                float sd2 = (float)n, sv = a.smooth[n];
+                float fdif[kMaxFeat];
+                if constexpr (FT) {
+                    sd2 = 0.f;
+#pragma unroll
+                    for (int c = 0; c < kMaxFeat; ++c) {
+                        fdif[c] = c < D ? fo[c] - sf[c * PL + o] : 0.f;
+                        sd2 = fmaf(fdif[c], fdif[c], sd2);
+                    }
+                    sv = exp2f(a.neg_gamma * sd2);
+                }
                 const float w = fmaf(a.w_app, av, a.w_smooth * sv);
-                float dk = 0.f;
+                float dk = 0.f, dkr = 0.f;
 #pragma unroll
                 for (int c = 0; c < CM; ++c) {
                     const float qn = sq[poff[c] + o];
+                    const float mn = sm[poff[c] + o];
                     dk = fmaf(dmq[c], qn, dk);
-                    dqa[c] = fmaf(w, sm[poff[c] + o], dqa[c]);
+                    dqa[c] = fmaf(w, mn, dqa[c]);
                     if (WM) ma[0][c] = fmaf(w, qn, ma[0][c]);
+                    if (FT) dkr = fmaf(mn, qo[c], dkr);
                 }
                 const float da = dk * av, ds = dk * sv;
                 g[0] += da;
                 g[1] = fmaf(da, (float)n, g[1]);
                 g[2] = fmaf(da, cd2, g[2]);
                 g[3] += ds;
-                g[4] = fmaf(ds, (float)n, g[4]);
+                g[4] = fmaf(ds, sd2, g[4]);
+                if constexpr (FT) {
+                    const float coef = -(dk + dkr) * a.w_smooth * sv * a.inv_gamma2;
+#pragma unroll
+                    for (int c = 0; c < kMaxFeat; ++c) dfa[c] = fmaf(coef, fdif[c], dfa[c]);
+                }
             }
         }
 #pragma unroll
         for (int c = 0; c < CM; ++c)
             if (c < C) a.dq_out[pix + c * hw] = dqa[c];
+        if constexpr (FT) {
+            float* df = a.dfeat + (long long)b * D * hw + (long long)py * a.W + px;
+#pragma unroll
+            for (int c = 0; c < kMaxFeat; ++c)
+                if (c < D) df[c * hw] = a.accumulate ? df[c * hw] + dfa[c] : dfa[c];
+        }
     }
     if constexpr (WM) {
         const bool ins[1] = {in};
@@ -328,25 +371,26 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(ReduceArgs a) {
     }
 }
 
-template <int K, int TH, int CM, bool V4>
+template <int K, int TH, int CM, bool V4, bool FT>
 hipError_t launch_msg_ktc(const BwdArgs& a, hipStream_t stream) {
-    const size_t lds = bwd_lds_bytes(K, a.C, TH, V4);
+    const size_t lds = bwd_lds_bytes(K, a.C, TH, V4, FT ? a.D : 0);
     const dim3 block(bwd_tile_w(K) * TH);
     if (a.gpart)
-        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, true, V4>), dim3(a.ntiles), block, lds,
-                           stream, a);
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, true, V4, FT>), dim3(a.ntiles), block,
+                           lds, stream, a);
     else
-        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, false, V4>), dim3(a.ntiles), block, lds,
-                           stream, a);
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, false, V4, FT>), dim3(a.ntiles), block,
+                           lds, stream, a);
     return hipGetLastError();
 }
 
 template <int K, int TH, int CM>
 hipError_t launch_msg_ktv(const BwdArgs& a, hipStream_t stream) {
+    if (a.sfeat) return launch_msg_ktc<K, TH, CM, false, true>(a, stream);
     if constexpr (K <= 7) {
-        if (a.vec4) return launch_msg_ktc<K, TH, CM, true>(a, stream);
+        if (a.vec4) return launch_msg_ktc<K, TH, CM, true, false>(a, stream);
     }
-    return launch_msg_ktc<K, TH, CM, false>(a, stream);
+    return launch_msg_ktc<K, TH, CM, false, false>(a, stream);
 }
 
 // The host derives the tiling (tiles_x, tiles_per_img, ntiles) from the
@@ -358,7 +402,8 @@ hipError_t launch_msg_k(const BwdArgs& a, hipStream_t stream) {
         else return launch_msg_ktv<K, 8, 8>(a, stream);
     }
     if constexpr (K <= 7) {
-        if (bwd_tile_h(K, a.C) == 8) return launch_msg_ktv<K, 8, kMaxC>(a, stream);
+        if (bwd_tile_h(K, a.C, a.sfeat ? a.D : 0) == 8)
+            return launch_msg_ktv<K, 8, kMaxC>(a, stream);
         if (a.C <= 21) return launch_msg_ktv<K, 16, 21>(a, stream);
         return launch_msg_ktv<K, 16, kMaxC>(a, stream);
     } else {
@@ -370,7 +415,8 @@ hipError_t launch_msg_k(const BwdArgs& a, hipStream_t stream) {
 
 hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream) {
     if (a.C < 1 || a.C > kMaxC || a.ntiles <= 0) return hipErrorInvalidValue;
-    if (bwd_lds_bytes(k, a.C) > 160 * 1024) return hipErrorInvalidValue;
+    if (a.sfeat && (a.D < 1 || a.D > kMaxFeat || a.vec4 || !a.dfeat)) return hipErrorInvalidValue;
+    if (bwd_lds_bytes(k, a.C, a.sfeat ? a.D : 0) > 160 * 1024) return hipErrorInvalidValue;
     if (a.vec4 && (!bwd_vec4_fits(k, a.C) || a.W % 4 != 0)) return hipErrorInvalidValue;
     switch (k) {
         case 1: return launch_msg_k<1>(a, stream);

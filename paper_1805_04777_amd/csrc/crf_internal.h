@@ -185,6 +185,31 @@ hipError_t launch_blur_update(const float* m_pooled, const float* unary,
                               int B, int C, int H, int W, int s,
                               hipStream_t stream);
 
+// ---- learnable smoothness features (the "+T" variant): one update with
+// the smoothness Gaussian on |F_p - F_q|^2 of a feature map F [B][D][H][W]
+// instead of |p - q|^2.  32 x 8 tiles, one pixel per thread.
+constexpr int kMaxFeat = 4;
+struct FeatArgs {
+    const float* src;    // Q_t [B][C][H][W]
+    const float* unary;  // U [B][C][H][W]
+    const float* image;  // [B][3][H][W]
+    const float* feat;   // F [B][D][H][W]
+    const float* mu;     // device C x C compatibility or null (Potts)
+    float* dst;          // Q_{t+1}
+    int C, H, W, D;
+    int tiles_x, tiles_per_img, ntiles;
+    int include_center;
+    float neg_beta;      // -log2(e) / (2 theta_beta^2)
+    float neg_gamma;     // -log2(e) / (2 theta_gamma^2)
+    float w_app, w_smooth;
+    float a_log2[kMaxN + 1];  // -n log2(e) / (2 theta_alpha^2)
+};
+constexpr int kFeatTW = 32, kFeatTH = 8;
+inline size_t feat_lds_bytes(int k, int C, int D) {
+    return sizeof(float) * (size_t)(3 + D + C) * (kFeatTW + k - 1) * (kFeatTH + k - 1);
+}
+hipError_t launch_feat_update(const FeatArgs& a, int k, hipStream_t stream);
+
 // ---- reverse mode (derivative of the unpooled mean-field)
 // Arguments of one adjoint-message launch: for every pixel x of the grid,
 //   dq_out_x(l) = sum_d K(x, x+d) dm_{x+d}(l)   (the transpose of the Eq. 6
@@ -192,6 +217,11 @@ hipError_t launch_blur_update(const float* m_pooled, const float* unary,
 // and the tile's sums over its pixels and taps of dk = sum_l dm_x(l) q_{x+d}(l)
 // times A, A |d|^2, A |I_x - I_{x+d}|^2, S, S |d|^2, where A and S are the
 // two Eq. 4 Gaussians without their weights, added into kpart[tile][5];
+// with learnable smoothness features the smoothness Gaussian S is taken on
+// |F_x - F_{x+d}|^2, the theta_gamma term on that distance, and
+//   dfeat_x += sum_d (dk(x, x+d) + dk(x+d, x)) (-w_smooth S / theta_gamma^2)
+//              (F_x - F_{x+d}),  dk(x+d, x) = sum_l dm_{x+d}(l) q_x(l)
+// (the pair (x, x+d) seen from both ends; K is symmetric);
 // when gpart is set, also the forward message M_x(l) = sum_d K(x, x+d)
 // q_{x+d}(l) and the tile's sum over its pixels of dp_x(l) M_x(l') (the
 // compatibility derivative), added into gpart[tile][l * C + l'].  Partial
@@ -201,6 +231,11 @@ struct BwdArgs {
     const float* dm;     // dL/dM^t [B][C][H][W]
     const float* feat;   // image [B][3][H][W]
     const float* dp;     // -dL/dZ^t [B][C][H][W] (read when gpart is set)
+    const float* sfeat;  // learnable smoothness features [B][D][H][W] or null
+    float* dfeat;        // dL/dF [B][D][H][W] (with sfeat)
+    int D;
+    float neg_gamma;     // -log2(e) / (2 theta_gamma^2) (with sfeat)
+    float inv_gamma2;    // 1 / theta_gamma^2 (with sfeat)
     float* dq_out;       // dL/dQ^t [B][C][H][W]
     float* gpart;        // [ntiles][C * C] or null
     float* kpart;        // [ntiles][5]
@@ -230,18 +265,21 @@ constexpr int bwd_gram_rows(int C) { return (C + 2) / 3 * 3; }
 constexpr int bwd_stage_w(int k, bool vec4) {
     return vec4 ? bwd_tile_w(k) + 8 : bwd_tile_w(k) + k - 1;
 }
-constexpr size_t bwd_lds_bytes(int k, int C, int rows, bool vec4 = false) {
-    const size_t stage = (size_t)(2 * C + 3) * bwd_stage_w(k, vec4) * (rows + k - 1);
+constexpr size_t bwd_lds_bytes(int k, int C, int rows, bool vec4 = false, int D = 0) {
+    const size_t stage = (size_t)(2 * C + 3 + D) * bwd_stage_w(k, vec4) * (rows + k - 1);
     const size_t nt = (size_t)bwd_tile_w(k) * rows;
     const size_t gram = 2 * (size_t)bwd_gram_rows(C) * (nt + 1);
     const size_t red = 9 * nt;
     const size_t g = gram > red ? gram : red;
     return sizeof(float) * (stage > g ? stage : g);
 }
-constexpr int bwd_tile_h(int k, int C) {
-    return k <= 7 && bwd_lds_bytes(k, C, 16) <= 160 * 1024 ? 16 : 8;
+// D: learnable smoothness feature planes staged besides (0 without).
+constexpr int bwd_tile_h(int k, int C, int D = 0) {
+    return k <= 7 && bwd_lds_bytes(k, C, 16, false, D) <= 160 * 1024 ? 16 : 8;
 }
-inline size_t bwd_lds_bytes(int k, int C) { return bwd_lds_bytes(k, C, bwd_tile_h(k, C)); }
+inline size_t bwd_lds_bytes(int k, int C, int D = 0) {
+    return bwd_lds_bytes(k, C, bwd_tile_h(k, C, D), false, D);
+}
 // whether the vec4 staging is built for (k, C) and fits the LDS
 constexpr bool bwd_vec4_fits(int k, int C) {
     return k <= 7 && bwd_lds_bytes(k, C, bwd_tile_h(k, C), true) <= 160 * 1024 - 256;

@@ -45,16 +45,18 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_struct_layout_matches_header(lib):
-    # 4 int32 + 5 float + pointer, no packing surprises
-    assert ctypes.sizeof(cc.CParams) == 4 * 4 + 5 * 4 + 4 + 8
+    # 4 int32 + 5 float (+ 4 padding) + pointer + pointer + int32 (+ 4 padding)
+    assert ctypes.sizeof(cc.CParams) == 4 * 4 + 5 * 4 + 4 + 8 + 8 + 4 + 4
     assert cc.CParams.compat.offset == 40
+    assert cc.CParams.features.offset == 48
+    assert cc.CParams.feature_dim.offset == 56
 
 
 def test_default_params(lib):
     p = cc.default_params()
     assert (p.filter_size, p.blur, p.include_center, p.variant) == (7, 1, False, cc.VARIANT_FUSED)
     assert (p.w_app, p.theta_alpha, p.theta_beta, p.w_smooth, p.theta_gamma) == (10, 80, 13, 3, 3)
-    assert p.compat is None
+    assert p.compat is None and p.features is None
 
 
 def test_status_strings(lib):

@@ -1,0 +1,156 @@
+"""GPU parity of the learnable smoothness features (the "+T" variant of
+Sec. 4.2) against the oracle, forward and derivative.
+
+Forward bar: the inference bar (1e-4 absolute per probability, argmax
+agreement >= 99.99%, rows summing to 1 within 1e-5).  Derivative bar: the
+reverse-mode bar (1e-4 of each tensor's largest magnitude; 1e-3 relative
+per kernel parameter), with dL/dF held to the same 1e-4 of its largest
+magnitude.
+"""
+import numpy as np
+import pytest
+
+from oracle import OracleParams
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def crf(torch_cuda):
+    from paper_1805_04777_amd import convcrf as cc
+    ctx = cc.ConvCRF(0)
+    yield ctx
+    ctx.close()
+
+
+def make_case(seed, B, C, H, W, D):
+    rng = np.random.default_rng(seed)
+    U = rng.normal(0.0, 1.5, (B, C, H, W)).astype(np.float32)
+    blocks = rng.integers(0, 4, (B, 3, (H + 7) // 8, (W + 7) // 8)) * 50.0
+    I = np.repeat(np.repeat(blocks, 8, axis=2), 8, axis=3)[:, :, :H, :W]
+    I = np.clip(np.rint(I + rng.normal(0.0, 8.0, I.shape)), 0, 255).astype(np.float32)
+    yy, xx = np.meshgrid(np.arange(H, dtype=np.float64), np.arange(W, dtype=np.float64),
+                         indexing="ij")
+    base = [yy, xx, np.zeros((H, W)), np.zeros((H, W))][:D]
+    F = (np.stack(base)[None].repeat(B, axis=0) + rng.normal(0.0, 0.5, (B, D, H, W)))
+    G = rng.normal(0.0, 1.0, (B, C, H, W)).astype(np.float32)
+    return U, I, F.astype(np.float32), G
+
+
+def params(torch, k, F, center=False, compat=None, **kw):
+    from paper_1805_04777_amd import convcrf as cc
+    base = dict(filter_size=k, include_center=center, w_app=10.0, theta_alpha=80.0,
+                theta_beta=13.0, w_smooth=3.0, theta_gamma=3.0, compat=compat,
+                features=None if F is None else torch.from_numpy(F).cuda())
+    base.update(kw)
+    return cc.Params(**base)
+
+
+def oparams(p):
+    return OracleParams(filter_size=p.filter_size, include_center=bool(p.include_center),
+                        w_app=p.w_app, theta_alpha=p.theta_alpha, theta_beta=p.theta_beta,
+                        w_smooth=p.w_smooth, theta_gamma=p.theta_gamma)
+
+
+CASES = [
+    # (seed, B, C, H, W, k, T, D, include_center, general compat)
+    (1, 1, 3, 20, 37, 3, 2, 2, False, False),
+    (2, 2, 5, 33, 40, 5, 3, 2, True, True),
+    (3, 1, 21, 40, 64, 7, 2, 2, False, False),
+    (4, 1, 19, 24, 36, 9, 2, 3, False, True),
+    (5, 1, 4, 17, 23, 13, 1, 1, True, False),
+    (6, 1, 24, 16, 24, 7, 1, 4, False, False),
+]
+
+
+@pytest.mark.parametrize("seed,B,C,H,W,k,T,D,center,gen_mu", CASES)
+def test_forward_with_features(torch_cuda, crf, oracle_mod, seed, B, C, H, W, k, T, D, center,
+                               gen_mu):
+    torch = torch_cuda
+    U, I, F, _ = make_case(seed, B, C, H, W, D)
+    mu = np.random.default_rng(seed + 100).normal(0.3, 0.5, (C, C)).astype(np.float32) \
+        if gen_mu else None
+    p = params(torch, k, F, center, mu)
+    Q = crf.meanfield(torch.from_numpy(U).cuda(), torch.from_numpy(I).cuda(), p, T)
+    torch.cuda.synchronize()
+    Qg = Q.cpu().numpy().astype(np.float64)
+    Qo = oracle_mod.meanfield(U, I, oparams(p), T, compat=mu, features=F)
+    err = np.abs(Qg - Qo).max()
+    print(f"case {seed}: forward max|dQ| {err:.2e}", flush=True)
+    assert err <= 1e-4
+    assert (Qg.argmax(1) == Qo.argmax(1)).mean() >= 0.9999
+    assert np.abs(Qg.sum(1) - 1.0).max() <= 1e-5
+
+
+def test_position_features_match_the_fused_path(torch_cuda, crf, oracle_mod):
+    """Features equal to the pixel positions reproduce Eq. 4: the feature
+    kernel and the fused kernel both meet the inference bar against the
+    oracle of Eq. 4, and each other."""
+    torch = torch_cuda
+    U, I, _, _ = make_case(7, 1, 21, 48, 64, 2)
+    yy, xx = np.meshgrid(np.arange(48, dtype=np.float32), np.arange(64, dtype=np.float32),
+                         indexing="ij")
+    pos = np.stack([yy, xx])[None].copy()
+    Ut, It = torch.from_numpy(U).cuda(), torch.from_numpy(I).cuda()
+    a = crf.meanfield(Ut, It, params(torch, 7, pos), 2).cpu().numpy().astype(np.float64)
+    b = crf.meanfield(Ut, It, params(torch, 7, None), 2).cpu().numpy().astype(np.float64)
+    o = oracle_mod.meanfield(U, I, OracleParams(filter_size=7), 2)
+    assert np.abs(a - o).max() <= 1e-4 and np.abs(b - o).max() <= 1e-4
+    assert np.abs(a - b).max() <= 1e-4
+
+
+@pytest.mark.parametrize("seed,B,C,H,W,k,T,D,center,gen_mu", CASES)
+def test_backward_with_features(torch_cuda, crf, oracle_mod, seed, B, C, H, W, k, T, D, center,
+                                gen_mu):
+    torch = torch_cuda
+    U, I, F, G = make_case(seed, B, C, H, W, D)
+    mu = np.random.default_rng(seed + 100).normal(0.3, 0.5, (C, C)).astype(np.float32) \
+        if gen_mu else None
+    p = params(torch, k, F, center, mu)
+    t = lambda x: torch.from_numpy(x).cuda()
+    dU, dmu, dk, dF = crf.meanfield_backward(t(U), t(I), p, T, t(G), grad_compat=True,
+                                             grad_kernel=True)
+    torch.cuda.synchronize()
+    got = [x.cpu().numpy().astype(np.float64) for x in (dU, dmu, dk, dF)]
+    ref = oracle_mod.meanfield_backward(U, I, oparams(p), T, G, compat=mu, features=F)
+    errs = []
+    for g, r, name in zip((got[0], got[1], got[3]), (ref[0], ref[1], ref[3]), ("dU", "dmu", "dF")):
+        e = np.abs(g - r).max() / np.abs(r).max()
+        errs.append(e)
+        assert e <= 1e-4, f"{name}: rel err {e:.2e}"
+    ek = np.abs(got[2] - ref[2]) / np.abs(ref[2])
+    assert np.all(ek <= 1e-3), ek
+    print(f"case {seed}: backward rel err dU {errs[0]:.1e} dmu {errs[1]:.1e} dF {errs[2]:.1e} "
+          f"dk {ek.max():.1e}", flush=True)
+
+
+def test_zero_iterations_give_zero_feature_derivative(torch_cuda, crf):
+    torch = torch_cuda
+    U, I, F, G = make_case(8, 1, 4, 12, 16, 2)
+    p = params(torch, 5, F)
+    t = lambda x: torch.from_numpy(x).cuda()
+    out = crf.meanfield_backward(t(U), t(I), p, 0, t(G))
+    torch.cuda.synchronize()
+    assert torch.all(out[3] == 0)
+
+
+def test_feature_errors(torch_cuda, crf):
+    from paper_1805_04777_amd import convcrf as cc
+    torch = torch_cuda
+    U, I, F, _ = make_case(9, 1, 4, 16, 16, 2)
+    Ut, It = torch.from_numpy(U).cuda(), torch.from_numpy(I).cuda()
+    with pytest.raises(cc.ConvCRFError) as e:
+        crf.meanfield(Ut, It, params(torch, 5, F, blur=2), 2)
+    assert e.value.status == cc.E_UNSUPPORTED
+    F5 = np.zeros((1, 5, 16, 16), np.float32)
+    with pytest.raises(cc.ConvCRFError) as e:
+        crf.meanfield(Ut, It, params(torch, 5, F5), 2)
+    assert e.value.status == cc.E_INVALID_ARG
