@@ -15,6 +15,9 @@ oracle timed on this host as a baseline.
 --backward times the reverse mode instead: one step = one call of
 convcrf_meanfield_backward (the forward rounds recomputed and kept, then every
 round undone, with the compatibility and kernel-parameter derivatives).
+--features runs the learnable-smoothness-feature variant (Sec. 4.2, "+T"):
+two feature planes, the pixel positions plus seeded N(0, 0.5) noise (with
+--backward, dL/dF is returned as well).
 """
 from __future__ import annotations
 
@@ -62,9 +65,10 @@ def bytes_per_pixel(C: int, first: bool) -> int:
     return 4 * C * (2 if first else 3) + 12
 
 
-def algorithmic_per_launch(kname: str, wl):
+def algorithmic_per_launch(kname: str, wl, D: int = 0):
     """(flops, HBM bytes) one launch of `kname` must spend on workload `wl`,
-    averaged over the launches of one call; fp32, Potts compatibility."""
+    averaged over the launches of one call; fp32, Potts compatibility; D
+    learnable smoothness feature planes (0 without)."""
     C, k, T, px = wl.C, wl.filter_size, wl.iters, wl.pixels
     if kname == "fused_iter":
         return (flops_per_pixel_iter(C, k, True) * px,
@@ -101,10 +105,19 @@ def algorithmic_per_launch(kname: str, wl):
         return 0, 0
     # reverse mode (compatibility and kernel-parameter derivatives requested)
     taps = k * k - 1
+    if kname == "feature_iter":
+        # per tap: the appearance weight (12), the feature distance and its
+        # Gaussian (3D + 2), the message (2C); per pixel unary add and softmax
+        # (5C + 1); reads Q_t, U, the image and the features, writes Q_t+1
+        return ((12 + 3 * D + 2 + 2 * C) * taps + 5 * C + 1) * px, (12 * C + 12 + 4 * D) * px
     if kname == "bwd_message":
         # per tap: the weight (12), dk = <dM_p, Q_q> (2C), dQ += w dM (2C),
         # M += w Q (2C), the five parameter sums (10); per pixel the outer
-        # product dP M^T (2C^2); reads Q^t, dM, dP and the image, writes dQ^t
+        # product dP M^T (2C^2); reads Q^t, dM, dP and the image, writes dQ^t.
+        # With features: the feature Gaussian (3D + 2), dk(x+d, x) (2C) and
+        # dL/dF (2D + 4) per tap; the features read, dL/dF read and written
+        if D:
+            return ((8 * C + 22 + 5 * D + 6) * taps + 2 * C * C) * px, (16 * C + 12 + 12 * D) * px
         return (6 * C + 22) * taps * px + 2 * C * C * px, (16 * C + 12) * px
     if kname == "bwd_point":
         # T + 1 launches per call: T undo a round (dot, dZ, dU, Potts dM: 7C
@@ -136,7 +149,7 @@ def load_traffic(workload: str, kernel: str):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(wl, U, I, budget_s: float = 10.0, backward: bool = False):
+def cpu_baseline(wl, U, I, budget_s: float = 10.0, backward: bool = False, features=None):
     """The oracle as it stands, on this host: the full workload, repeated
     until `budget_s` seconds have passed (median per call); with `backward`,
     its derivative (forward recomputed, then reversed) on the same inputs."""
@@ -152,9 +165,9 @@ def cpu_baseline(wl, U, I, budget_s: float = 10.0, backward: bool = False):
     while True:
         t0 = time.perf_counter()
         if backward:
-            oracle.meanfield_backward(U, I, p, wl.iters, G)
+            oracle.meanfield_backward(U, I, p, wl.iters, G, features=features)
         else:
-            oracle.meanfield(U, I, p, wl.iters)
+            oracle.meanfield(U, I, p, wl.iters, features=features)
         times.append(time.perf_counter() - t0)
         if time.perf_counter() - t_all >= budget_s or len(times) >= 50:
             break
@@ -163,7 +176,8 @@ def cpu_baseline(wl, U, I, budget_s: float = 10.0, backward: bool = False):
     return {"value": round(mpi / t, 3), "unit": UNIT, "cores": oracle.num_threads(),
             "kind": "oracle",
             "sample": f"the full {wl.name} workload ({wl.B}x{wl.C}x{wl.H}x{wl.W}, k={wl.filter_size}, "
-                      f"blur={wl.blur}, T={wl.iters}){', derivative' if backward else ''}, "
+                      f"blur={wl.blur}, T={wl.iters}){', derivative' if backward else ''}"
+                      f"{', learnable features D=2' if features is not None else ''}, "
                       f"{len(times)} calls, median {t * 1e3:.1f} ms/call, double precision"}
 
 
@@ -197,6 +211,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--backward", action="store_true",
                     help="time convcrf_meanfield_backward instead of the inference")
+    ap.add_argument("--features", action="store_true",
+                    help="learnable smoothness features (two planes)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="instead: time a plain device-to-device copy of this many MiB "
                          "(reference dispatch for the FETCH_SIZE / WRITE_SIZE counters)")
@@ -223,9 +239,18 @@ def main(argv=None):
     out = torch.empty_like(Ut)
     variant = {"fused": cc.VARIANT_FUSED, "materialised": cc.VARIANT_MATERIALISED,
                "resident": cc.VARIANT_RESIDENT}[args.variant]
+    D = 2 if args.features else 0
+    Fn = None
+    if args.features:
+        import numpy as np
+        yy, xx = np.meshgrid(np.arange(wl.H, dtype=np.float32), np.arange(wl.W, dtype=np.float32),
+                             indexing="ij")
+        Fn = (np.stack([yy, xx])[None].repeat(wl.B, axis=0) + np.random.default_rng(78).normal(
+            0.0, 0.5, (wl.B, 2, wl.H, wl.W))).astype(np.float32)
     p = cc.Params(filter_size=wl.filter_size, blur=wl.blur, variant=variant, w_app=wl.w_app,
                   theta_alpha=wl.theta_alpha, theta_beta=wl.theta_beta, w_smooth=wl.w_smooth,
-                  theta_gamma=wl.theta_gamma)
+                  theta_gamma=wl.theta_gamma,
+                  features=None if Fn is None else torch.from_numpy(Fn).to(dev))
     crf = cc.ConvCRF(0)
     stream = torch.cuda.current_stream(dev)
     if args.backward:
@@ -291,7 +316,7 @@ def main(argv=None):
     share = k_ms / sum(v[0] for v in launched.values())
     avg_s = ms / 1e3 * share / (k_n / args.steps)
     avg_s_events = k_ms / 1e3 / k_n
-    F, Bytes = algorithmic_per_launch(kname, wl)
+    F, Bytes = algorithmic_per_launch(kname, wl, D)
     alu_frac = F / avg_s / PEAK_VALU_FP32
     hbm_frac = Bytes / avg_s / PEAK_HBM
     # the roofline the kernel is closer to (the counters show neither saturated)
@@ -321,14 +346,15 @@ def main(argv=None):
         "config": {"workload": f"{wl.name}: B={wl.B} C={wl.C} {wl.H}x{wl.W} k={wl.filter_size} "
                                f"blur={wl.blur} T={wl.iters} Potts, "
                                + ("derivative (dU, dmu, d kernel parameters)" if args.backward
-                                  else args.variant),
+                                  else args.variant)
+                               + (", learnable smoothness features D=2" if args.features else ""),
                    "global_batch": wl.B, "variant": args.variant,
                    "direction": "backward" if args.backward else "forward"},
         "roofline": roof,
     }
     crf.close()
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(wl, U, I, backward=args.backward)
+        rec["cpu_baseline"] = cpu_baseline(wl, U, I, backward=args.backward, features=Fn)
     print(json.dumps(rec), flush=True)
     return 0
 

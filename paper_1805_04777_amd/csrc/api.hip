@@ -315,6 +315,10 @@ FeatArgs feat_args(const convcrf_params& p, const float* unary, const float* ima
     f.tiles_per_img = f.tiles_x * ((H + kFeatTH - 1) / kFeatTH);
     f.ntiles = f.tiles_per_img * B;
     f.include_center = p.include_center;
+    // 16-byte staging: whole vectors per row, every plane 16-byte aligned
+    f.vec4 = p.filter_size <= 7 && W % 4 == 0 && reinterpret_cast<uintptr_t>(image) % 16 == 0 &&
+             reinterpret_cast<uintptr_t>(p.features) % 16 == 0 &&
+             feat_lds_bytes(p.filter_size, C, p.feature_dim, true) <= kLdsLimit;
     f.neg_beta = (float)(-kLog2eD / (2.0 * (double)p.theta_beta * p.theta_beta));
     f.neg_gamma = (float)(-kLog2eD / (2.0 * (double)p.theta_gamma * p.theta_gamma));
     f.w_app = p.w_app;
@@ -527,6 +531,9 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
         if ((st = ensure(ctx, ctx->q_ws, qbytes)) != CONVCRF_OK) return st;
         float* ws = static_cast<float*>(ctx->q_ws.p);
         FeatArgs f = feat_args(p, unary, image, mu_dev, B, C, H, W);
+        // the staged Q planes live in q_out and the workspace
+        f.vec4 = f.vec4 && reinterpret_cast<uintptr_t>(q_out) % 16 == 0 &&
+                 reinterpret_cast<uintptr_t>(ws) % 16 == 0;
         float* q0 = iters % 2 == 0 ? q_out : ws;
         st = launch(ctx, kSoftmax, stream, "softmax",
                     [&] { return launch_softmax(unary, q0, B, C, H * W, stream); });
@@ -833,8 +840,9 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     ba.include_center = p.include_center;
     // 16-byte staging: whole vectors per row, every plane 16-byte aligned
     // (the image and the workspace slices; W % 4 == 0 keeps the planes so)
-    ba.vec4 = !p.features && bwd_vec4_fits(k, C) && W % 4 == 0 &&
+    ba.vec4 = bwd_vec4_fits(k, C, D) && W % 4 == 0 &&
               reinterpret_cast<uintptr_t>(image) % 16 == 0 &&
+              reinterpret_cast<uintptr_t>(p.features) % 16 == 0 &&
               reinterpret_cast<uintptr_t>(ctx->b_dm.p) % 16 == 0 &&
               reinterpret_cast<uintptr_t>(qbase) % 16 == 0;
     ba.neg_beta = (float)(-kLog2eD / (2.0 * tb * tb));

@@ -83,14 +83,18 @@ __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b
         const float* fb = a.feat + (long long)b * 3 * hw;
         const float* qb = a.q + (long long)b * C * hw;
         const float* mb = a.dm + (long long)b * C * hw;
-        const int nvec = (2 * C + 3) * LH * LQ;
+        const int D = a.sfeat ? a.D : 0;
+        const float* sb = a.sfeat ? a.sfeat + (long long)b * D * hw : fb;
+        const int nvec = (2 * C + 3 + D) * LH * LQ;
 #pragma unroll 8
         for (int e = threadIdx.x; e < nvec; e += NT) {
             const int pl = e / (LH * LQ), o = e - pl * (LH * LQ);
             const int ly = o / LQ, lq = o - ly * LQ;
             const int gy = y0 + ly, gx = x0 + 4 * lq;
-            const float* src = pl < 3 ? fb + pl * hw : (pl < 3 + C ? qb + (pl - 3) * hw
-                                                                   : mb + (pl - 3 - C) * hw);
+            const int pq = pl - 3 - D;
+            const float* src = pl < 3 ? fb + pl * hw
+                                      : (pq < 0 ? sb + (pl - 3) * hw
+                                                : (pq < C ? qb + pq * hw : mb + (pq - C) * hw));
             const bool ok = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
             const float4 v = *reinterpret_cast<const float4*>(src + (ok ? (long long)gy * a.W + gx : 0));
             *reinterpret_cast<float4*>(lds + pl * PL + ly * LW + 4 * lq) =
@@ -223,7 +227,6 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
     constexpr int R = (K - 1) / 2, LW = bwd_stage_w(K, V4), PL = LW * (TH + K - 1);
     constexpr int XO = V4 ? 4 : R;   // staged columns left of the tile
     static_assert(XO >= R, "vector staging needs k <= 9");
-    static_assert(!(V4 && FT), "feature planes are staged by scalars");
     extern __shared__ float lds[];
     const int C = a.C;
     const int D = FT ? a.D : 0;
@@ -386,10 +389,13 @@ hipError_t launch_msg_ktc(const BwdArgs& a, hipStream_t stream) {
 
 template <int K, int TH, int CM>
 hipError_t launch_msg_ktv(const BwdArgs& a, hipStream_t stream) {
-    if (a.sfeat) return launch_msg_ktc<K, TH, CM, false, true>(a, stream);
     if constexpr (K <= 7) {
-        if (a.vec4) return launch_msg_ktc<K, TH, CM, true, false>(a, stream);
+        if (a.vec4) {
+            if (a.sfeat) return launch_msg_ktc<K, TH, CM, true, true>(a, stream);
+            return launch_msg_ktc<K, TH, CM, true, false>(a, stream);
+        }
     }
+    if (a.sfeat) return launch_msg_ktc<K, TH, CM, false, true>(a, stream);
     return launch_msg_ktc<K, TH, CM, false, false>(a, stream);
 }
 
@@ -415,9 +421,10 @@ hipError_t launch_msg_k(const BwdArgs& a, hipStream_t stream) {
 
 hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream) {
     if (a.C < 1 || a.C > kMaxC || a.ntiles <= 0) return hipErrorInvalidValue;
-    if (a.sfeat && (a.D < 1 || a.D > kMaxFeat || a.vec4 || !a.dfeat)) return hipErrorInvalidValue;
-    if (bwd_lds_bytes(k, a.C, a.sfeat ? a.D : 0) > 160 * 1024) return hipErrorInvalidValue;
-    if (a.vec4 && (!bwd_vec4_fits(k, a.C) || a.W % 4 != 0)) return hipErrorInvalidValue;
+    const int D = a.sfeat ? a.D : 0;
+    if (a.sfeat && (a.D < 1 || a.D > kMaxFeat || !a.dfeat)) return hipErrorInvalidValue;
+    if (bwd_lds_bytes(k, a.C, D) > 160 * 1024) return hipErrorInvalidValue;
+    if (a.vec4 && (!bwd_vec4_fits(k, a.C, D) || a.W % 4 != 0)) return hipErrorInvalidValue;
     switch (k) {
         case 1: return launch_msg_k<1>(a, stream);
         case 3: return launch_msg_k<3>(a, stream);

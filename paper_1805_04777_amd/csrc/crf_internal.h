@@ -199,14 +199,18 @@ struct FeatArgs {
     int C, H, W, D;
     int tiles_x, tiles_per_img, ntiles;
     int include_center;
+    int vec4;            // stage 16-byte vectors
     float neg_beta;      // -log2(e) / (2 theta_beta^2)
     float neg_gamma;     // -log2(e) / (2 theta_gamma^2)
     float w_app, w_smooth;
     float a_log2[kMaxN + 1];  // -n log2(e) / (2 theta_alpha^2)
 };
+// With vec4 (k <= 7, W a multiple of 4, 16-byte aligned planes) the staged
+// rows start 4 columns left of the tile and hold kFeatTW + 8 columns.
 constexpr int kFeatTW = 32, kFeatTH = 8;
-inline size_t feat_lds_bytes(int k, int C, int D) {
-    return sizeof(float) * (size_t)(3 + D + C) * (kFeatTW + k - 1) * (kFeatTH + k - 1);
+inline size_t feat_lds_bytes(int k, int C, int D, bool vec4 = false) {
+    return sizeof(float) * (size_t)(3 + D + C) * (vec4 ? kFeatTW + 8 : kFeatTW + k - 1) *
+           (kFeatTH + k - 1);
 }
 hipError_t launch_feat_update(const FeatArgs& a, int k, hipStream_t stream);
 
@@ -280,9 +284,10 @@ constexpr int bwd_tile_h(int k, int C, int D = 0) {
 inline size_t bwd_lds_bytes(int k, int C, int D = 0) {
     return bwd_lds_bytes(k, C, bwd_tile_h(k, C, D), false, D);
 }
-// whether the vec4 staging is built for (k, C) and fits the LDS
-constexpr bool bwd_vec4_fits(int k, int C) {
-    return k <= 7 && bwd_lds_bytes(k, C, bwd_tile_h(k, C), true) <= 160 * 1024 - 256;
+// whether the vec4 staging is built for (k, C, D feature planes) and fits
+// the LDS
+constexpr bool bwd_vec4_fits(int k, int C, int D = 0) {
+    return k <= 7 && bwd_lds_bytes(k, C, bwd_tile_h(k, C, D), true, D) <= 160 * 1024 - 256;
 }
 
 hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream);

@@ -17,10 +17,12 @@
 namespace convcrf {
 namespace {
 
-template <int K, int CM>
+template <int K, int CM, bool V4>
 __global__ __launch_bounds__(kFeatTW * kFeatTH) void feat_update_kernel(FeatArgs a) {
     constexpr int TW = kFeatTW, TH = kFeatTH, NT = TW * TH;
-    constexpr int R = (K - 1) / 2, LW = TW + K - 1, PL = LW * (TH + K - 1);
+    constexpr int R = (K - 1) / 2, LW = V4 ? TW + 8 : TW + K - 1, PL = LW * (TH + K - 1);
+    constexpr int XO = V4 ? 4 : R;   // staged columns left of the tile
+    static_assert(XO >= R, "vector staging needs k <= 9");
     extern __shared__ float lds[];
     const int C = a.C, D = a.D;
     const float* sc = lds;                 // 3 colour planes
@@ -30,29 +32,48 @@ __global__ __launch_bounds__(kFeatTW * kFeatTH) void feat_update_kernel(FeatArgs
     const int b = tile / a.tiles_per_img;
     const int tr = tile - b * a.tiles_per_img;
     const int ty = tr / a.tiles_x, tx = tr - ty * a.tiles_x;
-    const int y0 = ty * TH - R, x0 = tx * TW - R;
+    const int y0 = ty * TH - R, x0 = tx * TW - XO;
     const long long hw = (long long)a.H * a.W;
     const float* ib = a.image + (long long)b * 3 * hw;
     const float* fb = a.feat + (long long)b * D * hw;
     const float* qb = a.src + (long long)b * C * hw;
     const int nplanes = 3 + D + C;
+    if constexpr (V4) {
+        // 16-byte vectors: x0 and LW multiples of 4, W a multiple of 4, so
+        // a vector lies wholly inside or outside the image
+        constexpr int LQ = LW / 4, LH = PL / LW;
+#pragma unroll 8
+        for (int e = threadIdx.x; e < nplanes * LH * LQ; e += NT) {
+            const int pl = e / (LH * LQ), o = e - pl * (LH * LQ);
+            const int ly = o / LQ, lq = o - ly * LQ;
+            const int gy = y0 + ly, gx = x0 + 4 * lq;
+            const float* src = pl < 3 ? ib + pl * hw
+                                      : (pl < 3 + D ? fb + (pl - 3) * hw : qb + (pl - 3 - D) * hw);
+            const bool ok = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
+            const float4 v = *reinterpret_cast<const float4*>(
+                src + (ok ? (long long)gy * a.W + gx : 0));
+            *reinterpret_cast<float4*>(lds + pl * PL + ly * LW + 4 * lq) =
+                ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    } else {
 #pragma unroll 16
-    for (int e = threadIdx.x; e < nplanes * PL; e += NT) {
-        const int pl = e / PL, o = e - pl * PL;
-        const int ly = o / LW, lx = o - ly * LW;
-        const int gy = y0 + ly, gx = x0 + lx;
-        const float* src = pl < 3 ? ib + pl * hw
-                                  : (pl < 3 + D ? fb + (pl - 3) * hw : qb + (pl - 3 - D) * hw);
-        const bool ok = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
-        const float v = src[ok ? (long long)gy * a.W + gx : 0];
-        lds[e] = ok ? v : 0.f;
+        for (int e = threadIdx.x; e < nplanes * PL; e += NT) {
+            const int pl = e / PL, o = e - pl * PL;
+            const int ly = o / LW, lx = o - ly * LW;
+            const int gy = y0 + ly, gx = x0 + lx;
+            const float* src = pl < 3 ? ib + pl * hw
+                                      : (pl < 3 + D ? fb + (pl - 3) * hw : qb + (pl - 3 - D) * hw);
+            const bool ok = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
+            const float v = src[ok ? (long long)gy * a.W + gx : 0];
+            lds[e] = ok ? v : 0.f;
+        }
     }
     __syncthreads();
 
     const int lx = threadIdx.x % TW, ly = threadIdx.x / TW;
     const int px = tx * TW + lx, py = ty * TH + ly;
     if (px >= a.W || py >= a.H) return;
-    const int oc = (ly + R) * LW + lx + R;
+    const int oc = (ly + R) * LW + lx + XO;
     const float ir = sc[oc], ig = sc[PL + oc], ibl = sc[2 * PL + oc];
     float fo[kMaxFeat];
 #pragma unroll
@@ -125,15 +146,25 @@ __global__ __launch_bounds__(kFeatTW * kFeatTH) void feat_update_kernel(FeatArgs
         if (c < C) a.dst[pix + c * hw] = z[c] * inv;
 }
 
-template <int K>
-hipError_t launch_k(const FeatArgs& a, hipStream_t stream) {
-    const size_t lds = feat_lds_bytes(K, a.C, a.D);
+template <int K, bool V4>
+hipError_t launch_kv(const FeatArgs& a, hipStream_t stream) {
+    const size_t lds = feat_lds_bytes(K, a.C, a.D, V4);
     const dim3 grid(a.ntiles), block(kFeatTW * kFeatTH);
     if (a.C <= 8)
-        hipLaunchKernelGGL((feat_update_kernel<K, 8>), grid, block, lds, stream, a);
+        hipLaunchKernelGGL((feat_update_kernel<K, 8, V4>), grid, block, lds, stream, a);
+    else if (a.C <= 21)
+        hipLaunchKernelGGL((feat_update_kernel<K, 21, V4>), grid, block, lds, stream, a);
     else
-        hipLaunchKernelGGL((feat_update_kernel<K, kMaxC>), grid, block, lds, stream, a);
+        hipLaunchKernelGGL((feat_update_kernel<K, kMaxC, V4>), grid, block, lds, stream, a);
     return hipGetLastError();
+}
+
+template <int K>
+hipError_t launch_k(const FeatArgs& a, hipStream_t stream) {
+    if constexpr (K <= 7) {
+        if (a.vec4) return launch_kv<K, true>(a, stream);
+    }
+    return launch_kv<K, false>(a, stream);
 }
 
 }  // namespace
@@ -141,7 +172,8 @@ hipError_t launch_k(const FeatArgs& a, hipStream_t stream) {
 hipError_t launch_feat_update(const FeatArgs& a, int k, hipStream_t stream) {
     if (a.C < 1 || a.C > kMaxC || a.D < 1 || a.D > kMaxFeat || a.ntiles <= 0)
         return hipErrorInvalidValue;
-    if (feat_lds_bytes(k, a.C, a.D) > 160 * 1024) return hipErrorInvalidValue;
+    if (feat_lds_bytes(k, a.C, a.D, a.vec4) > 160 * 1024) return hipErrorInvalidValue;
+    if (a.vec4 && (k > 7 || a.W % 4 != 0)) return hipErrorInvalidValue;
     switch (k) {
         case 1: return launch_k<1>(a, stream);
         case 3: return launch_k<3>(a, stream);

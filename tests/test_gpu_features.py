@@ -154,3 +154,19 @@ def test_feature_errors(torch_cuda, crf):
     with pytest.raises(cc.ConvCRFError) as e:
         crf.meanfield(Ut, It, params(torch, 5, F5), 2)
     assert e.value.status == cc.E_INVALID_ARG
+
+
+def test_unaligned_output_takes_the_scalar_staging(torch_cuda, crf):
+    """An output 4 bytes off a 16-byte boundary stages Q by scalars; the
+    arithmetic is the same, so the result is identical to the vector path."""
+    torch = torch_cuda
+    U, I, F, _ = make_case(10, 1, 21, 32, 48, 2)
+    Ut, It = torch.from_numpy(U).cuda(), torch.from_numpy(I).cuda()
+    p = params(torch, 7, F)
+    a = crf.meanfield(Ut, It, p, 3)
+    buf = torch.empty(U.size + 1, device="cuda")
+    out = buf[1:].view(U.shape)
+    assert out.data_ptr() % 16 != 0
+    b = crf.meanfield(Ut, It, p, 3, out=out)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
