@@ -13,58 +13,16 @@
 //                      recomputes the forward message M^t and sums
 //                      dP_p(l) M_p(l') over the tile's pixels.
 // bwd_reduce_kernel folds the per-tile partial sums.
+//
+// Built once per window side k with -DCRF_BWD_K=k (the adjoint-message
+// kernels of that k) and once without (the pointwise and reduction kernels
+// and the dispatch over k).
 #include "crf_internal.h"
 
 namespace convcrf {
 namespace {
 
-// ---------------------------------------------------------------- pointwise
-template <int CM>
-__global__ __launch_bounds__(256) void bwd_point_kernel(
-    const float* __restrict__ q, const float* __restrict__ dq, const float* __restrict__ mu,
-    float* __restrict__ du, float* __restrict__ dm, float* __restrict__ dp, int C,
-    long long hw, long long npix, int accumulate) {
-    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= npix) return;
-    const long long b = i / hw;
-    const long long base = b * C * hw + (i - b * hw);
-    float qv[CM], dz[CM];
-    float dot = 0.f;
-#pragma unroll
-    for (int c = 0; c < CM; ++c) {
-        if (c < C) {
-            qv[c] = q[base + c * hw];
-            dz[c] = dq[base + c * hw];
-            dot = fmaf(qv[c], dz[c], dot);
-        }
-    }
-    float sum = 0.f;
-#pragma unroll
-    for (int c = 0; c < CM; ++c) {
-        if (c < C) {
-            dz[c] = qv[c] * (dz[c] - dot);
-            sum += dz[c];
-            float* o = du + base + c * hw;
-            *o = accumulate ? *o + dz[c] : dz[c];
-            if (dp) dp[base + c * hw] = -dz[c];
-        }
-    }
-    if (!dm) return;
-    if (mu) {
-        for (int lp = 0; lp < C; ++lp) {
-            float acc = 0.f;
-#pragma unroll
-            for (int l = 0; l < CM; ++l)
-                if (l < C) acc = fmaf(mu[l * C + lp], -dz[l], acc);
-            dm[base + lp * hw] = acc;
-        }
-    } else {
-        // Potts, mu[l][l'] = [l != l']: dm(l') = -(sum_l dZ(l) - dZ(l'))
-#pragma unroll
-        for (int c = 0; c < CM; ++c)
-            if (c < C) dm[base + c * hw] = dz[c] - sum;
-    }
-}
+#if defined(CRF_BWD_K)
 
 // ---------------------------------------------------------- adjoint message
 
@@ -338,42 +296,6 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
     tile_param_sums<NT>(g, a, tile);
 }
 
-// ---------------------------------------------------------------- reduce
-struct ReduceArgs {
-    const float* gpart;
-    const float* kpart;
-    float* out_compat;
-    float* out_kernel;
-    int groups, C, ntiles;
-    float scale[5];
-};
-
-// Block e < C*C folds column e of gpart over its groups rows; block C*C + j
-// folds column j of kpart over its ntiles rows.  Strided per-thread sums,
-// then a tree, all in double.
-__global__ __launch_bounds__(256) void bwd_reduce_kernel(ReduceArgs a) {
-    __shared__ double red[256];
-    const int ne = a.C * a.C;
-    const int e = blockIdx.x;
-    const bool compat = e < ne;
-    if (compat ? !a.out_compat : !a.out_kernel) return;
-    const int rows = compat ? a.groups : a.ntiles;
-    const int stride = compat ? ne : 5;
-    const float* col = compat ? a.gpart + e : a.kpart + (e - ne);
-    double s = 0.0;
-    for (int r = threadIdx.x; r < rows; r += 256) s += (double)col[(long long)r * stride];
-    red[threadIdx.x] = s;
-    __syncthreads();
-    for (int h = 128; h > 0; h >>= 1) {
-        if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) {
-        if (compat) a.out_compat[e] = (float)red[0];
-        else a.out_kernel[e - ne] = (float)(red[0] * (double)a.scale[e - ne]);
-    }
-}
-
 template <int K, int TH, int CM, bool V4, bool FT>
 hipError_t launch_msg_ktc(const BwdArgs& a, hipStream_t stream) {
     const size_t lds = bwd_lds_bytes(K, a.C, TH, V4, FT ? a.D : 0);
@@ -419,6 +341,102 @@ hipError_t launch_msg_k(const BwdArgs& a, hipStream_t stream) {
 
 }  // namespace
 
+#define CONVCRF_BWD_CAT2(a, b) a##b
+#define CONVCRF_BWD_CAT(a, b) CONVCRF_BWD_CAT2(a, b)
+hipError_t CONVCRF_BWD_CAT(launch_bwd_msg_k, CRF_BWD_K)(const BwdArgs& a, hipStream_t stream) {
+    return launch_msg_k<CRF_BWD_K>(a, stream);
+}
+
+}  // namespace convcrf
+
+#else
+
+// ---------------------------------------------------------------- pointwise
+template <int CM>
+__global__ __launch_bounds__(256) void bwd_point_kernel(
+    const float* __restrict__ q, const float* __restrict__ dq, const float* __restrict__ mu,
+    float* __restrict__ du, float* __restrict__ dm, float* __restrict__ dp, int C,
+    long long hw, long long npix, int accumulate) {
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= npix) return;
+    const long long b = i / hw;
+    const long long base = b * C * hw + (i - b * hw);
+    float qv[CM], dz[CM];
+    float dot = 0.f;
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        if (c < C) {
+            qv[c] = q[base + c * hw];
+            dz[c] = dq[base + c * hw];
+            dot = fmaf(qv[c], dz[c], dot);
+        }
+    }
+    float sum = 0.f;
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        if (c < C) {
+            dz[c] = qv[c] * (dz[c] - dot);
+            sum += dz[c];
+            float* o = du + base + c * hw;
+            *o = accumulate ? *o + dz[c] : dz[c];
+            if (dp) dp[base + c * hw] = -dz[c];
+        }
+    }
+    if (!dm) return;
+    if (mu) {
+        for (int lp = 0; lp < C; ++lp) {
+            float acc = 0.f;
+#pragma unroll
+            for (int l = 0; l < CM; ++l)
+                if (l < C) acc = fmaf(mu[l * C + lp], -dz[l], acc);
+            dm[base + lp * hw] = acc;
+        }
+    } else {
+        // Potts, mu[l][l'] = [l != l']: dm(l') = -(sum_l dZ(l) - dZ(l'))
+#pragma unroll
+        for (int c = 0; c < CM; ++c)
+            if (c < C) dm[base + c * hw] = dz[c] - sum;
+    }
+}
+
+// ---------------------------------------------------------------- reduce
+struct ReduceArgs {
+    const float* gpart;
+    const float* kpart;
+    float* out_compat;
+    float* out_kernel;
+    int groups, C, ntiles;
+    float scale[5];
+};
+
+// Block e < C*C folds column e of gpart over its groups rows; block C*C + j
+// folds column j of kpart over its ntiles rows.  Strided per-thread sums,
+// then a tree, all in double.
+__global__ __launch_bounds__(256) void bwd_reduce_kernel(ReduceArgs a) {
+    __shared__ double red[256];
+    const int ne = a.C * a.C;
+    const int e = blockIdx.x;
+    const bool compat = e < ne;
+    if (compat ? !a.out_compat : !a.out_kernel) return;
+    const int rows = compat ? a.groups : a.ntiles;
+    const int stride = compat ? ne : 5;
+    const float* col = compat ? a.gpart + e : a.kpart + (e - ne);
+    double s = 0.0;
+    for (int r = threadIdx.x; r < rows; r += 256) s += (double)col[(long long)r * stride];
+    red[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if (threadIdx.x < h) red[threadIdx.x] += red[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        if (compat) a.out_compat[e] = (float)red[0];
+        else a.out_kernel[e - ne] = (float)(red[0] * (double)a.scale[e - ne]);
+    }
+}
+
+}  // namespace
+
 hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream) {
     if (a.C < 1 || a.C > kMaxC || a.ntiles <= 0) return hipErrorInvalidValue;
     const int D = a.sfeat ? a.D : 0;
@@ -426,14 +444,14 @@ hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream) {
     if (bwd_lds_bytes(k, a.C, D) > 160 * 1024) return hipErrorInvalidValue;
     if (a.vec4 && (!bwd_vec4_fits(k, a.C, D) || a.W % 4 != 0)) return hipErrorInvalidValue;
     switch (k) {
-        case 1: return launch_msg_k<1>(a, stream);
-        case 3: return launch_msg_k<3>(a, stream);
-        case 5: return launch_msg_k<5>(a, stream);
-        case 7: return launch_msg_k<7>(a, stream);
-        case 9: return launch_msg_k<9>(a, stream);
-        case 11: return launch_msg_k<11>(a, stream);
-        case 13: return launch_msg_k<13>(a, stream);
-        case 15: return launch_msg_k<15>(a, stream);
+        case 1: return launch_bwd_msg_k1(a, stream);
+        case 3: return launch_bwd_msg_k3(a, stream);
+        case 5: return launch_bwd_msg_k5(a, stream);
+        case 7: return launch_bwd_msg_k7(a, stream);
+        case 9: return launch_bwd_msg_k9(a, stream);
+        case 11: return launch_bwd_msg_k11(a, stream);
+        case 13: return launch_bwd_msg_k13(a, stream);
+        case 15: return launch_bwd_msg_k15(a, stream);
         default: return hipErrorInvalidValue;
     }
 }
@@ -466,3 +484,5 @@ hipError_t launch_bwd_reduce(const float* gpart, int groups, int C, float* out_c
 }
 
 }  // namespace convcrf
+
+#endif

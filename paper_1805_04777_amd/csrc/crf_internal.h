@@ -291,6 +291,15 @@ constexpr bool bwd_vec4_fits(int k, int C, int D = 0) {
 }
 
 hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream);
+// one per window side k (each compiled in its own object)
+hipError_t launch_bwd_msg_k1(const BwdArgs& a, hipStream_t stream);
+hipError_t launch_bwd_msg_k3(const BwdArgs& a, hipStream_t stream);
+hipError_t launch_bwd_msg_k5(const BwdArgs& a, hipStream_t stream);
+hipError_t launch_bwd_msg_k7(const BwdArgs& a, hipStream_t stream);
+hipError_t launch_bwd_msg_k9(const BwdArgs& a, hipStream_t stream);
+hipError_t launch_bwd_msg_k11(const BwdArgs& a, hipStream_t stream);
+hipError_t launch_bwd_msg_k13(const BwdArgs& a, hipStream_t stream);
+hipError_t launch_bwd_msg_k15(const BwdArgs& a, hipStream_t stream);
 
 // Softmax, unary and compatibility adjoints of one round, per pixel:
 //   dZ = Q (dQ - <Q, dQ>);  du = dZ (+ du when accumulate);
