@@ -725,7 +725,14 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     const convcrf_params p = *params;
     const int k = p.filter_size;
     const int D = p.features ? p.feature_dim : 0;
-    if (bwd_lds_bytes(k, C, D) > kLdsLimit)
+    // staging with buffer loads into LDS needs each image's planes under 2 GB;
+    // it pads every plane to whole 64-float rows, and is used only where that
+    // keeps the tile height (measured: 8-row tiles cost more than the
+    // scalar staging saves)
+    const long long hw_ll = (long long)H * W;
+    const bool dma = (long long)std::max(std::max(3, C), D) * hw_ll * 4 < (1LL << 31) &&
+                     bwd_tile_h(k, C, D, true) == bwd_tile_h(k, C, D, false);
+    if (bwd_lds_need(k, C, D, dma) > kBwdLdsLimit)
         return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
     const long long npix = (long long)B * H * W;
     const size_t qbytes = sizeof(float) * (size_t)npix * C;
@@ -744,7 +751,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     const float scale[5] = {1.f, (float)(p.w_app / (ta * ta * ta)),
                             (float)(p.w_app / (tb * tb * tb)), 1.f,
                             (float)(p.w_smooth / (tg * tg * tg))};
-    const int tw = bwd_tile_w(k), th = bwd_tile_h(k, C, D);
+    const int tw = bwd_tile_w(k), th = bwd_tile_h(k, C, D, dma);
     const long long ntiles_ll = (long long)((W + tw - 1) / tw) * ((H + th - 1) / th) * B;
     if (ntiles_ll > 0x7fffffffLL) return fail(ctx, CONVCRF_E_UNSUPPORTED, "too many tiles");
     const int ntiles = (int)ntiles_ll;
@@ -838,13 +845,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     ba.tiles_per_img = ba.tiles_x * ((H + th - 1) / th);
     ba.ntiles = ntiles;
     ba.include_center = p.include_center;
-    // 16-byte staging: whole vectors per row, every plane 16-byte aligned
-    // (the image and the workspace slices; W % 4 == 0 keeps the planes so)
-    ba.vec4 = bwd_vec4_fits(k, C, D) && W % 4 == 0 &&
-              reinterpret_cast<uintptr_t>(image) % 16 == 0 &&
-              reinterpret_cast<uintptr_t>(p.features) % 16 == 0 &&
-              reinterpret_cast<uintptr_t>(ctx->b_dm.p) % 16 == 0 &&
-              reinterpret_cast<uintptr_t>(qbase) % 16 == 0;
+    ba.dma = dma;
     ba.neg_beta = (float)(-kLog2eD / (2.0 * tb * tb));
     ba.w_app = p.w_app;
     ba.w_smooth = p.w_smooth;

@@ -18,6 +18,7 @@
 // kernels of that k) and once without (the pointwise and reduction kernels
 // and the dispatch over k).
 #include "crf_internal.h"
+#include "lds_dma.h"
 
 namespace convcrf {
 namespace {
@@ -27,39 +28,19 @@ namespace {
 // ---------------------------------------------------------- adjoint message
 
 // Tile plus halo of the 3 colour planes, the D feature planes (FT), the C
-// planes of Q^t and the C planes of dL/dM^t into LDS (LW x LH each, the
-// first staged column is x0, the first row y0); zero outside the image, so
-// that taps there contribute nothing to any sum.  V4: 16-byte vectors (x0
-// and LW multiples of 4, W a multiple of 4, 16-byte aligned planes).
-template <int NT, int LW, int PL, bool V4>
+// planes of Q^t and the C planes of dL/dM^t into LDS (LW x LH each at a
+// stride of PS floats, the first staged column is x0, the first row y0);
+// zero outside the image, so that taps there contribute nothing to any sum.
+//
+// DMA: every wave issues buffer loads that write 64 consecutive floats of a
+// plane straight into LDS (rows of the padded plane, spread over the waves),
+// with an out-of-range offset, which reads zero, for positions outside the
+// image; then waits for all of them.  Otherwise scalar loads through
+// registers, branch-free (an in-image address is read for every element and
+// the value dropped outside) so that many are in flight per thread.
+template <int NT, int LW, int PL, int PS, bool DMA>
 __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b, int y0,
                                              int x0) {
-    if constexpr (V4) {
-        constexpr int LQ = LW / 4, LH = PL / LW;
-        const int C = a.C;
-        const long long hw = (long long)a.H * a.W;
-        const float* fb = a.feat + (long long)b * 3 * hw;
-        const float* qb = a.q + (long long)b * C * hw;
-        const float* mb = a.dm + (long long)b * C * hw;
-        const int D = a.sfeat ? a.D : 0;
-        const float* sb = a.sfeat ? a.sfeat + (long long)b * D * hw : fb;
-        const int nvec = (2 * C + 3 + D) * LH * LQ;
-#pragma unroll 8
-        for (int e = threadIdx.x; e < nvec; e += NT) {
-            const int pl = e / (LH * LQ), o = e - pl * (LH * LQ);
-            const int ly = o / LQ, lq = o - ly * LQ;
-            const int gy = y0 + ly, gx = x0 + 4 * lq;
-            const int pq = pl - 3 - D;
-            const float* src = pl < 3 ? fb + pl * hw
-                                      : (pq < 0 ? sb + (pl - 3) * hw
-                                                : (pq < C ? qb + pq * hw : mb + (pq - C) * hw));
-            const bool ok = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
-            const float4 v = *reinterpret_cast<const float4*>(src + (ok ? (long long)gy * a.W + gx : 0));
-            *reinterpret_cast<float4*>(lds + pl * PL + ly * LW + 4 * lq) =
-                ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-        return;
-    }
     const int C = a.C;
     const long long hw = (long long)a.H * a.W;
     const float* fb = a.feat + (long long)b * 3 * hw;
@@ -67,9 +48,41 @@ __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b
     const float* mb = a.dm + (long long)b * C * hw;
     const int D = a.sfeat ? a.D : 0;
     const float* sb = a.sfeat ? a.sfeat + (long long)b * D * hw : fb;
+    if constexpr (DMA) {
+        constexpr int RP = PS / 64, NW = NT / 64, NS = (RP + NW - 1) / NW;
+        const int H = a.H, W = a.W;
+        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int lane = threadIdx.x & 63;
+        unsigned voff[NS];
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const int f = (wave + NW * s) * 64 + lane;
+            const int ly = f / LW, lx = f - ly * LW;
+            const int gy = y0 + ly, gx = x0 + lx;
+            const bool ok = f < PL && gy >= 0 && gy < H && gx >= 0 && gx < W;
+            voff[s] = ok ? (unsigned)(gy * W + gx) * 4u : kDmaOob;
+        }
+        const unsigned lds0 = (unsigned)(size_t)(__attribute__((address_space(3))) float*)lds;
+        auto issue = [&](rsrc_t r, int p, int lp) {
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                const int jr = wave + NW * s;
+                if (jr < RP)
+                    lds_dma(r, voff[s], (int)(p * hw * 4), lds0 + (unsigned)((lp * PS + jr * 64) * 4));
+            }
+        };
+        const rsrc_t rf = buffer_rsrc(fb, (unsigned)(3 * hw * 4));
+        const rsrc_t rs = buffer_rsrc(sb, (unsigned)((D > 0 ? D : 3) * hw * 4));
+        const rsrc_t rq = buffer_rsrc(qb, (unsigned)(C * hw * 4));
+        const rsrc_t rm = buffer_rsrc(mb, (unsigned)(C * hw * 4));
+        for (int ch = 0; ch < 3; ++ch) issue(rf, ch, ch);
+        for (int c = 0; c < D; ++c) issue(rs, c, 3 + c);
+        for (int c = 0; c < C; ++c) issue(rq, c, 3 + D + c);
+        for (int c = 0; c < C; ++c) issue(rm, c, 3 + D + C + c);
+        __builtin_amdgcn_s_waitcnt(vm_wait(0));
+        return;
+    }
     const int nplanes = 2 * C + 3 + D;
-    // branch-free (an in-image address is read for every element and the
-    // value dropped outside), so that many loads are in flight per thread
 #pragma unroll 16
     for (int e = threadIdx.x; e < nplanes * PL; e += NT) {
         const int pl = e / PL, o = e - pl * PL;
@@ -81,7 +94,7 @@ __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b
                                             : (pq < C ? qb + pq * hw : mb + (pq - C) * hw));
         const bool ok = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
         const float v = src[ok ? (long long)gy * a.W + gx : 0];
-        lds[e] = ok ? v : 0.f;
+        lds[pl * PS + o] = ok ? v : 0.f;
     }
 }
 
@@ -179,25 +192,25 @@ __device__ __forceinline__ void tile_gram(float* lds, const BwdArgs& a, int tile
 // One pixel per thread, 32 x TH tiles up to k = 7 (16 x 8 above).  CM >= C
 // classes are computed without branches: planes past C - 1 read plane C - 1 again and
 // are never stored, and their dL/dM is zero, so they add nothing to dk.
-template <int K, int TH, int CM, bool WM, bool V4, bool FT>
+template <int K, int TH, int CM, bool WM, bool DMA, bool FT>
 __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) {
     constexpr int TW = bwd_tile_w(K), NT = TW * TH;
-    constexpr int R = (K - 1) / 2, LW = bwd_stage_w(K, V4), PL = LW * (TH + K - 1);
-    constexpr int XO = V4 ? 4 : R;   // staged columns left of the tile
-    static_assert(XO >= R, "vector staging needs k <= 9");
+    constexpr int R = (K - 1) / 2, LW = TW + K - 1, PL = LW * (TH + K - 1);
+    constexpr int PS = bwd_plane(K, TH, DMA);   // plane stride in LDS
+    constexpr int XO = R;                       // staged columns left of the tile
     extern __shared__ float lds[];
     const int C = a.C;
     const int D = FT ? a.D : 0;
     const float* sc = lds;               // 3 colour planes
-    const float* sf = lds + 3 * PL;      // D feature planes (FT)
-    const float* sq = sf + D * PL;       // C planes of Q^t
-    const float* sm = sq + C * PL;       // C planes of dL/dM^t
+    const float* sf = lds + 3 * PS;      // D feature planes (FT)
+    const float* sq = sf + D * PS;       // C planes of Q^t
+    const float* sm = sq + C * PS;       // C planes of dL/dM^t
     const int tile = blockIdx.x;
     const int b = tile / a.tiles_per_img;
     const int tr = tile - b * a.tiles_per_img;
     const int ty = tr / a.tiles_x, tx = tr - ty * a.tiles_x;
     const long long hw = (long long)a.H * a.W;
-    stage_planes<NT, LW, PL, V4>(lds, a, b, ty * TH - R, tx * TW - XO);
+    stage_planes<NT, LW, PL, PS, DMA>(lds, a, b, ty * TH - R, tx * TW - XO);
     __syncthreads();
 
     const int lx = threadIdx.x % TW, ly = threadIdx.x / TW;
@@ -210,12 +223,12 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
     for (int c = 0; c < CM; ++c) ma[0][c] = 0.f;
     if (in) {
         const int oc = (ly + R) * LW + lx + XO;
-        const float ir = sc[oc], ig = sc[PL + oc], ib = sc[2 * PL + oc];
+        const float ir = sc[oc], ig = sc[PS + oc], ib = sc[2 * PS + oc];
         float dmq[CM], dqa[CM];
         int poff[CM];
 #pragma unroll
         for (int c = 0; c < CM; ++c) {
-            poff[c] = (c < C ? c : C - 1) * PL;
+            poff[c] = (c < C ? c : C - 1) * PS;
             dmq[c] = c < C ? sm[poff[c] + oc] : 0.f;
             dqa[c] = 0.f;
         }
@@ -223,7 +236,7 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
         float fo[kMaxFeat], dfa[kMaxFeat], qo[FT ? CM : 1];
 #pragma unroll
         for (int c = 0; c < kMaxFeat; ++c) {
-            fo[c] = FT && c < D ? sf[c * PL + oc] : 0.f;
+            fo[c] = FT && c < D ? sf[c * PS + oc] : 0.f;
             dfa[c] = 0.f;
         }
         if constexpr (FT) {
@@ -237,7 +250,7 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
             for (int dx = -R; dx <= R; ++dx) {
                 if (dx == 0 && dy == 0 && !a.include_center) continue;
                 const int o = oc + dy * LW + dx;
-                const float er = ir - sc[o], eg = ig - sc[PL + o], eb = ib - sc[2 * PL + o];
+                const float er = ir - sc[o], eg = ig - sc[PS + o], eb = ib - sc[2 * PS + o];
                 const float cd2 = fmaf(er, er, fmaf(eg, eg, eb * eb));
                 const int n = dx * dx + dy * dy;
                 const float av = exp2f(fmaf(a.neg_beta, cd2, a.a_log2[n]));
@@ -249,7 +262,7 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
                     sd2 = 0.f;
 #pragma unroll
                     for (int c = 0; c < kMaxFeat; ++c) {
-                        fdif[c] = c < D ? fo[c] - sf[c * PL + o] : 0.f;
+                        fdif[c] = c < D ? fo[c] - sf[c * PS + o] : 0.f;
                         sd2 = fmaf(fdif[c], fdif[c], sd2);
                     }
                     sv = exp2f(a.neg_gamma * sd2);
@@ -296,47 +309,45 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
     tile_param_sums<NT>(g, a, tile);
 }
 
-template <int K, int TH, int CM, bool V4, bool FT>
+template <int K, int TH, int CM, bool DMA, bool FT>
 hipError_t launch_msg_ktc(const BwdArgs& a, hipStream_t stream) {
-    const size_t lds = bwd_lds_bytes(K, a.C, TH, V4, FT ? a.D : 0);
+    const size_t lds = bwd_lds_bytes(K, a.C, TH, DMA, FT ? a.D : 0);
     const dim3 block(bwd_tile_w(K) * TH);
     if (a.gpart)
-        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, true, V4, FT>), dim3(a.ntiles), block,
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, true, DMA, FT>), dim3(a.ntiles), block,
                            lds, stream, a);
     else
-        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, false, V4, FT>), dim3(a.ntiles), block,
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, false, DMA, FT>), dim3(a.ntiles), block,
                            lds, stream, a);
     return hipGetLastError();
 }
 
 template <int K, int TH, int CM>
 hipError_t launch_msg_ktv(const BwdArgs& a, hipStream_t stream) {
-    if constexpr (K <= 7) {
-        if (a.vec4) {
-            if (a.sfeat) return launch_msg_ktc<K, TH, CM, true, true>(a, stream);
-            return launch_msg_ktc<K, TH, CM, true, false>(a, stream);
-        }
+    if (a.dma) {
+        if (a.sfeat) return launch_msg_ktc<K, TH, CM, true, true>(a, stream);
+        return launch_msg_ktc<K, TH, CM, true, false>(a, stream);
     }
     if (a.sfeat) return launch_msg_ktc<K, TH, CM, false, true>(a, stream);
     return launch_msg_ktc<K, TH, CM, false, false>(a, stream);
 }
 
+template <int K, int TH>
+hipError_t launch_msg_kt(const BwdArgs& a, hipStream_t stream) {
+    if (a.C <= 8) return launch_msg_ktv<K, TH, 8>(a, stream);
+    if (a.C <= 21) return launch_msg_ktv<K, TH, 21>(a, stream);
+    return launch_msg_ktv<K, TH, kMaxC>(a, stream);
+}
+
 // The host derives the tiling (tiles_x, tiles_per_img, ntiles) from the
-// same bwd_tile_w / bwd_tile_h, and vec4 from bwd_vec4_fits.
+// same bwd_tile_w / bwd_tile_h.
 template <int K>
 hipError_t launch_msg_k(const BwdArgs& a, hipStream_t stream) {
-    if (a.C <= 8) {
-        if constexpr (K <= 7) return launch_msg_ktv<K, 16, 8>(a, stream);
-        else return launch_msg_ktv<K, 8, 8>(a, stream);
-    }
     if constexpr (K <= 7) {
-        if (bwd_tile_h(K, a.C, a.sfeat ? a.D : 0) == 8)
-            return launch_msg_ktv<K, 8, kMaxC>(a, stream);
-        if (a.C <= 21) return launch_msg_ktv<K, 16, 21>(a, stream);
-        return launch_msg_ktv<K, 16, kMaxC>(a, stream);
-    } else {
-        return launch_msg_ktv<K, 8, kMaxC>(a, stream);
+        if (bwd_tile_h(K, a.C, a.sfeat ? a.D : 0, a.dma != 0) == 16)
+            return launch_msg_kt<K, 16>(a, stream);
     }
+    return launch_msg_kt<K, 8>(a, stream);
 }
 
 }  // namespace
@@ -441,8 +452,11 @@ hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream) {
     if (a.C < 1 || a.C > kMaxC || a.ntiles <= 0) return hipErrorInvalidValue;
     const int D = a.sfeat ? a.D : 0;
     if (a.sfeat && (a.D < 1 || a.D > kMaxFeat || !a.dfeat)) return hipErrorInvalidValue;
-    if (bwd_lds_bytes(k, a.C, D) > 160 * 1024) return hipErrorInvalidValue;
-    if (a.vec4 && (!bwd_vec4_fits(k, a.C, D) || a.W % 4 != 0)) return hipErrorInvalidValue;
+    if (bwd_lds_need(k, a.C, D, a.dma != 0) > kBwdLdsLimit) return hipErrorInvalidValue;
+    // buffer offsets of the DMA staging stay under 2 GB
+    const long long hw = (long long)a.H * a.W;
+    const int mp = a.C > 3 ? (a.C > D ? a.C : D) : (3 > D ? 3 : D);
+    if (a.dma && (long long)mp * hw * 4 >= (1LL << 31)) return hipErrorInvalidValue;
     switch (k) {
         case 1: return launch_bwd_msg_k1(a, stream);
         case 3: return launch_bwd_msg_k3(a, stream);

@@ -247,7 +247,8 @@ struct BwdArgs {
     int tiles_x, tiles_per_img, ntiles;
     int include_center;
     int accumulate;
-    int vec4;            // stage 16-byte vectors (see bwd_stage_vec4)
+    int dma;             // stage with buffer loads into LDS (each image's
+                         // planes under 2 GB; see bwd_plane)
     float neg_beta;      // -log2(e) / (2 theta_beta^2)
     float w_app, w_smooth;
     float a_log2[kMaxN + 1];    // -n log2(e) / (2 theta_alpha^2)
@@ -261,33 +262,30 @@ struct BwdArgs {
 // is reused afterwards for the tile's dp and M, C rounded up to a multiple
 // of 3, one row of tile pixels plus one each, and for the partial sums of
 // the 3 x 3 blocks (9 per thread).
-// With vec4 (k <= 7, W a multiple of 4, 16-byte aligned planes) the staged
-// rows start 4 columns left of the tile and hold tile width + 8 columns, so
-// that every 16-byte vector lies wholly inside or outside the image.
+// Staged with buffer loads into LDS (dma), each plane is padded to whole
+// 64-float rows of loads.  160 KB of LDS less 256 bytes for the static
+// partial sums.
 constexpr int bwd_tile_w(int k) { return k <= 7 ? 32 : 16; }
 constexpr int bwd_gram_rows(int C) { return (C + 2) / 3 * 3; }
-constexpr int bwd_stage_w(int k, bool vec4) {
-    return vec4 ? bwd_tile_w(k) + 8 : bwd_tile_w(k) + k - 1;
+constexpr int bwd_plane(int k, int rows, bool dma) {
+    return dma ? ((bwd_tile_w(k) + k - 1) * (rows + k - 1) + 63) / 64 * 64
+               : (bwd_tile_w(k) + k - 1) * (rows + k - 1);
 }
-constexpr size_t bwd_lds_bytes(int k, int C, int rows, bool vec4 = false, int D = 0) {
-    const size_t stage = (size_t)(2 * C + 3 + D) * bwd_stage_w(k, vec4) * (rows + k - 1);
+constexpr size_t bwd_lds_bytes(int k, int C, int rows, bool dma, int D) {
+    const size_t stage = (size_t)(2 * C + 3 + D) * bwd_plane(k, rows, dma);
     const size_t nt = (size_t)bwd_tile_w(k) * rows;
     const size_t gram = 2 * (size_t)bwd_gram_rows(C) * (nt + 1);
     const size_t red = 9 * nt;
     const size_t g = gram > red ? gram : red;
     return sizeof(float) * (stage > g ? stage : g);
 }
+constexpr size_t kBwdLdsLimit = 160 * 1024 - 256;
 // D: learnable smoothness feature planes staged besides (0 without).
-constexpr int bwd_tile_h(int k, int C, int D = 0) {
-    return k <= 7 && bwd_lds_bytes(k, C, 16, false, D) <= 160 * 1024 ? 16 : 8;
+constexpr int bwd_tile_h(int k, int C, int D, bool dma) {
+    return k <= 7 && bwd_lds_bytes(k, C, 16, dma, D) <= kBwdLdsLimit ? 16 : 8;
 }
-inline size_t bwd_lds_bytes(int k, int C, int D = 0) {
-    return bwd_lds_bytes(k, C, bwd_tile_h(k, C, D), false, D);
-}
-// whether the vec4 staging is built for (k, C, D feature planes) and fits
-// the LDS
-constexpr bool bwd_vec4_fits(int k, int C, int D = 0) {
-    return k <= 7 && bwd_lds_bytes(k, C, bwd_tile_h(k, C, D), true, D) <= 160 * 1024 - 256;
+inline size_t bwd_lds_need(int k, int C, int D, bool dma) {
+    return bwd_lds_bytes(k, C, bwd_tile_h(k, C, D, dma), dma, D);
 }
 
 hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream);

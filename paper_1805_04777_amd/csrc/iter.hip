@@ -25,6 +25,7 @@
 // (Sec. 4.2).
 
 #include "crf_internal.h"
+#include "lds_dma.h"
 
 #ifndef CRF_K
 #error "compile with -DCRF_K=<odd window side>"
@@ -631,13 +632,6 @@ hipError_t launch_res(const IterArgs& a, TileConfig t, size_t lds, int num_cus,
 }
 
 // ------------------------------------------------------------ streamed update
-// s_waitcnt operand that waits until at most n vector-memory operations of
-// the wave are outstanding (gfx9 encoding; expcnt and lgkmcnt untouched).
-constexpr int vm_wait(int n) {
-    const int v = n < 0 ? 0 : (n > 63 ? 63 : n);
-    return (v & 15) | (v >> 4) << 14 | 7 << 4 | 15 << 8;
-}
-
 // f(integral_constant<int, 0>), ..., f(integral_constant<int, N - 1>)
 template <typename F, int... I>
 __device__ __forceinline__ void static_for(F&& f, std::integer_sequence<int, I...>) {
@@ -663,40 +657,6 @@ __device__ __forceinline__ void static_for(F&& f, std::integer_sequence<int, I..
 // a dummy LDS row), so that a wave waits for a chunk with one constant
 // vmcnt.  Pixels outside the image get an out-of-range buffer offset, which
 // reads as zero: neighbours outside the image contribute nothing.
-// One 64-lane buffer load into LDS: lane l writes the dword at byte offset
-// voffset + soffset of the buffer (zero when out of range) to LDS byte
-// lds_base + 4 l.  Written as assembly so that the compiler neither counts
-// it nor waits for it before LDS reads of other rows: the caller waits with
-// an explicit vmcnt and a work-group barrier before reading what it wrote.
-typedef int rsrc_t __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ void lds_dma(rsrc_t rsrc, unsigned voffset, int soffset,
-                                        unsigned lds_base) {
-    asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dword %0, %1, %2 offen lds"
-                 :
-                 : "v"(voffset), "s"(rsrc), "s"(soffset), "s"(lds_base)
-                 : "memory", "m0");
-}
-
-// The same with 16 bytes per lane (LDS byte lds_base + 16 l); voffset and
-// soffset must be multiples of 16.
-__device__ __forceinline__ void lds_dma16(rsrc_t rsrc, unsigned voffset, int soffset,
-                                          unsigned lds_base) {
-    asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
-                 :
-                 : "v"(voffset), "s"(rsrc), "s"(soffset), "s"(lds_base)
-                 : "memory", "m0");
-}
-
-__device__ __forceinline__ rsrc_t buffer_rsrc(const float* base, unsigned bytes) {
-    const unsigned long long p = reinterpret_cast<unsigned long long>(base);
-    rsrc_t r;
-    r.x = (int)(unsigned)p;
-    r.y = (int)(unsigned)(p >> 32);            // stride 0
-    r.z = (int)bytes;                           // num_records
-    r.w = 0x00020000;                           // raw dword access
-    return r;
-}
-
 // Loads per wave of chunk k (classes [k CH, min((k + 1) CH, C))), 0 past
 // the last chunk.
 constexpr int stream_chunk_loads(int k, int C, int CH, int NJ) {
