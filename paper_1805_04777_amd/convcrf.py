@@ -106,6 +106,9 @@ def load_library(path: str = LIB_PATH):
     global _lib
     if _lib is not None:
         return _lib
+    # torch first: the library then binds the HIP runtime torch has loaded,
+    # rather than a second copy that would not see torch's devices
+    import torch  # noqa: F401
     if not os.path.exists(path):
         raise ConvCRFError(E_NO_DEVICE, f"{path} is not built; run "
                            "`python -m paper_1805_04777_amd.build`")
