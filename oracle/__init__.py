@@ -183,7 +183,7 @@ def meanfield(U, I, params: OracleParams, iters: int, compat=None, features=None
 
 def meanfield_backward(U, I, params: OracleParams, iters: int, G, compat=None,
                        features=None):
-    """Reverse-mode derivative of ``meanfield`` (no blur) for a loss whose
+    """Reverse-mode derivative of ``meanfield`` for a loss whose
     derivative with respect to the returned Q is G [B,C,H,W].  Returns
     (dU [B,C,H,W], dmu [C,C], dparams [5] in PARAM_NAMES order); dmu is the
     derivative with respect to the compatibility at ``compat`` (Potts when

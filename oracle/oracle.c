@@ -291,7 +291,7 @@ int oracle_meanfield(const double *U, const double *I, int B, int C, int H, int 
 }
 
 /* ------------------------------------------------------------------------
- * Reverse-mode derivative of oracle_meanfield without blur (s = 1).
+ * Reverse-mode derivative of oracle_meanfield.
  *
  * The loss is a scalar L whose derivative with respect to the returned Q^T
  * is G.  Every round of Alg. 1 is undone in reverse order, each step being
@@ -319,7 +319,10 @@ int oracle_meanfield(const double *U, const double *I, int B, int C, int H, int 
  * dU [B][C][H][W] is written; dmu (C*C, row-major, the derivative with
  * respect to mu at the given mu, Potts included) and dparams (5 values in
  * the order above) are written when not NULL, summed over the batch.
- * Returns 0, or -1 on arguments outside the definition (blur included).
+ * With blur s > 1 the message is the pooled one (the pooled Q^t's message
+ * on the pooled grid, bilinearly upsampled), undone as the transpose of the
+ * upsampling, the pooled message transposed, and the transpose of the
+ * pooling.  Returns 0, or -1 on arguments outside the definition.
  * ------------------------------------------------------------------------ */
 
 /* dK(p,q)/d(parameter) for the five Eq. 4 parameters; smo_d2 is the
@@ -348,7 +351,8 @@ static int in_window(int py, int px, int qy, int qx, int r, int include_center)
 /* Transpose of the Eq. 6 message for one image: dQ_q(l) = sum over the
  * pixels p whose window holds q of K(p,q) dM_p(l). */
 static void message_transpose(const double *dM, const double *I, const double *F, int d,
-                              int C, int H, int W, const oracle_params *p, double *dQ)
+                              int C, int H, int W, const oracle_params *p, double pos_scale,
+                              double *dQ)
 {
     const int r = (p->filter_size - 1) / 2;
     const long HW = (long)H * W;
@@ -370,7 +374,7 @@ static void message_transpose(const double *dM, const double *I, const double *F
                         double e = I[ch * HW + pi] - I[ch * HW + qi];
                         col += e * e;
                     }
-                    double dy = py - qy, dx = px - qx;
+                    double dy = pos_scale * (py - qy), dx = pos_scale * (px - qx);
                     double pos = dy * dy + dx * dx;
                     double kpq = kernel_eval(pos, col, smooth_d2(F, d, HW, pi, qi, pos), p);
                     for (int l = 0; l < C; ++l) dQ[l * HW + qi] += kpq * dM[l * HW + pi];
@@ -384,7 +388,7 @@ static void message_transpose(const double *dM, const double *I, const double *F
  * dK(p,q) * dK(p,q)/d(parameter), dK(p,q) = sum_l dM_p(l) Q_q(l). */
 static void message_param_grad(const double *dM, const double *Q, const double *I,
                                const double *F, int d, int C, int H, int W,
-                               const oracle_params *p, double acc[5])
+                               const oracle_params *p, double pos_scale, double acc[5])
 {
     const int r = (p->filter_size - 1) / 2;
     const long HW = (long)H * W;
@@ -402,7 +406,7 @@ static void message_param_grad(const double *dM, const double *Q, const double *
                         double e = I[ch * HW + pi] - I[ch * HW + qi];
                         col += e * e;
                     }
-                    double dy = qy - py, dx = qx - px;
+                    double dy = pos_scale * (qy - py), dx = pos_scale * (qx - px);
                     double pos = dy * dy + dx * dx;
                     double g[5];
                     kernel_param_derivs(pos, col, smooth_d2(F, d, HW, pi, qi, pos), p, g);
@@ -448,6 +452,44 @@ static void message_feature_grad(const double *dM, const double *Q, const double
     }
 }
 
+/* Transpose of oracle_upsample for `nch` planes: every full-resolution
+ * value Y[y][x] is sent back to the (up to four) pooled cells it was
+ * interpolated from, with the same weights.  X [nch][Hp][Wp] is overwritten. */
+static void upsample_transpose(const double *Y, int nch, int Hp, int Wp, int s, double *X)
+{
+    const int H = Hp * s, W = Wp * s;
+    memset(X, 0, sizeof(double) * (size_t)nch * Hp * Wp);
+    for (int c = 0; c < nch; ++c)
+        for (int y = 0; y < H; ++y) {
+            int y0, y1;
+            double fy;
+            src_coord(y, s, Hp, &y0, &y1, &fy);
+            for (int x = 0; x < W; ++x) {
+                int x0, x1;
+                double fx;
+                src_coord(x, s, Wp, &x0, &x1, &fx);
+                const double v = Y[((long)c * H + y) * W + x];
+                double *P = X + (long)c * Hp * Wp;
+                P[y0 * Wp + x0] += (1.0 - fy) * (1.0 - fx) * v;
+                P[y0 * Wp + x1] += (1.0 - fy) * fx * v;
+                P[y1 * Wp + x0] += fy * (1.0 - fx) * v;
+                P[y1 * Wp + x1] += fy * fx * v;
+            }
+        }
+}
+
+/* Transpose of oracle_avgpool: each full-resolution pixel receives its
+ * cell's value divided by s^2.  X [nch][H][W] is overwritten. */
+static void avgpool_transpose(const double *Y, int nch, int H, int W, int s, double *X)
+{
+    const int Hp = H / s, Wp = W / s;
+    for (int c = 0; c < nch; ++c)
+        for (int y = 0; y < H; ++y)
+            for (int x = 0; x < W; ++x)
+                X[((long)c * H + y) * W + x] =
+                    Y[((long)c * Hp + y / s) * Wp + x / s] / (double)(s * s);
+}
+
 /* Derivative of the softmax of one pixel: dz(l) = q(l) (dq(l) - <q, dq>). */
 static void softmax_adjoint_pixel(const double *q, const double *dq, long s, double *dz,
                                   long zs, int C)
@@ -465,16 +507,27 @@ int oracle_meanfield_backward_f(const double *U, const double *I, const double *
                                 double *dmu, double *dparams, double *dF)
 {
     if (B < 0 || C < 1 || H < 1 || W < 1 || T < 0 || !p) return -1;
-    if (p->filter_size < 1 || (p->filter_size & 1) == 0 || p->blur != 1) return -1;
+    if (p->filter_size < 1 || (p->filter_size & 1) == 0) return -1;
+    const int s = p->blur;
+    if (s < 1 || H % s || W % s || (F && s != 1)) return -1;
     if (C > 64 || (F && d < 1)) return -1;
     const long HW = (long)H * W;
     const long n = (long)C * HW;
+    const int Hp = H / s, Wp = W / s;
+    const long np = (long)C * Hp * Wp;
     double *Qs = (double *)malloc(sizeof(double) * (size_t)(T + 1) * n);
     double *Ms = (double *)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1) * n);
     double *dQ = (double *)malloc(sizeof(double) * n);
     double *dQprev = (double *)malloc(sizeof(double) * n);
     double *dP = (double *)malloc(sizeof(double) * n);
     double *dM = (double *)malloc(sizeof(double) * n);
+    /* blur: pooled Q^t and message of every round, pooled image, and the
+     * pooled derivatives */
+    double *Qps = s > 1 ? (double *)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1) * np) : NULL;
+    double *Mp = s > 1 ? (double *)malloc(sizeof(double) * np) : NULL;
+    double *Ip = s > 1 ? (double *)malloc(sizeof(double) * 3 * Hp * Wp) : NULL;
+    double *dMp = s > 1 ? (double *)malloc(sizeof(double) * np) : NULL;
+    double *dQp = s > 1 ? (double *)malloc(sizeof(double) * np) : NULL;
     if (dmu) memset(dmu, 0, sizeof(double) * (size_t)C * C);
     if (dparams) memset(dparams, 0, sizeof(double) * 5);
 
@@ -485,10 +538,17 @@ int oracle_meanfield_backward_f(const double *U, const double *I, const double *
         double *dFb = F && dF ? dF + (long)b * d * HW : NULL;
         double *dUb = dU + (long)b * n;
         if (dFb) memset(dFb, 0, sizeof(double) * (size_t)d * HW);
-        /* forward, keeping every Q^t and M^t */
+        /* forward, keeping every Q^t and M^t (and the pooled Q^t with blur) */
         oracle_softmax(Ub, C, H, W, Qs);
+        if (s > 1) oracle_avgpool(Ib, 3, H, W, s, Ip);
         for (int t = 0; t < T; ++t) {
-            message_f(Qs + (long)t * n, Ib, Fb, d, C, H, W, p, 1.0, Ms + (long)t * n);
+            if (s == 1) {
+                message_f(Qs + (long)t * n, Ib, Fb, d, C, H, W, p, 1.0, Ms + (long)t * n);
+            } else {
+                oracle_avgpool(Qs + (long)t * n, C, H, W, s, Qps + (long)t * np);
+                message_f(Qps + (long)t * np, Ip, NULL, 0, C, Hp, Wp, p, (double)s, Mp);
+                oracle_upsample(Mp, C, Hp, Wp, s, Ms + (long)t * n);
+            }
             oracle_update(Ub, Ms + (long)t * n, mu, C, HW, Qs + (long)(t + 1) * n);
         }
         /* reverse */
@@ -522,9 +582,20 @@ int oracle_meanfield_backward_f(const double *U, const double *I, const double *
                         for (long i = 0; i < HW; ++i) acc += dP[l * HW + i] * Mt[lp * HW + i];
                         dmu[l * C + lp] += acc;
                     }
-            if (dparams) message_param_grad(dM, Qt, Ib, Fb, d, C, H, W, p, dparams);
-            if (dFb) message_feature_grad(dM, Qt, Fb, d, C, H, W, p, dFb);
-            message_transpose(dM, Ib, Fb, d, C, H, W, p, dQprev);
+            if (s == 1) {
+                if (dparams) message_param_grad(dM, Qt, Ib, Fb, d, C, H, W, p, 1.0, dparams);
+                if (dFb) message_feature_grad(dM, Qt, Fb, d, C, H, W, p, dFb);
+                message_transpose(dM, Ib, Fb, d, C, H, W, p, 1.0, dQprev);
+            } else {
+                /* M = upsample(pooled message of avgpool(Q^t)): undo the
+                 * upsampling, the pooled message, then the pooling */
+                upsample_transpose(dM, C, Hp, Wp, s, dMp);
+                if (dparams)
+                    message_param_grad(dMp, Qps + (long)t * np, Ip, NULL, 0, C, Hp, Wp, p,
+                                       (double)s, dparams);
+                message_transpose(dMp, Ip, NULL, 0, C, Hp, Wp, p, (double)s, dQp);
+                avgpool_transpose(dQp, C, H, W, s, dQprev);
+            }
             memcpy(dQ, dQprev, sizeof(double) * n);
         }
         for (long i = 0; i < HW; ++i) {
@@ -539,6 +610,11 @@ int oracle_meanfield_backward_f(const double *U, const double *I, const double *
     free(dQprev);
     free(dP);
     free(dM);
+    free(Qps);
+    free(Mp);
+    free(Ip);
+    free(dMp);
+    free(dQp);
     return 0;
 }
 

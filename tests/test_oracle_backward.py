@@ -137,7 +137,53 @@ def test_gradient_of_zero_pairwise_weights_is_softmax_adjoint():
     np.testing.assert_allclose(dU, want, rtol=1e-12, atol=1e-14)
 
 
-def test_blur_is_rejected():
-    U, I, G, _ = _problem(13, 1, 2, 4, 4, False)
-    with pytest.raises(ValueError):
-        orc.meanfield_backward(U, I, orc.OracleParams(filter_size=3, blur=2), 1, G)
+BLUR_CASES = [
+    # (seed, B, C, H, W, k, T, s, include_center, general mu)
+    (13, 1, 3, 6, 8, 3, 2, 2, False, True),
+    (14, 2, 2, 8, 8, 3, 1, 4, True, False),
+    (15, 1, 3, 6, 9, 5, 2, 3, False, False),
+]
+
+
+@pytest.mark.parametrize("seed,B,C,H,W,k,T,s,center,gen_mu", BLUR_CASES)
+def test_blur_gradient_matches_finite_differences(seed, B, C, H, W, k, T, s, center, gen_mu):
+    """The pooled message (Sec. 4.2 blur): every unary, every compatibility
+    entry and every Eq. 4 parameter against central finite differences."""
+    U, I, G, mu = _problem(seed, B, C, H, W, gen_mu)
+    vals = dict(w_app=4.0, theta_alpha=3.0, theta_beta=30.0, w_smooth=1.5, theta_gamma=1.2)
+    params = orc.OracleParams(filter_size=k, blur=s, include_center=center, **vals)
+    dU, dmu, dp = orc.meanfield_backward(U, I, params, T, G, compat=mu)
+    fd = np.empty_like(U)
+    for idx in np.ndindex(U.shape):
+        def f(v):
+            Up = U.copy()
+            Up[idx] = v
+            return _loss(Up, I, params, T, G, mu)
+        fd[idx] = _fd(f, U[idx], 1e-5)
+    np.testing.assert_allclose(dU, fd, rtol=0, atol=1e-7 * max(1.0, np.abs(fd).max()))
+    base = mu if mu is not None else 1.0 - np.eye(C)
+    fdm = np.empty((C, C))
+    for a in range(C):
+        for b in range(C):
+            def g(v):
+                m = base.copy()
+                m[a, b] = v
+                return _loss(U, I, params, T, G, m)
+            fdm[a, b] = _fd(g, base[a, b], 1e-6)
+    assert np.abs(fdm).max() > 1e-4
+    np.testing.assert_allclose(dmu, fdm, rtol=0, atol=1e-7 * max(1.0, np.abs(fdm).max()))
+    for j, name in enumerate(orc.PARAM_NAMES):
+        h = 1e-6 * vals[name]
+        def q(v):
+            return _loss(U, I, orc.OracleParams(filter_size=k, blur=s, include_center=center,
+                                                **dict(vals, **{name: v})), T, G, mu)
+        fdp = _fd(q, vals[name], h)
+        assert abs(fdp - dp[j]) <= 2e-6 * abs(fdp) + 1e-9, (name, fdp, dp[j])
+
+
+def test_blur_of_one_is_the_unpooled_derivative():
+    U, I, G, mu = _problem(16, 1, 3, 6, 6, True)
+    a = orc.meanfield_backward(U, I, orc.OracleParams(filter_size=3), 2, G, compat=mu)
+    b = orc.meanfield_backward(U, I, orc.OracleParams(filter_size=3, blur=1), 2, G, compat=mu)
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
