@@ -105,6 +105,11 @@ def algorithmic_per_launch(kname: str, wl, D: int = 0):
         return 0, 0
     # reverse mode (compatibility and kernel-parameter derivatives requested)
     taps = k * k - 1
+    if kname == "bwd_message" and wl.blur > 1:
+        # on the pooled grid (the derivative of the blur variant): as above
+        # per pooled cell
+        npx = px // (wl.blur * wl.blur)
+        return (6 * C + 22) * taps * npx + 2 * C * C * npx, (16 * C + 12) * npx
     if kname == "feature_iter":
         # per tap: the appearance weight (12), the feature distance and its
         # Gaussian (3D + 2), the message (2C); per pixel unary add and softmax
@@ -254,9 +259,6 @@ def main(argv=None):
     crf = cc.ConvCRF(0)
     stream = torch.cuda.current_stream(dev)
     if args.backward:
-        if wl.blur != 1:
-            print("bench.py: the reverse mode is built for blur = 1 only", file=sys.stderr)
-            return 2
         import numpy as np
         Gt = torch.from_numpy(np.random.default_rng(77).normal(
             0.0, 1.0, U.shape).astype(np.float32)).to(dev)

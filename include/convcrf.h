@@ -153,8 +153,8 @@ convcrf_status convcrf_meanfield(convcrf_ctx *ctx, const float *unary,
                                  int W, const convcrf_params *params,
                                  int iters, float *q_out, void *stream);
 
-/* Reverse mode: the derivative of a scalar loss L through convcrf_meanfield
- * (no blur), for training the CRF by backpropagation through the unrolled
+/* Reverse mode: the derivative of a scalar loss L through convcrf_meanfield,
+ * for training the CRF by backpropagation through the unrolled
  * mean-field rounds of Alg. 1 (Sec. 1; Sec. 5.3 trains end to end through
  * five rounds).  The learnable parameters are the Eq. 4 weights and scales
  * (Sec. 3) and the compatibility (Sec. 4.2).  Given grad_q = dL/dQ for the
@@ -174,6 +174,9 @@ convcrf_status convcrf_meanfield(convcrf_ctx *ctx, const float *unary,
  * message transposed, which is the message itself applied to dL/dM because
  * K(p,q) = K(q,p) and the window is symmetric; the kernel-parameter terms are
  * sum over p and window neighbours q of (sum_l dL/dM_p(l) Q_q(l)) dK(p,q)/d;
+ * with blur s the message is the pooled one, undone as the transpose of the
+ * bilinear upsampling, the adjoint message on the pooled grid (offsets of s
+ * pixels) and the transpose of the average pooling;
  * with learnable features, dK/dF_p = -w_smooth S (F_p - F_q)/theta_gamma^2
  * = -dK/dF_q, gathered per pixel from both ends of every pair.
  * The forward rounds are recomputed inside the call (the unaries, image and
@@ -183,9 +186,9 @@ convcrf_status convcrf_meanfield(convcrf_ctx *ctx, const float *unary,
  * The context's workspace grows by (iters + 1) + 3 buffers of [B][C][H][W]
  * floats (Q^0..Q^T, two for dL/dQ, dL/dM), one more with grad_compat, and
  * per-tile partial sums.
- * Returns CONVCRF_E_UNSUPPORTED for blur != 1 or when the window and classes
- * exceed the LDS of one work-group (2C + 3 planes of the tile plus halo);
- * otherwise as convcrf_meanfield.  Asynchronous on `stream`. */
+ * Returns CONVCRF_E_UNSUPPORTED when the window and classes exceed the LDS of
+ * one work-group (2C + 3 planes of the tile plus halo); otherwise as
+ * convcrf_meanfield.  Asynchronous on `stream`. */
 convcrf_status convcrf_meanfield_backward(convcrf_ctx *ctx, const float *unary,
                                           const float *image, int B, int C,
                                           int H, int W,

@@ -218,7 +218,7 @@ class ConvCRF:
     def meanfield_backward(self, unary, image, params: Params, iters: int, grad_q,
                            grad_compat: bool = False, grad_kernel: bool = False,
                            out=None, stream=None):
-        """Derivative of a loss through ``meanfield`` (no blur): returns
+        """Derivative of a loss through ``meanfield``: returns
         (dL/dU [B,C,H,W], dL/dmu [C,C] or None, dL/d(Eq. 4 parameters) [5]
         or None) as float32 tensors on the unary's device, and with
         ``params.features`` a fourth value, dL/dfeatures; ``grad_q`` is

@@ -52,8 +52,9 @@ struct convcrf_ctx {
     bool coop = false;              // cooperative launches supported
     std::string err = "no error";
     DevBuf q_ws, q_ws2, kmat, pool_q, pool_m, pool_f, mu, sync;
-    // reverse mode: Q^0..Q^T, dL/dQ ping-pong, dL/dM, -dL/dZ, per-tile sums
-    DevBuf b_q, b_dq, b_dm, b_dp, b_gpart, b_kpart, b_df;
+    // reverse mode: Q^0..Q^T, dL/dQ ping-pong, dL/dM, -dL/dZ, per-tile sums,
+    // dL/dF when not requested, the pooled derivatives (blur)
+    DevBuf b_q, b_dq, b_dm, b_dp, b_gpart, b_kpart, b_df, b_pd;
     std::vector<float> mu_last;   // host copy of the uploaded compatibility
     float* mu_pinned = nullptr;   // pinned staging for the upload
     size_t mu_pinned_cap = 0;
@@ -441,7 +442,8 @@ void convcrf_destroy(convcrf_ctx* ctx) {
     (void)hipDeviceSynchronize();
     for (DevBuf* b : {&ctx->q_ws, &ctx->q_ws2, &ctx->kmat, &ctx->pool_q, &ctx->pool_m,
                       &ctx->pool_f, &ctx->mu, &ctx->sync, &ctx->b_q, &ctx->b_dq, &ctx->b_dm,
-                      &ctx->b_dp, &ctx->b_gpart, &ctx->b_kpart, &ctx->b_df})
+                      &ctx->b_dp, &ctx->b_gpart, &ctx->b_kpart, &ctx->b_df,
+                      &ctx->b_pd})
         if (b->p) (void)hipFree(b->p);
     if (ctx->mu_pinned) (void)hipHostFree(ctx->mu_pinned);
     if (ctx->mu_copied) (void)hipEventDestroy(ctx->mu_copied);
@@ -720,16 +722,18 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     if (!ctx) return fail(nullptr, CONVCRF_E_INVALID_ARG, "ctx is NULL");
     convcrf_status st = validate(ctx, B, C, H, W, params, iters);
     if (st != CONVCRF_OK) return st;
-    if (params->blur != 1)
-        return fail(ctx, CONVCRF_E_UNSUPPORTED, "the derivative is built for blur = 1 only");
     const convcrf_params p = *params;
     const int k = p.filter_size;
     const int D = p.features ? p.feature_dim : 0;
+    // the adjoint message runs on the grid of the message: the image, or
+    // with blur s the s x s pooled grid (offsets of s pixels)
+    const int s = p.blur;
+    const int Hg = H / s, Wg = W / s;
     // staging with buffer loads into LDS needs each image's planes under 2 GB;
     // it pads every plane to whole 64-float rows, and is used only where that
     // keeps the tile height (measured: 8-row tiles cost more than the
     // scalar staging saves)
-    const long long hw_ll = (long long)H * W;
+    const long long hw_ll = (long long)Hg * Wg;
     const bool dma = (long long)std::max(std::max(3, C), D) * hw_ll * 4 < (1LL << 31) &&
                      bwd_tile_h(k, C, D, true) == bwd_tile_h(k, C, D, false);
     if (bwd_lds_need(k, C, D, dma) > kBwdLdsLimit)
@@ -748,11 +752,14 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
 
     const double ta = p.theta_alpha, tb = p.theta_beta, tg = p.theta_gamma;
-    const float scale[5] = {1.f, (float)(p.w_app / (ta * ta * ta)),
+    // the kernel sums grid offsets n = dx^2 + dy^2; the squared distance in
+    // pixels is s^2 n
+    const double s2 = (double)s * s;
+    const float scale[5] = {1.f, (float)(s2 * p.w_app / (ta * ta * ta)),
                             (float)(p.w_app / (tb * tb * tb)), 1.f,
-                            (float)(p.w_smooth / (tg * tg * tg))};
+                            (float)(s2 * p.w_smooth / (tg * tg * tg))};
     const int tw = bwd_tile_w(k), th = bwd_tile_h(k, C, D, dma);
-    const long long ntiles_ll = (long long)((W + tw - 1) / tw) * ((H + th - 1) / th) * B;
+    const long long ntiles_ll = (long long)((Wg + tw - 1) / tw) * ((Hg + th - 1) / th) * B;
     if (ntiles_ll > 0x7fffffffLL) return fail(ctx, CONVCRF_E_UNSUPPORTED, "too many tiles");
     const int ntiles = (int)ntiles_ll;
     const bool run = npix > 0 && iters > 0;
@@ -791,6 +798,15 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         if (p.features && !grad_features &&
             (st = ensure(ctx, ctx->b_df, sizeof(float) * (size_t)npix * D)) != CONVCRF_OK)
             return st;
+        if (s > 1) {
+            // pooled image, pooled Q^t, pooled message, and the pooled dL/dM,
+            // -dL/dZ and dL/dQ
+            const size_t pb = sizeof(float) * (size_t)B * Hg * Wg;
+            if ((st = ensure(ctx, ctx->pool_f, pb * 3)) != CONVCRF_OK) return st;
+            if ((st = ensure(ctx, ctx->pool_q, pb * C)) != CONVCRF_OK) return st;
+            if ((st = ensure(ctx, ctx->pool_m, pb * C)) != CONVCRF_OK) return st;
+            if ((st = ensure(ctx, ctx->b_pd, pb * C * 3)) != CONVCRF_OK) return st;
+        }
     }
     char* qbase = static_cast<char*>(ctx->b_q.p);
     auto qs = [&](int t) { return reinterpret_cast<float*>(qbase + slice * t); };
@@ -799,7 +815,49 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     st = launch(ctx, kSoftmax, stream, "softmax",
                 [&] { return launch_softmax(unary, qs(0), B, C, H * W, stream); });
     if (st != CONVCRF_OK) return st;
-    if (run && p.features) {
+    float* pf = static_cast<float*>(ctx->pool_f.p);
+    float* pq = static_cast<float*>(ctx->pool_q.p);
+    float* pm = static_cast<float*>(ctx->pool_m.p);
+    if (run && s > 1) {
+        // the pooled message of Sec. 4.2 (as convcrf_meanfield), with every
+        // Q^t kept at full resolution
+        IterArgs a{};
+        a.mu = mu_dev;
+        a.include_center = p.include_center;
+        a.neg_beta = (float)(-kLog2eD / (2.0 * tb * tb));
+        a.center_w = (float)((double)p.w_app + (double)p.w_smooth);
+        fill_taps(p, s, a.taps);
+        const int nchunks = (C + kPmsgClasses - 1) / kPmsgClasses;
+        const size_t lds = pmsg_lds_bytes(k);
+        if (lds > kLdsLimit) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window exceeds LDS");
+        a.C = (C + nchunks - 1) / nchunks;
+        a.planes = C;
+        a.H = Hg;
+        a.W = Wg;
+        a.feat = pf;
+        a.src = pq;
+        a.dst = pm;
+        a.mode = kModeMessage;
+        a.tiles_x = (Wg + kPmsgTW - 1) / kPmsgTW;
+        a.tiles_per_img = a.tiles_x * ((Hg + kPmsgTH - 1) / kPmsgTH);
+        a.ntiles = a.tiles_per_img * B;
+        st = launch(ctx, kPool, stream, "blur_pool",
+                    [&] { return launch_pool(image, pf, B, 3, H, W, s, 0, stream); });
+        if (st != CONVCRF_OK) return st;
+        for (int t = 0; t < iters; ++t) {
+            st = launch(ctx, kPool, stream, "blur_pool",
+                        [&] { return launch_pool(qs(t), pq, B, C, H, W, s, 0, stream); });
+            if (st != CONVCRF_OK) return st;
+            st = launch(ctx, kBlurMsg, stream, "blur_message",
+                        [&] { return launch_pmsg(a, k, nchunks, lds, stream); });
+            if (st != CONVCRF_OK) return st;
+            st = launch(ctx, kBlurUpd, stream, "blur_update", [&] {
+                return launch_blur_update(pm, unary, mu_dev, qs(t + 1), nullptr, B, C, H, W, s,
+                                          stream);
+            });
+            if (st != CONVCRF_OK) return st;
+        }
+    } else if (run && p.features) {
         FeatArgs f = feat_args(p, unary, image, mu_dev, B, C, H, W);
         for (int t = 0; t < iters; ++t) {
             f.src = qs(t);
@@ -837,12 +895,12 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
 
     // reverse rounds
     BwdArgs ba{};
-    ba.feat = image;
+    ba.feat = s > 1 ? pf : image;
     ba.C = C;
-    ba.H = H;
-    ba.W = W;
-    ba.tiles_x = (W + tw - 1) / tw;
-    ba.tiles_per_img = ba.tiles_x * ((H + th - 1) / th);
+    ba.H = Hg;
+    ba.W = Wg;
+    ba.tiles_x = (Wg + tw - 1) / tw;
+    ba.tiles_per_img = ba.tiles_x * ((Hg + th - 1) / th);
     ba.ntiles = ntiles;
     ba.include_center = p.include_center;
     ba.dma = dma;
@@ -850,8 +908,8 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     ba.w_app = p.w_app;
     ba.w_smooth = p.w_smooth;
     for (int n = 0; n <= kMaxN; ++n) {
-        ba.a_log2[n] = (float)(-(double)n * kLog2eD / (2.0 * ta * ta));
-        ba.smooth[n] = (float)std::exp(-(double)n / (2.0 * tg * tg));
+        ba.a_log2[n] = (float)(-s2 * n * kLog2eD / (2.0 * ta * ta));
+        ba.smooth[n] = (float)std::exp(-s2 * n / (2.0 * tg * tg));
     }
     ba.dm = static_cast<const float*>(ctx->b_dm.p);
     ba.kpart = static_cast<float*>(ctx->b_kpart.p);
@@ -863,9 +921,14 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         ba.inv_gamma2 = (float)(1.0 / (tg * tg));
     }
     float* dp = grad_compat ? static_cast<float*>(ctx->b_dp.p) : nullptr;
-    ba.dp = dp;
     ba.gpart = grad_compat ? static_cast<float*>(ctx->b_gpart.p) : nullptr;
     float* dm = static_cast<float*>(ctx->b_dm.p);
+    // blur: the pooled dL/dM, -dL/dZ and dL/dQ
+    const size_t pn = (size_t)B * C * Hg * Wg;
+    float* pdm = static_cast<float*>(ctx->b_pd.p);
+    float* pdp = pdm ? pdm + pn : nullptr;
+    float* pdq = pdm ? pdm + 2 * pn : nullptr;
+    ba.dp = s > 1 ? (grad_compat ? pdp : nullptr) : dp;
     const float* dq = grad_q;
     for (int t = iters - 1; t >= 0; --t) {
         const int acc = t != iters - 1;
@@ -874,13 +937,43 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
                                     (long long)H * W, acc, stream);
         });
         if (st != CONVCRF_OK) return st;
-        ba.q = qs(t);
-        ba.dq_out = reinterpret_cast<float*>(static_cast<char*>(ctx->b_dq.p) + slice * (t & 1));
+        float* dq_next = reinterpret_cast<float*>(static_cast<char*>(ctx->b_dq.p) + slice * (t & 1));
         ba.accumulate = acc;
-        st = launch(ctx, kBwdMsg, stream, "bwd_message",
-                    [&] { return launch_bwd_message(ba, k, stream); });
-        if (st != CONVCRF_OK) return st;
-        dq = ba.dq_out;
+        if (s == 1) {
+            ba.q = qs(t);
+            ba.dq_out = dq_next;
+            st = launch(ctx, kBwdMsg, stream, "bwd_message",
+                        [&] { return launch_bwd_message(ba, k, stream); });
+            if (st != CONVCRF_OK) return st;
+        } else {
+            // M = upsample(pooled message of avgpool(Q^t)): the transpose of
+            // the upsampling (for dL/dM and, for dL/dmu, -dL/dZ), the pooled
+            // adjoint message, the transpose of the pooling
+            st = launch(ctx, kBwdPoint, stream, "bwd_point", [&] {
+                return launch_upsample_t(dm, pdm, B, C, Hg, Wg, s, stream);
+            });
+            if (st != CONVCRF_OK) return st;
+            if (grad_compat) {
+                st = launch(ctx, kBwdPoint, stream, "bwd_point", [&] {
+                    return launch_upsample_t(dp, pdp, B, C, Hg, Wg, s, stream);
+                });
+                if (st != CONVCRF_OK) return st;
+            }
+            st = launch(ctx, kPool, stream, "blur_pool",
+                        [&] { return launch_pool(qs(t), pq, B, C, H, W, s, 0, stream); });
+            if (st != CONVCRF_OK) return st;
+            ba.q = pq;
+            ba.dm = pdm;
+            ba.dq_out = pdq;
+            st = launch(ctx, kBwdMsg, stream, "bwd_message",
+                        [&] { return launch_bwd_message(ba, k, stream); });
+            if (st != CONVCRF_OK) return st;
+            st = launch(ctx, kBwdPoint, stream, "bwd_point", [&] {
+                return launch_pool_t(pdq, dq_next, B, C, Hg, Wg, s, stream);
+            });
+            if (st != CONVCRF_OK) return st;
+        }
+        dq = dq_next;
     }
     if (p.features && grad_features && !run) {
         // T = 0: Q = softmax(U) does not depend on the features

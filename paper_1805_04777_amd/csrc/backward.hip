@@ -410,6 +410,58 @@ __global__ __launch_bounds__(256) void bwd_point_kernel(
     }
 }
 
+// ------------------------------------------------------- blur transposes
+// Weight of pooled cell `cell` in the bilinear sample of output o, as the
+// forward upsampling takes it: source coordinate (o + 0.5) / s - 0.5,
+// clamped below at 0; cells i0 and i1 (clamped at n - 1) with 1 - f and f.
+__device__ __forceinline__ float up_weight(int o, int cell, int s, int n) {
+    float u = ((float)o + 0.5f) / (float)s - 0.5f;
+    u = fmaxf(u, 0.f);
+    int a = (int)u;
+    if (a > n - 1) a = n - 1;
+    const int i1 = a < n - 1 ? a + 1 : n - 1;
+    const float f = u - (float)a;
+    return (cell == a ? 1.f - f : 0.f) + (cell == i1 ? f : 0.f);
+}
+
+// One thread per pooled cell and plane; the full-resolution pixels that can
+// sample cell (Y, X) lie in rows [s (Y - 1), s (Y + 2)) and the same columns.
+__global__ __launch_bounds__(256) void upsample_t_kernel(const float* __restrict__ in,
+                                                         float* __restrict__ out, int Hp,
+                                                         int Wp, int s, long long ncell) {
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= ncell) return;
+    const int X = (int)(i % Wp);
+    const long long r = i / Wp;
+    const int Y = (int)(r % Hp);
+    const long long plane = r / Hp;
+    const int H = Hp * s, W = Wp * s;
+    const float* src = in + plane * H * W;
+    const int ylo = s * Y - s > 0 ? s * Y - s : 0, yhi = s * Y + 2 * s < H ? s * Y + 2 * s : H;
+    const int xlo = s * X - s > 0 ? s * X - s : 0, xhi = s * X + 2 * s < W ? s * X + 2 * s : W;
+    float acc = 0.f;
+    for (int y = ylo; y < yhi; ++y) {
+        const float wy = up_weight(y, Y, s, Hp);
+        float row = 0.f;
+        for (int x = xlo; x < xhi; ++x) row = fmaf(up_weight(x, X, s, Wp), src[(long long)y * W + x], row);
+        acc = fmaf(wy, row, acc);
+    }
+    out[i] = acc;
+}
+
+__global__ __launch_bounds__(256) void pool_t_kernel(const float* __restrict__ in,
+                                                     float* __restrict__ out, int Hp, int Wp,
+                                                     int s, float inv, long long npix) {
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= npix) return;
+    const int W = Wp * s, H = Hp * s;
+    const int x = (int)(i % W);
+    const long long r = i / W;
+    const int y = (int)(r % H);
+    const long long plane = r / H;
+    out[i] = in[(plane * Hp + y / s) * Wp + x / s] * inv;
+}
+
 // ---------------------------------------------------------------- reduce
 struct ReduceArgs {
     const float* gpart;
@@ -484,6 +536,28 @@ hipError_t launch_bwd_point(const float* q, const float* dq, const float* mu, fl
     else
         hipLaunchKernelGGL((bwd_point_kernel<kMaxC>), dim3((unsigned)blocks), dim3(256), 0,
                            stream, q, dq, mu, du, dm, dp, C, HW, npix, accumulate);
+    return hipGetLastError();
+}
+
+hipError_t launch_upsample_t(const float* in, float* out, int B, int C, int Hp, int Wp, int s,
+                             hipStream_t stream) {
+    const long long n = (long long)B * C * Hp * Wp;
+    if (n == 0) return hipSuccess;
+    const long long blocks = (n + 255) / 256;
+    if (blocks > 0x7fffffffLL || s < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(upsample_t_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, in, out,
+                       Hp, Wp, s, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_pool_t(const float* in, float* out, int B, int C, int Hp, int Wp, int s,
+                         hipStream_t stream) {
+    const long long n = (long long)B * C * Hp * Wp * s * s;
+    if (n == 0) return hipSuccess;
+    const long long blocks = (n + 255) / 256;
+    if (blocks > 0x7fffffffLL || s < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(pool_t_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, in, out, Hp,
+                       Wp, s, 1.f / (float)(s * s), n);
     return hipGetLastError();
 }
 

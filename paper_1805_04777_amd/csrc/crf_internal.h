@@ -308,6 +308,17 @@ hipError_t launch_bwd_point(const float* q, const float* dq, const float* mu, fl
                             float* dm, float* dp, int B, int C, long long HW,
                             int accumulate, hipStream_t stream);
 
+// Blur transposes (the pooled message of Sec. 4.2), [B][C] planes:
+// out [Hp][Wp] = the transpose of the bilinear x s upsampling (half-pixel
+// centres, edge clamp) of in [Hp s][Wp s]: each cell gathers the values
+// interpolated from it, with the same weights;
+hipError_t launch_upsample_t(const float* in, float* out, int B, int C, int Hp, int Wp, int s,
+                             hipStream_t stream);
+// out [Hp s][Wp s] = the transpose of the s x s average pooling of in
+// [Hp][Wp]: each pixel receives its cell's value / s^2.
+hipError_t launch_pool_t(const float* in, float* out, int B, int C, int Hp, int Wp, int s,
+                         hipStream_t stream);
+
 // out_compat[e] = sum_g gpart[g][e] over `groups` rows (C*C entries, when
 // out_compat is set);
 // out_kernel[j] = scale[j] * sum_t kpart[t][j] (5 entries, when set).

@@ -166,6 +166,50 @@ def test_large_window_adds_no_error_beyond_the_forward(torch_cuda, crf, oracle_m
         assert e <= min(1e-3, max(TOL_REL, 2.0 * fwd))
 
 
+BLUR_CASES = [
+    # (seed, B, C, H, W, k, T, s, general compat)
+    (31, 1, 3, 16, 24, 3, 2, 2, True),
+    (32, 2, 21, 32, 48, 5, 2, 4, False),
+    (33, 1, 19, 40, 64, 7, 3, 8, True),
+    (34, 1, 5, 24, 36, 11, 1, 4, False),
+]
+
+
+@pytest.mark.parametrize("seed,B,C,H,W,k,T,s,gen_mu", BLUR_CASES)
+def test_blur_backward_matches_oracle(torch_cuda, crf, oracle_mod, seed, B, C, H, W, k, T, s,
+                                      gen_mu):
+    """The pooled message (Sec. 4.2 blur): the transposes of the upsampling
+    and the pooling around the pooled adjoint message."""
+    U, I, G = make_case(seed, B, C, H, W)
+    mu = None
+    if gen_mu:
+        mu = np.random.default_rng(seed + 100).normal(0.3, 0.5, (C, C)).astype(np.float32)
+    p = params(k, False, mu, blur=s)
+    print(f"case blur seed={seed} B={B} C={C} {H}x{W} k={k} T={T} s={s}", flush=True)
+    got = run_gpu(torch_cuda, crf, U, I, G, p, T)
+    op = OracleParams(filter_size=k, blur=s, w_app=p.w_app, theta_alpha=p.theta_alpha,
+                      theta_beta=p.theta_beta, w_smooth=p.w_smooth, theta_gamma=p.theta_gamma)
+    ref = oracle_mod.meanfield_backward(U, I, op, T, G, compat=mu)
+    check(got, ref, f"blur seed {seed}", T)
+
+
+def test_blur_workload_backward_full(torch_cuda, crf, oracle_mod):
+    """The blur workload, 1 x 21 x 512 x 512, k = 11 on the 4 x 4 pooled
+    grid, T = 5, in full."""
+    wl = synth.WORKLOADS["blur"]
+    U, I, _ = synth.make_inputs(wl)
+    G = np.random.default_rng(78).normal(0.0, 1.0, U.shape).astype(np.float32)
+    p = params(wl.filter_size, blur=wl.blur, w_app=wl.w_app, theta_alpha=wl.theta_alpha,
+               theta_beta=wl.theta_beta, w_smooth=wl.w_smooth, theta_gamma=wl.theta_gamma)
+    print("case blur 1x21x512x512 k=11 s=4 T=5", flush=True)
+    got = run_gpu(torch_cuda, crf, U, I, G, p, wl.iters)
+    op = OracleParams(filter_size=wl.filter_size, blur=wl.blur, w_app=wl.w_app,
+                      theta_alpha=wl.theta_alpha, theta_beta=wl.theta_beta,
+                      w_smooth=wl.w_smooth, theta_gamma=wl.theta_gamma)
+    ref = oracle_mod.meanfield_backward(U, I, op, wl.iters, G)
+    check(got, ref, "blur workload", wl.iters)
+
+
 def test_outputs_are_independent_of_what_is_requested(torch_cuda, crf):
     U, I, G = make_case(21, 1, 21, 48, 64)
     p = params(7)
@@ -194,8 +238,8 @@ def test_backward_errors(torch_cuda, crf):
     U, I, G = make_case(22, 1, 4, 16, 16)
     t = lambda a: torch.from_numpy(a).cuda()
     with pytest.raises(cc.ConvCRFError) as e:
-        crf.meanfield_backward(t(U), t(I), params(5, blur=2), 2, t(G))
-    assert e.value.status == cc.E_UNSUPPORTED
+        crf.meanfield_backward(t(U), t(I), params(5, blur=3), 2, t(G))   # s not 1, 2, 4, 8
+    assert e.value.status == cc.E_INVALID_ARG
     Ut, Gt = t(U), t(G)
     with pytest.raises(cc.ConvCRFError) as e:
         crf.meanfield_backward(Ut, t(I), params(5), 2, Gt, out=Gt)   # overlaps grad_q
