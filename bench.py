@@ -133,6 +133,14 @@ def algorithmic_per_launch(kname: str, wl, D: int = 0):
         return rounds * px / (T + 1), rbytes * px / (T + 1)
     if kname == "bwd_reduce":
         return 0, 0
+    if kname == "bwd_blur_transpose":
+        # per round: the upsampling transposed for dL/dM and -dL/dZ (a
+        # 3s x 3s gather per cell and class, separable: about 12 flop per
+        # pixel and class; full-resolution planes read, pooled written) and
+        # the pooling transposed (pooled read, full-resolution written);
+        # averaged over the three launches
+        s2 = wl.blur * wl.blur
+        return 12 * C * px * 2 / 3 + C * px / 3, (4 * C + 4 * C / s2) * px
     raise KeyError(kname)
 
 

@@ -206,8 +206,9 @@ convcrf_status convcrf_profile_enable(convcrf_ctx *ctx, int enable);
 /* Total elapsed milliseconds and launch count of the kernels named `name`
  * ("fused_iter", "fused_resident", "sync_reset", "softmax", "build_kernel",
  * "materialised_iter", "blur_pool", "blur_message", "blur_update", and for
- * convcrf_meanfield_backward "bwd_point", "bwd_message", "bwd_reduce"
- * besides the forward's) since profiling was enabled.  "fused_resident" is one launch running all
+ * convcrf_meanfield_backward "bwd_point", "bwd_message", "bwd_reduce",
+ * "bwd_blur_transpose" besides the forward's; "feature_iter" with learnable
+ * features) since profiling was enabled.  "fused_resident" is one launch running all
  * iterations of a call (CONVCRF_VARIANT_RESIDENT); "fused_iter" one
  * iteration.
  * Synchronises on the recorded events.  An unknown or unused name gives

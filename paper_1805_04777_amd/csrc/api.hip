@@ -26,10 +26,11 @@ constexpr size_t kLdsLimit = 160 * 1024;  // gfx950 LDS per work-group
 const char* const kKernelNames[] = {"fused_iter",   "softmax",      "build_kernel",
                                     "materialised_iter", "blur_pool", "blur_message",
                                     "blur_update",  "fused_resident", "sync_reset",
-                                    "bwd_point", "bwd_message", "bwd_reduce", "feature_iter"};
+                                    "bwd_point", "bwd_message", "bwd_reduce", "feature_iter",
+                                    "bwd_blur_transpose"};
 enum KernelId {
     kFused = 0, kSoftmax, kBuild, kMatIter, kPool, kBlurMsg, kBlurUpd, kResident, kSyncReset,
-    kBwdPoint, kBwdMsg, kBwdReduce, kFeatIter, kNumKernels
+    kBwdPoint, kBwdMsg, kBwdReduce, kFeatIter, kBwdBlurT, kNumKernels
 };
 
 struct DevBuf {
@@ -949,12 +950,12 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
             // M = upsample(pooled message of avgpool(Q^t)): the transpose of
             // the upsampling (for dL/dM and, for dL/dmu, -dL/dZ), the pooled
             // adjoint message, the transpose of the pooling
-            st = launch(ctx, kBwdPoint, stream, "bwd_point", [&] {
+            st = launch(ctx, kBwdBlurT, stream, "bwd_blur_transpose", [&] {
                 return launch_upsample_t(dm, pdm, B, C, Hg, Wg, s, stream);
             });
             if (st != CONVCRF_OK) return st;
             if (grad_compat) {
-                st = launch(ctx, kBwdPoint, stream, "bwd_point", [&] {
+                st = launch(ctx, kBwdBlurT, stream, "bwd_blur_transpose", [&] {
                     return launch_upsample_t(dp, pdp, B, C, Hg, Wg, s, stream);
                 });
                 if (st != CONVCRF_OK) return st;
@@ -968,7 +969,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
             st = launch(ctx, kBwdMsg, stream, "bwd_message",
                         [&] { return launch_bwd_message(ba, k, stream); });
             if (st != CONVCRF_OK) return st;
-            st = launch(ctx, kBwdPoint, stream, "bwd_point", [&] {
+            st = launch(ctx, kBwdBlurT, stream, "bwd_blur_transpose", [&] {
                 return launch_pool_t(pdq, dq_next, B, C, Hg, Wg, s, stream);
             });
             if (st != CONVCRF_OK) return st;

@@ -414,8 +414,9 @@ __global__ __launch_bounds__(256) void bwd_point_kernel(
 // Weight of pooled cell `cell` in the bilinear sample of output o, as the
 // forward upsampling takes it: source coordinate (o + 0.5) / s - 0.5,
 // clamped below at 0; cells i0 and i1 (clamped at n - 1) with 1 - f and f.
-__device__ __forceinline__ float up_weight(int o, int cell, int s, int n) {
-    float u = ((float)o + 0.5f) / (float)s - 0.5f;
+// s is 2, 4 or 8, so the product with 1 / s is the exact quotient.
+__device__ __forceinline__ float up_weight(int o, int cell, float inv_s, int n) {
+    float u = ((float)o + 0.5f) * inv_s - 0.5f;
     u = fmaxf(u, 0.f);
     int a = (int)u;
     if (a > n - 1) a = n - 1;
@@ -424,8 +425,11 @@ __device__ __forceinline__ float up_weight(int o, int cell, int s, int n) {
     return (cell == a ? 1.f - f : 0.f) + (cell == i1 ? f : 0.f);
 }
 
-// One thread per pooled cell and plane; the full-resolution pixels that can
-// sample cell (Y, X) lie in rows [s (Y - 1), s (Y + 2)) and the same columns.
+// One thread per pooled cell and plane.  Output o samples cell i0 =
+// floor((o + 0.5) / s - 0.5) and i0 + 1, so the full-resolution pixels that
+// sample cell (Y, X) lie in rows [s Y - s/2, s Y + 3s/2) and the same
+// columns (the clamps at the edges only move pixels inside that range onto
+// the edge cells).
 __global__ __launch_bounds__(256) void upsample_t_kernel(const float* __restrict__ in,
                                                          float* __restrict__ out, int Hp,
                                                          int Wp, int s, long long ncell) {
@@ -435,15 +439,17 @@ __global__ __launch_bounds__(256) void upsample_t_kernel(const float* __restrict
     const long long r = i / Wp;
     const int Y = (int)(r % Hp);
     const long long plane = r / Hp;
-    const int H = Hp * s, W = Wp * s;
+    const int H = Hp * s, W = Wp * s, h = s / 2;
+    const float inv_s = 1.f / (float)s;
     const float* src = in + plane * H * W;
-    const int ylo = s * Y - s > 0 ? s * Y - s : 0, yhi = s * Y + 2 * s < H ? s * Y + 2 * s : H;
-    const int xlo = s * X - s > 0 ? s * X - s : 0, xhi = s * X + 2 * s < W ? s * X + 2 * s : W;
+    const int ylo = s * Y - h > 0 ? s * Y - h : 0, yhi = s * Y + s + h < H ? s * Y + s + h : H;
+    const int xlo = s * X - h > 0 ? s * X - h : 0, xhi = s * X + s + h < W ? s * X + s + h : W;
     float acc = 0.f;
     for (int y = ylo; y < yhi; ++y) {
-        const float wy = up_weight(y, Y, s, Hp);
+        const float wy = up_weight(y, Y, inv_s, Hp);
         float row = 0.f;
-        for (int x = xlo; x < xhi; ++x) row = fmaf(up_weight(x, X, s, Wp), src[(long long)y * W + x], row);
+        for (int x = xlo; x < xhi; ++x)
+            row = fmaf(up_weight(x, X, inv_s, Wp), src[(long long)y * W + x], row);
         acc = fmaf(wy, row, acc);
     }
     out[i] = acc;
@@ -544,7 +550,7 @@ hipError_t launch_upsample_t(const float* in, float* out, int B, int C, int Hp, 
     const long long n = (long long)B * C * Hp * Wp;
     if (n == 0) return hipSuccess;
     const long long blocks = (n + 255) / 256;
-    if (blocks > 0x7fffffffLL || s < 1) return hipErrorInvalidValue;
+    if (blocks > 0x7fffffffLL || (s != 2 && s != 4 && s != 8)) return hipErrorInvalidValue;
     hipLaunchKernelGGL(upsample_t_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, in, out,
                        Hp, Wp, s, n);
     return hipGetLastError();
