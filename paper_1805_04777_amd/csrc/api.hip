@@ -22,6 +22,9 @@ namespace {
 
 constexpr double kLog2eD = 1.4426950408889634073599;
 constexpr size_t kLdsLimit = 160 * 1024;  // gfx950 LDS per work-group
+// Most class groups the adjoint message splits its classes into (at least 4
+// classes per group).
+constexpr int kBwdClassGroups = 3;
 
 const char* const kKernelNames[] = {"fused_iter",   "softmax",      "build_kernel",
                                     "materialised_iter", "blur_pool", "blur_message",
@@ -734,10 +737,17 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     // it pads every plane to whole 64-float rows, and is used only where that
     // keeps the tile height (measured: 8-row tiles cost more than the
     // scalar staging saves)
+    // class groups of the adjoint message (grid dim y): every work-group
+    // stages and sums its group's classes only, which leaves room for more
+    // work-groups per CU and, on small grids, more work-groups; learnable
+    // features keep one group (dL/dF sums over all classes in one place)
+    int groups = D > 0 ? 1 : std::max(1, std::min(kBwdClassGroups, C / 4));
+    const int cgsize = (C + groups - 1) / groups;
+    groups = (C + cgsize - 1) / cgsize;
     const long long hw_ll = (long long)Hg * Wg;
     const bool dma = (long long)std::max(std::max(3, C), D) * hw_ll * 4 < (1LL << 31) &&
-                     bwd_tile_h(k, C, D, true) == bwd_tile_h(k, C, D, false);
-    if (bwd_lds_need(k, C, D, dma) > kBwdLdsLimit)
+                     bwd_tile_h(k, C, D, true, cgsize) == bwd_tile_h(k, C, D, false, cgsize);
+    if (bwd_lds_need(k, C, D, dma, cgsize) > kBwdLdsLimit)
         return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
     const long long npix = (long long)B * H * W;
     const size_t qbytes = sizeof(float) * (size_t)npix * C;
@@ -759,7 +769,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     const float scale[5] = {1.f, (float)(s2 * p.w_app / (ta * ta * ta)),
                             (float)(p.w_app / (tb * tb * tb)), 1.f,
                             (float)(s2 * p.w_smooth / (tg * tg * tg))};
-    const int tw = bwd_tile_w(k), th = bwd_tile_h(k, C, D, dma);
+    const int tw = bwd_tile_w(k), th = bwd_tile_h(k, C, D, dma, cgsize);
     const long long ntiles_ll = (long long)((Wg + tw - 1) / tw) * ((Hg + th - 1) / th) * B;
     if (ntiles_ll > 0x7fffffffLL) return fail(ctx, CONVCRF_E_UNSUPPORTED, "too many tiles");
     const int ntiles = (int)ntiles_ll;
@@ -794,7 +804,8 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
                 CONVCRF_OK)
                 return st;
         }
-        if ((st = ensure(ctx, ctx->b_kpart, sizeof(float) * (size_t)ntiles * 5)) != CONVCRF_OK)
+        if ((st = ensure(ctx, ctx->b_kpart, sizeof(float) * (size_t)ntiles * groups * 5)) !=
+            CONVCRF_OK)
             return st;
         if (p.features && !grad_features &&
             (st = ensure(ctx, ctx->b_df, sizeof(float) * (size_t)npix * D)) != CONVCRF_OK)
@@ -904,6 +915,8 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     ba.tiles_per_img = ba.tiles_x * ((Hg + th - 1) / th);
     ba.ntiles = ntiles;
     ba.include_center = p.include_center;
+    ba.cgroups = groups;
+    ba.cgsize = cgsize;
     ba.dma = dma;
     ba.neg_beta = (float)(-kLog2eD / (2.0 * tb * tb));
     ba.w_app = p.w_app;
@@ -997,7 +1010,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         return launch(ctx, kBwdReduce, stream, "bwd_reduce", [&] {
             return launch_bwd_reduce(static_cast<const float*>(ctx->b_gpart.p), run ? ntiles : 0,
                                      C, grad_compat, static_cast<const float*>(ctx->b_kpart.p),
-                                     run ? ntiles : 0, scale, grad_kernel, stream);
+                                     run ? ntiles * groups : 0, scale, grad_kernel, stream);
         });
     return CONVCRF_OK;
 }

@@ -40,7 +40,7 @@ namespace {
 // the value dropped outside) so that many are in flight per thread.
 template <int NT, int LW, int PL, int PS, bool DMA>
 __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b, int y0,
-                                             int x0) {
+                                             int x0, int c0, int CN) {
     const int C = a.C;
     const long long hw = (long long)a.H * a.W;
     const float* fb = a.feat + (long long)b * 3 * hw;
@@ -77,21 +77,22 @@ __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b
         const rsrc_t rm = buffer_rsrc(mb, (unsigned)(C * hw * 4));
         for (int ch = 0; ch < 3; ++ch) issue(rf, ch, ch);
         for (int c = 0; c < D; ++c) issue(rs, c, 3 + c);
-        for (int c = 0; c < C; ++c) issue(rq, c, 3 + D + c);
-        for (int c = 0; c < C; ++c) issue(rm, c, 3 + D + C + c);
+        for (int c = 0; c < CN; ++c) issue(rq, c0 + c, 3 + D + c);
+        for (int c = 0; c < CN; ++c) issue(rm, c0 + c, 3 + D + CN + c);
         __builtin_amdgcn_s_waitcnt(vm_wait(0));
         return;
     }
-    const int nplanes = 2 * C + 3 + D;
+    const int nplanes = 2 * CN + 3 + D;
 #pragma unroll 16
     for (int e = threadIdx.x; e < nplanes * PL; e += NT) {
         const int pl = e / PL, o = e - pl * PL;
         const int ly = o / LW, lx = o - ly * LW;
         const int gy = y0 + ly, gx = x0 + lx;
-        const int pq = pl - 3 - D;   // index among the Q and dL/dM planes
+        const int pq = pl - 3 - D;   // index among the group's Q and dL/dM planes
         const float* src = pl < 3 ? fb + pl * hw
                                   : (pq < 0 ? sb + (pl - 3) * hw
-                                            : (pq < C ? qb + pq * hw : mb + (pq - C) * hw));
+                                            : (pq < CN ? qb + (c0 + pq) * hw
+                                                       : mb + (c0 + pq - CN) * hw));
         const bool ok = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
         const float v = src[ok ? (long long)gy * a.W + gx : 0];
         lds[pl * PS + o] = ok ? v : 0.f;
@@ -101,7 +102,7 @@ __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b
 // The tile's sums of the five parameter terms over its threads, in a fixed
 // order, added into kpart[tile] (or written).
 template <int NT>
-__device__ __forceinline__ void tile_param_sums(float (&g)[5], const BwdArgs& a, int tile) {
+__device__ __forceinline__ void tile_param_sums(float (&g)[5], const BwdArgs& a, int row) {
     __shared__ float red[5][NT / 64];
 #pragma unroll
     for (int j = 0; j < 5; ++j)
@@ -115,7 +116,7 @@ __device__ __forceinline__ void tile_param_sums(float (&g)[5], const BwdArgs& a,
         const int j = threadIdx.x;
         float s = 0.f;
         for (int w = 0; w < NT / 64; ++w) s += red[j][w];
-        float* o = a.kpart + (long long)tile * 5 + j;
+        float* o = a.kpart + (long long)row * 5 + j;
         *o = a.accumulate ? *o + s : s;
     }
 }
@@ -126,34 +127,31 @@ __device__ __forceinline__ void tile_param_sums(float (&g)[5], const BwdArgs& a,
 // [B][C][H][W] planes.  dp and M go to LDS (zero for pixels outside the
 // image and rows past C), then each thread sums one 3 x 3 block of (l, l')
 // over one group of pixels, and the groups are added in order.
+// dp of all C classes (rows) against the M of the group's CN classes
+// c0 .. c0 + CN - 1 (columns); pix[i] is the offset of the pixel in plane 0.
 template <int NT, int PX, int CM>
-__device__ __forceinline__ void tile_gram(float* lds, const BwdArgs& a, int tile,
-                                          const float (&mv)[PX][CM], const bool (&in)[PX],
-                                          const long long (&pix)[PX]) {
+__device__ __forceinline__ void tile_gram(float* lds, const BwdArgs& a, int tile, int c0,
+                                          int CN, const float (&mv)[PX][CM],
+                                          const bool (&in)[PX], const long long (&pix)[PX]) {
     constexpr int NPIX = NT * PX, SP = NPIX + 1;
     const int C = a.C;
     const long long hw = (long long)a.H * a.W;
-    const int CP = bwd_gram_rows(C);
+    const int CP = bwd_gram_rows(C), CQ = bwd_gram_rows(CN);
     float* gp = lds;
     float* gm = lds + CP * SP;
     __syncthreads();  // the staged planes have been read
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
         const int col = PX * threadIdx.x + i;
+        for (int c = 0; c < CP; ++c)
+            gp[c * SP + col] = in[i] && c < C ? a.dp[pix[i] + c * hw] : 0.f;
 #pragma unroll
-        for (int c = 0; c < CM; ++c) {
-            if (c < CP) {
-                gp[c * SP + col] = in[i] && c < C ? a.dp[pix[i] + c * hw] : 0.f;
-                gm[c * SP + col] = in[i] && c < C ? mv[i][c] : 0.f;
-            }
-        }
-        for (int c = CM; c < CP; ++c) {   // rows past the held classes
-            gp[c * SP + col] = 0.f;
-            gm[c * SP + col] = 0.f;
-        }
+        for (int c = 0; c < CM; ++c)
+            if (c < CQ) gm[c * SP + col] = in[i] && c < CN ? mv[i][c] : 0.f;
+        for (int c = CM; c < CQ; ++c) gm[c * SP + col] = 0.f;   // past the held classes
     }
     __syncthreads();
-    const int nbc = CP / 3, nb = nbc * nbc;
+    const int nbr = CP / 3, nbc = CQ / 3, nb = nbr * nbc;
     const int ng = NT / nb;
     const int bi = threadIdx.x % nb, pg = threadIdx.x / nb;
     const int l0 = 3 * (bi / nbc), m0 = 3 * (bi % nbc);
@@ -182,8 +180,8 @@ __device__ __forceinline__ void tile_gram(float* lds, const BwdArgs& a, int tile
         for (int g = 0; g < ng; ++g) sum += gr[g * nb * 9 + idx];
         const int blk = idx / 9, e = idx - blk * 9;
         const int l = 3 * (blk / nbc) + e / 3, lp = 3 * (blk % nbc) + e % 3;
-        if (l < C && lp < C) {
-            float* o = a.gpart + (long long)tile * C * C + l * C + lp;
+        if (l < C && lp < CN) {
+            float* o = a.gpart + (long long)tile * C * C + l * C + c0 + lp;
             *o = a.accumulate ? *o + sum : sum;
         }
     }
@@ -203,14 +201,17 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
     const int D = FT ? a.D : 0;
     const float* sc = lds;               // 3 colour planes
     const float* sf = lds + 3 * PS;      // D feature planes (FT)
-    const float* sq = sf + D * PS;       // C planes of Q^t
-    const float* sm = sq + C * PS;       // C planes of dL/dM^t
     const int tile = blockIdx.x;
     const int b = tile / a.tiles_per_img;
     const int tr = tile - b * a.tiles_per_img;
     const int ty = tr / a.tiles_x, tx = tr - ty * a.tiles_x;
     const long long hw = (long long)a.H * a.W;
-    stage_planes<NT, LW, PL, PS, DMA>(lds, a, b, ty * TH - R, tx * TW - XO);
+    // this work-group's class group: classes c0 .. c0 + CN - 1
+    const int c0 = blockIdx.y * a.cgsize;
+    const int CN = C - c0 < a.cgsize ? C - c0 : a.cgsize;
+    stage_planes<NT, LW, PL, PS, DMA>(lds, a, b, ty * TH - R, tx * TW - XO, c0, CN);
+    const float* sq = sf + D * PS;       // the group's CN planes of Q^t
+    const float* sm = sq + CN * PS;      // the group's CN planes of dL/dM^t
     __syncthreads();
 
     const int lx = threadIdx.x % TW, ly = threadIdx.x / TW;
@@ -228,8 +229,8 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
         int poff[CM];
 #pragma unroll
         for (int c = 0; c < CM; ++c) {
-            poff[c] = (c < C ? c : C - 1) * PS;
-            dmq[c] = c < C ? sm[poff[c] + oc] : 0.f;
+            poff[c] = (c < CN ? c : CN - 1) * PS;
+            dmq[c] = c < CN ? sm[poff[c] + oc] : 0.f;
             dqa[c] = 0.f;
         }
         // FT: own features and Q, and the feature derivative of the pixel
@@ -241,7 +242,7 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
         }
         if constexpr (FT) {
 #pragma unroll
-            for (int c = 0; c < CM; ++c) qo[c] = c < C ? sq[poff[c] + oc] : 0.f;
+            for (int c = 0; c < CM; ++c) qo[c] = c < CN ? sq[poff[c] + oc] : 0.f;
         }
         constexpr int kRowUnroll = K <= 7 ? K : 1;   // a window row at once
 #pragma unroll 1
@@ -293,7 +294,7 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
         }
 #pragma unroll
         for (int c = 0; c < CM; ++c)
-            if (c < C) a.dq_out[pix + c * hw] = dqa[c];
+            if (c < CN) a.dq_out[pix + (c0 + c) * hw] = dqa[c];
         if constexpr (FT) {
             float* df = a.dfeat + (long long)b * D * hw + (long long)py * a.W + px;
 #pragma unroll
@@ -304,21 +305,21 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
     if constexpr (WM) {
         const bool ins[1] = {in};
         const long long pixs[1] = {pix};
-        tile_gram<NT, 1, CM>(lds, a, tile, ma, ins, pixs);
+        tile_gram<NT, 1, CM>(lds, a, tile, c0, CN, ma, ins, pixs);
     }
-    tile_param_sums<NT>(g, a, tile);
+    tile_param_sums<NT>(g, a, tile * a.cgroups + blockIdx.y);
 }
 
 template <int K, int TH, int CM, bool DMA, bool FT>
 hipError_t launch_msg_ktc(const BwdArgs& a, hipStream_t stream) {
-    const size_t lds = bwd_lds_bytes(K, a.C, TH, DMA, FT ? a.D : 0);
-    const dim3 block(bwd_tile_w(K) * TH);
+    const size_t lds = bwd_lds_bytes(K, a.C, TH, DMA, FT ? a.D : 0, a.cgsize);
+    const dim3 block(bwd_tile_w(K) * TH), grid(a.ntiles, a.cgroups);
     if (a.gpart)
-        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, true, DMA, FT>), dim3(a.ntiles), block,
-                           lds, stream, a);
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, true, DMA, FT>), grid, block, lds, stream,
+                           a);
     else
-        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, false, DMA, FT>), dim3(a.ntiles), block,
-                           lds, stream, a);
+        hipLaunchKernelGGL((bwd_msg_kernel<K, TH, CM, false, DMA, FT>), grid, block, lds,
+                           stream, a);
     return hipGetLastError();
 }
 
@@ -334,8 +335,8 @@ hipError_t launch_msg_ktv(const BwdArgs& a, hipStream_t stream) {
 
 template <int K, int TH>
 hipError_t launch_msg_kt(const BwdArgs& a, hipStream_t stream) {
-    if (a.C <= 8) return launch_msg_ktv<K, TH, 8>(a, stream);
-    if (a.C <= 21) return launch_msg_ktv<K, TH, 21>(a, stream);
+    if (a.cgsize <= 8) return launch_msg_ktv<K, TH, 8>(a, stream);
+    if (a.cgsize <= 21) return launch_msg_ktv<K, TH, 21>(a, stream);
     return launch_msg_ktv<K, TH, kMaxC>(a, stream);
 }
 
@@ -344,7 +345,7 @@ hipError_t launch_msg_kt(const BwdArgs& a, hipStream_t stream) {
 template <int K>
 hipError_t launch_msg_k(const BwdArgs& a, hipStream_t stream) {
     if constexpr (K <= 7) {
-        if (bwd_tile_h(K, a.C, a.sfeat ? a.D : 0, a.dma != 0) == 16)
+        if (bwd_tile_h(K, a.C, a.sfeat ? a.D : 0, a.dma != 0, a.cgsize) == 16)
             return launch_msg_kt<K, 16>(a, stream);
     }
     return launch_msg_kt<K, 8>(a, stream);
@@ -510,7 +511,10 @@ hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream) {
     if (a.C < 1 || a.C > kMaxC || a.ntiles <= 0) return hipErrorInvalidValue;
     const int D = a.sfeat ? a.D : 0;
     if (a.sfeat && (a.D < 1 || a.D > kMaxFeat || !a.dfeat)) return hipErrorInvalidValue;
-    if (bwd_lds_need(k, a.C, D, a.dma != 0) > kBwdLdsLimit) return hipErrorInvalidValue;
+    if (a.cgsize < 1 || a.cgroups < 1 || (long long)a.cgroups * a.cgsize < a.C ||
+        (a.cgroups - 1) * a.cgsize >= a.C || (a.sfeat && a.cgroups != 1) || a.cgroups > 65535)
+        return hipErrorInvalidValue;
+    if (bwd_lds_need(k, a.C, D, a.dma != 0, a.cgsize) > kBwdLdsLimit) return hipErrorInvalidValue;
     // buffer offsets of the DMA staging stay under 2 GB
     const long long hw = (long long)a.H * a.W;
     const int mp = a.C > 3 ? (a.C > D ? a.C : D) : (3 > D ? 3 : D);

@@ -220,7 +220,9 @@ hipError_t launch_feat_update(const FeatArgs& a, int k, hipStream_t stream);
 //                 message, using K(p,q) = K(q,p) and the symmetric window)
 // and the tile's sums over its pixels and taps of dk = sum_l dm_x(l) q_{x+d}(l)
 // times A, A |d|^2, A |I_x - I_{x+d}|^2, S, S |d|^2, where A and S are the
-// two Eq. 4 Gaussians without their weights, added into kpart[tile][5];
+// two Eq. 4 Gaussians without their weights, added into kpart[tile][group][5]
+// (each class group sums its own classes' part of dk: the five sums are
+// linear in it);
 // with learnable smoothness features the smoothness Gaussian S is taken on
 // |F_x - F_{x+d}|^2, the theta_gamma term on that distance, and
 //   dfeat_x += sum_d (dk(x, x+d) + dk(x+d, x)) (-w_smooth S / theta_gamma^2)
@@ -228,8 +230,9 @@ hipError_t launch_feat_update(const FeatArgs& a, int k, hipStream_t stream);
 // (the pair (x, x+d) seen from both ends; K is symmetric);
 // when gpart is set, also the forward message M_x(l) = sum_d K(x, x+d)
 // q_{x+d}(l) and the tile's sum over its pixels of dp_x(l) M_x(l') (the
-// compatibility derivative), added into gpart[tile][l * C + l'].  Partial
-// sums are written instead of added when `accumulate` is 0.
+// compatibility derivative) for every l and the group's l', added into
+// gpart[tile][l * C + l'].  Partial sums are written instead of added when
+// `accumulate` is 0.
 struct BwdArgs {
     const float* q;      // Q^t [B][C][H][W]
     const float* dm;     // dL/dM^t [B][C][H][W]
@@ -247,6 +250,9 @@ struct BwdArgs {
     int tiles_x, tiles_per_img, ntiles;
     int include_center;
     int accumulate;
+    int cgroups;         // class groups: grid dim y; group g takes classes
+    int cgsize;          // [g cgsize, min((g + 1) cgsize, C)) (1 group with
+                         // learnable features)
     int dma;             // stage with buffer loads into LDS (each image's
                          // planes under 2 GB; see bwd_plane)
     float neg_beta;      // -log2(e) / (2 theta_beta^2)
@@ -271,21 +277,22 @@ constexpr int bwd_plane(int k, int rows, bool dma) {
     return dma ? ((bwd_tile_w(k) + k - 1) * (rows + k - 1) + 63) / 64 * 64
                : (bwd_tile_w(k) + k - 1) * (rows + k - 1);
 }
-constexpr size_t bwd_lds_bytes(int k, int C, int rows, bool dma, int D) {
-    const size_t stage = (size_t)(2 * C + 3 + D) * bwd_plane(k, rows, dma);
+// cn: classes of one group (C with one group).
+constexpr size_t bwd_lds_bytes(int k, int C, int rows, bool dma, int D, int cn) {
+    const size_t stage = (size_t)(2 * cn + 3 + D) * bwd_plane(k, rows, dma);
     const size_t nt = (size_t)bwd_tile_w(k) * rows;
-    const size_t gram = 2 * (size_t)bwd_gram_rows(C) * (nt + 1);
+    const size_t gram = (size_t)(bwd_gram_rows(C) + bwd_gram_rows(cn)) * (nt + 1);
     const size_t red = 9 * nt;
     const size_t g = gram > red ? gram : red;
     return sizeof(float) * (stage > g ? stage : g);
 }
 constexpr size_t kBwdLdsLimit = 160 * 1024 - 256;
 // D: learnable smoothness feature planes staged besides (0 without).
-constexpr int bwd_tile_h(int k, int C, int D, bool dma) {
-    return k <= 7 && bwd_lds_bytes(k, C, 16, dma, D) <= kBwdLdsLimit ? 16 : 8;
+constexpr int bwd_tile_h(int k, int C, int D, bool dma, int cn) {
+    return k <= 7 && bwd_lds_bytes(k, C, 16, dma, D, cn) <= kBwdLdsLimit ? 16 : 8;
 }
-inline size_t bwd_lds_need(int k, int C, int D, bool dma) {
-    return bwd_lds_bytes(k, C, bwd_tile_h(k, C, D, dma), dma, D);
+inline size_t bwd_lds_need(int k, int C, int D, bool dma, int cn) {
+    return bwd_lds_bytes(k, C, bwd_tile_h(k, C, D, dma, cn), dma, D, cn);
 }
 
 hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream);
