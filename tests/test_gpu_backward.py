@@ -210,6 +210,20 @@ def test_blur_workload_backward_full(torch_cuda, crf, oracle_mod):
     check(got, ref, "blur workload", wl.iters)
 
 
+def test_street_backward_full(torch_cuda, crf, oracle_mod):
+    """The street workload, 1 x 19 x 1024 x 2048, k = 7, T = 5, in full
+    (19 classes: class groups of 7, 7 and 5)."""
+    wl = synth.WORKLOADS["street"]
+    U, I, _ = synth.make_inputs(wl)
+    G = np.random.default_rng(79).normal(0.0, 1.0, U.shape).astype(np.float32)
+    p = params(wl.filter_size, w_app=wl.w_app, theta_alpha=wl.theta_alpha,
+               theta_beta=wl.theta_beta, w_smooth=wl.w_smooth, theta_gamma=wl.theta_gamma)
+    print("case street 1x19x1024x2048 k=7 T=5", flush=True)
+    got = run_gpu(torch_cuda, crf, U, I, G, p, wl.iters)
+    ref = run_oracle(oracle_mod, U, I, G, p, wl.iters)
+    check(got, ref, "street", wl.iters)
+
+
 def test_outputs_are_independent_of_what_is_requested(torch_cuda, crf):
     U, I, G = make_case(21, 1, 21, 48, 64)
     p = params(7)
