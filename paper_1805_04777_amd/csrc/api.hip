@@ -245,6 +245,15 @@ hipError_t launch_stream(const IterArgs& a, int k, size_t lds, hipStream_t s) {
     }
 }
 
+hipError_t launch_ring(const IterArgs& a, int k, hipStream_t s) {
+    switch (k) {
+        case 3: return launch_ring_k3(a, s);
+        case 5: return launch_ring_k5(a, s);
+        case 7: return launch_ring_k7(a, s);
+        default: return hipErrorNotSupported;
+    }
+}
+
 hipError_t launch_resident(const IterArgs& a, int k, TileConfig t, size_t lds, int num_cus,
                            hipStream_t s, bool probe) {
     switch (k) {
@@ -276,9 +285,10 @@ TileConfig pick_tile(int k, int C, bool colour, bool compat) {
 // streamed: whether the streamed kernel runs the iterations (k = 3..7,
 // C = 19 or 21, whole float2 rows, unary rows in 16-byte pieces, buffers
 // under 2 GB, the LDS within bounds).
-void plan_unpooled(IterArgs& a, IterArgs& as, bool& streamed, size_t& lds_s, TileConfig tile,
-                   bool mat, int k, int B, int C, int H, int W, const float* unary,
-                   const float* image, const float* kmat, std::initializer_list<const void*> bufs) {
+void plan_unpooled(IterArgs& a, IterArgs& as, IterArgs& ar, bool& streamed, bool& ring,
+                   size_t& lds_s, TileConfig tile, bool mat, int k, int B, int C, int H, int W,
+                   const float* unary, const float* image, const float* kmat,
+                   std::initializer_list<const void*> bufs) {
     a.C = C;
     a.planes = C;
     a.H = H;
@@ -302,6 +312,12 @@ void plan_unpooled(IterArgs& a, IterArgs& as, bool& streamed, size_t& lds_s, Til
     as.tiles_x = (W + kStreamTW - 1) / kStreamTW;
     as.tiles_per_img = as.tiles_x * ((H + kStreamRows - 1) / kStreamRows);
     as.ntiles = as.tiles_per_img * B;
+    // the later streamed iterations on half-height tiles, two work-groups
+    // per CU (the first one stages all classes at once and keeps stream_kernel)
+    ar = as;
+    ar.tiles_per_img = as.tiles_x * ((H + kRingRows - 1) / kRingRows);
+    ar.ntiles = ar.tiles_per_img * B;
+    ring = streamed && ring_lds_bytes(k, C, C == 19 ? 4 : 3, a.mu != nullptr) <= kLdsLimit;
 }
 
 // Arguments of the learnable-feature update over B x C x H x W.
@@ -582,10 +598,10 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
                 if (st != CONVCRF_OK) return st;
             }
         }
-        IterArgs as;                          // the streamed launches' tiling
-        bool streamed = false;
+        IterArgs as, ar;                      // the streamed and ring launches' tilings
+        bool streamed = false, ring = false;
         size_t lds_s = 0;
-        plan_unpooled(a, as, streamed, lds_s, tile, mat, k, B, C, H, W, unary, image,
+        plan_unpooled(a, as, ar, streamed, ring, lds_s, tile, mat, k, B, C, H, W, unary, image,
                       static_cast<const float*>(ctx->kmat.p), {q_out, ctx->q_ws.p});
         // Resident variant: all iterations in one launch when every tile's
         // work-group fits on the device at once (Potts): the tile stays in
@@ -651,11 +667,12 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
         const float* cur = unary;
         for (int t = 0; t < iters; ++t) {
             float* dst = ((iters - 1 - t) % 2 == 0) ? q_out : ws;
-            a.src = as.src = cur;
-            a.dst = as.dst = dst;
-            a.first = as.first = t == 0;
+            a.src = as.src = ar.src = cur;
+            a.dst = as.dst = ar.dst = dst;
+            a.first = as.first = ar.first = t == 0;
             st = launch(ctx, mat ? kMatIter : kFused, stream, mat ? "materialised_iter" : "fused_iter",
                         [&] {
+                            if (ring && t > 0) return launch_ring(ar, k, stream);
                             return streamed ? launch_stream(as, k, lds_s, stream)
                                             : launch_iter(a, k, mat, tile, lds, stream);
                         });
@@ -888,16 +905,17 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         const TileConfig tile = pick_tile(k, C, true, mu_dev != nullptr);
         if (tile.rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
         const size_t lds = iter_lds_bytes(k, C, tile, true, mu_dev != nullptr);
-        IterArgs as;
-        bool streamed = false;
+        IterArgs as, ar;
+        bool streamed = false, ring = false;
         size_t lds_s = 0;
-        plan_unpooled(a, as, streamed, lds_s, tile, false, k, B, C, H, W, unary, image, nullptr,
-                      {qbase});
+        plan_unpooled(a, as, ar, streamed, ring, lds_s, tile, false, k, B, C, H, W, unary, image,
+                      nullptr, {qbase});
         for (int t = 0; t < iters; ++t) {
-            a.src = as.src = t == 0 ? unary : qs(t);
-            a.dst = as.dst = qs(t + 1);
-            a.first = as.first = t == 0;
+            a.src = as.src = ar.src = t == 0 ? unary : qs(t);
+            a.dst = as.dst = ar.dst = qs(t + 1);
+            a.first = as.first = ar.first = t == 0;
             st = launch(ctx, kFused, stream, "fused_iter", [&] {
+                if (ring && t > 0) return launch_ring(ar, k, stream);
                 return streamed ? launch_stream(as, k, lds_s, stream)
                                 : launch_iter(a, k, false, tile, lds, stream);
             });

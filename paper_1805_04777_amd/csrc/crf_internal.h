@@ -94,6 +94,21 @@ inline size_t stream_lds_bytes(int k, int C, bool with_compat) {
                             (with_compat ? ((size_t)C * C + 63) / 64 * 64 : 0) + 256);
 }
 
+// Ring update (the later iterations, k <= 7, C = 19 or 21): tiles of
+// kStreamTW x kRingRows pixels, 256 threads, the class chunks cycled through
+// three LDS slots and the unary loaded into registers, so that two
+// work-groups share a CU; LDS bytes of a work-group (three slots of CH
+// planes, the colours, the compatibility in whole rows when given, one dummy
+// row).
+constexpr int kRingRows = 8, kRingSlots = 3;
+constexpr int ring_plane(int k) {
+    return ((kRingRows + k - 1) * iter_lds_stride(k, 2, kStreamTW) + 63) / 64 * 64;
+}
+inline size_t ring_lds_bytes(int k, int C, int CH, bool with_compat) {
+    return sizeof(float) * ((size_t)(kRingSlots * CH + 3) * ring_plane(k) +
+                            (with_compat ? ((size_t)C * C + 63) / 64 * 64 : 0) + 256);
+}
+
 // Pooled message of the blur path: tiles of 16 x 8 cells, one wavefront per
 // window row (64 k threads), chunks of at most kPmsgClasses classes; LDS
 // bytes of a work-group (the chunk's planes and the colours with their halo,
@@ -138,6 +153,7 @@ inline size_t iter_lds_bytes(int k, int C, TileConfig t, bool with_colour, bool 
                                 hipStream_t stream);                         \
     hipError_t launch_stream_k##K(const IterArgs& a, size_t lds,             \
                                   hipStream_t stream);                       \
+    hipError_t launch_ring_k##K(const IterArgs& a, hipStream_t stream);      \
     hipError_t launch_pmsg_k##K(const IterArgs& a, int nchunks, size_t lds,  \
                                 hipStream_t stream);                         \
     hipError_t launch_rstream_k##K(const IterArgs& a, size_t lds,            \

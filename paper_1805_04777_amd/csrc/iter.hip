@@ -978,6 +978,221 @@ hipError_t launch_stream(const IterArgs& a, size_t lds, hipStream_t stream) {
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------- ring update
+// The later iterations on half-height tiles (kStreamTW x kRingRows, 256
+// threads, two pixels each) so that two work-groups share a CU and one's
+// waits overlap the other's arithmetic.  As stream_kernel, but the class
+// chunks cycle through kRingSlots LDS slots (chunk k in slot k mod 3; chunk
+// k + 2 is issued into the slot of chunk k - 1 once every wave is past it)
+// and each thread's unary comes straight into registers, issued first.
+template <int K, int CM, int CH>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void ring_kernel(const IterArgs a) {
+    constexpr int R = (K - 1) / 2;
+    constexpr int P = 2, TW = kStreamTW, ROWS = kRingRows, TPR = TW / P, NWAVE = 4;
+    static_assert(TPR * ROWS == 256, "256 threads, two pixels each");
+    constexpr int LW = TW + 2 * R, LH = ROWS + 2 * R;
+    constexpr int LS = iter_lds_stride(K, 2, TW);
+    constexpr int PLANE = ring_plane(K);
+    constexpr int NI = PLANE / 64;               // 64-float loads per plane
+    constexpr int NJ = (NI + NWAVE - 1) / NWAVE; // per wave and plane
+    constexpr int NW = P + K - 1;
+    constexpr int CTR = R * K + R;
+    constexpr int NCH = (CM + CH - 1) / CH;
+    constexpr unsigned kOob = 0x80000000u;
+    constexpr int MUP = (CM * CM + 63) / 64 * 64;
+    extern __shared__ float4 smem4[];
+    float* const smem = reinterpret_cast<float*>(smem4);
+    float* const Qs = smem;                              // [3][CH][PLANE]
+    float* const Cs = smem + kRingSlots * CH * PLANE;    // [3][PLANE]
+    float* const Ms = Cs + 3 * PLANE;                    // [CM][CM] (+ padding) when given
+    float* const dummy = Ms + (a.mu ? MUP : 0);          // one 256-float row
+    const unsigned lds0 = (unsigned)(size_t)(__attribute__((address_space(3))) float*)smem;
+    auto lds_addr = [&](const float* p) { return lds0 + (unsigned)((p - smem) * 4); };
+
+    const int H = a.H, W = a.W;
+    const int tile = xcd_tile(blockIdx.x, a.ntiles);
+    const int b = tile / a.tiles_per_img;
+    const int trem = tile - b * a.tiles_per_img;
+    const int tyi = trem / a.tiles_x;
+    const int y0 = tyi * ROWS;
+    const int x0 = (trem - tyi * a.tiles_x) * TW;
+    const size_t HW = (size_t)H * W;
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int tx = tid % TPR, ty = tid / TPR;
+    const int col0 = tx * P;
+    const int y = y0 + ty, xb = x0 + col0;
+    const bool pix_ok = y < H && xb < W;        // W even: both pixels or neither
+
+    // ---- the unary of this thread's pixels, into registers (issued before
+    // the LDS loads, so every wait below also covers it)
+    float u[P][CM];
+    {
+        const float* up = a.unary + (size_t)b * CM * HW + (size_t)(pix_ok ? y : 0) * W +
+                          (pix_ok ? xb : 0);
+#pragma unroll
+        for (int c = 0; c < CM; ++c) {
+            const float2 t = *reinterpret_cast<const float2*>(up + c * HW);
+            u[0][c] = t.x;
+            u[1][c] = t.y;
+        }
+    }
+
+    // ---- colours, then the first two chunks of Q_t
+    unsigned voff[NJ];
+    int dst[NJ];                                 // float offset in a plane, or -1: dummy
+#pragma unroll
+    for (int s = 0; s < NJ; ++s) {
+        const int j = wave + NWAVE * s;
+        const int f = j * 64 + lane;
+        const int r = f / LS, col = f - (f / LS) * LS;
+        const int gy = y0 - R + r, gx = x0 - R + col;
+        const bool in = j < NI && f < LH * LS && col < LW && gy >= 0 && gy < H && gx >= 0 && gx < W;
+        voff[s] = in ? (unsigned)((gy * W + gx) * 4) : kOob;
+        dst[s] = j < NI ? j * 64 : -1;
+    }
+    const rsrc_t rf = buffer_rsrc(a.feat + (size_t)b * 3 * HW, (unsigned)(3 * HW * 4));
+    const rsrc_t rq = buffer_rsrc(a.src + (size_t)b * CM * HW, (unsigned)(CM * HW * 4));
+    constexpr int NMU = (MUP / 64 + NWAVE - 1) / NWAVE;
+    const int nmu = a.mu ? NMU : 0;
+    const rsrc_t rm = buffer_rsrc(a.mu ? a.mu : a.feat, (unsigned)(CM * CM * 4));
+    for (int s = 0; s < nmu; ++s) {
+        const int j = wave + NWAVE * s;
+        lds_dma(rm, (unsigned)((j * 64 + lane) * 4), 0, lds_addr(j < MUP / 64 ? Ms + j * 64 : dummy));
+    }
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch)
+#pragma unroll
+        for (int s = 0; s < NJ; ++s)
+            lds_dma(rf, voff[s], (int)(ch * HW * 4),
+                    lds_addr(dst[s] >= 0 ? Cs + ch * PLANE + dst[s] : dummy));
+    // chunk k goes to slot k % kRingSlots
+    auto issue_chunk = [&](int k) {
+        const int c_lo = k * CH, c_hi = (k + 1) * CH < CM ? (k + 1) * CH : CM;
+        float* const slot = Qs + (k % kRingSlots) * CH * PLANE;
+        for (int c = c_lo; c < c_hi; ++c)
+#pragma unroll
+            for (int s = 0; s < NJ; ++s)
+                lds_dma(rq, voff[s], (int)(c * HW * 4),
+                        lds_addr(dst[s] >= 0 ? slot + (c - c_lo) * PLANE + dst[s] : dummy));
+    };
+    issue_chunk(0);
+    if (NCH > 1) issue_chunk(1);
+
+    // ---- colours landed: the window weights of both pixels, all rows
+    __builtin_amdgcn_s_waitcnt(vm_wait(stream_chunk_loads(0, CM, CH, NJ) +
+                                       stream_chunk_loads(1, CM, CH, NJ)));
+    __syncthreads();
+    float w[K][P][K];
+    {
+        float own[3][P];
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch)
+#pragma unroll
+            for (int i = 0; i < P; ++i) own[ch][i] = Cs[ch * PLANE + (ty + R) * LS + col0 + R + i];
+#pragma unroll
+        for (int dy = 0; dy < K; ++dy) {
+            float nc[3][NW];
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) lds_row<NW, P>(Cs + ch * PLANE + (ty + dy) * LS + col0, nc[ch]);
+#pragma unroll
+            for (int i = 0; i < P; ++i) {
+#pragma unroll
+                for (int dx = 0; dx < K; ++dx) {
+                    if (dy * K + dx == CTR) { w[dy][i][dx] = 0.f; continue; }
+                    const int n = (dx - R) * (dx - R) + (dy - R) * (dy - R);
+                    const float d0 = own[0][i] - nc[0][i + dx];
+                    const float d1 = own[1][i] - nc[1][i + dx];
+                    const float d2 = own[2][i] - nc[2][i + dx];
+                    const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
+                    w[dy][i][dx] = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, a.taps.app_log2[n])) +
+                                   a.taps.smooth[n];
+                }
+            }
+        }
+    }
+
+    float acc[P][CM];
+#pragma unroll
+    for (int i = 0; i < P; ++i)
+#pragma unroll
+        for (int c = 0; c < CM; ++c) acc[i][c] = 0.f;
+    static_for([&](auto kc) {
+        constexpr int k = decltype(kc)::value;
+        constexpr int c_lo = k * CH;
+        constexpr int c_hi = (k + 1) * CH < CM ? (k + 1) * CH : CM;
+        // chunk k landed (chunk k + 1 may still be in flight); every wave is
+        // past chunk k - 1, whose slot chunk k + 2 takes
+        __builtin_amdgcn_s_waitcnt(vm_wait(stream_chunk_loads(k + 1, CM, CH, NJ)));
+        __syncthreads();
+        if constexpr (k + 2 < NCH) issue_chunk(k + 2);
+        // the slot seen as planes c_lo .. c_hi - 1 of Q_t
+        const float* const qk = Qs + (k % kRingSlots) * CH * PLANE - c_lo * PLANE;
+        message_chunk<K, P, LS, PLANE, CM, c_lo, c_hi>(qk, ty, col0, w, acc);
+        if (a.include_center) {
+#pragma unroll
+            for (int c = c_lo; c < c_hi; ++c)
+#pragma unroll
+                for (int i = 0; i < P; ++i)
+                    acc[i][c] = fmaf(a.center_w, qk[c * PLANE + (ty + R) * LS + col0 + R + i],
+                                     acc[i][c]);
+        }
+    }, std::make_integer_sequence<int, NCH>{});
+    if (!pix_ok) return;
+
+    // ---- compatibility, unary, softmax (Alg. 1), store Q_{t+1}
+    if (a.mu) {
+        float z[P][CM];
+#pragma unroll
+        for (int l = 0; l < CM; ++l) {
+            float t[P];
+#pragma unroll
+            for (int i = 0; i < P; ++i) t[i] = 0.f;
+#pragma unroll
+            for (int lp = 0; lp < CM; ++lp) {
+                const float m = Ms[l * CM + lp];
+#pragma unroll
+                for (int i = 0; i < P; ++i) t[i] = fmaf(m, acc[i][lp], t[i]);
+            }
+#pragma unroll
+            for (int i = 0; i < P; ++i) z[i][l] = u[i][l] - t[i];
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int i = 0; i < P; ++i)
+#pragma unroll
+            for (int c = 0; c < CM; ++c) acc[i][c] = z[i][c];
+    } else {
+        // Potts: softmax(U + M)
+#pragma unroll
+        for (int i = 0; i < P; ++i)
+#pragma unroll
+            for (int c = 0; c < CM; ++c) acc[i][c] += u[i][c];
+    }
+#pragma unroll
+    for (int i = 0; i < P; ++i) softmax_regs<CM, true>(acc[i], CM);
+    float* __restrict__ qd = a.dst + (size_t)b * CM * HW + (size_t)y * W + xb;
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        float tmp[P];
+#pragma unroll
+        for (int i = 0; i < P; ++i) tmp[i] = acc[i][c];
+        *reinterpret_cast<typename Vec<P>::T*>(qd + c * HW) = Vec<P>::make(tmp);
+    }
+}
+
+template <int K, int CM, int CH>
+hipError_t launch_ring(const IterArgs& a, hipStream_t stream) {
+    auto fn = ring_kernel<K, CM, CH>;
+    hipError_t e = allow_full_lds(fn);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fn, dim3(a.ntiles), dim3(256), ring_lds_bytes(K, CM, CH, a.mu != nullptr),
+                       stream, a);
+    return hipGetLastError();
+}
+
 // ---------------------------------------------------- resident streamed form
 // All T iterations in one cooperative launch on the tiles of stream_kernel
 // (every tile's work-group co-resident).  The window weights (the colours do
@@ -1433,6 +1648,24 @@ hipError_t CRF_CAT(launch_stream_k, CRF_K)(const IterArgs& a, size_t lds, hipStr
         switch (a.C) {
             case 19: return launch_stream<K, 19, 4>(a, lds, stream);
             case 21: return launch_stream<K, 21, 3>(a, lds, stream);
+            default: return hipErrorNotSupported;
+        }
+    }
+}
+
+// Ring updates: as the streamed ones, later iterations only (the source is
+// Q_t), on kStreamTW x kRingRows tiles.
+hipError_t CRF_CAT(launch_ring_k, CRF_K)(const IterArgs& a, hipStream_t stream) {
+    constexpr int K = CRF_K;
+    if constexpr (K < 3 || K > 7) {
+        return hipErrorNotSupported;
+    } else {
+        if (a.mode != kModeUpdate || a.first || a.planes != a.C || !a.vec || (a.W & 3) ||
+            (size_t)a.C * a.H * a.W * 4 >= (1ull << 31))
+            return hipErrorNotSupported;
+        switch (a.C) {
+            case 19: return launch_ring<K, 19, 4>(a, stream);
+            case 21: return launch_ring<K, 21, 3>(a, stream);
             default: return hipErrorNotSupported;
         }
     }
