@@ -320,6 +320,37 @@ void plan_unpooled(IterArgs& a, IterArgs& as, IterArgs& ar, bool& streamed, bool
     ring = streamed && ring_lds_bytes(k, C, C == 19 ? 4 : 3, a.mu != nullptr) <= kLdsLimit;
 }
 
+// Ring launches for the learnable-feature iterations (Sec. 4.2, "+T") over
+// B x C x H x W: true and `ar` set when the shapes allow them (k = 3..7,
+// C = 19 or 21, 1..kMaxFeat feature planes, whole float2 rows with W a
+// multiple of 4, the unary 16-byte aligned, buffers under 2 GB, the LDS
+// within bounds); every iteration then reads Q_t (no first-iteration form).
+bool plan_feature_ring(IterArgs& ar, const convcrf_params& p, const float* unary,
+                       const float* image, const float* mu_dev, int B, int C, int H, int W,
+                       std::initializer_list<const void*> bufs) {
+    const int k = p.filter_size, D = p.feature_dim;
+    if (k < 3 || k > 7 || D < 1 || D > kMaxFeat || (size_t)D * H * W * 4 >= (1ull << 31))
+        return false;
+    IterArgs a{}, as{};
+    a.mu = mu_dev;
+    a.include_center = p.include_center;
+    a.neg_beta = (float)(-kLog2eD / (2.0 * (double)p.theta_beta * p.theta_beta));
+    a.center_w = (float)((double)p.w_app + (double)p.w_smooth);
+    fill_taps(p, 1, a.taps);
+    bool streamed = false, ring = false;
+    size_t lds_s = 0;
+    plan_unpooled(a, as, ar, streamed, ring, lds_s, TileConfig{32, 2, 32}, false, k, B, C, H, W,
+                  unary, image, nullptr, bufs);
+    if (!ring || ring_lds_bytes(k, C, C == 19 ? 4 : 3, mu_dev != nullptr, D) > kLdsLimit)
+        return false;
+    ar.sfeat = p.features;
+    ar.D = D;
+    ar.neg_gamma = (float)(-kLog2eD / (2.0 * (double)p.theta_gamma * p.theta_gamma));
+    ar.w_smooth = p.w_smooth;
+    ar.first = 0;
+    return true;
+}
+
 // Arguments of the learnable-feature update over B x C x H x W.
 FeatArgs feat_args(const convcrf_params& p, const float* unary, const float* image,
                    const float* mu_dev, int B, int C, int H, int W) {
@@ -556,16 +587,19 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
         // the staged Q planes live in q_out and the workspace
         f.vec4 = f.vec4 && reinterpret_cast<uintptr_t>(q_out) % 16 == 0 &&
                  reinterpret_cast<uintptr_t>(ws) % 16 == 0;
+        IterArgs ar{};
+        const bool ring = plan_feature_ring(ar, p, unary, image, mu_dev, B, C, H, W, {q_out, ws});
         float* q0 = iters % 2 == 0 ? q_out : ws;
         st = launch(ctx, kSoftmax, stream, "softmax",
                     [&] { return launch_softmax(unary, q0, B, C, H * W, stream); });
         if (st != CONVCRF_OK) return st;
         const float* cur = q0;
         for (int t = 0; t < iters; ++t) {
-            f.src = cur;
-            f.dst = ((iters - 1 - t) % 2 == 0) ? q_out : ws;
-            st = launch(ctx, kFeatIter, stream, "feature_iter",
-                        [&] { return launch_feat_update(f, k, stream); });
+            f.src = ar.src = cur;
+            f.dst = ar.dst = ((iters - 1 - t) % 2 == 0) ? q_out : ws;
+            st = launch(ctx, kFeatIter, stream, "feature_iter", [&] {
+                return ring ? launch_ring(ar, k, stream) : launch_feat_update(f, k, stream);
+            });
             if (st != CONVCRF_OK) return st;
             cur = f.dst;
         }
@@ -888,11 +922,14 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         }
     } else if (run && p.features) {
         FeatArgs f = feat_args(p, unary, image, mu_dev, B, C, H, W);
+        IterArgs ar{};
+        const bool ring = plan_feature_ring(ar, p, unary, image, mu_dev, B, C, H, W, {qbase});
         for (int t = 0; t < iters; ++t) {
-            f.src = qs(t);
-            f.dst = qs(t + 1);
-            st = launch(ctx, kFeatIter, stream, "feature_iter",
-                        [&] { return launch_feat_update(f, k, stream); });
+            f.src = ar.src = qs(t);
+            f.dst = ar.dst = qs(t + 1);
+            st = launch(ctx, kFeatIter, stream, "feature_iter", [&] {
+                return ring ? launch_ring(ar, k, stream) : launch_feat_update(f, k, stream);
+            });
             if (st != CONVCRF_OK) return st;
         }
     } else if (run) {

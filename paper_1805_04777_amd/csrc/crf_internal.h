@@ -63,6 +63,12 @@ struct IterArgs {
     unsigned int* sync;   // [0] error flag, [1 + tile] rings published by each
                           // tile; all zero before the launch
     int include_center;   // add (w_app + w_smooth) Q_p to the message
+    // learnable smoothness features (ring update only): F [B][D][H][W] or
+    // null; the smoothness Gaussian is then w_smooth exp2(neg_gamma |F_p -
+    // F_q|^2) instead of taps.smooth
+    const float* sfeat;
+    int D;
+    float neg_gamma, w_smooth;
     int mode;             // IterMode
     int vec;              // W % pix == 0 and planes aligned to 4*pix bytes:
                           // each thread loads and stores its pixels as one
@@ -104,8 +110,8 @@ constexpr int kRingRows = 8, kRingSlots = 3;
 constexpr int ring_plane(int k) {
     return ((kRingRows + k - 1) * iter_lds_stride(k, 2, kStreamTW) + 63) / 64 * 64;
 }
-inline size_t ring_lds_bytes(int k, int C, int CH, bool with_compat) {
-    return sizeof(float) * ((size_t)(kRingSlots * CH + 3) * ring_plane(k) +
+inline size_t ring_lds_bytes(int k, int C, int CH, bool with_compat, int D = 0) {
+    return sizeof(float) * ((size_t)(kRingSlots * CH + 3 + D) * ring_plane(k) +
                             (with_compat ? ((size_t)C * C + 63) / 64 * 64 : 0) + 256);
 }
 

@@ -985,7 +985,10 @@ hipError_t launch_stream(const IterArgs& a, size_t lds, hipStream_t stream) {
 // chunks cycle through kRingSlots LDS slots (chunk k in slot k mod 3; chunk
 // k + 2 is issued into the slot of chunk k - 1 once every wave is past it)
 // and each thread's unary comes straight into registers, issued first.
-template <int K, int CM, int CH>
+// FD > 0: learnable smoothness features (the "+T" variant of Sec. 4.2): the
+// FD feature planes are staged beside the colours and the smoothness Gaussian
+// of each weight is taken on the feature distance.
+template <int K, int CM, int CH, int FD>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void ring_kernel(const IterArgs a) {
     constexpr int R = (K - 1) / 2;
@@ -1003,10 +1006,13 @@ void ring_kernel(const IterArgs a) {
     constexpr int MUP = (CM * CM + 63) / 64 * 64;
     extern __shared__ float4 smem4[];
     float* const smem = reinterpret_cast<float*>(smem4);
+    constexpr bool FT = FD > 0;
+    constexpr int D = FD;
     float* const Qs = smem;                              // [3][CH][PLANE]
     float* const Cs = smem + kRingSlots * CH * PLANE;    // [3][PLANE]
     float* const Ms = Cs + 3 * PLANE;                    // [CM][CM] (+ padding) when given
     float* const dummy = Ms + (a.mu ? MUP : 0);          // one 256-float row
+    float* const Fs = dummy + 256;                       // [FD][PLANE]
     const unsigned lds0 = (unsigned)(size_t)(__attribute__((address_space(3))) float*)smem;
     auto lds_addr = [&](const float* p) { return lds0 + (unsigned)((p - smem) * 4); };
 
@@ -1068,6 +1074,15 @@ void ring_kernel(const IterArgs a) {
         for (int s = 0; s < NJ; ++s)
             lds_dma(rf, voff[s], (int)(ch * HW * 4),
                     lds_addr(dst[s] >= 0 ? Cs + ch * PLANE + dst[s] : dummy));
+    if constexpr (FT) {
+        const rsrc_t rs = buffer_rsrc(a.sfeat + (size_t)b * D * HW, (unsigned)(D * HW * 4));
+#pragma unroll
+        for (int ch = 0; ch < D; ++ch)
+#pragma unroll
+            for (int s = 0; s < NJ; ++s)
+                lds_dma(rs, voff[s], (int)(ch * HW * 4),
+                        lds_addr(dst[s] >= 0 ? Fs + ch * PLANE + dst[s] : dummy));
+    }
     // chunk k goes to slot k % kRingSlots
     auto issue_chunk = [&](int k) {
         const int c_lo = k * CH, c_hi = (k + 1) * CH < CM ? (k + 1) * CH : CM;
@@ -1094,6 +1109,29 @@ void ring_kernel(const IterArgs a) {
             for (int i = 0; i < P; ++i) own[ch][i] = Cs[ch * PLANE + (ty + R) * LS + col0 + R + i];
 #pragma unroll
         for (int dy = 0; dy < K; ++dy) {
+            // FT: the squared feature distance accumulates in w first, one
+            // plane at a time, to keep the register footprint of a row small
+            if constexpr (FT) {
+#pragma unroll
+                for (int i = 0; i < P; ++i)
+#pragma unroll
+                    for (int dx = 0; dx < K; ++dx) w[dy][i][dx] = 0.f;
+#pragma unroll
+                for (int ch = 0; ch < D; ++ch) {
+                    const float* const fp = Fs + ch * PLANE;
+                    float fo[P], nf[NW];
+#pragma unroll
+                    for (int i = 0; i < P; ++i) fo[i] = fp[(ty + R) * LS + col0 + R + i];
+                    lds_row<NW, P>(fp + (ty + dy) * LS + col0, nf);
+#pragma unroll
+                    for (int i = 0; i < P; ++i)
+#pragma unroll
+                        for (int dx = 0; dx < K; ++dx) {
+                            const float e = fo[i] - nf[i + dx];
+                            w[dy][i][dx] = fmaf(e, e, w[dy][i][dx]);
+                        }
+                }
+            }
             float nc[3][NW];
 #pragma unroll
             for (int ch = 0; ch < 3; ++ch) lds_row<NW, P>(Cs + ch * PLANE + (ty + dy) * LS + col0, nc[ch]);
@@ -1107,8 +1145,10 @@ void ring_kernel(const IterArgs a) {
                     const float d1 = own[1][i] - nc[1][i + dx];
                     const float d2 = own[2][i] - nc[2][i + dx];
                     const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
+                    const float smo = FT ? a.w_smooth * __builtin_amdgcn_exp2f(a.neg_gamma * w[dy][i][dx])
+                                         : a.taps.smooth[n];
                     w[dy][i][dx] = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, a.taps.app_log2[n])) +
-                                   a.taps.smooth[n];
+                                   smo;
                 }
             }
         }
@@ -1185,11 +1225,19 @@ void ring_kernel(const IterArgs a) {
 
 template <int K, int CM, int CH>
 hipError_t launch_ring(const IterArgs& a, hipStream_t stream) {
-    auto fn = ring_kernel<K, CM, CH>;
+    auto fn = ring_kernel<K, CM, CH, 0>;
+    switch (a.sfeat ? a.D : 0) {
+        case 0: break;
+        case 1: fn = ring_kernel<K, CM, CH, 1>; break;
+        case 2: fn = ring_kernel<K, CM, CH, 2>; break;
+        case 3: fn = ring_kernel<K, CM, CH, 3>; break;
+        case 4: fn = ring_kernel<K, CM, CH, 4>; break;
+        default: return hipErrorNotSupported;
+    }
     hipError_t e = allow_full_lds(fn);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(fn, dim3(a.ntiles), dim3(256), ring_lds_bytes(K, CM, CH, a.mu != nullptr),
-                       stream, a);
+    hipLaunchKernelGGL(fn, dim3(a.ntiles), dim3(256),
+                       ring_lds_bytes(K, CM, CH, a.mu != nullptr, a.sfeat ? a.D : 0), stream, a);
     return hipGetLastError();
 }
 
@@ -1661,7 +1709,8 @@ hipError_t CRF_CAT(launch_ring_k, CRF_K)(const IterArgs& a, hipStream_t stream) 
         return hipErrorNotSupported;
     } else {
         if (a.mode != kModeUpdate || a.first || a.planes != a.C || !a.vec || (a.W & 3) ||
-            (size_t)a.C * a.H * a.W * 4 >= (1ull << 31))
+            (size_t)a.C * a.H * a.W * 4 >= (1ull << 31) ||
+            (a.sfeat && (a.D < 1 || a.D > kMaxFeat || (size_t)a.D * a.H * a.W * 4 >= (1ull << 31))))
             return hipErrorNotSupported;
         switch (a.C) {
             case 19: return launch_ring<K, 19, 4>(a, stream);

@@ -68,6 +68,12 @@ CASES = [
     (4, 1, 19, 24, 36, 9, 2, 3, False, True),
     (5, 1, 4, 17, 23, 13, 1, 1, True, False),
     (6, 1, 24, 16, 24, 7, 1, 4, False, False),
+    # the ring kernel's feature mode (C = 19 or 21, W a multiple of 4,
+    # k = 3..7): every feature count, ragged rows and columns, B = 2
+    (11, 2, 19, 21, 68, 5, 3, 1, True, True),
+    (12, 1, 19, 30, 44, 3, 2, 3, False, False),
+    (13, 1, 21, 19, 36, 7, 3, 4, True, False),
+    (14, 1, 19, 13, 72, 7, 2, 2, True, True),
 ]
 
 
@@ -158,9 +164,10 @@ def test_feature_errors(torch_cuda, crf):
 
 def test_unaligned_output_takes_the_scalar_staging(torch_cuda, crf):
     """An output 4 bytes off a 16-byte boundary stages Q by scalars; the
-    arithmetic is the same, so the result is identical to the vector path."""
+    arithmetic is the same, so the result is identical to the vector path
+    (20 classes: the ring kernel does not take these shapes)."""
     torch = torch_cuda
-    U, I, F, _ = make_case(10, 1, 21, 32, 48, 2)
+    U, I, F, _ = make_case(10, 1, 20, 32, 48, 2)
     Ut, It = torch.from_numpy(U).cuda(), torch.from_numpy(I).cuda()
     p = params(torch, 7, F)
     a = crf.meanfield(Ut, It, p, 3)
@@ -170,3 +177,26 @@ def test_unaligned_output_takes_the_scalar_staging(torch_cuda, crf):
     b = crf.meanfield(Ut, It, p, 3, out=out)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+def test_ring_and_feature_kernel_agree(torch_cuda, crf, oracle_mod):
+    """21 classes: an aligned output runs the ring kernel's feature mode, an
+    output 4 bytes off an 8-byte boundary the feature kernel; both meet the
+    inference bar against the oracle and each other (their rounding differs,
+    so they are not bitwise equal)."""
+    torch = torch_cuda
+    U, I, F, _ = make_case(15, 1, 21, 40, 56, 3)
+    Ut, It = torch.from_numpy(U).cuda(), torch.from_numpy(I).cuda()
+    p = params(torch, 7, F, True)
+    a = crf.meanfield(Ut, It, p, 3)
+    buf = torch.empty(U.size + 1, device="cuda")
+    out = buf[1:].view(U.shape)
+    assert out.data_ptr() % 8 != 0
+    b = crf.meanfield(Ut, It, p, 3, out=out)
+    torch.cuda.synchronize()
+    a, b = (x.cpu().numpy().astype(np.float64) for x in (a, b))
+    o = oracle_mod.meanfield(U, I, oparams(p), 3, features=F)
+    ea, eb, eab = np.abs(a - o).max(), np.abs(b - o).max(), np.abs(a - b).max()
+    print(f"ring {ea:.2e}, feature kernel {eb:.2e}, between {eab:.2e}", flush=True)
+    assert ea <= 1e-4 and eb <= 1e-4 and eab <= 1e-4
+    assert eab > 0      # two different kernels: not the same path twice
