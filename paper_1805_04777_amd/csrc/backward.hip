@@ -244,51 +244,78 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
 #pragma unroll
             for (int c = 0; c < CM; ++c) qo[c] = c < CN ? sq[poff[c] + oc] : 0.f;
         }
-        constexpr int kRowUnroll = K <= 7 ? K : 1;   // a window row at once
+        // one tap: the offset's appearance log-prefactor al = a_log2[n], its
+        // smoothness Gaussian s0 = smooth[n] (positions) and nf = n
+        auto tap = [&](int dx, int dy, float al, float s0, float nf) {
+            const int o = oc + dy * LW + dx;
+            const float er = ir - sc[o], eg = ig - sc[PS + o], eb = ib - sc[2 * PS + o];
+            const float cd2 = fmaf(er, er, fmaf(eg, eg, eb * eb));
+            const float av = __builtin_amdgcn_exp2f(fmaf(a.neg_beta, cd2, al));
+            // the smoothness Gaussian and its squared distance: the
+            // positions, or the learnable features (FT)
+            float sd2 = nf, sv = s0;
+            float fdif[kMaxFeat];
+            if constexpr (FT) {
+                sd2 = 0.f;
+#pragma unroll
+                for (int c = 0; c < kMaxFeat; ++c) {
+                    fdif[c] = c < D ? fo[c] - sf[c * PS + o] : 0.f;
+                    sd2 = fmaf(fdif[c], fdif[c], sd2);
+                }
+                sv = __builtin_amdgcn_exp2f(a.neg_gamma * sd2);
+            }
+            const float w = fmaf(a.w_app, av, a.w_smooth * sv);
+            float dk = 0.f, dkr = 0.f;
+#pragma unroll
+            for (int c = 0; c < CM; ++c) {
+                const float qn = sq[poff[c] + o];
+                const float mn = sm[poff[c] + o];
+                dk = fmaf(dmq[c], qn, dk);
+                dqa[c] = fmaf(w, mn, dqa[c]);
+                if (WM) ma[0][c] = fmaf(w, qn, ma[0][c]);
+                if (FT) dkr = fmaf(mn, qo[c], dkr);
+            }
+            const float da = dk * av, ds = dk * sv;
+            g[0] += da;
+            g[1] = fmaf(da, nf, g[1]);
+            g[2] = fmaf(da, cd2, g[2]);
+            g[3] += ds;
+            g[4] = fmaf(ds, sd2, g[4]);
+            if constexpr (FT) {
+                const float coef = -(dk + dkr) * a.w_smooth * sv * a.inv_gamma2;
+#pragma unroll
+                for (int c = 0; c < kMaxFeat; ++c) dfa[c] = fmaf(coef, fdif[c], dfa[c]);
+            }
+        };
+        if constexpr (K <= 7) {
+            // a window row at once; the per-offset constants of the row are
+            // read once per row (n = dx^2 + dy^2 takes R + 1 values in it),
+            // so no table load waits inside the row
 #pragma unroll 1
-        for (int dy = -R; dy <= R; ++dy) {
-#pragma unroll kRowUnroll
-            for (int dx = -R; dx <= R; ++dx) {
-                if (dx == 0 && dy == 0 && !a.include_center) continue;
-                const int o = oc + dy * LW + dx;
-                const float er = ir - sc[o], eg = ig - sc[PS + o], eb = ib - sc[2 * PS + o];
-                const float cd2 = fmaf(er, er, fmaf(eg, eg, eb * eb));
-                const int n = dx * dx + dy * dy;
-                const float av = exp2f(fmaf(a.neg_beta, cd2, a.a_log2[n]));
-                // the smoothness Gaussian and its squared distance: the
-                // positions, or the learnable features (FT)
-                float sd2 = (float)n, sv = a.smooth[n];
-                float fdif[kMaxFeat];
-                if constexpr (FT) {
-                    sd2 = 0.f;
+            for (int dy = -R; dy <= R; ++dy) {
+                float ra[R + 1], rs[R + 1], rn[R + 1];
 #pragma unroll
-                    for (int c = 0; c < kMaxFeat; ++c) {
-                        fdif[c] = c < D ? fo[c] - sf[c * PS + o] : 0.f;
-                        sd2 = fmaf(fdif[c], fdif[c], sd2);
-                    }
-                    sv = exp2f(a.neg_gamma * sd2);
+                for (int j = 0; j <= R; ++j) {
+                    const int n = j * j + dy * dy;
+                    ra[j] = a.a_log2[n];
+                    rs[j] = a.smooth[n];
+                    rn[j] = (float)n;
                 }
-                const float w = fmaf(a.w_app, av, a.w_smooth * sv);
-                float dk = 0.f, dkr = 0.f;
 #pragma unroll
-                for (int c = 0; c < CM; ++c) {
-                    const float qn = sq[poff[c] + o];
-                    const float mn = sm[poff[c] + o];
-                    dk = fmaf(dmq[c], qn, dk);
-                    dqa[c] = fmaf(w, mn, dqa[c]);
-                    if (WM) ma[0][c] = fmaf(w, qn, ma[0][c]);
-                    if (FT) dkr = fmaf(mn, qo[c], dkr);
+                for (int dx = -R; dx <= R; ++dx) {
+                    if (dx == 0 && dy == 0 && !a.include_center) continue;
+                    const int j = dx < 0 ? -dx : dx;
+                    tap(dx, dy, ra[j], rs[j], rn[j]);
                 }
-                const float da = dk * av, ds = dk * sv;
-                g[0] += da;
-                g[1] = fmaf(da, (float)n, g[1]);
-                g[2] = fmaf(da, cd2, g[2]);
-                g[3] += ds;
-                g[4] = fmaf(ds, sd2, g[4]);
-                if constexpr (FT) {
-                    const float coef = -(dk + dkr) * a.w_smooth * sv * a.inv_gamma2;
-#pragma unroll
-                    for (int c = 0; c < kMaxFeat; ++c) dfa[c] = fmaf(coef, fdif[c], dfa[c]);
+            }
+        } else {
+#pragma unroll 1
+            for (int dy = -R; dy <= R; ++dy) {
+#pragma unroll 1
+                for (int dx = -R; dx <= R; ++dx) {
+                    if (dx == 0 && dy == 0 && !a.include_center) continue;
+                    const int n = dx * dx + dy * dy;
+                    tap(dx, dy, a.a_log2[n], a.smooth[n], (float)n);
                 }
             }
         }
@@ -335,6 +362,7 @@ hipError_t launch_msg_ktv(const BwdArgs& a, hipStream_t stream) {
 
 template <int K, int TH>
 hipError_t launch_msg_kt(const BwdArgs& a, hipStream_t stream) {
+    if (a.cgsize == 7) return launch_msg_ktv<K, TH, 7>(a, stream);   // 19 or 21 in three groups
     if (a.cgsize <= 8) return launch_msg_ktv<K, TH, 8>(a, stream);
     if (a.cgsize <= 21) return launch_msg_ktv<K, TH, 21>(a, stream);
     return launch_msg_ktv<K, TH, kMaxC>(a, stream);
