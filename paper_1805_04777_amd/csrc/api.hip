@@ -25,6 +25,7 @@ constexpr size_t kLdsLimit = 160 * 1024;  // gfx950 LDS per work-group
 // Most class groups the adjoint message splits its classes into (at least 4
 // classes per group).
 constexpr int kBwdClassGroups = 3;
+constexpr int kBwdMinGroups = 8;     // adjoint-message work-groups per CU sought on small grids
 
 const char* const kKernelNames[] = {"fused_iter",   "softmax",      "build_kernel",
                                     "materialised_iter", "blur_pool", "blur_message",
@@ -793,6 +794,16 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     // work-groups per CU and, on small grids, more work-groups; learnable
     // features keep one group (dL/dF sums over all classes in one place)
     int groups = D > 0 ? 1 : std::max(1, std::min(kBwdClassGroups, C / 4));
+    if (groups > 1) {
+        // small grids (the pooled grid of the blur variant): more groups,
+        // down to three classes each, until the launch has kBwdMinGroups
+        // work-groups per CU (the tiles of groups of at most 8 classes)
+        const long long t8 = (long long)((Wg + bwd_tile_w(k) - 1) / bwd_tile_w(k)) *
+                             ((Hg + 7) / 8) * B;
+        const long long want = (long long)kBwdMinGroups * ctx->num_cus;
+        if (t8 > 0 && t8 * groups < want)
+            groups = (int)std::max<long long>(groups, std::min<long long>(C / 3, (want + t8 - 1) / t8));
+    }
     const int cgsize = (C + groups - 1) / groups;
     groups = (C + cgsize - 1) / cgsize;
     const long long hw_ll = (long long)Hg * Wg;

@@ -360,10 +360,21 @@ hipError_t launch_msg_ktv(const BwdArgs& a, hipStream_t stream) {
     return launch_msg_ktc<K, TH, CM, false, false>(a, stream);
 }
 
+// The class loop runs CM >= cgsize classes; groups of up to 8 classes (8-row
+// tiles only) are instantiated at their own size.
 template <int K, int TH>
 hipError_t launch_msg_kt(const BwdArgs& a, hipStream_t stream) {
-    if (a.cgsize == 7) return launch_msg_ktv<K, TH, 7>(a, stream);   // 19 or 21 in three groups
-    if (a.cgsize <= 8) return launch_msg_ktv<K, TH, 8>(a, stream);
+    if constexpr (TH == 8) {
+        switch (a.cgsize) {
+            case 1: case 2: case 3: return launch_msg_ktv<K, TH, 3>(a, stream);
+            case 4: return launch_msg_ktv<K, TH, 4>(a, stream);
+            case 5: return launch_msg_ktv<K, TH, 5>(a, stream);
+            case 6: return launch_msg_ktv<K, TH, 6>(a, stream);
+            case 7: return launch_msg_ktv<K, TH, 7>(a, stream);
+            case 8: return launch_msg_ktv<K, TH, 8>(a, stream);
+            default: break;
+        }
+    }
     if (a.cgsize <= 21) return launch_msg_ktv<K, TH, 21>(a, stream);
     return launch_msg_ktv<K, TH, kMaxC>(a, stream);
 }

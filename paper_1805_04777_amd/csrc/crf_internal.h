@@ -310,8 +310,10 @@ constexpr size_t bwd_lds_bytes(int k, int C, int rows, bool dma, int D, int cn) 
 }
 constexpr size_t kBwdLdsLimit = 160 * 1024 - 256;
 // D: learnable smoothness feature planes staged besides (0 without).
+// 16 rows only for groups of more than 8 classes: with fewer, four 256-thread
+// work-groups per CU wait less at their barriers than two of 512.
 constexpr int bwd_tile_h(int k, int C, int D, bool dma, int cn) {
-    return k <= 7 && bwd_lds_bytes(k, C, 16, dma, D, cn) <= kBwdLdsLimit ? 16 : 8;
+    return k <= 7 && cn > 8 && bwd_lds_bytes(k, C, 16, dma, D, cn) <= kBwdLdsLimit ? 16 : 8;
 }
 inline size_t bwd_lds_need(int k, int C, int D, bool dma, int cn) {
     return bwd_lds_bytes(k, C, bwd_tile_h(k, C, D, dma, cn), dma, D, cn);
