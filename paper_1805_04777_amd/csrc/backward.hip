@@ -465,47 +465,103 @@ __device__ __forceinline__ float up_weight(int o, int cell, float inv_s, int n) 
     return (cell == a ? 1.f - f : 0.f) + (cell == i1 ? f : 0.f);
 }
 
-// One thread per pooled cell and plane.  Output o samples cell i0 =
-// floor((o + 0.5) / s - 0.5) and i0 + 1, so the full-resolution pixels that
-// sample cell (Y, X) lie in rows [s Y - s/2, s Y + 3s/2) and the same
-// columns (the clamps at the edges only move pixels inside that range onto
-// the edge cells).
+// Output o samples cell i0 = floor((o + 0.5) / s - 0.5) and i0 + 1, so the
+// full-resolution pixels that sample cell (Y, X) lie in rows [s Y - s/2,
+// s Y + 3s/2) and the same columns (the clamps at the edges only move
+// pixels inside that range onto the edge cells).  A work-group takes a
+// block of kUpTX x kUpTY cells of one plane: it stages the full-resolution
+// pixels under the block (zero outside the image) into LDS with coalesced
+// loads, then each thread sums the 2s x 2s window of its cell, row by row.
+constexpr int kUpTX = 64, kUpTY = 4;
+template <int S>
+constexpr int up_cols() { return S * kUpTX + S; }
+template <int S>
+constexpr int up_rows() { return S * kUpTY + S; }
+template <int S>
 __global__ __launch_bounds__(256) void upsample_t_kernel(const float* __restrict__ in,
                                                          float* __restrict__ out, int Hp,
-                                                         int Wp, int s, long long ncell) {
-    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= ncell) return;
-    const int X = (int)(i % Wp);
-    const long long r = i / Wp;
-    const int Y = (int)(r % Hp);
-    const long long plane = r / Hp;
-    const int H = Hp * s, W = Wp * s, h = s / 2;
-    const float inv_s = 1.f / (float)s;
+                                                         int Wp, int nbx, int nby) {
+    constexpr int h = S / 2, NX = 2 * S, COLS = up_cols<S>(), ROWS = up_rows<S>();
+    extern __shared__ float st[];                 // [ROWS][COLS]
+    const int H = Hp * S, W = Wp * S;
+    const long long blk = blockIdx.x;
+    const long long plane = blk / ((long long)nbx * nby);
+    const int rem = (int)(blk - plane * nbx * nby);
+    const int by = rem / nbx, bx = rem - by * nbx;
+    const int X0 = bx * kUpTX, Y0 = by * kUpTY;
+    const int gy0 = S * Y0 - h, gx0 = S * X0 - h;
     const float* src = in + plane * H * W;
-    const int ylo = s * Y - h > 0 ? s * Y - h : 0, yhi = s * Y + s + h < H ? s * Y + s + h : H;
-    const int xlo = s * X - h > 0 ? s * X - h : 0, xhi = s * X + s + h < W ? s * X + s + h : W;
-    float acc = 0.f;
-    for (int y = ylo; y < yhi; ++y) {
-        const float wy = up_weight(y, Y, inv_s, Hp);
-        float row = 0.f;
-        for (int x = xlo; x < xhi; ++x)
-            row = fmaf(up_weight(x, X, inv_s, Wp), src[(long long)y * W + x], row);
-        acc = fmaf(wy, row, acc);
+    // every load of the thread issued before the first LDS store
+    constexpr int NE = (ROWS * COLS + 255) / 256;
+    float v[NE];
+#pragma unroll
+    for (int k = 0; k < NE; ++k) {
+        const int e = threadIdx.x + 256 * k;
+        const int ly = e / COLS, lx = e - ly * COLS;
+        const int gy = gy0 + ly, gx = gx0 + lx;
+        const bool ok = e < ROWS * COLS && gy >= 0 && gy < H && gx >= 0 && gx < W;
+        v[k] = ok ? src[(long long)gy * W + gx] : 0.f;
     }
-    out[i] = acc;
+#pragma unroll
+    for (int k = 0; k < NE; ++k) {
+        const int e = threadIdx.x + 256 * k;
+        if (e < ROWS * COLS) st[e] = v[k];
+    }
+    __syncthreads();
+    const int tx = threadIdx.x % kUpTX, ty = threadIdx.x / kUpTX;
+    const int X = X0 + tx, Y = Y0 + ty;
+    if (X >= Wp || Y >= Hp) return;
+    const float inv_s = 1.f / (float)S;
+    float wx[NX];
+#pragma unroll
+    for (int j = 0; j < NX; ++j) {
+        const int x = S * X - h + j;
+        wx[j] = x >= 0 && x < W ? up_weight(x, X, inv_s, Wp) : 0.f;
+    }
+    float acc = 0.f;
+#pragma unroll
+    for (int jy = 0; jy < NX; ++jy) {
+        const int y = S * Y - h + jy;
+        if (y < 0 || y >= H) continue;
+        const float wy = up_weight(y, Y, inv_s, Hp);
+        const float* row = st + (S * ty + jy) * COLS + S * tx;
+        float t = 0.f;
+#pragma unroll
+        for (int j = 0; j < NX; ++j) t = fmaf(wx[j], row[j], t);
+        acc = fmaf(wy, t, acc);
+    }
+    out[(plane * Hp + Y) * Wp + X] = acc;
 }
 
+// blockIdx.y strides over the B * C * H full-resolution rows, kPoolTRows at
+// a time; V consecutive pixels per thread (one pooled cell when V <= S), a
+// vector store when V = 4.
+constexpr int kPoolTRows = 8;
+template <int S, int V>
 __global__ __launch_bounds__(256) void pool_t_kernel(const float* __restrict__ in,
                                                      float* __restrict__ out, int Hp, int Wp,
-                                                     int s, float inv, long long npix) {
-    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= npix) return;
-    const int W = Wp * s, H = Hp * s;
-    const int x = (int)(i % W);
-    const long long r = i / W;
-    const int y = (int)(r % H);
-    const long long plane = r / H;
-    out[i] = in[(plane * Hp + y / s) * Wp + x / s] * inv;
+                                                     long long nrows) {
+    const int W = Wp * S, H = Hp * S;
+    const int x = (blockIdx.x * blockDim.x + threadIdx.x) * V;
+    if (x >= W) return;
+    constexpr float inv = 1.f / (float)(S * S);
+    for (long long r0 = (long long)blockIdx.y * kPoolTRows; r0 < nrows;
+         r0 += (long long)gridDim.y * kPoolTRows) {
+#pragma unroll
+        for (int k = 0; k < kPoolTRows; ++k) {
+            const long long r = r0 + k;
+            if (r >= nrows) break;
+            const long long plane = r / H;
+            const int y = (int)(r - plane * H);
+            const float* src = in + (plane * Hp + y / S) * Wp;
+            if constexpr (V == 4) {
+                const float val = src[x / S] * inv;
+                *reinterpret_cast<float4*>(out + r * W + x) = make_float4(val, val, val, val);
+            } else {
+                out[r * W + x] = src[x / S] * inv;
+            }
+        }
+    }
 }
 
 // ---------------------------------------------------------------- reduce
@@ -588,26 +644,61 @@ hipError_t launch_bwd_point(const float* q, const float* dq, const float* mu, fl
     return hipGetLastError();
 }
 
+template <int S>
+hipError_t launch_up_t(const float* in, float* out, int B, int C, int Hp, int Wp,
+                       hipStream_t stream) {
+    const int nbx = (Wp + kUpTX - 1) / kUpTX, nby = (Hp + kUpTY - 1) / kUpTY;
+    const long long blocks = (long long)B * C * nbx * nby;
+    if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+    const size_t lds = sizeof(float) * up_rows<S>() * up_cols<S>();
+    auto fn = upsample_t_kernel<S>;
+    if (lds > 64 * 1024) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                 (int)lds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(256), lds, stream, in, out, Hp, Wp, nbx,
+                       nby);
+    return hipGetLastError();
+}
+
 hipError_t launch_upsample_t(const float* in, float* out, int B, int C, int Hp, int Wp, int s,
                              hipStream_t stream) {
-    const long long n = (long long)B * C * Hp * Wp;
-    if (n == 0) return hipSuccess;
-    const long long blocks = (n + 255) / 256;
-    if (blocks > 0x7fffffffLL || (s != 2 && s != 4 && s != 8)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(upsample_t_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, in, out,
-                       Hp, Wp, s, n);
+    if ((long long)B * C * Hp * Wp == 0) return hipSuccess;
+    switch (s) {
+        case 2: return launch_up_t<2>(in, out, B, C, Hp, Wp, stream);
+        case 4: return launch_up_t<4>(in, out, B, C, Hp, Wp, stream);
+        case 8: return launch_up_t<8>(in, out, B, C, Hp, Wp, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template <int S, int V>
+hipError_t launch_pool_t_sv(const float* in, float* out, int Hp, int Wp, long long nrows,
+                            hipStream_t stream) {
+    const long long W = (long long)Wp * S;
+    const long long ry = (nrows + kPoolTRows - 1) / kPoolTRows;
+    const dim3 grid((unsigned)((W / V + 255) / 256), (unsigned)(ry < 65535 ? ry : 65535));
+    hipLaunchKernelGGL((pool_t_kernel<S, V>), grid, dim3(256), 0, stream, in, out, Hp, Wp, nrows);
     return hipGetLastError();
 }
 
 hipError_t launch_pool_t(const float* in, float* out, int B, int C, int Hp, int Wp, int s,
                          hipStream_t stream) {
-    const long long n = (long long)B * C * Hp * Wp * s * s;
-    if (n == 0) return hipSuccess;
-    const long long blocks = (n + 255) / 256;
-    if (blocks > 0x7fffffffLL || s < 1) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(pool_t_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, in, out, Hp,
-                       Wp, s, 1.f / (float)(s * s), n);
-    return hipGetLastError();
+    const long long nrows = (long long)B * C * Hp * s;
+    const long long W = (long long)Wp * s;
+    if (nrows == 0 || W == 0) return hipSuccess;
+    if (W > 0x7fffffffLL) return hipErrorInvalidValue;
+    const bool vec = reinterpret_cast<uintptr_t>(out) % 16 == 0;   // W % 4 == 0 for s >= 4
+    switch (s) {
+        case 2: return launch_pool_t_sv<2, 1>(in, out, Hp, Wp, nrows, stream);
+        case 4: return vec ? launch_pool_t_sv<4, 4>(in, out, Hp, Wp, nrows, stream)
+                           : launch_pool_t_sv<4, 1>(in, out, Hp, Wp, nrows, stream);
+        case 8: return vec ? launch_pool_t_sv<8, 4>(in, out, Hp, Wp, nrows, stream)
+                           : launch_pool_t_sv<8, 1>(in, out, Hp, Wp, nrows, stream);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_bwd_reduce(const float* gpart, int groups, int C, float* out_compat,
