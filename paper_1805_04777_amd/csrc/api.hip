@@ -873,11 +873,12 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
             (st = ensure(ctx, ctx->b_df, sizeof(float) * (size_t)npix * D)) != CONVCRF_OK)
             return st;
         if (s > 1) {
-            // pooled image, pooled Q^t, pooled message, and the pooled dL/dM,
-            // -dL/dZ and dL/dQ
+            // pooled image, pooled Q^t for every round, pooled message, and
+            // the pooled dL/dM, -dL/dZ and dL/dQ
             const size_t pb = sizeof(float) * (size_t)B * Hg * Wg;
             if ((st = ensure(ctx, ctx->pool_f, pb * 3)) != CONVCRF_OK) return st;
-            if ((st = ensure(ctx, ctx->pool_q, pb * C)) != CONVCRF_OK) return st;
+            if ((st = ensure(ctx, ctx->pool_q, pb * C * std::max(iters, 1))) != CONVCRF_OK)
+                return st;
             if ((st = ensure(ctx, ctx->pool_m, pb * C)) != CONVCRF_OK) return st;
             if ((st = ensure(ctx, ctx->b_pd, pb * C * 3)) != CONVCRF_OK) return st;
         }
@@ -890,7 +891,10 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
                 [&] { return launch_softmax(unary, qs(0), B, C, H * W, stream); });
     if (st != CONVCRF_OK) return st;
     float* pf = static_cast<float*>(ctx->pool_f.p);
-    float* pq = static_cast<float*>(ctx->pool_q.p);
+    // pooled Q^t of round t (blur)
+    auto pqs = [&](int t) {
+        return static_cast<float*>(ctx->pool_q.p) + (size_t)t * B * C * Hg * Wg;
+    };
     float* pm = static_cast<float*>(ctx->pool_m.p);
     if (run && s > 1) {
         // the pooled message of Sec. 4.2 (as convcrf_meanfield), with every
@@ -909,7 +913,6 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         a.H = Hg;
         a.W = Wg;
         a.feat = pf;
-        a.src = pq;
         a.dst = pm;
         a.mode = kModeMessage;
         a.tiles_x = (Wg + kPmsgTW - 1) / kPmsgTW;
@@ -918,15 +921,19 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         st = launch(ctx, kPool, stream, "blur_pool",
                     [&] { return launch_pool(image, pf, B, 3, H, W, s, 0, stream); });
         if (st != CONVCRF_OK) return st;
+        // Q^0 pooled here; every update also writes its pooled Q^{t+1}, kept
+        // for the reverse rounds
+        st = launch(ctx, kPool, stream, "blur_pool",
+                    [&] { return launch_pool(qs(0), pqs(0), B, C, H, W, s, 0, stream); });
+        if (st != CONVCRF_OK) return st;
         for (int t = 0; t < iters; ++t) {
-            st = launch(ctx, kPool, stream, "blur_pool",
-                        [&] { return launch_pool(qs(t), pq, B, C, H, W, s, 0, stream); });
-            if (st != CONVCRF_OK) return st;
+            a.src = pqs(t);
             st = launch(ctx, kBlurMsg, stream, "blur_message",
                         [&] { return launch_pmsg(a, k, nchunks, lds, stream); });
             if (st != CONVCRF_OK) return st;
             st = launch(ctx, kBlurUpd, stream, "blur_update", [&] {
-                return launch_blur_update(pm, unary, mu_dev, qs(t + 1), nullptr, B, C, H, W, s,
+                return launch_blur_update(pm, unary, mu_dev, qs(t + 1),
+                                          t + 1 < iters ? pqs(t + 1) : nullptr, B, C, H, W, s,
                                           stream);
             });
             if (st != CONVCRF_OK) return st;
@@ -1039,10 +1046,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
                 });
                 if (st != CONVCRF_OK) return st;
             }
-            st = launch(ctx, kPool, stream, "blur_pool",
-                        [&] { return launch_pool(qs(t), pq, B, C, H, W, s, 0, stream); });
-            if (st != CONVCRF_OK) return st;
-            ba.q = pq;
+            ba.q = pqs(t);
             ba.dm = pdm;
             ba.dq_out = pdq;
             st = launch(ctx, kBwdMsg, stream, "bwd_message",

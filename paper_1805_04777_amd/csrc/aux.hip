@@ -6,7 +6,8 @@
 //   pool_kernel          s x s average pooling (blur path, Sec. 4.2)
 //   blur_update_kernel   bilinear upsampling of the pooled message, then
 //                        compatibility, unary and softmax (Alg. 1), writing
-//                        Q or its s x s average for the next pooled message
+//                        Q, its s x s average for the next pooled message,
+//                        or both
 #include "crf_internal.h"
 
 namespace convcrf {
@@ -165,7 +166,8 @@ __device__ __forceinline__ void src_coord(int o, int s, int n, int& i0, int& i1,
 
 // One blur iteration after the pooled message: bilinear upsampling of the
 // message, compatibility, unary and softmax (Alg. 1) per pixel, then the
-// full Q (last iteration) or its s x s average for the next pooled message.
+// full Q, its s x s average for the next pooled message, or both (each
+// output is written when its pointer is set).
 // Same layout as pool_kernel.
 template <int CM, bool EXACT>
 __global__ __launch_bounds__(512) void blur_update_kernel(
@@ -230,7 +232,7 @@ __global__ __launch_bounds__(512) void blur_update_kernel(
             for (int c = 0; c < CM; ++c)
                 if (EXACT || c < C) q[c * HW] = z[c];
         }
-        return;                                   // uniform over the grid
+        if (q_pooled == nullptr) return;          // uniform over the grid
     }
     if (cell_average<CM, EXACT>(z, C, s, red) && active) {
         float* dp = q_pooled + (size_t)b * C * HWp + (size_t)Y * Wp + x / s;
@@ -429,7 +431,7 @@ __global__ __launch_bounds__(512) void blur_update4_kernel(
                     *reinterpret_cast<float4*>(qd + (size_t)c * HW) =
                         make_float4(z[0][c], z[1][c], z[2][c], z[3][c]);
         }
-        return;                                   // uniform over the grid
+        if (q_pooled == nullptr) return;          // uniform over the grid
     }
     if (cell_average4<CM, EXACT>(psum, C, s, red) && active) {
         float* dp = q_pooled + (size_t)b * C * HWp + (size_t)Y * Wp + x / s;

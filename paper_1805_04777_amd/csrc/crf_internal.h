@@ -199,9 +199,9 @@ hipError_t launch_build_kernel(const float* image, float* out, int B, int H,
 hipError_t launch_pool(const float* src, float* dst, int B, int nch, int H,
                        int W, int s, int softmax_first, hipStream_t stream);
 // Bilinear upsampling of the pooled message M [B][C][H/s][W/s], then
-// compatibility, unary and softmax at full resolution.  If q_full is set
-// it receives Q [B][C][H][W]; otherwise q_pooled receives the s x s average
-// of Q, [B][C][H/s][W/s].
+// compatibility, unary and softmax at full resolution.  q_full (if set)
+// receives Q [B][C][H][W] and q_pooled (if set) the s x s average of Q,
+// [B][C][H/s][W/s].
 hipError_t launch_blur_update(const float* m_pooled, const float* unary,
                               const float* mu, float* q_full, float* q_pooled,
                               int B, int C, int H, int W, int s,
