@@ -854,18 +854,19 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         if ((st = upload_mu(ctx, p.compat, C, stream)) != CONVCRF_OK) return st;
         mu_dev = static_cast<const float*>(ctx->mu.p);
     }
+    const bool potts_dz = mu_dev == nullptr && C > 1;
     // workspace: Q^0 .. Q^T in 256-byte aligned slices
     const size_t slice = (qbytes + 255) / 256 * 256;
     if ((st = ensure(ctx, ctx->b_q, slice * (iters + 1))) != CONVCRF_OK) return st;
     if (run) {
         if ((st = ensure(ctx, ctx->b_dq, slice * 2)) != CONVCRF_OK) return st;
         if ((st = ensure(ctx, ctx->b_dm, slice)) != CONVCRF_OK) return st;
-        if (grad_compat) {
+        if (grad_compat && !potts_dz)
             if ((st = ensure(ctx, ctx->b_dp, slice)) != CONVCRF_OK) return st;
+        if (grad_compat)
             if ((st = ensure(ctx, ctx->b_gpart, sizeof(float) * (size_t)ntiles * C * C)) !=
                 CONVCRF_OK)
                 return st;
-        }
         if ((st = ensure(ctx, ctx->b_kpart, sizeof(float) * (size_t)ntiles * groups * 5)) !=
             CONVCRF_OK)
             return st;
@@ -1007,7 +1008,10 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         ba.neg_gamma = (float)(-kLog2eD / (2.0 * tg * tg));
         ba.inv_gamma2 = (float)(1.0 / (tg * tg));
     }
-    float* dp = grad_compat ? static_cast<float*>(ctx->b_dp.p) : nullptr;
+    // Potts (C > 1): the compatibility derivative takes -dL/dZ from dL/dM,
+    // so dL/dZ is neither written nor upsampled
+    float* dp = grad_compat && !potts_dz ? static_cast<float*>(ctx->b_dp.p) : nullptr;
+    ba.dm_sum_scale = grad_compat && potts_dz ? (float)(1.0 / (1.0 - (double)C)) : 0.f;
     ba.gpart = grad_compat ? static_cast<float*>(ctx->b_gpart.p) : nullptr;
     float* dm = static_cast<float*>(ctx->b_dm.p);
     // blur: the pooled dL/dM, -dL/dZ and dL/dQ
@@ -1015,7 +1019,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     float* pdm = static_cast<float*>(ctx->b_pd.p);
     float* pdp = pdm ? pdm + pn : nullptr;
     float* pdq = pdm ? pdm + 2 * pn : nullptr;
-    ba.dp = s > 1 ? (grad_compat ? pdp : nullptr) : dp;
+    ba.dp = s > 1 ? (dp ? pdp : nullptr) : dp;
     const float* dq = grad_q;
     for (int t = iters - 1; t >= 0; --t) {
         const int acc = t != iters - 1;
@@ -1040,7 +1044,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
                 return launch_upsample_t(dm, pdm, B, C, Hg, Wg, s, stream);
             });
             if (st != CONVCRF_OK) return st;
-            if (grad_compat) {
+            if (dp) {
                 st = launch(ctx, kBwdBlurT, stream, "bwd_blur_transpose", [&] {
                     return launch_upsample_t(dp, pdp, B, C, Hg, Wg, s, stream);
                 });

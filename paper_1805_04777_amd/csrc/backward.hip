@@ -143,8 +143,21 @@ __device__ __forceinline__ void tile_gram(float* lds, const BwdArgs& a, int tile
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
         const int col = PX * threadIdx.x + i;
-        for (int c = 0; c < CP; ++c)
-            gp[c * SP + col] = in[i] && c < C ? a.dp[pix[i] + c * hw] : 0.f;
+        if (a.dm_sum_scale != 0.f) {
+            // Potts: dM(l) = dZ(l) - sum_l' dZ(l'), so sum_l dM(l) = (1 - C)
+            // sum_l' dZ(l') and dZ(l) = dM(l) + sum_l' dM(l') / (1 - C)
+            float sum = 0.f;
+            for (int c = 0; c < CP; ++c) {
+                const float v = in[i] && c < C ? a.dm[pix[i] + c * hw] : 0.f;
+                gp[c * SP + col] = v;
+                sum += v;
+            }
+            const float sh = sum * a.dm_sum_scale;
+            for (int c = 0; c < C; ++c) gp[c * SP + col] = -(gp[c * SP + col] + sh);
+        } else {
+            for (int c = 0; c < CP; ++c)
+                gp[c * SP + col] = in[i] && c < C ? a.dp[pix[i] + c * hw] : 0.f;
+        }
 #pragma unroll
         for (int c = 0; c < CM; ++c)
             if (c < CQ) gm[c * SP + col] = in[i] && c < CN ? mv[i][c] : 0.f;

@@ -259,7 +259,10 @@ struct BwdArgs {
     const float* q;      // Q^t [B][C][H][W]
     const float* dm;     // dL/dM^t [B][C][H][W]
     const float* feat;   // image [B][3][H][W]
-    const float* dp;     // -dL/dZ^t [B][C][H][W] (read when gpart is set)
+    const float* dp;     // -dL/dZ^t [B][C][H][W] (read when gpart is set and
+                         // dm_sum_scale is 0)
+    float dm_sum_scale;  // Potts, C > 1: 1 / (1 - C), and -dL/dZ^t is taken from
+                         // dL/dM^t as -(dM(l) + dm_sum_scale sum_l' dM(l')); else 0
     const float* sfeat;  // learnable smoothness features [B][D][H][W] or null
     float* dfeat;        // dL/dF [B][D][H][W] (with sfeat)
     int D;
