@@ -59,7 +59,7 @@ struct convcrf_ctx {
     DevBuf q_ws, q_ws2, kmat, pool_q, pool_m, pool_f, mu, sync;
     // reverse mode: Q^0..Q^T, dL/dQ ping-pong, dL/dM, -dL/dZ, per-tile sums,
     // dL/dF when not requested, the pooled derivatives (blur)
-    DevBuf b_q, b_dq, b_dm, b_dp, b_gpart, b_kpart, b_df, b_pd;
+    DevBuf b_q, b_dq, b_dm, b_dp, b_gpart, b_kpart, b_df, b_pd, b_dfp;
     std::vector<float> mu_last;   // host copy of the uploaded compatibility
     float* mu_pinned = nullptr;   // pinned staging for the upload
     size_t mu_pinned_cap = 0;
@@ -495,7 +495,7 @@ void convcrf_destroy(convcrf_ctx* ctx) {
     for (DevBuf* b : {&ctx->q_ws, &ctx->q_ws2, &ctx->kmat, &ctx->pool_q, &ctx->pool_m,
                       &ctx->pool_f, &ctx->mu, &ctx->sync, &ctx->b_q, &ctx->b_dq, &ctx->b_dm,
                       &ctx->b_dp, &ctx->b_gpart, &ctx->b_kpart, &ctx->b_df,
-                      &ctx->b_pd})
+                      &ctx->b_pd, &ctx->b_dfp})
         if (b->p) (void)hipFree(b->p);
     if (ctx->mu_pinned) (void)hipHostFree(ctx->mu_pinned);
     if (ctx->mu_copied) (void)hipEventDestroy(ctx->mu_copied);
@@ -791,9 +791,10 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     // scalar staging saves)
     // class groups of the adjoint message (grid dim y): every work-group
     // stages and sums its group's classes only, which leaves room for more
-    // work-groups per CU and, on small grids, more work-groups; learnable
-    // features keep one group (dL/dF sums over all classes in one place)
-    int groups = D > 0 ? 1 : std::max(1, std::min(kBwdClassGroups, C / 4));
+    // work-groups per CU and, on small grids, more work-groups.  dL/dF is
+    // linear in the per-class sums, so with learnable features each group
+    // stores its part and a sum adds the parts in group order
+    int groups = std::max(1, std::min(kBwdClassGroups, C / 4));
     if (groups > 1) {
         // small grids (the pooled grid of the blur variant): more groups,
         // down to three classes each, until the launch has kBwdMinGroups
@@ -872,6 +873,10 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
             return st;
         if (p.features && !grad_features &&
             (st = ensure(ctx, ctx->b_df, sizeof(float) * (size_t)npix * D)) != CONVCRF_OK)
+            return st;
+        if (p.features && groups > 1 &&
+            (st = ensure(ctx, ctx->b_dfp, sizeof(float) * (size_t)npix * D * groups)) !=
+                CONVCRF_OK)
             return st;
         if (s > 1) {
             // pooled image, pooled Q^t for every round, pooled message, and
@@ -1004,6 +1009,11 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     if (p.features) {
         ba.sfeat = p.features;
         ba.dfeat = grad_features ? grad_features : static_cast<float*>(ctx->b_df.p);
+        if (groups > 1) {
+            // each class group stores its part of dL/dF; a sum adds them
+            ba.dfeat = static_cast<float*>(ctx->b_dfp.p);
+            ba.dfeat_gstride = npix * D;
+        }
         ba.D = D;
         ba.neg_gamma = (float)(-kLog2eD / (2.0 * tg * tg));
         ba.inv_gamma2 = (float)(1.0 / (tg * tg));
@@ -1036,6 +1046,13 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
             st = launch(ctx, kBwdMsg, stream, "bwd_message",
                         [&] { return launch_bwd_message(ba, k, stream); });
             if (st != CONVCRF_OK) return st;
+            if (ba.dfeat_gstride > 0) {
+                float* df = grad_features ? grad_features : static_cast<float*>(ctx->b_df.p);
+                st = launch(ctx, kBwdReduce, stream, "bwd_reduce", [&] {
+                    return launch_group_sum(ba.dfeat, groups, npix * D, df, acc, stream);
+                });
+                if (st != CONVCRF_OK) return st;
+            }
         } else {
             // M = upsample(pooled message of avgpool(Q^t)): the transpose of
             // the upsampling (for dL/dM and, for dL/dmu, -dL/dZ), the pooled

@@ -337,9 +337,17 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
             if (c < CN) a.dq_out[pix + (c0 + c) * hw] = dqa[c];
         if constexpr (FT) {
             float* df = a.dfeat + (long long)b * D * hw + (long long)py * a.W + px;
+            if (a.dfeat_gstride > 0) {
+                // this class group's part; the parts are added after the launch
+                df += blockIdx.y * a.dfeat_gstride;
 #pragma unroll
-            for (int c = 0; c < kMaxFeat; ++c)
-                if (c < D) df[c * hw] = a.accumulate ? df[c * hw] + dfa[c] : dfa[c];
+                for (int c = 0; c < kMaxFeat; ++c)
+                    if (c < D) df[c * hw] = dfa[c];
+            } else {
+#pragma unroll
+                for (int c = 0; c < kMaxFeat; ++c)
+                    if (c < D) df[c * hw] = a.accumulate ? df[c * hw] + dfa[c] : dfa[c];
+            }
         }
     }
     if constexpr (WM) {
@@ -578,6 +586,17 @@ __global__ __launch_bounds__(256) void pool_t_kernel(const float* __restrict__ i
 }
 
 // ---------------------------------------------------------------- reduce
+__global__ __launch_bounds__(256) void group_sum_kernel(const float* __restrict__ part,
+                                                        int groups, long long n,
+                                                        float* __restrict__ out,
+                                                        int accumulate) {
+    const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    float s = accumulate ? out[i] : 0.f;
+    for (int g = 0; g < groups; ++g) s += part[(long long)g * n + i];
+    out[i] = s;
+}
+
 struct ReduceArgs {
     const float* gpart;
     const float* kpart;
@@ -620,7 +639,8 @@ hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream) {
     const int D = a.sfeat ? a.D : 0;
     if (a.sfeat && (a.D < 1 || a.D > kMaxFeat || !a.dfeat)) return hipErrorInvalidValue;
     if (a.cgsize < 1 || a.cgroups < 1 || (long long)a.cgroups * a.cgsize < a.C ||
-        (a.cgroups - 1) * a.cgsize >= a.C || (a.sfeat && a.cgroups != 1) || a.cgroups > 65535)
+        (a.cgroups - 1) * a.cgsize >= a.C ||
+        (a.sfeat && a.cgroups != 1 && a.dfeat_gstride <= 0) || a.cgroups > 65535)
         return hipErrorInvalidValue;
     if (bwd_lds_need(k, a.C, D, a.dma != 0, a.cgsize) > kBwdLdsLimit) return hipErrorInvalidValue;
     // buffer offsets of the DMA staging stay under 2 GB
@@ -712,6 +732,16 @@ hipError_t launch_pool_t(const float* in, float* out, int B, int C, int Hp, int 
                            : launch_pool_t_sv<8, 1>(in, out, Hp, Wp, nrows, stream);
         default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_group_sum(const float* part, int groups, long long n, float* out,
+                            int accumulate, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const long long blocks = (n + 255) / 256;
+    if (blocks > 0x7fffffffLL || groups < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(group_sum_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, part,
+                       groups, n, out, accumulate);
+    return hipGetLastError();
 }
 
 hipError_t launch_bwd_reduce(const float* gpart, int groups, int C, float* out_compat,

@@ -265,6 +265,8 @@ struct BwdArgs {
                          // dL/dM^t as -(dM(l) + dm_sum_scale sum_l' dM(l')); else 0
     const float* sfeat;  // learnable smoothness features [B][D][H][W] or null
     float* dfeat;        // dL/dF [B][D][H][W] (with sfeat)
+    long long dfeat_gstride;  // > 0: class group g stores its part of dL/dF
+                              // (not accumulated) at dfeat + g * dfeat_gstride
     int D;
     float neg_gamma;     // -log2(e) / (2 theta_gamma^2) (with sfeat)
     float inv_gamma2;    // 1 / theta_gamma^2 (with sfeat)
@@ -357,6 +359,10 @@ hipError_t launch_pool_t(const float* in, float* out, int B, int C, int Hp, int 
 // out_compat is set);
 // out_kernel[j] = scale[j] * sum_t kpart[t][j] (5 entries, when set).
 // Sums in double, in a fixed order.
+// out[i] = (accumulate ? out[i] : 0) + sum over g < groups of part[g n + i],
+// in order of g (the class groups' parts of dL/dF).
+hipError_t launch_group_sum(const float* part, int groups, long long n, float* out,
+                            int accumulate, hipStream_t stream);
 hipError_t launch_bwd_reduce(const float* gpart, int groups, int C, float* out_compat,
                              const float* kpart, int ntiles, const float scale[5],
                              float* out_kernel, hipStream_t stream);
