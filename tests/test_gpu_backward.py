@@ -261,3 +261,27 @@ def test_backward_errors(torch_cuda, crf):
     with pytest.raises(cc.ConvCRFError) as e:
         crf.meanfield_backward(Ut, t(I), params(4), 2, Gt)            # even window
     assert e.value.status == cc.E_INVALID_ARG
+
+
+@pytest.mark.parametrize("blur,k,C,T", [(1, 7, 21, 3), (4, 5, 21, 2), (1, 5, 2, 2)])
+def test_potts_compat_derivative_matches_the_explicit_matrix(torch_cuda, crf, oracle_mod,
+                                                             blur, k, C, T):
+    """With Potts compatibility (no matrix given, C > 1) the compatibility
+    derivative takes -dL/dZ from dL/dM; with the same matrix 1 - I given
+    explicitly it reads the stored -dL/dZ.  Both meet the bar against the
+    oracle and agree with each other.  C = 2 is the smallest case of the
+    derivation (sum dM = -sum dZ).  Weights 3 and 1 keep |M| small: with a
+    matrix given, the forward forms U - mu M, which rounds at the scale of M
+    (the Potts form softmax(U + M) does not cancel)."""
+    U, I, G = make_case(41 + blur + C, 1, C, 32, 48)
+    potts = (1.0 - np.eye(C)).astype(np.float32)
+    w = dict(w_app=3.0, w_smooth=1.0)
+    a = run_gpu(torch_cuda, crf, U, I, G, params(k, False, None, blur=blur, **w), T)
+    b = run_gpu(torch_cuda, crf, U, I, G, params(k, False, potts, blur=blur, **w), T)
+    op = OracleParams(filter_size=k, blur=blur, **w)
+    ref = oracle_mod.meanfield_backward(U, I, op, T, G, compat=None)
+    check(a, ref, f"Potts, blur {blur}", T)
+    check(b, ref, f"explicit 1 - I, blur {blur}", T)
+    for x, y, name in zip(a, b, ("dU", "dmu", "dk")):
+        e = np.abs(x - y).max() / max(np.abs(y).max(), 1e-30)
+        assert e <= TOL_REL, f"{name}: Potts and explicit 1 - I differ by {e:.2e}"
