@@ -12,7 +12,10 @@
 //                      and, when the compatibility derivative is wanted,
 //                      recomputes the forward message M^t and sums
 //                      dP_p(l) M_p(l') over the tile's pixels.
-// bwd_reduce_kernel folds the per-tile partial sums.
+// bwd_reduce_kernel folds the per-tile partial sums; group_sum_kernel adds
+// the class groups' parts of dL/dF (learnable features).  upsample_t_kernel
+// and pool_t_kernel are the transposes of the blur variant's upsampling and
+// pooling.
 //
 // Built once per window side k with -DCRF_BWD_K=k (the adjoint-message
 // kernels of that k) and once without (the pointwise and reduction kernels
