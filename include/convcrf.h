@@ -98,7 +98,9 @@ typedef struct {
     float w_app;            /* w(1) of Eq. 4, >= 0 */
     float theta_alpha;      /* position scale of the appearance kernel, > 0 */
     float theta_beta;       /* colour scale of the appearance kernel, > 0 */
-    float w_smooth;         /* w(2) of Eq. 4, >= 0 */
+    float w_smooth;         /* w(2) of Eq. 4, any finite value (the
+                               smoothness term is added to the weight;
+                               Eq. 4 leaves its sign to training) */
     float theta_gamma;      /* position scale of the smoothness kernel, > 0 */
     const float *compat;    /* HOST pointer to C*C floats, row-major
                                mu[l][l'] (the 1x1-convolution compatibility
@@ -146,8 +148,8 @@ void convcrf_destroy(convcrf_ctx *ctx);
  * [B][C][H][W] buffer for the ping-pong of Q, plus pooled buffers for blur
  * or the kernel matrix for the materialised variant); it grows on demand,
  * is reused by later calls, and is freed by convcrf_destroy.  q_out must not
- * overlap unary or image.  Returns CONVCRF_E_HIP on a launch failure (the
- * message names the HIP error). */
+ * overlap unary, image or params->features.  Returns CONVCRF_E_HIP on a
+ * launch failure (the message names the HIP error). */
 convcrf_status convcrf_meanfield(convcrf_ctx *ctx, const float *unary,
                                  const float *image, int B, int C, int H,
                                  int W, const convcrf_params *params,
@@ -208,9 +210,10 @@ convcrf_status convcrf_profile_enable(convcrf_ctx *ctx, int enable);
  * "materialised_iter", "blur_pool", "blur_message", "blur_update", and for
  * convcrf_meanfield_backward "bwd_point", "bwd_message", "bwd_reduce",
  * "bwd_blur_transpose" besides the forward's; "feature_iter" with learnable
- * features) since profiling was enabled.  "fused_resident" is one launch running all
- * iterations of a call (CONVCRF_VARIANT_RESIDENT); "fused_iter" one
- * iteration.
+ * features, "fused_first") since profiling was enabled.  "fused_resident" is one
+ * launch running all iterations of a call (CONVCRF_VARIANT_RESIDENT);
+ * "fused_first" the first iteration of a fused call (it reads the unary and
+ * applies the initial softmax on the fly) and "fused_iter" each later one.
  * Synchronises on the recorded events.  An unknown or unused name gives
  * 0 ms and 0 launches. */
 convcrf_status convcrf_profile_read(convcrf_ctx *ctx, const char *name,
@@ -224,6 +227,24 @@ const char *convcrf_last_error(const convcrf_ctx *ctx);
 
 /* Static name of a status code. */
 const char *convcrf_status_string(convcrf_status s);
+
+/* The status name followed by the last detailed message on ctx (or of a
+ * context-free call if ctx is NULL), for `status` as returned by a call on
+ * ctx; "CONVCRF_OK" for CONVCRF_OK.  Never NULL; valid until the next call
+ * of this function on the same host thread. */
+const char *convcrf_strerror(const convcrf_ctx *ctx, convcrf_status status);
+
+/* Wait until the work enqueued on `stream` (a hipStream_t as void*, NULL =
+ * the null stream) has finished, then report whether a
+ * CONVCRF_VARIANT_RESIDENT call on ctx since the last check passed the bound
+ * of one of its neighbour waits (CONVCRF_E_HIP; its q_out is then not valid
+ * and the flag is cleared).  The resident launch synchronises neighbouring
+ * tiles with bounded waits so that it can never hang; a wait that gives up
+ * sets a device flag instead.  Every call on ctx also checks, without
+ * blocking, a copy of that flag taken after the last resident launch, and
+ * returns CONVCRF_E_HIP before enqueuing anything when it is set.  Other
+ * failures: CONVCRF_E_HIP with the HIP error. */
+convcrf_status convcrf_synchronize(convcrf_ctx *ctx, void *stream);
 
 #ifdef __cplusplus
 }

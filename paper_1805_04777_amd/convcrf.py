@@ -26,13 +26,14 @@ VARIANT_FUSED = 0
 VARIANT_MATERIALISED = 1
 VARIANT_RESIDENT = 2
 
-KERNEL_NAMES = ("fused_iter", "fused_resident", "sync_reset", "softmax", "build_kernel",
+KERNEL_NAMES = ("fused_first", "fused_iter", "fused_resident", "sync_reset", "softmax", "build_kernel",
                 "materialised_iter", "blur_pool", "blur_message", "blur_update",
                 "bwd_point", "bwd_message", "bwd_reduce", "feature_iter", "bwd_blur_transpose")
 
 EXPORTED = ("convcrf_default_params", "convcrf_validate", "convcrf_init", "convcrf_destroy",
             "convcrf_meanfield", "convcrf_meanfield_backward", "convcrf_profile_enable",
-            "convcrf_profile_read", "convcrf_last_error", "convcrf_status_string")
+            "convcrf_profile_read", "convcrf_last_error", "convcrf_status_string",
+            "convcrf_strerror", "convcrf_synchronize")
 
 # order of grad_kernel in convcrf_meanfield_backward
 KERNEL_PARAM_NAMES = ("w_app", "theta_alpha", "theta_beta", "w_smooth", "theta_gamma")
@@ -79,20 +80,42 @@ class Params:
     features: object = None
     _keep: list = field(default_factory=list, repr=False, compare=False)
 
-    def c(self) -> CParams:
+    def c(self, shape=None, device=None) -> CParams:
+        """The C struct.  With ``shape`` = (B, C, H, W) of the unary (and its
+        ``device``), ``compat`` must be C x C and ``features`` a float32
+        tensor [B, D, H, W] on that device: the library reads C*C floats from
+        the compatibility pointer and B*D*H*W from the features pointer
+        without being able to check either."""
         p = CParams(int(self.filter_size), int(self.blur), int(self.include_center),
                     int(self.variant), float(self.w_app), float(self.theta_alpha),
                     float(self.theta_beta), float(self.w_smooth), float(self.theta_gamma), None,
                     None, 0)
         if self.features is not None:
+            import torch
             f = self.features
-            if f.dtype.itemsize != 4 or not f.is_cuda or not f.is_contiguous() or f.dim() != 4:
+            if (not isinstance(f, torch.Tensor) or f.dtype != torch.float32 or not f.is_cuda
+                    or not f.is_contiguous() or f.dim() != 4):
                 raise ConvCRFError(E_INVALID_ARG, "features must be a contiguous 4-D float32 GPU tensor")
+            if shape is not None:
+                B, _, H, W = shape
+                if f.shape[0] != B or f.shape[2] != H or f.shape[3] != W:
+                    raise ConvCRFError(E_INVALID_ARG, f"features must be [B, D, H, W] = "
+                                       f"[{B}, D, {H}, {W}], got {list(f.shape)}")
+            if device is not None and f.device != device:
+                raise ConvCRFError(E_INVALID_ARG, f"features are on {f.device}, the unary on {device}")
             p.features = f.data_ptr()
             p.feature_dim = int(f.shape[1])
         if self.compat is not None:
             import numpy as np
-            mu = np.ascontiguousarray(np.asarray(self.compat, dtype=np.float32).ravel())
+            mu = np.asarray(self.compat)
+            if mu.dtype.kind not in "fiu":
+                raise ConvCRFError(E_INVALID_ARG, "compat must be a real C x C array")
+            mu = np.ascontiguousarray(mu, dtype=np.float32)
+            if shape is not None and mu.shape != (shape[1], shape[1]):
+                raise ConvCRFError(E_INVALID_ARG, f"compat must be C x C = {shape[1]} x {shape[1]}, "
+                                   f"got shape {mu.shape}")
+            if mu.ndim != 2 or mu.shape[0] != mu.shape[1]:
+                raise ConvCRFError(E_INVALID_ARG, f"compat must be a square matrix, got shape {mu.shape}")
             self._keep[:] = [mu]
             p.compat = mu.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
         return p
@@ -140,6 +163,10 @@ def load_library(path: str = LIB_PATH):
     lib.convcrf_last_error.argtypes = [vp]
     lib.convcrf_status_string.restype = ctypes.c_char_p
     lib.convcrf_status_string.argtypes = [ctypes.c_int]
+    lib.convcrf_strerror.restype = ctypes.c_char_p
+    lib.convcrf_strerror.argtypes = [vp, ctypes.c_int]
+    lib.convcrf_synchronize.restype = st
+    lib.convcrf_synchronize.argtypes = [vp, vp]
     _lib = lib
     return lib
 
@@ -147,7 +174,7 @@ def load_library(path: str = LIB_PATH):
 def _check(status: int, ctx=None):
     if status != OK:
         lib = load_library()
-        raise ConvCRFError(status, lib.convcrf_last_error(ctx).decode())
+        raise ConvCRFError(status, lib.convcrf_strerror(ctx, status).decode())
 
 
 def default_params() -> Params:
@@ -159,7 +186,11 @@ def default_params() -> Params:
 
 def validate(B: int, C: int, H: int, W: int, params: Params, iters: int) -> int:
     """Status that meanfield would return for these sizes (no device needed)."""
-    return int(load_library().convcrf_validate(B, C, H, W, ctypes.byref(params.c()), iters))
+    try:
+        cp = params.c((B, C, H, W))
+    except ConvCRFError as e:
+        return e.status
+    return int(load_library().convcrf_validate(B, C, H, W, ctypes.byref(cp), iters))
 
 
 class ConvCRF:
@@ -209,7 +240,7 @@ class ConvCRF:
         if stream is None:
             stream = torch.cuda.current_stream(unary.device)
         sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
-        cp = params.c()
+        cp = params.c((B, C, H, W), unary.device)
         _check(self._lib.convcrf_meanfield(self._h, unary.data_ptr(), image.data_ptr(), B, C, H, W,
                                            ctypes.byref(cp), int(iters), out.data_ptr(), sp),
                self._h)
@@ -241,7 +272,7 @@ class ConvCRF:
         if stream is None:
             stream = torch.cuda.current_stream(unary.device)
         sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
-        cp = params.c()
+        cp = params.c((B, C, H, W), unary.device)
         _check(self._lib.convcrf_meanfield_backward(
             self._h, unary.data_ptr(), image.data_ptr(), B, C, H, W, ctypes.byref(cp),
             int(iters), grad_q.data_ptr(), out.data_ptr(),
@@ -253,6 +284,16 @@ class ConvCRF:
     def last_error(self) -> str:
         """The library's last message for this context."""
         return self._lib.convcrf_last_error(self._h).decode()
+
+    def synchronize(self, stream=None):
+        """Wait for ``stream`` (default: torch's current stream on this
+        context's device) and raise if a resident call's bounded neighbour
+        wait gave up since the last check (its output is then invalid)."""
+        import torch
+        if stream is None:
+            stream = torch.cuda.current_stream(self.device)
+        sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+        _check(self._lib.convcrf_synchronize(self._h, sp), self._h)
 
     def profile_enable(self, on: bool = True):
         _check(self._lib.convcrf_profile_enable(self._h, int(bool(on))), self._h)

@@ -31,10 +31,10 @@ const char* const kKernelNames[] = {"fused_iter",   "softmax",      "build_kerne
                                     "materialised_iter", "blur_pool", "blur_message",
                                     "blur_update",  "fused_resident", "sync_reset",
                                     "bwd_point", "bwd_message", "bwd_reduce", "feature_iter",
-                                    "bwd_blur_transpose"};
+                                    "bwd_blur_transpose", "fused_first"};
 enum KernelId {
     kFused = 0, kSoftmax, kBuild, kMatIter, kPool, kBlurMsg, kBlurUpd, kResident, kSyncReset,
-    kBwdPoint, kBwdMsg, kBwdReduce, kFeatIter, kBwdBlurT, kNumKernels
+    kBwdPoint, kBwdMsg, kBwdReduce, kFeatIter, kBwdBlurT, kFusedFirst, kNumKernels
 };
 
 struct DevBuf {
@@ -64,6 +64,13 @@ struct convcrf_ctx {
     float* mu_pinned = nullptr;   // pinned staging for the upload
     size_t mu_pinned_cap = 0;
     hipEvent_t mu_copied = nullptr;
+    // the resident variant's bounded neighbour waits: sync.p[0] is a sticky
+    // device flag that a wait past its bound sets; a copy of it is read back
+    // without blocking (flag_event) and reported by the next call or by
+    // convcrf_synchronize
+    unsigned int* flag_host = nullptr;
+    hipEvent_t flag_event = nullptr;
+    bool flag_pending = false;
     bool profiling = false;
     std::vector<ProfRec> prof;
     std::vector<hipEvent_t> free_events;
@@ -99,6 +106,8 @@ convcrf_status validate(convcrf_ctx* ctx, int B, int C, int H, int W, const conv
     if (p->variant != CONVCRF_VARIANT_FUSED && p->variant != CONVCRF_VARIANT_MATERIALISED &&
         p->variant != CONVCRF_VARIANT_RESIDENT)
         return fail(ctx, CONVCRF_E_INVALID_ARG, "unknown variant");
+    // w_smooth may take either sign (the smoothness term is added to the
+    // weight); w_app is folded into an exponent as log2(w_app)
     if (!std::isfinite(p->w_app) || !std::isfinite(p->w_smooth))
         return fail(ctx, CONVCRF_E_INVALID_ARG, "kernel weights must be finite");
     if (p->w_app < 0.f)
@@ -416,6 +425,84 @@ convcrf_status upload_mu(convcrf_ctx* ctx, const float* mu, int C, hipStream_t s
     return CONVCRF_OK;
 }
 
+// Report a wait overrun of an earlier resident call: the sticky flag
+// sync[0] is copied to pinned host memory after each resident launch (when
+// no copy is outstanding).  Non-blocking: a copy not yet landed is left for
+// a later check.
+convcrf_status poll_overrun(convcrf_ctx* ctx) {
+    if (!ctx->flag_pending) return CONVCRF_OK;
+    const hipError_t e = hipEventQuery(ctx->flag_event);
+    if (e == hipErrorNotReady) {
+        (void)hipGetLastError();
+        return CONVCRF_OK;
+    }
+    ctx->flag_pending = false;
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipEventQuery(resident flag)");
+    if (*ctx->flag_host == 0) return CONVCRF_OK;
+    *ctx->flag_host = 0;
+    // clear the device flag (ordered after the copy that saw it)
+    const hipError_t z = launch_zero_u32(static_cast<unsigned int*>(ctx->sync.p), 1, nullptr);
+    if (z != hipSuccess) return hip_fail(ctx, z, "clearing the resident flag");
+    return fail(ctx, CONVCRF_E_HIP,
+                "an earlier CONVCRF_VARIANT_RESIDENT call passed the bound of a neighbour wait; "
+                "the Q it wrote is not valid");
+}
+
+// Blocking form: wait for the device and read the flag itself.
+convcrf_status check_overrun(convcrf_ctx* ctx) {
+    if (!ctx->sync.p) return CONVCRF_OK;
+    ctx->flag_pending = false;
+    unsigned int v = 0;
+    hipError_t e = hipMemcpy(&v, ctx->sync.p, sizeof(v), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(ctx, e, "reading the resident flag");
+    if (v == 0) return CONVCRF_OK;
+    e = launch_zero_u32(static_cast<unsigned int*>(ctx->sync.p), 1, nullptr);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(ctx, e, "clearing the resident flag");
+    return fail(ctx, CONVCRF_E_HIP,
+                "a CONVCRF_VARIANT_RESIDENT call passed the bound of a neighbour wait; the Q it "
+                "wrote is not valid");
+}
+
+// The flag words of a resident launch over `ntiles` tiles: sync[0] (sticky,
+// checked before the buffer is replaced) and one counter per tile.
+convcrf_status ensure_sync(convcrf_ctx* ctx, size_t ntiles, hipStream_t stream) {
+    const size_t bytes = (1 + ntiles) * sizeof(unsigned int);
+    if (ctx->sync.bytes >= bytes) return CONVCRF_OK;
+    convcrf_status st = check_overrun(ctx);
+    if (st != CONVCRF_OK) return st;
+    if ((st = ensure(ctx, ctx->sync, bytes)) != CONVCRF_OK) return st;
+    const hipError_t e = launch_zero_u32(static_cast<unsigned int*>(ctx->sync.p), 1, stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "clearing the resident flag");
+    return CONVCRF_OK;
+}
+
+// After a resident launch: copy the sticky flag back (one copy outstanding
+// at a time; a flag set meanwhile stays set for the next copy).
+convcrf_status queue_overrun_check(convcrf_ctx* ctx, hipStream_t stream) {
+    if (ctx->flag_pending) return CONVCRF_OK;
+    hipError_t e;
+    if (!ctx->flag_host) {
+        e = hipHostMalloc(reinterpret_cast<void**>(&ctx->flag_host), sizeof(unsigned int), 0);
+        if (e != hipSuccess) {
+            ctx->flag_host = nullptr;
+            return hip_fail(ctx, e, "hipHostMalloc(resident flag)");
+        }
+        *ctx->flag_host = 0;
+    }
+    if (!ctx->flag_event) {
+        e = hipEventCreateWithFlags(&ctx->flag_event, hipEventDisableTiming);
+        if (e != hipSuccess) return hip_fail(ctx, e, "hipEventCreate(resident flag)");
+    }
+    e = hipMemcpyAsync(ctx->flag_host, ctx->sync.p, sizeof(unsigned int), hipMemcpyDeviceToHost,
+                       stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipMemcpyAsync(resident flag)");
+    e = hipEventRecord(ctx->flag_event, stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipEventRecord(resident flag)");
+    ctx->flag_pending = true;
+    return CONVCRF_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -434,6 +521,22 @@ const char* convcrf_status_string(convcrf_status s) {
 
 const char* convcrf_last_error(const convcrf_ctx* ctx) {
     return ctx ? ctx->err.c_str() : g_last_error.c_str();
+}
+
+const char* convcrf_strerror(const convcrf_ctx* ctx, convcrf_status status) {
+    thread_local std::string text;
+    if (status == CONVCRF_OK) return convcrf_status_string(status);
+    text = std::string(convcrf_status_string(status)) + ": " + convcrf_last_error(ctx);
+    return text.c_str();
+}
+
+convcrf_status convcrf_synchronize(convcrf_ctx* ctx, void* stream) {
+    if (!ctx) return fail(nullptr, CONVCRF_E_INVALID_ARG, "ctx is NULL");
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(ctx, e, "hipStreamSynchronize");
+    return check_overrun(ctx);
 }
 
 convcrf_status convcrf_default_params(convcrf_params* p) {
@@ -499,6 +602,8 @@ void convcrf_destroy(convcrf_ctx* ctx) {
         if (b->p) (void)hipFree(b->p);
     if (ctx->mu_pinned) (void)hipHostFree(ctx->mu_pinned);
     if (ctx->mu_copied) (void)hipEventDestroy(ctx->mu_copied);
+    if (ctx->flag_host) (void)hipHostFree(ctx->flag_host);
+    if (ctx->flag_event) (void)hipEventDestroy(ctx->flag_event);
     for (auto& r : ctx->prof) {
         (void)hipEventDestroy(r.start);
         (void)hipEventDestroy(r.stop);
@@ -559,11 +664,15 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     const size_t ibytes = sizeof(float) * (size_t)npix * 3;
     if (overlaps(q_out, qbytes, unary, qbytes) || overlaps(q_out, qbytes, image, ibytes))
         return fail(ctx, CONVCRF_E_INVALID_ARG, "q_out overlaps unary or image");
+    if (params->features &&
+        overlaps(q_out, qbytes, params->features, sizeof(float) * (size_t)npix * params->feature_dim))
+        return fail(ctx, CONVCRF_E_INVALID_ARG, "q_out overlaps the features");
 
     const convcrf_params p = *params;
     hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    if ((st = poll_overrun(ctx)) != CONVCRF_OK) return st;
 
     if (iters == 0)
         return launch(ctx, kSoftmax, stream, "softmax",
@@ -645,9 +754,7 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
         if (p.variant == CONVCRF_VARIANT_RESIDENT && !mu_dev && iters >= 2 && ctx->coop &&
             streamed && as.ntiles <= 4 * ctx->num_cus) {
             if ((st = ensure(ctx, ctx->q_ws2, qbytes)) != CONVCRF_OK) return st;
-            if ((st = ensure(ctx, ctx->sync, (1 + (size_t)as.ntiles) * sizeof(unsigned int))) !=
-                CONVCRF_OK)
-                return st;
+            if ((st = ensure_sync(ctx, (size_t)as.ntiles, stream)) != CONVCRF_OK) return st;
             IterArgs r = as;
             r.src = unary;
             r.dst = q_out;
@@ -659,11 +766,13 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
             const hipError_t fits = launch_rstream(r, k, lds_s, ctx->num_cus, stream, true);
             if (fits == hipSuccess) {
                 st = launch(ctx, kSyncReset, stream, "sync_reset",
-                            [&] { return launch_zero_u32(r.sync, 1 + as.ntiles, stream); });
+                            [&] { return launch_zero_u32(r.sync + 1, as.ntiles, stream); });
                 if (st != CONVCRF_OK) return st;
-                return launch(ctx, kResident, stream, "fused_resident", [&] {
+                st = launch(ctx, kResident, stream, "fused_resident", [&] {
                     return launch_rstream(r, k, lds_s, ctx->num_cus, stream, false);
                 });
+                if (st != CONVCRF_OK) return st;
+                return queue_overrun_check(ctx, stream);
             }
             (void)hipGetLastError();  // refused: one launch per iteration below
             ctx->err = std::string("resident launch refused (") + hipGetErrorString(fits) +
@@ -672,9 +781,7 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
                    tile.pix == 2 && tile.width == 32 && k <= 7 &&
                    a.ntiles <= 4 * ctx->num_cus) {
             if ((st = ensure(ctx, ctx->q_ws2, qbytes)) != CONVCRF_OK) return st;
-            if ((st = ensure(ctx, ctx->sync, (1 + (size_t)a.ntiles) * sizeof(unsigned int))) !=
-                CONVCRF_OK)
-                return st;
+            if ((st = ensure_sync(ctx, (size_t)a.ntiles, stream)) != CONVCRF_OK) return st;
             IterArgs r = a;
             r.src = unary;
             r.dst = q_out;
@@ -686,11 +793,13 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
             const hipError_t fits = launch_resident(r, k, tile, lds, ctx->num_cus, stream, true);
             if (fits == hipSuccess) {
                 st = launch(ctx, kSyncReset, stream, "sync_reset",
-                            [&] { return launch_zero_u32(r.sync, 1 + a.ntiles, stream); });
+                            [&] { return launch_zero_u32(r.sync + 1, a.ntiles, stream); });
                 if (st != CONVCRF_OK) return st;
-                return launch(ctx, kResident, stream, "fused_resident", [&] {
+                st = launch(ctx, kResident, stream, "fused_resident", [&] {
                     return launch_resident(r, k, tile, lds, ctx->num_cus, stream, false);
                 });
+                if (st != CONVCRF_OK) return st;
+                return queue_overrun_check(ctx, stream);
             }
             (void)hipGetLastError();  // refused: one launch per iteration below
             ctx->err = std::string("resident launch refused (") + hipGetErrorString(fits) +
@@ -705,8 +814,8 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
             a.src = as.src = ar.src = cur;
             a.dst = as.dst = ar.dst = dst;
             a.first = as.first = ar.first = t == 0;
-            st = launch(ctx, mat ? kMatIter : kFused, stream, mat ? "materialised_iter" : "fused_iter",
-                        [&] {
+            st = launch(ctx, mat ? kMatIter : (t == 0 ? kFusedFirst : kFused), stream,
+                        mat ? "materialised_iter" : "fused_iter", [&] {
                             if (ring && t > 0) return launch_ring(ar, k, stream);
                             return streamed ? launch_stream(as, k, lds_s, stream)
                                             : launch_iter(a, k, mat, tile, lds, stream);
@@ -821,9 +930,22 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
                      overlaps(grad_unary, qbytes, image, ibytes) ||
                      overlaps(grad_unary, qbytes, grad_q, qbytes)))
         return fail(ctx, CONVCRF_E_INVALID_ARG, "grad_unary overlaps unary, image or grad_q");
+    if (npix > 0 && D > 0) {
+        const size_t fbytes = sizeof(float) * (size_t)npix * D;
+        if (overlaps(grad_unary, qbytes, p.features, fbytes))
+            return fail(ctx, CONVCRF_E_INVALID_ARG, "grad_unary overlaps the features");
+        if (grad_features && (overlaps(grad_features, fbytes, p.features, fbytes) ||
+                              overlaps(grad_features, fbytes, unary, qbytes) ||
+                              overlaps(grad_features, fbytes, image, ibytes) ||
+                              overlaps(grad_features, fbytes, grad_q, qbytes) ||
+                              overlaps(grad_features, fbytes, grad_unary, qbytes)))
+            return fail(ctx, CONVCRF_E_INVALID_ARG,
+                        "grad_features overlaps the features or another tensor");
+    }
     hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
     hipError_t e = hipSetDevice(ctx->device);
     if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+    if ((st = poll_overrun(ctx)) != CONVCRF_OK) return st;
 
     const double ta = p.theta_alpha, tb = p.theta_beta, tg = p.theta_gamma;
     // the kernel sums grid offsets n = dx^2 + dy^2; the squared distance in
@@ -975,7 +1097,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
             a.src = as.src = ar.src = t == 0 ? unary : qs(t);
             a.dst = as.dst = ar.dst = qs(t + 1);
             a.first = as.first = ar.first = t == 0;
-            st = launch(ctx, kFused, stream, "fused_iter", [&] {
+            st = launch(ctx, t == 0 ? kFusedFirst : kFused, stream, "fused_iter", [&] {
                 if (ring && t > 0) return launch_ring(ar, k, stream);
                 return streamed ? launch_stream(as, k, lds_s, stream)
                                 : launch_iter(a, k, false, tile, lds, stream);

@@ -8,6 +8,8 @@ import ctypes
 import os
 import re
 
+import numpy as np
+
 import pytest
 
 from paper_1805_04777_amd import convcrf as cc
@@ -133,3 +135,89 @@ def test_init_without_a_gpu_reports_no_device(lib):
     h = ctypes.c_void_p(1234)
     assert lib.convcrf_init(ctypes.byref(h), 0) == cc.E_NO_DEVICE
     assert h.value is None
+
+
+def test_strerror_names_the_status_and_the_message(lib):
+    assert lib.convcrf_strerror(None, cc.OK).decode() == "CONVCRF_OK"
+    assert lib.convcrf_validate(1, 21, 8, 8, None, 1) == cc.E_INVALID_ARG
+    text = lib.convcrf_strerror(None, cc.E_INVALID_ARG).decode()
+    assert text.startswith("CONVCRF_E_INVALID_ARG: ") and "params" in text
+
+
+def test_synchronize_rejects_a_null_context(lib):
+    assert lib.convcrf_synchronize(None, None) == cc.E_INVALID_ARG
+
+
+def test_negative_smoothness_weight_is_accepted(lib):
+    # Eq. 4 fixes no sign for the weights; only w_app is folded into log2
+    assert cc.validate(1, 21, 64, 64, P(w_smooth=-2.0), 5) == cc.OK
+    assert cc.validate(1, 21, 64, 64, P(w_app=-2.0), 5) == cc.E_UNSUPPORTED
+
+
+@pytest.mark.parametrize("compat", [
+    np.zeros((3, 3), np.float32),        # the wrong class count
+    np.zeros(21 * 21, np.float32),       # flat, not C x C
+    np.zeros((21, 20), np.float32),
+    [["a"] * 21] * 21,                   # not numbers
+])
+def test_compat_must_be_c_by_c(lib, compat):
+    assert cc.validate(1, 21, 8, 8, P(compat=compat), 1) == cc.E_INVALID_ARG
+    with pytest.raises(cc.ConvCRFError) as e:
+        P(compat=compat).c((1, 21, 8, 8))
+    assert e.value.status == cc.E_INVALID_ARG
+
+
+def test_compat_of_the_right_shape_is_passed_through(lib):
+    mu = np.arange(21 * 21, dtype=np.float64).reshape(21, 21)
+    p = P(compat=mu)
+    c = p.c((1, 21, 8, 8))
+    got = np.ctypeslib.as_array(c.compat, shape=(21 * 21,))
+    assert np.array_equal(got, mu.ravel().astype(np.float32))
+    assert cc.validate(1, 21, 8, 8, p, 1) == cc.OK
+
+
+class _FakeFeatures:
+    """Stands in for a CUDA tensor on a CPU-only host (the binding reads only
+    these attributes before handing the pointer to the library)."""
+
+    def __init__(self, shape, dtype=None, device="cuda:0"):
+        import torch
+        self.shape = tuple(shape)
+        self.dtype = torch.float32 if dtype is None else dtype
+        self.device = torch.device(device)
+        self.is_cuda = True
+
+    def is_contiguous(self):
+        return True
+
+    def dim(self):
+        return len(self.shape)
+
+    def data_ptr(self):
+        return 4096
+
+
+@pytest.mark.parametrize("shape,dtype,why", [
+    ((1, 2, 8, 8), "int32", "dtype"),
+    ((2, 2, 8, 8), None, "batch"),
+    ((1, 2, 8, 9), None, "width"),
+    ((1, 2, 7, 8), None, "height"),
+    ((1, 2, 8), None, "rank"),
+])
+def test_features_must_match_the_unary(lib, monkeypatch, shape, dtype, why):
+    import torch
+    monkeypatch.setattr(torch, "Tensor", _FakeFeatures)
+    f = _FakeFeatures(shape, getattr(torch, dtype) if dtype else None)
+    with pytest.raises(cc.ConvCRFError) as e:
+        P(features=f).c((1, 21, 8, 8), torch.device("cuda:0"))
+    assert e.value.status == cc.E_INVALID_ARG, why
+
+
+def test_features_must_be_on_the_unary_device(lib, monkeypatch):
+    import torch
+    monkeypatch.setattr(torch, "Tensor", _FakeFeatures)
+    f = _FakeFeatures((1, 2, 8, 8), device="cuda:1")
+    with pytest.raises(cc.ConvCRFError):
+        P(features=f).c((1, 21, 8, 8), torch.device("cuda:0"))
+    c = P(features=_FakeFeatures((1, 2, 8, 8))).c((1, 21, 8, 8), torch.device("cuda:0"))
+    assert c.feature_dim == 2 and c.features == 4096
