@@ -982,9 +982,10 @@ hipError_t launch_stream(const IterArgs& a, size_t lds, hipStream_t stream) {
 // The later iterations on half-height tiles (kStreamTW x kRingRows, 256
 // threads, two pixels each) so that two work-groups share a CU and one's
 // waits overlap the other's arithmetic.  As stream_kernel, but the class
-// chunks cycle through kRingSlots LDS slots (chunk k in slot k mod 3; chunk
-// k + 2 is issued into the slot of chunk k - 1 once every wave is past it)
-// and each thread's unary comes straight into registers, issued first.
+// chunks cycle through kRingSlots LDS slots (chunk k in slot k mod
+// kRingSlots; kRingSlots - 1 chunks are in flight, chunk k + kRingSlots - 1
+// being issued into the slot of chunk k - 1 once every wave is past it) and
+// each thread's unary comes straight into registers, issued mid-way.
 // FD > 0: learnable smoothness features (the "+T" variant of Sec. 4.2): the
 // FD feature planes are staged beside the colours and the smoothness Gaussian
 // of each weight is taken on the feature distance.
@@ -1031,20 +1032,6 @@ void ring_kernel(const IterArgs a) {
     const int col0 = tx * P;
     const int y = y0 + ty, xb = x0 + col0;
     const bool pix_ok = y < H && xb < W;        // W even: both pixels or neither
-
-    // ---- the unary of this thread's pixels, into registers (issued before
-    // the LDS loads, so every wait below also covers it)
-    float u[P][CM];
-    {
-        const float* up = a.unary + (size_t)b * CM * HW + (size_t)(pix_ok ? y : 0) * W +
-                          (pix_ok ? xb : 0);
-#pragma unroll
-        for (int c = 0; c < CM; ++c) {
-            const float2 t = *reinterpret_cast<const float2*>(up + c * HW);
-            u[0][c] = t.x;
-            u[1][c] = t.y;
-        }
-    }
 
     // ---- colours, then the first two chunks of Q_t
     unsigned voff[NJ];
@@ -1093,12 +1080,20 @@ void ring_kernel(const IterArgs a) {
                 lds_dma(rq, voff[s], (int)(c * HW * 4),
                         lds_addr(dst[s] >= 0 ? slot + (c - c_lo) * PLANE + dst[s] : dummy));
     };
-    issue_chunk(0);
-    if (NCH > 1) issue_chunk(1);
+    // AHEAD chunks in flight: the first AHEAD now, chunk k + AHEAD at chunk k
+    constexpr int AHEAD = kRingSlots - 1;
+    static_for([&](auto kc) {
+        if constexpr (decltype(kc)::value < NCH) issue_chunk(decltype(kc)::value);
+    }, std::make_integer_sequence<int, AHEAD>{});
+    // loads of chunks [k0, k0 + n) per wave
+    auto chunk_loads = [](int k0, int n) {
+        int t = 0;
+        for (int j = k0; j < k0 + n; ++j) t += stream_chunk_loads(j, CM, CH, NJ);
+        return t;
+    };
 
     // ---- colours landed: the window weights of both pixels, all rows
-    __builtin_amdgcn_s_waitcnt(vm_wait(stream_chunk_loads(0, CM, CH, NJ) +
-                                       stream_chunk_loads(1, CM, CH, NJ)));
+    __builtin_amdgcn_s_waitcnt(vm_wait(chunk_loads(0, AHEAD)));
     __syncthreads();
     float w[K][P][K];
     {
@@ -1159,15 +1154,33 @@ void ring_kernel(const IterArgs a) {
     for (int i = 0; i < P; ++i)
 #pragma unroll
         for (int c = 0; c < CM; ++c) acc[i][c] = 0.f;
+    // the unary of this thread's pixels goes straight into registers; it is
+    // needed only by the epilogue, so its loads are issued at chunk UK (after
+    // that chunk's own issue), which keeps them out of the launch's opening
+    // burst of colour and class-plane loads
+    constexpr int UK = NCH > 3 ? 1 : 0;
+    float u[P][CM];
     static_for([&](auto kc) {
         constexpr int k = decltype(kc)::value;
         constexpr int c_lo = k * CH;
         constexpr int c_hi = (k + 1) * CH < CM ? (k + 1) * CH : CM;
-        // chunk k landed (chunk k + 1 may still be in flight); every wave is
-        // past chunk k - 1, whose slot chunk k + 2 takes
-        __builtin_amdgcn_s_waitcnt(vm_wait(stream_chunk_loads(k + 1, CM, CH, NJ)));
+        // chunk k landed (the chunks after it that are in flight, and the
+        // unary when it went out after chunk k, may not have); every wave is
+        // past chunk k - 1, whose slot chunk k + AHEAD takes
+        __builtin_amdgcn_s_waitcnt(vm_wait(chunk_loads(k + 1, AHEAD - 1) +
+                                           (UK < k && k <= UK + AHEAD ? CM : 0)));
         __syncthreads();
-        if constexpr (k + 2 < NCH) issue_chunk(k + 2);
+        if constexpr (k + AHEAD < NCH) issue_chunk(k + AHEAD);
+        if constexpr (k == UK) {
+            const float* up = a.unary + (size_t)b * CM * HW + (size_t)(pix_ok ? y : 0) * W +
+                              (pix_ok ? xb : 0);
+#pragma unroll
+            for (int c = 0; c < CM; ++c) {
+                const float2 t = *reinterpret_cast<const float2*>(up + c * HW);
+                u[0][c] = t.x;
+                u[1][c] = t.y;
+            }
+        }
         // the slot seen as planes c_lo .. c_hi - 1 of Q_t
         const float* const qk = Qs + (k % kRingSlots) * CH * PLANE - c_lo * PLANE;
         message_chunk<K, P, LS, PLANE, CM, c_lo, c_hi>(qk, ty, col0, w, acc);
@@ -1180,6 +1193,7 @@ void ring_kernel(const IterArgs a) {
                                      acc[i][c]);
         }
     }, std::make_integer_sequence<int, NCH>{});
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));     // the unary
     if (!pix_ok) return;
 
     // ---- compatibility, unary, softmax (Alg. 1), store Q_{t+1}
