@@ -3,11 +3,11 @@
 Every comparison is element by element on the same seeded inputs: the max
 absolute difference of any probability must be <= 1e-4, the argmax label
 must agree on >= 99.99% of pixels, and every pixel's probabilities must sum
-to 1 within 1e-5.  The full-size workloads that the benchmark times are
-compared in full (512 x 512) or on crops: after T iterations with window
-radius r, a pixel's Q depends only on inputs within T*r pixels, so the oracle
-run on a crop padded by T*r (clipped at the image border) gives exactly the
-full-image values on the crop.
+to 1 within 1e-5.  The full-size workloads are compared in full, every pixel
+of every image (the batched 8 x 21 x 512 x 512 and the street 1 x 19 x 1024 x
+2048 workloads included).  Every call is followed by the context's
+synchronize, which raises if a resident launch's bounded neighbour wait ever
+gave up.
 """
 
 import dataclasses
@@ -63,7 +63,7 @@ def run_gpu(torch, crf, U, I, p, T):
     Ut = torch.from_numpy(np.ascontiguousarray(U, dtype=np.float32)).cuda()
     It = torch.from_numpy(np.ascontiguousarray(I, dtype=np.float32)).cuda()
     Q = crf.meanfield(Ut, It, p, T)
-    torch.cuda.synchronize()
+    crf.synchronize()
     return Q.cpu().numpy().astype(np.float64)
 
 
@@ -128,46 +128,30 @@ def test_blur_workload_full(torch_cuda, crf, oracle_mod):
           "blur workload")
 
 
-def crop_windows(H, W, size, rng, n_random):
-    wins = [(0, 0), (0, W - size), (H - size, 0), (H - size, W - size),
-            ((H - size) // 2, 0), (0, (W - size) // 2)]
-    for _ in range(n_random):
-        wins.append((int(rng.integers(0, H - size + 1)), int(rng.integers(0, W - size + 1))))
-    return wins
-
-
-def check_crops(torch, crf, oracle_mod, U, I, p, T, size, n_random, seed):
-    Qg = run_gpu(torch, crf, U, I, p, T)
-    B, C, H, W = U.shape
-    m = T * ((p.filter_size - 1) // 2)
-    rng = np.random.default_rng(seed)
-    worst = 0.0
-    for b in range(B):
-        for (y0, x0) in crop_windows(H, W, size, rng, n_random):
-            ya, yb = max(0, y0 - m), min(H, y0 + size + m)
-            xa, xb = max(0, x0 - m), min(W, x0 + size + m)
-            Qo = run_oracle(oracle_mod, U[b:b + 1, :, ya:yb, xa:xb], I[b:b + 1, :, ya:yb, xa:xb], p, T)
-            Qo = Qo[:, :, y0 - ya:y0 - ya + size, x0 - xa:x0 - xa + size]
-            worst = max(worst, check(Qg[b:b + 1, :, y0:y0 + size, x0:x0 + size], Qo,
-                                     f"image {b} crop ({y0},{x0})"))
-    # the rest of the output is still a distribution everywhere
-    assert np.abs(Qg.sum(1) - 1.0).max() <= ROWSUM
-    return worst
-
-
-def test_batched_workload_crops(torch_cuda, crf, oracle_mod):
-    # 8 x 21 x 512 x 512, k = 7: corners, edges and random interior crops of
-    # every image; batch items are independent
+def test_batched_workload_full(torch_cuda, crf, oracle_mod):
+    # 8 x 21 x 512 x 512, k = 7, 5 iterations: every pixel of every image
+    # (2.1 M pixels x 21 classes) against the oracle
     wl = synth.WORKLOADS["batched"]
-    U, I, _ = synth.make_inputs(wl)
-    check_crops(torch_cuda, crf, oracle_mod, U, I, lib_params(wl), wl.iters, 48, 2, seed=41)
+    U, I, L = synth.make_inputs(wl)
+    p = lib_params(wl)
+    Qg = run_gpu(torch_cuda, crf, U, I, p, wl.iters)
+    Qo = run_oracle(oracle_mod, U, I, p, wl.iters)
+    err = check(Qg, Qo, "batched workload")
+    print(f"batched 8x21x512x512: max |dQ| {err:.3e}")
+    assert (Qg.argmax(1) == L).mean() > (U.argmax(1) == L).mean() + 0.2
 
 
-def test_street_workload_crops(torch_cuda, crf, oracle_mod):
-    # 1 x 19 x 1024 x 2048, k = 7
+def test_street_workload_full(torch_cuda, crf, oracle_mod):
+    # 1 x 19 x 1024 x 2048, k = 7, 5 iterations: every pixel against the
+    # oracle (the C = 19 ring and first-iteration kernels at full size)
     wl = synth.WORKLOADS["street"]
-    U, I, _ = synth.make_inputs(wl)
-    check_crops(torch_cuda, crf, oracle_mod, U, I, lib_params(wl), wl.iters, 64, 10, seed=51)
+    U, I, L = synth.make_inputs(wl)
+    p = lib_params(wl)
+    Qg = run_gpu(torch_cuda, crf, U, I, p, wl.iters)
+    Qo = run_oracle(oracle_mod, U, I, p, wl.iters)
+    err = check(Qg, Qo, "street workload")
+    print(f"street 1x19x1024x2048: max |dQ| {err:.3e}")
+    assert (Qg.argmax(1) == L).mean() > (U.argmax(1) == L).mean() + 0.2
 
 
 # -------------------------------------------------- shapes, windows, classes
@@ -237,6 +221,17 @@ def test_general_compatibility(torch_cuda, crf, oracle_mod, C):
     mu2 = synth.random_compat(C, seed=C + 99)
     p = lib_params(filter_size=5, compat=mu2, w_app=2.0, w_smooth=0.7)
     check(run_gpu(torch_cuda, crf, U, I, p, 3), run_oracle(oracle_mod, U, I, p, 3), "compat 2")
+
+
+@pytest.mark.parametrize("w_smooth", [-2.0, -0.5])
+def test_negative_smoothness_weight(torch_cuda, crf, oracle_mod, w_smooth):
+    # Eq. 4 leaves the sign of the weights to training; a negative
+    # smoothness weight lowers every tap's weight by a per-offset constant
+    U, I = rand_case(640, 1, 21, 48, 68)
+    for variant, blur in ((0, 1), (1, 1), (0, 2)):
+        p = lib_params(filter_size=5, w_smooth=w_smooth, w_app=3.0, variant=variant, blur=blur)
+        check(run_gpu(torch_cuda, crf, U, I, p, 3), run_oracle(oracle_mod, U, I, p, 3),
+              f"w_smooth={w_smooth} variant={variant} blur={blur}")
 
 
 def test_include_center(torch_cuda, crf, oracle_mod):
@@ -312,10 +307,9 @@ def test_resident_bitwise_equals_fused(torch_cuda, crf, B, C, H, W, k, T):
     # exchanged border rings instead of HBM).  A stale or misplaced halo
     # value would change bits, so the two must agree exactly, here on i.i.d.
     # random logits and colours, up to 256 tiles with ragged edges.  (At
-    # 512 x 512 and C = 21 such inputs differ from the oracle by up to 1.7e-4
-    # at 8 of 262144 pixels: fp32 rounding of messages near 90, amplified
-    # over five iterations at pixels on a decision boundary; the
-    # workload-shaped scenes stay within 1e-4, see test_pascal_workload_full.)
+    # 512 x 512 and C = 21 such inputs cannot be computed to 1e-4 in float32
+    # at a few pixels on decision boundaries, whatever the summation order;
+    # test_conditioning.py pins that and applies the bar everywhere else.)
     U, I = rand_case(1000 + C + H, B, C, H, W)
     p = lib_params(filter_size=k)
     np.testing.assert_array_equal(run_gpu(torch_cuda, crf, U, I, p, T),
@@ -421,6 +415,15 @@ def test_errors_leave_output_untouched(torch_cuda, crf):
         crf.meanfield(U, I, lib_params(), -1, out=out)
     with pytest.raises(cc.ConvCRFError):  # output aliasing the input
         crf.meanfield(U, I, lib_params(), 2, out=U)
+    # output overlapping the learnable features (the first two planes of out)
+    feats = out[:, :2]
+    assert feats.is_contiguous()
+    with pytest.raises(cc.ConvCRFError) as e:
+        crf.meanfield(U, I, lib_params(features=feats), 2, out=out)
+    assert e.value.status == cc.E_INVALID_ARG and "features" in str(e.value)
+    # a compatibility matrix of the wrong size is refused before the call
+    with pytest.raises(cc.ConvCRFError):
+        crf.meanfield(U, I, lib_params(compat=np.eye(3, dtype=np.float32)), 2, out=out)
     torch.cuda.synchronize()
     assert bool((out == 7.0).all())
 
@@ -438,8 +441,12 @@ def test_profiling_counts_launches(torch_cuda, crf):
     mu = synth.random_compat(21, seed=1)
     crf.meanfield(U, I, lib_params(variant=2, compat=mu), 3)   # general mu: runs as fused
     torch.cuda.synchronize()
+    # the first iteration of each fused call is "fused_first", later ones
+    # "fused_iter" (the general-mu resident request runs as fused: 1 + 2)
     ms, n = crf.profile_read("fused_iter")
-    assert n == 18 and ms > 0
+    assert n == 14 and ms > 0
+    ms, n = crf.profile_read("fused_first")
+    assert n == 4 and ms > 0
     ms, n = crf.profile_read("fused_resident")
     assert n == 1 and ms > 0
     assert crf.profile_read("sync_reset")[1] == 1
