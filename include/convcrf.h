@@ -155,6 +155,31 @@ convcrf_status convcrf_meanfield(convcrf_ctx *ctx, const float *unary,
                                  int W, const convcrf_params *params,
                                  int iters, float *q_out, void *stream);
 
+/* convcrf_meanfield for callers that cannot allocate: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, kernels and results as convcrf_meanfield (bit for bit), but it
+ * calls no hipMalloc, hipFree, hipHostMalloc or other allocating routine:
+ * the Q ping-pong buffer, the pooled buffers of the blur path and the
+ * compatibility matrix live in a scratch array of 64 MiB per device, part of
+ * the library's code object, loaded with it and held until the process
+ * ends (its device address is taken by convcrf_init).  The compatibility
+ * matrix is handed to a kernel by value, so params->compat may be ordinary
+ * host memory.  Limits: the workspace of the call, 256-byte aligned slices
+ * of B*C*H*W floats for the ping-pong (iters >= 2 or learnable features),
+ * plus with blur s B*(H/s)*(W/s)*(2C+3) floats, plus C*C for a given
+ * compatibility, must fit in 64 MiB (1 x 21 x 512 x 512 needs 22 MB), else
+ * CONVCRF_E_UNSUPPORTED with the size in the message and nothing enqueued;
+ * the materialised variant is refused (CONVCRF_E_UNSUPPORTED) and the
+ * resident variant runs as CONVCRF_VARIANT_FUSED.  No profiling events are
+ * recorded for it.  Every call on a device shares that device's scratch
+ * array and leaves its contents behind (nothing in it needs to start at
+ * zero): calls that overlap on one GPU -- on different streams, or from
+ * different contexts or threads -- race and must be ordered by the caller. */
+convcrf_status convcrf_meanfield_noalloc(convcrf_ctx *ctx, const float *unary,
+                                         const float *image, int B, int C, int H,
+                                         int W, const convcrf_params *params,
+                                         int iters, float *q_out, void *stream);
+
 /* Reverse mode: the derivative of a scalar loss L through convcrf_meanfield,
  * for training the CRF by backpropagation through the unrolled
  * mean-field rounds of Alg. 1 (Sec. 1; Sec. 5.3 trains end to end through

@@ -33,7 +33,7 @@ KERNEL_NAMES = ("fused_first", "fused_iter", "fused_resident", "sync_reset", "so
 EXPORTED = ("convcrf_default_params", "convcrf_validate", "convcrf_init", "convcrf_destroy",
             "convcrf_meanfield", "convcrf_meanfield_backward", "convcrf_profile_enable",
             "convcrf_profile_read", "convcrf_last_error", "convcrf_status_string",
-            "convcrf_strerror", "convcrf_synchronize")
+            "convcrf_strerror", "convcrf_synchronize", "convcrf_meanfield_noalloc")
 
 # order of grad_kernel in convcrf_meanfield_backward
 KERNEL_PARAM_NAMES = ("w_app", "theta_alpha", "theta_beta", "w_smooth", "theta_gamma")
@@ -150,6 +150,8 @@ def load_library(path: str = LIB_PATH):
     lib.convcrf_meanfield.restype = st
     lib.convcrf_meanfield.argtypes = [vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                       ctypes.c_int, P(CParams), ctypes.c_int, vp, vp]
+    lib.convcrf_meanfield_noalloc.restype = st
+    lib.convcrf_meanfield_noalloc.argtypes = lib.convcrf_meanfield.argtypes
     lib.convcrf_meanfield_backward.restype = st
     lib.convcrf_meanfield_backward.argtypes = [vp, vp, vp, ctypes.c_int, ctypes.c_int,
                                                ctypes.c_int, ctypes.c_int, P(CParams),
@@ -221,10 +223,14 @@ class ConvCRF:
     def __exit__(self, *exc):
         self.close()
 
-    def meanfield(self, unary, image, params: Params, iters: int, out=None, stream=None):
+    def meanfield(self, unary, image, params: Params, iters: int, out=None, stream=None,
+                  noalloc: bool = False):
         """Q after ``iters`` mean-field rounds; unary [B,C,H,W], image
         [B,3,H,W], both contiguous float32 CUDA tensors.  Enqueued on
-        ``stream`` (default: torch's current stream); returns ``out``."""
+        ``stream`` (default: torch's current stream); returns ``out``.
+        ``noalloc`` calls convcrf_meanfield_noalloc (workspace in the
+        library's per-device scratch array; pass ``out`` to allocate
+        nothing on the torch side either)."""
         import torch
         for name, t in (("unary", unary), ("image", image)):
             if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous() or t.dim() != 4:
@@ -241,9 +247,9 @@ class ConvCRF:
             stream = torch.cuda.current_stream(unary.device)
         sp = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
         cp = params.c((B, C, H, W), unary.device)
-        _check(self._lib.convcrf_meanfield(self._h, unary.data_ptr(), image.data_ptr(), B, C, H, W,
-                                           ctypes.byref(cp), int(iters), out.data_ptr(), sp),
-               self._h)
+        fn = self._lib.convcrf_meanfield_noalloc if noalloc else self._lib.convcrf_meanfield
+        _check(fn(self._h, unary.data_ptr(), image.data_ptr(), B, C, H, W, ctypes.byref(cp),
+                  int(iters), out.data_ptr(), sp), self._h)
         return out
 
     def meanfield_backward(self, unary, image, params: Params, iters: int, grad_q,

@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstring>
 #include <initializer_list>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -17,6 +18,11 @@
 #include "crf_internal.h"
 
 using namespace convcrf;
+
+// Scratch memory of the allocation-free entry point (see scratch_address):
+// 64 MiB per device, zero at load, held until the process ends.
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
 
 namespace {
 
@@ -71,7 +77,9 @@ struct convcrf_ctx {
     unsigned int* flag_host = nullptr;
     hipEvent_t flag_event = nullptr;
     bool flag_pending = false;
+    void* scratch_ptr = nullptr;    // device address of this device's scratch array
     bool profiling = false;
+    bool no_events = false;         // set during an allocation-free call
     std::vector<ProfRec> prof;
     std::vector<hipEvent_t> free_events;
 };
@@ -193,13 +201,14 @@ hipEvent_t take_event(convcrf_ctx* ctx) {
 template <typename F>
 convcrf_status launch(convcrf_ctx* ctx, int kernel, hipStream_t stream, const char* what, F&& fn) {
     ProfRec rec{kernel, nullptr, nullptr};
-    if (ctx->profiling) {
+    const bool record = ctx->profiling && !ctx->no_events;
+    if (record) {
         rec.start = take_event(ctx);
         rec.stop = take_event(ctx);
         if (rec.start) (void)hipEventRecord(rec.start, stream);
     }
     hipError_t e = fn();
-    if (ctx->profiling && rec.start && rec.stop) {
+    if (record && rec.start && rec.stop) {
         (void)hipEventRecord(rec.stop, stream);
         ctx->prof.push_back(rec);
     }
@@ -503,6 +512,77 @@ convcrf_status queue_overrun_check(convcrf_ctx* ctx, hipStream_t stream) {
     return CONVCRF_OK;
 }
 
+// ---- the allocation-free entry point's scratch memory
+// One array per device, for callers that cannot allocate (graph capture,
+// serving loops): the Q ping-pong buffer, the pooled buffers of the blur
+// path and the compatibility matrix of a convcrf_meanfield_noalloc call are
+// carved from it.  Its name is a host-side stand-in: host code uses only the
+// device address hipGetSymbolAddress returns for it, taken once per device
+// (with that device current) by convcrf_init.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on `device` (current on entry), taken on
+// the first call for that device.
+hipError_t scratch_address(int device, void** out) {
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+    if (!g_scratch_ptr[device]) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[device] = ptr;
+    }
+    *out = g_scratch_ptr[device];
+    return hipSuccess;
+}
+
+// Where a call's workspace comes from: the context's growable buffers, or
+// consecutive 256-byte aligned slices of the scratch array (no allocation;
+// sizes beyond it are refused).
+struct Workspace {
+    char* base = nullptr;     // scratch address, or null: the context's buffers
+    size_t used = 0;
+    size_t need = 0;          // bytes the call asked of the scratch array
+};
+
+convcrf_status take(convcrf_ctx* ctx, Workspace& w, DevBuf& buf, size_t bytes, void** out) {
+    if (!w.base) {
+        convcrf_status st = ensure(ctx, buf, bytes);
+        if (st != CONVCRF_OK) return st;
+        *out = buf.p;
+        return CONVCRF_OK;
+    }
+    const size_t at = (w.used + 255) / 256 * 256;
+    w.need = at + bytes;
+    if (w.need > kNoAllocScratchBytes)
+        return fail(ctx, CONVCRF_E_UNSUPPORTED,
+                    "convcrf_meanfield_noalloc: this call needs " + std::to_string(w.need) +
+                        " bytes of workspace, more than its " +
+                        std::to_string(kNoAllocScratchBytes) + "-byte scratch array");
+    w.used = at + bytes;
+    *out = w.base + at;
+    return CONVCRF_OK;
+}
+
+// The compatibility matrix for an allocation-free call: copied into the
+// scratch slice by a kernel that takes the C x C values as its argument, so
+// that no pinned staging buffer is needed.
+convcrf_status upload_mu_noalloc(convcrf_ctx* ctx, Workspace& w, const float* mu, int C,
+                                 hipStream_t stream, const float** out) {
+    void* dst = nullptr;
+    DevBuf unused;
+    convcrf_status st = take(ctx, w, unused, sizeof(float) * (size_t)C * C, &dst);
+    if (st != CONVCRF_OK) return st;
+    CompatBlock blk{};
+    std::memcpy(blk.v, mu, sizeof(float) * (size_t)C * C);
+    const hipError_t e = launch_copy_compat(blk, C * C, static_cast<float*>(dst), stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "copying the compatibility matrix");
+    *out = static_cast<const float*>(dst);
+    return CONVCRF_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -581,6 +661,27 @@ convcrf_status convcrf_init(convcrf_ctx** out, int device) {
     if (!ctx) return fail(nullptr, CONVCRF_E_OOM, "context allocation failed");
     ctx->device = device;
     ctx->num_cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
+    {
+        // the scratch array's address on this device, with the device current
+        int prev = 0;
+        (void)hipGetDevice(&prev);
+        void* ptr = nullptr;
+        e = hipSetDevice(device);
+        if (e == hipSuccess) e = scratch_address(device, &ptr);
+        // the allocation-free entry point's one kernel of its own is launched
+        // once here (copying nothing), so that whatever the runtime sets up
+        // on a kernel's first launch happens at set-up, not inside that call
+        if (e == hipSuccess) e = launch_copy_compat(CompatBlock{}, 0, static_cast<float*>(ptr), nullptr);
+        if (e == hipSuccess) e = hipStreamSynchronize(nullptr);
+        (void)hipSetDevice(prev);
+        if (e != hipSuccess) {
+            delete ctx;
+            (void)hipGetLastError();
+            return fail(nullptr, CONVCRF_E_HIP,
+                        std::string("scratch array address: ") + hipGetErrorString(e));
+        }
+        ctx->scratch_ptr = ptr;
+    }
     int coop = 0;
     if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, device) == hipSuccess)
         ctx->coop = coop != 0;
@@ -651,9 +752,16 @@ convcrf_status convcrf_profile_read(convcrf_ctx* ctx, const char* name, double* 
     return CONVCRF_OK;
 }
 
-convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const float* image, int B,
-                                 int C, int H, int W, const convcrf_params* params, int iters,
-                                 float* q_out, void* stream_ptr) {
+}  // extern "C"
+
+namespace {
+
+// convcrf_meanfield, with its workspace from w (the context's buffers when
+// w.base is null, else the scratch array: no allocation, no events, the
+// materialised variant refused and the resident one run as fused).
+convcrf_status meanfield_impl(convcrf_ctx* ctx, const float* unary, const float* image, int B,
+                              int C, int H, int W, const convcrf_params* params, int iters,
+                              float* q_out, void* stream_ptr, Workspace& w) {
     if (!ctx) return fail(nullptr, CONVCRF_E_INVALID_ARG, "ctx is NULL");
     convcrf_status st = validate(ctx, B, C, H, W, params, iters);
     if (st != CONVCRF_OK) return st;
@@ -681,18 +789,29 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     const int k = p.filter_size;
     const int s = p.blur;
     const bool mat = p.variant == CONVCRF_VARIANT_MATERIALISED;
+    const bool noalloc = w.base != nullptr;
+    if (noalloc && mat)
+        return fail(ctx, CONVCRF_E_UNSUPPORTED,
+                    "convcrf_meanfield_noalloc: the materialised variant needs its kernel matrix "
+                    "allocated; use convcrf_meanfield");
     const float* mu_dev = nullptr;
     if (p.compat) {
-        st = upload_mu(ctx, p.compat, C, stream);
-        if (st != CONVCRF_OK) return st;
-        mu_dev = static_cast<const float*>(ctx->mu.p);
+        if (noalloc) {
+            st = upload_mu_noalloc(ctx, w, p.compat, C, stream, &mu_dev);
+            if (st != CONVCRF_OK) return st;
+        } else {
+            st = upload_mu(ctx, p.compat, C, stream);
+            if (st != CONVCRF_OK) return st;
+            mu_dev = static_cast<const float*>(ctx->mu.p);
+        }
     }
 
     if (p.features) {
         // learnable smoothness features: Q0 = softmax(U), then one update
         // launch per iteration, the last one into q_out
-        if ((st = ensure(ctx, ctx->q_ws, qbytes)) != CONVCRF_OK) return st;
-        float* ws = static_cast<float*>(ctx->q_ws.p);
+        void* wsp = nullptr;
+        if ((st = take(ctx, w, ctx->q_ws, qbytes, &wsp)) != CONVCRF_OK) return st;
+        float* ws = static_cast<float*>(wsp);
         FeatArgs f = feat_args(p, unary, image, mu_dev, B, C, H, W);
         // the staged Q planes live in q_out and the workspace
         f.vec4 = f.vec4 && reinterpret_cast<uintptr_t>(q_out) % 16 == 0 &&
@@ -727,8 +846,9 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
         const TileConfig tile = pick_tile(k, C, !mat, mu_dev != nullptr);
         if (tile.rows == 0) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window and classes exceed LDS");
         const size_t lds = iter_lds_bytes(k, C, tile, !mat, mu_dev != nullptr);
+        void* wsp = nullptr;
         if (iters > 1) {
-            st = ensure(ctx, ctx->q_ws, qbytes);
+            st = take(ctx, w, ctx->q_ws, qbytes, &wsp);
             if (st != CONVCRF_OK) return st;
         }
         if (mat) {
@@ -746,13 +866,13 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
         bool streamed = false, ring = false;
         size_t lds_s = 0;
         plan_unpooled(a, as, ar, streamed, ring, lds_s, tile, mat, k, B, C, H, W, unary, image,
-                      static_cast<const float*>(ctx->kmat.p), {q_out, ctx->q_ws.p});
+                      static_cast<const float*>(ctx->kmat.p), {q_out, wsp});
         // Resident variant: all iterations in one launch when every tile's
         // work-group fits on the device at once (Potts): the tile stays in
         // LDS and only border rings cross memory.  On the streamed tiles the
         // weights and the unary also stay in registers for the whole call.
-        if (p.variant == CONVCRF_VARIANT_RESIDENT && !mu_dev && iters >= 2 && ctx->coop &&
-            streamed && as.ntiles <= 4 * ctx->num_cus) {
+        if (p.variant == CONVCRF_VARIANT_RESIDENT && !noalloc && !mu_dev && iters >= 2 &&
+            ctx->coop && streamed && as.ntiles <= 4 * ctx->num_cus) {
             if ((st = ensure(ctx, ctx->q_ws2, qbytes)) != CONVCRF_OK) return st;
             if ((st = ensure_sync(ctx, (size_t)as.ntiles, stream)) != CONVCRF_OK) return st;
             IterArgs r = as;
@@ -777,8 +897,8 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
             (void)hipGetLastError();  // refused: one launch per iteration below
             ctx->err = std::string("resident launch refused (") + hipGetErrorString(fits) +
                        "); ran one launch per iteration";
-        } else if (p.variant == CONVCRF_VARIANT_RESIDENT && !mu_dev && iters >= 2 && ctx->coop &&
-                   tile.pix == 2 && tile.width == 32 && k <= 7 &&
+        } else if (p.variant == CONVCRF_VARIANT_RESIDENT && !noalloc && !mu_dev && iters >= 2 &&
+                   ctx->coop && tile.pix == 2 && tile.width == 32 && k <= 7 &&
                    a.ntiles <= 4 * ctx->num_cus) {
             if ((st = ensure(ctx, ctx->q_ws2, qbytes)) != CONVCRF_OK) return st;
             if ((st = ensure_sync(ctx, (size_t)a.ntiles, stream)) != CONVCRF_OK) return st;
@@ -805,7 +925,7 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
             ctx->err = std::string("resident launch refused (") + hipGetErrorString(fits) +
                        "); ran one launch per iteration";
         }
-        float* ws = static_cast<float*>(ctx->q_ws.p);
+        float* ws = static_cast<float*>(wsp);
         // the last iteration writes q_out; earlier ones alternate so that
         // source and destination always differ
         const float* cur = unary;
@@ -829,12 +949,13 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
     // ---- blur: message on the s x s pooled grid (Sec. 4.2)
     const int Hp = H / s, Wp = W / s;
     const size_t pbytes = sizeof(float) * (size_t)B * Hp * Wp;
-    if ((st = ensure(ctx, ctx->pool_q, pbytes * C)) != CONVCRF_OK) return st;
-    if ((st = ensure(ctx, ctx->pool_m, pbytes * C)) != CONVCRF_OK) return st;
-    if ((st = ensure(ctx, ctx->pool_f, pbytes * 3)) != CONVCRF_OK) return st;
-    float* qp = static_cast<float*>(ctx->pool_q.p);
-    float* mp = static_cast<float*>(ctx->pool_m.p);
-    float* fp = static_cast<float*>(ctx->pool_f.p);
+    void *qpv = nullptr, *mpv = nullptr, *fpv = nullptr;
+    if ((st = take(ctx, w, ctx->pool_q, pbytes * C, &qpv)) != CONVCRF_OK) return st;
+    if ((st = take(ctx, w, ctx->pool_m, pbytes * C, &mpv)) != CONVCRF_OK) return st;
+    if ((st = take(ctx, w, ctx->pool_f, pbytes * 3, &fpv)) != CONVCRF_OK) return st;
+    float* qp = static_cast<float*>(qpv);
+    float* mp = static_cast<float*>(mpv);
+    float* fp = static_cast<float*>(fpv);
     // pooled message: 16 x 8 cell tiles, one wavefront per window row, the
     // classes in chunks of at most kPmsgClasses (the message does not mix
     // classes; each chunk recomputes the weights)
@@ -876,6 +997,32 @@ convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const flo
         if (st != CONVCRF_OK) return st;
     }
     return CONVCRF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+convcrf_status convcrf_meanfield(convcrf_ctx* ctx, const float* unary, const float* image, int B,
+                                 int C, int H, int W, const convcrf_params* params, int iters,
+                                 float* q_out, void* stream_ptr) {
+    Workspace w;
+    return meanfield_impl(ctx, unary, image, B, C, H, W, params, iters, q_out, stream_ptr, w);
+}
+
+convcrf_status convcrf_meanfield_noalloc(convcrf_ctx* ctx, const float* unary, const float* image,
+                                         int B, int C, int H, int W,
+                                         const convcrf_params* params, int iters, float* q_out,
+                                         void* stream_ptr) {
+    if (!ctx) return fail(nullptr, CONVCRF_E_INVALID_ARG, "ctx is NULL");
+    if (!ctx->scratch_ptr) return fail(ctx, CONVCRF_E_HIP, "no scratch address for this device");
+    Workspace w;
+    w.base = static_cast<char*>(ctx->scratch_ptr);
+    ctx->no_events = true;
+    const convcrf_status st =
+        meanfield_impl(ctx, unary, image, B, C, H, W, params, iters, q_out, stream_ptr, w);
+    ctx->no_events = false;
+    return st;
 }
 
 convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,

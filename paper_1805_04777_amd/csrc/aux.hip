@@ -1,5 +1,6 @@
 // aux.hip -- the kernels around the fused iteration on gfx950:
 //   zero_u32_kernel      clears the synchronisation flags of a resident launch
+//   copy_compat_kernel   writes a compatibility matrix passed by value
 //   softmax_kernel       Q = softmax(U)                 (Alg. 1 initialisation)
 //   build_kernel_kernel  kernel matrix of Eq. 5, merged over both Gaussians
 //                        (materialised comparison variant, Sec. 4.1)
@@ -449,6 +450,17 @@ __global__ __launch_bounds__(256) void zero_u32_kernel(unsigned int* p, int n) {
 inline unsigned nblocks(long long n, int bs) { return (unsigned)((n + bs - 1) / bs); }
 
 }  // namespace
+
+__global__ __launch_bounds__(256) void copy_compat_kernel(const CompatBlock blk, int n,
+                                                          float* dst) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x) dst[i] = blk.v[i];
+}
+
+hipError_t launch_copy_compat(const CompatBlock& blk, int n, float* dst, hipStream_t stream) {
+    if (n < 0 || n > kMaxC * kMaxC) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(copy_compat_kernel, dim3(1), dim3(256), 0, stream, blk, n, dst);
+    return hipGetLastError();
+}
 
 hipError_t launch_zero_u32(unsigned int* p, int n, hipStream_t stream) {
     hipLaunchKernelGGL(zero_u32_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, p, n);

@@ -182,6 +182,14 @@ CONVCRF_DECLARE_ITER(15)
 // memset, so that the sequence may be captured in a graph).
 hipError_t launch_zero_u32(unsigned int* p, int n, hipStream_t stream);
 
+// A compatibility matrix passed by value (kernel argument), for callers that
+// cannot stage it through pinned host memory: copy_compat writes its first n
+// values to dst on the device.
+struct CompatBlock {
+    float v[kMaxC * kMaxC];
+};
+hipError_t launch_copy_compat(const CompatBlock& blk, int n, float* dst, hipStream_t stream);
+
 // Q = softmax(U) over classes, per pixel (Alg. 1 initialisation).
 hipError_t launch_softmax(const float* U, float* Q, int B, int C, int HW,
                           hipStream_t stream);
