@@ -38,24 +38,26 @@ METRIC_BWD = ("megapixel·iterations/sec and ms per 5-iter derivative (forward r
 UNIT = "MP·iter/s"
 
 # MI355X: FP32 vector peak 157.3 TFLOP/s (256 CUs at 2.4 GHz, 128 FP32 FMA
-# lanes per CU per clock).  The library is built without packed FP32, but
-# gfx950 issues two-operand-VGPR v_fmac_f32 at close to that rate as well, so
-# the published figure is the ceiling.  HBM3E: 8 TB/s.
+# lanes per CU per clock).  The library is built without packed FP32; gfx950
+# reaches that lane rate only by issuing VALU instructions of two waves of a
+# SIMD in the same cycle, which needs all-VGPR operands (measured with an FMA
+# loop: 118-123 lanes per clock per CU at two or more waves per SIMD, 59 at
+# one, about 62 with an SGPR or DPP operand).  HBM3E: 8 TB/s.
 PEAK_VALU_FP32 = 157.3e12
+PEAK_VALU_LANE_OPS = 256 * 128 * 2.4e9     # VALU lane-instructions per second at that peak
 PEAK_HBM = 8.0e12
 
 ITER_SRC = os.path.join(ROOT, "paper_1805_04777_amd", "csrc", "iter.hip")
-TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
+COUNTERS = os.path.join(ROOT, "profiles", "counters.json")
 
 
-def flops_per_pixel_iter(C: int, k: int, potts: bool) -> int:
-    """Algorithmic flops of one pixel-iteration of the fused path: message
-    2C(k^2-1), Gaussian weights 12 per tap (3 differences, squared norm,
-    exponent, exp, add), compatibility 2C^2 (C for Potts: Z = U + M), unary
-    add and softmax 5C + 1."""
+def flops_per_pixel_iter(C: int, k: int) -> int:
+    """Algorithmic flops of one pixel-iteration: message 2C(k^2-1), Gaussian
+    weights 12 per tap (3 differences, squared norm, exponent, exp, add),
+    compatibility 2C^2 (the C x C matrix-vector product; the library folds
+    Potts into Z = U + M, which needs fewer), unary add and softmax 5C + 1."""
     taps = k * k - 1
-    compat = C if potts else 2 * C * C
-    return 2 * C * taps + 12 * taps + compat + 5 * C + 1
+    return 2 * C * taps + 12 * taps + 2 * C * C + 5 * C + 1
 
 
 def bytes_per_pixel(C: int, first: bool) -> int:
@@ -66,16 +68,19 @@ def bytes_per_pixel(C: int, first: bool) -> int:
 
 
 def algorithmic_per_launch(kname: str, wl, D: int = 0):
-    """(flops, HBM bytes) one launch of `kname` must spend on workload `wl`,
-    averaged over the launches of one call; fp32, Potts compatibility; D
-    learnable smoothness feature planes (0 without)."""
+    """(flops, HBM bytes) one launch of `kname` must spend on workload `wl`
+    (averaged over its launches in one call); fp32; D learnable smoothness
+    feature planes (0 without).  fused_iter is one later iteration (reads
+    Q_t, U and the image, writes Q_t+1), fused_first the first one (reads U
+    and the image, writes Q_1; its softmax of U is counted with the update's)."""
     C, k, T, px = wl.C, wl.filter_size, wl.iters, wl.pixels
     if kname == "fused_iter":
-        return (flops_per_pixel_iter(C, k, True) * px,
-                (bytes_per_pixel(C, True) + (T - 1) * bytes_per_pixel(C, False)) / T * px)
+        return flops_per_pixel_iter(C, k) * px, bytes_per_pixel(C, False) * px
+    if kname == "fused_first":
+        return (flops_per_pixel_iter(C, k) + 5 * C + 1) * px, bytes_per_pixel(C, True) * px
     if kname == "materialised_iter":
         taps = k * k - 1
-        return ((flops_per_pixel_iter(C, k, True) - 12 * taps) * px,
+        return ((flops_per_pixel_iter(C, k) - 12 * taps) * px,
                 ((bytes_per_pixel(C, True) + (T - 1) * bytes_per_pixel(C, False)) / T + 4 * taps) * px)
     if kname == "build_kernel":
         taps = k * k - 1
@@ -83,7 +88,7 @@ def algorithmic_per_launch(kname: str, wl, D: int = 0):
     if kname == "fused_resident":
         # one launch = T iterations; bytes: U and the image read, Q written
         # (the tiles' border rings are the only other traffic)
-        return T * flops_per_pixel_iter(C, k, True) * px, (8 * C + 12) * px
+        return T * flops_per_pixel_iter(C, k) * px, (8 * C + 12) * px
     s2 = wl.blur * wl.blur
     npx = px // s2
     if kname == "blur_message":
@@ -149,17 +154,20 @@ def source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def load_traffic(workload: str, kernel: str):
-    """HBM bytes per launch from committed rocprofv3 counters, if they were
-    taken on the current kernel source."""
+def load_counters(workload: str, kernel: str):
+    """Counter figures per launch of `kernel` on `workload` from the committed
+    rocprofv3 passes (profiles/counters.json): HBM bytes (FETCH_SIZE and
+    WRITE_SIZE, scaled by what they read for a plain copy) and VALU
+    instructions (SQ_INSTS_VALU); None unless they were taken on the current
+    kernel source."""
     try:
-        with open(TRAFFIC) as f:
+        with open(COUNTERS) as f:
             rec = json.load(f)[f"{workload}/{kernel}"]
     except (OSError, KeyError, ValueError):
         return None
     if rec.get("source_sha256_16") != source_hash():
         return None
-    return rec.get("bytes_per_launch")
+    return rec
 
 
 def cpu_baseline(wl, U, I, budget_s: float = 10.0, backward: bool = False, features=None):
@@ -186,12 +194,45 @@ def cpu_baseline(wl, U, I, budget_s: float = 10.0, backward: bool = False, featu
             break
     t = float(np.median(times))
     mpi = wl.pixels * wl.iters / 1e6
+    single = None if backward or features is not None else cpu_single_thread(wl)
     return {"value": round(mpi / t, 3), "unit": UNIT, "cores": oracle.num_threads(),
-            "kind": "oracle",
+            "kind": "oracle", "single_thread": single,
             "sample": f"the full {wl.name} workload ({wl.B}x{wl.C}x{wl.H}x{wl.W}, k={wl.filter_size}, "
                       f"blur={wl.blur}, T={wl.iters}){', derivative' if backward else ''}"
                       f"{', learnable features D=2' if features is not None else ''}, "
                       f"{len(times)} calls, median {t * 1e3:.1f} ms/call, double precision"}
+
+
+def cpu_single_thread(wl):
+    """The oracle on one host thread (OMP_NUM_THREADS=1, in a child process,
+    since OpenMP reads it at start-up), on the top quarter of the first
+    image of the workload (the same per-pixel work; a few seconds)."""
+    import subprocess
+    rows = max(1, wl.H // 4)
+    code = (
+        "import sys, time, json\n"
+        f"sys.path.insert(0, {ROOT!r})\n"
+        "import oracle\n"
+        "from paper_1805_04777_amd import synth\n"
+        f"wl = synth.WORKLOADS[{wl.name!r}]\n"
+        "U, I, _ = synth.make_inputs(wl.with_(B=1))\n"
+        f"U = U[:, :, :{rows}].copy(); I = I[:, :, :{rows}].copy()\n"
+        "p = oracle.OracleParams(filter_size=wl.filter_size, blur=wl.blur, w_app=wl.w_app,"
+        " theta_alpha=wl.theta_alpha, theta_beta=wl.theta_beta, w_smooth=wl.w_smooth,"
+        " theta_gamma=wl.theta_gamma)\n"
+        "t0 = time.perf_counter(); oracle.meanfield(U, I, p, wl.iters); t = time.perf_counter() - t0\n"
+        "print(json.dumps({'s': t, 'threads': oracle.num_threads()}))\n")
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    try:
+        r = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True,
+                           timeout=120, check=True)
+        rec = json.loads(r.stdout.strip().splitlines()[-1])
+    except Exception as e:  # noqa: BLE001 - reported, not fatal
+        return {"error": str(e)[:200]}
+    mpi = rows * wl.W * wl.iters / 1e6
+    return {"value": round(mpi / rec["s"], 4), "unit": UNIT, "cores": rec["threads"],
+            "sample": f"rows 0..{rows - 1} of image 0 ({rows}x{wl.W}), one call, "
+                      f"{rec['s'] * 1e3:.0f} ms"}
 
 
 def copy_reference(torch, mib: int, steps: int) -> int:
@@ -322,28 +363,44 @@ def main(argv=None):
     # Events around every launch add about a microsecond each, so the
     # kernel's duration is taken from the timed region instead: its share of
     # the evented time, applied to the time per call, over its launches per
-    # call (on the fused path every launch is this kernel).
+    # call.
     share = k_ms / sum(v[0] for v in launched.values())
     avg_s = ms / 1e3 * share / (k_n / args.steps)
     avg_s_events = k_ms / 1e3 / k_n
     F, Bytes = algorithmic_per_launch(kname, wl, D)
     alu_frac = F / avg_s / PEAK_VALU_FP32
     hbm_frac = Bytes / avg_s / PEAK_HBM
-    # the roofline the kernel is closer to (the counters show neither saturated)
-    bound = "alu" if alu_frac >= hbm_frac else "hbm"
+    # Which ceiling binds is decided by the counters, when they were taken on
+    # the current source: the kernel's measured HBM traffic per second
+    # against 8 TB/s, and its measured VALU lane-instructions per second
+    # against the 157.3 TFLOP/s lane rate; the higher utilisation is the
+    # binding one.  Without current counters the algorithmic fractions decide.
+    ctr = load_counters(args.workload, kname)
+    if ctr:
+        hbm_util = ctr["bytes_per_launch"] / avg_s / PEAK_HBM
+        valu_util = ctr["valu_insts_per_launch"] * 64 / avg_s / PEAK_VALU_LANE_OPS
+        bound = "alu" if valu_util > hbm_util else "hbm"
+        rule = "counters: measured HBM bytes/s vs 8 TB/s against measured VALU lane-ops/s vs peak"
+    else:
+        hbm_util = valu_util = None
+        bound = "alu" if alu_frac >= hbm_frac else "hbm"
+        rule = "no counters on the current source: the larger algorithmic fraction"
     if bound == "alu":
         roof = {"bound": "alu", "achieved": round(F / avg_s / 1e12, 3), "peak": round(PEAK_VALU_FP32 / 1e12, 1),
                 "unit": "TFLOP/s", "frac": round(alu_frac, 4)}
     else:
         roof = {"bound": "hbm", "achieved": round(Bytes / avg_s / 1e9, 1), "peak": PEAK_HBM / 1e9,
                 "unit": "GB/s", "frac": round(hbm_frac, 4)}
-    roof["traffic"] = load_traffic(args.workload, kname)
+    roof["traffic"] = ctr["bytes_per_launch"] if ctr else None
     roof.update({
         "kernel": kname, "launches": k_n, "avg_launch_us": round(avg_s * 1e6, 3),
         "avg_launch_us_per_launch_events": round(avg_s_events * 1e6, 3),
         "algorithmic_flop_per_launch": int(F), "algorithmic_bytes_per_launch": int(Bytes),
         "alu_frac": round(alu_frac, 4), "hbm_frac": round(hbm_frac, 4),
-        "kernels_us_per_step": {n: round(v[0] * 1e3 / args.steps, 3) for n, v in launched.items()},
+        "bound_rule": rule,
+        "hbm_util_counters": None if hbm_util is None else round(hbm_util, 4),
+        "valu_util_counters": None if valu_util is None else round(valu_util, 4),
+        "evented_ms_per_step_by_kernel": {n: round(v[0] / args.steps, 5) for n, v in launched.items()},
     })
 
     rec = {
