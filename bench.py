@@ -100,6 +100,15 @@ def algorithmic_per_launch(kname: str, wl, D: int = 0):
         # launches) or the full Q (the last one)
         return ((6 + 1 + 5 + 1) * C * px,
                 4 * C * px + 4 * C * npx + ((T - 1) * 4 * C * npx + 4 * C * px) / T)
+    if kname == "blur_iteration":
+        # one fused iteration (4 x 4 pooling): the pooled message of every
+        # cell (weights 12 and message 2C per tap) and per pixel the bilinear
+        # sample (3C FMA), unary add and softmax (5C + 1) and the cell average
+        # (C); reads U, the pooled Q_t and colours, writes the pooled Q_t+1
+        # (T - 1 launches) or the full Q (the last)
+        taps = k * k - 1
+        return ((2 * C + 12) * taps * npx + (6 * C + 5 * C + 1 + C) * px,
+                4 * C * px + (4 * C + 12) * npx + ((T - 1) * 4 * C * npx + 4 * C * px) / T)
     if kname == "blur_pool":
         # two launches per call: softmax(U) pooled (21 planes) and the image
         # (3 planes); averaged

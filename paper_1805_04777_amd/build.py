@@ -1,9 +1,8 @@
 """Build ``libconvcrf.so`` (the HIP library behind include/convcrf.h) for gfx950.
 
 Every call compiles from source: each translation unit of ``csrc/`` goes to
-its own object (the fused iteration and the adjoint message once per window
-side k), in parallel, and
-the objects are linked into ``paper_1805_04777_amd/libconvcrf.so``.  Objects
+its own object (the fused iteration, the fused blur iteration and the adjoint
+message once per window side k), in parallel, and the objects are linked into ``paper_1805_04777_amd/libconvcrf.so``.  Objects
 live in ``_build/`` at the repository root.
 
     python -m paper_1805_04777_amd.build [--jobs N] [--verbose]
@@ -48,6 +47,8 @@ def _units():
                       [f"-DCRF_K={k}"]))
         units.append((os.path.join(CSRC, "backward.hip"), os.path.join(BUILD, f"bwd_k{k}.o"),
                       [f"-DCRF_BWD_K={k}"]))
+        units.append((os.path.join(CSRC, "blur.hip"), os.path.join(BUILD, f"blur_k{k}.o"),
+                      [f"-DCRF_BLUR_K={k}"]))
     for name in ("aux", "backward", "features", "api"):
         units.append((os.path.join(CSRC, f"{name}.hip"), os.path.join(BUILD, f"{name}.o"), []))
     return units

@@ -28,7 +28,8 @@ VARIANT_RESIDENT = 2
 
 KERNEL_NAMES = ("fused_first", "fused_iter", "fused_resident", "sync_reset", "softmax", "build_kernel",
                 "materialised_iter", "blur_pool", "blur_message", "blur_update",
-                "bwd_point", "bwd_message", "bwd_reduce", "feature_iter", "bwd_blur_transpose")
+                "bwd_point", "bwd_message", "bwd_reduce", "feature_iter", "bwd_blur_transpose",
+                "blur_iteration")
 
 EXPORTED = ("convcrf_default_params", "convcrf_validate", "convcrf_init", "convcrf_destroy",
             "convcrf_meanfield", "convcrf_meanfield_backward", "convcrf_profile_enable",

@@ -37,10 +37,10 @@ const char* const kKernelNames[] = {"fused_iter",   "softmax",      "build_kerne
                                     "materialised_iter", "blur_pool", "blur_message",
                                     "blur_update",  "fused_resident", "sync_reset",
                                     "bwd_point", "bwd_message", "bwd_reduce", "feature_iter",
-                                    "bwd_blur_transpose", "fused_first"};
+                                    "bwd_blur_transpose", "fused_first", "blur_iteration"};
 enum KernelId {
     kFused = 0, kSoftmax, kBuild, kMatIter, kPool, kBlurMsg, kBlurUpd, kResident, kSyncReset,
-    kBwdPoint, kBwdMsg, kBwdReduce, kFeatIter, kBwdBlurT, kFusedFirst, kNumKernels
+    kBwdPoint, kBwdMsg, kBwdReduce, kFeatIter, kBwdBlurT, kFusedFirst, kBlurIter, kNumKernels
 };
 
 struct DevBuf {
@@ -244,6 +244,23 @@ hipError_t launch_pmsg(const IterArgs& a, int k, int nchunks, size_t lds, hipStr
         default: return hipErrorInvalidValue;
     }
 }
+
+}  // namespace
+
+hipError_t convcrf::launch_blur_iter(const BlurIterArgs& a, int k, hipStream_t s) {
+    switch (k) {
+        case 3: return launch_blur_iter_k3(a, s);
+        case 5: return launch_blur_iter_k5(a, s);
+        case 7: return launch_blur_iter_k7(a, s);
+        case 9: return launch_blur_iter_k9(a, s);
+        case 11: return launch_blur_iter_k11(a, s);
+        case 13: return launch_blur_iter_k13(a, s);
+        case 15: return launch_blur_iter_k15(a, s);
+        default: return hipErrorNotSupported;
+    }
+}
+
+namespace {
 
 hipError_t launch_rstream(const IterArgs& a, int k, size_t lds, int num_cus, hipStream_t s,
                           bool probe) {
@@ -969,6 +986,42 @@ convcrf_status meanfield_impl(convcrf_ctx* ctx, const float* unary, const float*
     st = launch(ctx, kPool, stream, "blur_pool",
                 [&] { return launch_pool(unary, qp, B, C, H, W, s, 1, stream); });
     if (st != CONVCRF_OK) return st;
+
+    // 4 x 4 pooling: one fused launch per iteration (pooled message of each
+    // work-group's cells and the full-resolution update of its pixels), the
+    // pooled Q ping-ponging between qp and mp; the last one writes q_out
+    if (s == kFusedBlurFactor && k >= 3 && B <= 65535 &&
+        reinterpret_cast<uintptr_t>(unary) % 8 == 0 && reinterpret_cast<uintptr_t>(q_out) % 8 == 0 &&
+        blur_iter_lds_bytes(k, C == 19 || C == 21 ? C : (C <= 8 ? 8 : 24), mu_dev != nullptr) <=
+            kLdsLimit) {
+        BlurIterArgs bi{};
+        bi.pcol = fp;
+        bi.unary = unary;
+        bi.mu = mu_dev;
+        bi.B = B;
+        bi.C = C;
+        bi.H = H;
+        bi.W = W;
+        bi.Hp = Hp;
+        bi.Wp = Wp;
+        bi.include_center = p.include_center;
+        bi.center_w = a.center_w;
+        bi.neg_beta = a.neg_beta;
+        bi.taps = a.taps;
+        float* cur = qp;
+        float* nxt = mp;
+        for (int t = 0; t < iters; ++t) {
+            const bool last = t == iters - 1;
+            bi.qbar = cur;
+            bi.qbar_out = last ? nullptr : nxt;
+            bi.q_full = last ? q_out : nullptr;
+            st = launch(ctx, kBlurIter, stream, "blur_iteration",
+                        [&] { return launch_blur_iter(bi, k, stream); });
+            if (st != CONVCRF_OK) return st;
+            std::swap(cur, nxt);
+        }
+        return CONVCRF_OK;
+    }
 
     a.C = chunk;
     a.planes = C;

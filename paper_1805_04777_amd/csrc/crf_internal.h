@@ -215,6 +215,50 @@ hipError_t launch_blur_update(const float* m_pooled, const float* unary,
                               int B, int C, int H, int W, int s,
                               hipStream_t stream);
 
+// ---- one fused iteration of the blur path for a 4 x 4 pooling: the pooled
+// message of a work-group's 8 x 8 cells (and the one-cell ring its pixels'
+// bilinear upsampling reads) and the full-resolution update of its 32 x 32
+// pixels in one launch (grid ceil(Wp / 8) x ceil(Hp / 8) x B).
+constexpr int kFusedBlurFactor = 4, kFusedBlurCells = 8;
+struct BlurIterArgs {
+    const float* qbar;    // pooled Q_t [B][C][Hp][Wp]
+    const float* pcol;    // pooled colours [B][3][Hp][Wp]
+    const float* unary;   // U [B][C][H][W], 8-byte aligned
+    const float* mu;      // device C x C compatibility or null (Potts)
+    float* qbar_out;      // pooled Q_{t+1} (when q_full is null)
+    float* q_full;        // Q [B][C][H][W] (8-byte aligned), the last iteration
+    int B, C, H, W, Hp, Wp;
+    int include_center;
+    float center_w;       // K(p, p) = w_app + w_smooth when the centre is included
+    float neg_beta;       // -log2(e) / (2 theta_beta^2)
+    TapTable taps;        // per-offset constants on the pooled grid (step 4)
+};
+// LDS of one work-group: the pooled Q_t and colours over the footprint
+// ((8 + 2 + 2r) cells square), k row partials of a chunk of classes over the
+// 10 x 10 message tile, the message tile, and the compatibility when given.
+// The chunk is the most classes (up to CM) whose partials fit 160 KB with
+// the rest, compatibility included.
+constexpr int blur_iter_chunk(int k, int CM) {
+    const int fs = kFusedBlurCells + 2 + (k - 1), mt = (kFusedBlurCells + 2) * (kFusedBlurCells + 2);
+    const int room = 160 * 1024 / 4 - (CM + 3) * fs * fs - CM * mt - CM * CM;
+    const int ch = room / (k * mt);
+    return ch < 1 ? 1 : (ch > CM ? CM : ch);
+}
+inline size_t blur_iter_lds_bytes(int k, int CM, bool with_compat) {
+    const size_t fs = kFusedBlurCells + 2 + (k - 1), mt = (kFusedBlurCells + 2) * (kFusedBlurCells + 2);
+    return sizeof(float) * ((size_t)(CM + 3) * fs * fs + (size_t)k * blur_iter_chunk(k, CM) * mt +
+                            (size_t)CM * mt + (with_compat ? (size_t)CM * CM : 0));
+}
+hipError_t launch_blur_iter(const BlurIterArgs& a, int k, hipStream_t stream);
+hipError_t launch_blur_iter_k1(const BlurIterArgs& a, hipStream_t stream);
+hipError_t launch_blur_iter_k3(const BlurIterArgs& a, hipStream_t stream);
+hipError_t launch_blur_iter_k5(const BlurIterArgs& a, hipStream_t stream);
+hipError_t launch_blur_iter_k7(const BlurIterArgs& a, hipStream_t stream);
+hipError_t launch_blur_iter_k9(const BlurIterArgs& a, hipStream_t stream);
+hipError_t launch_blur_iter_k11(const BlurIterArgs& a, hipStream_t stream);
+hipError_t launch_blur_iter_k13(const BlurIterArgs& a, hipStream_t stream);
+hipError_t launch_blur_iter_k15(const BlurIterArgs& a, hipStream_t stream);
+
 // ---- learnable smoothness features (the "+T" variant): one update with
 // the smoothness Gaussian on |F_p - F_q|^2 of a feature map F [B][D][H][W]
 // instead of |p - q|^2.  32 x 8 tiles, one pixel per thread.

@@ -228,7 +228,7 @@ def test_negative_smoothness_weight(torch_cuda, crf, oracle_mod, w_smooth):
     # Eq. 4 leaves the sign of the weights to training; a negative
     # smoothness weight lowers every tap's weight by a per-offset constant
     U, I = rand_case(640, 1, 21, 48, 68)
-    for variant, blur in ((0, 1), (1, 1), (0, 2)):
+    for variant, blur in ((0, 1), (1, 1), (0, 2), (0, 4)):
         p = lib_params(filter_size=5, w_smooth=w_smooth, w_app=3.0, variant=variant, blur=blur)
         check(run_gpu(torch_cuda, crf, U, I, p, 3), run_oracle(oracle_mod, U, I, p, 3),
               f"w_smooth={w_smooth} variant={variant} blur={blur}")
@@ -237,7 +237,7 @@ def test_negative_smoothness_weight(torch_cuda, crf, oracle_mod, w_smooth):
 def test_include_center(torch_cuda, crf, oracle_mod):
     U, I = rand_case(600, 1, 21, 40, 40)
     for variant in (0, 1):
-        for blur in ((1, 2) if variant == 0 else (1,)):
+        for blur in ((1, 2, 4) if variant == 0 else (1,)):
             p = lib_params(filter_size=5, include_center=1, variant=variant, blur=blur,
                            w_app=1.5, w_smooth=0.5)
             check(run_gpu(torch_cuda, crf, U, I, p, 3), run_oracle(oracle_mod, U, I, p, 3),
@@ -248,7 +248,8 @@ def test_include_center(torch_cuda, crf, oracle_mod):
                                        (4, 5, 19, 36, 44), (8, 3, 21, 64, 128), (8, 7, 4, 40, 8),
                                        (4, 5, 21, 64, 64), (4, 3, 21, 128, 128), (2, 15, 13, 96, 80),
                                        (4, 5, 13, 32, 48), (8, 5, 19, 64, 72), (2, 9, 21, 32, 48),
-                                       (4, 13, 19, 64, 64)])
+                                       (4, 13, 19, 64, 64), (4, 7, 5, 40, 56), (4, 15, 21, 72, 40),
+                                       (4, 9, 24, 44, 100), (4, 3, 1, 32, 32)])
 def test_blur_shapes(torch_cuda, crf, oracle_mod, s, k, C, H, W):
     U, I = rand_case(700 + s * k + C, 2, C, H, W)
     p = lib_params(filter_size=k, blur=s)
@@ -452,8 +453,9 @@ def test_profiling_counts_launches(torch_cuda, crf):
     assert crf.profile_read("sync_reset")[1] == 1
     assert crf.profile_read("materialised_iter")[1] == 4
     assert crf.profile_read("build_kernel")[1] == 1
-    assert crf.profile_read("blur_message")[1] == 2
-    assert crf.profile_read("blur_update")[1] == 2
+    # 4 x 4 pooling: one fused launch per iteration
+    assert crf.profile_read("blur_iteration")[1] == 2
+    assert crf.profile_read("blur_message")[1] == 0 and crf.profile_read("blur_update")[1] == 0
     assert crf.profile_read("blur_pool")[1] == 2
     assert crf.profile_read("no_such_kernel") == (0.0, 0)
     crf.profile_enable(False)
