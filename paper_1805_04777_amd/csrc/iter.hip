@@ -983,9 +983,10 @@ hipError_t launch_stream(const IterArgs& a, size_t lds, hipStream_t stream) {
 // threads, two pixels each) so that two work-groups share a CU and one's
 // waits overlap the other's arithmetic.  As stream_kernel, but the class
 // chunks cycle through kRingSlots LDS slots (chunk k in slot k mod
-// kRingSlots; kRingSlots - 1 chunks are in flight, chunk k + kRingSlots - 1
-// being issued into the slot of chunk k - 1 once every wave is past it) and
-// each thread's unary comes straight into registers, issued mid-way.
+// kRingSlots; one chunk per slot is issued at the start, then chunk
+// k + kRingSlots - 1 goes into the slot of chunk k - 1 once every wave is
+// past it) and each thread's unary comes straight into registers, issued
+// once the first chunk has landed.
 // FD > 0: learnable smoothness features (the "+T" variant of Sec. 4.2): the
 // FD feature planes are staged beside the colours and the smoothness Gaussian
 // of each weight is taken on the feature distance.
@@ -1080,11 +1081,13 @@ void ring_kernel(const IterArgs a) {
                 lds_dma(rq, voff[s], (int)(c * HW * 4),
                         lds_addr(dst[s] >= 0 ? slot + (c - c_lo) * PLANE + dst[s] : dummy));
     };
-    // AHEAD chunks in flight: the first AHEAD now, chunk k + AHEAD at chunk k
-    constexpr int AHEAD = kRingSlots - 1;
+    // one chunk per slot now (A0 of them); from then on AHEAD = kRingSlots - 1
+    // chunks ahead: chunk k + AHEAD is issued at chunk k, into the slot of
+    // chunk k - 1
+    constexpr int A0 = kRingSlots, AHEAD = kRingSlots - 1;
     static_for([&](auto kc) {
         if constexpr (decltype(kc)::value < NCH) issue_chunk(decltype(kc)::value);
-    }, std::make_integer_sequence<int, AHEAD>{});
+    }, std::make_integer_sequence<int, A0>{});
     // loads of chunks [k0, k0 + n) per wave
     auto chunk_loads = [](int k0, int n) {
         int t = 0;
@@ -1093,7 +1096,7 @@ void ring_kernel(const IterArgs a) {
     };
 
     // ---- colours landed: the window weights of both pixels, all rows
-    __builtin_amdgcn_s_waitcnt(vm_wait(chunk_loads(0, AHEAD)));
+    __builtin_amdgcn_s_waitcnt(vm_wait(chunk_loads(0, A0)));
     __syncthreads();
     float w[K][P][K];
     {
@@ -1155,22 +1158,26 @@ void ring_kernel(const IterArgs a) {
 #pragma unroll
         for (int c = 0; c < CM; ++c) acc[i][c] = 0.f;
     // the unary of this thread's pixels goes straight into registers; it is
-    // needed only by the epilogue, so its loads are issued at chunk UK (after
-    // that chunk's own issue), which keeps them out of the launch's opening
-    // burst of colour and class-plane loads
-    constexpr int UK = NCH > 3 ? 1 : 0;
+    // needed only by the epilogue, so its loads are issued once chunk UK = 0
+    // has landed, which keeps them out of the launch's opening burst of
+    // colour and class-plane loads
+    constexpr int UK = 0;
     float u[P][CM];
     static_for([&](auto kc) {
         constexpr int k = decltype(kc)::value;
         constexpr int c_lo = k * CH;
         constexpr int c_hi = (k + 1) * CH < CM ? (k + 1) * CH : CM;
-        // chunk k landed (the chunks after it that are in flight, and the
-        // unary when it went out after chunk k, may not have); every wave is
-        // past chunk k - 1, whose slot chunk k + AHEAD takes
-        __builtin_amdgcn_s_waitcnt(vm_wait(chunk_loads(k + 1, AHEAD - 1) +
-                                           (UK < k && k <= UK + AHEAD ? CM : 0)));
+        // chunk k landed (the chunks issued after it, up to chunk `last`,
+        // and the unary when it went out after chunk k, may not have); every
+        // wave is past chunk k - 1, whose slot chunk k + AHEAD takes.  Chunk
+        // k was issued at chunk `sk` (-1: at the start).
+        constexpr int last0 = k == 0 ? A0 - 1 : (A0 - 1 > k - 1 + AHEAD ? A0 - 1 : k - 1 + AHEAD);
+        constexpr int last = last0 < NCH - 1 ? last0 : NCH - 1;
+        constexpr int sk = k < A0 ? -1 : k - AHEAD;
+        __builtin_amdgcn_s_waitcnt(vm_wait(chunk_loads(k + 1, last - k) +
+                                           (sk <= UK && UK < k ? CM : 0)));
         __syncthreads();
-        if constexpr (k + AHEAD < NCH) issue_chunk(k + AHEAD);
+        if constexpr (k + AHEAD < NCH && k + AHEAD > last) issue_chunk(k + AHEAD);
         if constexpr (k == UK) {
             const float* up = a.unary + (size_t)b * CM * HW + (size_t)(pix_ok ? y : 0) * W +
                               (pix_ok ? xb : 0);
