@@ -285,7 +285,11 @@ hipError_t launch_ring(const IterArgs& a, int k, hipStream_t s) {
     switch (k) {
         case 3: return launch_ring_k3(a, s);
         case 5: return launch_ring_k5(a, s);
-        case 7: return launch_ring_k7(a, s);
+        case 7: {
+            // Potts without a centre tap or features: the quad form
+            const hipError_t e = launch_quad_k7(a, s);
+            return e == hipErrorNotSupported ? launch_ring_k7(a, s) : e;
+        }
         default: return hipErrorNotSupported;
     }
 }

@@ -110,6 +110,12 @@ constexpr int kRingRows = 8, kRingSlots = 3;
 constexpr int ring_plane(int k) {
     return ((kRingRows + k - 1) * iter_lds_stride(k, 2, kStreamTW) + 63) / 64 * 64;
 }
+// The quad form of the k = 7 ring update (lane pairs on 4-pixel quads)
+// reads its staged rows with 16-byte LDS reads, so its row stride is padded
+// to a multiple of 4 floats; its plane is the same size as ring_plane(7).
+constexpr int kQuadStride = 72;
+constexpr int quad_plane() { return ((kRingRows + 6) * kQuadStride + 63) / 64 * 64; }
+static_assert(quad_plane() == ring_plane(7), "the quad update shares the ring's LDS plan");
 inline size_t ring_lds_bytes(int k, int C, int CH, bool with_compat, int D = 0) {
     return sizeof(float) * ((size_t)(kRingSlots * CH + 3 + D) * ring_plane(k) +
                             (with_compat ? ((size_t)C * C + 63) / 64 * 64 : 0) + 256);
@@ -177,6 +183,9 @@ CONVCRF_DECLARE_ITER(11)
 CONVCRF_DECLARE_ITER(13)
 CONVCRF_DECLARE_ITER(15)
 #undef CONVCRF_DECLARE_ITER
+// The k = 7 ring update in its quad form (Potts, no centre tap, no features;
+// C = 19 or 21); hipErrorNotSupported outside that.
+hipError_t launch_quad_k7(const IterArgs& a, hipStream_t stream);
 
 // Fill n words with zero (the flags of a resident launch: a kernel, not a
 // memset, so that the sequence may be captured in a graph).

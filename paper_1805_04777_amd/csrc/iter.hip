@@ -1262,6 +1262,313 @@ hipError_t launch_ring(const IterArgs& a, hipStream_t stream) {
     return hipGetLastError();
 }
 
+// ------------------------------------------------- quad update (k = 7, Potts)
+// Rounds 2..T of the k = 7 update with Potts compatibility, on the ring's
+// tiles, staging and class-chunk ring, with a thread layout that cuts the
+// LDS bytes of the message (which bound ring_kernel's message loop): a pair
+// of lanes shares four horizontally adjacent pixels.  The even lane applies
+// window rows 0, 1, 2 and the left half of row 3, the odd lane rows 4, 5, 6
+// and the right half of row 3: 24 taps each, the centre excluded; each lane
+// picks its per-offset constants once per tap.  Per (class, window row) a
+// lane reads 10 staged floats (rows
+// padded to 16 bytes: two 16-byte reads and an 8-byte one) for 28 FMAs,
+// where the two-pixel layout reads 8 for 14.  After each chunk the pair adds
+// its two partial messages with one DPP lane swap per class and pixel: the
+// even lane keeps pixels 0 and 1, the odd lane pixels 2 and 3, and each then
+// runs ring_kernel's epilogue on its two.
+template <int N>
+__device__ __forceinline__ void lds_row16(const float* p, float (&v)[N]) {
+    static_assert(N % 2 == 0, "row length must be even");
+#pragma unroll
+    for (int j = 0; j + 4 <= N; j += 4) {
+        const float4 t = *reinterpret_cast<const float4*>(p + j);
+        v[j] = t.x;
+        v[j + 1] = t.y;
+        v[j + 2] = t.z;
+        v[j + 3] = t.w;
+    }
+    if constexpr (N % 4 == 2) {
+        const float2 t = *reinterpret_cast<const float2*>(p + N - 2);
+        v[N - 2] = t.x;
+        v[N - 1] = t.y;
+    }
+}
+
+// x from the other lane of the pair (lanes 2m and 2m + 1)
+__device__ __forceinline__ float pair_swap(float x) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));
+}
+
+// One chunk of the quad message, classes [C_LO, C_HI): step t applies window
+// row t % 4 of class C_LO + t / 4 (rows 0..2 full, 3 the half row), read
+// from LDS two steps ahead, to the lane's four pixels.
+template <int PLANE, int LS, int C_LO, int C_HI>
+__device__ __forceinline__ void quad_chunk(const float* Qs, unsigned rbase, unsigned hbase,
+                                           const float (&w)[4][4][7], float (&acc)[4][C_HI - C_LO]) {
+    constexpr int NC = C_HI - C_LO, nsteps = NC * 4, kDepth = 3;
+    float qr[kDepth][10];
+    // per class one base for the full rows (rows at immediate offsets from
+    // it) and one for the half row, opaque to the compiler so that it does
+    // not fold them into per-step address registers
+    const float* qb[NC];
+    const float* hb[NC];
+#pragma unroll
+    for (int i = 0; i < NC; ++i) {
+        unsigned off = (unsigned)((C_LO + i) * PLANE) + rbase;
+        unsigned hoff = (unsigned)((C_LO + i) * PLANE) + hbase;
+        asm volatile("" : "+v"(off), "+v"(hoff));
+        qb[i] = Qs + off;
+        hb[i] = Qs + hoff;
+    }
+    auto rd = [&](int t, float (&v)[10]) {
+        const float* const q = t % 4 == 3 ? hb[t / 4] : qb[t / 4] + (t % 4) * LS;
+        if (t % 4 == 3) {
+            float h[6];
+            lds_row16<6>(q, h);
+#pragma unroll
+            for (int j = 0; j < 6; ++j) v[j] = h[j];
+        } else {
+            lds_row16<10>(q, v);
+        }
+    };
+#pragma unroll
+    for (int t = 0; t < kDepth - 1; ++t)
+        if (t < nsteps) rd(t, qr[t]);
+#pragma unroll
+    for (int t = 0; t < nsteps; ++t) {
+        const int nx = t + kDepth - 1;
+        if (nx < nsteps) rd(nx, qr[nx % kDepth]);
+        const int c = t / 4, j = t % 4;
+        const int ntap = j == 3 ? 3 : 7;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int d = 0; d < ntap; ++d) acc[i][c] = fmaf(w[j][i][d], qr[t % kDepth][i + d], acc[i][c]);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+template <int CM, int CH>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void quad_kernel(const IterArgs a) {
+    constexpr int K = 7, R = 3;
+    constexpr int TW = kStreamTW, ROWS = kRingRows, NWAVE = 4;
+    constexpr int LW = TW + 2 * R, LH = ROWS + 2 * R;
+    constexpr int LS = kQuadStride;
+    constexpr int PLANE = quad_plane();
+    constexpr int NI = PLANE / 64;               // 64-float loads per plane
+    constexpr int NJ = (NI + NWAVE - 1) / NWAVE; // per wave and plane
+    constexpr int NCH = (CM + CH - 1) / CH;
+    constexpr unsigned kOob = 0x80000000u;
+    static_assert(4 * 16 == TW && 2 * 16 * ROWS == 256, "16 pixel quads per row, a lane pair each");
+    extern __shared__ float4 smem4[];
+    float* const smem = reinterpret_cast<float*>(smem4);
+    float* const Qs = smem;                              // [kRingSlots][CH][PLANE]
+    float* const Cs = smem + kRingSlots * CH * PLANE;    // [3][PLANE]
+    float* const dummy = Cs + 3 * PLANE;                 // one 256-float row
+    const unsigned lds0 = (unsigned)(size_t)(__attribute__((address_space(3))) float*)smem;
+    auto lds_addr = [&](const float* p) { return lds0 + (unsigned)((p - smem) * 4); };
+
+    const int H = a.H, W = a.W;
+    const int tile = xcd_tile(blockIdx.x, a.ntiles);
+    const int b = tile / a.tiles_per_img;
+    const int trem = tile - b * a.tiles_per_img;
+    const int tyi = trem / a.tiles_x;
+    const int y0 = tyi * ROWS;
+    const int x0 = (trem - tyi * a.tiles_x) * TW;
+    const size_t HW = (size_t)H * W;
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int half = tid & 1, ty = tid >> 5;
+    const int cq = 4 * ((tid >> 1) & 15);        // staged column of pixel 0's window
+    const int y = y0 + ty, xo = x0 + cq + 2 * half;   // the lane's two output pixels
+    const bool pix_ok = y < H && x0 + cq < W;    // W % 4 == 0: all four or none
+
+    // ---- colours, then the first chunks of Q_t (as ring_kernel)
+    unsigned voff[NJ];
+    int dst[NJ];
+#pragma unroll
+    for (int s = 0; s < NJ; ++s) {
+        const int j = wave + NWAVE * s;
+        const int f = j * 64 + lane;
+        const int r = f / LS, col = f - (f / LS) * LS;
+        const int gy = y0 - R + r, gx = x0 - R + col;
+        const bool in = j < NI && f < LH * LS && col < LW && gy >= 0 && gy < H && gx >= 0 && gx < W;
+        voff[s] = in ? (unsigned)((gy * W + gx) * 4) : kOob;
+        dst[s] = j < NI ? j * 64 : -1;
+    }
+    const rsrc_t rf = buffer_rsrc(a.feat + (size_t)b * 3 * HW, (unsigned)(3 * HW * 4));
+    const rsrc_t rq = buffer_rsrc(a.src + (size_t)b * CM * HW, (unsigned)(CM * HW * 4));
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch)
+#pragma unroll
+        for (int s = 0; s < NJ; ++s)
+            lds_dma(rf, voff[s], (int)(ch * HW * 4),
+                    lds_addr(dst[s] >= 0 ? Cs + ch * PLANE + dst[s] : dummy));
+    auto issue_chunk = [&](int k) {
+        const int c_lo = k * CH, c_hi = (k + 1) * CH < CM ? (k + 1) * CH : CM;
+        float* const slot = Qs + (k % kRingSlots) * CH * PLANE;
+        for (int c = c_lo; c < c_hi; ++c)
+#pragma unroll
+            for (int s = 0; s < NJ; ++s)
+                lds_dma(rq, voff[s], (int)(c * HW * 4),
+                        lds_addr(dst[s] >= 0 ? slot + (c - c_lo) * PLANE + dst[s] : dummy));
+    };
+    constexpr int A0 = kRingSlots, AHEAD = kRingSlots - 1;
+    static_for([&](auto kc) {
+        if constexpr (decltype(kc)::value < NCH) issue_chunk(decltype(kc)::value);
+    }, std::make_integer_sequence<int, A0>{});
+    auto chunk_loads = [](int k0, int n) {
+        int t = 0;
+        for (int j = k0; j < k0 + n; ++j) t += stream_chunk_loads(j, CM, CH, NJ);
+        return t;
+    };
+
+    // this lane's window rows: full rows R (half + 1) + j, j < R, at
+    // rbase + j LS, and the half row R at hbase
+    const unsigned rbase = (unsigned)((ty + (R + 1) * half) * LS + cq);
+    const unsigned hbase = (unsigned)((ty + R) * LS + cq + (R + 1) * half);
+
+    // ---- colours landed: the weights of the lane's 4 x 24 taps
+    __builtin_amdgcn_s_waitcnt(vm_wait(chunk_loads(0, A0)));
+    __syncthreads();
+    float w[4][4][K];
+    {
+        float own[3][4];
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch) {
+            float r[10];
+            lds_row16<10>(Cs + ch * PLANE + (ty + R) * LS + cq, r);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) own[ch][i] = r[R + i];
+        }
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+            float nc[3][10];
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) lds_row16<10>(Cs + ch * PLANE + rbase + j * LS, nc[ch]);
+#pragma unroll
+            for (int dx = 0; dx < K; ++dx) {
+                // |d|^2 of the tap for the even lane (row j) and the odd one (row R + 1 + j)
+                const int ne = (dx - R) * (dx - R) + (R - j) * (R - j);
+                const int no = (dx - R) * (dx - R) + (j + 1) * (j + 1);
+                float ae = a.taps.app_log2[ne], ao = a.taps.app_log2[no];
+                float se = a.taps.smooth[ne], so = a.taps.smooth[no];
+                asm volatile("" : "+s"(ae), "+s"(ao), "+s"(se), "+s"(so));
+                const float ca = half ? ao : ae;
+                const float cs = half ? so : se;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float d0 = own[0][i] - nc[0][i + dx];
+                    const float d1 = own[1][i] - nc[1][i + dx];
+                    const float d2 = own[2][i] - nc[2][i + dx];
+                    const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
+                    w[j][i][dx] = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, ca)) + cs;
+                }
+            }
+        }
+        // the half row: taps dx = d (even lane) or R + 1 + d (odd lane)
+        float hc[3][6];
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch) lds_row16<6>(Cs + ch * PLANE + hbase, hc[ch]);
+#pragma unroll
+        for (int d = 0; d < R; ++d) {
+            const int nl = (R - d) * (R - d), nr = (d + 1) * (d + 1);
+            // both constants as scalars first, then the lane's choice
+            float al = a.taps.app_log2[nl], ar = a.taps.app_log2[nr];
+            float sl = a.taps.smooth[nl], sr = a.taps.smooth[nr];
+            asm volatile("" : "+s"(al), "+s"(ar), "+s"(sl), "+s"(sr));
+            const float ca = half ? ar : al;
+            const float cs = half ? sr : sl;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float d0 = own[0][i] - hc[0][i + d];
+                const float d1 = own[1][i] - hc[1][i + d];
+                const float d2 = own[2][i] - hc[2][i + d];
+                const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
+                w[3][i][d] = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, ca)) + cs;
+            }
+        }
+    }
+
+    // keep the weights' arithmetic above the chunk loop, where the unary's
+    // registers are not yet live
+    __builtin_amdgcn_sched_barrier(0);
+    // the message of the lane's two pixels, completed chunk by chunk; the
+    // unary (Potts: Z = U + M) is loaded at the last chunk, where it first
+    // has registers to land in
+    float fin[2][CM];
+    float u[2][CM];
+    constexpr int UK = NCH - 1;
+    static_for([&](auto kc) {
+        constexpr int k = decltype(kc)::value;
+        constexpr int c_lo = k * CH;
+        constexpr int c_hi = (k + 1) * CH < CM ? (k + 1) * CH : CM;
+        constexpr int last0 = k == 0 ? A0 - 1 : (A0 - 1 > k - 1 + AHEAD ? A0 - 1 : k - 1 + AHEAD);
+        constexpr int last = last0 < NCH - 1 ? last0 : NCH - 1;
+        constexpr int sk = k < A0 ? -1 : k - AHEAD;
+        __builtin_amdgcn_s_waitcnt(vm_wait(chunk_loads(k + 1, last - k) +
+                                           (sk <= UK && UK < k ? CM : 0)));
+        __syncthreads();
+        if constexpr (k + AHEAD < NCH && k + AHEAD > last) issue_chunk(k + AHEAD);
+        if constexpr (k == UK) {
+            // buffer loads: one lane offset and a scalar offset per class, so
+            // that no 64-bit address is held per class
+            const __amdgpu_buffer_rsrc_t ru = __builtin_amdgcn_make_buffer_rsrc(
+                (void*)(a.unary + (size_t)b * CM * HW), (short)0, (int)(CM * HW * 4), 0x00020000);
+            const int uoff = pix_ok ? (y * W + xo) * 4 : 0;
+#pragma unroll
+            for (int c = 0; c < CM; ++c) {
+                const auto t = __builtin_amdgcn_raw_buffer_load_b64(ru, uoff, (int)(c * HW * 4), 0);
+                u[0][c] = __int_as_float((int)t[0]);
+                u[1][c] = __int_as_float((int)t[1]);
+            }
+        }
+        float acc[4][c_hi - c_lo];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int c = 0; c < c_hi - c_lo; ++c) acc[i][c] = 0.f;
+        const float* const qk = Qs + (k % kRingSlots) * CH * PLANE;
+        quad_chunk<PLANE, LS, c_lo, c_hi>(qk - c_lo * PLANE, rbase, hbase, w, acc);
+#pragma unroll
+        for (int c = 0; c < c_hi - c_lo; ++c)
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const float mine = half ? acc[2 + i][c] : acc[i][c];
+                const float send = half ? acc[i][c] : acc[2 + i][c];
+                fin[i][c_lo + c] = mine + pair_swap(send);
+                // materialised here: sunk to the epilogue, the add would keep
+                // both of its operands live through the remaining chunks
+                asm volatile("" : "+v"(fin[i][c_lo + c]));
+            }
+    }, std::make_integer_sequence<int, NCH>{});
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));     // the unary
+    if (!pix_ok) return;
+
+    // ---- Potts: softmax(U + M), store Q_{t+1}
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+#pragma unroll
+        for (int c = 0; c < CM; ++c) fin[i][c] += u[i][c];
+        softmax_regs<CM, true>(fin[i], CM);
+    }
+    float* __restrict__ qd = a.dst + (size_t)b * CM * HW + (size_t)y * W + xo;
+#pragma unroll
+    for (int c = 0; c < CM; ++c)
+        *reinterpret_cast<float2*>(qd + c * HW) = make_float2(fin[0][c], fin[1][c]);
+}
+
+template <int CM, int CH>
+hipError_t launch_quad(const IterArgs& a, hipStream_t stream) {
+    auto fn = quad_kernel<CM, CH>;
+    hipError_t e = allow_full_lds(fn);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fn, dim3(a.ntiles), dim3(256), ring_lds_bytes(7, CM, CH, false, 0), stream, a);
+    return hipGetLastError();
+}
+
 // ---------------------------------------------------- resident streamed form
 // All T iterations in one cooperative launch on the tiles of stream_kernel
 // (every tile's work-group co-resident).  The window weights (the colours do
@@ -1740,6 +2047,21 @@ hipError_t CRF_CAT(launch_ring_k, CRF_K)(const IterArgs& a, hipStream_t stream) 
         }
     }
 }
+
+#if CRF_K == 7
+// Quad updates: the ring's rounds 2..T at k = 7 with Potts compatibility,
+// no centre tap and no learnable features.
+hipError_t launch_quad_k7(const IterArgs& a, hipStream_t stream) {
+    if (a.mode != kModeUpdate || a.first || a.planes != a.C || !a.vec || (a.W & 3) || a.mu ||
+        a.include_center || a.sfeat || (size_t)a.C * a.H * a.W * 4 >= (1ull << 31))
+        return hipErrorNotSupported;
+    switch (a.C) {
+        case 19: return launch_quad<19, 4>(a, stream);
+        case 21: return launch_quad<21, 3>(a, stream);
+        default: return hipErrorNotSupported;
+    }
+}
+#endif
 
 // Resident launches are built for the two-pixel, one-group tile of k <= 7
 // and Potts compatibility.
