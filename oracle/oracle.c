@@ -36,6 +36,11 @@
  *     are s times the grid offsets), then bilinearly upsampled with
  *     half-pixel centres and edge clamping before the compatibility step
  *                                                             (Sec. 4.2)
+ *   - blur together with learnable smoothness features: the features are
+ *     pooled like the colours (s x s block means, once per image) and the
+ *     smoothness Gaussian takes the squared distance of the pooled features
+ *     of the two cells; features equal to the positions pool to the block
+ *     centres, which reproduces the pooled Eq. 4 above
  */
 #include <math.h>
 #include <stdlib.h>
@@ -239,7 +244,7 @@ void oracle_upsample(const double *X, int nch, int Hp, int Wp, int s, double *Y)
  * I: [B][3][H][W] (RGB on its own 0..255 scale).  Returns 0 on success, -1 on
  * an argument the definition does not cover. */
 /* F: learnable smoothness features [B][d][H][W], or NULL for the positions
- * (no blur with F). */
+ * (with blur, pooled to the s x s cells like the colours). */
 int oracle_meanfield_f(const double *U, const double *I, const double *F, int d, int B,
                        int C, int H, int W, const oracle_params *p, const double *mu, int T,
                        double *Q)
@@ -248,7 +253,7 @@ int oracle_meanfield_f(const double *U, const double *I, const double *F, int d,
     if (p->filter_size < 1 || (p->filter_size & 1) == 0) return -1;
     const int s = p->blur;
     if (s < 1 || H % s || W % s) return -1;
-    if (F && (d < 1 || s != 1)) return -1;
+    if (F && d < 1) return -1;
     const long HW = (long)H * W;
     const int Hp = H / s, Wp = W / s;
     const long HWp = (long)Hp * Wp;
@@ -258,18 +263,21 @@ int oracle_meanfield_f(const double *U, const double *I, const double *F, int d,
     double *Qp = s > 1 ? (double *)malloc(sizeof(double) * C * HWp) : NULL;
     double *Mp = s > 1 ? (double *)malloc(sizeof(double) * C * HWp) : NULL;
     double *Ip = s > 1 ? (double *)malloc(sizeof(double) * 3 * HWp) : NULL;
+    double *Fp = s > 1 && F ? (double *)malloc(sizeof(double) * d * HWp) : NULL;
 
     for (int b = 0; b < B; ++b) {
         const double *Ub = U + (long)b * C * HW;
         const double *Ib = I + (long)b * 3 * HW;
+        const double *Fb = F ? F + (long)b * d * HW : NULL;
         oracle_softmax(Ub, C, H, W, Qt);
         if (s > 1) oracle_avgpool(Ib, 3, H, W, s, Ip);
+        if (Fp) oracle_avgpool(Fb, d, H, W, s, Fp);
         for (int t = 0; t < T; ++t) {
             if (s == 1) {
-                message_f(Qt, Ib, F ? F + (long)b * d * HW : NULL, d, C, H, W, p, 1.0, M);
+                message_f(Qt, Ib, Fb, d, C, H, W, p, 1.0, M);
             } else {
                 oracle_avgpool(Qt, C, H, W, s, Qp);
-                oracle_message(Qp, Ip, C, Hp, Wp, p, (double)s, Mp);
+                message_f(Qp, Ip, Fp, d, C, Hp, Wp, p, (double)s, Mp);
                 oracle_upsample(Mp, C, Hp, Wp, s, M);
             }
             oracle_update(Ub, M, mu, C, HW, Qt);
@@ -281,6 +289,7 @@ int oracle_meanfield_f(const double *U, const double *I, const double *F, int d,
     free(Qp);
     free(Mp);
     free(Ip);
+    free(Fp);
     return 0;
 }
 
@@ -509,7 +518,7 @@ int oracle_meanfield_backward_f(const double *U, const double *I, const double *
     if (B < 0 || C < 1 || H < 1 || W < 1 || T < 0 || !p) return -1;
     if (p->filter_size < 1 || (p->filter_size & 1) == 0) return -1;
     const int s = p->blur;
-    if (s < 1 || H % s || W % s || (F && s != 1)) return -1;
+    if (s < 1 || H % s || W % s) return -1;
     if (C > 64 || (F && d < 1)) return -1;
     const long HW = (long)H * W;
     const long n = (long)C * HW;
@@ -528,6 +537,9 @@ int oracle_meanfield_backward_f(const double *U, const double *I, const double *
     double *Ip = s > 1 ? (double *)malloc(sizeof(double) * 3 * Hp * Wp) : NULL;
     double *dMp = s > 1 ? (double *)malloc(sizeof(double) * np) : NULL;
     double *dQp = s > 1 ? (double *)malloc(sizeof(double) * np) : NULL;
+    /* blur with features: the pooled features and their derivative */
+    double *Fp = s > 1 && F ? (double *)malloc(sizeof(double) * (size_t)d * Hp * Wp) : NULL;
+    double *dFp = s > 1 && F ? (double *)malloc(sizeof(double) * (size_t)d * Hp * Wp) : NULL;
     if (dmu) memset(dmu, 0, sizeof(double) * (size_t)C * C);
     if (dparams) memset(dparams, 0, sizeof(double) * 5);
 
@@ -538,15 +550,17 @@ int oracle_meanfield_backward_f(const double *U, const double *I, const double *
         double *dFb = F && dF ? dF + (long)b * d * HW : NULL;
         double *dUb = dU + (long)b * n;
         if (dFb) memset(dFb, 0, sizeof(double) * (size_t)d * HW);
+        if (dFp) memset(dFp, 0, sizeof(double) * (size_t)d * Hp * Wp);
         /* forward, keeping every Q^t and M^t (and the pooled Q^t with blur) */
         oracle_softmax(Ub, C, H, W, Qs);
         if (s > 1) oracle_avgpool(Ib, 3, H, W, s, Ip);
+        if (Fp) oracle_avgpool(Fb, d, H, W, s, Fp);
         for (int t = 0; t < T; ++t) {
             if (s == 1) {
                 message_f(Qs + (long)t * n, Ib, Fb, d, C, H, W, p, 1.0, Ms + (long)t * n);
             } else {
                 oracle_avgpool(Qs + (long)t * n, C, H, W, s, Qps + (long)t * np);
-                message_f(Qps + (long)t * np, Ip, NULL, 0, C, Hp, Wp, p, (double)s, Mp);
+                message_f(Qps + (long)t * np, Ip, Fp, d, C, Hp, Wp, p, (double)s, Mp);
                 oracle_upsample(Mp, C, Hp, Wp, s, Ms + (long)t * n);
             }
             oracle_update(Ub, Ms + (long)t * n, mu, C, HW, Qs + (long)(t + 1) * n);
@@ -591,13 +605,18 @@ int oracle_meanfield_backward_f(const double *U, const double *I, const double *
                  * upsampling, the pooled message, then the pooling */
                 upsample_transpose(dM, C, Hp, Wp, s, dMp);
                 if (dparams)
-                    message_param_grad(dMp, Qps + (long)t * np, Ip, NULL, 0, C, Hp, Wp, p,
+                    message_param_grad(dMp, Qps + (long)t * np, Ip, Fp, d, C, Hp, Wp, p,
                                        (double)s, dparams);
-                message_transpose(dMp, Ip, NULL, 0, C, Hp, Wp, p, (double)s, dQp);
+                if (dFb)
+                    message_feature_grad(dMp, Qps + (long)t * np, Fp, d, C, Hp, Wp, p, dFp);
+                message_transpose(dMp, Ip, Fp, d, C, Hp, Wp, p, (double)s, dQp);
                 avgpool_transpose(dQp, C, H, W, s, dQprev);
             }
             memcpy(dQ, dQprev, sizeof(double) * n);
         }
+        /* blur: dL/dF is the transpose of the pooling applied to the
+         * derivative with respect to the pooled features */
+        if (dFb && s > 1) avgpool_transpose(dFp, d, H, W, s, dFb);
         for (long i = 0; i < HW; ++i) {
             double dz[64];
             softmax_adjoint_pixel(Qs + i, dQ + i, HW, dz, 1, C);
@@ -615,6 +634,8 @@ int oracle_meanfield_backward_f(const double *U, const double *I, const double *
     free(Ip);
     free(dMp);
     free(dQp);
+    free(Fp);
+    free(dFp);
     return 0;
 }
 

@@ -8,6 +8,11 @@ every window, which a very wide theta_gamma reproduces; scaling the features
 and theta_gamma together changes nothing.  Derivative: central finite
 differences of the forward for every feature entry and, with features
 present, for the unaries, the compatibility and the Eq. 4 parameters.
+
+With blur (Sec. 4.2) the features are pooled to the s x s cells like the
+colours: position features then reproduce the pooled kernel, constant ones a
+flat smoothness term, only cell means matter, and the derivative (finite
+differences again) is the same for every pixel of a cell.
 """
 import numpy as np
 import pytest
@@ -113,7 +118,96 @@ def test_position_features_give_the_same_other_derivatives():
         np.testing.assert_allclose(x, y, rtol=1e-11, atol=1e-12)
 
 
-def test_features_with_blur_are_rejected():
-    U, I, G, F, _ = _problem(9, 1, 2, 4, 4)
-    with pytest.raises(ValueError):
-        orc.meanfield(U, I, orc.OracleParams(filter_size=3, blur=2), 1, features=F)
+# ---- blur together with learnable features: the features are pooled to the
+# s x s cells like the colours, and the smoothness Gaussian takes the pooled
+# features' distance between cells.
+
+def _blur_problem(seed, B, C, H, W, d=2):
+    U, I, G, F, pos = _problem(seed, B, C, H, W, d=max(d, 2))
+    return U, I, G, np.ascontiguousarray(F[:, :d]), pos
+
+
+@pytest.mark.parametrize("s,k,center", [(2, 3, False), (2, 5, True), (4, 3, False)])
+def test_blur_position_features_reproduce_the_pooled_kernel(s, k, center):
+    # block means of the pixel coordinates are the cell centres, whose
+    # differences are s times the grid offsets: the pooled Eq. 4
+    U, I, _, _, pos = _blur_problem(11, 2, 3, 4 * s, 3 * s)
+    p = orc.OracleParams(filter_size=k, blur=s, include_center=center, **VALS)
+    np.testing.assert_allclose(orc.meanfield(U, I, p, 3, features=pos), orc.meanfield(U, I, p, 3),
+                               rtol=0, atol=1e-13)
+
+
+def test_blur_constant_features_make_the_smoothness_term_flat():
+    U, I, _, _, pos = _blur_problem(12, 1, 3, 8, 12)
+    p = orc.OracleParams(filter_size=5, blur=2, **VALS)
+    wide = orc.OracleParams(filter_size=5, blur=2, **dict(VALS, theta_gamma=1e9))
+    np.testing.assert_allclose(orc.meanfield(U, I, p, 2, features=np.full_like(pos, -3.0)),
+                               orc.meanfield(U, I, wide, 2), rtol=0, atol=1e-12)
+
+
+def test_blur_features_see_only_cell_means():
+    # moving feature mass inside a cell leaves the pooled features, and so Q,
+    # unchanged
+    U, I, _, F, _ = _blur_problem(13, 1, 3, 8, 8)
+    p = orc.OracleParams(filter_size=3, blur=2, **VALS)
+    F2 = F.copy()
+    F2[:, :, 0::2, 0::2] += 0.7
+    F2[:, :, 1::2, 1::2] -= 0.7
+    np.testing.assert_allclose(orc.meanfield(U, I, p, 2, features=F2),
+                               orc.meanfield(U, I, p, 2, features=F), rtol=0, atol=1e-13)
+    F3 = F.copy()
+    F3[:, :, 0, 0] += 0.7                 # one cell's mean moves: Q moves
+    assert np.abs(orc.meanfield(U, I, p, 2, features=F3) -
+                  orc.meanfield(U, I, p, 2, features=F)).max() > 1e-6
+
+
+BLUR_CASES = [(21, 1, 3, 6, 8, 2, 3, 2, False, False, 2), (22, 2, 2, 8, 8, 4, 3, 2, True, True, 1),
+              (23, 1, 2, 6, 4, 2, 5, 1, False, True, 3)]
+
+
+@pytest.mark.parametrize("seed,B,C,H,W,s,k,T,center,gen_mu,d", BLUR_CASES)
+def test_blur_feature_gradient_matches_finite_differences(seed, B, C, H, W, s, k, T, center,
+                                                          gen_mu, d):
+    U, I, G, F, _ = _blur_problem(seed, B, C, H, W, d)
+    mu = np.random.default_rng(seed).normal(0.3, 0.5, (C, C)) if gen_mu else None
+    p = orc.OracleParams(filter_size=k, blur=s, include_center=center, **VALS)
+    dU, dmu, dp, dF = orc.meanfield_backward(U, I, p, T, G, compat=mu, features=F)
+    h = 1e-6
+    fd = np.empty_like(F)
+    for idx in np.ndindex(F.shape):
+        def f(v):
+            Fp = F.copy()
+            Fp[idx] = v
+            return _loss(U, I, p, T, G, mu, Fp)
+        fd[idx] = (f(F[idx] + h) - f(F[idx] - h)) / (2 * h)
+    assert np.abs(fd).max() > 1e-4
+    np.testing.assert_allclose(dF, fd, rtol=0, atol=1e-7 * max(1.0, np.abs(fd).max()))
+    # every pixel of a cell gets the same derivative (the pooling's transpose)
+    for b in range(B):
+        for c in range(d):
+            cells = dF[b, c].reshape(H // s, s, W // s, s)
+            assert np.ptp(cells, axis=(1, 3)).max() <= 1e-15 * max(1.0, np.abs(dF).max())
+    for idx in list(np.ndindex(U.shape))[::5]:
+        def g(v):
+            Up = U.copy()
+            Up[idx] = v
+            return _loss(Up, I, p, T, G, mu, F)
+        fdu = (g(U[idx] + 1e-5) - g(U[idx] - 1e-5)) / 2e-5
+        assert abs(fdu - dU[idx]) <= 1e-7 * max(1.0, np.abs(dU).max())
+    for j, name in enumerate(orc.PARAM_NAMES):
+        hh = 1e-6 * VALS[name]
+        def q(v):
+            return _loss(U, I, orc.OracleParams(filter_size=k, blur=s, include_center=center,
+                                                **dict(VALS, **{name: v})), T, G, mu, F)
+        fdp = (q(VALS[name] + hh) - q(VALS[name] - hh)) / (2 * hh)
+        assert abs(fdp - dp[j]) <= 2e-6 * abs(fdp) + 1e-9, (name, fdp, dp[j])
+
+
+def test_blur_position_features_give_the_same_other_derivatives():
+    U, I, G, _, pos = _blur_problem(24, 1, 3, 8, 6)
+    mu = np.random.default_rng(24).normal(0.3, 0.5, (3, 3))
+    p = orc.OracleParams(filter_size=3, blur=2, **VALS)
+    a = orc.meanfield_backward(U, I, p, 2, G, compat=mu)
+    b = orc.meanfield_backward(U, I, p, 2, G, compat=mu, features=pos)
+    for x, y in zip(a, b[:3]):
+        np.testing.assert_allclose(x, y, rtol=1e-11, atol=1e-12)
