@@ -92,8 +92,10 @@ def algorithmic_per_launch(kname: str, wl, D: int = 0):
     s2 = wl.blur * wl.blur
     npx = px // s2
     if kname == "blur_message":
-        # pooled grid: read pooled Q and features, write pooled message
-        return (2 * C * (k * k - 1) + 12 * (k * k - 1)) * npx, (8 * C + 12) * npx
+        # pooled grid: read pooled Q and colours (and D pooled feature planes,
+        # whose Gaussian costs 3D + 2 per tap), write pooled message
+        fg = 3 * D + 2 if D else 0
+        return (2 * C + 12 + fg) * (k * k - 1) * npx, (8 * C + 12 + 4 * D) * npx
     if kname == "blur_update":
         # per pixel: bilinear sample of C pooled messages (3 FMA each), unary
         # add, softmax, s*s average; reads U, writes the pooled Q (T - 1
@@ -120,9 +122,11 @@ def algorithmic_per_launch(kname: str, wl, D: int = 0):
     # reverse mode (compatibility and kernel-parameter derivatives requested)
     taps = k * k - 1
     if kname == "bwd_message" and wl.blur > 1:
-        # on the pooled grid (the derivative of the blur variant): as above
+        # on the pooled grid (the derivative of the blur variant): as below
         # per pooled cell
         npx = px // (wl.blur * wl.blur)
+        if D:
+            return ((8 * C + 22 + 5 * D + 6) * taps + 2 * C * C) * npx, (16 * C + 12 + 12 * D) * npx
         return (6 * C + 22) * taps * npx + 2 * C * C * npx, (16 * C + 12) * npx
     if kname == "feature_iter":
         # per tap: the appearance weight (12), the feature distance and its

@@ -112,9 +112,13 @@ typedef struct {
                                |F_p - F_q|^2 in place of |p - q|^2 (the "+T"
                                variant of Sec. 4.2, whose features start as
                                the pixel positions); the appearance Gaussian
-                               keeps the positions.  blur must be 1; the
-                               variant field is ignored (one kernel computes
-                               it, weights recomputed per pixel and tap). */
+                               keeps the positions.  With blur s > 1 the
+                               features are s x s average pooled like the
+                               colours and the pooled message takes the
+                               distance of the pooled features (position
+                               features then pool to the cell centres, the
+                               pooled Eq. 4).  The variant field is ignored
+                               (weights recomputed per pixel and tap). */
     int32_t feature_dim;    /* D, 1 <= D <= 4, with features */
 } convcrf_params;
 
@@ -166,7 +170,8 @@ convcrf_status convcrf_meanfield(convcrf_ctx *ctx, const float *unary,
  * matrix is handed to a kernel by value, so params->compat may be ordinary
  * host memory.  Limits: the workspace of the call, 256-byte aligned slices
  * of B*C*H*W floats for the ping-pong (iters >= 2 or learnable features),
- * plus with blur s B*(H/s)*(W/s)*(2C+3) floats, plus C*C for a given
+ * plus with blur s B*(H/s)*(W/s)*(2C+3+D) floats (D learnable feature
+ * planes, if any), plus C*C for a given
  * compatibility, must fit in 64 MiB (1 x 21 x 512 x 512 needs 22 MB), else
  * CONVCRF_E_UNSUPPORTED with the size in the message and nothing enqueued;
  * the materialised variant is refused (CONVCRF_E_UNSUPPORTED) and the
@@ -205,7 +210,8 @@ convcrf_status convcrf_meanfield_noalloc(convcrf_ctx *ctx, const float *unary,
  * bilinear upsampling, the adjoint message on the pooled grid (offsets of s
  * pixels) and the transpose of the average pooling;
  * with learnable features, dK/dF_p = -w_smooth S (F_p - F_q)/theta_gamma^2
- * = -dK/dF_q, gathered per pixel from both ends of every pair.
+ * = -dK/dF_q, gathered per pixel from both ends of every pair (with blur on
+ * the pooled features, then sent through the transpose of their pooling).
  * The forward rounds are recomputed inside the call (the unaries, image and
  * params must be those of the forward call); `variant` is ignored.
  * unary, image, grad_q: DEVICE pointers, as for convcrf_meanfield; grad_q

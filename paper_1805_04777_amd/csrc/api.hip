@@ -134,9 +134,9 @@ convcrf_status validate(convcrf_ctx* ctx, int B, int C, int H, int W, const conv
     if (p->features) {
         if (p->feature_dim < 1 || p->feature_dim > kMaxFeat)
             return fail(ctx, CONVCRF_E_INVALID_ARG, "feature_dim must be 1 .. 4 with features");
-        if (s != 1)
-            return fail(ctx, CONVCRF_E_UNSUPPORTED, "learnable features are built for blur = 1 only");
-        if (feat_lds_bytes(k, C, p->feature_dim) > kLdsLimit)
+        // with blur the features are pooled and staged by the pooled message
+        if (s == 1 ? feat_lds_bytes(k, C, p->feature_dim) > kLdsLimit
+                   : pmsg_lds_bytes(k, p->feature_dim) > kLdsLimit)
             return fail(ctx, CONVCRF_E_UNSUPPORTED, "window, classes and features exceed LDS");
     }
     const long long npix = (long long)B * H * W;
@@ -827,7 +827,7 @@ convcrf_status meanfield_impl(convcrf_ctx* ctx, const float* unary, const float*
         }
     }
 
-    if (p.features) {
+    if (p.features && s == 1) {
         // learnable smoothness features: Q0 = softmax(U), then one update
         // launch per iteration, the last one into q_out
         void* wsp = nullptr;
@@ -973,20 +973,30 @@ convcrf_status meanfield_impl(convcrf_ctx* ctx, const float* unary, const float*
     void *qpv = nullptr, *mpv = nullptr, *fpv = nullptr;
     if ((st = take(ctx, w, ctx->pool_q, pbytes * C, &qpv)) != CONVCRF_OK) return st;
     if ((st = take(ctx, w, ctx->pool_m, pbytes * C, &mpv)) != CONVCRF_OK) return st;
-    if ((st = take(ctx, w, ctx->pool_f, pbytes * 3, &fpv)) != CONVCRF_OK) return st;
+    // pooled colours, then (learnable features) the pooled features
+    const int D = p.features ? p.feature_dim : 0;
+    const size_t fcol = ((size_t)B * 3 * Hp * Wp + 63) / 64 * 64;   // floats, whole 256 B
+    if ((st = take(ctx, w, ctx->pool_f, sizeof(float) * fcol + pbytes * D, &fpv)) != CONVCRF_OK)
+        return st;
     float* qp = static_cast<float*>(qpv);
     float* mp = static_cast<float*>(mpv);
     float* fp = static_cast<float*>(fpv);
+    float* sfp = D > 0 ? fp + fcol : nullptr;
     // pooled message: 16 x 8 cell tiles, one wavefront per window row, the
     // classes in chunks of at most kPmsgClasses (the message does not mix
     // classes; each chunk recomputes the weights)
     const int nchunks = (C + kPmsgClasses - 1) / kPmsgClasses;
     const int chunk = (C + nchunks - 1) / nchunks;
-    const size_t lds = pmsg_lds_bytes(k);
+    const size_t lds = pmsg_lds_bytes(k, D);
     if (lds > kLdsLimit) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window exceeds LDS");
     st = launch(ctx, kPool, stream, "blur_pool",
                 [&] { return launch_pool(image, fp, B, 3, H, W, s, 0, stream); });
     if (st != CONVCRF_OK) return st;
+    if (D > 0) {
+        st = launch(ctx, kPool, stream, "blur_pool",
+                    [&] { return launch_pool(p.features, sfp, B, D, H, W, s, 0, stream); });
+        if (st != CONVCRF_OK) return st;
+    }
     st = launch(ctx, kPool, stream, "blur_pool",
                 [&] { return launch_pool(unary, qp, B, C, H, W, s, 1, stream); });
     if (st != CONVCRF_OK) return st;
@@ -994,7 +1004,8 @@ convcrf_status meanfield_impl(convcrf_ctx* ctx, const float* unary, const float*
     // 4 x 4 pooling: one fused launch per iteration (pooled message of each
     // work-group's cells and the full-resolution update of its pixels), the
     // pooled Q ping-ponging between qp and mp; the last one writes q_out
-    if (s == kFusedBlurFactor && k >= 3 && B <= 65535 &&
+    // (the learnable features take the three-kernel form below)
+    if (s == kFusedBlurFactor && k >= 3 && B <= 65535 && D == 0 &&
         reinterpret_cast<uintptr_t>(unary) % 8 == 0 && reinterpret_cast<uintptr_t>(q_out) % 8 == 0 &&
         blur_iter_lds_bytes(k, C == 19 || C == 21 ? C : (C <= 8 ? 8 : 24), mu_dev != nullptr) <=
             kLdsLimit) {
@@ -1042,6 +1053,10 @@ convcrf_status meanfield_impl(convcrf_ctx* ctx, const float* unary, const float*
     a.tiles_per_img = a.tiles_x * ((Hp + kPmsgTH - 1) / kPmsgTH);
     a.ntiles = a.tiles_per_img * B;
     a.vec = 0;
+    a.sfeat = sfp;
+    a.D = D;
+    a.w_smooth = p.w_smooth;
+    a.neg_gamma = (float)(-kLog2eD / (2.0 * (double)p.theta_gamma * p.theta_gamma));
     for (int t = 0; t < iters; ++t) {
         st = launch(ctx, kBlurMsg, stream, "blur_message",
                     [&] { return launch_pmsg(a, k, nchunks, lds, stream); });
@@ -1153,16 +1168,19 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
 
     const double ta = p.theta_alpha, tb = p.theta_beta, tg = p.theta_gamma;
     // the kernel sums grid offsets n = dx^2 + dy^2; the squared distance in
-    // pixels is s^2 n
+    // pixels is s^2 n.  With learnable features the smoothness sum is taken
+    // on the feature distance itself, which needs no such scale.
     const double s2 = (double)s * s;
+    const double s2g = D > 0 ? 1.0 : s2;
     const float scale[5] = {1.f, (float)(s2 * p.w_app / (ta * ta * ta)),
                             (float)(p.w_app / (tb * tb * tb)), 1.f,
-                            (float)(s2 * p.w_smooth / (tg * tg * tg))};
+                            (float)(s2g * p.w_smooth / (tg * tg * tg))};
     const int tw = bwd_tile_w(k), th = bwd_tile_h(k, C, D, dma, cgsize);
     const long long ntiles_ll = (long long)((Wg + tw - 1) / tw) * ((Hg + th - 1) / th) * B;
     if (ntiles_ll > 0x7fffffffLL) return fail(ctx, CONVCRF_E_UNSUPPORTED, "too many tiles");
     const int ntiles = (int)ntiles_ll;
     const bool run = npix > 0 && iters > 0;
+    const long long npg = (long long)B * Hg * Wg;   // pixels of the message grid
     if (p.features && grad_features && npix > 0 &&
         overlaps(grad_features, sizeof(float) * (size_t)npix * D, p.features,
                  sizeof(float) * (size_t)npix * D))
@@ -1197,18 +1215,22 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         if ((st = ensure(ctx, ctx->b_kpart, sizeof(float) * (size_t)ntiles * groups * 5)) !=
             CONVCRF_OK)
             return st;
-        if (p.features && !grad_features &&
-            (st = ensure(ctx, ctx->b_df, sizeof(float) * (size_t)npix * D)) != CONVCRF_OK)
+        // dL/dF on the grid of the message (with blur, of the pooled features:
+        // always a workspace buffer, the pooling's transpose writes grad_features)
+        if (p.features && (!grad_features || s > 1) &&
+            (st = ensure(ctx, ctx->b_df, sizeof(float) * (size_t)npg * D)) != CONVCRF_OK)
             return st;
         if (p.features && groups > 1 &&
-            (st = ensure(ctx, ctx->b_dfp, sizeof(float) * (size_t)npix * D * groups)) !=
+            (st = ensure(ctx, ctx->b_dfp, sizeof(float) * (size_t)npg * D * groups)) !=
                 CONVCRF_OK)
             return st;
         if (s > 1) {
             // pooled image, pooled Q^t for every round, pooled message, and
             // the pooled dL/dM, -dL/dZ and dL/dQ
             const size_t pb = sizeof(float) * (size_t)B * Hg * Wg;
-            if ((st = ensure(ctx, ctx->pool_f, pb * 3)) != CONVCRF_OK) return st;
+            const size_t fcol = ((size_t)B * 3 * Hg * Wg + 63) / 64 * 64;
+            if ((st = ensure(ctx, ctx->pool_f, sizeof(float) * fcol + pb * D)) != CONVCRF_OK)
+                return st;
             if ((st = ensure(ctx, ctx->pool_q, pb * C * std::max(iters, 1))) != CONVCRF_OK)
                 return st;
             if ((st = ensure(ctx, ctx->pool_m, pb * C)) != CONVCRF_OK) return st;
@@ -1223,6 +1245,8 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
                 [&] { return launch_softmax(unary, qs(0), B, C, H * W, stream); });
     if (st != CONVCRF_OK) return st;
     float* pf = static_cast<float*>(ctx->pool_f.p);
+    // blur with learnable features: the pooled features follow the pooled colours
+    float* psf = s > 1 && D > 0 ? pf + ((size_t)B * 3 * Hg * Wg + 63) / 64 * 64 : nullptr;
     // pooled Q^t of round t (blur)
     auto pqs = [&](int t) {
         return static_cast<float*>(ctx->pool_q.p) + (size_t)t * B * C * Hg * Wg;
@@ -1238,8 +1262,12 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         a.center_w = (float)((double)p.w_app + (double)p.w_smooth);
         fill_taps(p, s, a.taps);
         const int nchunks = (C + kPmsgClasses - 1) / kPmsgClasses;
-        const size_t lds = pmsg_lds_bytes(k);
+        const size_t lds = pmsg_lds_bytes(k, D);
         if (lds > kLdsLimit) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window exceeds LDS");
+        a.sfeat = psf;
+        a.D = D;
+        a.w_smooth = p.w_smooth;
+        a.neg_gamma = (float)(-kLog2eD / (2.0 * tg * tg));
         a.C = (C + nchunks - 1) / nchunks;
         a.planes = C;
         a.H = Hg;
@@ -1253,6 +1281,11 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         st = launch(ctx, kPool, stream, "blur_pool",
                     [&] { return launch_pool(image, pf, B, 3, H, W, s, 0, stream); });
         if (st != CONVCRF_OK) return st;
+        if (D > 0) {
+            st = launch(ctx, kPool, stream, "blur_pool",
+                        [&] { return launch_pool(p.features, psf, B, D, H, W, s, 0, stream); });
+            if (st != CONVCRF_OK) return st;
+        }
         // Q^0 pooled here; every update also writes its pooled Q^{t+1}, kept
         // for the reverse rounds
         st = launch(ctx, kPool, stream, "blur_pool",
@@ -1332,13 +1365,16 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     }
     ba.dm = static_cast<const float*>(ctx->b_dm.p);
     ba.kpart = static_cast<float*>(ctx->b_kpart.p);
+    // dL/dF lands on the message's grid: grad_features itself without blur,
+    // the pooled derivative in the workspace with it
+    float* const df_grid = grad_features && s == 1 ? grad_features : static_cast<float*>(ctx->b_df.p);
     if (p.features) {
-        ba.sfeat = p.features;
-        ba.dfeat = grad_features ? grad_features : static_cast<float*>(ctx->b_df.p);
+        ba.sfeat = s > 1 ? psf : p.features;
+        ba.dfeat = df_grid;
         if (groups > 1) {
             // each class group stores its part of dL/dF; a sum adds them
             ba.dfeat = static_cast<float*>(ctx->b_dfp.p);
-            ba.dfeat_gstride = npix * D;
+            ba.dfeat_gstride = npg * D;
         }
         ba.D = D;
         ba.neg_gamma = (float)(-kLog2eD / (2.0 * tg * tg));
@@ -1373,9 +1409,8 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
                         [&] { return launch_bwd_message(ba, k, stream); });
             if (st != CONVCRF_OK) return st;
             if (ba.dfeat_gstride > 0) {
-                float* df = grad_features ? grad_features : static_cast<float*>(ctx->b_df.p);
                 st = launch(ctx, kBwdReduce, stream, "bwd_reduce", [&] {
-                    return launch_group_sum(ba.dfeat, groups, npix * D, df, acc, stream);
+                    return launch_group_sum(ba.dfeat, groups, npg * D, df_grid, acc, stream);
                 });
                 if (st != CONVCRF_OK) return st;
             }
@@ -1399,12 +1434,26 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
             st = launch(ctx, kBwdMsg, stream, "bwd_message",
                         [&] { return launch_bwd_message(ba, k, stream); });
             if (st != CONVCRF_OK) return st;
+            if (ba.dfeat_gstride > 0) {
+                st = launch(ctx, kBwdReduce, stream, "bwd_reduce", [&] {
+                    return launch_group_sum(ba.dfeat, groups, npg * D, df_grid, acc, stream);
+                });
+                if (st != CONVCRF_OK) return st;
+            }
             st = launch(ctx, kBwdBlurT, stream, "bwd_blur_transpose", [&] {
                 return launch_pool_t(pdq, dq_next, B, C, Hg, Wg, s, stream);
             });
             if (st != CONVCRF_OK) return st;
         }
         dq = dq_next;
+    }
+    if (p.features && grad_features && run && s > 1) {
+        // dL/dF: the transpose of the features' pooling (each pixel gets its
+        // cell's derivative / s^2)
+        st = launch(ctx, kBwdBlurT, stream, "bwd_blur_transpose", [&] {
+            return launch_pool_t(df_grid, grad_features, B, D, Hg, Wg, s, stream);
+        });
+        if (st != CONVCRF_OK) return st;
     }
     if (p.features && grad_features && !run) {
         // T = 0: Q = softmax(U) does not depend on the features

@@ -126,9 +126,9 @@ inline size_t ring_lds_bytes(int k, int C, int CH, bool with_compat, int D = 0) 
 // bytes of a work-group (the chunk's planes and the colours with their halo,
 // and the k row partials of every class and cell).
 constexpr int kPmsgClasses = 12, kPmsgTW = 16, kPmsgTH = 8;
-inline size_t pmsg_lds_bytes(int k) {
+inline size_t pmsg_lds_bytes(int k, int D = 0) {
     const int lh = kPmsgTH + k - 1, ls = (kPmsgTW + k - 1 + 1) / 2 * 2;
-    return sizeof(float) * ((size_t)(kPmsgClasses + 3) * lh * ls +
+    return sizeof(float) * ((size_t)(kPmsgClasses + 3 + D) * lh * ls +
                             (size_t)k * kPmsgClasses * kPmsgTW * kPmsgTH);
 }
 

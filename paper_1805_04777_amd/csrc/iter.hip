@@ -1809,7 +1809,10 @@ hipError_t launch_rstream(const IterArgs& a, size_t lds, int num_cus, hipStream_
 // wave computes the weights of its window row once (2 cells per lane) and
 // applies them to all classes of the chunk, and the k row partials are
 // summed in LDS, each wave finalising every k-th class.  Output: the raw
-// message M (no compatibility, unary or softmax).
+// message M (no compatibility, unary or softmax).  FD > 0: learnable
+// smoothness features (the "+T" variant of Sec. 4.2) pooled to the cells
+// like the colours, staged beside them; the smoothness Gaussian of each
+// weight is taken on the pooled feature distance.
 template <int K>
 struct PmsgShape {
     static constexpr int R = (K - 1) / 2, P = 2, TW = 16, TH = 8;
@@ -1817,7 +1820,7 @@ struct PmsgShape {
     static constexpr int PLANE = LH * LS, NPX = TW * TH;
 };
 
-template <int K, int CM>
+template <int K, int CM, int FD>
 __global__ __launch_bounds__(64 * K) void pmsg_kernel(const IterArgs a) {
     using PS = PmsgShape<K>;
     constexpr int R = PS::R, P = PS::P, TW = PS::TW, TH = PS::TH, LW = PS::LW, LH = PS::LH;
@@ -1829,7 +1832,8 @@ __global__ __launch_bounds__(64 * K) void pmsg_kernel(const IterArgs a) {
     float* const smem = reinterpret_cast<float*>(smem4);
     float* const Qs = smem;                      // [CM][PLANE]
     float* const Cs = smem + CM * PLANE;         // [3][PLANE]
-    float* const Ps = Cs + 3 * PLANE;            // [K][CM][NPX] row partials
+    float* const Fs = Cs + 3 * PLANE;            // [FD][PLANE] pooled features
+    float* const Ps = Fs + FD * PLANE;           // [K][CM][NPX] row partials
 
     const int C = min(a.C, a.planes - (int)blockIdx.y * a.C);
     const int H = a.H, W = a.W;
@@ -1841,13 +1845,14 @@ __global__ __launch_bounds__(64 * K) void pmsg_kernel(const IterArgs a) {
     const size_t HW = (size_t)H * W;
     const float* __restrict__ src = a.src + ((size_t)b * a.planes + (size_t)blockIdx.y * a.C) * HW;
     const float* __restrict__ feat = a.feat + (size_t)b * 3 * HW;
+    const float* __restrict__ sfeat = FD > 0 ? a.sfeat + (size_t)b * FD * HW : nullptr;
 
-    // ---- stage the chunk's planes and the colours, zero outside the grid;
-    // every load of a thread is issued before its LDS stores
+    // ---- stage the chunk's planes, the colours and the features, zero
+    // outside the grid; every load of a thread is issued before its LDS stores
     constexpr int NT = 64 * K;
-    constexpr int PER = ((CM + 3) * LH * LW + NT - 1) / NT;
+    constexpr int PER = ((CM + 3 + FD) * LH * LW + NT - 1) / NT;
     const int tid = threadIdx.x;
-    const int nstage = (C + 3) * LH * LW;
+    const int nstage = (C + 3 + FD) * LH * LW;
     float v[PER];
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
@@ -1857,7 +1862,10 @@ __global__ __launch_bounds__(64 * K) void pmsg_kernel(const IterArgs a) {
         const int gy = y0 - R + r, gx = x0 - R + cc;
         const bool in = idx < nstage && gy >= 0 && gy < H && gx >= 0 && gx < W;
         const size_t g = in ? (size_t)gy * W + gx : 0;
-        v[j] = in ? (pl < C ? src[(size_t)pl * HW + g] : feat[(size_t)(pl - C) * HW + g]) : 0.f;
+        v[j] = in ? (pl < C       ? src[(size_t)pl * HW + g]
+                     : pl < C + 3 ? feat[(size_t)(pl - C) * HW + g]
+                                  : sfeat[(size_t)(pl - C - 3) * HW + g])
+                  : 0.f;
     }
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
@@ -1865,7 +1873,8 @@ __global__ __launch_bounds__(64 * K) void pmsg_kernel(const IterArgs a) {
         if (idx >= nstage) continue;
         const int pl = idx / (LH * LW), rem = idx - pl * (LH * LW);
         const int r = rem / LW, cc = rem - (rem / LW) * LW;
-        (pl < C ? Qs + pl * PLANE : Cs + (pl - C) * PLANE)[r * LS + cc] = v[j];
+        (pl < C ? Qs + pl * PLANE : pl < C + 3 ? Cs + (pl - C) * PLANE : Fs + (pl - C - 3) * PLANE)
+            [r * LS + cc] = v[j];
     }
     __syncthreads();
 
@@ -1881,6 +1890,28 @@ __global__ __launch_bounds__(64 * K) void pmsg_kernel(const IterArgs a) {
             for (int i = 0; i < P; ++i) own[ch][i] = Cs[ch * PLANE + (ty + R) * LS + col0 + R + i];
             lds_row<NW, P>(Cs + ch * PLANE + (ty + grp) * LS + col0, nc[ch]);
         }
+        // FD: the squared feature distance of every tap of the row
+        float fd2[P][K];
+        if constexpr (FD > 0) {
+#pragma unroll
+            for (int i = 0; i < P; ++i)
+#pragma unroll
+                for (int dx = 0; dx < K; ++dx) fd2[i][dx] = 0.f;
+#pragma unroll
+            for (int ch = 0; ch < FD; ++ch) {
+                float fo[P], nf[NW];
+#pragma unroll
+                for (int i = 0; i < P; ++i) fo[i] = Fs[ch * PLANE + (ty + R) * LS + col0 + R + i];
+                lds_row<NW, P>(Fs + ch * PLANE + (ty + grp) * LS + col0, nf);
+#pragma unroll
+                for (int i = 0; i < P; ++i)
+#pragma unroll
+                    for (int dx = 0; dx < K; ++dx) {
+                        const float e = fo[i] - nf[i + dx];
+                        fd2[i][dx] = fmaf(e, e, fd2[i][dx]);
+                    }
+            }
+        }
         const int dy = grp - R;
 #pragma unroll
         for (int i = 0; i < P; ++i) {
@@ -1891,8 +1922,10 @@ __global__ __launch_bounds__(64 * K) void pmsg_kernel(const IterArgs a) {
                 const float d1 = own[1][i] - nc[1][i + dx];
                 const float d2 = own[2][i] - nc[2][i + dx];
                 const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
+                const float smo = FD > 0 ? a.w_smooth * __builtin_amdgcn_exp2f(a.neg_gamma * fd2[i][dx])
+                                         : a.taps.smooth[n];
                 const float v = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, a.taps.app_log2[n])) +
-                                a.taps.smooth[n];
+                                smo;
                 // the centre: excluded, or K(p, p) when it is included
                 w[i][dx] = (n == 0) ? (a.include_center ? a.center_w : 0.f) : v;
             }
@@ -1942,7 +1975,15 @@ __global__ __launch_bounds__(64 * K) void pmsg_kernel(const IterArgs a) {
 
 template <int K>
 hipError_t launch_pmsg_cm(const IterArgs& a, int nchunks, size_t lds, hipStream_t stream) {
-    auto fn = pmsg_kernel<K, kPmsgClasses>;
+    auto fn = pmsg_kernel<K, kPmsgClasses, 0>;
+    switch (a.sfeat ? a.D : 0) {
+        case 0: break;
+        case 1: fn = pmsg_kernel<K, kPmsgClasses, 1>; break;
+        case 2: fn = pmsg_kernel<K, kPmsgClasses, 2>; break;
+        case 3: fn = pmsg_kernel<K, kPmsgClasses, 3>; break;
+        case 4: fn = pmsg_kernel<K, kPmsgClasses, 4>; break;
+        default: return hipErrorInvalidValue;
+    }
     hipError_t e = allow_full_lds(fn);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(a.ntiles, nchunks), dim3(64 * K), lds, stream, a);
