@@ -276,7 +276,11 @@ hipError_t launch_stream(const IterArgs& a, int k, size_t lds, hipStream_t s) {
     switch (k) {
         case 3: return launch_stream_k3(a, lds, s);
         case 5: return launch_stream_k5(a, lds, s);
-        case 7: return launch_stream_k7(a, lds, s);
+        case 7: {
+            // the first round, Potts without a centre tap: the quad form
+            const hipError_t e = a.first ? launch_quad_first_k7(a, s) : hipErrorNotSupported;
+            return e == hipErrorNotSupported ? launch_stream_k7(a, lds, s) : e;
+        }
         default: return hipErrorNotSupported;
     }
 }

@@ -116,6 +116,9 @@ constexpr int ring_plane(int k) {
 constexpr int kQuadStride = 72;
 constexpr int quad_plane() { return ((kRingRows + 6) * kQuadStride + 63) / 64 * 64; }
 static_assert(quad_plane() == ring_plane(7), "the quad update shares the ring's LDS plan");
+// and the first round's, on the streamed tiles, the same size as stream_plane(7)
+constexpr int quad_first_plane() { return ((kStreamRows + 6) * kQuadStride + 63) / 64 * 64; }
+static_assert(quad_first_plane() == stream_plane(7), "the quad first round shares the streamed LDS plan");
 inline size_t ring_lds_bytes(int k, int C, int CH, bool with_compat, int D = 0) {
     return sizeof(float) * ((size_t)(kRingSlots * CH + 3 + D) * ring_plane(k) +
                             (with_compat ? ((size_t)C * C + 63) / 64 * 64 : 0) + 256);
@@ -186,6 +189,8 @@ CONVCRF_DECLARE_ITER(15)
 // The k = 7 ring update in its quad form (Potts, no centre tap, no features;
 // C = 19 or 21); hipErrorNotSupported outside that.
 hipError_t launch_quad_k7(const IterArgs& a, hipStream_t stream);
+// The first round (softmax(U) staged in LDS) in the same quad layout.
+hipError_t launch_quad_first_k7(const IterArgs& a, hipStream_t stream);
 
 // Fill n words with zero (the flags of a resident launch: a kernel, not a
 // memset, so that the sequence may be captured in a graph).

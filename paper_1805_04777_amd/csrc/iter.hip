@@ -1560,6 +1560,208 @@ void quad_kernel(const IterArgs a) {
         *reinterpret_cast<float2*>(qd + c * HW) = make_float2(fin[0][c], fin[1][c]);
 }
 
+// The first round of the k = 7 Potts update in the quad layout, on the
+// tiles of stream_kernel<..., FIRST> (64 x 16 pixels, 512 threads, all planes
+// of U staged at once, softmax(U) applied to the staged halo tile in LDS).
+// Everything is on chip before the message, so its loop runs at the LDS
+// rate, which the quad layout lowers; each lane keeps the unary of its two
+// pixels, read from LDS before the softmax.
+template <int CM, int CH>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void quad_first_kernel(const IterArgs a) {
+    constexpr int K = 7, R = 3;
+    constexpr int TW = kStreamTW, ROWS = kStreamRows, NWAVE = 8;
+    constexpr int LW = TW + 2 * R, LH = ROWS + 2 * R;
+    constexpr int LS = kQuadStride;
+    constexpr int PLANE = quad_first_plane();
+    constexpr int NI = PLANE / 64;               // 64-float loads per plane
+    constexpr int NJ = (NI + NWAVE - 1) / NWAVE; // per wave and plane
+    constexpr int NCH = (CM + CH - 1) / CH;
+    constexpr unsigned kOob = 0x80000000u;
+    static_assert(2 * 16 * ROWS == 512, "16 pixel quads per row, a lane pair each");
+    extern __shared__ float4 smem4[];
+    float* const smem = reinterpret_cast<float*>(smem4);
+    float* const Qs = smem;                      // [CM][PLANE]
+    float* const Cs = smem + CM * PLANE;         // [3][PLANE]
+    float* const dummy = Cs + 3 * PLANE;         // one 256-float row
+    const unsigned lds0 = (unsigned)(size_t)(__attribute__((address_space(3))) float*)smem;
+    auto lds_addr = [&](const float* p) { return lds0 + (unsigned)((p - smem) * 4); };
+
+    const int H = a.H, W = a.W;
+    const int tile = xcd_tile(blockIdx.x, a.ntiles);
+    const int b = tile / a.tiles_per_img;
+    const int trem = tile - b * a.tiles_per_img;
+    const int tyi = trem / a.tiles_x;
+    const int y0 = tyi * ROWS;
+    const int x0 = (trem - tyi * a.tiles_x) * TW;
+    const size_t HW = (size_t)H * W;
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int half = tid & 1, ty = tid >> 5;
+    const int cq = 4 * ((tid >> 1) & 15);
+    const int y = y0 + ty, xo = x0 + cq + 2 * half;
+    const bool pix_ok = y < H && x0 + cq < W;
+
+    // ---- every load into LDS: the colours, then U class by class
+    unsigned voff[NJ];
+    int dst[NJ];
+#pragma unroll
+    for (int s = 0; s < NJ; ++s) {
+        const int j = wave + NWAVE * s;
+        const int f = j * 64 + lane;
+        const int r = f / LS, col = f - (f / LS) * LS;
+        const int gy = y0 - R + r, gx = x0 - R + col;
+        const bool in = j < NI && f < LH * LS && col < LW && gy >= 0 && gy < H && gx >= 0 && gx < W;
+        voff[s] = in ? (unsigned)((gy * W + gx) * 4) : kOob;
+        dst[s] = j < NI ? j * 64 : -1;
+    }
+    const rsrc_t rf = buffer_rsrc(a.feat + (size_t)b * 3 * HW, (unsigned)(3 * HW * 4));
+    const rsrc_t rq = buffer_rsrc(a.src + (size_t)b * CM * HW, (unsigned)(CM * HW * 4));
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch)
+#pragma unroll
+        for (int s = 0; s < NJ; ++s)
+            lds_dma(rf, voff[s], (int)(ch * HW * 4),
+                    lds_addr(dst[s] >= 0 ? Cs + ch * PLANE + dst[s] : dummy));
+    for (int c = 0; c < CM; ++c)
+#pragma unroll
+        for (int s = 0; s < NJ; ++s)
+            lds_dma(rq, voff[s], (int)(c * HW * 4),
+                    lds_addr(dst[s] >= 0 ? Qs + c * PLANE + dst[s] : dummy));
+
+    const unsigned rbase = (unsigned)((ty + (R + 1) * half) * LS + cq);
+    const unsigned hbase = (unsigned)((ty + R) * LS + cq + (R + 1) * half);
+
+    // ---- colours landed (the class planes may not have): the weights
+    // (a wait beyond the 63 loads a wave can have outstanding is clamped:
+    // the loads before the last 63 issued have completed by then)
+    __builtin_amdgcn_s_waitcnt(vm_wait(NJ * CM));
+    __syncthreads();
+    float w[4][4][K];
+    {
+        float own[3][4];
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch) {
+            float r[10];
+            lds_row16<10>(Cs + ch * PLANE + (ty + R) * LS + cq, r);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) own[ch][i] = r[R + i];
+        }
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+            float nc[3][10];
+#pragma unroll
+            for (int ch = 0; ch < 3; ++ch) lds_row16<10>(Cs + ch * PLANE + rbase + j * LS, nc[ch]);
+#pragma unroll
+            for (int dx = 0; dx < K; ++dx) {
+                const int ne = (dx - R) * (dx - R) + (R - j) * (R - j);
+                const int no = (dx - R) * (dx - R) + (j + 1) * (j + 1);
+                float ae = a.taps.app_log2[ne], ao = a.taps.app_log2[no];
+                float se = a.taps.smooth[ne], so = a.taps.smooth[no];
+                asm volatile("" : "+s"(ae), "+s"(ao), "+s"(se), "+s"(so));
+                const float ca = half ? ao : ae;
+                const float cs = half ? so : se;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float d0 = own[0][i] - nc[0][i + dx];
+                    const float d1 = own[1][i] - nc[1][i + dx];
+                    const float d2 = own[2][i] - nc[2][i + dx];
+                    const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
+                    w[j][i][dx] = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, ca)) + cs;
+                }
+            }
+        }
+        float hc[3][6];
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch) lds_row16<6>(Cs + ch * PLANE + hbase, hc[ch]);
+#pragma unroll
+        for (int d = 0; d < R; ++d) {
+            const int nl = (R - d) * (R - d), nr = (d + 1) * (d + 1);
+            float al = a.taps.app_log2[nl], ar = a.taps.app_log2[nr];
+            float sl = a.taps.smooth[nl], sr = a.taps.smooth[nr];
+            asm volatile("" : "+s"(al), "+s"(ar), "+s"(sl), "+s"(sr));
+            const float ca = half ? ar : al;
+            const float cs = half ? sr : sl;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float d0 = own[0][i] - hc[0][i + d];
+                const float d1 = own[1][i] - hc[1][i + d];
+                const float d2 = own[2][i] - hc[2][i + d];
+                const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
+                w[3][i][d] = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, ca)) + cs;
+            }
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // ---- every plane landed: the lane's unary (Z = U + M, Potts), then
+    // softmax(U) over the staged in-image positions (outside stays zero)
+    __builtin_amdgcn_s_waitcnt(vm_wait(0));
+    __syncthreads();
+    float fin[2][CM];
+    // staged column of the lane's first pixel: cq + 2 half + R (odd: two
+    // dword reads)
+    const int upos = (ty + R) * LS + cq + 2 * half + R;
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        fin[0][c] = Qs[c * PLANE + upos];
+        fin[1][c] = Qs[c * PLANE + upos + 1];
+    }
+    __syncthreads();
+    for (int pos = tid; pos < LH * LS; pos += 512) {
+        const int r = pos / LS, col = pos - (pos / LS) * LS;
+        const int gy = y0 - R + r, gx = x0 - R + col;
+        if (col >= LW || gy < 0 || gy >= H || gx < 0 || gx >= W) continue;
+        float z[CM];
+#pragma unroll
+        for (int c = 0; c < CM; ++c) z[c] = Qs[c * PLANE + pos];
+        softmax_regs<CM, true>(z, CM);
+#pragma unroll
+        for (int c = 0; c < CM; ++c) Qs[c * PLANE + pos] = z[c];
+    }
+    __syncthreads();
+
+    // ---- the message, chunk by chunk, each chunk's pair sums added to fin
+    static_for([&](auto kc) {
+        constexpr int k = decltype(kc)::value;
+        constexpr int c_lo = k * CH;
+        constexpr int c_hi = (k + 1) * CH < CM ? (k + 1) * CH : CM;
+        float acc[4][c_hi - c_lo];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int c = 0; c < c_hi - c_lo; ++c) acc[i][c] = 0.f;
+        quad_chunk<PLANE, LS, c_lo, c_hi>(Qs, rbase, hbase, w, acc);
+#pragma unroll
+        for (int c = 0; c < c_hi - c_lo; ++c)
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const float mine = half ? acc[2 + i][c] : acc[i][c];
+                const float send = half ? acc[i][c] : acc[2 + i][c];
+                fin[i][c_lo + c] += mine + pair_swap(send);
+                asm volatile("" : "+v"(fin[i][c_lo + c]));
+            }
+    }, std::make_integer_sequence<int, NCH>{});
+    if (!pix_ok) return;
+
+#pragma unroll
+    for (int i = 0; i < 2; ++i) softmax_regs<CM, true>(fin[i], CM);
+    float* __restrict__ qd = a.dst + (size_t)b * CM * HW + (size_t)y * W + xo;
+#pragma unroll
+    for (int c = 0; c < CM; ++c)
+        *reinterpret_cast<float2*>(qd + c * HW) = make_float2(fin[0][c], fin[1][c]);
+}
+
+template <int CM, int CH>
+hipError_t launch_quad_first(const IterArgs& a, hipStream_t stream) {
+    auto fn = quad_first_kernel<CM, CH>;
+    hipError_t e = allow_full_lds(fn);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(fn, dim3(a.ntiles), dim3(512), stream_lds_bytes(7, CM, false), stream, a);
+    return hipGetLastError();
+}
+
 template <int CM, int CH>
 hipError_t launch_quad(const IterArgs& a, hipStream_t stream) {
     auto fn = quad_kernel<CM, CH>;
@@ -2099,6 +2301,20 @@ hipError_t launch_quad_k7(const IterArgs& a, hipStream_t stream) {
     switch (a.C) {
         case 19: return launch_quad<19, 4>(a, stream);
         case 21: return launch_quad<21, 3>(a, stream);
+        default: return hipErrorNotSupported;
+    }
+}
+
+// The first round in the quad layout on the streamed tiles (a.first, the
+// source U; the unary 16-byte aligned as for stream_kernel).
+hipError_t launch_quad_first_k7(const IterArgs& a, hipStream_t stream) {
+    if (a.mode != kModeUpdate || !a.first || a.planes != a.C || !a.vec || (a.W & 3) || a.mu ||
+        a.include_center || a.sfeat || reinterpret_cast<uintptr_t>(a.unary) % 16 != 0 ||
+        (size_t)a.C * a.H * a.W * 4 >= (1ull << 31))
+        return hipErrorNotSupported;
+    switch (a.C) {
+        case 19: return launch_quad_first<19, 4>(a, stream);
+        case 21: return launch_quad_first<21, 3>(a, stream);
         default: return hipErrorNotSupported;
     }
 }
