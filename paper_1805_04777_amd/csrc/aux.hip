@@ -14,27 +14,7 @@
 namespace convcrf {
 namespace {
 
-constexpr float kLog2e = 1.4426950408889634f;
 
-template <int CM, bool EXACT>
-__device__ __forceinline__ void softmax_regs(float (&z)[CM], int C) {
-    float m = z[0];
-#pragma unroll
-    for (int c = 1; c < CM; ++c)
-        if (EXACT || c < C) m = fmaxf(m, z[c]);
-    const float mb = m * kLog2e;
-    float s = 0.f;
-#pragma unroll
-    for (int c = 0; c < CM; ++c) {
-        if (EXACT || c < C) {
-            z[c] = __builtin_amdgcn_exp2f(fmaf(z[c], kLog2e, -mb));
-            s += z[c];
-        }
-    }
-    const float inv = 1.0f / s;
-#pragma unroll
-    for (int c = 0; c < CM; ++c) z[c] *= inv;
-}
 
 // ---------------------------------------------------------------- softmax
 template <int CM, bool EXACT>

@@ -30,7 +30,6 @@
 namespace convcrf {
 namespace {
 
-constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kS = kFusedBlurFactor;          // pixels per cell side
 constexpr int kNC = kFusedBlurCells;          // own cells per work-group side
 constexpr int kMT = kNC + 2;                  // message tile side: own cells and a ring of one
@@ -46,25 +45,6 @@ struct BlurShape {
     static constexpr int NPAIR = kMT / 2 * kMT;            // lanes with a pair of cells
 };
 
-template <int CM, bool EXACT>
-__device__ __forceinline__ void softmax_regs(float (&z)[CM], int C) {
-    float m = z[0];
-#pragma unroll
-    for (int c = 1; c < CM; ++c)
-        if (EXACT || c < C) m = fmaxf(m, z[c]);
-    const float mb = m * kLog2e;
-    float s = 0.f;
-#pragma unroll
-    for (int c = 0; c < CM; ++c) {
-        if (EXACT || c < C) {
-            z[c] = __builtin_amdgcn_exp2f(fmaf(z[c], kLog2e, -mb));
-            s += z[c];
-        }
-    }
-    const float inv = 1.0f / s;
-#pragma unroll
-    for (int c = 0; c < CM; ++c) z[c] *= inv;
-}
 
 // Half-pixel-centred bilinear source of output pixel o on a grid of n cells
 // of kS pixels: (o + 0.5) / kS - 0.5, clamped at 0 and n - 1.

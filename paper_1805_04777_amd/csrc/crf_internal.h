@@ -433,6 +433,30 @@ hipError_t launch_bwd_reduce(const float* gpart, int groups, int C, float* out_c
                              const float* kpart, int ntiles, const float scale[5],
                              float* out_kernel, hipStream_t stream);
 
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Alg. 1 normalisation in registers: softmax over the first C of CM values,
+// maximum subtracted, one hardware exp2 per value.
+template <int CM, bool EXACT>
+__device__ __forceinline__ void softmax_regs(float (&z)[CM], int C) {
+    float m = z[0];
+#pragma unroll
+    for (int c = 1; c < CM; ++c)
+        if (EXACT || c < C) m = fmaxf(m, z[c]);
+    const float mb = m * kLog2e;
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        if (EXACT || c < C) {
+            z[c] = __builtin_amdgcn_exp2f(fmaf(z[c], kLog2e, -mb));
+            s += z[c];
+        }
+    }
+    const float inv = 1.0f / s;
+#pragma unroll
+    for (int c = 0; c < CM; ++c) z[c] *= inv;
+}
+
 // Block-to-tile order that keeps the tiles of one XCD spatially contiguous.
 // Work-groups are dispatched round-robin over the 8 XCDs of the chip, so
 // block b runs on XCD b % 8; XCD x receives the contiguous tile range that
