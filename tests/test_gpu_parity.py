@@ -182,11 +182,12 @@ def test_ragged_shapes(torch_cuda, crf, oracle_mod, H, W):
 @pytest.mark.parametrize("B,C,k,H,W,T,compat", [
     (1, 21, 7, 40, 72, 3, False), (1, 21, 7, 40, 72, 3, True), (2, 19, 5, 18, 68, 2, True),
     (1, 21, 3, 33, 100, 4, False), (1, 19, 7, 70, 132, 1, False), (1, 21, 5, 16, 64, 2, True),
-    (2, 21, 7, 17, 4, 3, False)])
+    (2, 21, 7, 17, 4, 3, False), (2, 19, 7, 21, 68, 3, False), (1, 19, 7, 9, 196, 4, True)])
 def test_streamed_path(torch_cuda, crf, oracle_mod, B, C, k, H, W, T, compat):
     # widths that are multiples of 4 with 19 or 21 classes and k <= 7 take the
     # streamed update (64 x 16 tiles here partial on both axes; T = 1 runs
-    # its first-iteration form only)
+    # its first-iteration form only; k = 7 with Potts runs the quad forms of
+    # the first and the later rounds, with a compatibility matrix the ring)
     U, I = rand_case(1300 + C + k + H + W, B, C, H, W)
     mu = synth.random_compat(C, seed=k) if compat else None
     p = lib_params(filter_size=k, compat=mu, w_app=2.0, w_smooth=0.7) if compat else lib_params(filter_size=k)
