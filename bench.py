@@ -112,9 +112,14 @@ def algorithmic_per_launch(kname: str, wl, D: int = 0):
         return ((2 * C + 12) * taps * npx + (6 * C + 5 * C + 1 + C) * px,
                 4 * C * px + (4 * C + 12) * npx + ((T - 1) * 4 * C * npx + 4 * C * px) / T)
     if kname == "blur_pool":
-        # two launches per call: softmax(U) pooled (21 planes) and the image
-        # (3 planes); averaged
-        return ((5 * C + 1) * px + C * px + 3 * px) / 2, (4 * (C + 3) * (px + npx)) / 2
+        if wl.blur == 4 and not D:
+            # one launch per call: softmax(U) and the image, averaged over the
+            # cells; reads U and the image, writes the pooled Q and colours
+            return (5 * C + 1 + C + 3) * px, 4 * (C + 3) * (px + npx)
+        # one launch per pooled tensor (the image, the features, softmax(U)),
+        # averaged over them
+        n = 3 if D else 2
+        return ((5 * C + 1 + C + 3 + D) * px / n, 4 * (C + 3 + D) * (px + npx) / n)
     if kname == "softmax":
         return (5 * C + 1) * px, 8 * C * px
     if kname == "sync_reset":

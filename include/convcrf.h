@@ -238,9 +238,11 @@ convcrf_status convcrf_profile_enable(convcrf_ctx *ctx, int enable);
 
 /* Total elapsed milliseconds and launch count of the kernels named `name`
  * ("fused_iter", "fused_resident", "sync_reset", "softmax", "build_kernel",
- * "materialised_iter", "blur_pool", "blur_message", "blur_update",
- * "blur_iteration" (the fused pooled message and update of one iteration,
- * used for blur 4), and for
+ * "materialised_iter", "blur_pool" (the pooled initialisation of the blur
+ * path: one launch per call for blur 4, else one per pooled tensor),
+ * "blur_message", "blur_update" (one each per blur iteration), "blur_iteration"
+ * (the fused pooled message and update of one iteration, used for blur 4
+ * instead of those two), and for
  * convcrf_meanfield_backward "bwd_point", "bwd_message", "bwd_reduce",
  * "bwd_blur_transpose" besides the forward's; "feature_iter" with learnable
  * features, "fused_first") since profiling was enabled.  "fused_resident" is one

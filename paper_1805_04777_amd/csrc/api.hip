@@ -986,33 +986,29 @@ convcrf_status meanfield_impl(convcrf_ctx* ctx, const float* unary, const float*
     float* mp = static_cast<float*>(mpv);
     float* fp = static_cast<float*>(fpv);
     float* sfp = D > 0 ? fp + fcol : nullptr;
-    // pooled message: 16 x 8 cell tiles, one wavefront per window row, the
-    // classes in chunks of at most kPmsgClasses (the message does not mix
-    // classes; each chunk recomputes the weights)
-    const int nchunks = (C + kPmsgClasses - 1) / kPmsgClasses;
-    const int chunk = (C + nchunks - 1) / nchunks;
-    const size_t lds = pmsg_lds_bytes(k, D);
-    if (lds > kLdsLimit) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window exceeds LDS");
-    st = launch(ctx, kPool, stream, "blur_pool",
-                [&] { return launch_pool(image, fp, B, 3, H, W, s, 0, stream); });
-    if (st != CONVCRF_OK) return st;
-    if (D > 0) {
-        st = launch(ctx, kPool, stream, "blur_pool",
-                    [&] { return launch_pool(p.features, sfp, B, D, H, W, s, 0, stream); });
-        if (st != CONVCRF_OK) return st;
-    }
-    st = launch(ctx, kPool, stream, "blur_pool",
-                [&] { return launch_pool(unary, qp, B, C, H, W, s, 1, stream); });
-    if (st != CONVCRF_OK) return st;
-
-    // 4 x 4 pooling: one fused launch per iteration (pooled message of each
+    // 4 x 4 pooling, D = 0: one launch initialises (softmax(U) and the image,
+    // pooled), then one fused launch per iteration (pooled message of each
     // work-group's cells and the full-resolution update of its pixels), the
-    // pooled Q ping-ponging between qp and mp; the last one writes q_out
-    // (the learnable features take the three-kernel form below)
-    if (s == kFusedBlurFactor && k >= 3 && B <= 65535 && D == 0 &&
-        reinterpret_cast<uintptr_t>(unary) % 8 == 0 && reinterpret_cast<uintptr_t>(q_out) % 8 == 0 &&
+    // pooled Q ping-ponging between qp and mp; the last one writes q_out.
+    // Learnable features and other poolings take the general form below.
+    const auto al8 = [](const void* ptr) { return reinterpret_cast<uintptr_t>(ptr) % 8 == 0; };
+    if (s == kFusedBlurFactor && k >= 3 && B <= 65535 && D == 0 && al8(unary) && al8(q_out) &&
+        al8(image) && (Hp + kBlurInitTY - 1) / kBlurInitTY <= 65535 &&
         blur_iter_lds_bytes(k, C == 19 || C == 21 ? C : (C <= 8 ? 8 : 24), mu_dev != nullptr) <=
             kLdsLimit) {
+        BlurInitArgs bin{};
+        bin.unary = unary;
+        bin.image = image;
+        bin.qbar = qp;
+        bin.pcol = fp;
+        bin.B = B;
+        bin.C = C;
+        bin.H = H;
+        bin.W = W;
+        bin.Hp = Hp;
+        bin.Wp = Wp;
+        st = launch(ctx, kPool, stream, "blur_pool", [&] { return launch_blur_init(bin, stream); });
+        if (st != CONVCRF_OK) return st;
         BlurIterArgs bi{};
         bi.pcol = fp;
         bi.unary = unary;
@@ -1041,6 +1037,25 @@ convcrf_status meanfield_impl(convcrf_ctx* ctx, const float* unary, const float*
         }
         return CONVCRF_OK;
     }
+
+    // pooled message: 16 x 8 cell tiles, one wavefront per window row, the
+    // classes in chunks of at most kPmsgClasses (the message does not mix
+    // classes; each chunk recomputes the weights)
+    const int nchunks = (C + kPmsgClasses - 1) / kPmsgClasses;
+    const int chunk = (C + nchunks - 1) / nchunks;
+    const size_t lds = pmsg_lds_bytes(k, D);
+    if (lds > kLdsLimit) return fail(ctx, CONVCRF_E_UNSUPPORTED, "window exceeds LDS");
+    st = launch(ctx, kPool, stream, "blur_pool",
+                [&] { return launch_pool(image, fp, B, 3, H, W, s, 0, stream); });
+    if (st != CONVCRF_OK) return st;
+    if (D > 0) {
+        st = launch(ctx, kPool, stream, "blur_pool",
+                    [&] { return launch_pool(p.features, sfp, B, D, H, W, s, 0, stream); });
+        if (st != CONVCRF_OK) return st;
+    }
+    st = launch(ctx, kPool, stream, "blur_pool",
+                [&] { return launch_pool(unary, qp, B, C, H, W, s, 1, stream); });
+    if (st != CONVCRF_OK) return st;
 
     a.C = chunk;
     a.planes = C;

@@ -8,7 +8,9 @@
 //   blur_update_kernel   bilinear upsampling of the pooled message, then
 //                        compatibility, unary and softmax (Alg. 1), writing
 //                        Q, its s x s average for the next pooled message,
-//                        or both
+//                        or both (any s; blur_update4_kernel for s = 4, 8)
+//   blur_init_kernel     initialisation of the fused blur path (4 x 4):
+//                        softmax(U) and the image, pooled, in one launch
 #include "crf_internal.h"
 
 namespace convcrf {
@@ -422,6 +424,64 @@ __global__ __launch_bounds__(512) void blur_update4_kernel(
     }
 }
 
+// ------------------------------------------- blur initialisation, 4 x 4 cells
+// Initialisation of the blur path for a 4 x 4 pooling (Alg. 1, Sec. 4.2):
+// Q_0 = softmax(U) per pixel and its 4 x 4 cell averages, and the cell
+// averages of the image (the pooled colours of the message's weights), in
+// one launch.  A work-group owns 8 x 4 cells (32 x 16 pixels): eight
+// consecutive lanes per cell and two horizontally adjacent pixels per lane,
+// so a wavefront reads 128-byte rows of every plane; a cell's sums are taken
+// across its eight lanes.
+template <int CM, bool EXACT>
+__global__ __launch_bounds__(256) void blur_init_kernel(const BlurInitArgs a) {
+    constexpr int TX = kBlurInitTX, TY = kBlurInitTY, S4 = kFusedBlurFactor;
+    static_assert(TX * TY * 8 == 256, "eight lanes per cell");
+    const int C = EXACT ? CM : a.C;
+    const int H = a.H, W = a.W, Hp = a.Hp, Wp = a.Wp;
+    const int b = blockIdx.z;
+    const size_t HW = (size_t)H * W, HWp = (size_t)Hp * Wp;
+    const int tid = threadIdx.x, ci = tid >> 3, jj = tid & 7;
+    const int ccy = blockIdx.y * TY + ci / TX, ccx = blockIdx.x * TX + ci % TX;   // own cell
+    const int py = ccy * S4 + (jj >> 1), px = ccx * S4 + 2 * (jj & 1);
+    const bool pix_ok = ccy < Hp && ccx < Wp;                                     // H, W multiples of 4
+    // every load is issued (planes past C read plane 0 and are ignored)
+    const size_t poff = (size_t)(pix_ok ? py : 0) * W + (pix_ok ? px : 0);
+    float z0[CM], z1[CM];
+    {
+        const float* up = a.unary + (size_t)b * a.C * HW + poff;
+#pragma unroll
+        for (int c = 0; c < CM; ++c) {
+            const float2 t =
+                *reinterpret_cast<const float2*>(up + (size_t)(EXACT || c < C ? c : 0) * HW);
+            z0[c] = t.x;
+            z1[c] = t.y;
+        }
+    }
+    float2 im[3];
+    {
+        const float* ip = a.image + (size_t)b * 3 * HW + poff;
+#pragma unroll
+        for (int ch = 0; ch < 3; ++ch) im[ch] = *reinterpret_cast<const float2*>(ip + (size_t)ch * HW);
+    }
+    softmax_regs<CM, EXACT>(z0, C);
+    softmax_regs<CM, EXACT>(z1, C);
+    const size_t cell = (size_t)(pix_ok ? ccy : 0) * Wp + (pix_ok ? ccx : 0);
+    constexpr float inv = 1.0f / (S4 * S4);
+    float* dq = a.qbar + (size_t)b * a.C * HWp + cell;
+#pragma unroll
+    for (int c = 0; c < CM; ++c) {
+        if (!EXACT && c >= C) continue;
+        const float t = cell_sum8(z0[c] + z1[c]);
+        if (jj == 0 && pix_ok) dq[(size_t)c * HWp] = t * inv;
+    }
+    float* dc = a.pcol + (size_t)b * 3 * HWp + cell;
+#pragma unroll
+    for (int ch = 0; ch < 3; ++ch) {
+        const float t = cell_sum8(im[ch].x + im[ch].y);
+        if (jj == 0 && pix_ok) dc[(size_t)ch * HWp] = t * inv;
+    }
+}
+
 __global__ __launch_bounds__(256) void zero_u32_kernel(unsigned int* p, int n) {
     for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
         p[i] = 0u;
@@ -511,6 +571,23 @@ hipError_t launch_blur_update(const float* m_pooled, const float* unary, const f
     else if (C == 19) hipLaunchKernelGGL((blur_update_kernel<19, true>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, C, H, W, s);
     else if (C <= 8) hipLaunchKernelGGL((blur_update_kernel<8, false>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, C, H, W, s);
     else hipLaunchKernelGGL((blur_update_kernel<24, false>), grid, block, 0, stream, m_pooled, unary, mu, q_full, q_pooled, C, H, W, s);
+    return hipGetLastError();
+}
+
+hipError_t launch_blur_init(const BlurInitArgs& a, hipStream_t stream) {
+    const auto al8 = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 8 == 0; };
+    if (a.C < 1 || a.C > kMaxC || a.B < 1 || a.B > 65535 || a.Hp < 1 || a.Wp < 1 ||
+        a.Hp * kFusedBlurFactor != a.H || a.Wp * kFusedBlurFactor != a.W ||
+        (a.Hp + kBlurInitTY - 1) / kBlurInitTY > 65535 || !a.unary || !a.image || !a.qbar ||
+        !a.pcol || !al8(a.unary) || !al8(a.image))
+        return hipErrorInvalidValue;
+    const dim3 grid((a.Wp + kBlurInitTX - 1) / kBlurInitTX, (a.Hp + kBlurInitTY - 1) / kBlurInitTY,
+                    a.B);
+    const dim3 block(256);
+    if (a.C == 21) hipLaunchKernelGGL((blur_init_kernel<21, true>), grid, block, 0, stream, a);
+    else if (a.C == 19) hipLaunchKernelGGL((blur_init_kernel<19, true>), grid, block, 0, stream, a);
+    else if (a.C <= 8) hipLaunchKernelGGL((blur_init_kernel<8, false>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((blur_init_kernel<24, false>), grid, block, 0, stream, a);
     return hipGetLastError();
 }
 

@@ -6,21 +6,25 @@
 // one image and, in one launch:
 //   1. stages the pooled Q_t and the pooled colours of its cells, a one-cell
 //      ring around them and the r-cell window halo of that ring into LDS
-//      (zero outside the grid), then prefetches the unary of its 1024 pixels
-//      into registers, which arrives under the message;
+//      (zero outside the grid; 16-byte loads where the grid rows allow);
 //   2. computes the pooled message (Eq. 6 on the pooled grid, offsets of 4
 //      pixels, Eq. 4 weights from pooled colours) for its 8 x 8 cells and the
 //      one-cell ring that the bilinear upsampling of its pixels reads: each
-//      of the 8 wavefronts takes window rows w and w + 8, each lane two
-//      horizontally adjacent cells, the rows' weights in registers and
-//      applied to every class; the k row partials are summed in LDS (all
-//      classes at once where they fit, else a chunk at a time);
+//      of the 8 wavefronts takes window rows w and w + 8; a lane holds the
+//      rows' weights of four horizontally adjacent cells in registers and
+//      reads each staged row once (16-byte reads) for all four, the two
+//      halves of a wavefront taking the even and the odd classes; the k row
+//      partials are summed in LDS (all classes at once where they fit, else a
+//      chunk at a time).  The unary of its 1024 pixels is prefetched into
+//      registers under this step;
 //   3. per pixel: bilinear upsampling of the message (half-pixel centres,
 //      edge clamp), compatibility, unary and softmax (Alg. 1), then either
 //      the full-resolution Q (the last iteration) or its 4 x 4 cell average,
 //      the pooled Q_{t+1} the next launch reads.
 // So each iteration reads the unary once and the pooled state, and the
-// pooled message is never written to memory.
+// pooled message is never written to memory.  The first iteration's input,
+// softmax(U) and the image averaged over the cells, comes from one
+// initialisation launch (blur_init_kernel).
 #include "crf_internal.h"
 
 #ifndef CRF_BLUR_K
@@ -39,10 +43,12 @@ struct BlurShape {
     static constexpr int R = (K - 1) / 2;
     static constexpr int FS = kMT + 2 * R;                  // footprint side (cells)
     static constexpr int FP = FS * FS;
+    static constexpr int LS = kFusedBlurRowStride;          // LDS row stride (floats)
+    static constexpr int FPL = FS * LS;                     // LDS plane (floats)
+    static_assert(LS >= FS && LS % 2 == 0, "whole 8-byte rows");
     static constexpr int NWAVE = 8;
     static constexpr int NT = 64 * NWAVE;                  // threads
     static constexpr int RW = (K + NWAVE - 1) / NWAVE;     // window rows per wave
-    static constexpr int NPAIR = kMT / 2 * kMT;            // lanes with a pair of cells
 };
 
 
@@ -58,20 +64,26 @@ __device__ __forceinline__ void src_coord(int o, int n, int& i0, int& i1, float&
     f = u - (float)a;
 }
 
-template <int K, int CM, bool EXACT>
+// VEC: 16-byte staging loads (Wp a multiple of 4, 16-byte aligned planes):
+// each footprint row is read as whole float4s of its grid row, which never
+// straddle the grid's edges, and shifted into place in LDS.
+template <int K, int CM, bool EXACT, bool VEC>
 __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurIterArgs a) {
     using BS = BlurShape<K>;
     constexpr int R = BS::R, FS = BS::FS, FP = BS::FP, NT = BS::NT, RW = BS::RW;
+    constexpr int LS = BS::LS, FPL = BS::FPL;
     constexpr int MTC = kMT * kMT;
     constexpr int NW = K + 1;                      // footprint cells one lane's row reads (even)
     constexpr int kChunk = blur_iter_chunk(K, CM); // classes per row-partial round
+    constexpr int kSlots = blur_iter_slots(K, CM); // its class slots (even)
+    constexpr int MTCP = kFusedBlurPartStride;     // row-partial plane (floats)
     static_assert(NW % 2 == 0 && FS % 2 == 0 && FP % 2 == 0, "8-byte rows");
     extern __shared__ float4 smem4[];
     float* const smem = reinterpret_cast<float*>(smem4);
-    float* const Qf = smem;                        // [CM][FS][FS] pooled Q_t
-    float* const Cf = Qf + CM * FP;                // [3][FS][FS] pooled colours
-    float* const Pt = Cf + 3 * FP;                 // [K][kChunk][MTC] row partials
-    float* const Mt = Pt + K * kChunk * MTC;       // [CM][MTC] pooled message
+    float* const Qf = smem;                        // [CM][FS][LS] pooled Q_t
+    float* const Cf = Qf + CM * FPL;               // [3][FS][LS] pooled colours
+    float* const Pt = Cf + 3 * FPL;                // [K][kSlots][MTCP] row partials
+    float* const Mt = Pt + K * kSlots * MTCP;      // [CM][MTC] pooled message
     float* const Mu = Mt + CM * MTC;               // [CM][CM] compatibility, when given
 
     const int C = EXACT ? CM : a.C;
@@ -81,45 +93,19 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
     const size_t HWp = (size_t)Hp * Wp, HW = (size_t)H * W;
     const int tid = threadIdx.x;
 
-    // ---- staging loads (pooled Q_t and colours over the footprint, zero
-    // outside the grid), all issued before any LDS store
-    constexpr int NST = (CM + 3) * FP;
-    constexpr int PER = (NST + NT - 1) / NT;
-    const float* __restrict__ qsrc = a.qbar + (size_t)b * a.C * HWp;
-    const float* __restrict__ csrc = a.pcol + (size_t)b * 3 * HWp;
-    float v[PER];
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int idx = tid + j * NT;
-        const int pl = idx / FP, rem = idx - pl * FP;
-        const int r = rem / FS, cc = rem - r * FS;
-        const int gy = cy0 - 1 - R + r, gx = cx0 - 1 - R + cc;
-        const bool plane_ok = idx < NST && (pl >= CM || EXACT || pl < C);
-        const bool in = plane_ok && gy >= 0 && gy < Hp && gx >= 0 && gx < Wp;
-        const size_t g = in ? (size_t)gy * Wp + gx : 0;
-        v[j] = in ? (pl < CM ? qsrc[(size_t)pl * HWp + g] : csrc[(size_t)(pl - CM) * HWp + g]) : 0.f;
-    }
-
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int idx = tid + j * NT;
-        if (idx < NST) smem[idx] = v[j];
-    }
-    if (a.mu)
-        for (int i = tid; i < C * C; i += NT) Mu[(i / C) * CM + i % C] = a.mu[i];
-
-    // ---- unary prefetch, issued once the staged values are stored so that
-    // no wait above covers it: every thread owns two horizontally adjacent
-    // pixels, eight threads per cell (cell-major, so that a cell's threads
-    // are consecutive lanes); every load is issued (planes past C read plane
-    // 0 and are ignored)
+    // every thread owns two horizontally adjacent pixels, eight threads per
+    // cell (cell-major, so that a cell's threads are consecutive lanes)
     static_assert(NT == kNC * kNC * 8, "two pixels per thread");
     const int ci = tid >> 3, jj = tid & 7;
     const int ccy = cy0 + ci / kNC, ccx = cx0 + ci % kNC;           // own cell
     const int py = ccy * kS + (jj >> 1), px = ccx * kS + 2 * (jj & 1);
     const bool pix_ok = ccy < Hp && ccx < Wp;                       // H, W multiples of kS
+    // unary prefetch, issued after the window weights (under the message,
+    // which needs none of it; issued with the staging loads it would compete
+    // with them); every load is issued (planes past C read plane 0 and are
+    // ignored)
     float u0[CM], u1[CM];
-    {
+    const auto load_unary = [&] {
         const float* up = a.unary + (size_t)b * a.C * HW + (size_t)(pix_ok ? py : 0) * W +
                           (pix_ok ? px : 0);
 #pragma unroll
@@ -129,30 +115,115 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
             u0[c] = t.x;
             u1[c] = t.y;
         }
+    };
+
+    // ---- staging loads (pooled Q_t and colours over the footprint, zero
+    // outside the grid), all issued before any LDS store
+    const float* __restrict__ qsrc = a.qbar + (size_t)b * a.C * HWp;
+    const float* __restrict__ csrc = a.pcol + (size_t)b * 3 * HWp;
+    if constexpr (VEC) {
+        constexpr int RA = (R + 1 + 3) / 4 * 4;         // left halo (R + 1) in whole float4s
+        constexpr int OFF = RA - (R + 1);               // LDS column = 4 f + e - OFF
+        constexpr int NV = (RA + kNC + 1 + R + 3) / 4;  // float4s per footprint row
+        constexpr int NSTV = (CM + 3) * FS * NV;
+        constexpr int PER = (NSTV + NT - 1) / NT;
+        static_assert(kNC % 4 == 0 && 4 * NV - OFF >= FS, "the float4s cover the footprint");
+        float4 v[PER];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int idx = tid + j * NT;
+            const int pl = idx / (FS * NV), rem = idx - pl * (FS * NV);
+            const int r = rem / NV, f = rem - r * NV;
+            const int gy = cy0 - 1 - R + r, gx = cx0 - RA + 4 * f;
+            const bool plane_ok = idx < NSTV && (pl >= CM || EXACT || pl < C);
+            const bool in = plane_ok && gy >= 0 && gy < Hp && gx >= 0 && gx < Wp;
+            const size_t g = in ? (size_t)gy * Wp + gx : 0;
+            v[j] = in ? *reinterpret_cast<const float4*>(pl < CM ? qsrc + (size_t)pl * HWp + g
+                                                              : csrc + (size_t)(pl - CM) * HWp + g)
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int idx = tid + j * NT;
+            if (idx >= NSTV) continue;
+            const int pl = idx / (FS * NV), rem = idx - pl * (FS * NV);
+            const int r = rem / NV, f = rem - r * NV;
+            float* row = smem + pl * FPL + r * LS;
+            const float e4[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int col = 4 * f + e - OFF;
+                if (col >= 0 && col < FS) row[col] = e4[e];
+            }
+        }
+    } else {
+        constexpr int NST = (CM + 3) * FP;
+        constexpr int PER = (NST + NT - 1) / NT;
+        float v[PER];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int idx = tid + j * NT;
+            const int pl = idx / FP, rem = idx - pl * FP;
+            const int r = rem / FS, cc = rem - r * FS;
+            const int gy = cy0 - 1 - R + r, gx = cx0 - 1 - R + cc;
+            const bool plane_ok = idx < NST && (pl >= CM || EXACT || pl < C);
+            const bool in = plane_ok && gy >= 0 && gy < Hp && gx >= 0 && gx < Wp;
+            const size_t g = in ? (size_t)gy * Wp + gx : 0;
+            v[j] = in ? (pl < CM ? qsrc[(size_t)pl * HWp + g] : csrc[(size_t)(pl - CM) * HWp + g])
+                      : 0.f;
+        }
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int idx = tid + j * NT;
+            if (idx >= NST) continue;
+            const int pl = idx / FP, rem = idx - pl * FP;
+            const int r = rem / FS, cc = rem - r * FS;
+            smem[pl * FPL + r * LS + cc] = v[j];
+        }
     }
+    if (a.mu)
+        for (int i = tid; i < C * C; i += NT) Mu[(i / C) * CM + i % C] = a.mu[i];
     __syncthreads();
 
-    // ---- pooled message: wave w takes window rows w + 8 j (j < RW), lane
-    // l < NPAIR the cells (mi, mj) and (mi, mj + 1) of the message tile
-    const int wave = tid >> 6, lane = tid & 63;
-    const bool msg = lane < BS::NPAIR;
-    const int mi = lane / (kMT / 2), mj = 2 * (lane % (kMT / 2));
-    float w[RW][2][K];
+    // ---- pooled message: wavefront w takes window rows w + 8 j (j < RW).
+    // Lane (h, mi, qd): half h = lane / 32 takes the classes of parity h,
+    // (mi, qd) the four cells (mi, 4 qd + i), i < 4, of the 10 x 10 message
+    // tile (qd = 2 computes two cells past the tile, which are discarded), so
+    // one 16-byte-aligned row read of k + 3 staged values feeds 4k FMAs and a
+    // wavefront instruction serves two classes.
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int h = lane >> 5, sub = lane & 31;
+    const bool msg = sub < 3 * kMT;
+    const int mi = msg ? sub / 3 : 0, qd = msg ? sub % 3 : 0, mj = 4 * qd;
+    constexpr int QW = (K + 3 + 3) / 4 * 4;       // staged values one row read covers
+    static_assert(kMT == 10 && LS % 4 == 0 && LS >= 8 + QW, "16-byte reads inside a staged row");
+    // window weights of the lane's four cells: this half computes cells
+    // 2h, 2h + 1 and takes the other two from its partner lane (lane ^ 32,
+    // the same cells in the other half)
+    float w[RW][4][K];
     if (msg) {
         float own[3][2];
 #pragma unroll
         for (int ch = 0; ch < 3; ++ch)
 #pragma unroll
-            for (int i = 0; i < 2; ++i) own[ch][i] = Cf[ch * FP + (mi + R) * FS + mj + R + i];
+            for (int i = 0; i < 2; ++i)
+                own[ch][i] = Cf[ch * FPL + (mi + R) * LS + mj + 2 * h + R + i];
 #pragma unroll
         for (int j = 0; j < RW; ++j) {
             const int dy = wave + BS::NWAVE * j;
             if (dy >= K) continue;
             float nc[3][NW];
 #pragma unroll
-            for (int ch = 0; ch < 3; ++ch)
+            for (int ch = 0; ch < 3; ++ch) {
+                const float2* r2 =
+                    reinterpret_cast<const float2*>(Cf + ch * FPL + (mi + dy) * LS + mj + 2 * h);
 #pragma unroll
-                for (int x = 0; x < NW; ++x) nc[ch][x] = Cf[ch * FP + (mi + dy) * FS + mj + x];
+                for (int x = 0; x < NW / 2; ++x) {
+                    const float2 t = r2[x];
+                    nc[ch][2 * x] = t.x;
+                    nc[ch][2 * x + 1] = t.y;
+                }
+            }
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
 #pragma unroll
@@ -165,37 +236,67 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
                     const float k = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, a.taps.app_log2[n])) +
                                     a.taps.smooth[n];
                     // the centre tap: excluded, or K(p, p) when included
-                    w[j][i][dx] = (dy == R && dx == R) ? (a.include_center ? a.center_w : 0.f) : k;
+                    const float mine =
+                        (dy == R && dx == R) ? (a.include_center ? a.center_w : 0.f) : k;
+                    // the partner's value: v_permlane32_swap of (mine, mine) leaves
+                    // lanes 0..31 of the first result and 32..63 of the second
+                    // as they were and swaps the other halves
+                    const auto sw = __builtin_amdgcn_permlane32_swap(
+                        __builtin_bit_cast(unsigned, mine), __builtin_bit_cast(unsigned, mine),
+                        false, false);
+                    const float other = __builtin_bit_cast(float, h ? sw[0] : sw[1]);
+                    w[j][i][dx] = h ? other : mine;
+                    w[j][2 + i][dx] = h ? mine : other;
                 }
             }
         }
     }
+    load_unary();
     for (int c0 = 0; c0 < C; c0 += kChunk) {
         const int cn = C - c0 < kChunk ? C - c0 : kChunk;
         if (msg) {
 #pragma unroll
             for (int j = 0; j < RW; ++j) {
-                const int dy = wave + BS::NWAVE * j;
+                const int dy = wave + BS::NWAVE * j;   // uniform over the wavefront
                 if (dy >= K) continue;
-                for (int cl = 0; cl < cn; ++cl) {
-                    // FS and mj are even: the row starts on 8 bytes
-                    const float2* row = reinterpret_cast<const float2*>(
-                        Qf + (c0 + cl) * FP + (mi + dy) * FS + mj);
-                    float q[NW];
+                // class slots cl = 2 t + h of the chunk, straight-line, the row
+                // of slot t + 1 read while slot t is summed (slots past C read a
+                // zero or unused plane; their partials are never summed)
+                const auto load_row = [&](int t, float (&q)[QW]) {
+                    const int cl = 2 * t + h;
+                    const int c = c0 + cl < CM ? c0 + cl : CM - 1;
+                    const float4* row =
+                        reinterpret_cast<const float4*>(Qf + c * FPL + (mi + dy) * LS + mj);
 #pragma unroll
-                    for (int x = 0; x < NW / 2; ++x) {
-                        const float2 t = row[x];
-                        q[2 * x] = t.x;
-                        q[2 * x + 1] = t.y;
+                    for (int x = 0; x < QW / 4; ++x) {
+                        const float4 v4 = row[x];
+                        q[4 * x] = v4.x;
+                        q[4 * x + 1] = v4.y;
+                        q[4 * x + 2] = v4.z;
+                        q[4 * x + 3] = v4.w;
                     }
-                    float m0 = 0.f, m1 = 0.f;
+                };
+                constexpr int NSL = kSlots / 2;
+                float qb[2][QW];
+                load_row(0, qb[0]);
+                // the second pair of cells of qd = 2 lies past the tile: its
+                // partials go to the plane's spare floats
+                const int far = (qd < 2 ? mi * kMT + mj + 2 : MTC);
 #pragma unroll
-                    for (int dx = 0; dx < K; ++dx) {
-                        m0 = fmaf(w[j][0][dx], q[dx], m0);
-                        m1 = fmaf(w[j][1][dx], q[dx + 1], m1);
-                    }
-                    *reinterpret_cast<float2*>(Pt + (dy * kChunk + cl) * MTC + mi * kMT + mj) =
-                        make_float2(m0, m1);
+                for (int t = 0; t < NSL; ++t) {
+                    if (t + 1 < NSL) load_row(t + 1, qb[(t + 1) & 1]);
+                    // keep those reads above the FMAs
+                    __builtin_amdgcn_sched_barrier(0);
+                    const float (&q)[QW] = qb[t & 1];
+                    float m[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int dx = 0; dx < K; ++dx)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) m[i] = fmaf(w[j][i][dx], q[i + dx], m[i]);
+                    float* pp = Pt + (dy * kSlots + 2 * t + h) * MTCP;
+                    *reinterpret_cast<float2*>(pp + mi * kMT + mj) = make_float2(m[0], m[1]);
+                    *reinterpret_cast<float2*>(pp + far) = make_float2(m[2], m[3]);
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
         }
@@ -204,13 +305,16 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
             const int cl = i / MTC, cell = i - cl * MTC;
             float m = 0.f;
 #pragma unroll
-            for (int r = 0; r < K; ++r) m += Pt[(r * kChunk + cl) * MTC + cell];
+            for (int r = 0; r < K; ++r) m += Pt[(r * kSlots + cl) * MTCP + cell];
             Mt[(c0 + cl) * MTC + cell] = m;
         }
         __syncthreads();
     }
 
     // ---- per pixel: bilinear message, compatibility, unary, softmax
+    // both pixels of a lane lie in the same half of their cell (px is even),
+    // so they have the same two source columns and differ only in the
+    // horizontal fraction
     int ya, yb, xa, xb, xa1, xb1;
     float fy, fx0, fx1;
     src_coord(py, Hp, ya, yb, fy);
@@ -220,8 +324,6 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
     const int ty0 = ya - (cy0 - 1), ty1 = yb - (cy0 - 1);
     const int o00 = ty0 * kMT + xa - (cx0 - 1), o01 = ty0 * kMT + xb - (cx0 - 1);
     const int o10 = ty1 * kMT + xa - (cx0 - 1), o11 = ty1 * kMT + xb - (cx0 - 1);
-    const int p00 = ty0 * kMT + xa1 - (cx0 - 1), p01 = ty0 * kMT + xb1 - (cx0 - 1);
-    const int p10 = ty1 * kMT + xa1 - (cx0 - 1), p11 = ty1 * kMT + xb1 - (cx0 - 1);
     float z0[CM], z1[CM];
 #pragma unroll
     for (int c = 0; c < CM; ++c) {
@@ -230,16 +332,12 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
             continue;
         }
         const float* m = Mt + c * MTC;
-        {
-            const float top = fmaf(fx0, m[o01] - m[o00], m[o00]);
-            const float bot = fmaf(fx0, m[o11] - m[o10], m[o10]);
-            z0[c] = fmaf(fy, bot - top, top);
-        }
-        {
-            const float top = fmaf(fx1, m[p01] - m[p00], m[p00]);
-            const float bot = fmaf(fx1, m[p11] - m[p10], m[p10]);
-            z1[c] = fmaf(fy, bot - top, top);
-        }
+        const float a00 = m[o00], a01 = m[o01], a10 = m[o10], a11 = m[o11];
+        const float d0 = a01 - a00, d1 = a11 - a10;
+        const float t0 = fmaf(fx0, d0, a00), b0 = fmaf(fx0, d1, a10);
+        const float t1 = fmaf(fx1, d0, a00), b1 = fmaf(fx1, d1, a10);
+        z0[c] = fmaf(fy, b0 - t0, t0);
+        z1[c] = fmaf(fy, b1 - t1, t1);
     }
     if (a.mu) {
         float t0[CM], t1[CM];
@@ -284,23 +382,28 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
 #pragma unroll
     for (int c = 0; c < CM; ++c) {
         if (!EXACT && c >= C) continue;
-        float t = z0[c] + z1[c];
-        t += __shfl_xor(t, 1, 64);
-        t += __shfl_xor(t, 2, 64);
-        t += __shfl_xor(t, 4, 64);
+        const float t = cell_sum8(z0[c] + z1[c]);
         if (jj == 0 && pix_ok) dq[(size_t)c * HWp] = t * (1.0f / (kS * kS));
     }
 }
 
-template <int K, int CM, bool EXACT>
-hipError_t launch_one(const BlurIterArgs& a, size_t lds, hipStream_t stream) {
-    auto fn = blur_iter_kernel<K, CM, EXACT>;
+template <int K, int CM, bool EXACT, bool VEC>
+hipError_t launch_vec(const BlurIterArgs& a, size_t lds, hipStream_t stream) {
+    auto fn = blur_iter_kernel<K, CM, EXACT, VEC>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     const dim3 grid((a.Wp + kNC - 1) / kNC, (a.Hp + kNC - 1) / kNC, a.B);
     hipLaunchKernelGGL(fn, grid, dim3(BlurShape<K>::NT), lds, stream, a);
     return hipGetLastError();
+}
+
+template <int K, int CM, bool EXACT>
+hipError_t launch_one(const BlurIterArgs& a, size_t lds, hipStream_t stream) {
+    const auto al16 = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
+    if (a.Wp % 4 == 0 && al16(a.qbar) && al16(a.pcol))
+        return launch_vec<K, CM, EXACT, true>(a, lds, stream);
+    return launch_vec<K, CM, EXACT, false>(a, lds, stream);
 }
 
 }  // namespace

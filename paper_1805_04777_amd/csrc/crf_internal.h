@@ -234,6 +234,7 @@ hipError_t launch_blur_update(const float* m_pooled, const float* unary,
 // bilinear upsampling reads) and the full-resolution update of its 32 x 32
 // pixels in one launch (grid ceil(Wp / 8) x ceil(Hp / 8) x B).
 constexpr int kFusedBlurFactor = 4, kFusedBlurCells = 8;
+constexpr int kFusedBlurRowStride = 28;   // LDS row stride of the staged footprint (floats)
 struct BlurIterArgs {
     const float* qbar;    // pooled Q_t [B][C][Hp][Wp]
     const float* pcol;    // pooled colours [B][3][Hp][Wp]
@@ -248,19 +249,27 @@ struct BlurIterArgs {
     TapTable taps;        // per-offset constants on the pooled grid (step 4)
 };
 // LDS of one work-group: the pooled Q_t and colours over the footprint
-// ((8 + 2 + 2r) cells square), k row partials of a chunk of classes over the
-// 10 x 10 message tile, the message tile, and the compatibility when given.
-// The chunk is the most classes (up to CM) whose partials fit 160 KB with
-// the rest, compatibility included.
-constexpr int blur_iter_chunk(int k, int CM) {
+// ((8 + 2 + 2r) cells square, rows kFusedBlurRowStride floats apart), k row
+// partials of a chunk of classes over the 10 x 10 message tile (planes of
+// kFusedBlurPartStride floats, two spare), the message tile, and the
+// compatibility when given.  A chunk's class slots are even (two classes per
+// wavefront instruction): the most that fit 160 KB with the rest,
+// compatibility included, up to the classes rounded up to even.
+constexpr int kFusedBlurPartStride = (kFusedBlurCells + 2) * (kFusedBlurCells + 2) + 2;
+constexpr int blur_iter_slots(int k, int CM) {
     const int fs = kFusedBlurCells + 2 + (k - 1), mt = (kFusedBlurCells + 2) * (kFusedBlurCells + 2);
-    const int room = 160 * 1024 / 4 - (CM + 3) * fs * fs - CM * mt - CM * CM;
-    const int ch = room / (k * mt);
-    return ch < 1 ? 1 : (ch > CM ? CM : ch);
+    const int room = 160 * 1024 / 4 - (CM + 3) * fs * kFusedBlurRowStride - CM * mt - CM * CM;
+    const int cap = room / (k * kFusedBlurPartStride) / 2 * 2, full = (CM + 1) / 2 * 2;
+    const int sl = cap < full ? cap : full;
+    return sl < 2 ? 2 : sl;
+}
+constexpr int blur_iter_chunk(int k, int CM) {
+    return blur_iter_slots(k, CM) < CM ? blur_iter_slots(k, CM) : CM;
 }
 inline size_t blur_iter_lds_bytes(int k, int CM, bool with_compat) {
     const size_t fs = kFusedBlurCells + 2 + (k - 1), mt = (kFusedBlurCells + 2) * (kFusedBlurCells + 2);
-    return sizeof(float) * ((size_t)(CM + 3) * fs * fs + (size_t)k * blur_iter_chunk(k, CM) * mt +
+    return sizeof(float) * ((size_t)(CM + 3) * fs * kFusedBlurRowStride +
+                            (size_t)k * blur_iter_slots(k, CM) * kFusedBlurPartStride +
                             (size_t)CM * mt + (with_compat ? (size_t)CM * CM : 0));
 }
 hipError_t launch_blur_iter(const BlurIterArgs& a, int k, hipStream_t stream);
@@ -272,6 +281,19 @@ hipError_t launch_blur_iter_k9(const BlurIterArgs& a, hipStream_t stream);
 hipError_t launch_blur_iter_k11(const BlurIterArgs& a, hipStream_t stream);
 hipError_t launch_blur_iter_k13(const BlurIterArgs& a, hipStream_t stream);
 hipError_t launch_blur_iter_k15(const BlurIterArgs& a, hipStream_t stream);
+
+// ---- initialisation of the fused blur path (4 x 4 pooling): softmax(U)
+// and the image, averaged over the cells, in one launch over tiles of
+// kBlurInitTX x kBlurInitTY cells.
+constexpr int kBlurInitTX = 8, kBlurInitTY = 4;
+struct BlurInitArgs {
+    const float* unary;   // U [B][C][H][W], 8-byte aligned
+    const float* image;   // [B][3][H][W], 8-byte aligned
+    float* qbar;          // pooled softmax(U) [B][C][Hp][Wp] (out)
+    float* pcol;          // pooled colours [B][3][Hp][Wp] (out)
+    int B, C, H, W, Hp, Wp;
+};
+hipError_t launch_blur_init(const BlurInitArgs& a, hipStream_t stream);
 
 // ---- learnable smoothness features (the "+T" variant): one update with
 // the smoothness Gaussian on |F_p - F_q|^2 of a feature map F [B][D][H][W]
@@ -437,6 +459,16 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 // Alg. 1 normalisation in registers: softmax over the first C of CM values,
 // maximum subtracted, one hardware exp2 per value.
+// Sum over the eight consecutive lanes of a cell (complete in every lane of
+// the eight): two quad permutations, then the other quad.
+__device__ __forceinline__ float cell_sum8(float t) {
+    t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0xB1, 0xF,
+                                                            0xF, false));   // quad_perm [1, 0, 3, 2]
+    t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0x4E, 0xF,
+                                                            0xF, false));   // quad_perm [2, 3, 0, 1]
+    return t + __shfl_xor(t, 4, 64);
+}
+
 template <int CM, bool EXACT>
 __device__ __forceinline__ void softmax_regs(float (&z)[CM], int C) {
     float m = z[0];
