@@ -472,13 +472,13 @@ __global__ __launch_bounds__(256) void blur_init_kernel(const BlurInitArgs a) {
     for (int c = 0; c < CM; ++c) {
         if (!EXACT && c >= C) continue;
         const float t = cell_sum8(z0[c] + z1[c]);
-        if (jj == 0 && pix_ok) dq[(size_t)c * HWp] = t * inv;
+        if (jj == 4 && pix_ok) dq[(size_t)c * HWp] = t * inv;
     }
     float* dc = a.pcol + (size_t)b * 3 * HWp + cell;
 #pragma unroll
     for (int ch = 0; ch < 3; ++ch) {
         const float t = cell_sum8(im[ch].x + im[ch].y);
-        if (jj == 0 && pix_ok) dc[(size_t)ch * HWp] = t * inv;
+        if (jj == 4 && pix_ok) dc[(size_t)ch * HWp] = t * inv;
     }
 }
 

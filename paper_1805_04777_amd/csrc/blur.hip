@@ -322,8 +322,7 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
     src_coord(px + 1, Wp, xa1, xb1, fx1);
     // message-tile coordinates of the four taps (the ring covers them)
     const int ty0 = ya - (cy0 - 1), ty1 = yb - (cy0 - 1);
-    const int o00 = ty0 * kMT + xa - (cx0 - 1), o01 = ty0 * kMT + xb - (cx0 - 1);
-    const int o10 = ty1 * kMT + xa - (cx0 - 1), o11 = ty1 * kMT + xb - (cx0 - 1);
+    const int o00 = ty0 * kMT + xa - (cx0 - 1), o10 = ty1 * kMT + xa - (cx0 - 1);
     float z0[CM], z1[CM];
 #pragma unroll
     for (int c = 0; c < CM; ++c) {
@@ -331,8 +330,11 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
             z0[c] = z1[c] = 0.f;
             continue;
         }
+        // the two source columns are adjacent, or one column at the right
+        // edge (the ring keeps o00 + 1 inside the tile row): paired reads
         const float* m = Mt + c * MTC;
-        const float a00 = m[o00], a01 = m[o01], a10 = m[o10], a11 = m[o11];
+        const float a00 = m[o00], n01 = m[o00 + 1], a10 = m[o10], n11 = m[o10 + 1];
+        const float a01 = xb != xa ? n01 : a00, a11 = xb != xa ? n11 : a10;
         const float d0 = a01 - a00, d1 = a11 - a10;
         const float t0 = fmaf(fx0, d0, a00), b0 = fmaf(fx0, d1, a10);
         const float t1 = fmaf(fx1, d0, a00), b1 = fmaf(fx1, d1, a10);
@@ -383,7 +385,7 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
     for (int c = 0; c < CM; ++c) {
         if (!EXACT && c >= C) continue;
         const float t = cell_sum8(z0[c] + z1[c]);
-        if (jj == 0 && pix_ok) dq[(size_t)c * HWp] = t * (1.0f / (kS * kS));
+        if (jj == 4 && pix_ok) dq[(size_t)c * HWp] = t * (1.0f / (kS * kS));
     }
 }
 

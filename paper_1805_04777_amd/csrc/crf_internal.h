@@ -459,14 +459,16 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 // Alg. 1 normalisation in registers: softmax over the first C of CM values,
 // maximum subtracted, one hardware exp2 per value.
-// Sum over the eight consecutive lanes of a cell (complete in every lane of
-// the eight): two quad permutations, then the other quad.
+// Sum over the eight consecutive lanes of a cell (lanes 8g .. 8g + 7),
+// complete in lanes 8g + 4 .. 8g + 7: two quad permutations, then the lower
+// quad shifted up by four within the 16-lane row (row_shr:4).
 __device__ __forceinline__ float cell_sum8(float t) {
     t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0xB1, 0xF,
                                                             0xF, false));   // quad_perm [1, 0, 3, 2]
     t += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, t), 0x4E, 0xF,
                                                             0xF, false));   // quad_perm [2, 3, 0, 1]
-    return t + __shfl_xor(t, 4, 64);
+    return t + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, t),
+                                                                     0x114, 0xF, 0xF, false));
 }
 
 template <int CM, bool EXACT>
