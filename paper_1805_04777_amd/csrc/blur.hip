@@ -38,7 +38,7 @@ constexpr int kS = kFusedBlurFactor;          // pixels per cell side
 constexpr int kNC = kFusedBlurCells;          // own cells per work-group side
 constexpr int kMT = kNC + 2;                  // message tile side: own cells and a ring of one
 
-template <int K>
+template <int K, int CM>
 struct BlurShape {
     static constexpr int R = (K - 1) / 2;
     static constexpr int FS = kMT + 2 * R;                  // footprint side (cells)
@@ -46,9 +46,13 @@ struct BlurShape {
     static constexpr int LS = kFusedBlurRowStride;          // LDS row stride (floats)
     static constexpr int FPL = FS * LS;                     // LDS plane (floats)
     static_assert(LS >= FS && LS % 2 == 0, "whole 8-byte rows");
-    static constexpr int NWAVE = 8;
+    // one wavefront per window row for k = 9, 11 (three per SIMD, so at
+    // most 168 VGPRs: up to 21 classes), else eight; the first NPIX threads
+    // also own the pixels
+    static constexpr int NWAVE = K > 8 && K <= 11 && CM <= 21 ? K : 8;
     static constexpr int NT = 64 * NWAVE;                  // threads
     static constexpr int RW = (K + NWAVE - 1) / NWAVE;     // window rows per wave
+    static constexpr int NPIX = kNC * kNC * 8;             // threads with two pixels each
 };
 
 
@@ -68,8 +72,8 @@ __device__ __forceinline__ void src_coord(int o, int n, int& i0, int& i1, float&
 // each footprint row is read as whole float4s of its grid row, which never
 // straddle the grid's edges, and shifted into place in LDS.
 template <int K, int CM, bool EXACT, bool VEC>
-__global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurIterArgs a) {
-    using BS = BlurShape<K>;
+__global__ __launch_bounds__((BlurShape<K, CM>::NT)) void blur_iter_kernel(const BlurIterArgs a) {
+    using BS = BlurShape<K, CM>;
     constexpr int R = BS::R, FS = BS::FS, FP = BS::FP, NT = BS::NT, RW = BS::RW;
     constexpr int LS = BS::LS, FPL = BS::FPL;
     constexpr int MTC = kMT * kMT;
@@ -95,11 +99,12 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
 
     // every thread owns two horizontally adjacent pixels, eight threads per
     // cell (cell-major, so that a cell's threads are consecutive lanes)
-    static_assert(NT == kNC * kNC * 8, "two pixels per thread");
+    static_assert(BS::NPIX == 512 && NT >= BS::NPIX, "two pixels per thread");
+    const bool pix_thread = tid < BS::NPIX;            // uniform over the wavefront
     const int ci = tid >> 3, jj = tid & 7;
     const int ccy = cy0 + ci / kNC, ccx = cx0 + ci % kNC;           // own cell
     const int py = ccy * kS + (jj >> 1), px = ccx * kS + 2 * (jj & 1);
-    const bool pix_ok = ccy < Hp && ccx < Wp;                       // H, W multiples of kS
+    const bool pix_ok = pix_thread && ccy < Hp && ccx < Wp;         // H, W multiples of kS
     // unary prefetch, issued after the window weights (under the message,
     // which needs none of it; issued with the staging loads it would compete
     // with them); every load is issued (planes past C read plane 0 and are
@@ -116,6 +121,23 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
             u1[c] = t.y;
         }
     };
+
+    // the tap constants of this wavefront's window rows, read into scalar
+    // registers now so that their latency passes under the staging (rows past
+    // the window read row k - 1's and are not used)
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    float tca[RW][K], tcs[RW][K];
+#pragma unroll
+    for (int j = 0; j < RW; ++j) {
+        const int dy = wave + BS::NWAVE * j < K ? wave + BS::NWAVE * j : K - 1;
+#pragma unroll
+        for (int dx = 0; dx < K; ++dx) {
+            const int n = (dx - R) * (dx - R) + (dy - R) * (dy - R);
+            tca[j][dx] = a.taps.app_log2[n];
+            tcs[j][dx] = a.taps.smooth[n];
+            asm volatile("" : "+s"(tca[j][dx]), "+s"(tcs[j][dx]));
+        }
+    }
 
     // ---- staging loads (pooled Q_t and colours over the footprint, zero
     // outside the grid), all issued before any LDS store
@@ -191,7 +213,7 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
     // tile (qd = 2 computes two cells past the tile, which are discarded), so
     // one 16-byte-aligned row read of k + 3 staged values feeds 4k FMAs and a
     // wavefront instruction serves two classes.
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+    const int lane = tid & 63;
     const int h = lane >> 5, sub = lane & 31;
     const bool msg = sub < 3 * kMT;
     const int mi = msg ? sub / 3 : 0, qd = msg ? sub % 3 : 0, mj = 4 * qd;
@@ -228,13 +250,12 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
             for (int i = 0; i < 2; ++i) {
 #pragma unroll
                 for (int dx = 0; dx < K; ++dx) {
-                    const int n = (dx - R) * (dx - R) + (dy - R) * (dy - R);
                     const float d0 = own[0][i] - nc[0][i + dx];
                     const float d1 = own[1][i] - nc[1][i + dx];
                     const float d2 = own[2][i] - nc[2][i + dx];
                     const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
-                    const float k = __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, a.taps.app_log2[n])) +
-                                    a.taps.smooth[n];
+                    const float k =
+                        __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, tca[j][dx])) + tcs[j][dx];
                     // the centre tap: excluded, or K(p, p) when included
                     const float mine =
                         (dy == R && dx == R) ? (a.include_center ? a.center_w : 0.f) : k;
@@ -251,7 +272,7 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
             }
         }
     }
-    load_unary();
+    if (pix_thread) load_unary();
     for (int c0 = 0; c0 < C; c0 += kChunk) {
         const int cn = C - c0 < kChunk ? C - c0 : kChunk;
         if (msg) {
@@ -310,6 +331,8 @@ __global__ __launch_bounds__(BlurShape<K>::NT) void blur_iter_kernel(const BlurI
         }
         __syncthreads();
     }
+    // the message-only wavefronts are done (no barrier follows)
+    if (!pix_thread) return;
 
     // ---- per pixel: bilinear message, compatibility, unary, softmax
     // both pixels of a lane lie in the same half of their cell (px is even),
@@ -396,7 +419,7 @@ hipError_t launch_vec(const BlurIterArgs& a, size_t lds, hipStream_t stream) {
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     const dim3 grid((a.Wp + kNC - 1) / kNC, (a.Hp + kNC - 1) / kNC, a.B);
-    hipLaunchKernelGGL(fn, grid, dim3(BlurShape<K>::NT), lds, stream, a);
+    hipLaunchKernelGGL(fn, grid, dim3(BlurShape<K, CM>::NT), lds, stream, a);
     return hipGetLastError();
 }
 
