@@ -259,9 +259,11 @@ __global__ __launch_bounds__((BlurShape<K, CM>::NT)) void blur_iter_kernel(const
                     // the centre tap: excluded, or K(p, p) when included
                     const float mine =
                         (dy == R && dx == R) ? (a.include_center ? a.center_w : 0.f) : k;
-                    // the partner's value: v_permlane32_swap of (mine, mine) leaves
-                    // lanes 0..31 of the first result and 32..63 of the second
-                    // as they were and swaps the other halves
+                    // the partner's value by v_permlane32_swap of (mine, mine); both
+                    // results are read through h, which is right whether the two
+                    // operands get one register (both results then the swapped
+                    // value) or two (lanes 0..31 of the first and 32..63 of the
+                    // second unchanged, the other halves swapped)
                     const auto sw = __builtin_amdgcn_permlane32_swap(
                         __builtin_bit_cast(unsigned, mine), __builtin_bit_cast(unsigned, mine),
                         false, false);
