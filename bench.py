@@ -104,18 +104,21 @@ def algorithmic_per_launch(kname: str, wl, D: int = 0):
                 4 * C * px + 4 * C * npx + ((T - 1) * 4 * C * npx + 4 * C * px) / T)
     if kname == "blur_iteration":
         # one fused iteration (4 x 4 pooling): the pooled message of every
-        # cell (weights 12 and message 2C per tap) and per pixel the bilinear
-        # sample (3C FMA), unary add and softmax (5C + 1) and the cell average
-        # (C); reads U, the pooled Q_t and colours, writes the pooled Q_t+1
+        # cell (weights 12, with D pooled feature planes their Gaussian 3D + 2,
+        # and message 2C per tap) and per pixel the bilinear sample (3C FMA),
+        # unary add and softmax (5C + 1) and the cell average (C); reads U,
+        # the pooled Q_t, colours and features, writes the pooled Q_t+1
         # (T - 1 launches) or the full Q (the last)
         taps = k * k - 1
-        return ((2 * C + 12) * taps * npx + (6 * C + 5 * C + 1 + C) * px,
-                4 * C * px + (4 * C + 12) * npx + ((T - 1) * 4 * C * npx + 4 * C * px) / T)
+        fg = 3 * D + 2 if D else 0
+        return ((2 * C + 12 + fg) * taps * npx + (6 * C + 5 * C + 1 + C) * px,
+                4 * C * px + (4 * C + 12 + 4 * D) * npx + ((T - 1) * 4 * C * npx + 4 * C * px) / T)
     if kname == "blur_pool":
-        if wl.blur == 4 and not D:
-            # one launch per call: softmax(U) and the image, averaged over the
-            # cells; reads U and the image, writes the pooled Q and colours
-            return (5 * C + 1 + C + 3) * px, 4 * (C + 3) * (px + npx)
+        if wl.blur == 4:
+            # one launch per call: softmax(U), the image and the D feature
+            # planes, averaged over the cells; reads them, writes the pooled
+            # planes
+            return (5 * C + 1 + C + 3 + D) * px, 4 * (C + 3 + D) * (px + npx)
         # one launch per pooled tensor (the image, the features, softmax(U)),
         # averaged over them
         n = 3 if D else 2

@@ -986,16 +986,17 @@ convcrf_status meanfield_impl(convcrf_ctx* ctx, const float* unary, const float*
     float* mp = static_cast<float*>(mpv);
     float* fp = static_cast<float*>(fpv);
     float* sfp = D > 0 ? fp + fcol : nullptr;
-    // 4 x 4 pooling, D = 0: one launch initialises (softmax(U) and the image,
-    // pooled), then one fused launch per iteration (pooled message of each
-    // work-group's cells and the full-resolution update of its pixels), the
-    // pooled Q ping-ponging between qp and mp; the last one writes q_out.
-    // Learnable features and other poolings take the general form below.
+    // 4 x 4 pooling: one launch initialises (softmax(U), the image and the
+    // learnable features, pooled), then one fused launch per iteration (pooled
+    // message of each work-group's cells and the full-resolution update of its
+    // pixels), the pooled Q ping-ponging between qp and mp; the last one
+    // writes q_out.  Other poolings take the general form below.
     const auto al8 = [](const void* ptr) { return reinterpret_cast<uintptr_t>(ptr) % 8 == 0; };
-    if (s == kFusedBlurFactor && k >= 3 && B <= 65535 && D == 0 && al8(unary) && al8(q_out) &&
-        al8(image) && (Hp + kBlurInitTY - 1) / kBlurInitTY <= 65535 &&
-        blur_iter_lds_bytes(k, C == 19 || C == 21 ? C : (C <= 8 ? 8 : 24), mu_dev != nullptr) <=
-            kLdsLimit) {
+    if (s == kFusedBlurFactor && k >= 3 && B <= 65535 && D <= kMaxFeat && al8(unary) &&
+        al8(q_out) && al8(image) && (D == 0 || al8(p.features)) &&
+        (Hp + kBlurInitTY - 1) / kBlurInitTY <= 65535 &&
+        blur_iter_lds_bytes(k, C == 19 || C == 21 ? C : (C <= 8 ? 8 : 24), mu_dev != nullptr,
+                            D > 0 ? kMaxFeat : 0) <= kLdsLimit) {
         BlurInitArgs bin{};
         bin.unary = unary;
         bin.image = image;
@@ -1007,6 +1008,9 @@ convcrf_status meanfield_impl(convcrf_ctx* ctx, const float* unary, const float*
         bin.W = W;
         bin.Hp = Hp;
         bin.Wp = Wp;
+        bin.feat = D > 0 ? p.features : nullptr;
+        bin.pfeat = D > 0 ? sfp : nullptr;
+        bin.D = D;
         st = launch(ctx, kPool, stream, "blur_pool", [&] { return launch_blur_init(bin, stream); });
         if (st != CONVCRF_OK) return st;
         BlurIterArgs bi{};
@@ -1023,6 +1027,10 @@ convcrf_status meanfield_impl(convcrf_ctx* ctx, const float* unary, const float*
         bi.center_w = a.center_w;
         bi.neg_beta = a.neg_beta;
         bi.taps = a.taps;
+        bi.sfeat = D > 0 ? sfp : nullptr;
+        bi.D = D;
+        bi.w_smooth = p.w_smooth;
+        bi.neg_gamma = (float)(-kLog2eD / (2.0 * (double)p.theta_gamma * p.theta_gamma));
         float* cur = qp;
         float* nxt = mp;
         for (int t = 0; t < iters; ++t) {

@@ -427,8 +427,8 @@ __global__ __launch_bounds__(512) void blur_update4_kernel(
 // ------------------------------------------- blur initialisation, 4 x 4 cells
 // Initialisation of the blur path for a 4 x 4 pooling (Alg. 1, Sec. 4.2):
 // Q_0 = softmax(U) per pixel and its 4 x 4 cell averages, and the cell
-// averages of the image (the pooled colours of the message's weights), in
-// one launch.  A work-group owns 8 x 4 cells (32 x 16 pixels): eight
+// averages of the image (the pooled colours of the message's weights) and of
+// the learnable features when given, in one launch.  A work-group owns 8 x 4 cells (32 x 16 pixels): eight
 // consecutive lanes per cell and two horizontally adjacent pixels per lane,
 // so a wavefront reads 128-byte rows of every plane; a cell's sums are taken
 // across its eight lanes.
@@ -479,6 +479,15 @@ __global__ __launch_bounds__(256) void blur_init_kernel(const BlurInitArgs a) {
     for (int ch = 0; ch < 3; ++ch) {
         const float t = cell_sum8(im[ch].x + im[ch].y);
         if (jj == 4 && pix_ok) dc[(size_t)ch * HWp] = t * inv;
+    }
+    if (a.feat) {   // uniform over the grid
+        const float* fp = a.feat + (size_t)b * a.D * HW + poff;
+        float* df = a.pfeat + (size_t)b * a.D * HWp + cell;
+        for (int d = 0; d < a.D; ++d) {
+            const float2 v = *reinterpret_cast<const float2*>(fp + (size_t)d * HW);
+            const float t = cell_sum8(v.x + v.y);
+            if (jj == 4 && pix_ok) df[(size_t)d * HWp] = t * inv;
+        }
     }
 }
 
@@ -579,7 +588,8 @@ hipError_t launch_blur_init(const BlurInitArgs& a, hipStream_t stream) {
     if (a.C < 1 || a.C > kMaxC || a.B < 1 || a.B > 65535 || a.Hp < 1 || a.Wp < 1 ||
         a.Hp * kFusedBlurFactor != a.H || a.Wp * kFusedBlurFactor != a.W ||
         (a.Hp + kBlurInitTY - 1) / kBlurInitTY > 65535 || !a.unary || !a.image || !a.qbar ||
-        !a.pcol || !al8(a.unary) || !al8(a.image))
+        !a.pcol || !al8(a.unary) || !al8(a.image) || a.D < 0 || a.D > kMaxFeat ||
+        (a.feat && (!a.pfeat || a.D < 1 || !al8(a.feat))))
         return hipErrorInvalidValue;
     const dim3 grid((a.Wp + kBlurInitTX - 1) / kBlurInitTX, (a.Hp + kBlurInitTY - 1) / kBlurInitTY,
                     a.B);

@@ -38,7 +38,7 @@ constexpr int kS = kFusedBlurFactor;          // pixels per cell side
 constexpr int kNC = kFusedBlurCells;          // own cells per work-group side
 constexpr int kMT = kNC + 2;                  // message tile side: own cells and a ring of one
 
-template <int K, int CM>
+template <int K, int CM, bool FT>
 struct BlurShape {
     static constexpr int R = (K - 1) / 2;
     static constexpr int FS = kMT + 2 * R;                  // footprint side (cells)
@@ -47,9 +47,10 @@ struct BlurShape {
     static constexpr int FPL = FS * LS;                     // LDS plane (floats)
     static_assert(LS >= FS && LS % 2 == 0, "whole 8-byte rows");
     // one wavefront per window row for k = 9, 11 (three per SIMD, so at
-    // most 168 VGPRs: up to 21 classes), else eight; the first NPIX threads
-    // also own the pixels
-    static constexpr int NWAVE = K > 8 && K <= 11 && CM <= 21 ? K : 8;
+    // most 168 VGPRs: up to 21 classes, no feature planes), else eight; the
+    // first NPIX threads also own the pixels
+    static constexpr int NWAVE = K > 8 && K <= 11 && CM <= 21 && !FT ? K : 8;
+    static constexpr int FD = FT ? kMaxFeat : 0;           // staged feature planes
     static constexpr int NT = 64 * NWAVE;                  // threads
     static constexpr int RW = (K + NWAVE - 1) / NWAVE;     // window rows per wave
     static constexpr int NPIX = kNC * kNC * 8;             // threads with two pixels each
@@ -71,22 +72,29 @@ __device__ __forceinline__ void src_coord(int o, int n, int& i0, int& i1, float&
 // VEC: 16-byte staging loads (Wp a multiple of 4, 16-byte aligned planes):
 // each footprint row is read as whole float4s of its grid row, which never
 // straddle the grid's edges, and shifted into place in LDS.
-template <int K, int CM, bool EXACT, bool VEC>
-__global__ __launch_bounds__((BlurShape<K, CM>::NT)) void blur_iter_kernel(const BlurIterArgs a) {
-    using BS = BlurShape<K, CM>;
+// FT: learnable smoothness features (the "+T" variant): D <= kMaxFeat pooled
+// feature planes are staged after the colours (planes past D read zero) and
+// the smoothness Gaussian of a tap is w_smooth exp(-|F_p - F_q|^2 / 2 theta_gamma^2)
+// on them instead of the per-offset constant.
+template <int K, int CM, bool EXACT, bool VEC, bool FT>
+__global__ __launch_bounds__((BlurShape<K, CM, FT>::NT)) void blur_iter_kernel(const BlurIterArgs a) {
+    using BS = BlurShape<K, CM, FT>;
+    constexpr int FD = BS::FD;
+    constexpr int NAUX = 3 + FD;                   // colour and feature planes
     constexpr int R = BS::R, FS = BS::FS, FP = BS::FP, NT = BS::NT, RW = BS::RW;
     constexpr int LS = BS::LS, FPL = BS::FPL;
     constexpr int MTC = kMT * kMT;
     constexpr int NW = K + 1;                      // footprint cells one lane's row reads (even)
-    constexpr int kChunk = blur_iter_chunk(K, CM); // classes per row-partial round
-    constexpr int kSlots = blur_iter_slots(K, CM); // its class slots (even)
+    constexpr int kChunk = blur_iter_chunk(K, CM, FD); // classes per row-partial round
+    constexpr int kSlots = blur_iter_slots(K, CM, FD); // its class slots (even)
     constexpr int MTCP = kFusedBlurPartStride;     // row-partial plane (floats)
     static_assert(NW % 2 == 0 && FS % 2 == 0 && FP % 2 == 0, "8-byte rows");
     extern __shared__ float4 smem4[];
     float* const smem = reinterpret_cast<float*>(smem4);
     float* const Qf = smem;                        // [CM][FS][LS] pooled Q_t
     float* const Cf = Qf + CM * FPL;               // [3][FS][LS] pooled colours
-    float* const Pt = Cf + 3 * FPL;                // [K][kSlots][MTCP] row partials
+    float* const Ff = Cf + 3 * FPL;                // [FD][FS][LS] pooled features (FT)
+    float* const Pt = Ff + FD * FPL;               // [K][kSlots][MTCP] row partials
     float* const Mt = Pt + K * kSlots * MTCP;      // [CM][MTC] pooled message
     float* const Mu = Mt + CM * MTC;               // [CM][CM] compatibility, when given
 
@@ -143,11 +151,21 @@ __global__ __launch_bounds__((BlurShape<K, CM>::NT)) void blur_iter_kernel(const
     // outside the grid), all issued before any LDS store
     const float* __restrict__ qsrc = a.qbar + (size_t)b * a.C * HWp;
     const float* __restrict__ csrc = a.pcol + (size_t)b * 3 * HWp;
+    const float* __restrict__ fsrc = FT ? a.sfeat + (size_t)b * a.D * HWp : csrc;
+    // plane pl of the staged block: Q (pl < CM), colours, features (FT)
+    const auto plane_src = [&](int pl) {
+        return pl < CM ? qsrc + (size_t)pl * HWp
+                       : (pl < CM + 3 ? csrc + (size_t)(pl - CM) * HWp
+                                      : fsrc + (size_t)(pl - CM - 3) * HWp);
+    };
+    const auto plane_ok = [&](int pl) {
+        return pl < CM ? (EXACT || pl < C) : (pl < CM + 3 || pl - CM - 3 < a.D);
+    };
     if constexpr (VEC) {
         constexpr int RA = (R + 1 + 3) / 4 * 4;         // left halo (R + 1) in whole float4s
         constexpr int OFF = RA - (R + 1);               // LDS column = 4 f + e - OFF
         constexpr int NV = (RA + kNC + 1 + R + 3) / 4;  // float4s per footprint row
-        constexpr int NSTV = (CM + 3) * FS * NV;
+        constexpr int NSTV = (CM + NAUX) * FS * NV;
         constexpr int PER = (NSTV + NT - 1) / NT;
         static_assert(kNC % 4 == 0 && 4 * NV - OFF >= FS, "the float4s cover the footprint");
         float4 v[PER];
@@ -157,11 +175,10 @@ __global__ __launch_bounds__((BlurShape<K, CM>::NT)) void blur_iter_kernel(const
             const int pl = idx / (FS * NV), rem = idx - pl * (FS * NV);
             const int r = rem / NV, f = rem - r * NV;
             const int gy = cy0 - 1 - R + r, gx = cx0 - RA + 4 * f;
-            const bool plane_ok = idx < NSTV && (pl >= CM || EXACT || pl < C);
-            const bool in = plane_ok && gy >= 0 && gy < Hp && gx >= 0 && gx < Wp;
+            const bool in =
+                idx < NSTV && plane_ok(pl) && gy >= 0 && gy < Hp && gx >= 0 && gx < Wp;
             const size_t g = in ? (size_t)gy * Wp + gx : 0;
-            v[j] = in ? *reinterpret_cast<const float4*>(pl < CM ? qsrc + (size_t)pl * HWp + g
-                                                              : csrc + (size_t)(pl - CM) * HWp + g)
+            v[j] = in ? *reinterpret_cast<const float4*>(plane_src(in ? pl : 0) + g)
                       : make_float4(0.f, 0.f, 0.f, 0.f);
         }
 #pragma unroll
@@ -179,7 +196,7 @@ __global__ __launch_bounds__((BlurShape<K, CM>::NT)) void blur_iter_kernel(const
             }
         }
     } else {
-        constexpr int NST = (CM + 3) * FP;
+        constexpr int NST = (CM + NAUX) * FP;
         constexpr int PER = (NST + NT - 1) / NT;
         float v[PER];
 #pragma unroll
@@ -188,11 +205,10 @@ __global__ __launch_bounds__((BlurShape<K, CM>::NT)) void blur_iter_kernel(const
             const int pl = idx / FP, rem = idx - pl * FP;
             const int r = rem / FS, cc = rem - r * FS;
             const int gy = cy0 - 1 - R + r, gx = cx0 - 1 - R + cc;
-            const bool plane_ok = idx < NST && (pl >= CM || EXACT || pl < C);
-            const bool in = plane_ok && gy >= 0 && gy < Hp && gx >= 0 && gx < Wp;
+            const bool in =
+                idx < NST && plane_ok(pl) && gy >= 0 && gy < Hp && gx >= 0 && gx < Wp;
             const size_t g = in ? (size_t)gy * Wp + gx : 0;
-            v[j] = in ? (pl < CM ? qsrc[(size_t)pl * HWp + g] : csrc[(size_t)(pl - CM) * HWp + g])
-                      : 0.f;
+            v[j] = in ? plane_src(in ? pl : 0)[g] : 0.f;
         }
 #pragma unroll
         for (int j = 0; j < PER; ++j) {
@@ -224,9 +240,11 @@ __global__ __launch_bounds__((BlurShape<K, CM>::NT)) void blur_iter_kernel(const
     // the same cells in the other half)
     float w[RW][4][K];
     if (msg) {
-        float own[3][2];
+        // own colours (and features, FT) of the lane's two cells: the colour
+        // and feature planes follow each other in LDS
+        float own[NAUX][2];
 #pragma unroll
-        for (int ch = 0; ch < 3; ++ch)
+        for (int ch = 0; ch < NAUX; ++ch)
 #pragma unroll
             for (int i = 0; i < 2; ++i)
                 own[ch][i] = Cf[ch * FPL + (mi + R) * LS + mj + 2 * h + R + i];
@@ -234,9 +252,9 @@ __global__ __launch_bounds__((BlurShape<K, CM>::NT)) void blur_iter_kernel(const
         for (int j = 0; j < RW; ++j) {
             const int dy = wave + BS::NWAVE * j;
             if (dy >= K) continue;
-            float nc[3][NW];
+            float nc[NAUX][NW];
 #pragma unroll
-            for (int ch = 0; ch < 3; ++ch) {
+            for (int ch = 0; ch < NAUX; ++ch) {
                 const float2* r2 =
                     reinterpret_cast<const float2*>(Cf + ch * FPL + (mi + dy) * LS + mj + 2 * h);
 #pragma unroll
@@ -254,8 +272,18 @@ __global__ __launch_bounds__((BlurShape<K, CM>::NT)) void blur_iter_kernel(const
                     const float d1 = own[1][i] - nc[1][i + dx];
                     const float d2 = own[2][i] - nc[2][i + dx];
                     const float col2 = fmaf(d2, d2, fmaf(d1, d1, d0 * d0));
+                    float smo = tcs[j][dx];
+                    if constexpr (FT) {
+                        float fd2 = 0.f;
+#pragma unroll
+                        for (int d = 0; d < FD; ++d) {
+                            const float e = own[3 + d][i] - nc[3 + d][i + dx];
+                            fd2 = fmaf(e, e, fd2);
+                        }
+                        smo = a.w_smooth * __builtin_amdgcn_exp2f(a.neg_gamma * fd2);
+                    }
                     const float k =
-                        __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, tca[j][dx])) + tcs[j][dx];
+                        __builtin_amdgcn_exp2f(fmaf(col2, a.neg_beta, tca[j][dx])) + smo;
                     // the centre tap: excluded, or K(p, p) when included
                     const float mine =
                         (dy == R && dx == R) ? (a.include_center ? a.center_w : 0.f) : k;
@@ -414,23 +442,30 @@ __global__ __launch_bounds__((BlurShape<K, CM>::NT)) void blur_iter_kernel(const
     }
 }
 
-template <int K, int CM, bool EXACT, bool VEC>
-hipError_t launch_vec(const BlurIterArgs& a, size_t lds, hipStream_t stream) {
-    auto fn = blur_iter_kernel<K, CM, EXACT, VEC>;
+template <int K, int CM, bool EXACT, bool VEC, bool FT>
+hipError_t launch_vec(const BlurIterArgs& a, hipStream_t stream) {
+    const size_t lds = blur_iter_lds_bytes(K, CM, a.mu != nullptr, FT ? kMaxFeat : 0);
+    auto fn = blur_iter_kernel<K, CM, EXACT, VEC, FT>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
     const dim3 grid((a.Wp + kNC - 1) / kNC, (a.Hp + kNC - 1) / kNC, a.B);
-    hipLaunchKernelGGL(fn, grid, dim3(BlurShape<K, CM>::NT), lds, stream, a);
+    hipLaunchKernelGGL(fn, grid, dim3(BlurShape<K, CM, FT>::NT), lds, stream, a);
     return hipGetLastError();
 }
 
-template <int K, int CM, bool EXACT>
-hipError_t launch_one(const BlurIterArgs& a, size_t lds, hipStream_t stream) {
+template <int K, int CM, bool EXACT, bool FT>
+hipError_t launch_ft(const BlurIterArgs& a, hipStream_t stream) {
     const auto al16 = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
-    if (a.Wp % 4 == 0 && al16(a.qbar) && al16(a.pcol))
-        return launch_vec<K, CM, EXACT, true>(a, lds, stream);
-    return launch_vec<K, CM, EXACT, false>(a, lds, stream);
+    if (a.Wp % 4 == 0 && al16(a.qbar) && al16(a.pcol) && (!FT || al16(a.sfeat)))
+        return launch_vec<K, CM, EXACT, true, FT>(a, stream);
+    return launch_vec<K, CM, EXACT, false, FT>(a, stream);
+}
+
+template <int K, int CM, bool EXACT>
+hipError_t launch_one(const BlurIterArgs& a, hipStream_t stream) {
+    if (a.D > 0) return launch_ft<K, CM, EXACT, true>(a, stream);
+    return launch_ft<K, CM, EXACT, false>(a, stream);
 }
 
 }  // namespace
@@ -444,16 +479,16 @@ hipError_t CRF_CAT(launch_blur_iter_k, CRF_BLUR_K)(const BlurIterArgs& a, hipStr
         return hipErrorNotSupported;
     } else {
         if (a.C < 1 || a.C > kMaxC || a.Hp * kS != a.H || a.Wp * kS != a.W || a.B < 1 ||
-            a.B > 65535 || a.Hp > 65535 * kNC)
+            a.B > 65535 || a.Hp > 65535 * kNC || a.D < 0 || a.D > kMaxFeat ||
+            (a.D > 0 && !a.sfeat))
             return hipErrorInvalidValue;
-        const bool mu = a.mu != nullptr;
         switch (a.C) {
-            case 19: return launch_one<K, 19, true>(a, blur_iter_lds_bytes(K, 19, mu), stream);
-            case 21: return launch_one<K, 21, true>(a, blur_iter_lds_bytes(K, 21, mu), stream);
+            case 19: return launch_one<K, 19, true>(a, stream);
+            case 21: return launch_one<K, 21, true>(a, stream);
             default: break;
         }
-        if (a.C <= 8) return launch_one<K, 8, false>(a, blur_iter_lds_bytes(K, 8, mu), stream);
-        return launch_one<K, 24, false>(a, blur_iter_lds_bytes(K, 24, mu), stream);
+        if (a.C <= 8) return launch_one<K, 8, false>(a, stream);
+        return launch_one<K, 24, false>(a, stream);
     }
 }
 

@@ -247,29 +247,34 @@ struct BlurIterArgs {
     float center_w;       // K(p, p) = w_app + w_smooth when the centre is included
     float neg_beta;       // -log2(e) / (2 theta_beta^2)
     TapTable taps;        // per-offset constants on the pooled grid (step 4)
+    const float* sfeat;   // pooled learnable features [B][D][Hp][Wp] (D > 0), else null
+    int D;                // feature planes, 0 .. kMaxFeat
+    float w_smooth;       // the smoothness weight (features)
+    float neg_gamma;      // -log2(e) / (2 theta_gamma^2) (features)
 };
 // LDS of one work-group: the pooled Q_t and colours over the footprint
-// ((8 + 2 + 2r) cells square, rows kFusedBlurRowStride floats apart), k row
+// ((8 + 2 + 2r) cells square, rows kFusedBlurRowStride floats apart; with
+// learnable features, fd feature planes after the colours), k row
 // partials of a chunk of classes over the 10 x 10 message tile (planes of
 // kFusedBlurPartStride floats, two spare), the message tile, and the
 // compatibility when given.  A chunk's class slots are even (two classes per
 // wavefront instruction): the most that fit 160 KB with the rest,
 // compatibility included, up to the classes rounded up to even.
 constexpr int kFusedBlurPartStride = (kFusedBlurCells + 2) * (kFusedBlurCells + 2) + 2;
-constexpr int blur_iter_slots(int k, int CM) {
+constexpr int blur_iter_slots(int k, int CM, int fd = 0) {
     const int fs = kFusedBlurCells + 2 + (k - 1), mt = (kFusedBlurCells + 2) * (kFusedBlurCells + 2);
-    const int room = 160 * 1024 / 4 - (CM + 3) * fs * kFusedBlurRowStride - CM * mt - CM * CM;
+    const int room = 160 * 1024 / 4 - (CM + 3 + fd) * fs * kFusedBlurRowStride - CM * mt - CM * CM;
     const int cap = room / (k * kFusedBlurPartStride) / 2 * 2, full = (CM + 1) / 2 * 2;
     const int sl = cap < full ? cap : full;
     return sl < 2 ? 2 : sl;
 }
-constexpr int blur_iter_chunk(int k, int CM) {
-    return blur_iter_slots(k, CM) < CM ? blur_iter_slots(k, CM) : CM;
+constexpr int blur_iter_chunk(int k, int CM, int fd = 0) {
+    return blur_iter_slots(k, CM, fd) < CM ? blur_iter_slots(k, CM, fd) : CM;
 }
-inline size_t blur_iter_lds_bytes(int k, int CM, bool with_compat) {
+inline size_t blur_iter_lds_bytes(int k, int CM, bool with_compat, int fd = 0) {
     const size_t fs = kFusedBlurCells + 2 + (k - 1), mt = (kFusedBlurCells + 2) * (kFusedBlurCells + 2);
-    return sizeof(float) * ((size_t)(CM + 3) * fs * kFusedBlurRowStride +
-                            (size_t)k * blur_iter_slots(k, CM) * kFusedBlurPartStride +
+    return sizeof(float) * ((size_t)(CM + 3 + fd) * fs * kFusedBlurRowStride +
+                            (size_t)k * blur_iter_slots(k, CM, fd) * kFusedBlurPartStride +
                             (size_t)CM * mt + (with_compat ? (size_t)CM * CM : 0));
 }
 hipError_t launch_blur_iter(const BlurIterArgs& a, int k, hipStream_t stream);
@@ -282,16 +287,18 @@ hipError_t launch_blur_iter_k11(const BlurIterArgs& a, hipStream_t stream);
 hipError_t launch_blur_iter_k13(const BlurIterArgs& a, hipStream_t stream);
 hipError_t launch_blur_iter_k15(const BlurIterArgs& a, hipStream_t stream);
 
-// ---- initialisation of the fused blur path (4 x 4 pooling): softmax(U)
-// and the image, averaged over the cells, in one launch over tiles of
-// kBlurInitTX x kBlurInitTY cells.
+// ---- initialisation of the fused blur path (4 x 4 pooling): softmax(U),
+// the image and the learnable features (if any), averaged over the cells, in
+// one launch over tiles of kBlurInitTX x kBlurInitTY cells.
 constexpr int kBlurInitTX = 8, kBlurInitTY = 4;
 struct BlurInitArgs {
     const float* unary;   // U [B][C][H][W], 8-byte aligned
     const float* image;   // [B][3][H][W], 8-byte aligned
     float* qbar;          // pooled softmax(U) [B][C][Hp][Wp] (out)
     float* pcol;          // pooled colours [B][3][Hp][Wp] (out)
-    int B, C, H, W, Hp, Wp;
+    const float* feat;    // learnable features [B][D][H][W] (8-byte aligned), or null
+    float* pfeat;         // pooled features [B][D][Hp][Wp] (out, with feat)
+    int B, C, H, W, Hp, Wp, D;
 };
 hipError_t launch_blur_init(const BlurInitArgs& a, hipStream_t stream);
 

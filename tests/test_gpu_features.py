@@ -95,7 +95,13 @@ BLUR_CASES = [
 ]
 
 
-@pytest.mark.parametrize("seed,B,C,H,W,k,T,D,center,gen_mu,s,tg", BLUR_CASES)
+# forward only: the fused 4 x 4 round with features on a ragged grid (Hp = 9,
+# Wp = 13, so the word-by-word staging), 13 classes (the general class width),
+# two window rows per wavefront (k = 9 with features) and a general compatibility
+BLUR_FWD_EXTRA = [(36, 2, 13, 36, 52, 9, 2, 3, False, True, 4, 5.0)]
+
+
+@pytest.mark.parametrize("seed,B,C,H,W,k,T,D,center,gen_mu,s,tg", BLUR_CASES + BLUR_FWD_EXTRA)
 def test_forward_with_features_and_blur(torch_cuda, crf, oracle_mod, seed, B, C, H, W, k, T, D,
                                         center, gen_mu, s, tg):
     torch = torch_cuda
