@@ -9,8 +9,10 @@
 //      (zero outside the grid; 16-byte loads where the grid rows allow);
 //   2. computes the pooled message (Eq. 6 on the pooled grid, offsets of 4
 //      pixels, Eq. 4 weights from pooled colours) for its 8 x 8 cells and the
-//      one-cell ring that the bilinear upsampling of its pixels reads: each
-//      of the 8 wavefronts takes window rows w and w + 8; a lane holds the
+//      one-cell ring that the bilinear upsampling of its pixels reads: one
+//      wavefront per window row for k = 9, 11 (up to 21 classes, no feature
+//      planes), else eight wavefronts taking rows w and w + 8 (the first 512
+//      threads also own the pixels); a lane holds the
 //      rows' weights of four horizontally adjacent cells in registers and
 //      reads each staged row once (16-byte reads) for all four, the two
 //      halves of a wavefront taking the even and the odd classes; the k row
@@ -23,8 +25,8 @@
 //      the pooled Q_{t+1} the next launch reads.
 // So each iteration reads the unary once and the pooled state, and the
 // pooled message is never written to memory.  The first iteration's input,
-// softmax(U) and the image averaged over the cells, comes from one
-// initialisation launch (blur_init_kernel).
+// softmax(U), the image and the learnable features averaged over the cells,
+// comes from one initialisation launch (blur_init_kernel).
 #include "crf_internal.h"
 
 #ifndef CRF_BLUR_K
@@ -223,7 +225,7 @@ __global__ __launch_bounds__((BlurShape<K, CM, FT>::NT)) void blur_iter_kernel(c
         for (int i = tid; i < C * C; i += NT) Mu[(i / C) * CM + i % C] = a.mu[i];
     __syncthreads();
 
-    // ---- pooled message: wavefront w takes window rows w + 8 j (j < RW).
+    // ---- pooled message: wavefront w takes window rows w + NWAVE j (j < RW).
     // Lane (h, mi, qd): half h = lane / 32 takes the classes of parity h,
     // (mi, qd) the four cells (mi, 4 qd + i), i < 4, of the 10 x 10 message
     // tile (qd = 2 computes two cells past the tile, which are discarded), so
