@@ -201,6 +201,12 @@ def test_iteration_counts(torch_cuda, crf, oracle_mod, T):
     for variant in (0, 1):
         p = lib_params(filter_size=5, variant=variant)
         check(run_gpu(torch_cuda, crf, U, I, p, T), run_oracle(oracle_mod, U, I, p, T), f"T={T}")
+    # the blur path on a 10 x 13-cell grid: the fused 4 x 4 form (T = 1: the
+    # first round is also the last and writes Q) and the general form
+    for blur in (4, 2):
+        p = lib_params(filter_size=5, blur=blur)
+        check(run_gpu(torch_cuda, crf, U, I, p, T), run_oracle(oracle_mod, U, I, p, T),
+              f"T={T} blur={blur}")
 
 
 def test_zero_iterations_is_softmax(torch_cuda, crf):
