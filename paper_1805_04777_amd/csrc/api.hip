@@ -1318,17 +1318,52 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         st = launch(ctx, kPool, stream, "blur_pool",
                     [&] { return launch_pool(qs(0), pqs(0), B, C, H, W, s, 0, stream); });
         if (st != CONVCRF_OK) return st;
-        for (int t = 0; t < iters; ++t) {
-            a.src = pqs(t);
-            st = launch(ctx, kBlurMsg, stream, "blur_message",
-                        [&] { return launch_pmsg(a, k, nchunks, lds, stream); });
-            if (st != CONVCRF_OK) return st;
-            st = launch(ctx, kBlurUpd, stream, "blur_update", [&] {
-                return launch_blur_update(pm, unary, mu_dev, qs(t + 1),
-                                          t + 1 < iters ? pqs(t + 1) : nullptr, B, C, H, W, s,
-                                          stream);
-            });
-            if (st != CONVCRF_OK) return st;
+        // 4 x 4 pooling: the fused round (as convcrf_meanfield), writing both
+        // Q^{t+1} and its pooled form
+        const auto al8 = [](const void* ptr) { return reinterpret_cast<uintptr_t>(ptr) % 8 == 0; };
+        if (s == kFusedBlurFactor && k >= 3 && B <= 65535 && D <= kMaxFeat && al8(unary) &&
+            al8(qs(0)) && Hg <= 65535 * kFusedBlurCells &&
+            blur_iter_lds_bytes(k, C == 19 || C == 21 ? C : (C <= 8 ? 8 : 24), mu_dev != nullptr,
+                                D > 0 ? kMaxFeat : 0) <= kLdsLimit) {
+            BlurIterArgs bi{};
+            bi.pcol = pf;
+            bi.unary = unary;
+            bi.mu = mu_dev;
+            bi.B = B;
+            bi.C = C;
+            bi.H = H;
+            bi.W = W;
+            bi.Hp = Hg;
+            bi.Wp = Wg;
+            bi.include_center = p.include_center;
+            bi.center_w = a.center_w;
+            bi.neg_beta = a.neg_beta;
+            bi.taps = a.taps;
+            bi.sfeat = psf;
+            bi.D = D;
+            bi.w_smooth = p.w_smooth;
+            bi.neg_gamma = a.neg_gamma;
+            for (int t = 0; t < iters; ++t) {
+                bi.qbar = pqs(t);
+                bi.q_full = qs(t + 1);
+                bi.qbar_out = t + 1 < iters ? pqs(t + 1) : nullptr;
+                st = launch(ctx, kBlurIter, stream, "blur_iteration",
+                            [&] { return launch_blur_iter(bi, k, stream); });
+                if (st != CONVCRF_OK) return st;
+            }
+        } else {
+            for (int t = 0; t < iters; ++t) {
+                a.src = pqs(t);
+                st = launch(ctx, kBlurMsg, stream, "blur_message",
+                            [&] { return launch_pmsg(a, k, nchunks, lds, stream); });
+                if (st != CONVCRF_OK) return st;
+                st = launch(ctx, kBlurUpd, stream, "blur_update", [&] {
+                    return launch_blur_update(pm, unary, mu_dev, qs(t + 1),
+                                              t + 1 < iters ? pqs(t + 1) : nullptr, B, C, H, W,
+                                              s, stream);
+                });
+                if (st != CONVCRF_OK) return st;
+            }
         }
     } else if (run && p.features) {
         FeatArgs f = feat_args(p, unary, image, mu_dev, B, C, H, W);

@@ -425,17 +425,17 @@ __global__ __launch_bounds__((BlurShape<K, CM, FT>::NT)) void blur_iter_kernel(c
     }
     softmax_regs<CM, EXACT>(z0, C);
     softmax_regs<CM, EXACT>(z1, C);
-    if (a.q_full) {
-        if (!pix_ok) return;
+    if (a.q_full && pix_ok) {
         float* q = a.q_full + (size_t)b * a.C * HW + (size_t)py * W + px;
 #pragma unroll
         for (int c = 0; c < CM; ++c)
             if (EXACT || c < C)
                 *reinterpret_cast<float2*>(q + (size_t)c * HW) = make_float2(z0[c], z1[c]);
-        return;
     }
+    if (!a.qbar_out) return;   // uniform over the grid
     // the cell's 16 pixels: two per lane, eight consecutive lanes
-    float* dq = a.qbar_out + (size_t)b * a.C * HWp + (size_t)ccy * Wp + ccx;
+    float* dq = a.qbar_out + (size_t)b * a.C * HWp + (size_t)(pix_ok ? ccy : 0) * Wp +
+                (pix_ok ? ccx : 0);
 #pragma unroll
     for (int c = 0; c < CM; ++c) {
         if (!EXACT && c >= C) continue;
@@ -482,7 +482,7 @@ hipError_t CRF_CAT(launch_blur_iter_k, CRF_BLUR_K)(const BlurIterArgs& a, hipStr
     } else {
         if (a.C < 1 || a.C > kMaxC || a.Hp * kS != a.H || a.Wp * kS != a.W || a.B < 1 ||
             a.B > 65535 || a.Hp > 65535 * kNC || a.D < 0 || a.D > kMaxFeat ||
-            (a.D > 0 && !a.sfeat))
+            (a.D > 0 && !a.sfeat) || (!a.q_full && !a.qbar_out))
             return hipErrorInvalidValue;
         switch (a.C) {
             case 19: return launch_one<K, 19, true>(a, stream);

@@ -240,8 +240,9 @@ struct BlurIterArgs {
     const float* pcol;    // pooled colours [B][3][Hp][Wp]
     const float* unary;   // U [B][C][H][W], 8-byte aligned
     const float* mu;      // device C x C compatibility or null (Potts)
-    float* qbar_out;      // pooled Q_{t+1} (when q_full is null)
-    float* q_full;        // Q [B][C][H][W] (8-byte aligned), the last iteration
+    float* qbar_out;      // pooled Q_{t+1}, or null
+    float* q_full;        // Q_{t+1} [B][C][H][W] (8-byte aligned), or null (at least one
+                          // of the two is given: both for the reverse mode's recompute)
     int B, C, H, W, Hp, Wp;
     int include_center;
     float center_w;       // K(p, p) = w_app + w_smooth when the centre is included
