@@ -1267,10 +1267,6 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     char* qbase = static_cast<char*>(ctx->b_q.p);
     auto qs = [&](int t) { return reinterpret_cast<float*>(qbase + slice * t); };
 
-    // forward: Q^0 = softmax(U), then the fused rounds, keeping every Q^t
-    st = launch(ctx, kSoftmax, stream, "softmax",
-                [&] { return launch_softmax(unary, qs(0), B, C, H * W, stream); });
-    if (st != CONVCRF_OK) return st;
     float* pf = static_cast<float*>(ctx->pool_f.p);
     // blur with learnable features: the pooled features follow the pooled colours
     float* psf = s > 1 && D > 0 ? pf + ((size_t)B * 3 * Hg * Wg + 63) / 64 * 64 : nullptr;
@@ -1279,6 +1275,40 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         return static_cast<float*>(ctx->pool_q.p) + (size_t)t * B * C * Hg * Wg;
     };
     float* pm = static_cast<float*>(ctx->pool_m.p);
+    // 4 x 4 pooling: the recompute takes the fused form of convcrf_meanfield
+    // (one initialisation launch, then one fused round per iteration, each
+    // writing Q^{t+1} and its pooled form)
+    const auto al8 = [](const void* ptr) { return reinterpret_cast<uintptr_t>(ptr) % 8 == 0; };
+    const bool fused_blur =
+        run && s == kFusedBlurFactor && k >= 3 && B <= 65535 && D <= kMaxFeat && al8(unary) &&
+        al8(image) && (D == 0 || al8(p.features)) && al8(qs(0)) &&
+        (Hg + kBlurInitTY - 1) / kBlurInitTY <= 65535 &&
+        blur_iter_lds_bytes(k, C == 19 || C == 21 ? C : (C <= 8 ? 8 : 24), mu_dev != nullptr,
+                            D > 0 ? kMaxFeat : 0) <= kLdsLimit;
+
+    // forward: Q^0 = softmax(U), then the rounds, keeping every Q^t
+    if (fused_blur) {
+        BlurInitArgs bin{};
+        bin.unary = unary;
+        bin.image = image;
+        bin.q_full = qs(0);
+        bin.qbar = pqs(0);
+        bin.pcol = pf;
+        bin.B = B;
+        bin.C = C;
+        bin.H = H;
+        bin.W = W;
+        bin.Hp = Hg;
+        bin.Wp = Wg;
+        bin.feat = D > 0 ? p.features : nullptr;
+        bin.pfeat = psf;
+        bin.D = D;
+        st = launch(ctx, kPool, stream, "blur_pool", [&] { return launch_blur_init(bin, stream); });
+    } else {
+        st = launch(ctx, kSoftmax, stream, "softmax",
+                    [&] { return launch_softmax(unary, qs(0), B, C, H * W, stream); });
+    }
+    if (st != CONVCRF_OK) return st;
     if (run && s > 1) {
         // the pooled message of Sec. 4.2 (as convcrf_meanfield), with every
         // Q^t kept at full resolution
@@ -1305,26 +1335,23 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
         a.tiles_x = (Wg + kPmsgTW - 1) / kPmsgTW;
         a.tiles_per_img = a.tiles_x * ((Hg + kPmsgTH - 1) / kPmsgTH);
         a.ntiles = a.tiles_per_img * B;
-        st = launch(ctx, kPool, stream, "blur_pool",
-                    [&] { return launch_pool(image, pf, B, 3, H, W, s, 0, stream); });
-        if (st != CONVCRF_OK) return st;
-        if (D > 0) {
+        if (!fused_blur) {
             st = launch(ctx, kPool, stream, "blur_pool",
-                        [&] { return launch_pool(p.features, psf, B, D, H, W, s, 0, stream); });
+                        [&] { return launch_pool(image, pf, B, 3, H, W, s, 0, stream); });
+            if (st != CONVCRF_OK) return st;
+            if (D > 0) {
+                st = launch(ctx, kPool, stream, "blur_pool", [&] {
+                    return launch_pool(p.features, psf, B, D, H, W, s, 0, stream);
+                });
+                if (st != CONVCRF_OK) return st;
+            }
+            // Q^0 pooled here; every update also writes its pooled Q^{t+1},
+            // kept for the reverse rounds
+            st = launch(ctx, kPool, stream, "blur_pool",
+                        [&] { return launch_pool(qs(0), pqs(0), B, C, H, W, s, 0, stream); });
             if (st != CONVCRF_OK) return st;
         }
-        // Q^0 pooled here; every update also writes its pooled Q^{t+1}, kept
-        // for the reverse rounds
-        st = launch(ctx, kPool, stream, "blur_pool",
-                    [&] { return launch_pool(qs(0), pqs(0), B, C, H, W, s, 0, stream); });
-        if (st != CONVCRF_OK) return st;
-        // 4 x 4 pooling: the fused round (as convcrf_meanfield), writing both
-        // Q^{t+1} and its pooled form
-        const auto al8 = [](const void* ptr) { return reinterpret_cast<uintptr_t>(ptr) % 8 == 0; };
-        if (s == kFusedBlurFactor && k >= 3 && B <= 65535 && D <= kMaxFeat && al8(unary) &&
-            al8(qs(0)) && Hg <= 65535 * kFusedBlurCells &&
-            blur_iter_lds_bytes(k, C == 19 || C == 21 ? C : (C <= 8 ? 8 : 24), mu_dev != nullptr,
-                                D > 0 ? kMaxFeat : 0) <= kLdsLimit) {
+        if (fused_blur) {
             BlurIterArgs bi{};
             bi.pcol = pf;
             bi.unary = unary;

@@ -10,7 +10,8 @@
 //                        Q, its s x s average for the next pooled message,
 //                        or both (any s; blur_update4_kernel for s = 4, 8)
 //   blur_init_kernel     initialisation of the fused blur path (4 x 4):
-//                        softmax(U) and the image, pooled, in one launch
+//                        softmax(U), the image and the features, pooled,
+//                        in one launch, and optionally softmax(U) itself
 #include "crf_internal.h"
 
 namespace convcrf {
@@ -428,7 +429,8 @@ __global__ __launch_bounds__(512) void blur_update4_kernel(
 // Initialisation of the blur path for a 4 x 4 pooling (Alg. 1, Sec. 4.2):
 // Q_0 = softmax(U) per pixel and its 4 x 4 cell averages, and the cell
 // averages of the image (the pooled colours of the message's weights) and of
-// the learnable features when given, in one launch.  A work-group owns 8 x 4 cells (32 x 16 pixels): eight
+// the learnable features when given, in one launch; optionally Q_0 itself as
+// well.  A work-group owns 8 x 4 cells (32 x 16 pixels): eight
 // consecutive lanes per cell and two horizontally adjacent pixels per lane,
 // so a wavefront reads 128-byte rows of every plane; a cell's sums are taken
 // across its eight lanes.
@@ -465,6 +467,13 @@ __global__ __launch_bounds__(256) void blur_init_kernel(const BlurInitArgs a) {
     }
     softmax_regs<CM, EXACT>(z0, C);
     softmax_regs<CM, EXACT>(z1, C);
+    if (a.q_full && pix_ok) {   // Q_0 itself, for the reverse mode's recompute
+        float* qf = a.q_full + (size_t)b * a.C * HW + poff;
+#pragma unroll
+        for (int c = 0; c < CM; ++c)
+            if (EXACT || c < C)
+                *reinterpret_cast<float2*>(qf + (size_t)c * HW) = make_float2(z0[c], z1[c]);
+    }
     const size_t cell = (size_t)(pix_ok ? ccy : 0) * Wp + (pix_ok ? ccx : 0);
     constexpr float inv = 1.0f / (S4 * S4);
     float* dq = a.qbar + (size_t)b * a.C * HWp + cell;
@@ -589,7 +598,7 @@ hipError_t launch_blur_init(const BlurInitArgs& a, hipStream_t stream) {
         a.Hp * kFusedBlurFactor != a.H || a.Wp * kFusedBlurFactor != a.W ||
         (a.Hp + kBlurInitTY - 1) / kBlurInitTY > 65535 || !a.unary || !a.image || !a.qbar ||
         !a.pcol || !al8(a.unary) || !al8(a.image) || a.D < 0 || a.D > kMaxFeat ||
-        (a.feat && (!a.pfeat || a.D < 1 || !al8(a.feat))))
+        (a.feat && (!a.pfeat || a.D < 1 || !al8(a.feat))) || (a.q_full && !al8(a.q_full)))
         return hipErrorInvalidValue;
     const dim3 grid((a.Wp + kBlurInitTX - 1) / kBlurInitTX, (a.Hp + kBlurInitTY - 1) / kBlurInitTY,
                     a.B);

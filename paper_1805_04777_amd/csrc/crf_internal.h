@@ -299,6 +299,7 @@ struct BlurInitArgs {
     float* pcol;          // pooled colours [B][3][Hp][Wp] (out)
     const float* feat;    // learnable features [B][D][H][W] (8-byte aligned), or null
     float* pfeat;         // pooled features [B][D][Hp][Wp] (out, with feat)
+    float* q_full;        // softmax(U) itself [B][C][H][W] (out, 8-byte aligned), or null
     int B, C, H, W, Hp, Wp, D;
 };
 hipError_t launch_blur_init(const BlurInitArgs& a, hipStream_t stream);

@@ -467,3 +467,29 @@ def test_profiling_counts_launches(torch_cuda, crf):
     assert crf.profile_read("blur_pool")[1] == 1
     assert crf.profile_read("no_such_kernel") == (0.0, 0)
     crf.profile_enable(False)
+
+
+def test_profiling_counts_blur_backward(torch_cuda, crf):
+    """The reverse mode recomputes the forward pass.  With 4 x 4 pooling that
+    is one initialisation launch (softmax(U) itself and pooled, the pooled
+    image) and one fused round per iteration; with 2 x 2 pooling the general
+    form: softmax, two poolings, then a message and an update per iteration."""
+    torch = torch_cuda
+    U = torch.randn(1, 21, 64, 64, device="cuda")
+    I = torch.rand(1, 3, 64, 64, device="cuda")
+    G = torch.randn_like(U)
+    crf.profile_enable(True)
+    crf.meanfield_backward(U, I, lib_params(blur=4, filter_size=5), 3, G)
+    torch.cuda.synchronize()
+    assert crf.profile_read("blur_pool")[1] == 1
+    assert crf.profile_read("softmax")[1] == 0
+    assert crf.profile_read("blur_iteration")[1] == 3
+    assert crf.profile_read("blur_message")[1] == 0 and crf.profile_read("blur_update")[1] == 0
+    crf.profile_enable(True)
+    crf.meanfield_backward(U, I, lib_params(blur=2, filter_size=5), 3, G)
+    torch.cuda.synchronize()
+    assert crf.profile_read("softmax")[1] == 1
+    assert crf.profile_read("blur_pool")[1] == 2
+    assert crf.profile_read("blur_message")[1] == 3 and crf.profile_read("blur_update")[1] == 3
+    assert crf.profile_read("blur_iteration")[1] == 0
+    crf.profile_enable(False)
