@@ -151,22 +151,31 @@ def algorithmic_per_launch(kname: str, wl, D: int = 0):
             return ((8 * C + 22 + 5 * D + 6) * taps + 2 * C * C) * px, (16 * C + 12 + 12 * D) * px
         return (6 * C + 22) * taps * px + 2 * C * C * px, (16 * C + 12) * px
     if kname == "bwd_point":
-        # T + 1 launches per call: T undo a round (dot, dZ, dU, Potts dM: 7C
-        # flops; read Q, dQ and dU except on the first, write dU, dM and -dZ),
-        # the last one only the initial softmax (5C; read Q, dQ, dU, write dU)
+        # T + 1 launches per call.  T undo a round: dot, dZ, dU and the Potts
+        # dM (7C flops); read Q, dQ and, except on the first, dU; write dU
+        # and dM (with Potts no -dZ plane is written).  The last one takes
+        # only the initial softmax's adjoint (5C; read Q, dQ, dU, write dU).
+        # dQ is grad_q on the first; with blur the later ones read it on the
+        # pooled grid (the pooling's transpose applied in place).
+        dq_later = 4 * C / (wl.blur * wl.blur)
         rounds = 7 * C * T + 5 * C
-        rbytes = 20 * C * T + 4 * C * (T - 1) + 16 * C
+        rbytes = (12 * C * T + 4 * C + dq_later * (T - 1) + 4 * C * (T - 1)
+                  + 12 * C + dq_later)
         return rounds * px / (T + 1), rbytes * px / (T + 1)
     if kname == "bwd_reduce":
         return 0, 0
     if kname == "bwd_blur_transpose":
-        # per round: the upsampling transposed for dL/dM and -dL/dZ (a
-        # 3s x 3s gather per cell and class, separable: about 12 flop per
-        # pixel and class; full-resolution planes read, pooled written) and
-        # the pooling transposed (pooled read, full-resolution written);
-        # averaged over the three launches
+        # one launch per round (with Potts -dL/dZ follows from dL/dM): the
+        # bilinear upsampling transposed for dL/dM, each full-resolution
+        # value reaching four cells (8 flop per pixel and class; the
+        # full-resolution planes read, the pooled ones written); with
+        # features one more at the end, the pooling's transpose of dL/dF
+        # (pooled read, full resolution written).  Averaged over the launches.
         s2 = wl.blur * wl.blur
-        return 12 * C * px * 2 / 3 + C * px / 3, (4 * C + 4 * C / s2) * px
+        n = T + (1 if D else 0)
+        fl = 8 * C * px * T + D * px
+        by = 4 * (C * T + D) * (px + px / s2)
+        return fl / n, by / n
     raise KeyError(kname)
 
 

@@ -1231,7 +1231,8 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     const size_t slice = (qbytes + 255) / 256 * 256;
     if ((st = ensure(ctx, ctx->b_q, slice * (iters + 1))) != CONVCRF_OK) return st;
     if (run) {
-        if ((st = ensure(ctx, ctx->b_dq, slice * 2)) != CONVCRF_OK) return st;
+        // dL/dQ^t ping-pong at full resolution (with blur it stays pooled)
+        if (s == 1 && (st = ensure(ctx, ctx->b_dq, slice * 2)) != CONVCRF_OK) return st;
         if ((st = ensure(ctx, ctx->b_dm, slice)) != CONVCRF_OK) return st;
         if (grad_compat && !potts_dz)
             if ((st = ensure(ctx, ctx->b_dp, slice)) != CONVCRF_OK) return st;
@@ -1481,17 +1482,21 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     float* pdp = pdm ? pdm + pn : nullptr;
     float* pdq = pdm ? pdm + 2 * pn : nullptr;
     ba.dp = s > 1 ? (dp ? pdp : nullptr) : dp;
+    // dL/dQ^{t+1}: grad_q for the last round; with blur, the pooled adjoint of
+    // the round after (dq_s = s), read in place through the pooling's transpose
     const float* dq = grad_q;
+    int dq_s = 1;
     for (int t = iters - 1; t >= 0; --t) {
         const int acc = t != iters - 1;
         st = launch(ctx, kBwdPoint, stream, "bwd_point", [&] {
             return launch_bwd_point(qs(t + 1), dq, mu_dev, grad_unary, dm, dp, B, C,
-                                    (long long)H * W, acc, stream);
+                                    (long long)H * W, acc, stream, W, dq_s);
         });
         if (st != CONVCRF_OK) return st;
-        float* dq_next = reinterpret_cast<float*>(static_cast<char*>(ctx->b_dq.p) + slice * (t & 1));
+        float* dq_next = nullptr;
         ba.accumulate = acc;
         if (s == 1) {
+            dq_next = reinterpret_cast<float*>(static_cast<char*>(ctx->b_dq.p) + slice * (t & 1));
             ba.q = qs(t);
             ba.dq_out = dq_next;
             st = launch(ctx, kBwdMsg, stream, "bwd_message",
@@ -1505,8 +1510,9 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
             }
         } else {
             // M = upsample(pooled message of avgpool(Q^t)): the transpose of
-            // the upsampling (for dL/dM and, for dL/dmu, -dL/dZ), the pooled
-            // adjoint message, the transpose of the pooling
+            // the upsampling (for dL/dM and, for dL/dmu, -dL/dZ), then the
+            // pooled adjoint message; the pooling's transpose is applied by
+            // the next bwd_point as it reads dL/dQ^t
             st = launch(ctx, kBwdBlurT, stream, "bwd_blur_transpose", [&] {
                 return launch_upsample_t(dm, pdm, B, C, Hg, Wg, s, stream);
             });
@@ -1529,10 +1535,8 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
                 });
                 if (st != CONVCRF_OK) return st;
             }
-            st = launch(ctx, kBwdBlurT, stream, "bwd_blur_transpose", [&] {
-                return launch_pool_t(pdq, dq_next, B, C, Hg, Wg, s, stream);
-            });
-            if (st != CONVCRF_OK) return st;
+            dq_next = pdq;
+            dq_s = s;
         }
         dq = dq_next;
     }
@@ -1558,7 +1562,7 @@ convcrf_status convcrf_meanfield_backward(convcrf_ctx* ctx, const float* unary,
     // Q^0 = softmax(U)
     st = launch(ctx, kBwdPoint, stream, "bwd_point", [&] {
         return launch_bwd_point(qs(0), dq, nullptr, grad_unary, nullptr, nullptr, B, C,
-                                (long long)H * W, iters > 0, stream);
+                                (long long)H * W, iters > 0, stream, W, dq_s);
     });
     if (st != CONVCRF_OK) return st;
     if (grad_compat || grad_kernel)

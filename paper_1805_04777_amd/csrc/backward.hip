@@ -427,22 +427,33 @@ hipError_t CONVCRF_BWD_CAT(launch_bwd_msg_k, CRF_BWD_K)(const BwdArgs& a, hipStr
 #else
 
 // ---------------------------------------------------------------- pointwise
-template <int CM>
+// S > 1: dL/dQ is given on the S x S pooled grid (the pooled adjoint of the
+// blur variant's message); pixel (y, x) takes its cell's value / S^2, the
+// transpose of the average pooling, read in place (W is the image width).
+template <int CM, int S>
 __global__ __launch_bounds__(256) void bwd_point_kernel(
     const float* __restrict__ q, const float* __restrict__ dq, const float* __restrict__ mu,
     float* __restrict__ du, float* __restrict__ dm, float* __restrict__ dp, int C,
-    long long hw, long long npix, int accumulate) {
+    long long hw, long long npix, int accumulate, int W) {
     const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= npix) return;
     const long long b = i / hw;
     const long long base = b * C * hw + (i - b * hw);
+    long long dbase = base, dstride = hw;
+    if constexpr (S > 1) {
+        const int pix = (int)(i - b * hw);   // hw < 2^31
+        const int y = pix / W, x = pix - y * W;
+        dstride = hw / (S * S);
+        dbase = b * C * dstride + (long long)(y / S) * (W / S) + x / S;
+    }
+    constexpr float inv = 1.f / (float)(S * S);
     float qv[CM], dz[CM];
     float dot = 0.f;
 #pragma unroll
     for (int c = 0; c < CM; ++c) {
         if (c < C) {
             qv[c] = q[base + c * hw];
-            dz[c] = dq[base + c * hw];
+            dz[c] = S > 1 ? dq[dbase + c * dstride] * inv : dq[base + c * hw];
             dot = fmaf(qv[c], dz[c], dot);
         }
     }
@@ -663,20 +674,36 @@ hipError_t launch_bwd_message(const BwdArgs& a, int k, hipStream_t stream) {
     }
 }
 
+template <int S>
+void launch_bwd_point_s(const float* q, const float* dq, const float* mu, float* du, float* dm,
+                        float* dp, int C, long long HW, long long npix, int accumulate, int W,
+                        unsigned blocks, hipStream_t stream) {
+    if (C <= 8)
+        hipLaunchKernelGGL((bwd_point_kernel<8, S>), dim3(blocks), dim3(256), 0, stream, q, dq,
+                           mu, du, dm, dp, C, HW, npix, accumulate, W);
+    else
+        hipLaunchKernelGGL((bwd_point_kernel<kMaxC, S>), dim3(blocks), dim3(256), 0, stream, q,
+                           dq, mu, du, dm, dp, C, HW, npix, accumulate, W);
+}
+
 hipError_t launch_bwd_point(const float* q, const float* dq, const float* mu, float* du,
                             float* dm, float* dp, int B, int C, long long HW, int accumulate,
-                            hipStream_t stream) {
+                            hipStream_t stream, int W, int s) {
     const long long npix = (long long)B * HW;
     if (npix == 0) return hipSuccess;
     if (C < 1 || C > kMaxC) return hipErrorInvalidValue;
+    if (s > 1 && (W < s || W % s != 0 || HW % W != 0 || (HW / W) % s != 0 || HW > 0x7fffffffLL))
+        return hipErrorInvalidValue;
     const long long blocks = (npix + 255) / 256;
     if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
-    if (C <= 8)
-        hipLaunchKernelGGL((bwd_point_kernel<8>), dim3((unsigned)blocks), dim3(256), 0, stream,
-                           q, dq, mu, du, dm, dp, C, HW, npix, accumulate);
-    else
-        hipLaunchKernelGGL((bwd_point_kernel<kMaxC>), dim3((unsigned)blocks), dim3(256), 0,
-                           stream, q, dq, mu, du, dm, dp, C, HW, npix, accumulate);
+    const unsigned nb = (unsigned)blocks;
+    switch (s) {
+        case 1: launch_bwd_point_s<1>(q, dq, mu, du, dm, dp, C, HW, npix, accumulate, W, nb, stream); break;
+        case 2: launch_bwd_point_s<2>(q, dq, mu, du, dm, dp, C, HW, npix, accumulate, W, nb, stream); break;
+        case 4: launch_bwd_point_s<4>(q, dq, mu, du, dm, dp, C, HW, npix, accumulate, W, nb, stream); break;
+        case 8: launch_bwd_point_s<8>(q, dq, mu, du, dm, dp, C, HW, npix, accumulate, W, nb, stream); break;
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

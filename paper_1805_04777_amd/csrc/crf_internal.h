@@ -437,9 +437,11 @@ hipError_t launch_bwd_msg_k15(const BwdArgs& a, hipStream_t stream);
 //   dm(l') = -sum_l mu[l][l'] dZ(l) (mu null = Potts) when dm is set;
 //   dp = -dZ when dp is set.
 // q, dq, du, dm, dp: [B][C][H][W] with HW = H * W pixels per plane.
+// s > 1: dq is dL/dQ on the s x s pooled grid [B][C][HW / s^2] of an image
+// W pixels wide (s = 2, 4, 8), each pixel taking its cell's value / s^2.
 hipError_t launch_bwd_point(const float* q, const float* dq, const float* mu, float* du,
                             float* dm, float* dp, int B, int C, long long HW,
-                            int accumulate, hipStream_t stream);
+                            int accumulate, hipStream_t stream, int W = 0, int s = 1);
 
 // Blur transposes (the pooled message of Sec. 4.2), [B][C] planes:
 // out [Hp][Wp] = the transpose of the bilinear x s upsampling (half-pixel
