@@ -303,36 +303,24 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
                 for (int c = 0; c < kMaxFeat; ++c) dfa[c] = fmaf(coef, fdif[c], dfa[c]);
             }
         };
-        if constexpr (K <= 7) {
-            // a window row at once; the per-offset constants of the row are
-            // read once per row (n = dx^2 + dy^2 takes R + 1 values in it),
-            // so no table load waits inside the row
+        // a window row at once; the per-offset constants of the row are read
+        // once per row (n = dx^2 + dy^2 takes R + 1 values in it), so no
+        // table load waits inside the row
 #pragma unroll 1
-            for (int dy = -R; dy <= R; ++dy) {
-                float ra[R + 1], rs[R + 1], rn[R + 1];
+        for (int dy = -R; dy <= R; ++dy) {
+            float ra[R + 1], rs[R + 1], rn[R + 1];
 #pragma unroll
-                for (int j = 0; j <= R; ++j) {
-                    const int n = j * j + dy * dy;
-                    ra[j] = a.a_log2[n];
-                    rs[j] = a.smooth[n];
-                    rn[j] = (float)n;
-                }
-#pragma unroll
-                for (int dx = -R; dx <= R; ++dx) {
-                    if (dx == 0 && dy == 0 && !a.include_center) continue;
-                    const int j = dx < 0 ? -dx : dx;
-                    tap(dx, dy, ra[j], rs[j], rn[j]);
-                }
+            for (int j = 0; j <= R; ++j) {
+                const int n = j * j + dy * dy;
+                ra[j] = a.a_log2[n];
+                rs[j] = a.smooth[n];
+                rn[j] = (float)n;
             }
-        } else {
-#pragma unroll 1
-            for (int dy = -R; dy <= R; ++dy) {
-#pragma unroll 1
-                for (int dx = -R; dx <= R; ++dx) {
-                    if (dx == 0 && dy == 0 && !a.include_center) continue;
-                    const int n = dx * dx + dy * dy;
-                    tap(dx, dy, a.a_log2[n], a.smooth[n], (float)n);
-                }
+#pragma unroll
+            for (int dx = -R; dx <= R; ++dx) {
+                if (dx == 0 && dy == 0 && !a.include_center) continue;
+                const int j = dx < 0 ? -dx : dx;
+                tap(dx, dy, ra[j], rs[j], rn[j]);
             }
         }
 #pragma unroll
