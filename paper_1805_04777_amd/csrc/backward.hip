@@ -146,20 +146,34 @@ __device__ __forceinline__ void tile_gram(float* lds, const BwdArgs& a, int tile
 #pragma unroll
     for (int i = 0; i < PX; ++i) {
         const int col = PX * threadIdx.x + i;
-        if (a.dm_sum_scale != 0.f) {
+        // every class of the pixel loaded before the first is stored, all in
+        // flight at once (pixels outside the image read pixel 0 of image 0
+        // and classes past C the last class, both dropped)
+        const bool potts = a.dm_sum_scale != 0.f;
+        const float* src = (potts ? a.dm : a.dp) + (in[i] ? pix[i] : 0);
+        float v[kMaxC];
+#pragma unroll
+        for (int c = 0; c < kMaxC; ++c) v[c] = src[(long long)(c < C ? c : C - 1) * hw];
+        if (potts) {
             // Potts: dM(l) = dZ(l) - sum_l' dZ(l'), so sum_l dM(l) = (1 - C)
             // sum_l' dZ(l') and dZ(l) = dM(l) + sum_l' dM(l') / (1 - C)
             float sum = 0.f;
-            for (int c = 0; c < CP; ++c) {
-                const float v = in[i] && c < C ? a.dm[pix[i] + c * hw] : 0.f;
-                gp[c * SP + col] = v;
-                sum += v;
+#pragma unroll
+            for (int c = 0; c < kMaxC; ++c) {
+                if (c < CP) {
+                    const float x = in[i] && c < C ? v[c] : 0.f;
+                    gp[c * SP + col] = x;
+                    sum += x;
+                }
             }
             const float sh = sum * a.dm_sum_scale;
-            for (int c = 0; c < C; ++c) gp[c * SP + col] = -(gp[c * SP + col] + sh);
+#pragma unroll
+            for (int c = 0; c < kMaxC; ++c)
+                if (c < C) gp[c * SP + col] = -((in[i] ? v[c] : 0.f) + sh);
         } else {
-            for (int c = 0; c < CP; ++c)
-                gp[c * SP + col] = in[i] && c < C ? a.dp[pix[i] + c * hw] : 0.f;
+#pragma unroll
+            for (int c = 0; c < kMaxC; ++c)
+                if (c < CP) gp[c * SP + col] = in[i] && c < C ? v[c] : 0.f;
         }
 #pragma unroll
         for (int c = 0; c < CM; ++c)
