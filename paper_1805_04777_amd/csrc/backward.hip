@@ -449,24 +449,33 @@ __global__ __launch_bounds__(256) void bwd_point_kernel(
         dbase = b * C * dstride + (long long)(y / S) * (W / S) + x / S;
     }
     constexpr float inv = 1.f / (float)(S * S);
-    float qv[CM], dz[CM];
-    float dot = 0.f;
+    // every load issued before the first is used (classes past C re-read
+    // the last class and are dropped)
+    float qv[CM], dz[CM], uo[CM];
 #pragma unroll
     for (int c = 0; c < CM; ++c) {
-        if (c < C) {
-            qv[c] = q[base + c * hw];
-            dz[c] = S > 1 ? dq[dbase + c * dstride] * inv : dq[base + c * hw];
-            dot = fmaf(qv[c], dz[c], dot);
-        }
+        const int cc = c < C ? c : C - 1;
+        qv[c] = q[base + cc * hw];
+        dz[c] = S > 1 ? dq[dbase + cc * dstride] * inv : dq[base + cc * hw];
     }
+    if (accumulate) {
+#pragma unroll
+        for (int c = 0; c < CM; ++c) uo[c] = du[base + (c < C ? c : C - 1) * hw];
+    } else {
+#pragma unroll
+        for (int c = 0; c < CM; ++c) uo[c] = 0.f;
+    }
+    float dot = 0.f;
+#pragma unroll
+    for (int c = 0; c < CM; ++c)
+        if (c < C) dot = fmaf(qv[c], dz[c], dot);
     float sum = 0.f;
 #pragma unroll
     for (int c = 0; c < CM; ++c) {
         if (c < C) {
             dz[c] = qv[c] * (dz[c] - dot);
             sum += dz[c];
-            float* o = du + base + c * hw;
-            *o = accumulate ? *o + dz[c] : dz[c];
+            du[base + c * hw] = accumulate ? uo[c] + dz[c] : dz[c];
             if (dp) dp[base + c * hw] = -dz[c];
         }
     }
