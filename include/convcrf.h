@@ -244,7 +244,10 @@ convcrf_status convcrf_profile_enable(convcrf_ctx *ctx, int enable);
  * (the fused pooled message and update of one iteration, used for blur 4
  * instead of those two), and for
  * convcrf_meanfield_backward "bwd_point", "bwd_message", "bwd_reduce",
- * "bwd_blur_transpose" besides the forward's; "feature_iter" with learnable
+ * "bwd_blur_transpose" (with blur: the upsampling's transpose, one per reverse
+ * round with Potts and two with a general compatibility, and with learnable
+ * features one more for dL/dF through the pooling) besides the forward's;
+ * "feature_iter" with learnable
  * features, "fused_first") since profiling was enabled.  "fused_resident" is one
  * launch running all iterations of a call (CONVCRF_VARIANT_RESIDENT);
  * "fused_first" the first iteration of a fused call (it reads the unary and
