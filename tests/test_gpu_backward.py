@@ -172,6 +172,9 @@ BLUR_CASES = [
     (32, 2, 21, 32, 48, 5, 2, 4, False),
     (33, 1, 19, 40, 64, 7, 3, 8, True),
     (34, 1, 5, 24, 36, 11, 1, 4, False),
+    # 4 x 4 with a general compatibility: the fused recompute with mu, the
+    # -dL/dZ plane and its upsampling transpose, a 9 x 11-cell grid
+    (35, 1, 8, 36, 44, 7, 2, 4, True),
 ]
 
 
