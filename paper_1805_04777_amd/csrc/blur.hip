@@ -20,9 +20,10 @@
 //      chunk at a time).  The unary of its 1024 pixels is prefetched into
 //      registers under this step;
 //   3. per pixel: bilinear upsampling of the message (half-pixel centres,
-//      edge clamp), compatibility, unary and softmax (Alg. 1), then either
-//      the full-resolution Q (the last iteration) or its 4 x 4 cell average,
-//      the pooled Q_{t+1} the next launch reads.
+//      edge clamp), compatibility, unary and softmax (Alg. 1), then the
+//      full-resolution Q (the last iteration), its 4 x 4 cell average (the
+//      pooled Q_{t+1} the next launch reads), or both (every round of the
+//      reverse mode's recompute, which keeps Q^t and its pooled form).
 // So each iteration reads the unary once and the pooled state, and the
 // pooled message is never written to memory.  The first iteration's input,
 // softmax(U), the image and the learnable features averaged over the cells,
