@@ -611,14 +611,23 @@ __global__ __launch_bounds__(256) void pool_t_kernel(const float* __restrict__ i
 }
 
 // ---------------------------------------------------------------- reduce
+constexpr int kMaxGroupSum = kMaxC / 3;
 __global__ __launch_bounds__(256) void group_sum_kernel(const float* __restrict__ part,
                                                         int groups, long long n,
                                                         float* __restrict__ out,
                                                         int accumulate) {
     const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
+    // at most kMaxGroupSum parts (groups of at least three of at most kMaxC
+    // classes), all loaded before the first is added; the sum in group order
+    float v[kMaxGroupSum];
+#pragma unroll
+    for (int g = 0; g < kMaxGroupSum; ++g)
+        v[g] = part[(long long)(g < groups ? g : groups - 1) * n + i];
     float s = accumulate ? out[i] : 0.f;
-    for (int g = 0; g < groups; ++g) s += part[(long long)g * n + i];
+#pragma unroll
+    for (int g = 0; g < kMaxGroupSum; ++g)
+        if (g < groups) s += v[g];
     out[i] = s;
 }
 
@@ -643,8 +652,17 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(ReduceArgs a) {
     const int rows = compat ? a.groups : a.ntiles;
     const int stride = compat ? ne : 5;
     const float* col = compat ? a.gpart + e : a.kpart + (e - ne);
+    // four rows' loads in flight at a time, added in row order
     double s = 0.0;
-    for (int r = threadIdx.x; r < rows; r += 256) s += (double)col[(long long)r * stride];
+    int r = threadIdx.x;
+    for (; r + 3 * 256 < rows; r += 4 * 256) {
+        float v[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) v[j] = col[(long long)(r + 256 * j) * stride];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s += (double)v[j];
+    }
+    for (; r < rows; r += 256) s += (double)col[(long long)r * stride];
     red[threadIdx.x] = s;
     __syncthreads();
     for (int h = 128; h > 0; h >>= 1) {
@@ -779,7 +797,7 @@ hipError_t launch_group_sum(const float* part, int groups, long long n, float* o
                             int accumulate, hipStream_t stream) {
     if (n == 0) return hipSuccess;
     const long long blocks = (n + 255) / 256;
-    if (blocks > 0x7fffffffLL || groups < 1) return hipErrorInvalidValue;
+    if (blocks > 0x7fffffffLL || groups < 1 || groups > kMaxGroupSum) return hipErrorInvalidValue;
     hipLaunchKernelGGL(group_sum_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, part,
                        groups, n, out, accumulate);
     return hipGetLastError();
