@@ -31,9 +31,10 @@ namespace {
 // ---------------------------------------------------------- adjoint message
 
 // Tile plus halo of the 3 colour planes, the D feature planes (FT), the C
-// planes of Q^t and the C planes of dL/dM^t into LDS (LW x LH each at a
-// stride of PS floats, the first staged column is x0, the first row y0);
-// zero outside the image, so that taps there contribute nothing to any sum.
+// planes of Q^t and the C planes of dL/dM^t into LDS (LW x LH each, rows LS
+// >= LW floats apart and planes PS floats apart, the first staged column is
+// x0, the first row y0); zero outside the image and in the row padding, so
+// that taps there contribute nothing to any sum.
 //
 // DMA: every wave issues buffer loads that write 64 consecutive floats of a
 // plane straight into LDS (rows of the padded plane, spread over the waves),
@@ -41,7 +42,7 @@ namespace {
 // image; then waits for all of them.  Otherwise scalar loads through
 // registers, branch-free (an in-image address is read for every element and
 // the value dropped outside) so that many are in flight per thread.
-template <int NT, int LW, int PL, int PS, bool DMA>
+template <int NT, int LW, int LS, int PL, int PS, bool DMA>
 __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b, int y0,
                                              int x0, int c0, int CN) {
     const int C = a.C;
@@ -60,9 +61,9 @@ __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
             const int f = (wave + NW * s) * 64 + lane;
-            const int ly = f / LW, lx = f - ly * LW;
+            const int ly = f / LS, lx = f - ly * LS;
             const int gy = y0 + ly, gx = x0 + lx;
-            const bool ok = f < PL && gy >= 0 && gy < H && gx >= 0 && gx < W;
+            const bool ok = f < PL && lx < LW && gy >= 0 && gy < H && gx >= 0 && gx < W;
             voff[s] = ok ? (unsigned)(gy * W + gx) * 4u : kDmaOob;
         }
         const unsigned lds0 = (unsigned)(size_t)(__attribute__((address_space(3))) float*)lds;
@@ -89,14 +90,14 @@ __device__ __forceinline__ void stage_planes(float* lds, const BwdArgs& a, int b
 #pragma unroll 16
     for (int e = threadIdx.x; e < nplanes * PL; e += NT) {
         const int pl = e / PL, o = e - pl * PL;
-        const int ly = o / LW, lx = o - ly * LW;
+        const int ly = o / LS, lx = o - ly * LS;
         const int gy = y0 + ly, gx = x0 + lx;
         const int pq = pl - 3 - D;   // index among the group's Q and dL/dM planes
         const float* src = pl < 3 ? fb + pl * hw
                                   : (pq < 0 ? sb + (pl - 3) * hw
                                             : (pq < CN ? qb + (c0 + pq) * hw
                                                        : mb + (c0 + pq - CN) * hw));
-        const bool ok = gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
+        const bool ok = lx < LW && gy >= 0 && gy < a.H && gx >= 0 && gx < a.W;
         const float v = src[ok ? (long long)gy * a.W + gx : 0];
         lds[pl * PS + o] = ok ? v : 0.f;
     }
@@ -223,7 +224,8 @@ __device__ __forceinline__ void tile_gram(float* lds, const BwdArgs& a, int tile
 template <int K, int TH, int CM, bool WM, bool DMA, bool FT>
 __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) {
     constexpr int TW = bwd_tile_w(K), NT = TW * TH;
-    constexpr int R = (K - 1) / 2, LW = TW + K - 1, PL = LW * (TH + K - 1);
+    constexpr int R = (K - 1) / 2, LW = TW + K - 1, LS = bwd_row_stride(K);
+    constexpr int PL = LS * (TH + K - 1);
     constexpr int PS = bwd_plane(K, TH, DMA);   // plane stride in LDS
     constexpr int XO = R;                       // staged columns left of the tile
     extern __shared__ float lds[];
@@ -239,7 +241,7 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
     // this work-group's class group: classes c0 .. c0 + CN - 1
     const int c0 = blockIdx.y * a.cgsize;
     const int CN = C - c0 < a.cgsize ? C - c0 : a.cgsize;
-    stage_planes<NT, LW, PL, PS, DMA>(lds, a, b, ty * TH - R, tx * TW - XO, c0, CN);
+    stage_planes<NT, LW, LS, PL, PS, DMA>(lds, a, b, ty * TH - R, tx * TW - XO, c0, CN);
     const float* sq = sf + D * PS;       // the group's CN planes of Q^t
     const float* sm = sq + CN * PS;      // the group's CN planes of dL/dM^t
     __syncthreads();
@@ -253,7 +255,7 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
 #pragma unroll
     for (int c = 0; c < CM; ++c) ma[0][c] = 0.f;
     if (in) {
-        const int oc = (ly + R) * LW + lx + XO;
+        const int oc = (ly + R) * LS + lx + XO;
         const float ir = sc[oc], ig = sc[PS + oc], ib = sc[2 * PS + oc];
         float dmq[CM], dqa[CM];
         int poff[CM];
@@ -277,7 +279,7 @@ __global__ __launch_bounds__(bwd_tile_w(K) * TH) void bwd_msg_kernel(BwdArgs a) 
         // one tap: the offset's appearance log-prefactor al = a_log2[n], its
         // smoothness Gaussian s0 = smooth[n] (positions) and nf = n
         auto tap = [&](int dx, int dy, float al, float s0, float nf) {
-            const int o = oc + dy * LW + dx;
+            const int o = oc + dy * LS + dx;
             const float er = ir - sc[o], eg = ig - sc[PS + o], eb = ib - sc[2 * PS + o];
             const float cd2 = fmaf(er, er, fmaf(eg, eg, eb * eb));
             const float av = __builtin_amdgcn_exp2f(fmaf(a.neg_beta, cd2, al));

@@ -397,9 +397,15 @@ struct BwdArgs {
 // partial sums.
 constexpr int bwd_tile_w(int k) { return k <= 7 ? 32 : 16; }
 constexpr int bwd_gram_rows(int C) { return (C + 2) / 3 * 3; }
+// Floats between staged rows in LDS.  A half-wavefront (32 lanes) reads one
+// row of a 32-pixel tile, but two rows of a 16-pixel one (k > 7); those rows
+// are padded to 48 floats, 16 banks apart, so the two fall in disjoint banks
+// (26 floats at k = 11 wrapped ten lanes onto the same banks).
+constexpr int bwd_row_stride(int k) { return bwd_tile_w(k) == 16 ? 48 : bwd_tile_w(k) + k - 1; }
+static_assert(bwd_row_stride(15) >= 16 + 15 - 1, "the padded rows hold the staged columns");
 constexpr int bwd_plane(int k, int rows, bool dma) {
-    return dma ? ((bwd_tile_w(k) + k - 1) * (rows + k - 1) + 63) / 64 * 64
-               : (bwd_tile_w(k) + k - 1) * (rows + k - 1);
+    return dma ? (bwd_row_stride(k) * (rows + k - 1) + 63) / 64 * 64
+               : bwd_row_stride(k) * (rows + k - 1);
 }
 // cn: classes of one group (C with one group).
 constexpr size_t bwd_lds_bytes(int k, int C, int rows, bool dma, int D, int cn) {
