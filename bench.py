@@ -179,23 +179,33 @@ def algorithmic_per_launch(kname: str, wl, D: int = 0):
     raise KeyError(kname)
 
 
-def source_hash() -> str:
-    with open(ITER_SRC, "rb") as f:
+def source_hash(path: str = ITER_SRC) -> str:
+    with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def load_counters(workload: str, kernel: str):
+def counters_key(workload: str, kernel: str, D: int = 0) -> str:
+    """Key of a kernel's record in profiles/counters.json; runs with learnable
+    features have their own records."""
+    return f"{workload}{'+features' if D else ''}/{kernel}"
+
+
+def load_counters(workload: str, kernel: str, D: int = 0):
     """Counter figures per launch of `kernel` on `workload` from the committed
     rocprofv3 passes (profiles/counters.json): HBM bytes (FETCH_SIZE and
     WRITE_SIZE, scaled by what they read for a plain copy) and VALU
     instructions (SQ_INSTS_VALU); None unless they were taken on the current
-    kernel source."""
+    source of the kernel (the file a record names, csrc/iter.hip if none)."""
     try:
         with open(COUNTERS) as f:
-            rec = json.load(f)[f"{workload}/{kernel}"]
+            rec = json.load(f)[counters_key(workload, kernel, D)]
     except (OSError, KeyError, ValueError):
         return None
-    if rec.get("source_sha256_16") != source_hash():
+    src = os.path.join(os.path.dirname(ITER_SRC), rec.get("source", "iter.hip"))
+    try:
+        if rec.get("source_sha256_16") != source_hash(src):
+            return None
+    except OSError:
         return None
     return rec
 
@@ -405,7 +415,7 @@ def main(argv=None):
     # against 8 TB/s, and its measured VALU lane-instructions per second
     # against the 157.3 TFLOP/s lane rate; the higher utilisation is the
     # binding one.  Without current counters the algorithmic fractions decide.
-    ctr = load_counters(args.workload, kname)
+    ctr = load_counters(args.workload, kname, D)
     if ctr:
         hbm_util = ctr["bytes_per_launch"] / avg_s / PEAK_HBM
         valu_util = ctr["valu_insts_per_launch"] * 64 / avg_s / PEAK_VALU_LANE_OPS
