@@ -216,9 +216,11 @@ convcrf_status convcrf_meanfield_noalloc(convcrf_ctx *ctx, const float *unary,
  * params must be those of the forward call); `variant` is ignored.
  * unary, image, grad_q: DEVICE pointers, as for convcrf_meanfield; grad_q
  * [B][C][H][W].  grad_unary must not overlap unary, image or grad_q.
- * The context's workspace grows by (iters + 1) + 3 buffers of [B][C][H][W]
- * floats (Q^0..Q^T, two for dL/dQ, dL/dM), one more with grad_compat, and
- * per-tile partial sums.
+ * The context's workspace grows by (iters + 1) + 1 buffers of [B][C][H][W]
+ * floats (Q^0..Q^T, dL/dM), two more for dL/dQ without blur (with blur it
+ * stays on the pooled grid), one more (-dL/dZ) with grad_compat and a general
+ * compatibility, with blur the pooled Q^t of every round and three pooled
+ * adjoint tensors, and per-tile partial sums.
  * Returns CONVCRF_E_UNSUPPORTED when the window and classes exceed the LDS of
  * one work-group (2C + 3 planes of the tile plus halo); otherwise as
  * convcrf_meanfield.  Asynchronous on `stream`. */
