@@ -10,8 +10,8 @@
 //   2. computes the pooled message (Eq. 6 on the pooled grid, offsets of 4
 //      pixels, Eq. 4 weights from pooled colours) for its 8 x 8 cells and the
 //      one-cell ring that the bilinear upsampling of its pixels reads: one
-//      wavefront per window row for k = 9, 11 (up to 21 classes, no feature
-//      planes), else eight wavefronts taking rows w and w + 8 (the first 512
+//      wavefront per window row for k = 9, 11 (up to 21 classes, with or
+//      without feature planes), else eight wavefronts taking rows w and w + 8 (the first 512
 //      threads also own the pixels); a lane holds the
 //      rows' weights of four horizontally adjacent cells in registers and
 //      reads each staged row once (16-byte reads) for all four, the two
@@ -50,9 +50,9 @@ struct BlurShape {
     static constexpr int FPL = FS * LS;                     // LDS plane (floats)
     static_assert(LS >= FS && LS % 2 == 0, "whole 8-byte rows");
     // one wavefront per window row for k = 9, 11 (three per SIMD, so at
-    // most 168 VGPRs: up to 21 classes, no feature planes), else eight; the
-    // first NPIX threads also own the pixels
-    static constexpr int NWAVE = K > 8 && K <= 11 && CM <= 21 && !FT ? K : 8;
+    // most 168 VGPRs: up to 21 classes, with or without feature planes),
+    // else eight; the first NPIX threads also own the pixels
+    static constexpr int NWAVE = K > 8 && K <= 11 && CM <= 21 ? K : 8;
     static constexpr int FD = FT ? kMaxFeat : 0;           // staged feature planes
     static constexpr int NT = 64 * NWAVE;                  // threads
     static constexpr int RW = (K + NWAVE - 1) / NWAVE;     // window rows per wave
