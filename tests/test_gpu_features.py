@@ -98,7 +98,13 @@ BLUR_CASES = [
 # forward only: the fused 4 x 4 round with features on a ragged grid (Hp = 9,
 # Wp = 13, so the word-by-word staging), 13 classes (the general class width),
 # two window rows per wavefront (k = 9 with features) and a general compatibility
-BLUR_FWD_EXTRA = [(36, 2, 13, 36, 52, 9, 2, 3, False, True, 4, 5.0)]
+BLUR_FWD_EXTRA = [(36, 2, 13, 36, 52, 9, 2, 3, False, True, 4, 5.0),
+                  # one wavefront per window row with features: 19 classes at
+                  # k = 9 with four feature planes (the most registers), a
+                  # general compatibility, a 10 x 12-cell grid; 6 classes (the
+                  # eight-class width) at k = 11 with one plane, B = 2 and the centre
+                  (37, 1, 19, 40, 48, 9, 2, 4, False, True, 4, 3.0),
+                  (38, 2, 6, 32, 44, 11, 3, 1, True, False, 4, 3.0)]
 
 
 @pytest.mark.parametrize("seed,B,C,H,W,k,T,D,center,gen_mu,s,tg", BLUR_CASES + BLUR_FWD_EXTRA)
