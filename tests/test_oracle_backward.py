@@ -142,6 +142,7 @@ BLUR_CASES = [
     (13, 1, 3, 6, 8, 3, 2, 2, False, True),
     (14, 2, 2, 8, 8, 3, 1, 4, True, False),
     (15, 1, 3, 6, 9, 5, 2, 3, False, False),
+    (16, 1, 2, 16, 16, 3, 2, 8, False, True),   # s = 8: a 2 x 2 pooled grid
 ]
 
 
@@ -150,7 +151,10 @@ def test_blur_gradient_matches_finite_differences(seed, B, C, H, W, k, T, s, cen
     """The pooled message (Sec. 4.2 blur): every unary, every compatibility
     entry and every Eq. 4 parameter against central finite differences."""
     U, I, G, mu = _problem(seed, B, C, H, W, gen_mu)
-    vals = dict(w_app=4.0, theta_alpha=3.0, theta_beta=30.0, w_smooth=1.5, theta_gamma=1.2)
+    # with s = 8 the pooled cells lie 8 pixels apart: a smoothness width on
+    # that scale, so that its derivative stands above the differences' noise
+    vals = dict(w_app=4.0, theta_alpha=3.0, theta_beta=30.0, w_smooth=1.5,
+                theta_gamma=1.2 if s < 8 else 9.0)
     params = orc.OracleParams(filter_size=k, blur=s, include_center=center, **vals)
     dU, dmu, dp = orc.meanfield_backward(U, I, params, T, G, compat=mu)
     fd = np.empty_like(U)
