@@ -162,7 +162,8 @@ def test_blur_features_see_only_cell_means():
 
 
 BLUR_CASES = [(21, 1, 3, 6, 8, 2, 3, 2, False, False, 2), (22, 2, 2, 8, 8, 4, 3, 2, True, True, 1),
-              (23, 1, 2, 6, 4, 2, 5, 1, False, True, 3)]
+              (23, 1, 2, 6, 4, 2, 5, 1, False, True, 3),
+              (24, 1, 2, 16, 16, 8, 3, 2, False, True, 2)]   # s = 8: a 2 x 2 pooled grid
 
 
 @pytest.mark.parametrize("seed,B,C,H,W,s,k,T,center,gen_mu,d", BLUR_CASES)
@@ -170,7 +171,10 @@ def test_blur_feature_gradient_matches_finite_differences(seed, B, C, H, W, s, k
                                                           gen_mu, d):
     U, I, G, F, _ = _blur_problem(seed, B, C, H, W, d)
     mu = np.random.default_rng(seed).normal(0.3, 0.5, (C, C)) if gen_mu else None
-    p = orc.OracleParams(filter_size=k, blur=s, include_center=center, **VALS)
+    # the features are positions plus noise: with s = 8 the pooled features of
+    # neighbouring cells lie 8 apart, so a smoothness width on that scale
+    vals = dict(VALS, theta_gamma=9.0) if s == 8 else VALS
+    p = orc.OracleParams(filter_size=k, blur=s, include_center=center, **vals)
     dU, dmu, dp, dF = orc.meanfield_backward(U, I, p, T, G, compat=mu, features=F)
     h = 1e-6
     fd = np.empty_like(F)
@@ -195,11 +199,11 @@ def test_blur_feature_gradient_matches_finite_differences(seed, B, C, H, W, s, k
         fdu = (g(U[idx] + 1e-5) - g(U[idx] - 1e-5)) / 2e-5
         assert abs(fdu - dU[idx]) <= 1e-7 * max(1.0, np.abs(dU).max())
     for j, name in enumerate(orc.PARAM_NAMES):
-        hh = 1e-6 * VALS[name]
+        hh = 1e-6 * vals[name]
         def q(v):
             return _loss(U, I, orc.OracleParams(filter_size=k, blur=s, include_center=center,
-                                                **dict(VALS, **{name: v})), T, G, mu, F)
-        fdp = (q(VALS[name] + hh) - q(VALS[name] - hh)) / (2 * hh)
+                                                **dict(vals, **{name: v})), T, G, mu, F)
+        fdp = (q(vals[name] + hh) - q(vals[name] - hh)) / (2 * hh)
         assert abs(fdp - dp[j]) <= 2e-6 * abs(fdp) + 1e-9, (name, fdp, dp[j])
 
 
