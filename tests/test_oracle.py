@@ -240,7 +240,7 @@ def test_pool_and_upsample_match_torch(oracle_mod, s, H, W):
     np.testing.assert_allclose(oracle_mod.upsample(Y, s), ref, rtol=0, atol=1e-14)
 
 
-@pytest.mark.parametrize("s,k", [(2, 3), (4, 5), (4, 11)])
+@pytest.mark.parametrize("s,k", [(2, 3), (4, 5), (4, 11), (8, 3)])
 def test_blur_decomposes_into_pool_message_upsample(oracle_mod, s, k):
     # pooled positions are block centres, so a pooled offset d is s*d full-res
     # pixels -- equivalently the un-scaled grid with theta_alpha, theta_gamma
