@@ -292,3 +292,78 @@ def test_ring_and_feature_kernel_agree(torch_cuda, crf, oracle_mod):
     print(f"ring {ea:.2e}, feature kernel {eb:.2e}, between {eab:.2e}", flush=True)
     assert ea <= 1e-4 and eb <= 1e-4 and eab <= 1e-4
     assert eab > 0      # two different kernels: not the same path twice
+
+
+def bench_features(wl):
+    """The feature planes `bench.py --features` times: the pixel coordinates
+    (row, column) plus N(0, 0.5), seed 78."""
+    yy, xx = np.meshgrid(np.arange(wl.H, dtype=np.float32), np.arange(wl.W, dtype=np.float32),
+                         indexing="ij")
+    return (np.stack([yy, xx])[None].repeat(wl.B, axis=0) + np.random.default_rng(78).normal(
+        0.0, 0.5, (wl.B, 2, wl.H, wl.W))).astype(np.float32)
+
+
+def workload_params(torch, wl, F):
+    return params(torch, wl.filter_size, F, blur=wl.blur, w_app=wl.w_app,
+                  theta_alpha=wl.theta_alpha, theta_beta=wl.theta_beta, w_smooth=wl.w_smooth,
+                  theta_gamma=wl.theta_gamma)
+
+
+@pytest.mark.parametrize("name", ["pascal", "blur"])
+def test_feature_workload_full(torch_cuda, crf, oracle_mod, name):
+    """The workloads `bench.py --features` times, every pixel and class:
+    1 x 21 x 512 x 512 with two feature planes, k = 7 (the ring kernel's
+    feature mode) or k = 11 on the 4 x 4 pooled grid (the fused round's)."""
+    from paper_1805_04777_amd import synth
+    torch = torch_cuda
+    wl = synth.WORKLOADS[name]
+    U, I, _ = synth.make_inputs(wl)
+    F = bench_features(wl)
+    p = workload_params(torch, wl, F)
+    print(f"case {name} with features, full", flush=True)
+    Q = crf.meanfield(torch.from_numpy(U).cuda(), torch.from_numpy(I).cuda(), p, wl.iters)
+    torch.cuda.synchronize()
+    Qg = Q.cpu().numpy().astype(np.float64)
+    Qo = oracle_mod.meanfield(U, I, oparams(p), wl.iters, features=F)
+    err = np.abs(Qg - Qo).max()
+    agree = (Qg.argmax(1) == Qo.argmax(1)).mean()
+    print(f"{name} with features: max|dQ| {err:.2e}, argmax agreement {agree:.6f}", flush=True)
+    assert err <= 1e-4
+    assert agree >= 0.9999
+    assert np.abs(Qg.sum(1) - 1.0).max() <= 1e-5
+
+
+def test_feature_workload_backward_full(torch_cuda, crf, oracle_mod):
+    """The derivative `bench.py --backward --features` times on the pascal
+    workload (1 x 21 x 512 x 512, k = 7, T = 5, two feature planes), in full."""
+    from paper_1805_04777_amd import synth
+    torch = torch_cuda
+    wl = synth.WORKLOADS["pascal"]
+    U, I, _ = synth.make_inputs(wl)
+    F = bench_features(wl)
+    G = np.random.default_rng(77).normal(0.0, 1.0, U.shape).astype(np.float32)
+    p = workload_params(torch, wl, F)
+    print("case pascal with features, derivative, full", flush=True)
+    t = lambda x: torch.from_numpy(x).cuda()
+    dU, dmu, dk, dF = crf.meanfield_backward(t(U), t(I), p, wl.iters, t(G), grad_compat=True,
+                                             grad_kernel=True)
+    torch.cuda.synchronize()
+    got = [x.cpu().numpy().astype(np.float64) for x in (dU, dmu, dk, dF)]
+    ref = oracle_mod.meanfield_backward(U, I, oparams(p), wl.iters, G, features=F)
+    for g, r, nm in zip((got[0], got[1], got[3]), (ref[0], ref[1], ref[3]), ("dU", "dmu", "dF")):
+        e = np.abs(g - r).max() / np.abs(r).max()
+        print(f"pascal with features: {nm} rel err {e:.2e}", flush=True)
+        assert e <= 1e-4, f"{nm}: rel err {e:.2e}"
+    # the five parameter derivatives as one vector, held to its own scale as
+    # the tensors above are (1e-4 of its largest entry), and each entry to
+    # 1e-3 relative where its sum does not cancel (at least 1e-2 of the
+    # largest): with these features the theta_gamma sum over every pixel pair
+    # cancels to about 1.6e-3 of the scale (0.77 against 4.9 without them)
+    ek = np.abs(got[2] - ref[2]) / np.abs(ref[2])
+    scale = np.abs(ref[2]).max()
+    for j in range(5):
+        print(f"pascal with features: parameter {j}: gpu {got[2][j]:.9e} oracle {ref[2][j]:.9e} "
+              f"rel err {ek[j]:.2e}", flush=True)
+    assert np.abs(got[2] - ref[2]).max() <= 1e-4 * scale
+    big = np.abs(ref[2]) >= 1e-2 * scale
+    assert big.sum() >= 3 and np.all(ek[big] <= 1e-3), ek
