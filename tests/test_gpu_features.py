@@ -333,17 +333,19 @@ def test_feature_workload_full(torch_cuda, crf, oracle_mod, name):
     assert np.abs(Qg.sum(1) - 1.0).max() <= 1e-5
 
 
-def test_feature_workload_backward_full(torch_cuda, crf, oracle_mod):
-    """The derivative `bench.py --backward --features` times on the pascal
-    workload (1 x 21 x 512 x 512, k = 7, T = 5, two feature planes), in full."""
+@pytest.mark.parametrize("name", ["pascal", "blur"])
+def test_feature_workload_backward_full(torch_cuda, crf, oracle_mod, name):
+    """The derivative `bench.py --backward --features` times (1 x 21 x 512 x
+    512, T = 5, two feature planes; k = 7, or k = 11 on the 4 x 4 pooled
+    grid), in full."""
     from paper_1805_04777_amd import synth
     torch = torch_cuda
-    wl = synth.WORKLOADS["pascal"]
+    wl = synth.WORKLOADS[name]
     U, I, _ = synth.make_inputs(wl)
     F = bench_features(wl)
     G = np.random.default_rng(77).normal(0.0, 1.0, U.shape).astype(np.float32)
     p = workload_params(torch, wl, F)
-    print("case pascal with features, derivative, full", flush=True)
+    print(f"case {name} with features, derivative, full", flush=True)
     t = lambda x: torch.from_numpy(x).cuda()
     dU, dmu, dk, dF = crf.meanfield_backward(t(U), t(I), p, wl.iters, t(G), grad_compat=True,
                                              grad_kernel=True)
@@ -352,7 +354,7 @@ def test_feature_workload_backward_full(torch_cuda, crf, oracle_mod):
     ref = oracle_mod.meanfield_backward(U, I, oparams(p), wl.iters, G, features=F)
     for g, r, nm in zip((got[0], got[1], got[3]), (ref[0], ref[1], ref[3]), ("dU", "dmu", "dF")):
         e = np.abs(g - r).max() / np.abs(r).max()
-        print(f"pascal with features: {nm} rel err {e:.2e}", flush=True)
+        print(f"{name} with features: {nm} rel err {e:.2e}", flush=True)
         assert e <= 1e-4, f"{nm}: rel err {e:.2e}"
     # the five parameter derivatives as one vector, held to its own scale as
     # the tensors above are (1e-4 of its largest entry), and each entry to
@@ -362,7 +364,7 @@ def test_feature_workload_backward_full(torch_cuda, crf, oracle_mod):
     ek = np.abs(got[2] - ref[2]) / np.abs(ref[2])
     scale = np.abs(ref[2]).max()
     for j in range(5):
-        print(f"pascal with features: parameter {j}: gpu {got[2][j]:.9e} oracle {ref[2][j]:.9e} "
+        print(f"{name} with features: parameter {j}: gpu {got[2][j]:.9e} oracle {ref[2][j]:.9e} "
               f"rel err {ek[j]:.2e}", flush=True)
     assert np.abs(got[2] - ref[2]).max() <= 1e-4 * scale
     big = np.abs(ref[2]) >= 1e-2 * scale
